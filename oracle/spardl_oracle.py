@@ -1,0 +1,344 @@
+"""Plain CPU oracle of SparDL's sparse synchronisation with one team (d = 1).
+
+TEST INFRASTRUCTURE ONLY -- see the package docstring.  Nothing in the product
+path may import this module.
+
+What is computed, and where the paper defines it (SparDL, arXiv 2304.00737):
+
+* residual add: each worker adds its stored residual to its fresh gradient
+  (Sec. III-B "Partitioning"; first step of Algorithm 1).
+* partitioning into P blocks and l+1 bags (Sec. III-B "Partitioning",
+  Example 1).
+* block-wise top-k/P sparsification (Sec. III-B; top-k as defined in Sec. II
+  "Top-k sparsification").
+* Spar-Reduce-Scatter transmission: l = ceil(log2 P) steps; at step i worker w
+  sends bag B_{l-i+1} to w + 2^{l-i} and receives the matching bag from
+  w - 2^{l-i}, adds received entries into its held blocks by index and keeps
+  the top k/P of every held block (Sec. III-B "Transmission with
+  sparsification", Example 2, Theorem 1).
+* final All-Gather of the P reduced blocks and decode to a dense update
+  (end of Sec. III-B; Sec. II for All-Gather semantics).
+* global residual collection (Sec. III-C, Algorithm 1).
+
+Readings taken where the paper is silent or ambiguous (each one is listed in
+the design notes of the repository):
+
+* fp32 throughout; every addition is one IEEE fp32 round-to-nearest-even add.
+* top-k order: larger |v| first, compared on the fp32 bit pattern with the
+  sign bit cleared; equal |v| -> lower index first.  Exactly k entries are kept
+  (zeros and cancelled sums included) whenever at least k exist.
+* blocks: block b covers [floor(b n / P), floor((b+1) n / P)).
+* 0-based workers and blocks; worker w's preservation block is block w.
+* eager sparsification: every block is sparsified locally before the first
+  step and every held block that received entries is re-sparsified after each
+  step (the variant the main text of Sec. III-B describes).
+* residual collection: the in-procedure drops of one block at one worker over
+  several steps are accumulated (not overwritten), in ascending step order,
+  on top of the local residual.
+* index sums add the held value and the received value (two operands; IEEE
+  addition is commutative so operand order does not change the bits).
+
+Arrays: values are numpy float32, indices numpy int64 (global indices within a
+worker's flat gradient, i.e. in [0, n)).
+"""
+
+from __future__ import annotations
+
+from dataclasses import dataclass, field
+
+import numpy as np
+
+# ----------------------------------------------------------------------------
+# Partitioning and schedule (Sec. III-B "Partitioning", Example 1,
+# "Transmission with sparsification", Example 2, Theorem 1)
+# ----------------------------------------------------------------------------
+
+
+def block_bounds(n: int, P: int) -> list[int]:
+    """Start offsets of the P blocks plus the end: block b = [s_b, s_{b+1}).
+
+    Sec. III-B splits the flat gradient into P blocks without saying how a
+    remainder is spread; the reading used here is s_b = floor(b * n / P).
+    """
+    return [(b * n) // P for b in range(P + 1)]
+
+
+def num_steps(P: int) -> int:
+    """l = ceil(log2 P), the number of transmission steps (Sec. III-B); 0 for P = 1."""
+    l = 0
+    while (1 << l) < P:
+        l += 1
+    return l
+
+
+def srs_partition_bags(P: int, w: int) -> list[list[int]]:
+    """Bags B_0 .. B_l of worker w (Sec. III-B "Partitioning", Example 1).
+
+    The P blocks are laid out on a circle starting at block w.  B_0 = {w} is
+    the preservation bag; sending bag B_j takes the next 2^(j-1) blocks, and
+    the last bag holds whatever remains (E = P - 2^(l-1) blocks).
+    """
+    l = num_steps(P)
+    circle = [(w + t) % P for t in range(P)]
+    bags = [circle[0:1]]
+    pos = 1
+    for j in range(1, l + 1):
+        size = 1 << (j - 1)
+        bags.append(circle[pos:pos + size])
+        pos += size
+    assert pos >= P and sum(len(b) for b in bags) == P
+    return bags
+
+
+@dataclass(frozen=True)
+class SRSStep:
+    """One transmission step i (1-based) of Spar-Reduce-Scatter."""
+
+    i: int
+    distance: int                 # 2^(l-i)
+    target: tuple[int, ...]       # target[w] = w + distance (mod P)
+    source: tuple[int, ...]       # source[w] = w - distance (mod P)
+    sent_bag: tuple[tuple[int, ...], ...]      # blocks worker w sends at this step
+    received_bag: tuple[tuple[int, ...], ...]  # blocks worker w receives at this step
+
+
+def srs_schedule(P: int) -> list[SRSStep]:
+    """The l transmission steps (Sec. III-B "Transmission with sparsification").
+
+    At step i worker w sends its bag B_{l-i+1} to worker w + 2^(l-i) and
+    receives bag B_{l-i+1} of worker w - 2^(l-i) (indices mod P).
+    """
+    l = num_steps(P)
+    bags = [srs_partition_bags(P, w) for w in range(P)]
+    steps = []
+    for i in range(1, l + 1):
+        dist = 1 << (l - i)
+        j = l - i + 1
+        target = tuple((w + dist) % P for w in range(P))
+        source = tuple((w - dist) % P for w in range(P))
+        sent = tuple(tuple(bags[w][j]) for w in range(P))
+        recv = tuple(tuple(bags[source[w]][j]) for w in range(P))
+        steps.append(SRSStep(i, dist, target, source, sent, recv))
+    return steps
+
+
+# ----------------------------------------------------------------------------
+# Top-k sparsification (Sec. II "Top-k sparsification")
+# ----------------------------------------------------------------------------
+
+
+def magnitude_key(vals: np.ndarray) -> np.ndarray:
+    """|v| as an unsigned integer: the fp32 bit pattern with the sign bit cleared.
+
+    For finite floats this orders exactly like |v|, and it makes -0.0 and +0.0
+    equal, as they are in magnitude.
+    """
+    v = np.ascontiguousarray(vals, dtype=np.float32)
+    return v.view(np.uint32) & np.uint32(0x7FFFFFFF)
+
+
+def top_k(idx: np.ndarray, vals: np.ndarray, k: int) -> np.ndarray:
+    """Positions (into idx/vals) of the k entries with the largest |v|.
+
+    Ties in |v| go to the lower index.  The positions are returned ordered by
+    ascending index.  The selection uses one library primitive (a partial
+    sort) on a combined key that is unique per entry: |v| in the high 32 bits
+    and the complement of the index in the low 32 bits, so a larger combined
+    key means "better" under exactly the order above.
+    """
+    m = len(idx)
+    if k >= m:
+        sel = np.arange(m)
+    else:
+        key = magnitude_key(vals).astype(np.uint64)
+        comp = np.uint64(0xFFFFFFFF) - np.asarray(idx, dtype=np.uint64)
+        combined = (key << np.uint64(32)) | comp
+        sel = np.argpartition(combined, m - k)[m - k:]
+    order = np.argsort(np.asarray(idx)[sel], kind="stable")
+    return sel[order]
+
+
+def local_sparsify(block_vals: np.ndarray, base: int, k: int) -> tuple[np.ndarray, np.ndarray]:
+    """Top-k/P of one dense block (Sec. III-B): returns (global idx, val), idx ascending."""
+    idx = np.arange(base, base + len(block_vals), dtype=np.int64)
+    pos = top_k(idx, block_vals, k)
+    return idx[pos], np.asarray(block_vals, dtype=np.float32)[pos].copy()
+
+
+# ----------------------------------------------------------------------------
+# Summation by index and re-sparsification (Sec. III-B; the SGA example of Sec. I)
+# ----------------------------------------------------------------------------
+
+
+def index_sum(h_idx, h_val, r_idx, r_val) -> tuple[np.ndarray, np.ndarray]:
+    """Add received sparse entries into held sparse entries "according to the
+    gradient indexes" (Sec. III-B): the union of both index sets, with
+    held + received (one fp32 add) where an index is in both.  Sorted by index.
+    """
+    h_idx = np.asarray(h_idx, dtype=np.int64)
+    r_idx = np.asarray(r_idx, dtype=np.int64)
+    h_val = np.asarray(h_val, dtype=np.float32)
+    r_val = np.asarray(r_val, dtype=np.float32)
+    u_idx = np.union1d(h_idx, r_idx)
+    u_val = np.empty(len(u_idx), dtype=np.float32)
+    hp = np.searchsorted(u_idx, h_idx)
+    rp = np.searchsorted(u_idx, r_idx)
+    u_val[hp] = h_val
+    in_both = np.isin(r_idx, h_idx)
+    u_val[rp[~in_both]] = r_val[~in_both]
+    u_val[rp[in_both]] = u_val[rp[in_both]] + r_val[in_both]
+    return u_idx, u_val
+
+
+def merge_and_resparsify(h_idx, h_val, r_idx, r_val, k: int):
+    """Index-sum one received block into the held block, then keep its top k.
+
+    Returns (kept_idx, kept_val, dropped_idx, dropped_val); both parts are
+    sorted by index.  The dropped part is this worker's in-procedure residual
+    for the block at this step (Sec. III-C).
+    """
+    u_idx, u_val = index_sum(h_idx, h_val, r_idx, r_val)
+    keep = top_k(u_idx, u_val, k)
+    mask = np.zeros(len(u_idx), dtype=bool)
+    mask[keep] = True
+    return u_idx[mask], u_val[mask], u_idx[~mask], u_val[~mask]
+
+
+# ----------------------------------------------------------------------------
+# The step (Algorithm 1 with d = 1)
+# ----------------------------------------------------------------------------
+
+
+def residual_add(acc: np.ndarray, grad: np.ndarray) -> np.ndarray:
+    """G + xi in fp32 (first step of Algorithm 1)."""
+    return (np.asarray(acc, dtype=np.float32) + np.asarray(grad, dtype=np.float32)).astype(np.float32)
+
+
+def spar_reduce_scatter(S: dict, P: int, k: int, blocks=None):
+    """Run the l transmission steps on the sparse blocks S[(w, b)] = (idx, val).
+
+    Messages of step i carry the sender's blocks as they stood at the start of
+    step i.  Only blocks in ``blocks`` (default: all) are processed; blocks never
+    exchange data with one another, so restricting the set is exact.
+
+    Returns drops[(i, w, b)] = (idx, val): what worker w discarded from block b
+    at step i.  S is updated in place; S[(w, b)] keeps the state a block had
+    when worker w sent it away.
+    """
+    wanted = set(range(P)) if blocks is None else set(blocks)
+    held = [set(range(P)) for _ in range(P)]
+    drops = {}
+    for step in srs_schedule(P):
+        sent_state = {}
+        for w in range(P):
+            for b in step.sent_bag[w]:
+                assert b in held[w], "a sent block must still be held"
+                if b in wanted:
+                    sent_state[(w, b)] = S[(w, b)]
+        for w in range(P):
+            for b in step.sent_bag[w]:
+                held[w].discard(b)
+        for w in range(P):
+            src = step.source[w]
+            for b in step.received_bag[w]:
+                # Theorem 1: every received block is still held by the receiver.
+                assert b in held[w], "Theorem 1 violated"
+                if b not in wanted:
+                    continue
+                h_idx, h_val = S[(w, b)]
+                r_idx, r_val = sent_state[(src, b)]
+                kept_i, kept_v, drop_i, drop_v = merge_and_resparsify(h_idx, h_val, r_idx, r_val, k)
+                S[(w, b)] = (kept_i, kept_v)
+                drops[(step.i, w, b)] = (drop_i, drop_v)
+    for w in range(P):
+        assert held[w] == {w}, "after l steps worker w holds only block w"
+    return drops
+
+
+def allgather_densify(final: dict, bounds: list[int], blocks) -> dict:
+    """Dense update restricted to each listed block: the final value at every
+    index that survived to the end of Spar-Reduce-Scatter, +0.0 elsewhere.
+    The All-Gather gives every worker all P final blocks (Sec. III-B end), so
+    the result is the same on every worker.
+    """
+    out = {}
+    for b in blocks:
+        dense = np.zeros(bounds[b + 1] - bounds[b], dtype=np.float32)
+        idx, val = final[b]
+        dense[np.asarray(idx) - bounds[b]] = val
+        out[b] = dense
+    return out
+
+
+def global_residual_collect(A_block: np.ndarray, base: int, local_idx, final_idx, drops_in_order):
+    """New residual of one worker on one block (Sec. III-C, Algorithm 1).
+
+    Algorithm 1 keeps a copy of A = G + xi and, at every index I of the final
+    global gradients, replaces the copy by what this worker discarded there.
+    What worker w discarded at x is A[x] if w did not select x locally, 0 if it
+    did, plus every in-procedure drop w made at x (in step order).  Indices
+    outside I keep A[x]: local and end-procedure residuals stay where they
+    arose.
+    """
+    xi = np.array(A_block, dtype=np.float32, copy=True)
+    final_idx = np.asarray(final_idx, dtype=np.int64)
+    L = np.asarray(local_idx, dtype=np.int64)
+    L_in = L[np.isin(L, final_idx)]
+    xi[L_in - base] = np.float32(0.0)
+    for d_idx, d_val in drops_in_order:
+        d_idx = np.asarray(d_idx, dtype=np.int64)
+        m = np.isin(d_idx, final_idx)
+        pos = d_idx[m] - base
+        xi[pos] = xi[pos] + np.asarray(d_val, dtype=np.float32)[m]
+    return xi
+
+
+@dataclass
+class SparDLStepResult:
+    """Everything one oracle step produces, keyed by worker w and block b."""
+
+    bounds: list
+    blocks: list
+    local: dict = field(default_factory=dict)    # (w, b) -> (idx, val) after local top-k
+    S: dict = field(default_factory=dict)        # (w, b) -> (idx, val) after all steps
+    drops: dict = field(default_factory=dict)    # (i, w, b) -> (idx, val)
+    final: dict = field(default_factory=dict)    # b -> (idx, val) = S[(b, b)]
+    dense: dict = field(default_factory=dict)    # b -> dense update on block b
+    residual: dict = field(default_factory=dict)  # (w, b) -> new residual on block b
+
+
+def _block_of(row, b, bounds):
+    if isinstance(row, dict):
+        return row[b]
+    return row[bounds[b]:bounds[b + 1]]
+
+
+def spardl_step(acc, grad, P: int, n: int, k: int, blocks=None) -> SparDLStepResult:
+    """One SparDL synchronisation (d = 1) for P workers.
+
+    acc[w], grad[w]: worker w's residual and fresh gradient, either full rows
+    of length n or dicts {b: block array} holding at least the listed blocks.
+    k is the per-block count k/P.  The new residual is written back into acc
+    (in place) on the listed blocks; the result object holds the rest.
+    """
+    bounds = block_bounds(n, P)
+    blocks = list(range(P)) if blocks is None else sorted(blocks)
+    res = SparDLStepResult(bounds=bounds, blocks=blocks)
+    A = {}
+    for w in range(P):
+        for b in blocks:
+            A[(w, b)] = residual_add(_block_of(acc[w], b, bounds), _block_of(grad[w], b, bounds))
+            res.local[(w, b)] = local_sparsify(A[(w, b)], bounds[b], k)
+            res.S[(w, b)] = res.local[(w, b)]
+    res.drops = spar_reduce_scatter(res.S, P, k, blocks)
+    res.final = {b: res.S[(b, b)] for b in blocks}
+    res.dense = allgather_densify(res.final, bounds, blocks)
+    l = num_steps(P)
+    for w in range(P):
+        for b in blocks:
+            in_order = [res.drops[(i, w, b)] for i in range(1, l + 1) if (i, w, b) in res.drops]
+            xi = global_residual_collect(A[(w, b)], bounds[b], res.local[(w, b)][0],
+                                         res.final[b][0], in_order)
+            res.residual[(w, b)] = xi
+            _block_of(acc[w], b, bounds)[...] = xi
+    return res

@@ -1,0 +1,93 @@
+"""Independent pure-Python brute force of one SparDL step (d = 1), for tiny inputs.
+
+Written separately from the oracle, in a different style (dicts of
+index -> fp32 value, Python's sorted(), a closed-form bag layout, and an
+explicit per-worker "discarded" ledger for the residual), so that the oracle
+can be pinned against it.  It follows the paper (SparDL, arXiv 2304.00737):
+Sec. II (top-k), Sec. III-B (partitioning, transmission with sparsification),
+Sec. III-C / Algorithm 1 (global residual collection).
+"""
+
+from __future__ import annotations
+
+import numpy as np
+
+F32 = np.float32
+
+
+def _mag(v) -> int:
+    return int(np.array([v], dtype=np.float32).view(np.uint32)[0]) & 0x7FFFFFFF
+
+
+def bf_topk(d: dict, k: int) -> dict:
+    """Keep the k entries of largest |v|, ties to the lower index (full sort)."""
+    ranked = sorted(d.items(), key=lambda kv: (-_mag(kv[1]), kv[0]))
+    return dict(ranked[:k])
+
+
+def bf_merge(held: dict, recv: dict) -> dict:
+    out = dict(held)
+    for x, v in recv.items():
+        out[x] = F32(out[x] + v) if x in out else F32(v)
+    return out
+
+
+def bf_step(acc_rows, grad_rows, P: int, k: int):
+    """Returns (dense u, new residual rows, final dicts per block, drops, local)."""
+    n = len(acc_rows[0])
+    s = [b * n // P for b in range(P + 1)]
+    A = [[F32(F32(acc_rows[w][x]) + F32(grad_rows[w][x])) for x in range(n)] for w in range(P)]
+
+    state = {}
+    local = {}
+    for w in range(P):
+        for b in range(P):
+            block = {x: A[w][x] for x in range(s[b], s[b + 1])}
+            state[(w, b)] = bf_topk(block, k)
+            local[(w, b)] = dict(state[(w, b)])
+
+    l = 0
+    while (1 << l) < P:
+        l += 1
+    drops = {}
+    for i in range(1, l + 1):
+        dist = 1 << (l - i)
+        # bag B_{l-i+1} of worker w sits at circle positions [2^(l-i), 2^(l-i+1)) from w
+        lo, hi = 1 << (l - i), min(1 << (l - i + 1), P)
+        inbox = {}
+        for w in range(P):
+            dst = (w + dist) % P
+            inbox[dst] = [(b, dict(state[(w, b)])) for b in ((w + t) % P for t in range(lo, hi))]
+        for r in range(P):
+            for b, msg in inbox[r]:
+                merged = bf_merge(state[(r, b)], msg)
+                kept = bf_topk(merged, k)
+                state[(r, b)] = kept
+                drops[(i, r, b)] = {x: v for x, v in merged.items() if x not in kept}
+
+    final = {b: state[(b, b)] for b in range(P)}
+    u = [F32(0.0)] * n
+    for b in range(P):
+        for x, v in final[b].items():
+            u[x] = v
+    I = set()
+    for b in range(P):
+        I |= set(final[b].keys())
+
+    new_res = []
+    for w in range(P):
+        ledger = {}
+        for x in range(n):
+            b = next(bb for bb in range(P) if s[bb] <= x < s[bb + 1])
+            if x not in local[(w, b)]:
+                ledger[x] = A[w][x]
+        for i in range(1, l + 1):
+            for (ii, ww, b), d in drops.items():
+                if ii == i and ww == w:
+                    for x, v in d.items():
+                        ledger[x] = F32(ledger.get(x, F32(0.0)) + v)
+        row = []
+        for x in range(n):
+            row.append(ledger.get(x, F32(0.0)) if x in I else A[w][x])
+        new_res.append(row)
+    return u, new_res, final, drops, local
