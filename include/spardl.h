@@ -1,0 +1,163 @@
+/* spardl.h -- C ABI of libspardl.so: the per-worker compute path of SparDL's
+ * sparse gradient synchronisation with one team (d = 1), for AMD Instinct
+ * MI355X (gfx950).
+ *
+ * Paper: M. Zhao et al., "SparDL: Distributed Deep Learning Training with
+ * Efficient Sparse Communication", arXiv 2304.00737.  Section numbers below
+ * refer to it.
+ *
+ * Model.  P data-parallel workers each hold a flat fp32 gradient of n values
+ * and a residual of the same size.  The gradient is split into P contiguous
+ * blocks, block b = [floor(b n / P), floor((b+1) n / P)).  A sparse block is
+ * exactly k_blk (index, value) pairs sorted by ascending index; indices are
+ * int32 offsets into the worker's flat gradient (so n < 2^31).  Several
+ * workers' rows may live in one allocation with a row stride ("ld", in
+ * elements).  "Top-k" always means: larger |v| first, where |v| is compared
+ * as the fp32 bit pattern with the sign bit cleared; equal |v| -> lower index
+ * first.  All value arithmetic is IEEE fp32 round-to-nearest-even addition;
+ * results are deterministic (bit-identical run to run).
+ *
+ * Sparse state layout used by the SRS calls: sp_idx/sp_val[w][b][k_blk] for
+ * worker w and block b (row-major, P * P * k_blk entries each).
+ *
+ * Conventions for every call below.
+ *  - Pointers named acc, grad, sp_*, local_idx, drop_*, dense and ws are
+ *    DEVICE pointers owned by the caller.  The library allocates nothing,
+ *    keeps no state between calls, never synchronises and never copies
+ *    between host and device.
+ *  - Arguments are validated on the host first; on error nothing is enqueued
+ *    and a negative status is returned.  Otherwise kernels are enqueued on
+ *    `stream` and SPARDL_OK is returned; results are valid once the stream
+ *    reaches that point.
+ *  - ws is scratch device memory of at least spardl_workspace_bytes(...)
+ *    bytes, 256-byte aligned; its content on entry is ignored except where a
+ *    flag says otherwise.  The first 4 bytes of ws hold an error word that
+ *    each call clears and that kernels set if an internal check fails (see
+ *    SPARDL_WS_ERR_*); read it after the stream completes if needed.
+ *  - Calls on different streams must use different ws and disjoint outputs.
+ */
+#ifndef SPARDL_H
+#define SPARDL_H
+
+#include <stddef.h>
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+enum {
+  SPARDL_OK = 0,
+  SPARDL_EINVAL = -1,    /* an argument is NULL, out of range or misaligned */
+  SPARDL_ECAPACITY = -2, /* ws_bytes is below spardl_workspace_bytes(...) */
+  SPARDL_EDEVICE = -3    /* a kernel launch failed (hipGetLastError) */
+};
+
+/* Bits of the error word at the start of ws (set by kernels, cleared by calls). */
+#define SPARDL_WS_ERR_LOOKBACK 1u  /* a tile's ordered-prefix wait exceeded its spin bound */
+#define SPARDL_WS_ERR_COUNT 2u     /* a selection did not produce exactly k_blk entries */
+
+/* Flag for spardl_block_topk: the level-1 |v| histograms of acc are already in
+ * ws, written by the immediately preceding spardl_residual_add call with the
+ * same acc, ld_acc, nworkers, n, P and ws (fused pass; saves one read of acc). */
+#define SPARDL_TOPK_HIST_READY 1
+
+/* Static text for a status code. */
+const char* spardl_strerror(int status);
+
+/* Spar-Reduce-Scatter schedule (Sec. III-B "Partitioning" and "Transmission
+ * with sparsification", Examples 1-2, Theorem 1).  Host only; no GPU needed.
+ * Returns l = ceil(log2 P) (0 for P = 1), or SPARDL_EINVAL for P < 1.  If the
+ * arrays are non-NULL they receive, for steps i = 1..l at position i-1:
+ * distance[i-1] = 2^(l-i) (worker w sends to w + distance and receives from
+ * w - distance, mod P) and bag_blocks[i-1] = number of blocks in the bag sent
+ * and received at step i (P - 2^(l-1) at step 1, 2^(l-i) afterwards).  At
+ * step i worker w receives blocks (w + t) mod P for t < bag_blocks[i-1].
+ * Arrays must hold at least 32 entries. */
+int spardl_srs_plan(int32_t P, int32_t* distance, int32_t* bag_blocks);
+
+/* Bytes of ws that every call below needs for these sizes (nworkers = rows
+ * passed to spardl_block_topk / spardl_residual_add).  0 on invalid sizes. */
+size_t spardl_workspace_bytes(int32_t nworkers, int32_t P, int64_t n, int32_t k_blk);
+
+/* Residual add (Sec. III-B "Partitioning": each worker adds its residual
+ * xi^{t-1} to its new gradient; first step of Algorithm 1):
+ *   acc[w*ld_acc + x] = acc[w*ld_acc + x] + grad[w*ld_grad + x]
+ * for w < nworkers, x < n, in place.  acc then holds A = G + xi, which also
+ * serves as the copy that Algorithm 1 keeps for residual collection.
+ * If P > 0 and ws != NULL, the same pass also records, for each of the P
+ * blocks of each row, the level-1 |v| histogram that spardl_block_topk needs
+ * (pass it SPARDL_TOPK_HIST_READY).  P = 0 (ws ignored) is a plain add.
+ * Errors: EINVAL for NULL acc/grad, nworkers < 1, n < 1 or n >= 2^31,
+ * ld < n, P < 0, P > n; ECAPACITY if P > 0 and ws is too small. */
+int spardl_residual_add(float* acc, int64_t ld_acc, const float* grad, int64_t ld_grad,
+                        int32_t nworkers, int64_t n, int32_t P, void* ws, size_t ws_bytes,
+                        hipStream_t stream);
+
+/* Block-wise top-k (Sec. III-B: every worker sparsifies each of its P blocks
+ * to its top k/P values; top-k as in Sec. II).  For w < nworkers, b < P:
+ *   sp_idx/sp_val[(w*P + b)*k_blk + j], j < k_blk = the top-k_blk entries of
+ *   block b of row w of acc, sorted by ascending index.
+ * local_idx (optional, may be NULL) receives a second copy of the indices;
+ * spardl_residual_collect needs it after the SRS steps have overwritten sp.
+ * flags: 0 or SPARDL_TOPK_HIST_READY.
+ * Errors: EINVAL for NULL acc/sp/ws, nworkers < 1, P < 1, n < P, n >= 2^31,
+ * ld_acc < n, k_blk < 1 or k_blk > floor(n / P); ECAPACITY if ws is small. */
+int spardl_block_topk(const float* acc, int64_t ld_acc, int32_t nworkers, int64_t n, int32_t P,
+                      int32_t k_blk, int32_t flags, int32_t* sp_idx, float* sp_val,
+                      int32_t* local_idx, void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* One Spar-Reduce-Scatter step `round` in [1, l] for all P workers at once
+ * (Sec. III-B "Transmission with sparsification").  With d = 2^(l-round) and
+ * m = bag_blocks of that step (see spardl_srs_plan), for every worker w and
+ * t < m, block b = (w + t) mod P of worker w receives block b of worker
+ * (w - d) mod P: the two sparse blocks are summed by index (held + received
+ * where both have an index), the top k_blk of the union are kept in
+ * sp[w][b] (sorted by index, in place), and the rest -- this worker's
+ * in-procedure residual for the block at this step (Sec. III-C) -- go to
+ *   drop_idx/drop_val[(w*m + t)*k_blk + j], j < drop_cnt[w*m + t]
+ * sorted by index (the union has between k_blk and 2 k_blk entries, so
+ * 0 <= drop_cnt <= k_blk).  Steps must be run in order 1..l.
+ * Errors: EINVAL for NULL pointers, P < 2, n < P, n >= 2^31, k_blk out of
+ * [1, floor(n/P)], round outside [1, l]; ECAPACITY if ws is too small. */
+int spardl_sparse_merge_topk(int32_t* sp_idx, float* sp_val, int32_t P, int64_t n, int32_t k_blk,
+                             int32_t round, int32_t* drop_idx, float* drop_val, int32_t* drop_cnt,
+                             void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* Final All-Gather and decode (end of Sec. III-B; Algorithm 1 "All-Gather all
+ * blocks from all workers").  After step l, worker b holds the reduced block
+ * b in sp[b][b]; the All-Gather gives every worker all P of them, which on
+ * one device is the identity.  Writes the dense update once:
+ *   dense[x] = value of x in the final block containing x, if x is there;
+ *   dense[x] = +0.0f otherwise;     for x < n.
+ * Errors: EINVAL for NULL pointers, P < 1, n < P, n >= 2^31, k_blk out of
+ * [1, floor(n/P)]. */
+int spardl_allgather_densify(const int32_t* sp_idx, const float* sp_val, int32_t P, int64_t n,
+                             int32_t k_blk, float* dense, hipStream_t stream);
+
+/* Global residual collection (Sec. III-C, Algorithm 1).  Let I be the set of
+ * indices in the final blocks sp[b][b], b < P.  For every worker w < P (row w
+ * of acc holds A_w = G + xi from spardl_residual_add):
+ *   acc[w][x] = 0.0f           for x in I that w selected locally
+ *                              (local_idx[w][*][*] from spardl_block_topk);
+ *   acc[w][x] = acc[w][x] + v  for every in-procedure drop (x, v) of w with
+ *                              x in I, steps 1..l in that order;
+ *   other entries keep A_w    (local and end-procedure residuals).
+ * The result is xi^t_w, the residual for the next iteration.
+ * drop_idx/drop_val/drop_cnt are HOST arrays of l DEVICE pointers (element
+ * i-1 = the buffers passed to spardl_sparse_merge_topk for step i); they may
+ * be NULL when P = 1.
+ * Errors: EINVAL for NULL pointers, P < 1, n < P, n >= 2^31, ld_acc < n,
+ * k_blk out of [1, floor(n/P)]; ECAPACITY if ws is too small. */
+int spardl_residual_collect(float* acc, int64_t ld_acc, int32_t P, int64_t n, int32_t k_blk,
+                            const int32_t* local_idx, const int32_t* sp_idx,
+                            const int32_t* const* drop_idx, const float* const* drop_val,
+                            const int32_t* const* drop_cnt, void* ws, size_t ws_bytes,
+                            hipStream_t stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SPARDL_H */

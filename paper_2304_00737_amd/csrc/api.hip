@@ -1,0 +1,288 @@
+// C ABI of libspardl (declared in include/spardl.h): argument checks,
+// workspace layout and kernel sequencing.  Nothing here allocates,
+// synchronises or copies between host and device.
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <algorithm>
+
+#include "../../include/spardl.h"
+#include "common.hpp"
+#include "launch.hpp"
+
+using namespace spardl;
+
+namespace {
+
+constexpr int64_t kMaxN = (int64_t)INT32_MAX;   // indices are int32: n < 2^31
+
+inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+inline int32_t steps_of(int32_t P) {
+  int32_t l = 0;
+  while ((1ll << l) < P) ++l;
+  return l;
+}
+
+// blocks in the bag of step i (1-based) of Spar-Reduce-Scatter
+inline int32_t bag_of(int32_t P, int32_t l, int32_t i) {
+  return i == 1 ? P - (1 << (l - 1)) : (1 << (l - i));
+}
+
+inline int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
+
+// Workspace layout.  Everything before the candidate region depends only on
+// (P, n, k_blk), so every call finds the same offsets; the candidate region
+// takes the rest of ws (index array, then value array, split in the middle).
+struct Layout {
+  size_t err = 0, bitmap = 0, hist1 = 0, state = 0, tick_a = 0, tick_b = 0, stat_a = 0, stat_b = 0;
+  size_t fixed_end = 0;
+  int64_t units = 0, tiles_tk = 0, etiles_tk = 0, tiles_mg = 0, etiles_mg = 0;
+  int64_t stat_a_n = 0, stat_b_n = 0;
+  int64_t pairs_max = 0;
+};
+
+Layout make_layout(int32_t P, int64_t n, int32_t kb) {
+  Layout L;
+  const int32_t l = steps_of(P);
+  int64_t mmax = 0;   // largest bag over the steps (step 1 is not always the largest)
+  for (int32_t i = 1; i <= l; ++i) mmax = std::max<int64_t>(mmax, bag_of(P, l, i));
+  const int64_t maxlen = ceil_div(n, P);
+  L.pairs_max = (int64_t)P * mmax;
+  L.units = std::max<int64_t>((int64_t)P * P, L.pairs_max);
+  L.tiles_tk = ceil_div(maxlen, STREAM_TILE);
+  L.etiles_tk = ceil_div(maxlen, EMIT_TILE);
+  L.tiles_mg = ceil_div(2ll * kb, MERGE_TILE);
+  L.etiles_mg = ceil_div(2ll * kb, EMIT_TILE);
+  L.stat_a_n = std::max<int64_t>((int64_t)P * P * L.tiles_tk, L.pairs_max * L.tiles_mg);
+  L.stat_b_n = std::max<int64_t>((int64_t)P * P * L.etiles_tk, L.pairs_max * L.etiles_mg);
+  size_t off = 256;
+  L.bitmap = off;
+  off += align256((size_t)ceil_div(n, 32) * 4);
+  L.hist1 = off;
+  off += align256((size_t)L.units * NB1 * 4);
+  L.state = off;
+  off += align256((size_t)L.units * ST_WORDS * 4);
+  L.tick_a = off;
+  off += align256((size_t)L.units * 4);
+  L.tick_b = off;
+  off += align256((size_t)L.units * 4);
+  L.stat_a = off;
+  off += align256((size_t)L.stat_a_n * 8);
+  L.stat_b = off;
+  off += align256((size_t)L.stat_b_n * 8);
+  L.fixed_end = off;
+  return L;
+}
+
+inline size_t cand_bytes(int64_t entries) { return 2 * align256((size_t)entries * 4); }
+
+struct Ws {
+  char* base;
+  uint32_t* err;
+  uint32_t* bitmap;
+  uint32_t* hist1;
+  uint32_t* state;
+  uint32_t* tick_a;
+  uint32_t* tick_b;
+  uint64_t* stat_a;
+  uint64_t* stat_b;
+  int32_t* cand_idx;
+  float* cand_val;
+};
+
+Ws carve(void* ws, size_t ws_bytes, const Layout& L) {
+  Ws w;
+  w.base = (char*)ws;
+  w.err = (uint32_t*)(w.base + L.err);
+  w.bitmap = (uint32_t*)(w.base + L.bitmap);
+  w.hist1 = (uint32_t*)(w.base + L.hist1);
+  w.state = (uint32_t*)(w.base + L.state);
+  w.tick_a = (uint32_t*)(w.base + L.tick_a);
+  w.tick_b = (uint32_t*)(w.base + L.tick_b);
+  w.stat_a = (uint64_t*)(w.base + L.stat_a);
+  w.stat_b = (uint64_t*)(w.base + L.stat_b);
+  const size_t half = ws_bytes > L.fixed_end ? ((ws_bytes - L.fixed_end) / 2) & ~(size_t)255 : 0;
+  w.cand_idx = (int32_t*)(w.base + L.fixed_end);
+  w.cand_val = (float*)(w.base + L.fixed_end + half);
+  return w;
+}
+
+inline bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+
+// float4 streaming is used when every block start, the row length and the
+// row strides are multiples of 4 and the base pointers are 16-byte aligned.
+bool blocks_vec4(int64_t n, int32_t P) {
+  if (n % 4) return false;
+  for (int64_t b = 0; b <= P; ++b)
+    if (blk_start(b, n, P) % 4) return false;
+  return true;
+}
+
+bool sizes_ok(int32_t P, int64_t n, int32_t kb) {
+  if (P < 1 || n < P || n > kMaxN) return false;
+  if (kb < 1 || (int64_t)kb > n / P) return false;
+  return true;
+}
+
+struct Fill {
+  FillRanges r{};
+  Fill& add(void* p, int64_t words) {
+    if (words > 0) {
+      r.ptr[r.count] = (uint32_t*)p;
+      r.len[r.count] = words;
+      ++r.count;
+    }
+    return *this;
+  }
+};
+
+#define SPARDL_TRY(expr)                      \
+  do {                                        \
+    if ((expr) != hipSuccess) return SPARDL_EDEVICE; \
+  } while (0)
+
+}  // namespace
+
+extern "C" {
+
+const char* spardl_strerror(int status) {
+  switch (status) {
+    case SPARDL_OK: return "ok";
+    case SPARDL_EINVAL: return "invalid argument";
+    case SPARDL_ECAPACITY: return "workspace too small";
+    case SPARDL_EDEVICE: return "kernel launch failed";
+    default: return "unknown status";
+  }
+}
+
+int spardl_srs_plan(int32_t P, int32_t* distance, int32_t* bag_blocks) {
+  if (P < 1) return SPARDL_EINVAL;
+  const int32_t l = steps_of(P);
+  for (int32_t i = 1; i <= l; ++i) {
+    if (distance) distance[i - 1] = 1 << (l - i);
+    if (bag_blocks) bag_blocks[i - 1] = bag_of(P, l, i);
+  }
+  return l;
+}
+
+size_t spardl_workspace_bytes(int32_t nworkers, int32_t P, int64_t n, int32_t k_blk) {
+  if (!sizes_ok(P, n, k_blk) || nworkers < 1 || nworkers > P) return 0;
+  const Layout L = make_layout(P, n, k_blk);
+  const int64_t cand = std::max<int64_t>((int64_t)nworkers * n, L.pairs_max * 2ll * k_blk);
+  return L.fixed_end + cand_bytes(cand);
+}
+
+int spardl_residual_add(float* acc, int64_t ld_acc, const float* grad, int64_t ld_grad,
+                        int32_t nworkers, int64_t n, int32_t P, void* ws, size_t ws_bytes,
+                        hipStream_t stream) {
+  if (!acc || !grad || nworkers < 1 || n < 1 || n > kMaxN || ld_acc < n || ld_grad < n || P < 0 ||
+      P > n)
+    return SPARDL_EINVAL;
+  if (P == 0 || ws == nullptr) {
+    const bool v4 = aligned16(acc) && aligned16(grad) && ld_acc % 4 == 0 && ld_grad % 4 == 0 && n % 4 == 0;
+    SPARDL_TRY(launch_residual_add(acc, ld_acc, grad, ld_grad, nworkers, n, 1, v4, nullptr, stream));
+    return SPARDL_OK;
+  }
+  if (nworkers > P) return SPARDL_EINVAL;
+  // Only the histogram region is used; its offset and size depend on (P, n).
+  const Layout L = make_layout(P, n, 1);
+  if (ws_bytes < L.state) return SPARDL_ECAPACITY;
+  Ws w = carve(ws, ws_bytes, L);
+  const bool v4 = aligned16(acc) && aligned16(grad) && ld_acc % 4 == 0 && ld_grad % 4 == 0 && blocks_vec4(n, P);
+  SPARDL_TRY(launch_fill(Fill().add(w.hist1, (int64_t)nworkers * P * NB1).r, stream));
+  SPARDL_TRY(launch_residual_add(acc, ld_acc, grad, ld_grad, nworkers, n, P, v4, w.hist1, stream));
+  return SPARDL_OK;
+}
+
+int spardl_block_topk(const float* acc, int64_t ld_acc, int32_t nworkers, int64_t n, int32_t P,
+                      int32_t k_blk, int32_t flags, int32_t* sp_idx, float* sp_val, int32_t* local_idx,
+                      void* ws, size_t ws_bytes, hipStream_t stream) {
+  if (!acc || !sp_idx || !sp_val || !ws || nworkers < 1 || nworkers > P || !sizes_ok(P, n, k_blk) ||
+      ld_acc < n || (flags & ~SPARDL_TOPK_HIST_READY))
+    return SPARDL_EINVAL;
+  const size_t need = spardl_workspace_bytes(nworkers, P, n, k_blk);
+  if (need == 0) return SPARDL_EINVAL;
+  if (ws_bytes < need) return SPARDL_ECAPACITY;
+  const Layout L = make_layout(P, n, k_blk);
+  Ws w = carve(ws, ws_bytes, L);
+  const int64_t units = (int64_t)nworkers * P;
+  const bool v4 = aligned16(acc) && ld_acc % 4 == 0 && blocks_vec4(n, P);
+  Fill f;
+  f.add(w.err, 64).add(w.state, units * ST_WORDS).add(w.tick_a, units).add(w.tick_b, units);
+  f.add(w.stat_a, 2 * units * L.tiles_tk).add(w.stat_b, 2 * units * L.etiles_tk);
+  if (!(flags & SPARDL_TOPK_HIST_READY)) f.add(w.hist1, units * NB1);
+  SPARDL_TRY(launch_fill(f.r, stream));
+  if (!(flags & SPARDL_TOPK_HIST_READY))
+    SPARDL_TRY(launch_hist1(acc, ld_acc, nworkers, n, P, v4, w.hist1, stream));
+  SPARDL_TRY(launch_select1(w.hist1, w.state, units, (uint32_t)k_blk, w.err, stream));
+  SPARDL_TRY(launch_collect(acc, ld_acc, nworkers, n, P, v4, (int32_t)L.tiles_tk, w.state, w.tick_a,
+                            w.stat_a, w.cand_idx, w.cand_val, w.err, stream));
+  SPARDL_TRY(launch_thresh(w.cand_val, 0, units, n, P, k_blk, w.state, w.err, stream));
+  SPARDL_TRY(launch_emit(0, w.cand_idx, w.cand_val, units, n, P, k_blk, 1, w.state, w.tick_b, w.stat_b,
+                         (int32_t)L.etiles_tk, sp_idx, sp_val, local_idx, nullptr, nullptr, nullptr, w.err,
+                         stream));
+  return SPARDL_OK;
+}
+
+int spardl_sparse_merge_topk(int32_t* sp_idx, float* sp_val, int32_t P, int64_t n, int32_t k_blk,
+                             int32_t round, int32_t* drop_idx, float* drop_val, int32_t* drop_cnt,
+                             void* ws, size_t ws_bytes, hipStream_t stream) {
+  if (!sp_idx || !sp_val || !drop_idx || !drop_val || !drop_cnt || !ws || P < 2 ||
+      !sizes_ok(P, n, k_blk))
+    return SPARDL_EINVAL;
+  const int32_t l = steps_of(P);
+  if (round < 1 || round > l) return SPARDL_EINVAL;
+  const Layout L = make_layout(P, n, k_blk);
+  if (ws_bytes < L.fixed_end + cand_bytes(L.pairs_max * 2ll * k_blk)) return SPARDL_ECAPACITY;
+  Ws w = carve(ws, ws_bytes, L);
+  const int32_t d = 1 << (l - round);
+  const int32_t m = bag_of(P, l, round);
+  const int64_t pairs = (int64_t)P * m;
+  Fill f;
+  f.add(w.err, 64).add(w.hist1, pairs * NB1).add(w.state, pairs * ST_WORDS).add(w.tick_a, pairs);
+  f.add(w.tick_b, pairs).add(w.stat_a, 2 * pairs * L.tiles_mg).add(w.stat_b, 2 * pairs * L.etiles_mg);
+  SPARDL_TRY(launch_fill(f.r, stream));
+  SPARDL_TRY(launch_merge(sp_idx, sp_val, P, k_blk, d, m, (int32_t)L.tiles_mg, w.tick_a, w.stat_a,
+                          w.hist1, w.state, w.cand_idx, w.cand_val, w.err, stream));
+  SPARDL_TRY(launch_select1(w.hist1, w.state, pairs, (uint32_t)k_blk, w.err, stream));
+  SPARDL_TRY(launch_thresh(w.cand_val, 1, pairs, n, P, k_blk, w.state, w.err, stream));
+  SPARDL_TRY(launch_emit(1, w.cand_idx, w.cand_val, pairs, n, P, k_blk, m, w.state, w.tick_b, w.stat_b,
+                         (int32_t)L.etiles_mg, sp_idx, sp_val, nullptr, drop_idx, drop_val, drop_cnt,
+                         w.err, stream));
+  return SPARDL_OK;
+}
+
+int spardl_allgather_densify(const int32_t* sp_idx, const float* sp_val, int32_t P, int64_t n,
+                             int32_t k_blk, float* dense, hipStream_t stream) {
+  if (!sp_idx || !sp_val || !dense || !sizes_ok(P, n, k_blk)) return SPARDL_EINVAL;
+  SPARDL_TRY(launch_densify(sp_idx, sp_val, P, n, k_blk, dense, aligned16(dense), stream));
+  return SPARDL_OK;
+}
+
+int spardl_residual_collect(float* acc, int64_t ld_acc, int32_t P, int64_t n, int32_t k_blk,
+                            const int32_t* local_idx, const int32_t* sp_idx,
+                            const int32_t* const* drop_idx, const float* const* drop_val,
+                            const int32_t* const* drop_cnt, void* ws, size_t ws_bytes,
+                            hipStream_t stream) {
+  if (!acc || !local_idx || !sp_idx || !ws || !sizes_ok(P, n, k_blk) || ld_acc < n)
+    return SPARDL_EINVAL;
+  const int32_t l = steps_of(P);
+  if (l > 0 && (!drop_idx || !drop_val || !drop_cnt)) return SPARDL_EINVAL;
+  for (int32_t i = 0; i < l; ++i)
+    if (!drop_idx[i] || !drop_val[i] || !drop_cnt[i]) return SPARDL_EINVAL;
+  const Layout L = make_layout(P, n, k_blk);
+  if (ws_bytes < L.hist1) return SPARDL_ECAPACITY;
+  Ws w = carve(ws, ws_bytes, L);
+  SPARDL_TRY(launch_bitmap(sp_idx, P, n, k_blk, w.bitmap, stream));
+  SPARDL_TRY(launch_grc_zero(acc, ld_acc, P, n, k_blk, local_idx, w.bitmap, stream));
+  for (int32_t i = 1; i <= l; ++i) {
+    const int32_t m = bag_of(P, l, i);
+    SPARDL_TRY(launch_grc_drops(acc, ld_acc, n, m, k_blk, P * m, drop_idx[i - 1], drop_val[i - 1],
+                                drop_cnt[i - 1], w.bitmap, stream));
+  }
+  return SPARDL_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,214 @@
+// Device helpers shared by the SparDL kernels (gfx950, wave64).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace spardl {
+
+// ---------------------------------------------------------------- radix digits
+// The 31-bit magnitude key |v| (fp32 bits without the sign) is selected on in
+// three digits: bits 30..19 (4096 bins), 18..8 (2048 bins), 7..0 (256 bins).
+constexpr int D1_SHIFT = 19;
+constexpr int NB1 = 4096;
+constexpr int D2_SHIFT = 8;
+constexpr int NB2 = 2048;
+constexpr int NB3 = 256;
+
+// ---------------------------------------------------------------- tiling
+constexpr int WAVE = 64;
+constexpr int UNIT = 4096;            // elements one wave streams (16 float4 per lane)
+constexpr int STREAM_WAVES = 4;       // waves per workgroup in the streaming kernels
+constexpr int STREAM_TILE = UNIT * STREAM_WAVES;
+constexpr int MERGE_THREADS = 256;
+constexpr int MERGE_PER_THREAD = 16;
+constexpr int MERGE_TILE = MERGE_THREADS * MERGE_PER_THREAD;   // merged positions per workgroup
+constexpr int EMIT_THREADS = 512;
+constexpr int EMIT_PER_THREAD = 16;
+constexpr int EMIT_TILE = EMIT_THREADS * EMIT_PER_THREAD;      // candidates per emit tile
+constexpr int EMIT_WGS_PER_UNIT = 8;
+constexpr int THRESH_THREADS = 1024;
+constexpr int DENSE_TILE = 4096;
+
+// ---------------------------------------------------------------- state words
+// Per selection unit (a (worker, block) pair or a merge pair), 16 u32:
+enum : int {
+  ST_T1 = 0,        // level-1 threshold bin
+  ST_ABOVE1 = 1,    // entries in bins above ST_T1
+  ST_NEED1 = 2,     // entries still needed from bin ST_T1
+  ST_CNT1 = 3,      // entries in bin ST_T1
+  ST_TGE = 4,       // every candidate with key >= ST_TGE is selected
+  ST_TEQ = 5,       // ... and the first ST_NEEDEQ (by index) with key == ST_TEQ
+  ST_NEEDEQ = 6,
+  ST_COUNT = 7,     // number of candidates (dense, index-ordered)
+  ST_WORDS = 16
+};
+
+constexpr uint32_t ERR_LOOKBACK = 1u;
+constexpr uint32_t ERR_COUNT = 2u;
+
+__device__ __forceinline__ uint32_t mag_key(float v) { return __float_as_uint(v) & 0x7FFFFFFFu; }
+
+__host__ __device__ __forceinline__ int64_t blk_start(int64_t b, int64_t n, int64_t P) {
+  return (b * n) / P;
+}
+
+__device__ __forceinline__ int64_t block_of(int64_t x, int64_t n, int64_t P) {
+  int64_t b = (x * P) / n;
+  while (b + 1 < P && blk_start(b + 1, n, P) <= x) ++b;
+  while (b > 0 && blk_start(b, n, P) > x) --b;
+  return b;
+}
+
+__device__ __forceinline__ int lane_id() { return threadIdx.x & (WAVE - 1); }
+__device__ __forceinline__ int wave_id() { return threadIdx.x / WAVE; }
+
+__device__ __forceinline__ uint32_t popc64(uint64_t m) { return (uint32_t)__popcll(m); }
+
+// Inclusive prefix sum across the 64 lanes of a wave.
+__device__ __forceinline__ uint32_t wave_incl_scan(uint32_t v) {
+  const int lane = lane_id();
+#pragma unroll
+  for (int d = 1; d < WAVE; d <<= 1) {
+    uint32_t t = __shfl_up(v, d, WAVE);
+    if (lane >= d) v += t;
+  }
+  return v;
+}
+
+__device__ __forceinline__ uint32_t wave_sum(uint32_t v) {
+#pragma unroll
+  for (int d = WAVE / 2; d > 0; d >>= 1) v += __shfl_xor(v, d, WAVE);
+  return v;
+}
+
+// Exclusive prefix sum of one value per thread over the workgroup, in thread
+// order.  `scratch` needs blockDim/64 + 1 words of LDS.  Returns the exclusive
+// prefix and writes the workgroup total to *total.  Contains barriers.
+__device__ __forceinline__ uint32_t block_excl_scan(uint32_t v, uint32_t* scratch, uint32_t* total) {
+  const int nw = blockDim.x / WAVE;
+  uint32_t incl = wave_incl_scan(v);
+  if (lane_id() == WAVE - 1) scratch[wave_id()] = incl;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    uint32_t run = 0;
+    for (int i = 0; i < nw; ++i) {
+      uint32_t t = scratch[i];
+      scratch[i] = run;
+      run += t;
+    }
+    scratch[nw] = run;
+  }
+  __syncthreads();
+  uint32_t r = scratch[wave_id()] + incl - v;
+  *total = scratch[nw];
+  __syncthreads();
+  return r;
+}
+
+// Select on a histogram in descending bin order: find bin T such that
+// count(bins > T) < need <= count(bins >= T).  hist is in LDS with nb bins.
+// Every thread gets the answer.  `scratch` needs blockDim/64 + 4 words of LDS.
+// If the histogram holds fewer than `need` entries, *ok is 0 and T = 0.
+__device__ __forceinline__ void block_select_desc(const uint32_t* hist, int nb, uint32_t need,
+                                                  uint32_t* scratch, uint32_t* T, uint32_t* above,
+                                                  uint32_t* cnt, uint32_t* ok) {
+  const int nt = blockDim.x;
+  const int per = (nb + nt - 1) / nt;
+  // thread t owns bins [nb - per (t+1), nb - per t) (the highest bins go to thread 0)
+  const int hi = nb - per * (int)threadIdx.x;
+  const int lo = hi - per;
+  uint32_t s = 0;
+  for (int bin = hi - 1; bin >= lo && bin >= 0; --bin) s += hist[bin];
+  uint32_t tot;
+  uint32_t ex = block_excl_scan(s, scratch, &tot);
+  const int nw = nt / WAVE;
+  if (threadIdx.x == 0) scratch[nw + 1] = 0;   // found flag
+  __syncthreads();
+  if (ex < need && ex + s >= need) {
+    uint32_t run = ex;
+    for (int bin = hi - 1; bin >= lo && bin >= 0; --bin) {
+      uint32_t h = hist[bin];
+      if (run + h >= need) {
+        scratch[nw + 1] = 1;
+        scratch[nw + 2] = (uint32_t)bin;
+        scratch[nw + 3] = run;
+        break;
+      }
+      run += h;
+    }
+  }
+  __syncthreads();
+  *ok = scratch[nw + 1];
+  if (*ok) {
+    *T = scratch[nw + 2];
+    *above = scratch[nw + 3];
+    *cnt = hist[*T];
+  } else {
+    *T = 0;
+    *above = 0;
+    *cnt = 0;
+  }
+  __syncthreads();
+}
+
+// ---------------------------------------------------------------- ordered prefix across tiles
+// Decoupled look-back (single-pass ordered prefix): each tile of a unit
+// publishes its own aggregate, then walks back over its predecessors until it
+// meets an inclusive prefix.  Tiles take their index from a ticket counter in
+// start order, so every predecessor is already running and finishes its own
+// publication without waiting on later tiles.  The wait is additionally
+// bounded: past LB_SPIN_LIMIT polls the tile records ERR_LOOKBACK and carries
+// on with a wrong prefix, so the kernel always exits.
+// A status word is [63:62] flag (0 none, 1 aggregate, 2 inclusive),
+// [61:31] field b, [30:0] field a.
+constexpr uint64_t LB_AGG = 1ull << 62;
+constexpr uint64_t LB_INC = 2ull << 62;
+constexpr uint32_t LB_SPIN_LIMIT = 1u << 22;
+
+__device__ __forceinline__ uint64_t lb_pack(uint64_t flag, uint32_t a, uint32_t b) {
+  return flag | ((uint64_t)(b & 0x7FFFFFFFu) << 31) | (uint64_t)(a & 0x7FFFFFFFu);
+}
+
+__device__ __forceinline__ void lb_store(uint64_t* p, uint64_t v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+__device__ __forceinline__ uint64_t lb_load(uint64_t* p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Called by one thread.  st = the unit's status words (one per tile).
+__device__ __forceinline__ void lookback(uint64_t* st, uint32_t tile, uint32_t agg_a, uint32_t agg_b,
+                                         uint32_t* ex_a, uint32_t* ex_b, uint32_t* err) {
+  if (tile == 0) {
+    lb_store(&st[0], lb_pack(LB_INC, agg_a, agg_b));
+    *ex_a = 0;
+    *ex_b = 0;
+    return;
+  }
+  lb_store(&st[tile], lb_pack(LB_AGG, agg_a, agg_b));
+  uint32_t a = 0, b = 0, spins = 0;
+  int64_t t = (int64_t)tile - 1;
+  for (;;) {
+    uint64_t s = lb_load(&st[t]);
+    uint64_t f = s >> 62;
+    if (f == 0) {
+      if (++spins > LB_SPIN_LIMIT) {
+        atomicOr(err, ERR_LOOKBACK);
+        break;
+      }
+      __builtin_amdgcn_s_sleep(1);
+      continue;
+    }
+    a += (uint32_t)(s & 0x7FFFFFFFu);
+    b += (uint32_t)((s >> 31) & 0x7FFFFFFFu);
+    if (f == 2 || t == 0) break;
+    --t;
+  }
+  *ex_a = a;
+  *ex_b = b;
+  lb_store(&st[tile], lb_pack(LB_INC, a + agg_a, b + agg_b));
+}
+
+}  // namespace spardl

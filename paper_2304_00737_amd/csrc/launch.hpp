@@ -1,0 +1,49 @@
+// Host-side launchers of the kernels in kernels.hip (internal to libspardl).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace spardl {
+
+constexpr int FILL_MAX = 8;
+struct FillRanges {
+  uint32_t* ptr[FILL_MAX];
+  int64_t len[FILL_MAX];
+  int count;
+};
+
+hipError_t launch_fill(const FillRanges& r, hipStream_t s);
+hipError_t launch_residual_add(float* acc, int64_t ld_acc, const float* grad, int64_t ld_grad,
+                               int32_t nworkers, int64_t n, int32_t P, bool vec4, uint32_t* hist1,
+                               hipStream_t s);
+hipError_t launch_hist1(const float* acc, int64_t ld_acc, int32_t nworkers, int64_t n, int32_t P,
+                        bool vec4, uint32_t* hist1, hipStream_t s);
+hipError_t launch_select1(const uint32_t* hist1, uint32_t* state, int64_t nunits, uint32_t need,
+                          uint32_t* err, hipStream_t s);
+hipError_t launch_collect(const float* acc, int64_t ld_acc, int32_t nworkers, int64_t n, int32_t P,
+                          bool vec4, int32_t tiles_per_unit, uint32_t* state, uint32_t* tickets,
+                          uint64_t* status, int32_t* cand_idx, float* cand_val, uint32_t* err,
+                          hipStream_t s);
+hipError_t launch_thresh(const float* cand_val, int mode, int64_t nunits, int64_t n, int32_t P,
+                         int32_t kb, uint32_t* state, uint32_t* err, hipStream_t s);
+hipError_t launch_emit(int mode, const int32_t* cand_idx, const float* cand_val, int64_t nunits,
+                       int64_t n, int32_t P, int32_t kb, int32_t m, const uint32_t* state,
+                       uint32_t* tickets, uint64_t* status, int32_t tiles_per_unit, int32_t* out_idx,
+                       float* out_val, int32_t* local_idx, int32_t* drop_idx, float* drop_val,
+                       int32_t* drop_cnt, uint32_t* err, hipStream_t s);
+hipError_t launch_merge(const int32_t* sp_idx, const float* sp_val, int32_t P, int32_t kb, int32_t d,
+                        int32_t m, int32_t tiles_per_pair, uint32_t* tickets, uint64_t* status,
+                        uint32_t* hist1, uint32_t* state, int32_t* U_idx, float* U_val, uint32_t* err,
+                        hipStream_t s);
+hipError_t launch_densify(const int32_t* sp_idx, const float* sp_val, int32_t P, int64_t n, int32_t kb,
+                          float* dense, bool vec4, hipStream_t s);
+hipError_t launch_bitmap(const int32_t* sp_idx, int32_t P, int64_t n, int32_t kb, uint32_t* bm,
+                         hipStream_t s);
+hipError_t launch_grc_zero(float* acc, int64_t ld_acc, int32_t P, int64_t n, int32_t kb, const int32_t* local_idx,
+                           const uint32_t* bm, hipStream_t s);
+hipError_t launch_grc_drops(float* acc, int64_t ld_acc, int64_t n, int32_t m, int32_t kb, int32_t npairs,
+                            const int32_t* drop_idx, const float* drop_val, const int32_t* drop_cnt,
+                            const uint32_t* bm, hipStream_t s);
+
+}  // namespace spardl

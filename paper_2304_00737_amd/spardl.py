@@ -1,0 +1,190 @@
+"""Thin Python binding of libspardl.so (argument marshalling only).
+
+Every function has the name of the C entry point in include/spardl.h without
+the ``spardl_`` prefix, takes torch tensors for device buffers (torch is used
+for device memory and streams only), checks the returned status and raises
+SpardlError on failure.  All compute runs in the HIP kernels of libspardl.so;
+there is no fallback: if the library is missing, importing this module fails.
+"""
+
+from __future__ import annotations
+
+import ctypes
+import os
+
+import torch
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libspardl.so")
+
+OK, EINVAL, ECAPACITY, EDEVICE = 0, -1, -2, -3
+TOPK_HIST_READY = 1
+WS_ERR_LOOKBACK = 1
+WS_ERR_COUNT = 2
+
+if not os.path.exists(LIB_PATH):
+    raise ImportError(f"{LIB_PATH} is not built (run __graft_entry__.build()); "
+                      "there is no fallback implementation")
+
+_lib = ctypes.CDLL(LIB_PATH)
+_p, _i32, _i64, _sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t
+
+_lib.spardl_strerror.argtypes = [ctypes.c_int]
+_lib.spardl_strerror.restype = ctypes.c_char_p
+_lib.spardl_srs_plan.argtypes = [_i32, _p, _p]
+_lib.spardl_srs_plan.restype = ctypes.c_int
+_lib.spardl_workspace_bytes.argtypes = [_i32, _i32, _i64, _i32]
+_lib.spardl_workspace_bytes.restype = _sz
+_lib.spardl_residual_add.argtypes = [_p, _i64, _p, _i64, _i32, _i64, _i32, _p, _sz, _p]
+_lib.spardl_block_topk.argtypes = [_p, _i64, _i32, _i64, _i32, _i32, _i32, _p, _p, _p, _p, _sz, _p]
+_lib.spardl_sparse_merge_topk.argtypes = [_p, _p, _i32, _i64, _i32, _i32, _p, _p, _p, _p, _sz, _p]
+_lib.spardl_allgather_densify.argtypes = [_p, _p, _i32, _i64, _i32, _p, _p]
+_lib.spardl_residual_collect.argtypes = [_p, _i64, _i32, _i64, _i32, _p, _p, _p, _p, _p, _p, _sz, _p]
+for _f in ("residual_add", "block_topk", "sparse_merge_topk", "allgather_densify", "residual_collect"):
+    getattr(_lib, "spardl_" + _f).restype = ctypes.c_int
+
+
+class SpardlError(RuntimeError):
+    def __init__(self, fn: str, status: int):
+        super().__init__(f"spardl_{fn}: {_lib.spardl_strerror(status).decode()} ({status})")
+        self.status = status
+
+
+def _check(fn: str, status: int) -> None:
+    if status != OK:
+        raise SpardlError(fn, status)
+
+
+def _ptr(t) -> int:
+    if t is None:
+        return None
+    if isinstance(t, int):
+        return t
+    return t.data_ptr()
+
+
+def _stream(stream) -> int:
+    if stream is None:
+        return torch.cuda.current_stream().cuda_stream
+    if isinstance(stream, int):
+        return stream
+    return stream.cuda_stream
+
+
+def _ld(t, n) -> int:
+    return t.stride(0) if t.dim() == 2 else n
+
+
+def strerror(status: int) -> str:
+    return _lib.spardl_strerror(status).decode()
+
+
+def srs_plan(P: int):
+    """(l, distances, bag_blocks) of the Spar-Reduce-Scatter steps."""
+    dist = (ctypes.c_int32 * 32)()
+    bags = (ctypes.c_int32 * 32)()
+    l = _lib.spardl_srs_plan(P, dist, bags)
+    if l < 0:
+        raise SpardlError("srs_plan", l)
+    return l, list(dist[:l]), list(bags[:l])
+
+
+def workspace_bytes(nworkers: int, P: int, n: int, k_blk: int) -> int:
+    return int(_lib.spardl_workspace_bytes(nworkers, P, n, k_blk))
+
+
+def residual_add(acc, grad, nworkers: int, n: int, P: int = 0, ws=None, *, ld_acc=None, ld_grad=None,
+                 stream=None) -> None:
+    ld_acc = _ld(acc, n) if ld_acc is None else ld_acc
+    ld_grad = _ld(grad, n) if ld_grad is None else ld_grad
+    ws_bytes = ws.numel() * ws.element_size() if ws is not None else 0
+    _check("residual_add", _lib.spardl_residual_add(_ptr(acc), ld_acc, _ptr(grad), ld_grad, nworkers, n, P,
+                                                    _ptr(ws), ws_bytes, _stream(stream)))
+
+
+def block_topk(acc, nworkers: int, n: int, P: int, k_blk: int, sp_idx, sp_val, local_idx=None, ws=None,
+               flags: int = 0, *, ld_acc=None, stream=None) -> None:
+    ld_acc = _ld(acc, n) if ld_acc is None else ld_acc
+    _check("block_topk", _lib.spardl_block_topk(_ptr(acc), ld_acc, nworkers, n, P, k_blk, flags, _ptr(sp_idx),
+                                                _ptr(sp_val), _ptr(local_idx), _ptr(ws),
+                                                ws.numel() * ws.element_size(), _stream(stream)))
+
+
+def sparse_merge_topk(sp_idx, sp_val, P: int, n: int, k_blk: int, round: int, drop_idx, drop_val, drop_cnt,
+                      ws, *, stream=None) -> None:
+    _check("sparse_merge_topk", _lib.spardl_sparse_merge_topk(
+        _ptr(sp_idx), _ptr(sp_val), P, n, k_blk, round, _ptr(drop_idx), _ptr(drop_val), _ptr(drop_cnt),
+        _ptr(ws), ws.numel() * ws.element_size(), _stream(stream)))
+
+
+def allgather_densify(sp_idx, sp_val, P: int, n: int, k_blk: int, dense, *, stream=None) -> None:
+    _check("allgather_densify", _lib.spardl_allgather_densify(_ptr(sp_idx), _ptr(sp_val), P, n, k_blk,
+                                                              _ptr(dense), _stream(stream)))
+
+
+def residual_collect(acc, P: int, n: int, k_blk: int, local_idx, sp_idx, drop_idx, drop_val, drop_cnt, ws,
+                     *, ld_acc=None, stream=None) -> None:
+    """drop_idx / drop_val / drop_cnt: sequences of l tensors (one per step)."""
+    ld_acc = _ld(acc, n) if ld_acc is None else ld_acc
+    l = len(drop_idx)
+    arr = lambda ts: (ctypes.c_void_p * max(l, 1))(*[_ptr(t) for t in ts]) if l else None
+    _check("residual_collect", _lib.spardl_residual_collect(
+        _ptr(acc), ld_acc, P, n, k_blk, _ptr(local_idx), _ptr(sp_idx), arr(drop_idx), arr(drop_val),
+        arr(drop_cnt), _ptr(ws), ws.numel() * ws.element_size(), _stream(stream)))
+
+
+def ws_error(ws) -> int:
+    """Error word at the start of a workspace (synchronises the current stream)."""
+    return int(ws[:4].view(torch.int32).cpu().item())
+
+
+class SparDLStep:
+    """Buffers for P simulated workers and one synchronisation step through the C ABI.
+
+    acc[P, n] holds the residual between steps.  After step(grad): dense holds
+    the global update, sp_idx/sp_val the sparse state (final block b in
+    sp[b, b]), local_idx the local selections and drop_* the per-step drops.
+    """
+
+    def __init__(self, P: int, n: int, k_blk: int, device="cuda", fused: bool = True):
+        self.P, self.n, self.k_blk, self.fused = P, n, k_blk, fused
+        dev = torch.device(device)
+        self.acc = torch.zeros((P, n), dtype=torch.float32, device=dev)
+        self.sp_idx = torch.empty((P, P, k_blk), dtype=torch.int32, device=dev)
+        self.sp_val = torch.empty((P, P, k_blk), dtype=torch.float32, device=dev)
+        self.local_idx = torch.empty((P, P, k_blk), dtype=torch.int32, device=dev)
+        self.l, self.distance, self.bags = srs_plan(P)
+        self.drop_idx = [torch.empty((P, m, k_blk), dtype=torch.int32, device=dev) for m in self.bags]
+        self.drop_val = [torch.empty((P, m, k_blk), dtype=torch.float32, device=dev) for m in self.bags]
+        self.drop_cnt = [torch.empty((P, m), dtype=torch.int32, device=dev) for m in self.bags]
+        self.dense = torch.empty(n, dtype=torch.float32, device=dev)
+        self.ws = torch.empty(workspace_bytes(P, P, n, k_blk), dtype=torch.uint8, device=dev)
+
+    def residual_add(self, grad, stream=None):
+        if self.fused:
+            residual_add(self.acc, grad, self.P, self.n, self.P, self.ws, stream=stream)
+        else:
+            residual_add(self.acc, grad, self.P, self.n, 0, None, stream=stream)
+
+    def block_topk(self, stream=None):
+        block_topk(self.acc, self.P, self.n, self.P, self.k_blk, self.sp_idx, self.sp_val, self.local_idx,
+                   self.ws, TOPK_HIST_READY if self.fused else 0, stream=stream)
+
+    def merge_round(self, i: int, stream=None):
+        sparse_merge_topk(self.sp_idx, self.sp_val, self.P, self.n, self.k_blk, i, self.drop_idx[i - 1],
+                          self.drop_val[i - 1], self.drop_cnt[i - 1], self.ws, stream=stream)
+
+    def densify(self, stream=None):
+        allgather_densify(self.sp_idx, self.sp_val, self.P, self.n, self.k_blk, self.dense, stream=stream)
+
+    def collect(self, stream=None):
+        residual_collect(self.acc, self.P, self.n, self.k_blk, self.local_idx, self.sp_idx, self.drop_idx,
+                         self.drop_val, self.drop_cnt, self.ws, stream=stream)
+
+    def step(self, grad, stream=None):
+        self.residual_add(grad, stream)
+        self.block_topk(stream)
+        for i in range(1, self.l + 1):
+            self.merge_round(i, stream)
+        self.densify(stream)
+        self.collect(stream)

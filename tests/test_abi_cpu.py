@@ -1,0 +1,116 @@
+"""C-ABI checks that need no GPU: the library loads, exports every entry point
+declared in include/spardl.h, its host-side schedule matches the paper's
+examples and the oracle's schedule, and argument errors are reported before
+anything is enqueued."""
+
+import ctypes
+import json
+import os
+import re
+
+import pytest
+
+from oracle import spardl_oracle as so
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+LIB = os.path.join(ROOT, "paper_2304_00737_amd", "libspardl.so")
+HEADER = os.path.join(ROOT, "include", "spardl.h")
+
+pytestmark = pytest.mark.skipif(not os.path.exists(LIB), reason="libspardl.so not built")
+
+
+def _lib():
+    lib = ctypes.CDLL(LIB)
+    lib.spardl_srs_plan.argtypes = [ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p]
+    lib.spardl_workspace_bytes.argtypes = [ctypes.c_int32, ctypes.c_int32, ctypes.c_int64, ctypes.c_int32]
+    lib.spardl_workspace_bytes.restype = ctypes.c_size_t
+    lib.spardl_strerror.restype = ctypes.c_char_p
+    return lib
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    return sorted(set(re.findall(r"^\s*(?:const\s+)?\w+\*?\s+(spardl_\w+)\s*\(", text, re.M)))
+
+
+def test_exports_every_declared_symbol():
+    names = declared_functions()
+    assert len(names) >= 8
+    lib = _lib()
+    for name in names:
+        assert hasattr(lib, name), name
+
+
+def test_srs_plan_matches_oracle_and_examples():
+    lib = _lib()
+    for P in range(1, 200):
+        d = (ctypes.c_int32 * 32)()
+        m = (ctypes.c_int32 * 32)()
+        l = lib.spardl_srs_plan(P, d, m)
+        steps = so.srs_schedule(P)
+        assert l == len(steps) == so.num_steps(P)
+        for st in steps:
+            assert d[st.i - 1] == st.distance
+            assert m[st.i - 1] == len(st.received_bag[0])
+            for w in range(P):
+                # the library's closed form: worker w receives blocks w .. w+m-1 from w - d
+                assert list(st.received_bag[w]) == [(w + t) % P for t in range(m[st.i - 1])]
+                assert st.source[w] == (w - d[st.i - 1]) % P
+    g = json.load(open(os.path.join(ROOT, "tests", "golden", "srs_examples_p6.json")))
+    d = (ctypes.c_int32 * 32)()
+    m = (ctypes.c_int32 * 32)()
+    assert lib.spardl_srs_plan(6, d, m) == g["l"]
+    assert [d[i] for i in range(3)] == [s["distance"] for s in g["steps"]]
+    assert [m[i] for i in range(3)] == [s["sent_blocks"] for s in g["steps"]]
+    assert lib.spardl_srs_plan(0, None, None) == -1
+
+
+def test_workspace_bytes():
+    lib = _lib()
+    assert lib.spardl_workspace_bytes(1, 4, 100, 0) == 0          # k_blk < 1
+    assert lib.spardl_workspace_bytes(1, 4, 100, 26) == 0         # k_blk > floor(n/P)
+    assert lib.spardl_workspace_bytes(5, 4, 100, 3) == 0          # nworkers > P
+    assert lib.spardl_workspace_bytes(1, 4, 2 ** 31, 3) == 0      # n >= 2^31
+    a = lib.spardl_workspace_bytes(1, 8, 25_600_000, 32_000)
+    b = lib.spardl_workspace_bytes(8, 8, 25_600_000, 32_000)
+    assert 0 < a < b and b - a >= 7 * 25_600_000 * 8
+    assert a % 256 == 0 and b % 256 == 0
+
+
+def test_argument_errors_enqueue_nothing():
+    """Invalid calls return a status before any HIP call (safe without a GPU)."""
+    lib = _lib()
+    p = ctypes.c_void_p(0x1000)      # never dereferenced: validation fails first
+    null = ctypes.c_void_p(0)
+    i64, i32, sz = ctypes.c_int64, ctypes.c_int32, ctypes.c_size_t
+    EINVAL, ECAP = -1, -2
+    # residual_add: NULL acc, ld < n, P > n
+    assert lib.spardl_residual_add(null, i64(10), p, i64(10), i32(1), i64(10), i32(0), null, sz(0), null) == EINVAL
+    assert lib.spardl_residual_add(p, i64(9), p, i64(10), i32(1), i64(10), i32(0), null, sz(0), null) == EINVAL
+    assert lib.spardl_residual_add(p, i64(10), p, i64(10), i32(1), i64(10), i32(11), p, sz(1 << 20), null) == EINVAL
+    assert lib.spardl_residual_add(p, i64(100), p, i64(100), i32(2), i64(100), i32(4), p, sz(16), null) == ECAP
+    # block_topk: k_blk too large, flags unknown, nworkers > P, small workspace
+    assert lib.spardl_block_topk(p, i64(100), i32(1), i64(100), i32(4), i32(26), i32(0), p, p, null, p,
+                                 sz(1 << 30), null) == EINVAL
+    assert lib.spardl_block_topk(p, i64(100), i32(1), i64(100), i32(4), i32(3), i32(4), p, p, null, p,
+                                 sz(1 << 30), null) == EINVAL
+    assert lib.spardl_block_topk(p, i64(100), i32(5), i64(100), i32(4), i32(3), i32(0), p, p, null, p,
+                                 sz(1 << 30), null) == EINVAL
+    assert lib.spardl_block_topk(p, i64(100), i32(1), i64(100), i32(4), i32(3), i32(0), p, p, null, p,
+                                 sz(64), null) == ECAP
+    # merge: P < 2, round out of range, small workspace
+    assert lib.spardl_sparse_merge_topk(p, p, i32(1), i64(100), i32(3), i32(1), p, p, p, p, sz(1 << 30), null) == EINVAL
+    assert lib.spardl_sparse_merge_topk(p, p, i32(6), i64(600), i32(3), i32(4), p, p, p, p, sz(1 << 30), null) == EINVAL
+    assert lib.spardl_sparse_merge_topk(p, p, i32(6), i64(600), i32(3), i32(0), p, p, p, p, sz(1 << 30), null) == EINVAL
+    assert lib.spardl_sparse_merge_topk(p, p, i32(6), i64(600), i32(3), i32(1), p, p, p, p, sz(64), null) == ECAP
+    # densify: n < P, NULL output
+    assert lib.spardl_allgather_densify(p, p, i32(8), i64(7), i32(1), p, null) == EINVAL
+    assert lib.spardl_allgather_densify(p, p, i32(2), i64(8), i32(1), null, null) == EINVAL
+    # residual_collect: missing per-step drop arrays for P > 1
+    assert lib.spardl_residual_collect(p, i64(100), i32(4), i64(100), i32(3), p, p, null, null, null, p,
+                                       sz(1 << 30), null) == EINVAL
+    arr = (ctypes.c_void_p * 2)(0x1000, 0)
+    assert lib.spardl_residual_collect(p, i64(100), i32(4), i64(100), i32(3), p, p, arr, arr, arr, p,
+                                       sz(1 << 30), null) == EINVAL
+    for s in (0, -1, -2, -3, 7):
+        assert lib.spardl_strerror(s)
