@@ -1,0 +1,213 @@
+"""Throughput of one full SparDL synchronisation step (d = 1) on one MI355X.
+
+A step is the whole hot path for P simulated workers over one batch of
+gradients: residual add (fused level-1 histogram), block top-k/P, the
+ceil(log2 P) Spar-Reduce-Scatter steps, the All-Gather decode to a dense
+update, and global residual collection.  The default workload is the
+ResNet-50-sized one: P = 8, n = 25.6M fp32 per worker, density 1%, three
+distinct gradient batches cycled with the residual carried across steps.
+Inputs are generated on the host and resident in HBM before timing starts.
+
+Prints one JSON line (see the "metric" field); timing uses HIP events on the
+stream the kernels run on.
+"""
+
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0   # MI355X HBM3E peak, GB/s
+
+
+def _kernel_src_hash() -> str:
+    h = hashlib.sha256()
+    for f in ("kernels.hip", "common.hpp", "api.hip"):
+        with open(os.path.join(ROOT, "paper_2304_00737_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def _traffic_from_profiles(kernel: str, src_hash: str, units_per_launch: float):
+    """HBM bytes per launch from committed rocprofv3 counter runs, if they were
+    taken on the current kernel source; otherwise None."""
+    path = os.path.join(ROOT, "profiles", "traffic.json")
+    try:
+        with open(path) as fh:
+            rec = json.load(fh)
+    except (OSError, ValueError):
+        return None
+    k = rec.get("kernels", {}).get(kernel)
+    if not k or rec.get("src_hash") != src_hash:
+        return None
+    return k.get("bytes_per_launch")
+
+
+def cpu_baseline(wl, max_seconds: float = 25.0):
+    """The oracle, as it stands, on a bounded sample of the same workload:
+    whole block indices of one step (blocks never interact, so a block index
+    is a self-contained unit of the step)."""
+    import numpy as np
+
+    from oracle import spardl_oracle as so
+    from paper_2304_00737_amd import workloads as W
+
+    P, n, kb = wl.P, wl.n, wl.k_blk
+    bounds = so.block_bounds(n, P)
+    done_elems, elapsed, blocks = 0, 0.0, []
+    for b in range(P):
+        acc = [{b: np.zeros(bounds[b + 1] - bounds[b], np.float32)} for _ in range(P)]
+        grad = [{b: W.gradient(wl, 1, w, bounds[b], bounds[b + 1] - bounds[b])} for w in range(P)]
+        t0 = time.perf_counter()
+        so.spardl_step(acc, grad, P, n, kb, blocks=[b])
+        elapsed += time.perf_counter() - t0
+        done_elems += P * (bounds[b + 1] - bounds[b])
+        blocks.append(b)
+        if elapsed > max_seconds:
+            break
+    return {"value": done_elems / elapsed, "unit": "elements/s", "cores": 1, "kind": "oracle",
+            "sample": f"step 1 of the same workload restricted to block indices {blocks} of {P} "
+                      f"({done_elems} gradient elements, {elapsed:.1f} s; numpy, single thread)"}
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=30)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", type=int, default=2, help="synthetic workload id (1-4)")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+
+    if args.gpus != 1:
+        print(json.dumps({"error": "this build runs the P simulated workers on one GPU; "
+                                   "--gpus must be 1 (no multi-GPU path is built)"}))
+        return 2
+
+    import numpy as np
+    import torch
+
+    from paper_2304_00737_amd import spardl
+    from paper_2304_00737_amd import workloads as W
+
+    wl = W.config(args.workload)
+    P, n, kb = wl.P, wl.n, wl.k_blk
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+
+    # inputs: the workload's distinct gradient batches, resident in HBM
+    t0 = time.time()
+    grads = []
+    for t in range(1, wl.steps + 1):
+        g = torch.empty((P, n), dtype=torch.float32, device=dev)
+        host = np.empty(n, np.float32)
+        for w in range(P):
+            W.fill(host, wl, t, w)
+            g[w].copy_(torch.from_numpy(host))
+        grads.append(g)
+    torch.cuda.synchronize()
+    print(f"# generated {wl.steps} x {P} x {n} gradients in {time.time() - t0:.1f}s", file=sys.stderr, flush=True)
+
+    st = spardl.SparDLStep(P, n, kb, device=dev)
+    stream = torch.cuda.current_stream()
+
+    calls = ["residual_add", "block_topk"] + [f"merge_step{i}" for i in range(1, st.l + 1)] + \
+            ["allgather_densify", "residual_collect"]
+
+    def run_step(j, ev=None):
+        g = grads[j % len(grads)]
+        fns = [lambda: st.residual_add(g), st.block_topk] + \
+              [(lambda i=i: st.merge_round(i)) for i in range(1, st.l + 1)] + [st.densify, st.collect]
+        for c, f in enumerate(fns):
+            if ev is not None:
+                ev[c][0].record(stream)
+            f()
+            if ev is not None:
+                ev[c][1].record(stream)
+
+    for j in range(args.warmup):
+        run_step(j)
+    torch.cuda.synchronize()
+    assert spardl.ws_error(st.ws) == 0
+
+    evs = [[[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in calls] for _ in range(args.steps)]
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    wall0 = time.perf_counter()
+    start.record(stream)
+    for j in range(args.steps):
+        run_step(args.warmup + j, evs[j])
+    end.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - wall0
+    assert spardl.ws_error(st.ws) == 0
+    total_ms = start.elapsed_time(end)
+    ms_per_step = total_ms / args.steps
+    per_call_ms = {c: sum(evs[j][ci][0].elapsed_time(evs[j][ci][1]) for j in range(args.steps)) / args.steps
+                   for ci, c in enumerate(calls)}
+
+    elems = P * n
+    value = elems / (ms_per_step * 1e-3)
+
+    # algorithmic HBM bytes per call (values and indices are 4 bytes)
+    pairs = [P * m for m in st.bags]
+    alg = {
+        "residual_add": 12.0 * P * n,                              # read G, read xi, write A
+        "block_topk": 4.0 * P * n + 12.0 * P * P * kb,             # read A; write idx, val, local idx
+        "allgather_densify": 4.0 * n + 8.0 * P * kb,               # write u; read the final blocks
+    }
+    for i, pc in enumerate(pairs, start=1):
+        alg[f"merge_step{i}"] = 32.0 * pc * kb                     # read held + received, write kept + dropped
+    dc = [t.cpu().numpy() for t in st.drop_cnt]
+    drops_total = float(sum(int(d.sum()) for d in dc))
+    # read local idx, final idx, drop lists; read+write touched residual entries (upper bound)
+    alg["residual_collect"] = 4.0 * P * P * kb + 4.0 * P * kb + 8.0 * drops_total + 8.0 * (P * P * kb + drops_total)
+    dominant = max(calls, key=lambda c: per_call_ms[c])
+    dom_ms = per_call_ms[dominant]
+    achieved = alg[dominant] / (dom_ms * 1e-3) / 1e9
+    src_hash = _kernel_src_hash()
+    traffic = _traffic_from_profiles(dominant, src_hash, 1.0)
+    core_bytes = sum(v for k, v in alg.items() if k != "allgather_densify")
+    full_bytes = sum(alg.values())
+
+    out = {
+        "metric": "gradient elements/sec per full SparDL step (P=8 virtual); % of HBM peak",
+        "value": value,
+        "unit": "elements/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": wl.name, "P": P, "n_per_worker": n, "density": f"{wl.density[0]}/{wl.density[1]}",
+                   "k_per_block": kb, "gradient_batches": wl.steps, "residual": "carried across steps",
+                   "segments": len(wl.seg_len), "seed": W.SEED_BASE},
+        "roofline": {"bound": "hbm", "kernel": dominant, "achieved": achieved, "peak": HBM_PEAK_GBS,
+                     "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS, "traffic": traffic,
+                     "alg_bytes_per_launch": alg[dominant], "avg_launch_ms": dom_ms},
+        "step_roofline": {"alg_bytes_full": full_bytes, "alg_bytes_core": core_bytes,
+                          "achieved_full_GBs": full_bytes / (ms_per_step * 1e-3) / 1e9,
+                          "frac_full": full_bytes / (ms_per_step * 1e-3) / 1e9 / HBM_PEAK_GBS},
+        "per_call_ms": per_call_ms,
+        "wall_s_timed": wall,
+        "kernel_src": src_hash,
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(wl)
+    print(json.dumps(out), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

@@ -34,13 +34,13 @@ inline int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 
 // Workspace layout.  Everything before the candidate region depends only on
 // (P, n, k_blk), so every call finds the same offsets; the candidate region
-// takes the rest of ws (index array, then value array, split in the middle).
+// takes the rest of ws, split into three equal arrays (candidate index,
+// candidate value, threshold-bin key).
 struct Layout {
-  size_t err = 0, bitmap = 0, hist1 = 0, state = 0, tick_a = 0, tick_b = 0, stat_a = 0, stat_b = 0;
+  size_t err = 0, bitmap = 0, hist1 = 0, state = 0, slot_cnt = 0, slot_nbin = 0, slot_above = 0, pre_all = 0,
+         pre_ge = 0, pre_eq = 0;
   size_t fixed_end = 0;
-  int64_t units = 0, tiles_tk = 0, etiles_tk = 0, tiles_mg = 0, etiles_mg = 0;
-  int64_t stat_a_n = 0, stat_b_n = 0;
-  int64_t pairs_max = 0;
+  int64_t units = 0, tiles_tk = 0, groups_tk = 0, tiles_mg = 0, slot_n = 0, pairs_max = 0;
 };
 
 Layout make_layout(int32_t P, int64_t n, int32_t kb) {
@@ -51,61 +51,61 @@ Layout make_layout(int32_t P, int64_t n, int32_t kb) {
   const int64_t maxlen = ceil_div(n, P);
   L.pairs_max = (int64_t)P * mmax;
   L.units = std::max<int64_t>((int64_t)P * P, L.pairs_max);
-  L.tiles_tk = ceil_div(maxlen, STREAM_TILE);
-  L.etiles_tk = ceil_div(maxlen, EMIT_TILE);
+  L.tiles_tk = ceil_div(maxlen, SLOT);
+  L.groups_tk = ceil_div(L.tiles_tk, EMIT_GROUP_TK);
   L.tiles_mg = ceil_div(2ll * kb, MERGE_TILE);
-  L.etiles_mg = ceil_div(2ll * kb, EMIT_TILE);
-  L.stat_a_n = std::max<int64_t>((int64_t)P * P * L.tiles_tk, L.pairs_max * L.tiles_mg);
-  L.stat_b_n = std::max<int64_t>((int64_t)P * P * L.etiles_tk, L.pairs_max * L.etiles_mg);
+  L.slot_n = std::max<int64_t>((int64_t)P * P * L.tiles_tk, L.pairs_max * L.tiles_mg);
   size_t off = 256;
   L.bitmap = off;
   off += align256((size_t)ceil_div(n, 32) * 4);
   L.hist1 = off;
-  off += align256((size_t)L.units * NB1 * 4);
+  off += align256((size_t)L.units * HCOPIES * NB1 * 4);
   L.state = off;
   off += align256((size_t)L.units * ST_WORDS * 4);
-  L.tick_a = off;
-  off += align256((size_t)L.units * 4);
-  L.tick_b = off;
-  off += align256((size_t)L.units * 4);
-  L.stat_a = off;
-  off += align256((size_t)L.stat_a_n * 8);
-  L.stat_b = off;
-  off += align256((size_t)L.stat_b_n * 8);
+  L.slot_cnt = off;
+  off += align256((size_t)L.slot_n * 4);
+  L.slot_nbin = off;
+  off += align256((size_t)L.slot_n * 4);
+  L.slot_above = off;
+  off += align256((size_t)L.slot_n * 4);
+  L.pre_all = off;
+  off += align256((size_t)L.slot_n * 4);
+  L.pre_ge = off;
+  off += align256((size_t)L.slot_n * 4);
+  L.pre_eq = off;
+  off += align256((size_t)L.slot_n * 4);
   L.fixed_end = off;
   return L;
 }
 
-inline size_t cand_bytes(int64_t entries) { return 2 * align256((size_t)entries * 4); }
+inline size_t cand_bytes(int64_t entries) { return 3 * align256((size_t)entries * 4); }
 
 struct Ws {
   char* base;
-  uint32_t* err;
-  uint32_t* bitmap;
-  uint32_t* hist1;
-  uint32_t* state;
-  uint32_t* tick_a;
-  uint32_t* tick_b;
-  uint64_t* stat_a;
-  uint64_t* stat_b;
+  uint32_t *err, *bitmap, *hist1, *state, *slot_cnt, *slot_nbin, *slot_above, *pre_all, *pre_ge, *pre_eq;
   int32_t* cand_idx;
   float* cand_val;
+  uint32_t* bin_key;
 };
 
 Ws carve(void* ws, size_t ws_bytes, const Layout& L) {
   Ws w;
   w.base = (char*)ws;
-  w.err = (uint32_t*)(w.base + L.err);
-  w.bitmap = (uint32_t*)(w.base + L.bitmap);
-  w.hist1 = (uint32_t*)(w.base + L.hist1);
-  w.state = (uint32_t*)(w.base + L.state);
-  w.tick_a = (uint32_t*)(w.base + L.tick_a);
-  w.tick_b = (uint32_t*)(w.base + L.tick_b);
-  w.stat_a = (uint64_t*)(w.base + L.stat_a);
-  w.stat_b = (uint64_t*)(w.base + L.stat_b);
-  const size_t half = ws_bytes > L.fixed_end ? ((ws_bytes - L.fixed_end) / 2) & ~(size_t)255 : 0;
+  auto at = [&](size_t off) { return (uint32_t*)(w.base + off); };
+  w.err = at(L.err);
+  w.bitmap = at(L.bitmap);
+  w.hist1 = at(L.hist1);
+  w.state = at(L.state);
+  w.slot_cnt = at(L.slot_cnt);
+  w.slot_nbin = at(L.slot_nbin);
+  w.slot_above = at(L.slot_above);
+  w.pre_all = at(L.pre_all);
+  w.pre_ge = at(L.pre_ge);
+  w.pre_eq = at(L.pre_eq);
+  const size_t q = ws_bytes > L.fixed_end ? ((ws_bytes - L.fixed_end) / 3) & ~(size_t)255 : 0;
   w.cand_idx = (int32_t*)(w.base + L.fixed_end);
-  w.cand_val = (float*)(w.base + L.fixed_end + half);
+  w.cand_val = (float*)(w.base + L.fixed_end + q);
+  w.bin_key = at(L.fixed_end + 2 * q);
   return w;
 }
 
@@ -186,12 +186,12 @@ int spardl_residual_add(float* acc, int64_t ld_acc, const float* grad, int64_t l
     return SPARDL_OK;
   }
   if (nworkers > P) return SPARDL_EINVAL;
-  // Only the histogram region is used; its offset and size depend on (P, n).
+  // Only the level-1 histogram region is used; its offset and size depend on (P, n).
   const Layout L = make_layout(P, n, 1);
   if (ws_bytes < L.state) return SPARDL_ECAPACITY;
   Ws w = carve(ws, ws_bytes, L);
   const bool v4 = aligned16(acc) && aligned16(grad) && ld_acc % 4 == 0 && ld_grad % 4 == 0 && blocks_vec4(n, P);
-  SPARDL_TRY(launch_fill(Fill().add(w.hist1, (int64_t)nworkers * P * NB1).r, stream));
+  SPARDL_TRY(launch_fill(Fill().add(w.hist1, (int64_t)nworkers * P * HCOPIES * NB1).r, stream));
   SPARDL_TRY(launch_residual_add(acc, ld_acc, grad, ld_grad, nworkers, n, P, v4, w.hist1, stream));
   return SPARDL_OK;
 }
@@ -209,20 +209,21 @@ int spardl_block_topk(const float* acc, int64_t ld_acc, int32_t nworkers, int64_
   Ws w = carve(ws, ws_bytes, L);
   const int64_t units = (int64_t)nworkers * P;
   const bool v4 = aligned16(acc) && ld_acc % 4 == 0 && blocks_vec4(n, P);
+  const int32_t smax = (int32_t)L.tiles_tk, gmax = (int32_t)L.groups_tk;
   Fill f;
-  f.add(w.err, 64).add(w.state, units * ST_WORDS).add(w.tick_a, units).add(w.tick_b, units);
-  f.add(w.stat_a, 2 * units * L.tiles_tk).add(w.stat_b, 2 * units * L.etiles_tk);
-  if (!(flags & SPARDL_TOPK_HIST_READY)) f.add(w.hist1, units * NB1);
+  f.add(w.err, 64);
+  if (!(flags & SPARDL_TOPK_HIST_READY)) f.add(w.hist1, units * HCOPIES * NB1);
   SPARDL_TRY(launch_fill(f.r, stream));
   if (!(flags & SPARDL_TOPK_HIST_READY))
     SPARDL_TRY(launch_hist1(acc, ld_acc, nworkers, n, P, v4, w.hist1, stream));
   SPARDL_TRY(launch_select1(w.hist1, w.state, units, (uint32_t)k_blk, w.err, stream));
-  SPARDL_TRY(launch_collect(acc, ld_acc, nworkers, n, P, v4, (int32_t)L.tiles_tk, w.state, w.tick_a,
-                            w.stat_a, w.cand_idx, w.cand_val, w.err, stream));
-  SPARDL_TRY(launch_thresh(w.cand_val, 0, units, n, P, k_blk, w.state, w.err, stream));
-  SPARDL_TRY(launch_emit(0, w.cand_idx, w.cand_val, units, n, P, k_blk, 1, w.state, w.tick_b, w.stat_b,
-                         (int32_t)L.etiles_tk, sp_idx, sp_val, local_idx, nullptr, nullptr, nullptr, w.err,
-                         stream));
+  SPARDL_TRY(launch_collect(acc, ld_acc, nworkers, n, P, v4, smax, w.state, w.slot_cnt, w.slot_nbin,
+                            w.cand_idx, w.cand_val, w.bin_key, stream));
+  SPARDL_TRY(launch_thresh(0, units, n, P, k_blk, smax, 4, w.state, w.slot_cnt, w.slot_nbin, w.slot_above,
+                           w.bin_key, w.pre_all, w.pre_ge, w.pre_eq, nullptr, w.err, stream));
+  SPARDL_TRY(launch_emit(0, w.cand_idx, w.cand_val, units, n, P, k_blk, 1, smax, EMIT_GROUP_TK, gmax, w.state,
+                         w.slot_cnt, w.pre_all, w.pre_ge, w.pre_eq, sp_idx, sp_val, local_idx, nullptr, nullptr,
+                         w.err, stream));
   return SPARDL_OK;
 }
 
@@ -240,17 +241,17 @@ int spardl_sparse_merge_topk(int32_t* sp_idx, float* sp_val, int32_t P, int64_t 
   const int32_t d = 1 << (l - round);
   const int32_t m = bag_of(P, l, round);
   const int64_t pairs = (int64_t)P * m;
-  Fill f;
-  f.add(w.err, 64).add(w.hist1, pairs * NB1).add(w.state, pairs * ST_WORDS).add(w.tick_a, pairs);
-  f.add(w.tick_b, pairs).add(w.stat_a, 2 * pairs * L.tiles_mg).add(w.stat_b, 2 * pairs * L.etiles_mg);
-  SPARDL_TRY(launch_fill(f.r, stream));
-  SPARDL_TRY(launch_merge(sp_idx, sp_val, P, k_blk, d, m, (int32_t)L.tiles_mg, w.tick_a, w.stat_a,
-                          w.hist1, w.state, w.cand_idx, w.cand_val, w.err, stream));
-  SPARDL_TRY(launch_select1(w.hist1, w.state, pairs, (uint32_t)k_blk, w.err, stream));
-  SPARDL_TRY(launch_thresh(w.cand_val, 1, pairs, n, P, k_blk, w.state, w.err, stream));
-  SPARDL_TRY(launch_emit(1, w.cand_idx, w.cand_val, pairs, n, P, k_blk, m, w.state, w.tick_b, w.stat_b,
-                         (int32_t)L.etiles_mg, sp_idx, sp_val, nullptr, drop_idx, drop_val, drop_cnt,
-                         w.err, stream));
+  const int32_t smax = (int32_t)L.tiles_mg;
+  SPARDL_TRY(launch_fill(Fill().add(w.err, 64).add(w.hist1, pairs * NB1).r, stream));
+  SPARDL_TRY(launch_merge(sp_idx, sp_val, P, k_blk, d, m, smax, w.hist1, w.slot_cnt, w.cand_idx, w.cand_val,
+                          stream));
+  SPARDL_TRY(launch_mscan(w.cand_val, pairs, k_blk, smax, w.hist1, w.state, w.slot_cnt, w.slot_nbin,
+                          w.slot_above, w.bin_key, w.err, stream));
+  SPARDL_TRY(launch_thresh(1, pairs, n, P, k_blk, smax, 64, w.state, w.slot_cnt, w.slot_nbin, w.slot_above,
+                           w.bin_key, w.pre_all, w.pre_ge, w.pre_eq, drop_cnt, w.err, stream));
+  SPARDL_TRY(launch_emit(1, w.cand_idx, w.cand_val, pairs, n, P, k_blk, m, smax, 1, smax, w.state, w.slot_cnt,
+                         w.pre_all, w.pre_ge, w.pre_eq, sp_idx, sp_val, nullptr, drop_idx, drop_val, w.err,
+                         stream));
   return SPARDL_OK;
 }
 

@@ -16,19 +16,22 @@ constexpr int NB2 = 2048;
 constexpr int NB3 = 256;
 
 // ---------------------------------------------------------------- tiling
+// Streaming kernels are one-shot workgroups over small contiguous tiles,
+// dispatched in address order (this keeps DRAM pages open and beats both
+// larger per-lane batches and workgroups that walk long ranges).
 constexpr int WAVE = 64;
-constexpr int UNIT = 4096;            // elements one wave streams (16 float4 per lane)
-constexpr int STREAM_WAVES = 4;       // waves per workgroup in the streaming kernels
-constexpr int STREAM_TILE = UNIT * STREAM_WAVES;
+constexpr int ADD_F4 = 2;                        // float4 per lane per array in the residual add
+constexpr int ADD_TILE = 256 * ADD_F4 * 4;       // elements per residual-add workgroup
+constexpr int SLOT = 4096;                       // elements per candidate slot (one collect workgroup)
+constexpr int EMIT_GROUP_TK = 16;                // slots per emit workgroup, block top-k
+constexpr int EMIT_J = 16;                       // entries per thread per emit chunk
+constexpr int EMIT_CHUNK = 256 * EMIT_J;
 constexpr int MERGE_THREADS = 256;
 constexpr int MERGE_PER_THREAD = 16;
 constexpr int MERGE_TILE = MERGE_THREADS * MERGE_PER_THREAD;   // merged positions per workgroup
-constexpr int EMIT_THREADS = 512;
-constexpr int EMIT_PER_THREAD = 16;
-constexpr int EMIT_TILE = EMIT_THREADS * EMIT_PER_THREAD;      // candidates per emit tile
-constexpr int EMIT_WGS_PER_UNIT = 8;
-constexpr int THRESH_THREADS = 1024;
 constexpr int DENSE_TILE = 4096;
+constexpr int HCOPIES = 16;                      // level-1 histogram copies per block (spreads the flush atomics)
+constexpr int SLOT_LDS = 4096;                   // slots per chunk in the threshold kernel's per-slot pass
 
 // ---------------------------------------------------------------- state words
 // Per selection unit (a (worker, block) pair or a merge pair), 16 u32:
@@ -40,12 +43,15 @@ enum : int {
   ST_TGE = 4,       // every candidate with key >= ST_TGE is selected
   ST_TEQ = 5,       // ... and the first ST_NEEDEQ (by index) with key == ST_TEQ
   ST_NEEDEQ = 6,
-  ST_COUNT = 7,     // number of candidates (dense, index-ordered)
   ST_WORDS = 16
 };
 
 constexpr uint32_t ERR_LOOKBACK = 1u;
-constexpr uint32_t ERR_COUNT = 2u;
+constexpr uint32_t ERR_COUNT = 2u;            // a selection could not find its threshold
+constexpr uint32_t ERR_COUNT_L23 = 2u | 4u;   // ... at level 2 or 3
+constexpr uint32_t ERR_COUNT_POS = 2u | 8u;   // an emitted position fell outside [0, k_blk)
+constexpr uint32_t ERR_COUNT_DROP = 2u | 16u; // a drop position fell outside [0, k_blk)
+constexpr uint32_t ERR_COUNT_SUM = 2u | 32u;  // the emitted selection does not have k_blk entries
 
 __device__ __forceinline__ uint32_t mag_key(float v) { return __float_as_uint(v) & 0x7FFFFFFFu; }
 
@@ -152,6 +158,24 @@ __device__ __forceinline__ void block_select_desc(const uint32_t* hist, int nb, 
   __syncthreads();
 }
 
+// Copy count words from global memory to LDS with every load issued before
+// the first LDS write (one memory round trip instead of one per iteration).
+// PER >= ceil(count / blockDim.x) must hold.  No barrier included.
+template <int PER>
+__device__ __forceinline__ void g2lds(uint32_t* lds, const uint32_t* __restrict__ g, int count) {
+  uint32_t r[PER];
+#pragma unroll
+  for (int u = 0; u < PER; ++u) {
+    const int i = threadIdx.x + u * blockDim.x;
+    r[u] = i < count ? g[i] : 0u;
+  }
+#pragma unroll
+  for (int u = 0; u < PER; ++u) {
+    const int i = threadIdx.x + u * blockDim.x;
+    if (i < count) lds[i] = r[u];
+  }
+}
+
 // ---------------------------------------------------------------- ordered prefix across tiles
 // Decoupled look-back (single-pass ordered prefix): each tile of a unit
 // publishes its own aggregate, then walks back over its predecessors until it
@@ -178,37 +202,93 @@ __device__ __forceinline__ uint64_t lb_load(uint64_t* p) {
   return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
-// Called by one thread.  st = the unit's status words (one per tile).
-__device__ __forceinline__ void lookback(uint64_t* st, uint32_t tile, uint32_t agg_a, uint32_t agg_b,
-                                         uint32_t* ex_a, uint32_t* ex_b, uint32_t* err) {
+// Called by all 64 lanes of one wave; every lane receives the exclusive
+// prefix.  The wave inspects 64 predecessors per round trip: it waits until
+// every tile up to the nearest inclusive one has published, adds their
+// aggregates and stops there.  st = the unit's status words (one per tile).
+__device__ __forceinline__ void lookback_wave(uint64_t* st, uint32_t tile, uint32_t agg_a, uint32_t agg_b,
+                                              uint32_t* ex_a, uint32_t* ex_b, uint32_t* err) {
+  const int lane = lane_id();
   if (tile == 0) {
-    lb_store(&st[0], lb_pack(LB_INC, agg_a, agg_b));
+    if (lane == 0) lb_store(&st[0], lb_pack(LB_INC, agg_a, agg_b));
     *ex_a = 0;
     *ex_b = 0;
     return;
   }
-  lb_store(&st[tile], lb_pack(LB_AGG, agg_a, agg_b));
+  if (lane == 0) lb_store(&st[tile], lb_pack(LB_AGG, agg_a, agg_b));
   uint32_t a = 0, b = 0, spins = 0;
-  int64_t t = (int64_t)tile - 1;
+  int64_t top = (int64_t)tile - 1;   // window: tiles top, top-1, ..., top-63
   for (;;) {
-    uint64_t s = lb_load(&st[t]);
-    uint64_t f = s >> 62;
-    if (f == 0) {
+    const int64_t t = top - lane;
+    const uint64_t s = t >= 0 ? lb_load(&st[t]) : LB_INC;
+    const uint64_t inc = __ballot((s >> 62) == 2);
+    const uint64_t none = __ballot((s >> 62) == 0);
+    const int first = inc ? (__ffsll((unsigned long long)inc) - 1) : (WAVE - 1);
+    const uint64_t upto = first == WAVE - 1 ? ~0ull : ((2ull << first) - 1ull);
+    if (none & upto) {
       if (++spins > LB_SPIN_LIMIT) {
-        atomicOr(err, ERR_LOOKBACK);
+        if (lane == 0) atomicOr(err, ERR_LOOKBACK);
         break;
       }
       __builtin_amdgcn_s_sleep(1);
       continue;
     }
-    a += (uint32_t)(s & 0x7FFFFFFFu);
-    b += (uint32_t)((s >> 31) & 0x7FFFFFFFu);
-    if (f == 2 || t == 0) break;
-    --t;
+    const bool take = lane <= first;
+    a += wave_sum(take ? (uint32_t)(s & 0x7FFFFFFFu) : 0u);
+    b += wave_sum(take ? (uint32_t)((s >> 31) & 0x7FFFFFFFu) : 0u);
+    if (inc) break;
+    top -= WAVE;
   }
+  if (lane == 0) lb_store(&st[tile], lb_pack(LB_INC, a + agg_a, b + agg_b));
   *ex_a = a;
   *ex_b = b;
-  lb_store(&st[tile], lb_pack(LB_INC, a + agg_a, b + agg_b));
+}
+
+// ---------------------------------------------------------------- cooperative searches
+// Number of leading positions p in [lo, hi) for which the monotone predicate
+// pred(p) holds (true ... true false ... false), found by the whole workgroup
+// with a (blockDim+1)-ary search: every round tests blockDim points at once,
+// so a range of 2^15 needs two rounds of loads.  `cnt` needs blockDim/64 + 1
+// words of LDS.  Contains barriers; every thread gets the answer.
+template <typename Pred>
+__device__ __forceinline__ int32_t wg_partition_point(int32_t lo, int32_t hi, Pred pred, uint32_t* cnt) {
+  const int nt = blockDim.x;
+  const int nw = nt / WAVE;
+  while (hi > lo) {
+    const int32_t S = hi - lo;
+    int32_t p;
+    bool active;
+    if (S <= nt) {
+      p = lo + (int32_t)threadIdx.x;
+      active = (int32_t)threadIdx.x < S;
+    } else {
+      p = lo + (int32_t)(((int64_t)S * (threadIdx.x + 1)) / (nt + 1));
+      active = true;
+    }
+    const bool t = active && pred(p);
+    const uint64_t m = __ballot(t);
+    if (lane_id() == 0) cnt[wave_id()] = popc64(m);
+    __syncthreads();
+    int32_t c = 0;
+    for (int i = 0; i < nw; ++i) c += (int32_t)cnt[i];
+    __syncthreads();
+    if (S <= nt) {
+      lo += c;
+      hi = lo;
+    } else {
+      const int32_t new_lo = c == 0 ? lo : lo + (int32_t)(((int64_t)S * c) / (nt + 1)) + 1;
+      const int32_t new_hi = c == nt ? hi : lo + (int32_t)(((int64_t)S * (c + 1)) / (nt + 1));
+      lo = new_lo;
+      hi = new_hi;
+    }
+  }
+  return lo;
+}
+
+// First position j in [0, len) with a[j] >= x (len if none); a sorted ascending.
+__device__ __forceinline__ int32_t wg_lower_bound(const int32_t* __restrict__ a, int32_t len, int64_t x,
+                                                  uint32_t* cnt) {
+  return wg_partition_point(0, len, [&](int32_t p) { return (int64_t)a[p] < x; }, cnt);
 }
 
 }  // namespace spardl

@@ -7,18 +7,21 @@
 //
 // Exact top-k is a radix select on the 31-bit magnitude key in three digits
 // (12/11/8 bits).  Dense blocks: the level-1 histogram is built while
-// streaming (fused with the residual add), one more streaming pass keeps the
-// entries at or above the level-1 threshold bin as index-ordered candidates,
-// and the remaining digits are resolved on those candidates only.  Merges of
-// two sorted sparse blocks use merge-path tiles; their union is treated like
-// the candidates of a dense block.  Ordered compaction across workgroups uses
-// a bounded decoupled look-back.  No floating-point atomics are used anywhere,
-// so every result is bit-reproducible.
+// streaming (fused with the residual add); one more streaming pass keeps the
+// entries at or above the level-1 threshold bin as candidates in per-tile
+// slots (index order inside a slot) and the threshold-bin keys beside them;
+// the last two digits are resolved on those keys only; an ordered emit writes
+// the selection.  Merges of two sorted sparse blocks use merge-path tiles and
+// feed the same threshold and emit stages.  The only cross-workgroup ordering
+// (the emit) uses a bounded decoupled look-back.  No floating-point atomics
+// are used anywhere, so every result is bit-reproducible.
 
 #include "common.hpp"
 #include "launch.hpp"
 
 namespace spardl {
+
+typedef float f4v __attribute__((ext_vector_type(4)));
 
 // ============================================================================ fill
 // Zero up to FILL_MAX word ranges in one launch (counters, histograms and
@@ -39,9 +42,10 @@ __global__ __launch_bounds__(256) void k_fill(FillRanges r) {
 }
 
 // ============================================================================ a1: residual add
-// One workgroup = STREAM_WAVES waves; each wave streams one UNIT of one block
-// of one row.  With HIST, every sum's level-1 digit is counted in an LDS
-// histogram that is flushed (non-zero bins only) into the block's global one.
+// One workgroup = one tile of ADD_TILE elements of one block of one row.
+// With HIST, every sum's level-1 digit is counted in an LDS histogram that is
+// flushed (non-zero bins only) into the block's global one.  The gradient is
+// read once, so it is loaded non-temporally.
 template <int VEC, bool HIST>
 __global__ __launch_bounds__(256) void k_residual_add(float* __restrict__ acc, int64_t ld_acc,
                                                       const float* __restrict__ grad, int64_t ld_grad,
@@ -52,59 +56,57 @@ __global__ __launch_bounds__(256) void k_residual_add(float* __restrict__ acc, i
   const int64_t wb = blockIdx.x / G;
   const int64_t b = wb % P, w = wb / P;
   const int64_t s = blk_start(b, n, P), e = blk_start(b + 1, n, P);
-  const int lane = lane_id();
+  const int64_t t0 = s + (int64_t)g * ADD_TILE;
+  if (t0 >= e) return;
   if (HIST) {
-    for (int i = threadIdx.x; i < NB1; i += blockDim.x) h[i] = 0u;
+    for (int i = threadIdx.x; i < NB1; i += 256) h[i] = 0u;
     __syncthreads();
   }
-  const int64_t u0 = s + ((int64_t)g * STREAM_WAVES + wave_id()) * UNIT;
   float* __restrict__ A = acc + w * ld_acc;
   const float* __restrict__ Gr = grad + w * ld_grad;
-  if (u0 < e) {
-    if (VEC == 4) {
-      float4 a[16], gg[16];
+  if (VEC == 4) {
+    f4v a[ADD_F4], gg[ADD_F4];
 #pragma unroll
-      for (int j = 0; j < 16; ++j) {
-        const int64_t off = u0 + j * 256 + lane * 4;
-        if (off < e) {
-          a[j] = *reinterpret_cast<const float4*>(A + off);
-          gg[j] = *reinterpret_cast<const float4*>(Gr + off);
+    for (int j = 0; j < ADD_F4; ++j) {
+      const int64_t off = t0 + ((int64_t)j * 256 + threadIdx.x) * 4;
+      if (off < e) {
+        a[j] = *reinterpret_cast<const f4v*>(A + off);
+        gg[j] = __builtin_nontemporal_load(reinterpret_cast<const f4v*>(Gr + off));
+      }
+    }
+#pragma unroll
+    for (int j = 0; j < ADD_F4; ++j) {
+      const int64_t off = t0 + ((int64_t)j * 256 + threadIdx.x) * 4;
+      if (off < e) {
+        f4v r;
+        r.x = a[j].x + gg[j].x;
+        r.y = a[j].y + gg[j].y;
+        r.z = a[j].z + gg[j].z;
+        r.w = a[j].w + gg[j].w;
+        *reinterpret_cast<f4v*>(A + off) = r;
+        if (HIST) {
+          atomicAdd(&h[mag_key(r.x) >> D1_SHIFT], 1u);
+          atomicAdd(&h[mag_key(r.y) >> D1_SHIFT], 1u);
+          atomicAdd(&h[mag_key(r.z) >> D1_SHIFT], 1u);
+          atomicAdd(&h[mag_key(r.w) >> D1_SHIFT], 1u);
         }
       }
+    }
+  } else {
 #pragma unroll
-      for (int j = 0; j < 16; ++j) {
-        const int64_t off = u0 + j * 256 + lane * 4;
-        if (off < e) {
-          float4 r;
-          r.x = a[j].x + gg[j].x;
-          r.y = a[j].y + gg[j].y;
-          r.z = a[j].z + gg[j].z;
-          r.w = a[j].w + gg[j].w;
-          *reinterpret_cast<float4*>(A + off) = r;
-          if (HIST) {
-            atomicAdd(&h[mag_key(r.x) >> D1_SHIFT], 1u);
-            atomicAdd(&h[mag_key(r.y) >> D1_SHIFT], 1u);
-            atomicAdd(&h[mag_key(r.z) >> D1_SHIFT], 1u);
-            atomicAdd(&h[mag_key(r.w) >> D1_SHIFT], 1u);
-          }
-        }
-      }
-    } else {
-#pragma unroll 16
-      for (int j = 0; j < 64; ++j) {
-        const int64_t off = u0 + j * 64 + lane;
-        if (off < e) {
-          const float r = A[off] + Gr[off];
-          A[off] = r;
-          if (HIST) atomicAdd(&h[mag_key(r) >> D1_SHIFT], 1u);
-        }
+    for (int j = 0; j < ADD_F4 * 4; ++j) {
+      const int64_t off = t0 + (int64_t)j * 256 + threadIdx.x;
+      if (off < e) {
+        const float r = A[off] + Gr[off];
+        A[off] = r;
+        if (HIST) atomicAdd(&h[mag_key(r) >> D1_SHIFT], 1u);
       }
     }
   }
   if (HIST) {
     __syncthreads();
-    uint32_t* __restrict__ H = hist1 + wb * NB1;
-    for (int i = threadIdx.x; i < NB1; i += blockDim.x) {
+    uint32_t* __restrict__ H = hist1 + (wb * HCOPIES + blockIdx.x % HCOPIES) * NB1;
+    for (int i = threadIdx.x; i < NB1; i += 256) {
       const uint32_t c = h[i];
       if (c) atomicAdd(&H[i], c);
     }
@@ -120,54 +122,61 @@ __global__ __launch_bounds__(256) void k_hist1(const float* __restrict__ acc, in
   const int64_t wb = blockIdx.x / G;
   const int64_t b = wb % P, w = wb / P;
   const int64_t s = blk_start(b, n, P), e = blk_start(b + 1, n, P);
-  const int lane = lane_id();
-  for (int i = threadIdx.x; i < NB1; i += blockDim.x) h[i] = 0u;
+  const int64_t t0 = s + (int64_t)g * ADD_TILE;
+  if (t0 >= e) return;
+  for (int i = threadIdx.x; i < NB1; i += 256) h[i] = 0u;
   __syncthreads();
-  const int64_t u0 = s + ((int64_t)g * STREAM_WAVES + wave_id()) * UNIT;
   const float* __restrict__ A = acc + w * ld_acc;
-  if (u0 < e) {
-    if (VEC == 4) {
-      float4 a[16];
+  if (VEC == 4) {
 #pragma unroll
-      for (int j = 0; j < 16; ++j) {
-        const int64_t off = u0 + j * 256 + lane * 4;
-        if (off < e) a[j] = *reinterpret_cast<const float4*>(A + off);
+    for (int j = 0; j < ADD_F4; ++j) {
+      const int64_t off = t0 + ((int64_t)j * 256 + threadIdx.x) * 4;
+      if (off < e) {
+        const f4v a = *reinterpret_cast<const f4v*>(A + off);
+        atomicAdd(&h[mag_key(a.x) >> D1_SHIFT], 1u);
+        atomicAdd(&h[mag_key(a.y) >> D1_SHIFT], 1u);
+        atomicAdd(&h[mag_key(a.z) >> D1_SHIFT], 1u);
+        atomicAdd(&h[mag_key(a.w) >> D1_SHIFT], 1u);
       }
+    }
+  } else {
 #pragma unroll
-      for (int j = 0; j < 16; ++j) {
-        const int64_t off = u0 + j * 256 + lane * 4;
-        if (off < e) {
-          atomicAdd(&h[mag_key(a[j].x) >> D1_SHIFT], 1u);
-          atomicAdd(&h[mag_key(a[j].y) >> D1_SHIFT], 1u);
-          atomicAdd(&h[mag_key(a[j].z) >> D1_SHIFT], 1u);
-          atomicAdd(&h[mag_key(a[j].w) >> D1_SHIFT], 1u);
-        }
-      }
-    } else {
-#pragma unroll 16
-      for (int j = 0; j < 64; ++j) {
-        const int64_t off = u0 + j * 64 + lane;
-        if (off < e) atomicAdd(&h[mag_key(A[off]) >> D1_SHIFT], 1u);
-      }
+    for (int j = 0; j < ADD_F4 * 4; ++j) {
+      const int64_t off = t0 + (int64_t)j * 256 + threadIdx.x;
+      if (off < e) atomicAdd(&h[mag_key(A[off]) >> D1_SHIFT], 1u);
     }
   }
   __syncthreads();
-  uint32_t* __restrict__ H = hist1 + wb * NB1;
-  for (int i = threadIdx.x; i < NB1; i += blockDim.x) {
+  uint32_t* __restrict__ H = hist1 + (wb * HCOPIES + blockIdx.x % HCOPIES) * NB1;
+  for (int i = threadIdx.x; i < NB1; i += 256) {
     const uint32_t c = h[i];
     if (c) atomicAdd(&H[i], c);
   }
 }
 
 // ============================================================================ level-1 select
-__global__ __launch_bounds__(256) void k_select1(const uint32_t* __restrict__ hist1,
-                                                 uint32_t* __restrict__ state, uint32_t need,
-                                                 uint32_t* __restrict__ err) {
+// The block's histogram is the sum of its HCOPIES copies; every load is in
+// flight before the first add.
+__global__ __launch_bounds__(1024) void k_select1(const uint32_t* __restrict__ hist1,
+                                                  uint32_t* __restrict__ state, uint32_t need,
+                                                  uint32_t* __restrict__ err) {
+  constexpr int NT = 1024, PER = NB1 / NT;
   __shared__ uint32_t h[NB1];
-  __shared__ uint32_t scratch[16];
+  __shared__ uint32_t scratch[24];
   const int64_t u = blockIdx.x;
-  const uint32_t* __restrict__ H = hist1 + u * NB1;
-  for (int i = threadIdx.x; i < NB1; i += blockDim.x) h[i] = H[i];
+  const uint32_t* __restrict__ H = hist1 + u * HCOPIES * NB1;
+  uint32_t r[PER][HCOPIES];
+#pragma unroll
+  for (int q = 0; q < PER; ++q)
+#pragma unroll
+    for (int k = 0; k < HCOPIES; ++k) r[q][k] = H[k * NB1 + q * NT + threadIdx.x];
+#pragma unroll
+  for (int q = 0; q < PER; ++q) {
+    uint32_t c = 0;
+#pragma unroll
+    for (int k = 0; k < HCOPIES; ++k) c += r[q][k];
+    h[q * NT + threadIdx.x] = c;
+  }
   __syncthreads();
   uint32_t T, above, cnt, ok;
   block_select_desc(h, NB1, need, scratch, &T, &above, &cnt, &ok);
@@ -181,235 +190,420 @@ __global__ __launch_bounds__(256) void k_select1(const uint32_t* __restrict__ hi
   }
 }
 
-// ============================================================================ a3: ordered candidates
-// Each wave holds 64 values per lane in registers, counts the entries whose
-// key lies at or above the level-1 threshold bin, the workgroup gets its
-// output offset from the look-back, and the wave writes its candidates in
-// index order: (register j, lane, component c) is ascending index.
+// ============================================================================ candidate slots
+// Candidates of a selection unit live in fixed slots, one per producer
+// workgroup, each holding its entries densely and in index order from the
+// slot start; the keys of its threshold-bin entries sit at the same offsets
+// of a parallel array.
+//  mode 0 (block top-k): unit (w, b), region = the block's span of a
+//          row-sized buffer, slot = SLOT elements of the block;
+//  mode 1 (merge):       unit = pair, region = 2 k_blk entries,
+//          slot = MERGE_TILE merged positions.
+struct SlotGeom {
+  int64_t base;    // first entry of the unit's region
+  int32_t ss;      // slot size
+  int32_t nslots;  // slots of this unit
+};
+
+__device__ __forceinline__ SlotGeom slot_geom(int mode, int64_t unit, int64_t n, int64_t P, int64_t kb) {
+  SlotGeom g;
+  if (mode == 0) {
+    const int64_t b = unit % P, w = unit / P;
+    const int64_t s = blk_start(b, n, P), e = blk_start(b + 1, n, P);
+    g.base = w * n + s;
+    g.ss = SLOT;
+    g.nslots = (int32_t)((e - s + SLOT - 1) / SLOT);
+  } else {
+    g.base = unit * 2 * kb;
+    g.ss = MERGE_TILE;
+    g.nslots = (int32_t)((2 * kb + MERGE_TILE - 1) / MERGE_TILE);
+  }
+  return g;
+}
+
+// ============================================================================ a3: candidates
+// One workgroup per slot of SLOT elements: keeps the entries whose key lies
+// at or above the level-1 threshold bin, in index order -- element order is
+// (register j, thread, component c) -- and the keys of the entries inside the
+// threshold bin.  No atomics and no waiting on other workgroups.
 template <int VEC>
 __global__ __launch_bounds__(256) void k_collect(const float* __restrict__ acc, int64_t ld_acc,
-                                                 int64_t n, int32_t P, int32_t tiles_per_unit,
-                                                 uint32_t* __restrict__ state, uint32_t* __restrict__ tickets,
-                                                 uint64_t* __restrict__ status,
+                                                 int64_t n, int32_t P, int32_t smax,
+                                                 const uint32_t* __restrict__ state,
+                                                 uint32_t* __restrict__ slot_cnt, uint32_t* __restrict__ slot_nbin,
                                                  int32_t* __restrict__ cand_idx, float* __restrict__ cand_val,
-                                                 uint32_t* __restrict__ err) {
-  __shared__ uint32_t sh[16];
-  const int64_t unit = blockIdx.x / tiles_per_unit;
+                                                 uint32_t* __restrict__ bin_key) {
+  constexpr int NJ = VEC == 4 ? SLOT / 1024 : SLOT / 256;   // register rows per thread
+  constexpr int NC = VEC;                                   // components per row
+  constexpr int NW = 4;
+  __shared__ uint32_t cc[NJ * NW], cb[NJ * NW];
+  __shared__ uint32_t tot[2];
+  const int64_t unit = blockIdx.x / smax;
+  const int32_t slot = (int32_t)(blockIdx.x % smax);
   const int64_t b = unit % P, w = unit / P;
   const int64_t s = blk_start(b, n, P), e = blk_start(b + 1, n, P);
-  const int64_t len = e - s;
-  const uint32_t ntiles = (uint32_t)((len + STREAM_TILE - 1) / STREAM_TILE);
-  if (threadIdx.x == 0) sh[0] = atomicAdd(&tickets[unit], 1u);
-  __syncthreads();
-  const uint32_t tile = sh[0];
-  if (tile >= ntiles) return;
-  const uint32_t tlo = state[unit * ST_WORDS + ST_T1] << D1_SHIFT;
+  const int64_t t0 = s + (int64_t)slot * SLOT;
+  if (t0 >= e) return;
+  const uint32_t T1 = state[unit * ST_WORDS + ST_T1];
+  const uint32_t tlo = T1 << D1_SHIFT;
   const int lane = lane_id(), wv = wave_id();
-  const int64_t u0 = s + (int64_t)tile * STREAM_TILE + (int64_t)wv * UNIT;
   const float* __restrict__ A = acc + w * ld_acc;
   const uint64_t lt = __lanemask_lt();
 
-  float v[64];
-  if (VEC == 4) {
+  float v[NJ * NC];
+  auto pos_of = [&](int j, int c) -> int64_t {
+    return VEC == 4 ? t0 + ((int64_t)j * 256 + threadIdx.x) * 4 + c : t0 + (int64_t)j * 256 + threadIdx.x;
+  };
 #pragma unroll
-    for (int j = 0; j < 16; ++j) {
-      const int64_t off = u0 + j * 256 + lane * 4;
-      float4 q = make_float4(0.f, 0.f, 0.f, 0.f);
-      if (off < e) q = *reinterpret_cast<const float4*>(A + off);
+  for (int j = 0; j < NJ; ++j) {
+    if (VEC == 4) {
+      f4v q = {0.f, 0.f, 0.f, 0.f};
+      if (pos_of(j, 0) < e) q = *reinterpret_cast<const f4v*>(A + pos_of(j, 0));
       v[4 * j + 0] = q.x;
       v[4 * j + 1] = q.y;
       v[4 * j + 2] = q.z;
       v[4 * j + 3] = q.w;
-    }
-  } else {
-#pragma unroll
-    for (int j = 0; j < 64; ++j) {
-      const int64_t off = u0 + j * 64 + lane;
-      v[j] = off < e ? A[off] : 0.f;
+    } else {
+      v[j] = pos_of(j, 0) < e ? A[pos_of(j, 0)] : 0.f;
     }
   }
-  // element position of register r of this lane
-  auto pos_of = [&](int r) -> int64_t {
-    return VEC == 4 ? u0 + (r >> 2) * 256 + lane * 4 + (r & 3) : u0 + r * 64 + lane;
-  };
-  uint32_t wcount = 0;
 #pragma unroll
-  for (int r = 0; r < 64; ++r) {
-    const bool p = pos_of(r) < e && mag_key(v[r]) >= tlo;
-    wcount += popc64(__ballot(p));
+  for (int j = 0; j < NJ; ++j) {
+    uint32_t nc = 0, nb = 0;
+#pragma unroll
+    for (int c = 0; c < NC; ++c) {
+      const uint32_t key = mag_key(v[j * NC + c]);
+      const bool valid = pos_of(j, c) < e;
+      nc += popc64(__ballot(valid && key >= tlo));
+      nb += popc64(__ballot(valid && (key >> D1_SHIFT) == T1));
+    }
+    if (lane == 0) {
+      cc[j * NW + wv] = nc;
+      cb[j * NW + wv] = nb;
+    }
   }
-  if (lane == 0) sh[1 + wv] = wcount;
   __syncthreads();
+  if (wv == 0) {   // exclusive scans over (j, wave) in j-major order
+    const uint32_t x = lane < NJ * NW ? cc[lane] : 0u, y = lane < NJ * NW ? cb[lane] : 0u;
+    const uint32_t xi = wave_incl_scan(x), yi = wave_incl_scan(y);
+    if (lane < NJ * NW) {
+      cc[lane] = xi - x;
+      cb[lane] = yi - y;
+    }
+    if (lane == WAVE - 1) {
+      tot[0] = xi;
+      tot[1] = yi;
+    }
+  }
+  __syncthreads();
+  const int64_t si = unit * smax + slot;
   if (threadIdx.x == 0) {
-    uint32_t run = 0;
-    for (int i = 0; i < STREAM_WAVES; ++i) {
-      const uint32_t c = sh[1 + i];
-      sh[1 + i] = run;
-      run += c;
-    }
-    uint32_t ex, exb;
-    lookback(status + unit * tiles_per_unit, tile, run, 0u, &ex, &exb, err);
-    sh[8] = ex;
-    if (tile == ntiles - 1) state[unit * ST_WORDS + ST_COUNT] = ex + run;
+    slot_cnt[si] = tot[0];
+    slot_nbin[si] = tot[1];
   }
+  const int64_t cbase = w * n + t0;
+#pragma unroll
+  for (int j = 0; j < NJ; ++j) {
+    bool pc_[NC], pb_[NC];
+    uint32_t pc = cc[j * NW + wv], pb = cb[j * NW + wv];
+#pragma unroll
+    for (int c = 0; c < NC; ++c) {
+      const uint32_t key = mag_key(v[j * NC + c]);
+      const bool valid = pos_of(j, c) < e;
+      pc_[c] = valid && key >= tlo;
+      pb_[c] = valid && (key >> D1_SHIFT) == T1;
+      pc += popc64(__ballot(pc_[c]) & lt);
+      pb += popc64(__ballot(pb_[c]) & lt);
+    }
+#pragma unroll
+    for (int c = 0; c < NC; ++c) {
+      if (pc_[c]) {
+        cand_idx[cbase + pc] = (int32_t)pos_of(j, c);
+        cand_val[cbase + pc] = v[j * NC + c];
+        ++pc;
+      }
+      if (pb_[c]) {
+        bin_key[cbase + pb] = mag_key(v[j * NC + c]);
+        ++pb;
+      }
+    }
+  }
+}
+
+// ============================================================================ merge: per-slot scan
+// For a merge, the level-1 threshold is known only once the whole union is
+// built.  One workgroup per slot recomputes the unit's level-1 select from
+// its histogram (identical in every workgroup), then stores the keys of the
+// slot's entries inside the threshold bin and their count -- the same
+// threshold-bin outputs k_collect produces for a dense block.
+__global__ __launch_bounds__(256) void k_mscan(const float* __restrict__ U_val, int32_t kb, int32_t smax,
+                                               const uint32_t* __restrict__ hist1, uint32_t* __restrict__ state,
+                                               const uint32_t* __restrict__ slot_cnt,
+                                               uint32_t* __restrict__ slot_nbin, uint32_t* __restrict__ slot_above,
+                                               uint32_t* __restrict__ bin_key, uint32_t* __restrict__ err) {
+  constexpr int NT = 256, NJ = MERGE_TILE / NT;
+  __shared__ uint32_t h[NB1];
+  __shared__ uint32_t scratch[16];
+  const int64_t unit = blockIdx.x / smax;
+  const int32_t slot = (int32_t)(blockIdx.x % smax);
+  g2lds<NB1 / NT>(h, hist1 + unit * NB1, NB1);
   __syncthreads();
-  const int64_t cbase = w * n + s;
-  uint32_t run = sh[8] + sh[1 + wv];
-  if (VEC == 4) {
+  uint32_t T1, above1, cnt1, ok;
+  block_select_desc(h, NB1, (uint32_t)kb, scratch, &T1, &above1, &cnt1, &ok);
+  if (threadIdx.x == 0 && slot == 0) {
+    uint32_t* st = state + unit * ST_WORDS;
+    if (!ok) atomicOr(err, ERR_COUNT);
+    st[ST_T1] = T1;
+    st[ST_ABOVE1] = above1;
+    st[ST_NEED1] = ok ? (uint32_t)kb - above1 : 0u;
+    st[ST_CNT1] = cnt1;
+  }
+  const int64_t base = unit * 2 * (int64_t)kb + (int64_t)slot * MERGE_TILE;
+  const uint32_t count = min(slot_cnt[unit * smax + slot], (uint32_t)MERGE_TILE);
+  // thread t owns entries [t NJ, t NJ + NJ) of the slot, so its bin keys are contiguous
+  uint32_t key[NJ];
+  uint32_t nbin = 0, nab = 0;
 #pragma unroll
-    for (int j = 0; j < 16; ++j) {
-      bool p[4];
-      uint64_t m[4];
+  for (int j = 0; j < NJ; ++j) {
+    const uint32_t p = threadIdx.x * NJ + j;
+    key[j] = p < count ? mag_key(U_val[base + p]) : 0xFFFFFFFFu;
+    const bool valid = key[j] != 0xFFFFFFFFu;
+    nbin += (valid && (key[j] >> D1_SHIFT) == T1) ? 1u : 0u;
+    nab += (valid && (key[j] >> D1_SHIFT) > T1) ? 1u : 0u;
+  }
+  uint32_t tbin, tab;
+  block_excl_scan(nab, scratch, &tab);
+  uint32_t q = block_excl_scan(nbin, scratch, &tbin);
+  if (threadIdx.x == 0) {
+    slot_nbin[unit * smax + slot] = tbin;
+    slot_above[unit * smax + slot] = tab;
+  }
 #pragma unroll
-      for (int c = 0; c < 4; ++c) {
-        p[c] = pos_of(4 * j + c) < e && mag_key(v[4 * j + c]) >= tlo;
-        m[c] = __ballot(p[c]);
-      }
-      uint32_t before = popc64(m[0] & lt) + popc64(m[1] & lt) + popc64(m[2] & lt) + popc64(m[3] & lt);
-#pragma unroll
-      for (int c = 0; c < 4; ++c) {
-        if (p[c]) {
-          const uint32_t pos = run + before;
-          if ((int64_t)pos < len) {
-            cand_idx[cbase + pos] = (int32_t)pos_of(4 * j + c);
-            cand_val[cbase + pos] = v[4 * j + c];
-          } else {
-            atomicOr(err, ERR_COUNT);
-          }
-          ++before;
-        }
-      }
-      run += popc64(m[0]) + popc64(m[1]) + popc64(m[2]) + popc64(m[3]);
-    }
-  } else {
-#pragma unroll
-    for (int r = 0; r < 64; ++r) {
-      const bool p = pos_of(r) < e && mag_key(v[r]) >= tlo;
-      const uint64_t m = __ballot(p);
-      if (p) {
-        const uint32_t pos = run + popc64(m & lt);
-        if ((int64_t)pos < len) {
-          cand_idx[cbase + pos] = (int32_t)pos_of(r);
-          cand_val[cbase + pos] = v[r];
-        } else {
-          atomicOr(err, ERR_COUNT);
-        }
-      }
-      run += popc64(m);
+  for (int j = 0; j < NJ; ++j) {
+    if (key[j] != 0xFFFFFFFFu && (key[j] >> D1_SHIFT) == T1) {
+      bin_key[base + q] = key[j];
+      ++q;
     }
   }
 }
 
-// Start of a unit's candidate region.  Top-k: unit = (w, b), region = the
-// block's own span of a row-sized buffer.  Merge: unit = pair, 2 k_blk slots.
-__device__ __forceinline__ int64_t cand_base(int mode, int64_t unit, int64_t n, int64_t P, int64_t kb) {
-  if (mode == 0) {
-    const int64_t b = unit % P, w = unit / P;
-    return w * n + blk_start(b, n, P);
+// ============================================================================ exact threshold
+// One workgroup per unit.  The threshold-bin keys are gathered straight from
+// the slots (LPS lanes per slot; each lane walks its slot's keys with several
+// loads in flight) into the level-2 and then the level-3 histogram.  Result:
+// select every key >= TGE, plus the first NEEDEQ (by index) with key TEQ.
+template <typename F>
+__device__ __forceinline__ void for_each_bin_key(const uint32_t* __restrict__ K, const SlotGeom& g,
+                                                 const uint32_t* __restrict__ nbin, int lps, F f) {
+  const int nt = blockDim.x;
+  const int per_round = nt / lps;
+  const int sl = threadIdx.x / lps, li = threadIdx.x % lps;
+  for (int32_t s0 = 0; s0 < g.nslots; s0 += per_round) {
+    const int32_t slot = s0 + sl;
+    uint32_t nb = 0;
+    if (slot < g.nslots) nb = min(nbin[slot], (uint32_t)g.ss);
+    const uint32_t* __restrict__ Ks = K + (int64_t)slot * g.ss;
+    for (uint32_t k0 = li; k0 < nb; k0 += 4 * lps) {
+      uint32_t key[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const uint32_t k = k0 + u * lps;
+        key[u] = k < nb ? Ks[k] : 0xFFFFFFFFu;
+      }
+#pragma unroll
+      for (int u = 0; u < 4; ++u)
+        if (key[u] != 0xFFFFFFFFu) f(key[u]);
+    }
   }
-  return unit * 2 * kb;
 }
 
-// Capacity of a unit's candidate region (the block length, or 2 k_blk).
-__device__ __forceinline__ int64_t cand_cap(int mode, int64_t unit, int64_t n, int64_t P, int64_t kb) {
-  if (mode == 0) {
-    const int64_t b = unit % P;
-    return blk_start(b + 1, n, P) - blk_start(b, n, P);
-  }
-  return 2 * kb;
-}
-
-// ============================================================================ levels 2 and 3
-// One workgroup per unit resolves the exact threshold on its candidates:
-// select keys >= ST_TGE, plus the first ST_NEEDEQ (by index) with key ST_TEQ.
-__global__ __launch_bounds__(1024) void k_thresh(const float* __restrict__ cand_val, int mode, int64_t n,
-                                                 int32_t P, int32_t kb, uint32_t* __restrict__ state,
+__global__ __launch_bounds__(1024) void k_thresh(int mode, int64_t n, int32_t P, int32_t kb, int32_t smax,
+                                                 int lps, uint32_t* __restrict__ state,
+                                                 const uint32_t* __restrict__ slot_cnt,
+                                                 const uint32_t* __restrict__ slot_nbin,
+                                                 const uint32_t* __restrict__ slot_above,
+                                                 const uint32_t* __restrict__ bin_key,
+                                                 uint32_t* __restrict__ pre_all, uint32_t* __restrict__ pre_ge,
+                                                 uint32_t* __restrict__ pre_eq, int32_t* __restrict__ drop_cnt,
                                                  uint32_t* __restrict__ err) {
   __shared__ uint32_t h[NB2];
+  __shared__ uint32_t cg[SLOT_LDS], ce[SLOT_LDS];
   __shared__ uint32_t scratch[24];
   const int64_t unit = blockIdx.x;
   uint32_t* st = state + unit * ST_WORDS;
+  const SlotGeom g = slot_geom(mode, unit, n, P, kb);
+  const uint32_t* __restrict__ K = bin_key + g.base;
+  const uint32_t* __restrict__ cnt = slot_cnt + unit * smax;
+  const uint32_t* __restrict__ nbn = slot_nbin + unit * smax;
   const uint32_t T1 = st[ST_T1], need1 = st[ST_NEED1], cnt1 = st[ST_CNT1];
-  const uint32_t C = min(st[ST_COUNT], (uint32_t)cand_cap(mode, unit, n, P, kb));
-  if (need1 == cnt1) {
-    if (threadIdx.x == 0) {
-      st[ST_TGE] = T1 << D1_SHIFT;
-      st[ST_TEQ] = 0u;
-      st[ST_NEEDEQ] = 0u;
+  uint32_t ok;
+
+  uint32_t tge = T1 << D1_SHIFT, teq = 0u, need_eq = 0u;
+  if (need1 != cnt1) {
+    for (int i = threadIdx.x; i < NB2; i += blockDim.x) h[i] = 0u;
+    __syncthreads();
+    for_each_bin_key(K, g, nbn, lps, [&](uint32_t key) { atomicAdd(&h[(key >> D2_SHIFT) & (NB2 - 1)], 1u); });
+    __syncthreads();
+    uint32_t T2, above2, cnt2;
+    block_select_desc(h, NB2, need1, scratch, &T2, &above2, &cnt2, &ok);
+    if (!ok && threadIdx.x == 0) atomicOr(err, ERR_COUNT_L23);
+    const uint32_t need2 = need1 - above2;
+    const uint32_t pre23 = (T1 << (D1_SHIFT - D2_SHIFT)) | T2;   // top 23 bits of the key
+    tge = pre23 << D2_SHIFT;
+    if (ok && need2 != cnt2) {
+      for (int i = threadIdx.x; i < NB3; i += blockDim.x) h[i] = 0u;
+      __syncthreads();
+      for_each_bin_key(K, g, nbn, lps, [&](uint32_t key) {
+        if ((key >> D2_SHIFT) == pre23) atomicAdd(&h[key & (NB3 - 1)], 1u);
+      });
+      __syncthreads();
+      uint32_t T3, above3, cnt3;
+      block_select_desc(h, NB3, need2, scratch, &T3, &above3, &cnt3, &ok);
+      if (!ok && threadIdx.x == 0) atomicOr(err, ERR_COUNT_L23);
+      const uint32_t need3 = need2 - above3;
+      const uint32_t T = (pre23 << D2_SHIFT) | T3;
+      if (need3 == cnt3) {
+        tge = T;
+      } else {
+        tge = T + 1u;
+        teq = T;
+        need_eq = need3;
+      }
     }
-    return;
   }
-  const float* __restrict__ V = cand_val + cand_base(mode, unit, n, P, kb);
-  for (int i = threadIdx.x; i < NB2; i += blockDim.x) h[i] = 0u;
-  __syncthreads();
-  for (uint32_t p = threadIdx.x; p < C; p += blockDim.x) {
-    const uint32_t key = mag_key(V[p]);
-    if ((key >> D1_SHIFT) == T1) atomicAdd(&h[(key >> D2_SHIFT) & (NB2 - 1)], 1u);
-  }
-  __syncthreads();
-  uint32_t T2, above2, cnt2, ok;
-  block_select_desc(h, NB2, need1, scratch, &T2, &above2, &cnt2, &ok);
-  const uint32_t need2 = need1 - above2;
-  const uint32_t pre = (T1 << (D1_SHIFT - D2_SHIFT)) | T2;   // top 23 bits of the key
-  if (!ok || need2 == cnt2) {
-    if (threadIdx.x == 0) {
-      if (!ok) atomicOr(err, ERR_COUNT);
-      st[ST_TGE] = pre << D2_SHIFT;
-      st[ST_TEQ] = 0u;
-      st[ST_NEEDEQ] = 0u;
+
+  // Per slot: ge = entries above the threshold bin + its bin keys >= TGE;
+  // eq = bin keys == TEQ; then exclusive prefixes in slot (= index) order.
+  const int nt = blockDim.x;
+  const int per_round = nt / lps;
+  const int sl = threadIdx.x / lps, li = threadIdx.x % lps;
+  uint32_t run_all = 0, run_ge = 0, run_eq = 0;
+  for (int32_t c0 = 0; c0 < g.nslots; c0 += SLOT_LDS) {
+    const int32_t nc = min(SLOT_LDS, g.nslots - c0);
+    for (int32_t s0 = 0; s0 < nc; s0 += per_round) {
+      const int32_t slot = c0 + s0 + sl;
+      uint32_t nb = 0;
+      if (s0 + sl < nc) nb = min(nbn[slot], (uint32_t)g.ss);
+      const uint32_t* __restrict__ Ks = K + (int64_t)slot * g.ss;
+      uint32_t cgt = 0, ceq = 0;
+      for (uint32_t k0 = li; k0 < nb; k0 += 4 * lps) {
+        uint32_t key[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          const uint32_t k = k0 + u * lps;
+          key[u] = k < nb ? Ks[k] : 0xFFFFFFFFu;
+        }
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          if (key[u] == 0xFFFFFFFFu) continue;
+          if (key[u] >= tge) ++cgt;
+          else if (need_eq != 0u && key[u] == teq) ++ceq;
+        }
+      }
+      for (int d = lps / 2; d > 0; d >>= 1) {   // reduce over the slot's lanes (aligned groups)
+        cgt += __shfl_xor(cgt, d, WAVE);
+        ceq += __shfl_xor(ceq, d, WAVE);
+      }
+      if (li == 0 && s0 + sl < nc) {
+        const uint32_t c = min(cnt[slot], (uint32_t)g.ss);
+        const uint32_t above = mode == 0 ? c - min(nbn[slot], c) : slot_above[unit * smax + slot];
+        cg[s0 + sl] = above + cgt;
+        ce[s0 + sl] = ceq;
+      }
     }
-    return;
+    __syncthreads();
+    uint32_t a[4], gg[4], ee[4], sa = 0, sg = 0, se = 0;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const int i = 4 * threadIdx.x + k;
+      a[k] = i < nc ? min(cnt[c0 + i], (uint32_t)g.ss) : 0u;
+      gg[k] = i < nc ? cg[i] : 0u;
+      ee[k] = i < nc ? ce[i] : 0u;
+      sa += a[k];
+      sg += gg[k];
+      se += ee[k];
+    }
+    uint32_t ta, tg, te;
+    uint32_t xa = block_excl_scan(sa, scratch, &ta);
+    uint32_t xg = block_excl_scan(sg, scratch, &tg);
+    uint32_t xe = block_excl_scan(se, scratch, &te);
+    const int64_t o = unit * smax + c0;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const int i = 4 * threadIdx.x + k;
+      if (i < nc) {
+        pre_all[o + i] = run_all + xa;
+        pre_ge[o + i] = run_ge + xg;
+        pre_eq[o + i] = run_eq + xe;
+      }
+      xa += a[k];
+      xg += gg[k];
+      xe += ee[k];
+    }
+    run_all += ta;
+    run_ge += tg;
+    run_eq += te;
+    __syncthreads();
   }
-  for (int i = threadIdx.x; i < NB3; i += blockDim.x) h[i] = 0u;
-  __syncthreads();
-  for (uint32_t p = threadIdx.x; p < C; p += blockDim.x) {
-    const uint32_t key = mag_key(V[p]);
-    if ((key >> D2_SHIFT) == pre) atomicAdd(&h[key & (NB3 - 1)], 1u);
-  }
-  __syncthreads();
-  uint32_t T3, above3, cnt3;
-  block_select_desc(h, NB3, need2, scratch, &T3, &above3, &cnt3, &ok);
   if (threadIdx.x == 0) {
-    if (!ok) atomicOr(err, ERR_COUNT);
-    const uint32_t need3 = need2 - above3;
-    const uint32_t T = (pre << D2_SHIFT) | T3;
-    if (need3 == cnt3) {
-      st[ST_TGE] = T;
-      st[ST_TEQ] = 0u;
-      st[ST_NEEDEQ] = 0u;
-    } else {
-      st[ST_TGE] = T + 1u;
-      st[ST_TEQ] = T;
-      st[ST_NEEDEQ] = need3;
-    }
+    if (run_ge + (run_eq < need_eq ? run_eq : need_eq) != (uint32_t)kb) atomicOr(err, ERR_COUNT_SUM);
+    st[ST_TGE] = tge;
+    st[ST_TEQ] = teq;
+    st[ST_NEEDEQ] = need_eq;
+    if (mode == 1) drop_cnt[unit] = (int32_t)(run_all - (uint32_t)kb);
   }
 }
 
 // ============================================================================ ordered emit
-// Candidates are dense and index-ordered.  An entry is selected if its key is
-// >= TGE, or equals TEQ and fewer than NEEDEQ equal keys precede it.  The
-// number of selected entries before position p is
-//   (#ge before p) + min(#eq before p, NEEDEQ),
-// so a tile only needs the two counts of everything before it (look-back).
+// One workgroup per group of G consecutive slots.  An entry is selected if its
+// key is >= TGE, or equals TEQ and fewer than NEEDEQ equal keys precede it, so
+// the number of selected entries before an entry is
+//   (#ge before it) + min(#eq before it, NEEDEQ),
+// with the counts before the group taken from the per-slot prefixes.
+// Unselected entries of a merge go to the drop list at
+// (#entries before) - (#selected before).
 // MODE 0 (block top-k): selected -> sp (and local_idx).  MODE 1 (merge):
 // selected -> sp[w][b] in place, the rest -> the step's drop lists.
 template <int MODE>
-__global__ __launch_bounds__(EMIT_THREADS) void k_emit(
+__global__ __launch_bounds__(256) void k_emit(
     const int32_t* __restrict__ cand_idx, const float* __restrict__ cand_val, int64_t n, int32_t P,
-    int32_t kb, int32_t m, const uint32_t* __restrict__ state, uint32_t* __restrict__ tickets,
-    uint64_t* __restrict__ status, int32_t tiles_per_unit, int32_t* __restrict__ out_idx,
+    int32_t kb, int32_t m, int32_t smax, int32_t G, int32_t gmax, const uint32_t* __restrict__ state,
+    const uint32_t* __restrict__ slot_cnt, const uint32_t* __restrict__ pre_all,
+    const uint32_t* __restrict__ pre_ge, const uint32_t* __restrict__ pre_eq, int32_t* __restrict__ out_idx,
     float* __restrict__ out_val, int32_t* __restrict__ local_idx, int32_t* __restrict__ drop_idx,
-    float* __restrict__ drop_val, int32_t* __restrict__ drop_cnt, uint32_t* __restrict__ err) {
-  constexpr int NWV = EMIT_THREADS / WAVE;
-  constexpr int NJ = EMIT_PER_THREAD;
+    float* __restrict__ drop_val, uint32_t* __restrict__ err) {
+  constexpr int NT = 256, NWV = NT / WAVE, NJ = EMIT_J;
+  __shared__ uint32_t pre[EMIT_GROUP_TK + 1];
   __shared__ uint32_t cge[NJ * NWV], ceq[NJ * NWV];
-  __shared__ uint32_t sh[8];
-  const int64_t unit = blockIdx.x / EMIT_WGS_PER_UNIT;
+  __shared__ uint32_t sh[2];
+  const int64_t unit = blockIdx.x / gmax;
+  const int32_t grp = (int32_t)(blockIdx.x % gmax);
+  const SlotGeom g = slot_geom(MODE, unit, n, P, kb);
+  const int32_t s_lo = grp * G;
+  if (s_lo >= g.nslots) return;
+  const int32_t ns = min(G, g.nslots - s_lo);
+  const uint32_t* __restrict__ cnt = slot_cnt + unit * smax;
+  const int lane = lane_id(), wv = wave_id();
+  if (wv == 0) {   // exclusive prefix of the group's slot counts
+    const uint32_t c = lane < ns ? min(cnt[s_lo + lane], (uint32_t)g.ss) : 0u;
+    const uint32_t ci = wave_incl_scan(c);
+    if (lane <= ns) pre[lane] = ci - c;
+  }
+  __syncthreads();
+  const uint32_t E = pre[ns];
+  if (E == 0) return;
   const uint32_t* st = state + unit * ST_WORDS;
-  const uint32_t C = min(st[ST_COUNT], (uint32_t)cand_cap(MODE, unit, n, P, kb));
   const uint32_t tge = st[ST_TGE], teq = st[ST_TEQ], need_eq = st[ST_NEEDEQ];
-  const uint32_t ntiles = (C + EMIT_TILE - 1) / EMIT_TILE;
-  const int64_t base = cand_base(MODE, unit, n, P, kb);
+  const int64_t si = unit * smax + s_lo;
+  const uint32_t all_before = pre_all[si];
+  uint32_t run_g = pre_ge[si], run_e = pre_eq[si];
+  auto addr = [&](uint32_t p) -> int64_t {   // entry p of the group (index order) -> address
+    int32_t lo = 0;
+#pragma unroll
+    for (int step = EMIT_GROUP_TK / 2; step >= 1; step >>= 1)
+      if (lo + step < ns && pre[lo + step] <= p) lo += step;
+    return g.base + (int64_t)(s_lo + lo) * g.ss + (p - pre[lo]);
+  };
   int64_t o;
   if (MODE == 0) {
     o = unit * kb;
@@ -417,75 +611,51 @@ __global__ __launch_bounds__(EMIT_THREADS) void k_emit(
     const int64_t w = unit / m, t = unit % m, b = (w + t) % P;
     o = (w * P + b) * kb;
   }
-  const int lane = lane_id(), wv = wave_id();
   const uint64_t lt = __lanemask_lt();
-  for (;;) {
-    if (threadIdx.x == 0) sh[0] = atomicAdd(&tickets[unit], 1u);
-    __syncthreads();
-    const uint32_t tile = sh[0];
-    if (tile >= ntiles) break;
-    const uint32_t p0 = tile * EMIT_TILE;
+  for (uint32_t c0 = 0; c0 < E; c0 += EMIT_CHUNK) {
     int32_t ix[NJ];
     float vx[NJ];
     uint64_t mg[NJ], me[NJ];
 #pragma unroll
     for (int j = 0; j < NJ; ++j) {
-      const uint32_t p = p0 + j * EMIT_THREADS + threadIdx.x;
+      const uint32_t p = c0 + j * NT + threadIdx.x;
       ix[j] = -1;
       vx[j] = 0.f;
-      if (p < C) {
-        ix[j] = cand_idx[base + p];
-        vx[j] = cand_val[base + p];
+      if (p < E) {
+        const int64_t a = addr(p);
+        ix[j] = cand_idx[a];
+        vx[j] = cand_val[a];
       }
     }
 #pragma unroll
     for (int j = 0; j < NJ; ++j) {
-      const uint32_t p = p0 + j * EMIT_THREADS + threadIdx.x;
+      const uint32_t p = c0 + j * NT + threadIdx.x;
       const uint32_t key = mag_key(vx[j]);
-      const bool valid = p < C;
-      mg[j] = __ballot(valid && key >= tge);
-      me[j] = __ballot(valid && need_eq != 0u && key == teq);
+      mg[j] = __ballot(p < E && key >= tge);
+      me[j] = __ballot(p < E && need_eq != 0u && key == teq);
       if (lane == 0) {
         cge[j * NWV + wv] = popc64(mg[j]);
         ceq[j * NWV + wv] = popc64(me[j]);
       }
     }
     __syncthreads();
-    if (wv == 0) {
-      // exclusive scan over (j, wave) in j-major order: 2 entries per lane
-      const uint32_t g0 = cge[2 * lane], g1 = cge[2 * lane + 1];
-      const uint32_t e0 = ceq[2 * lane], e1 = ceq[2 * lane + 1];
-      const uint32_t gi = wave_incl_scan(g0 + g1), ei = wave_incl_scan(e0 + e1);
-      cge[2 * lane] = gi - g0 - g1;
-      cge[2 * lane + 1] = gi - g1;
-      ceq[2 * lane] = ei - e0 - e1;
-      ceq[2 * lane + 1] = ei - e1;
+    if (wv == 0) {   // exclusive scan over (j, wave) in j-major order: one entry per lane
+      const uint32_t gv = cge[lane], ev = ceq[lane];
+      const uint32_t gi = wave_incl_scan(gv), ei = wave_incl_scan(ev);
+      cge[lane] = gi - gv;
+      ceq[lane] = ei - ev;
       if (lane == WAVE - 1) {
-        sh[1] = gi;
-        sh[2] = ei;
+        sh[0] = gi;
+        sh[1] = ei;
       }
     }
     __syncthreads();
-    if (threadIdx.x == 0) {
-      uint32_t exg, exe;
-      lookback(status + unit * tiles_per_unit, tile, sh[1], sh[2], &exg, &exe, err);
-      sh[3] = exg;
-      sh[4] = exe;
-      if (tile == ntiles - 1) {
-        const uint32_t tot_eq = exe + sh[2];
-        const uint32_t sel = exg + sh[1] + (tot_eq < need_eq ? tot_eq : need_eq);
-        if (sel != (uint32_t)kb) atomicOr(err, ERR_COUNT);
-        if (MODE == 1) drop_cnt[unit] = (int32_t)(C - (uint32_t)kb);
-      }
-    }
-    __syncthreads();
-    const uint32_t exg = sh[3], exe = sh[4];
 #pragma unroll
     for (int j = 0; j < NJ; ++j) {
-      const uint32_t p = p0 + j * EMIT_THREADS + threadIdx.x;
-      if (p < C) {
-        const uint32_t ge_pre = exg + cge[j * NWV + wv] + popc64(mg[j] & lt);
-        const uint32_t eq_pre = exe + ceq[j * NWV + wv] + popc64(me[j] & lt);
+      const uint32_t p = c0 + j * NT + threadIdx.x;
+      if (p < E) {
+        const uint32_t ge_pre = run_g + cge[j * NWV + wv] + popc64(mg[j] & lt);
+        const uint32_t eq_pre = run_e + ceq[j * NWV + wv] + popc64(me[j] & lt);
         const bool is_ge = (mg[j] >> lane) & 1ull;
         const bool is_eq = (me[j] >> lane) & 1ull;
         const uint32_t sel_before = ge_pre + (eq_pre < need_eq ? eq_pre : need_eq);
@@ -496,19 +666,21 @@ __global__ __launch_bounds__(EMIT_THREADS) void k_emit(
             out_val[o + sel_before] = vx[j];
             if (MODE == 0 && local_idx) local_idx[o + sel_before] = ix[j];
           } else {
-            atomicOr(err, ERR_COUNT);
+            atomicOr(err, ERR_COUNT_POS);
           }
         } else if (MODE == 1) {
-          const uint32_t dpos = p - sel_before;
+          const uint32_t dpos = all_before + p - sel_before;
           if (dpos < (uint32_t)kb) {
             drop_idx[unit * kb + dpos] = ix[j];
             drop_val[unit * kb + dpos] = vx[j];
           } else {
-            atomicOr(err, ERR_COUNT);
+            atomicOr(err, ERR_COUNT_DROP);
           }
         }
       }
     }
+    run_g += sh[0];
+    run_e += sh[1];
     __syncthreads();
   }
 }
@@ -517,76 +689,71 @@ __global__ __launch_bounds__(EMIT_THREADS) void k_emit(
 // Pair (w, t): held = sp[w][b], received = sp[(w - d) mod P][b], b = (w+t) mod P.
 // The merged sequence orders by index with the held entry first on equal
 // indices; the held entry then emits held + received and the received entry
-// leaves a hole.  Tile = MERGE_TILE merged positions; the emitted (hole-free)
-// union is written densely in index order via the look-back, and its level-1
-// histogram is accumulated for the selection.
+// leaves a hole.  Tile = MERGE_TILE merged positions; its hole-free part is
+// written densely into the tile's slot, and the level-1 histogram of the
+// union is accumulated for the selection.
 __global__ __launch_bounds__(MERGE_THREADS) void k_merge(
     const int32_t* __restrict__ sp_idx, const float* __restrict__ sp_val, int32_t P, int32_t kb,
-    int32_t d, int32_t m, int32_t tiles_per_pair, uint32_t* __restrict__ tickets,
-    uint64_t* __restrict__ status, uint32_t* __restrict__ hist1, uint32_t* __restrict__ state,
-    int32_t* __restrict__ U_idx, float* __restrict__ U_val, uint32_t* __restrict__ err) {
+    int32_t d, int32_t m, int32_t tiles_per_pair, uint32_t* __restrict__ hist1,
+    uint32_t* __restrict__ slot_cnt, int32_t* __restrict__ U_idx, float* __restrict__ U_val) {
   // held entries a0-1 .. a1 at [0, nh + 2), received b0 .. b1 at [nh + 2, nh + nr + 3)
   __shared__ int32_t cI[MERGE_TILE + 3];
   __shared__ float cV[MERGE_TILE + 3];
   __shared__ uint32_t hist[NB1];
   __shared__ uint32_t scratch[16];
-  __shared__ uint32_t sh[8];
   const int64_t pair = blockIdx.x / tiles_per_pair;
+  const int32_t tile = (int32_t)(blockIdx.x % tiles_per_pair);
   const int64_t w = pair / m, t = pair % m, b = (w + t) % P, src = (w - d + P) % P;
   const int32_t* __restrict__ Hi = sp_idx + (w * P + b) * kb;
   const float* __restrict__ Hv = sp_val + (w * P + b) * kb;
   const int32_t* __restrict__ Ri = sp_idx + (src * P + b) * kb;
   const float* __restrict__ Rv = sp_val + (src * P + b) * kb;
-  const uint32_t L2 = 2u * (uint32_t)kb;
-  const uint32_t ntiles = (L2 + MERGE_TILE - 1) / MERGE_TILE;
-  if (threadIdx.x == 0) sh[0] = atomicAdd(&tickets[pair], 1u);
+  const int32_t L2 = 2 * kb;
   for (int i = threadIdx.x; i < NB1; i += blockDim.x) hist[i] = 0u;
-  __syncthreads();
-  const uint32_t tile = sh[0];
-  if (tile >= ntiles) return;
-  const int32_t Q0 = (int32_t)(tile * MERGE_TILE);
-  const int32_t Q1 = (int32_t)min(tile * MERGE_TILE + MERGE_TILE, L2);
-  // split(q) = number of held entries among the first q merged positions
-  if (threadIdx.x < 2) {
-    const int32_t q = threadIdx.x == 0 ? Q0 : Q1;
-    int32_t lo = max(0, q - kb), hi = min(q, kb);
-    while (lo < hi) {
-      const int32_t mid = (lo + hi) >> 1;
-      if (Hi[mid] <= Ri[q - mid - 1]) lo = mid + 1;
-      else hi = mid;
-    }
-    sh[1 + threadIdx.x] = (uint32_t)lo;
-  }
-  __syncthreads();
-  const int32_t a0 = (int32_t)sh[1], a1 = (int32_t)sh[2];
+  const int32_t Q0 = tile * MERGE_TILE;
+  const int32_t Q1 = min(Q0 + MERGE_TILE, L2);
+  // split(q) = number of held entries among the first q merged positions:
+  // the first a in [max(0, q-kb), min(q, kb)) whose held entry does not go
+  // before received entry q-a-1 (held goes first on equal indices).
+  auto split = [&](int32_t q) {
+    return wg_partition_point(max(0, q - kb), min(q, kb),
+                              [&](int32_t a) { return Hi[a] <= Ri[q - a - 1]; }, scratch);
+  };
+  const int32_t a0 = split(Q0);
+  const int32_t a1 = split(Q1);
   const int32_t b0 = Q0 - a0, b1 = Q1 - a1;
   const int32_t nh = a1 - a0, nr = b1 - b0;
   int32_t* hI = cI;
   float* hV = cV;
   int32_t* rI = cI + nh + 2;
   float* rV = cV + nh + 2;
-  for (int i = threadIdx.x; i <= nh + 1; i += blockDim.x) {
-    // hI[i] = held[a0 - 1 + i]; outside [0, kb): -1 before, INT_MAX after
-    const int32_t gi = a0 - 1 + i;
-    if (gi < 0) {
-      hI[i] = -1;
-      hV[i] = 0.f;
-    } else if (gi >= kb) {
-      hI[i] = INT32_MAX;
-      hV[i] = 0.f;
-    } else {
-      hI[i] = Hi[gi];
-      hV[i] = Hv[gi];
+  {
+    // hI[i] = held[a0 - 1 + i] (outside [0, kb): -1 before, INT_MAX after), i <= nh + 1;
+    // rI[i] = recv[b0 + i] (INT_MAX past the end), i <= nr.  All loads first.
+    constexpr int SU = (MERGE_TILE + 3 + MERGE_THREADS - 1) / MERGE_THREADS;
+    int32_t ti[SU];
+    float tv[SU];
+#pragma unroll
+    for (int u = 0; u < SU; ++u) {
+      const int i = threadIdx.x + u * MERGE_THREADS;   // position in the combined buffer
+      ti[u] = INT32_MAX;
+      tv[u] = 0.f;
+      if (i <= nh + 1) {
+        const int32_t gi = a0 - 1 + i;
+        if (gi < 0) ti[u] = -1;
+        else if (gi < kb) { ti[u] = Hi[gi]; tv[u] = Hv[gi]; }
+      } else if (i <= nh + 2 + nr) {
+        const int32_t gj = b0 + (i - nh - 2);
+        if (gj < kb) { ti[u] = Ri[gj]; tv[u] = Rv[gj]; }
+      }
     }
-  }
-  for (int i = threadIdx.x; i <= nr; i += blockDim.x) {
-    const int32_t gj = b0 + i;
-    if (gj >= kb) {
-      rI[i] = INT32_MAX;
-      rV[i] = 0.f;
-    } else {
-      rI[i] = Ri[gj];
-      rV[i] = Rv[gj];
+#pragma unroll
+    for (int u = 0; u < SU; ++u) {
+      const int i = threadIdx.x + u * MERGE_THREADS;
+      if (i <= nh + 2 + nr) {
+        cI[i] = ti[u];
+        cV[i] = tv[u];
+      }
     }
   }
   __syncthreads();
@@ -639,28 +806,18 @@ __global__ __launch_bounds__(MERGE_THREADS) void k_merge(
     }
   }
   uint32_t tot;
-  const uint32_t excl = block_excl_scan(cnt, scratch, &tot);
-  if (threadIdx.x == 0) {
-    uint32_t ex, exb;
-    lookback(status + pair * tiles_per_pair, tile, tot, 0u, &ex, &exb, err);
-    sh[3] = ex;
-    if (tile == ntiles - 1) state[pair * ST_WORDS + ST_COUNT] = ex + tot;
-  }
-  __syncthreads();
-  uint32_t pos = sh[3] + excl;
-  const int64_t ubase = pair * (int64_t)L2;
+  uint32_t pos = block_excl_scan(cnt, scratch, &tot);
+  if (threadIdx.x == 0) slot_cnt[pair * tiles_per_pair + tile] = tot;
+  const int64_t ubase = pair * (int64_t)L2 + Q0;
 #pragma unroll
   for (int k = 0; k < MERGE_PER_THREAD; ++k) {
     if (eok[k]) {
-      if (pos < L2) {
-        U_idx[ubase + pos] = ei[k];
-        U_val[ubase + pos] = ev[k];
-      } else {
-        atomicOr(err, ERR_COUNT);
-      }
+      U_idx[ubase + pos] = ei[k];
+      U_val[ubase + pos] = ev[k];
       ++pos;
     }
   }
+  __syncthreads();
   uint32_t* __restrict__ H = hist1 + pair * NB1;
   for (int i = threadIdx.x; i < NB1; i += blockDim.x) {
     const uint32_t c = hist[i];
@@ -672,22 +829,12 @@ __global__ __launch_bounds__(MERGE_THREADS) void k_merge(
 // Tile [t0, t0 + DENSE_TILE) of the output is assembled in LDS: zeros, then
 // the final entries whose index falls in the tile (found by binary search in
 // the index-sorted final blocks sp[b][b]), then streamed out.
-__device__ __forceinline__ int32_t lower_bound_i32(const int32_t* __restrict__ a, int32_t len, int64_t x) {
-  int32_t lo = 0, hi = len;
-  while (lo < hi) {
-    const int32_t mid = (lo + hi) >> 1;
-    if ((int64_t)a[mid] < x) lo = mid + 1;
-    else hi = mid;
-  }
-  return lo;
-}
-
 template <int VEC>
 __global__ __launch_bounds__(256) void k_densify(const int32_t* __restrict__ sp_idx,
                                                  const float* __restrict__ sp_val, int32_t P, int64_t n,
                                                  int32_t kb, float* __restrict__ dense) {
   __shared__ float tileb[DENSE_TILE];
-  __shared__ int32_t rng[2];
+  __shared__ uint32_t cnt[8];
   const int64_t t0 = (int64_t)blockIdx.x * DENSE_TILE;
   const int64_t t1 = min(t0 + DENSE_TILE, n);
   for (int i = threadIdx.x; i < DENSE_TILE; i += blockDim.x) tileb[i] = 0.f;
@@ -695,13 +842,9 @@ __global__ __launch_bounds__(256) void k_densify(const int32_t* __restrict__ sp_
   for (int64_t b = blo; b <= bhi; ++b) {
     const int32_t* Fi = sp_idx + (b * P + b) * kb;
     const float* Fv = sp_val + (b * P + b) * kb;
-    __syncthreads();
-    if (threadIdx.x == 0) {
-      rng[0] = lower_bound_i32(Fi, kb, t0);
-      rng[1] = lower_bound_i32(Fi, kb, t1);
-    }
-    __syncthreads();
-    for (int32_t j = rng[0] + (int32_t)threadIdx.x; j < rng[1]; j += blockDim.x) {
+    const int32_t jlo = wg_lower_bound(Fi, kb, t0, cnt);
+    const int32_t jhi = wg_lower_bound(Fi, kb, t1, cnt);
+    for (int32_t j = jlo + (int32_t)threadIdx.x; j < jhi; j += blockDim.x) {
       const int64_t r = (int64_t)Fi[j] - t0;
       if (r >= 0 && r < DENSE_TILE) tileb[r] = Fv[j];
     }
@@ -730,20 +873,16 @@ __global__ __launch_bounds__(256) void k_bitmap(const int32_t* __restrict__ sp_i
                                                 int32_t kb, uint32_t* __restrict__ bm) {
   constexpr int WORDS = DENSE_TILE / 32;
   __shared__ uint32_t words[WORDS];
-  __shared__ int32_t rng[2];
+  __shared__ uint32_t cnt[8];
   const int64_t t0 = (int64_t)blockIdx.x * DENSE_TILE;
   const int64_t t1 = min(t0 + DENSE_TILE, n);
   for (int i = threadIdx.x; i < WORDS; i += blockDim.x) words[i] = 0u;
   const int64_t blo = block_of(t0, n, P), bhi = block_of(t1 - 1, n, P);
   for (int64_t b = blo; b <= bhi; ++b) {
     const int32_t* Fi = sp_idx + (b * P + b) * kb;
-    __syncthreads();
-    if (threadIdx.x == 0) {
-      rng[0] = lower_bound_i32(Fi, kb, t0);
-      rng[1] = lower_bound_i32(Fi, kb, t1);
-    }
-    __syncthreads();
-    for (int32_t j = rng[0] + (int32_t)threadIdx.x; j < rng[1]; j += blockDim.x) {
+    const int32_t jlo = wg_lower_bound(Fi, kb, t0, cnt);
+    const int32_t jhi = wg_lower_bound(Fi, kb, t1, cnt);
+    for (int32_t j = jlo + (int32_t)threadIdx.x; j < jhi; j += blockDim.x) {
       const int64_t r = (int64_t)Fi[j] - t0;
       if (r >= 0 && r < DENSE_TILE) atomicOr(&words[r >> 5], 1u << (r & 31));
     }
@@ -814,8 +953,7 @@ hipError_t launch_residual_add(float* acc, int64_t ld_acc, const float* grad, in
                                hipStream_t s) {
   const int32_t PP = hist1 ? P : 1;
   const int64_t maxlen = (n + PP - 1) / PP;
-  const int64_t units = (maxlen + UNIT - 1) / UNIT;
-  const int32_t G = (int32_t)((units + STREAM_WAVES - 1) / STREAM_WAVES);
+  const int32_t G = (int32_t)((maxlen + ADD_TILE - 1) / ADD_TILE);
   const dim3 grid((unsigned)((int64_t)nworkers * PP * G));
   if (hist1) {
     if (vec4) hipLaunchKernelGGL((k_residual_add<4, true>), grid, dim3(256), 0, s, acc, ld_acc, grad, ld_grad, n, PP, G, hist1);
@@ -830,8 +968,7 @@ hipError_t launch_residual_add(float* acc, int64_t ld_acc, const float* grad, in
 hipError_t launch_hist1(const float* acc, int64_t ld_acc, int32_t nworkers, int64_t n, int32_t P,
                         bool vec4, uint32_t* hist1, hipStream_t s) {
   const int64_t maxlen = (n + P - 1) / P;
-  const int64_t units = (maxlen + UNIT - 1) / UNIT;
-  const int32_t G = (int32_t)((units + STREAM_WAVES - 1) / STREAM_WAVES);
+  const int32_t G = (int32_t)((maxlen + ADD_TILE - 1) / ADD_TILE);
   const dim3 grid((unsigned)((int64_t)nworkers * P * G));
   if (vec4) hipLaunchKernelGGL(k_hist1<4>, grid, dim3(256), 0, s, acc, ld_acc, n, P, G, hist1);
   else hipLaunchKernelGGL(k_hist1<1>, grid, dim3(256), 0, s, acc, ld_acc, n, P, G, hist1);
@@ -840,45 +977,55 @@ hipError_t launch_hist1(const float* acc, int64_t ld_acc, int32_t nworkers, int6
 
 hipError_t launch_select1(const uint32_t* hist1, uint32_t* state, int64_t nunits, uint32_t need,
                           uint32_t* err, hipStream_t s) {
-  hipLaunchKernelGGL(k_select1, dim3((unsigned)nunits), dim3(256), 0, s, hist1, state, need, err);
+  hipLaunchKernelGGL(k_select1, dim3((unsigned)nunits), dim3(1024), 0, s, hist1, state, need, err);
   return hipGetLastError();
 }
 
 hipError_t launch_collect(const float* acc, int64_t ld_acc, int32_t nworkers, int64_t n, int32_t P,
-                          bool vec4, int32_t tiles_per_unit, uint32_t* state, uint32_t* tickets,
-                          uint64_t* status, int32_t* cand_idx, float* cand_val, uint32_t* err,
+                          bool vec4, int32_t smax, const uint32_t* state, uint32_t* slot_cnt,
+                          uint32_t* slot_nbin, int32_t* cand_idx, float* cand_val, uint32_t* bin_key,
                           hipStream_t s) {
-  const dim3 grid((unsigned)((int64_t)nworkers * P * tiles_per_unit));
-  if (vec4) hipLaunchKernelGGL(k_collect<4>, grid, dim3(256), 0, s, acc, ld_acc, n, P, tiles_per_unit, state, tickets, status, cand_idx, cand_val, err);
-  else hipLaunchKernelGGL(k_collect<1>, grid, dim3(256), 0, s, acc, ld_acc, n, P, tiles_per_unit, state, tickets, status, cand_idx, cand_val, err);
+  const dim3 grid((unsigned)((int64_t)nworkers * P * smax));
+  if (vec4) hipLaunchKernelGGL(k_collect<4>, grid, dim3(256), 0, s, acc, ld_acc, n, P, smax, state, slot_cnt, slot_nbin, cand_idx, cand_val, bin_key);
+  else hipLaunchKernelGGL(k_collect<1>, grid, dim3(256), 0, s, acc, ld_acc, n, P, smax, state, slot_cnt, slot_nbin, cand_idx, cand_val, bin_key);
   return hipGetLastError();
 }
 
-hipError_t launch_thresh(const float* cand_val, int mode, int64_t nunits, int64_t n, int32_t P,
-                         int32_t kb, uint32_t* state, uint32_t* err, hipStream_t s) {
-  hipLaunchKernelGGL(k_thresh, dim3((unsigned)nunits), dim3(THRESH_THREADS), 0, s, cand_val, mode, n, P, kb, state, err);
+hipError_t launch_mscan(const float* U_val, int64_t npairs, int32_t kb, int32_t smax, const uint32_t* hist1,
+                        uint32_t* state, const uint32_t* slot_cnt, uint32_t* slot_nbin, uint32_t* slot_above,
+                        uint32_t* bin_key, uint32_t* err, hipStream_t s) {
+  hipLaunchKernelGGL(k_mscan, dim3((unsigned)(npairs * smax)), dim3(256), 0, s, U_val, kb, smax, hist1, state,
+                     slot_cnt, slot_nbin, slot_above, bin_key, err);
   return hipGetLastError();
 }
 
-hipError_t launch_emit(int mode, const int32_t* cand_idx, const float* cand_val, int64_t nunits,
-                       int64_t n, int32_t P, int32_t kb, int32_t m, const uint32_t* state,
-                       uint32_t* tickets, uint64_t* status, int32_t tiles_per_unit, int32_t* out_idx,
-                       float* out_val, int32_t* local_idx, int32_t* drop_idx, float* drop_val,
-                       int32_t* drop_cnt, uint32_t* err, hipStream_t s) {
-  const dim3 grid((unsigned)(nunits * EMIT_WGS_PER_UNIT));
+hipError_t launch_thresh(int mode, int64_t nunits, int64_t n, int32_t P, int32_t kb, int32_t smax, int lps,
+                         uint32_t* state, const uint32_t* slot_cnt, const uint32_t* slot_nbin,
+                         const uint32_t* slot_above, const uint32_t* bin_key, uint32_t* pre_all,
+                         uint32_t* pre_ge, uint32_t* pre_eq, int32_t* drop_cnt, uint32_t* err, hipStream_t s) {
+  hipLaunchKernelGGL(k_thresh, dim3((unsigned)nunits), dim3(1024), 0, s, mode, n, P, kb, smax, lps, state,
+                     slot_cnt, slot_nbin, slot_above, bin_key, pre_all, pre_ge, pre_eq, drop_cnt, err);
+  return hipGetLastError();
+}
+
+hipError_t launch_emit(int mode, const int32_t* cand_idx, const float* cand_val, int64_t nunits, int64_t n,
+                       int32_t P, int32_t kb, int32_t m, int32_t smax, int32_t G, int32_t gmax,
+                       const uint32_t* state, const uint32_t* slot_cnt, const uint32_t* pre_all,
+                       const uint32_t* pre_ge, const uint32_t* pre_eq, int32_t* out_idx, float* out_val,
+                       int32_t* local_idx, int32_t* drop_idx, float* drop_val, uint32_t* err, hipStream_t s) {
+  const dim3 grid((unsigned)(nunits * gmax));
   if (mode == 0)
-    hipLaunchKernelGGL(k_emit<0>, grid, dim3(EMIT_THREADS), 0, s, cand_idx, cand_val, n, P, kb, m, state, tickets, status, tiles_per_unit, out_idx, out_val, local_idx, drop_idx, drop_val, drop_cnt, err);
+    hipLaunchKernelGGL(k_emit<0>, grid, dim3(256), 0, s, cand_idx, cand_val, n, P, kb, m, smax, G, gmax, state, slot_cnt, pre_all, pre_ge, pre_eq, out_idx, out_val, local_idx, drop_idx, drop_val, err);
   else
-    hipLaunchKernelGGL(k_emit<1>, grid, dim3(EMIT_THREADS), 0, s, cand_idx, cand_val, n, P, kb, m, state, tickets, status, tiles_per_unit, out_idx, out_val, local_idx, drop_idx, drop_val, drop_cnt, err);
+    hipLaunchKernelGGL(k_emit<1>, grid, dim3(256), 0, s, cand_idx, cand_val, n, P, kb, m, smax, G, gmax, state, slot_cnt, pre_all, pre_ge, pre_eq, out_idx, out_val, local_idx, drop_idx, drop_val, err);
   return hipGetLastError();
 }
 
-hipError_t launch_merge(const int32_t* sp_idx, const float* sp_val, int32_t P, int32_t kb, int32_t d,
-                        int32_t m, int32_t tiles_per_pair, uint32_t* tickets, uint64_t* status,
-                        uint32_t* hist1, uint32_t* state, int32_t* U_idx, float* U_val, uint32_t* err,
-                        hipStream_t s) {
+hipError_t launch_merge(const int32_t* sp_idx, const float* sp_val, int32_t P, int32_t kb, int32_t d, int32_t m,
+                        int32_t tiles_per_pair, uint32_t* hist1, uint32_t* slot_cnt, int32_t* U_idx,
+                        float* U_val, hipStream_t s) {
   const dim3 grid((unsigned)((int64_t)P * m * tiles_per_pair));
-  hipLaunchKernelGGL(k_merge, grid, dim3(MERGE_THREADS), 0, s, sp_idx, sp_val, P, kb, d, m, tiles_per_pair, tickets, status, hist1, state, U_idx, U_val, err);
+  hipLaunchKernelGGL(k_merge, grid, dim3(MERGE_THREADS), 0, s, sp_idx, sp_val, P, kb, d, m, tiles_per_pair, hist1, slot_cnt, U_idx, U_val);
   return hipGetLastError();
 }
 
