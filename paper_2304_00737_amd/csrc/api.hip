@@ -219,7 +219,7 @@ int spardl_block_topk(const float* acc, int64_t ld_acc, int32_t nworkers, int64_
   SPARDL_TRY(launch_select1(w.hist1, w.state, units, (uint32_t)k_blk, w.err, stream));
   SPARDL_TRY(launch_collect(acc, ld_acc, nworkers, n, P, v4, smax, w.state, w.slot_cnt, w.slot_nbin,
                             w.cand_idx, w.cand_val, w.bin_key, stream));
-  SPARDL_TRY(launch_thresh(0, units, n, P, k_blk, smax, 4, w.state, w.slot_cnt, w.slot_nbin, w.slot_above,
+  SPARDL_TRY(launch_thresh(0, units, n, P, k_blk, smax, 1, nullptr, w.cand_val, w.state, w.slot_cnt, w.slot_nbin,
                            w.bin_key, w.pre_all, w.pre_ge, w.pre_eq, nullptr, w.err, stream));
   SPARDL_TRY(launch_emit(0, w.cand_idx, w.cand_val, units, n, P, k_blk, 1, smax, EMIT_GROUP_TK, gmax, w.state,
                          w.slot_cnt, w.pre_all, w.pre_ge, w.pre_eq, sp_idx, sp_val, local_idx, nullptr, nullptr,
@@ -245,9 +245,7 @@ int spardl_sparse_merge_topk(int32_t* sp_idx, float* sp_val, int32_t P, int64_t 
   SPARDL_TRY(launch_fill(Fill().add(w.err, 64).add(w.hist1, pairs * NB1).r, stream));
   SPARDL_TRY(launch_merge(sp_idx, sp_val, P, k_blk, d, m, smax, w.hist1, w.slot_cnt, w.cand_idx, w.cand_val,
                           stream));
-  SPARDL_TRY(launch_mscan(w.cand_val, pairs, k_blk, smax, w.hist1, w.state, w.slot_cnt, w.slot_nbin,
-                          w.slot_above, w.bin_key, w.err, stream));
-  SPARDL_TRY(launch_thresh(1, pairs, n, P, k_blk, smax, 64, w.state, w.slot_cnt, w.slot_nbin, w.slot_above,
+  SPARDL_TRY(launch_thresh(1, pairs, n, P, k_blk, smax, 1, w.hist1, w.cand_val, w.state, w.slot_cnt, w.slot_nbin,
                            w.bin_key, w.pre_all, w.pre_ge, w.pre_eq, drop_cnt, w.err, stream));
   SPARDL_TRY(launch_emit(1, w.cand_idx, w.cand_val, pairs, n, P, k_blk, m, smax, 1, smax, w.state, w.slot_cnt,
                          w.pre_all, w.pre_ge, w.pre_eq, sp_idx, sp_val, nullptr, drop_idx, drop_val, w.err,

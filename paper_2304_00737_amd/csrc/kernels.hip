@@ -201,6 +201,7 @@ __global__ __launch_bounds__(1024) void k_select1(const uint32_t* __restrict__ h
 //          slot = MERGE_TILE merged positions.
 struct SlotGeom {
   int64_t base;    // first entry of the unit's region
+  int64_t len;     // length of the unit's region (slot s holds at most min(ss, len - s ss))
   int32_t ss;      // slot size
   int32_t nslots;  // slots of this unit
 };
@@ -211,10 +212,12 @@ __device__ __forceinline__ SlotGeom slot_geom(int mode, int64_t unit, int64_t n,
     const int64_t b = unit % P, w = unit / P;
     const int64_t s = blk_start(b, n, P), e = blk_start(b + 1, n, P);
     g.base = w * n + s;
+    g.len = e - s;
     g.ss = SLOT;
     g.nslots = (int32_t)((e - s + SLOT - 1) / SLOT);
   } else {
     g.base = unit * 2 * kb;
+    g.len = 2 * kb;
     g.ss = MERGE_TILE;
     g.nslots = (int32_t)((2 * kb + MERGE_TILE - 1) / MERGE_TILE);
   }
@@ -330,135 +333,218 @@ __global__ __launch_bounds__(256) void k_collect(const float* __restrict__ acc, 
   }
 }
 
-// ============================================================================ merge: per-slot scan
-// For a merge, the level-1 threshold is known only once the whole union is
-// built.  One workgroup per slot recomputes the unit's level-1 select from
-// its histogram (identical in every workgroup), then stores the keys of the
-// slot's entries inside the threshold bin and their count -- the same
-// threshold-bin outputs k_collect produces for a dense block.
-__global__ __launch_bounds__(256) void k_mscan(const float* __restrict__ U_val, int32_t kb, int32_t smax,
-                                               const uint32_t* __restrict__ hist1, uint32_t* __restrict__ state,
-                                               const uint32_t* __restrict__ slot_cnt,
-                                               uint32_t* __restrict__ slot_nbin, uint32_t* __restrict__ slot_above,
-                                               uint32_t* __restrict__ bin_key, uint32_t* __restrict__ err) {
-  constexpr int NT = 256, NJ = MERGE_TILE / NT;
-  __shared__ uint32_t h[NB1];
-  __shared__ uint32_t scratch[16];
-  const int64_t unit = blockIdx.x / smax;
-  const int32_t slot = (int32_t)(blockIdx.x % smax);
-  g2lds<NB1 / NT>(h, hist1 + unit * NB1, NB1);
-  __syncthreads();
-  uint32_t T1, above1, cnt1, ok;
-  block_select_desc(h, NB1, (uint32_t)kb, scratch, &T1, &above1, &cnt1, &ok);
-  if (threadIdx.x == 0 && slot == 0) {
-    uint32_t* st = state + unit * ST_WORDS;
-    if (!ok) atomicOr(err, ERR_COUNT);
-    st[ST_T1] = T1;
-    st[ST_ABOVE1] = above1;
-    st[ST_NEED1] = ok ? (uint32_t)kb - above1 : 0u;
-    st[ST_CNT1] = cnt1;
-  }
-  const int64_t base = unit * 2 * (int64_t)kb + (int64_t)slot * MERGE_TILE;
-  const uint32_t count = min(slot_cnt[unit * smax + slot], (uint32_t)MERGE_TILE);
-  // thread t owns entries [t NJ, t NJ + NJ) of the slot, so its bin keys are contiguous
-  uint32_t key[NJ];
-  uint32_t nbin = 0, nab = 0;
-#pragma unroll
-  for (int j = 0; j < NJ; ++j) {
-    const uint32_t p = threadIdx.x * NJ + j;
-    key[j] = p < count ? mag_key(U_val[base + p]) : 0xFFFFFFFFu;
-    const bool valid = key[j] != 0xFFFFFFFFu;
-    nbin += (valid && (key[j] >> D1_SHIFT) == T1) ? 1u : 0u;
-    nab += (valid && (key[j] >> D1_SHIFT) > T1) ? 1u : 0u;
-  }
-  uint32_t tbin, tab;
-  block_excl_scan(nab, scratch, &tab);
-  uint32_t q = block_excl_scan(nbin, scratch, &tbin);
-  if (threadIdx.x == 0) {
-    slot_nbin[unit * smax + slot] = tbin;
-    slot_above[unit * smax + slot] = tab;
-  }
-#pragma unroll
-  for (int j = 0; j < NJ; ++j) {
-    if (key[j] != 0xFFFFFFFFu && (key[j] >> D1_SHIFT) == T1) {
-      bin_key[base + q] = key[j];
-      ++q;
-    }
-  }
-}
-
 // ============================================================================ exact threshold
-// One workgroup per unit.  The threshold-bin keys are gathered straight from
-// the slots (LPS lanes per slot; each lane walks its slot's keys with several
-// loads in flight) into the level-2 and then the level-3 histogram.  Result:
-// select every key >= TGE, plus the first NEEDEQ (by index) with key TEQ.
+// One workgroup per unit.  Resolves the exact threshold -- select every key
+// >= TGE, plus the first NEEDEQ (by index) with key TEQ -- and turns per-slot
+// counts into exclusive prefixes in index order for the emitter.
+//
+// Only the entries of the level-1 threshold bin need levels 2 and 3.  For a
+// dense block they were stored per slot by k_collect; for a merge they are
+// picked out of the union here (after the level-1 select on the union's
+// histogram, which is done here too).  When the bin fits (THRESH_CACHE
+// entries) its keys and slot numbers are gathered once into LDS and every
+// later step runs from LDS; otherwise each step re-reads global memory.
+constexpr int THRESH_CACHE = 8192;
+constexpr int GATHER_U = 8;    // loads in flight per lane in the gathers
+
+struct ThreshSmem {
+  uint32_t h[NB1];
+  uint32_t ck[THRESH_CACHE];   // cached key
+  uint32_t cs[THRESH_CACHE];   // cached slot
+  uint32_t cg[SLOT_LDS];       // per-slot count of selected-by-key (>= TGE)
+  uint32_t ce[SLOT_LDS];       // per-slot count of key == TEQ
+  uint32_t scratch[24];
+  uint32_t ncache;
+};
+
+// Threshold-bin keys of a dense block, stored per slot: f(key, slot, valid),
+// called by every lane of a wave together (so f may use ballots).  lps
+// lanes per slot, each with up to GATHER_U loads in flight.
 template <typename F>
-__device__ __forceinline__ void for_each_bin_key(const uint32_t* __restrict__ K, const SlotGeom& g,
-                                                 const uint32_t* __restrict__ nbin, int lps, F f) {
-  const int nt = blockDim.x;
-  const int per_round = nt / lps;
+__device__ __forceinline__ void visit_bin_keys(const uint32_t* __restrict__ K, const SlotGeom& g,
+                                               const uint32_t* __restrict__ nbin, int32_t s_begin,
+                                               int32_t s_end, int lps, F f) {
+  const int per_round = blockDim.x / lps;
   const int sl = threadIdx.x / lps, li = threadIdx.x % lps;
-  for (int32_t s0 = 0; s0 < g.nslots; s0 += per_round) {
+  for (int32_t s0 = s_begin; s0 < s_end; s0 += per_round) {
     const int32_t slot = s0 + sl;
-    uint32_t nb = 0;
-    if (slot < g.nslots) nb = min(nbin[slot], (uint32_t)g.ss);
-    const uint32_t* __restrict__ Ks = K + (int64_t)slot * g.ss;
-    for (uint32_t k0 = li; k0 < nb; k0 += 4 * lps) {
-      uint32_t key[4];
+    const bool live = slot < s_end;
+    const uint32_t* __restrict__ Ks = K + (int64_t)(live ? slot : s_begin) * g.ss;
+    // the slot's count and its first keys are loaded together (keys past the
+    // count are read from inside the slot and discarded)
+    const int64_t room = g.len - (int64_t)(live ? slot : s_begin) * g.ss;   // entries inside the region
+    const uint32_t cap = (uint32_t)min(min((int64_t)g.ss, room), (int64_t)GATHER_U * lps);
+    uint32_t key[GATHER_U];
 #pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        const uint32_t k = k0 + u * lps;
-        key[u] = k < nb ? Ks[k] : 0xFFFFFFFFu;
+    for (int u = 0; u < GATHER_U; ++u) {
+      const uint32_t k = u * lps + li;
+      key[u] = k < cap ? Ks[k] : 0u;
+    }
+    const uint32_t nb = live ? min(nbin[slot], (uint32_t)g.ss) : 0u;
+#pragma unroll
+    for (int u = 0; u < GATHER_U; ++u) {
+      const uint32_t k = u * lps + li;
+      f(key[u], slot, k < nb);
+    }
+    uint32_t wmax = nb;   // the wave continues as long as its longest slot needs
+#pragma unroll
+    for (int d = WAVE / 2; d > 0; d >>= 1) wmax = max(wmax, (uint32_t)__shfl_xor(wmax, d, WAVE));
+    for (uint32_t k0 = GATHER_U * lps; k0 < wmax; k0 += GATHER_U * lps) {
+#pragma unroll
+      for (int u = 0; u < GATHER_U; ++u) {
+        const uint32_t k = k0 + u * lps + li;
+        key[u] = k < nb ? Ks[k] : 0u;
       }
 #pragma unroll
-      for (int u = 0; u < 4; ++u)
-        if (key[u] != 0xFFFFFFFFu) f(key[u]);
+      for (int u = 0; u < GATHER_U; ++u) {
+        const uint32_t k = k0 + u * lps + li;
+        f(key[u], slot, k < nb);
+      }
     }
   }
 }
 
-__global__ __launch_bounds__(1024) void k_thresh(int mode, int64_t n, int32_t P, int32_t kb, int32_t smax,
-                                                 int lps, uint32_t* __restrict__ state,
+// Every entry of a merge union: f(key, slot, valid), called by all lanes
+// together (a wave's 64 positions always lie in one slot).  Values are loaded
+// together with the slot counts; positions past a slot's count are read from
+// inside the unit's region and discarded.
+template <typename F>
+__device__ __forceinline__ void visit_union(const float* __restrict__ V, const SlotGeom& g,
+                                            const uint32_t* __restrict__ cnt, int32_t s_begin, int32_t s_end,
+                                            F f) {
+  const int nt = blockDim.x;
+  const int64_t p_end = min((int64_t)s_end * g.ss, g.len);   // never read past the unit's region
+  for (int64_t p0 = (int64_t)s_begin * g.ss; p0 < p_end; p0 += (int64_t)GATHER_U * nt) {
+    float val[GATHER_U];
+    uint32_t c[GATHER_U];
+#pragma unroll
+    for (int u = 0; u < GATHER_U; ++u) {
+      const int64_t p = min(p0 + (int64_t)u * nt + threadIdx.x, p_end - 1);
+      val[u] = V[p];
+      c[u] = cnt[p / g.ss];
+    }
+#pragma unroll
+    for (int u = 0; u < GATHER_U; ++u) {
+      const int64_t p = p0 + (int64_t)u * nt + threadIdx.x;
+      const int32_t slot = (int32_t)(min(p, p_end - 1) / g.ss);
+      const bool valid = p < p_end && (uint32_t)(p - (int64_t)slot * g.ss) < min(c[u], (uint32_t)g.ss);
+      f(mag_key(val[u]), slot, valid);
+    }
+  }
+}
+
+template <int mode>
+__global__ __launch_bounds__(1024) void k_thresh(int64_t n, int32_t P, int32_t kb, int32_t smax,
+                                                 int lps, const uint32_t* __restrict__ hist1,
+                                                 const float* __restrict__ U_val, uint32_t* __restrict__ state,
                                                  const uint32_t* __restrict__ slot_cnt,
                                                  const uint32_t* __restrict__ slot_nbin,
-                                                 const uint32_t* __restrict__ slot_above,
                                                  const uint32_t* __restrict__ bin_key,
                                                  uint32_t* __restrict__ pre_all, uint32_t* __restrict__ pre_ge,
                                                  uint32_t* __restrict__ pre_eq, int32_t* __restrict__ drop_cnt,
                                                  uint32_t* __restrict__ err) {
-  __shared__ uint32_t h[NB2];
-  __shared__ uint32_t cg[SLOT_LDS], ce[SLOT_LDS];
-  __shared__ uint32_t scratch[24];
+  __shared__ ThreshSmem L;
+  constexpr int NT = 1024;
   const int64_t unit = blockIdx.x;
   uint32_t* st = state + unit * ST_WORDS;
   const SlotGeom g = slot_geom(mode, unit, n, P, kb);
-  const uint32_t* __restrict__ K = bin_key + g.base;
   const uint32_t* __restrict__ cnt = slot_cnt + unit * smax;
   const uint32_t* __restrict__ nbn = slot_nbin + unit * smax;
-  const uint32_t T1 = st[ST_T1], need1 = st[ST_NEED1], cnt1 = st[ST_CNT1];
+  const uint32_t* __restrict__ K = bin_key + g.base;
+  const float* __restrict__ V = U_val + g.base;
+  const int lane = lane_id();
+  const uint64_t lt = __lanemask_lt();
   uint32_t ok;
 
+  // ---- level 1
+  uint32_t T1, need1, cnt1;
+  if constexpr (mode == 1) {
+    g2lds<NB1 / NT>(L.h, hist1 + unit * NB1, NB1);
+    __syncthreads();
+    uint32_t above1;
+    block_select_desc(L.h, NB1, (uint32_t)kb, L.scratch, &T1, &above1, &cnt1, &ok);
+    if (!ok && threadIdx.x == 0) atomicOr(err, ERR_COUNT);
+    need1 = ok ? (uint32_t)kb - above1 : 0u;
+  } else {
+    T1 = st[ST_T1];
+    need1 = st[ST_NEED1];
+    cnt1 = st[ST_CNT1];
+  }
+  const bool cached = cnt1 <= (uint32_t)THRESH_CACHE && (mode == 0 || g.nslots <= SLOT_LDS);
+
+  // ---- gather the threshold bin into LDS (mode 1 also counts the above-bin entries per slot)
+  if (cached) {
+    if (threadIdx.x == 0) L.ncache = 0u;
+    for (int i = threadIdx.x; i < SLOT_LDS; i += NT) {
+      L.cg[i] = 0u;
+      L.ce[i] = 0u;
+    }
+    __syncthreads();
+    auto append = [&](bool take, uint32_t key, int32_t slot) {   // wave-aggregated LDS append
+      const uint64_t mk = __ballot(take);
+      if (mk == 0ull) return;
+      uint32_t base = 0;
+      if (lane == 0) base = atomicAdd(&L.ncache, popc64(mk));
+      base = __shfl(base, 0, WAVE);
+      if (take) {
+        const uint32_t q = base + popc64(mk & lt);
+        if (q < (uint32_t)THRESH_CACHE) {
+          L.ck[q] = key;
+          L.cs[q] = (uint32_t)slot;
+        }
+      }
+    };
+    if constexpr (mode == 0) {
+      visit_bin_keys(K, g, nbn, 0, g.nslots, lps,
+                     [&](uint32_t key, int32_t slot, bool valid) { append(valid, key, slot); });
+    } else {
+      visit_union(V, g, cnt, 0, g.nslots, [&](uint32_t key, int32_t slot, bool valid) {
+        const uint32_t d1 = key >> D1_SHIFT;
+        const uint64_t ma = __ballot(valid && d1 > T1);
+        if (lane == 0 && ma) atomicAdd(&L.cg[slot], popc64(ma));
+        append(valid && d1 == T1, key, slot);
+      });
+    }
+    __syncthreads();
+  }
+  const uint32_t ncache = cached ? min(L.ncache, (uint32_t)THRESH_CACHE) : 0u;
+  // every threshold-bin entry: from the cache, or from global memory
+  auto visit_bin = [&](auto f) {
+    if (cached) {
+      for (uint32_t i = threadIdx.x; i < ncache; i += NT) f(L.ck[i], (int32_t)L.cs[i]);
+    } else if constexpr (mode == 0) {
+      visit_bin_keys(K, g, nbn, 0, g.nslots, lps, [&](uint32_t key, int32_t slot, bool valid) {
+        if (valid) f(key, slot);
+      });
+    } else {
+      visit_union(V, g, cnt, 0, g.nslots, [&](uint32_t key, int32_t slot, bool valid) {
+        if (valid && (key >> D1_SHIFT) == T1) f(key, slot);
+      });
+    }
+  };
+
+  // ---- levels 2 and 3
   uint32_t tge = T1 << D1_SHIFT, teq = 0u, need_eq = 0u;
   if (need1 != cnt1) {
-    for (int i = threadIdx.x; i < NB2; i += blockDim.x) h[i] = 0u;
+    for (int i = threadIdx.x; i < NB2; i += NT) L.h[i] = 0u;
     __syncthreads();
-    for_each_bin_key(K, g, nbn, lps, [&](uint32_t key) { atomicAdd(&h[(key >> D2_SHIFT) & (NB2 - 1)], 1u); });
+    visit_bin([&](uint32_t key, int32_t) { atomicAdd(&L.h[(key >> D2_SHIFT) & (NB2 - 1)], 1u); });
     __syncthreads();
     uint32_t T2, above2, cnt2;
-    block_select_desc(h, NB2, need1, scratch, &T2, &above2, &cnt2, &ok);
+    block_select_desc(L.h, NB2, need1, L.scratch, &T2, &above2, &cnt2, &ok);
     if (!ok && threadIdx.x == 0) atomicOr(err, ERR_COUNT_L23);
     const uint32_t need2 = need1 - above2;
     const uint32_t pre23 = (T1 << (D1_SHIFT - D2_SHIFT)) | T2;   // top 23 bits of the key
     tge = pre23 << D2_SHIFT;
     if (ok && need2 != cnt2) {
-      for (int i = threadIdx.x; i < NB3; i += blockDim.x) h[i] = 0u;
+      for (int i = threadIdx.x; i < NB3; i += NT) L.h[i] = 0u;
       __syncthreads();
-      for_each_bin_key(K, g, nbn, lps, [&](uint32_t key) {
-        if ((key >> D2_SHIFT) == pre23) atomicAdd(&h[key & (NB3 - 1)], 1u);
+      visit_bin([&](uint32_t key, int32_t) {
+        if ((key >> D2_SHIFT) == pre23) atomicAdd(&L.h[key & (NB3 - 1)], 1u);
       });
       __syncthreads();
       uint32_t T3, above3, cnt3;
-      block_select_desc(h, NB3, need2, scratch, &T3, &above3, &cnt3, &ok);
+      block_select_desc(L.h, NB3, need2, L.scratch, &T3, &above3, &cnt3, &ok);
       if (!ok && threadIdx.x == 0) atomicOr(err, ERR_COUNT_L23);
       const uint32_t need3 = need2 - above3;
       const uint32_t T = (pre23 << D2_SHIFT) | T3;
@@ -472,43 +558,46 @@ __global__ __launch_bounds__(1024) void k_thresh(int mode, int64_t n, int32_t P,
     }
   }
 
-  // Per slot: ge = entries above the threshold bin + its bin keys >= TGE;
-  // eq = bin keys == TEQ; then exclusive prefixes in slot (= index) order.
-  const int nt = blockDim.x;
-  const int per_round = nt / lps;
-  const int sl = threadIdx.x / lps, li = threadIdx.x % lps;
+  // ---- per-slot counts (>= TGE, == TEQ) and their exclusive prefixes, in slot chunks
   uint32_t run_all = 0, run_ge = 0, run_eq = 0;
   for (int32_t c0 = 0; c0 < g.nslots; c0 += SLOT_LDS) {
     const int32_t nc = min(SLOT_LDS, g.nslots - c0);
-    for (int32_t s0 = 0; s0 < nc; s0 += per_round) {
-      const int32_t slot = c0 + s0 + sl;
-      uint32_t nb = 0;
-      if (s0 + sl < nc) nb = min(nbn[slot], (uint32_t)g.ss);
-      const uint32_t* __restrict__ Ks = K + (int64_t)slot * g.ss;
-      uint32_t cgt = 0, ceq = 0;
-      for (uint32_t k0 = li; k0 < nb; k0 += 4 * lps) {
-        uint32_t key[4];
-#pragma unroll
-        for (int u = 0; u < 4; ++u) {
-          const uint32_t k = k0 + u * lps;
-          key[u] = k < nb ? Ks[k] : 0xFFFFFFFFu;
+    const int32_t c1 = c0 + nc;
+    // start values: entries above the threshold bin are selected by key
+    if (!(mode == 1 && cached)) {
+      __syncthreads();
+      for (int i = threadIdx.x; i < SLOT_LDS; i += NT) {
+        uint32_t a = 0u;
+        if (mode == 0 && i < nc) {
+          const uint32_t c = min(cnt[c0 + i], (uint32_t)g.ss);
+          a = c - min(nbn[c0 + i], c);
         }
-#pragma unroll
-        for (int u = 0; u < 4; ++u) {
-          if (key[u] == 0xFFFFFFFFu) continue;
-          if (key[u] >= tge) ++cgt;
-          else if (need_eq != 0u && key[u] == teq) ++ceq;
+        L.cg[i] = a;
+        L.ce[i] = 0u;
+      }
+      __syncthreads();
+    }
+    if (mode == 1 && !cached) {
+      if constexpr (mode == 1) visit_union(V, g, cnt, c0, c1, [&](uint32_t key, int32_t slot, bool valid) {
+        const uint64_t mg = __ballot(valid && key >= tge);
+        const uint64_t me = __ballot(valid && need_eq != 0u && key == teq);
+        if (lane == 0) {
+          if (mg) atomicAdd(&L.cg[slot - c0], popc64(mg));
+          if (me) atomicAdd(&L.ce[slot - c0], popc64(me));
         }
-      }
-      for (int d = lps / 2; d > 0; d >>= 1) {   // reduce over the slot's lanes (aligned groups)
-        cgt += __shfl_xor(cgt, d, WAVE);
-        ceq += __shfl_xor(ceq, d, WAVE);
-      }
-      if (li == 0 && s0 + sl < nc) {
-        const uint32_t c = min(cnt[slot], (uint32_t)g.ss);
-        const uint32_t above = mode == 0 ? c - min(nbn[slot], c) : slot_above[unit * smax + slot];
-        cg[s0 + sl] = above + cgt;
-        ce[s0 + sl] = ceq;
+      });
+    } else {
+      auto count_bin = [&](uint32_t key, int32_t slot) {
+        if (slot < c0 || slot >= c1) return;
+        if (key >= tge) atomicAdd(&L.cg[slot - c0], 1u);
+        else if (need_eq != 0u && key == teq) atomicAdd(&L.ce[slot - c0], 1u);
+      };
+      if (cached) {
+        for (uint32_t i = threadIdx.x; i < ncache; i += NT) count_bin(L.ck[i], (int32_t)L.cs[i]);
+      } else if constexpr (mode == 0) {
+        visit_bin_keys(K, g, nbn, c0, c1, lps, [&](uint32_t key, int32_t slot, bool valid) {
+          if (valid) count_bin(key, slot);
+        });
       }
     }
     __syncthreads();
@@ -517,16 +606,16 @@ __global__ __launch_bounds__(1024) void k_thresh(int mode, int64_t n, int32_t P,
     for (int k = 0; k < 4; ++k) {
       const int i = 4 * threadIdx.x + k;
       a[k] = i < nc ? min(cnt[c0 + i], (uint32_t)g.ss) : 0u;
-      gg[k] = i < nc ? cg[i] : 0u;
-      ee[k] = i < nc ? ce[i] : 0u;
+      gg[k] = i < nc ? L.cg[i] : 0u;
+      ee[k] = i < nc ? L.ce[i] : 0u;
       sa += a[k];
       sg += gg[k];
       se += ee[k];
     }
     uint32_t ta, tg, te;
-    uint32_t xa = block_excl_scan(sa, scratch, &ta);
-    uint32_t xg = block_excl_scan(sg, scratch, &tg);
-    uint32_t xe = block_excl_scan(se, scratch, &te);
+    uint32_t xa = block_excl_scan(sa, L.scratch, &ta);
+    uint32_t xg = block_excl_scan(sg, L.scratch, &tg);
+    uint32_t xe = block_excl_scan(se, L.scratch, &te);
     const int64_t o = unit * smax + c0;
 #pragma unroll
     for (int k = 0; k < 4; ++k) {
@@ -543,10 +632,10 @@ __global__ __launch_bounds__(1024) void k_thresh(int mode, int64_t n, int32_t P,
     run_all += ta;
     run_ge += tg;
     run_eq += te;
-    __syncthreads();
   }
   if (threadIdx.x == 0) {
     if (run_ge + (run_eq < need_eq ? run_eq : need_eq) != (uint32_t)kb) atomicOr(err, ERR_COUNT_SUM);
+    st[ST_T1] = T1;
     st[ST_TGE] = tge;
     st[ST_TEQ] = teq;
     st[ST_NEEDEQ] = need_eq;
@@ -991,20 +1080,16 @@ hipError_t launch_collect(const float* acc, int64_t ld_acc, int32_t nworkers, in
   return hipGetLastError();
 }
 
-hipError_t launch_mscan(const float* U_val, int64_t npairs, int32_t kb, int32_t smax, const uint32_t* hist1,
-                        uint32_t* state, const uint32_t* slot_cnt, uint32_t* slot_nbin, uint32_t* slot_above,
-                        uint32_t* bin_key, uint32_t* err, hipStream_t s) {
-  hipLaunchKernelGGL(k_mscan, dim3((unsigned)(npairs * smax)), dim3(256), 0, s, U_val, kb, smax, hist1, state,
-                     slot_cnt, slot_nbin, slot_above, bin_key, err);
-  return hipGetLastError();
-}
-
 hipError_t launch_thresh(int mode, int64_t nunits, int64_t n, int32_t P, int32_t kb, int32_t smax, int lps,
-                         uint32_t* state, const uint32_t* slot_cnt, const uint32_t* slot_nbin,
-                         const uint32_t* slot_above, const uint32_t* bin_key, uint32_t* pre_all,
-                         uint32_t* pre_ge, uint32_t* pre_eq, int32_t* drop_cnt, uint32_t* err, hipStream_t s) {
-  hipLaunchKernelGGL(k_thresh, dim3((unsigned)nunits), dim3(1024), 0, s, mode, n, P, kb, smax, lps, state,
-                     slot_cnt, slot_nbin, slot_above, bin_key, pre_all, pre_ge, pre_eq, drop_cnt, err);
+                         const uint32_t* hist1, const float* U_val, uint32_t* state, const uint32_t* slot_cnt,
+                         const uint32_t* slot_nbin, const uint32_t* bin_key, uint32_t* pre_all, uint32_t* pre_ge,
+                         uint32_t* pre_eq, int32_t* drop_cnt, uint32_t* err, hipStream_t s) {
+  if (mode == 0)
+    hipLaunchKernelGGL(k_thresh<0>, dim3((unsigned)nunits), dim3(1024), 0, s, n, P, kb, smax, lps, hist1, U_val,
+                       state, slot_cnt, slot_nbin, bin_key, pre_all, pre_ge, pre_eq, drop_cnt, err);
+  else
+    hipLaunchKernelGGL(k_thresh<1>, dim3((unsigned)nunits), dim3(1024), 0, s, n, P, kb, smax, lps, hist1, U_val,
+                       state, slot_cnt, slot_nbin, bin_key, pre_all, pre_ge, pre_eq, drop_cnt, err);
   return hipGetLastError();
 }
 
