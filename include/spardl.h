@@ -30,10 +30,14 @@
  *    `stream` and SPARDL_OK is returned; results are valid once the stream
  *    reaches that point.
  *  - ws is scratch device memory of at least spardl_workspace_bytes(...)
- *    bytes, 256-byte aligned; its content on entry is ignored except where a
- *    flag says otherwise.  The first 4 bytes of ws hold an error word that
- *    each call clears and that kernels set if an internal check fails (see
- *    SPARDL_WS_ERR_*); read it after the stream completes if needed.
+ *    bytes, 256-byte aligned (EINVAL otherwise), prepared once by
+ *    spardl_workspace_init before its first use.  Between calls it keeps its
+ *    level-1 histograms at zero: the call that consumes a histogram clears it,
+ *    so no call spends a memset on them.  The first 4 bytes of ws hold an
+ *    error word that spardl_workspace_init clears and that kernels OR bits
+ *    into if an internal check fails (see SPARDL_WS_ERR_*); it stays set until
+ *    the next spardl_workspace_init.  Read it after the stream completes.
+ *    After an error, prepare the workspace again before reusing it.
  *  - Calls on different streams must use different ws and disjoint outputs.
  */
 #ifndef SPARDL_H
@@ -54,9 +58,13 @@ enum {
   SPARDL_EDEVICE = -3    /* a kernel launch failed (hipGetLastError) */
 };
 
-/* Bits of the error word at the start of ws (set by kernels, cleared by calls). */
-#define SPARDL_WS_ERR_LOOKBACK 1u  /* a tile's ordered-prefix wait exceeded its spin bound */
-#define SPARDL_WS_ERR_COUNT 2u     /* a selection did not produce exactly k_blk entries */
+/* Bits of the error word at the start of ws (set by kernels, cleared by
+ * spardl_workspace_init).  Bit 1 is set whenever a selection's counts are
+ * inconsistent (a histogram whose total is not the number of entries it
+ * covers, no threshold found, an output position outside [0, k_blk), or a
+ * selection without exactly k_blk entries); bits 2-5 tell which check. */
+#define SPARDL_WS_ERR_LOOKBACK 1u  /* reserved (no kernel waits on another workgroup) */
+#define SPARDL_WS_ERR_COUNT 2u     /* a selection's counts are inconsistent */
 
 /* Flag for spardl_block_topk: the level-1 |v| histograms of acc are already in
  * ws, written by the immediately preceding spardl_residual_add call with the
@@ -81,6 +89,15 @@ int spardl_srs_plan(int32_t P, int32_t* distance, int32_t* bag_blocks);
  * passed to spardl_block_topk / spardl_residual_add).  0 on invalid sizes. */
 size_t spardl_workspace_bytes(int32_t nworkers, int32_t P, int64_t n, int32_t k_blk);
 
+/* Prepares ws for calls with these sizes: clears the error word and the
+ * level-1 histograms (one small fill kernel on `stream`).  Call it once after
+ * allocating ws, and again after any call left an error bit set.
+ * Errors: EINVAL for NULL or misaligned ws or invalid sizes (as
+ * spardl_workspace_bytes); ECAPACITY if ws_bytes is below
+ * spardl_workspace_bytes(nworkers, P, n, k_blk). */
+int spardl_workspace_init(int32_t nworkers, int32_t P, int64_t n, int32_t k_blk, void* ws, size_t ws_bytes,
+                          hipStream_t stream);
+
 /* Residual add (Sec. III-B "Partitioning": each worker adds its residual
  * xi^{t-1} to its new gradient; first step of Algorithm 1):
  *   acc[w*ld_acc + x] = acc[w*ld_acc + x] + grad[w*ld_grad + x]
@@ -88,7 +105,9 @@ size_t spardl_workspace_bytes(int32_t nworkers, int32_t P, int64_t n, int32_t k_
  * serves as the copy that Algorithm 1 keeps for residual collection.
  * If P > 0 and ws != NULL, the same pass also records, for each of the P
  * blocks of each row, the level-1 |v| histogram that spardl_block_topk needs
- * (pass it SPARDL_TOPK_HIST_READY).  P = 0 (ws ignored) is a plain add.
+ * (pass it SPARDL_TOPK_HIST_READY; that call consumes and clears it, so call
+ * it before the next residual add with this ws).  P = 0 (ws ignored) is a
+ * plain add.
  * Errors: EINVAL for NULL acc/grad, nworkers < 1, n < 1 or n >= 2^31,
  * ld < n, P < 0, P > n; ECAPACITY if P > 0 and ws is too small. */
 int spardl_residual_add(float* acc, int64_t ld_acc, const float* grad, int64_t ld_grad,

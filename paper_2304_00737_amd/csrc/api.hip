@@ -37,8 +37,8 @@ inline int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 // takes the rest of ws, split into three equal arrays (candidate index,
 // candidate value, threshold-bin key).
 struct Layout {
-  size_t err = 0, bitmap = 0, hist1 = 0, state = 0, slot_cnt = 0, slot_nbin = 0, slot_above = 0, pre_all = 0,
-         pre_ge = 0, pre_eq = 0;
+  size_t err = 0, bitmap = 0, hist1 = 0, state = 0, slot_cnt = 0, slot_nbin = 0, pre_all = 0, pre_ge = 0,
+         pre_eq = 0;
   size_t fixed_end = 0;
   int64_t units = 0, tiles_tk = 0, groups_tk = 0, tiles_mg = 0, slot_n = 0, pairs_max = 0;
 };
@@ -66,8 +66,6 @@ Layout make_layout(int32_t P, int64_t n, int32_t kb) {
   off += align256((size_t)L.slot_n * 4);
   L.slot_nbin = off;
   off += align256((size_t)L.slot_n * 4);
-  L.slot_above = off;
-  off += align256((size_t)L.slot_n * 4);
   L.pre_all = off;
   off += align256((size_t)L.slot_n * 4);
   L.pre_ge = off;
@@ -82,7 +80,7 @@ inline size_t cand_bytes(int64_t entries) { return 3 * align256((size_t)entries 
 
 struct Ws {
   char* base;
-  uint32_t *err, *bitmap, *hist1, *state, *slot_cnt, *slot_nbin, *slot_above, *pre_all, *pre_ge, *pre_eq;
+  uint32_t *err, *bitmap, *hist1, *state, *slot_cnt, *slot_nbin, *pre_all, *pre_ge, *pre_eq;
   int32_t* cand_idx;
   float* cand_val;
   uint32_t* bin_key;
@@ -98,7 +96,6 @@ Ws carve(void* ws, size_t ws_bytes, const Layout& L) {
   w.state = at(L.state);
   w.slot_cnt = at(L.slot_cnt);
   w.slot_nbin = at(L.slot_nbin);
-  w.slot_above = at(L.slot_above);
   w.pre_all = at(L.pre_all);
   w.pre_ge = at(L.pre_ge);
   w.pre_eq = at(L.pre_eq);
@@ -110,6 +107,7 @@ Ws carve(void* ws, size_t ws_bytes, const Layout& L) {
 }
 
 inline bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+inline bool ws_misaligned(const void* ws) { return ((uintptr_t)ws & 255u) != 0; }
 
 // float4 streaming is used when every block start, the row length and the
 // row strides are multiples of 4 and the base pointers are 16-byte aligned.
@@ -170,8 +168,20 @@ int spardl_srs_plan(int32_t P, int32_t* distance, int32_t* bag_blocks) {
 size_t spardl_workspace_bytes(int32_t nworkers, int32_t P, int64_t n, int32_t k_blk) {
   if (!sizes_ok(P, n, k_blk) || nworkers < 1 || nworkers > P) return 0;
   const Layout L = make_layout(P, n, k_blk);
-  const int64_t cand = std::max<int64_t>((int64_t)nworkers * n, L.pairs_max * 2ll * k_blk);
+  const int64_t cand = std::max<int64_t>((int64_t)nworkers * n, L.pairs_max * L.tiles_mg * MERGE_TILE);
   return L.fixed_end + cand_bytes(cand);
+}
+
+int spardl_workspace_init(int32_t nworkers, int32_t P, int64_t n, int32_t k_blk, void* ws, size_t ws_bytes,
+                          hipStream_t stream) {
+  if (!ws || ws_misaligned(ws)) return SPARDL_EINVAL;
+  const size_t need = spardl_workspace_bytes(nworkers, P, n, k_blk);
+  if (need == 0) return SPARDL_EINVAL;
+  if (ws_bytes < need) return SPARDL_ECAPACITY;
+  const Layout L = make_layout(P, n, k_blk);
+  Ws w = carve(ws, ws_bytes, L);
+  SPARDL_TRY(launch_fill(Fill().add(w.err, 64).add(w.hist1, L.units * HCOPIES * NB1).r, stream));
+  return SPARDL_OK;
 }
 
 int spardl_residual_add(float* acc, int64_t ld_acc, const float* grad, int64_t ld_grad,
@@ -185,13 +195,12 @@ int spardl_residual_add(float* acc, int64_t ld_acc, const float* grad, int64_t l
     SPARDL_TRY(launch_residual_add(acc, ld_acc, grad, ld_grad, nworkers, n, 1, v4, nullptr, stream));
     return SPARDL_OK;
   }
-  if (nworkers > P) return SPARDL_EINVAL;
+  if (nworkers > P || ws_misaligned(ws)) return SPARDL_EINVAL;
   // Only the level-1 histogram region is used; its offset and size depend on (P, n).
   const Layout L = make_layout(P, n, 1);
   if (ws_bytes < L.state) return SPARDL_ECAPACITY;
   Ws w = carve(ws, ws_bytes, L);
   const bool v4 = aligned16(acc) && aligned16(grad) && ld_acc % 4 == 0 && ld_grad % 4 == 0 && blocks_vec4(n, P);
-  SPARDL_TRY(launch_fill(Fill().add(w.hist1, (int64_t)nworkers * P * HCOPIES * NB1).r, stream));
   SPARDL_TRY(launch_residual_add(acc, ld_acc, grad, ld_grad, nworkers, n, P, v4, w.hist1, stream));
   return SPARDL_OK;
 }
@@ -200,7 +209,7 @@ int spardl_block_topk(const float* acc, int64_t ld_acc, int32_t nworkers, int64_
                       int32_t k_blk, int32_t flags, int32_t* sp_idx, float* sp_val, int32_t* local_idx,
                       void* ws, size_t ws_bytes, hipStream_t stream) {
   if (!acc || !sp_idx || !sp_val || !ws || nworkers < 1 || nworkers > P || !sizes_ok(P, n, k_blk) ||
-      ld_acc < n || (flags & ~SPARDL_TOPK_HIST_READY))
+      ld_acc < n || (flags & ~SPARDL_TOPK_HIST_READY) || ws_misaligned(ws))
     return SPARDL_EINVAL;
   const size_t need = spardl_workspace_bytes(nworkers, P, n, k_blk);
   if (need == 0) return SPARDL_EINVAL;
@@ -210,13 +219,11 @@ int spardl_block_topk(const float* acc, int64_t ld_acc, int32_t nworkers, int64_
   const int64_t units = (int64_t)nworkers * P;
   const bool v4 = aligned16(acc) && ld_acc % 4 == 0 && blocks_vec4(n, P);
   const int32_t smax = (int32_t)L.tiles_tk, gmax = (int32_t)L.groups_tk;
-  Fill f;
-  f.add(w.err, 64);
-  if (!(flags & SPARDL_TOPK_HIST_READY)) f.add(w.hist1, units * HCOPIES * NB1);
-  SPARDL_TRY(launch_fill(f.r, stream));
-  if (!(flags & SPARDL_TOPK_HIST_READY))
+  if (!(flags & SPARDL_TOPK_HIST_READY)) {
+    SPARDL_TRY(launch_fill(Fill().add(w.hist1, units * HCOPIES * NB1).r, stream));
     SPARDL_TRY(launch_hist1(acc, ld_acc, nworkers, n, P, v4, w.hist1, stream));
-  SPARDL_TRY(launch_select1(w.hist1, w.state, units, (uint32_t)k_blk, w.err, stream));
+  }
+  SPARDL_TRY(launch_select1(w.hist1, w.state, units, n, P, (uint32_t)k_blk, w.err, stream));
   SPARDL_TRY(launch_collect(acc, ld_acc, nworkers, n, P, v4, smax, w.state, w.slot_cnt, w.slot_nbin,
                             w.cand_idx, w.cand_val, w.bin_key, stream));
   SPARDL_TRY(launch_thresh(0, units, n, P, k_blk, smax, 1, nullptr, w.cand_val, w.state, w.slot_cnt, w.slot_nbin,
@@ -230,19 +237,18 @@ int spardl_block_topk(const float* acc, int64_t ld_acc, int32_t nworkers, int64_
 int spardl_sparse_merge_topk(int32_t* sp_idx, float* sp_val, int32_t P, int64_t n, int32_t k_blk,
                              int32_t round, int32_t* drop_idx, float* drop_val, int32_t* drop_cnt,
                              void* ws, size_t ws_bytes, hipStream_t stream) {
-  if (!sp_idx || !sp_val || !drop_idx || !drop_val || !drop_cnt || !ws || P < 2 ||
+  if (!sp_idx || !sp_val || !drop_idx || !drop_val || !drop_cnt || !ws || ws_misaligned(ws) || P < 2 ||
       !sizes_ok(P, n, k_blk))
     return SPARDL_EINVAL;
   const int32_t l = steps_of(P);
   if (round < 1 || round > l) return SPARDL_EINVAL;
   const Layout L = make_layout(P, n, k_blk);
-  if (ws_bytes < L.fixed_end + cand_bytes(L.pairs_max * 2ll * k_blk)) return SPARDL_ECAPACITY;
+  if (ws_bytes < L.fixed_end + cand_bytes(L.pairs_max * L.tiles_mg * MERGE_TILE)) return SPARDL_ECAPACITY;
   Ws w = carve(ws, ws_bytes, L);
   const int32_t d = 1 << (l - round);
   const int32_t m = bag_of(P, l, round);
   const int64_t pairs = (int64_t)P * m;
   const int32_t smax = (int32_t)L.tiles_mg;
-  SPARDL_TRY(launch_fill(Fill().add(w.err, 64).add(w.hist1, pairs * NB1).r, stream));
   SPARDL_TRY(launch_merge(sp_idx, sp_val, P, k_blk, d, m, smax, w.hist1, w.slot_cnt, w.cand_idx, w.cand_val,
                           stream));
   SPARDL_TRY(launch_thresh(1, pairs, n, P, k_blk, smax, 1, w.hist1, w.cand_val, w.state, w.slot_cnt, w.slot_nbin,
@@ -265,7 +271,7 @@ int spardl_residual_collect(float* acc, int64_t ld_acc, int32_t P, int64_t n, in
                             const int32_t* const* drop_idx, const float* const* drop_val,
                             const int32_t* const* drop_cnt, void* ws, size_t ws_bytes,
                             hipStream_t stream) {
-  if (!acc || !local_idx || !sp_idx || !ws || !sizes_ok(P, n, k_blk) || ld_acc < n)
+  if (!acc || !local_idx || !sp_idx || !ws || ws_misaligned(ws) || !sizes_ok(P, n, k_blk) || ld_acc < n)
     return SPARDL_EINVAL;
   const int32_t l = steps_of(P);
   if (l > 0 && (!drop_idx || !drop_val || !drop_cnt)) return SPARDL_EINVAL;

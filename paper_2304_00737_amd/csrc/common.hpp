@@ -46,7 +46,6 @@ enum : int {
   ST_WORDS = 16
 };
 
-constexpr uint32_t ERR_LOOKBACK = 1u;
 constexpr uint32_t ERR_COUNT = 2u;            // a selection could not find its threshold
 constexpr uint32_t ERR_COUNT_L23 = 2u | 4u;   // ... at level 2 or 3
 constexpr uint32_t ERR_COUNT_POS = 2u | 8u;   // an emitted position fell outside [0, k_blk)
@@ -116,9 +115,10 @@ __device__ __forceinline__ uint32_t block_excl_scan(uint32_t v, uint32_t* scratc
 // count(bins > T) < need <= count(bins >= T).  hist is in LDS with nb bins.
 // Every thread gets the answer.  `scratch` needs blockDim/64 + 4 words of LDS.
 // If the histogram holds fewer than `need` entries, *ok is 0 and T = 0.
+// *total (optional) receives the number of entries in the histogram.
 __device__ __forceinline__ void block_select_desc(const uint32_t* hist, int nb, uint32_t need,
                                                   uint32_t* scratch, uint32_t* T, uint32_t* above,
-                                                  uint32_t* cnt, uint32_t* ok) {
+                                                  uint32_t* cnt, uint32_t* ok, uint32_t* total = nullptr) {
   const int nt = blockDim.x;
   const int per = (nb + nt - 1) / nt;
   // thread t owns bins [nb - per (t+1), nb - per t) (the highest bins go to thread 0)
@@ -128,6 +128,7 @@ __device__ __forceinline__ void block_select_desc(const uint32_t* hist, int nb, 
   for (int bin = hi - 1; bin >= lo && bin >= 0; --bin) s += hist[bin];
   uint32_t tot;
   uint32_t ex = block_excl_scan(s, scratch, &tot);
+  if (total) *total = tot;
   const int nw = nt / WAVE;
   if (threadIdx.x == 0) scratch[nw + 1] = 0;   // found flag
   __syncthreads();
@@ -174,74 +175,6 @@ __device__ __forceinline__ void g2lds(uint32_t* lds, const uint32_t* __restrict_
     const int i = threadIdx.x + u * blockDim.x;
     if (i < count) lds[i] = r[u];
   }
-}
-
-// ---------------------------------------------------------------- ordered prefix across tiles
-// Decoupled look-back (single-pass ordered prefix): each tile of a unit
-// publishes its own aggregate, then walks back over its predecessors until it
-// meets an inclusive prefix.  Tiles take their index from a ticket counter in
-// start order, so every predecessor is already running and finishes its own
-// publication without waiting on later tiles.  The wait is additionally
-// bounded: past LB_SPIN_LIMIT polls the tile records ERR_LOOKBACK and carries
-// on with a wrong prefix, so the kernel always exits.
-// A status word is [63:62] flag (0 none, 1 aggregate, 2 inclusive),
-// [61:31] field b, [30:0] field a.
-constexpr uint64_t LB_AGG = 1ull << 62;
-constexpr uint64_t LB_INC = 2ull << 62;
-constexpr uint32_t LB_SPIN_LIMIT = 1u << 22;
-
-__device__ __forceinline__ uint64_t lb_pack(uint64_t flag, uint32_t a, uint32_t b) {
-  return flag | ((uint64_t)(b & 0x7FFFFFFFu) << 31) | (uint64_t)(a & 0x7FFFFFFFu);
-}
-
-__device__ __forceinline__ void lb_store(uint64_t* p, uint64_t v) {
-  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-
-__device__ __forceinline__ uint64_t lb_load(uint64_t* p) {
-  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-
-// Called by all 64 lanes of one wave; every lane receives the exclusive
-// prefix.  The wave inspects 64 predecessors per round trip: it waits until
-// every tile up to the nearest inclusive one has published, adds their
-// aggregates and stops there.  st = the unit's status words (one per tile).
-__device__ __forceinline__ void lookback_wave(uint64_t* st, uint32_t tile, uint32_t agg_a, uint32_t agg_b,
-                                              uint32_t* ex_a, uint32_t* ex_b, uint32_t* err) {
-  const int lane = lane_id();
-  if (tile == 0) {
-    if (lane == 0) lb_store(&st[0], lb_pack(LB_INC, agg_a, agg_b));
-    *ex_a = 0;
-    *ex_b = 0;
-    return;
-  }
-  if (lane == 0) lb_store(&st[tile], lb_pack(LB_AGG, agg_a, agg_b));
-  uint32_t a = 0, b = 0, spins = 0;
-  int64_t top = (int64_t)tile - 1;   // window: tiles top, top-1, ..., top-63
-  for (;;) {
-    const int64_t t = top - lane;
-    const uint64_t s = t >= 0 ? lb_load(&st[t]) : LB_INC;
-    const uint64_t inc = __ballot((s >> 62) == 2);
-    const uint64_t none = __ballot((s >> 62) == 0);
-    const int first = inc ? (__ffsll((unsigned long long)inc) - 1) : (WAVE - 1);
-    const uint64_t upto = first == WAVE - 1 ? ~0ull : ((2ull << first) - 1ull);
-    if (none & upto) {
-      if (++spins > LB_SPIN_LIMIT) {
-        if (lane == 0) atomicOr(err, ERR_LOOKBACK);
-        break;
-      }
-      __builtin_amdgcn_s_sleep(1);
-      continue;
-    }
-    const bool take = lane <= first;
-    a += wave_sum(take ? (uint32_t)(s & 0x7FFFFFFFu) : 0u);
-    b += wave_sum(take ? (uint32_t)((s >> 31) & 0x7FFFFFFFu) : 0u);
-    if (inc) break;
-    top -= WAVE;
-  }
-  if (lane == 0) lb_store(&st[tile], lb_pack(LB_INC, a + agg_a, b + agg_b));
-  *ex_a = a;
-  *ex_b = b;
 }
 
 // ---------------------------------------------------------------- cooperative searches

@@ -12,9 +12,9 @@
 // slots (index order inside a slot) and the threshold-bin keys beside them;
 // the last two digits are resolved on those keys only; an ordered emit writes
 // the selection.  Merges of two sorted sparse blocks use merge-path tiles and
-// feed the same threshold and emit stages.  The only cross-workgroup ordering
-// (the emit) uses a bounded decoupled look-back.  No floating-point atomics
-// are used anywhere, so every result is bit-reproducible.
+// feed the same threshold and emit stages.  No workgroup ever waits on
+// another, and no floating-point atomics are used anywhere, so every result
+// is bit-reproducible.
 
 #include "common.hpp"
 #include "launch.hpp"
@@ -156,15 +156,17 @@ __global__ __launch_bounds__(256) void k_hist1(const float* __restrict__ acc, in
 
 // ============================================================================ level-1 select
 // The block's histogram is the sum of its HCOPIES copies; every load is in
-// flight before the first add.
-__global__ __launch_bounds__(1024) void k_select1(const uint32_t* __restrict__ hist1,
-                                                  uint32_t* __restrict__ state, uint32_t need,
+// flight before the first add.  The copies are cleared once read (the
+// workspace keeps its histograms at zero between steps), and their total
+// must equal the block length.
+__global__ __launch_bounds__(1024) void k_select1(uint32_t* __restrict__ hist1, uint32_t* __restrict__ state,
+                                                  int64_t n, int32_t P, uint32_t need,
                                                   uint32_t* __restrict__ err) {
   constexpr int NT = 1024, PER = NB1 / NT;
   __shared__ uint32_t h[NB1];
   __shared__ uint32_t scratch[24];
   const int64_t u = blockIdx.x;
-  const uint32_t* __restrict__ H = hist1 + u * HCOPIES * NB1;
+  uint32_t* __restrict__ H = hist1 + u * HCOPIES * NB1;
   uint32_t r[PER][HCOPIES];
 #pragma unroll
   for (int q = 0; q < PER; ++q)
@@ -174,15 +176,19 @@ __global__ __launch_bounds__(1024) void k_select1(const uint32_t* __restrict__ h
   for (int q = 0; q < PER; ++q) {
     uint32_t c = 0;
 #pragma unroll
-    for (int k = 0; k < HCOPIES; ++k) c += r[q][k];
+    for (int k = 0; k < HCOPIES; ++k) {
+      c += r[q][k];
+      H[k * NB1 + q * NT + threadIdx.x] = 0u;
+    }
     h[q * NT + threadIdx.x] = c;
   }
   __syncthreads();
-  uint32_t T, above, cnt, ok;
-  block_select_desc(h, NB1, need, scratch, &T, &above, &cnt, &ok);
+  uint32_t T, above, cnt, ok, total;
+  block_select_desc(h, NB1, need, scratch, &T, &above, &cnt, &ok, &total);
   if (threadIdx.x == 0) {
+    const int64_t b = u % P;
     uint32_t* st = state + u * ST_WORDS;
-    if (!ok) atomicOr(err, ERR_COUNT);
+    if (!ok || (int64_t)total != blk_start(b + 1, n, P) - blk_start(b, n, P)) atomicOr(err, ERR_COUNT);
     st[ST_T1] = T;
     st[ST_ABOVE1] = above;
     st[ST_NEED1] = ok ? need - above : 0u;
@@ -197,8 +203,8 @@ __global__ __launch_bounds__(1024) void k_select1(const uint32_t* __restrict__ h
 // of a parallel array.
 //  mode 0 (block top-k): unit (w, b), region = the block's span of a
 //          row-sized buffer, slot = SLOT elements of the block;
-//  mode 1 (merge):       unit = pair, region = 2 k_blk entries,
-//          slot = MERGE_TILE merged positions.
+//  mode 1 (merge):       unit = pair, region = 2 k_blk merged positions
+//          rounded up to whole slots of MERGE_TILE positions.
 struct SlotGeom {
   int64_t base;    // first entry of the unit's region
   int64_t len;     // length of the unit's region (slot s holds at most min(ss, len - s ss))
@@ -216,10 +222,10 @@ __device__ __forceinline__ SlotGeom slot_geom(int mode, int64_t unit, int64_t n,
     g.ss = SLOT;
     g.nslots = (int32_t)((e - s + SLOT - 1) / SLOT);
   } else {
-    g.base = unit * 2 * kb;
+    g.nslots = (int32_t)((2 * kb + MERGE_TILE - 1) / MERGE_TILE);
+    g.base = unit * g.nslots * MERGE_TILE;   // whole slots per unit: float4-aligned, full last slot
     g.len = 2 * kb;
     g.ss = MERGE_TILE;
-    g.nslots = (int32_t)((2 * kb + MERGE_TILE - 1) / MERGE_TILE);
   }
   return g;
 }
@@ -433,9 +439,392 @@ __device__ __forceinline__ void visit_union(const float* __restrict__ V, const S
   }
 }
 
+// ---- resident fast paths
+// When a unit's threshold-bin entries (block top-k) or its whole union
+// (merge) fit in registers -- 16 entries per thread -- they are loaded once,
+// with every load in flight together, and levels 2, 3 and the per-slot counts
+// run on registers and LDS only.  Otherwise the general path below re-reads
+// global memory for each pass.
+constexpr int FAST_SLOTS = 8192;                 // block top-k: slots per unit
+constexpr int FAST_R0 = 32;                      // block top-k: consecutive bin entries per thread
+constexpr int FAST_CAP0 = 1024 * FAST_R0;        // block top-k: bin entries per register-resident chunk
+constexpr int FAST_ROWS = 16;                    // merge: slots per unit, one float4 per thread each
+constexpr uint32_t KEY_NONE = 0xFFFFFFFFu;       // marks a register that holds no entry (keys are 31-bit)
+static_assert(MERGE_TILE == 4 * 1024, "a merge slot is one float4 per thread of the threshold kernel");
+
+struct FastSmem {
+  uint32_t pref[FAST_SLOTS + 1];   // block top-k: exclusive prefix of bin entries per slot; merge: slot counts
+  union {
+    uint16_t slotid[FAST_CAP0];    // block top-k: slot of each entry of chunk 0 (used before the histograms)
+    struct {
+      uint32_t h[NB1];
+      uint32_t cg[FAST_SLOTS];     // per-slot count of selected-by-key (>= TGE) bin entries
+      uint32_t ce[FAST_SLOTS];     // per-slot count of key == TEQ
+    } c;
+  } u;
+  uint32_t scratch[24];
+};
+
+union ThreshLds {
+  ThreshSmem g;
+  FastSmem f;
+};
+
+// Levels 2 and 3 over the threshold-bin keys: visit(f) calls f(key) for
+// every entry in bin T1.  Returns the threshold as (tge, teq, need_eq).
+template <typename Visit>
+__device__ __forceinline__ void resolve_low_digits(uint32_t T1, uint32_t need1, uint32_t cnt1, uint32_t* h,
+                                                   uint32_t* scratch, uint32_t* err, Visit visit, uint32_t& tge,
+                                                   uint32_t& teq, uint32_t& need_eq) {
+  constexpr int NT = 1024;
+  tge = T1 << D1_SHIFT;
+  teq = 0u;
+  need_eq = 0u;
+  if (need1 == cnt1) return;
+  __syncthreads();
+  for (int i = threadIdx.x; i < NB2; i += NT) h[i] = 0u;
+  __syncthreads();
+  visit([&](uint32_t key) { atomicAdd(&h[(key >> D2_SHIFT) & (NB2 - 1)], 1u); });
+  __syncthreads();
+  uint32_t T2, above2, cnt2, ok;
+  block_select_desc(h, NB2, need1, scratch, &T2, &above2, &cnt2, &ok);
+  if (!ok) {
+    if (threadIdx.x == 0) atomicOr(err, ERR_COUNT_L23);
+    return;
+  }
+  const uint32_t need2 = need1 - above2;
+  const uint32_t pre23 = (T1 << (D1_SHIFT - D2_SHIFT)) | T2;   // top 23 bits of the key
+  tge = pre23 << D2_SHIFT;
+  if (need2 == cnt2) return;
+  for (int i = threadIdx.x; i < NB3; i += NT) h[i] = 0u;
+  __syncthreads();
+  visit([&](uint32_t key) {
+    if ((key >> D2_SHIFT) == pre23) atomicAdd(&h[key & (NB3 - 1)], 1u);
+  });
+  __syncthreads();
+  uint32_t T3, above3, cnt3;
+  block_select_desc(h, NB3, need2, scratch, &T3, &above3, &cnt3, &ok);
+  if (!ok) {
+    if (threadIdx.x == 0) atomicOr(err, ERR_COUNT_L23);
+    return;
+  }
+  const uint32_t need3 = need2 - above3;
+  const uint32_t T = (pre23 << D2_SHIFT) | T3;
+  if (need3 == cnt3) {
+    tge = T;
+  } else {
+    tge = T + 1u;
+    teq = T;
+    need_eq = need3;
+  }
+}
+
+__device__ __forceinline__ void finish_unit(uint32_t* st, uint32_t T1, uint32_t tge, uint32_t teq, uint32_t need_eq,
+                                            uint32_t tot_all, uint32_t tot_ge, uint32_t tot_eq, int32_t kb,
+                                            int32_t* drop_cnt, int64_t unit, uint32_t* err, uint32_t hist_total) {
+  if (tot_ge + (tot_eq < need_eq ? tot_eq : need_eq) != (uint32_t)kb) atomicOr(err, ERR_COUNT_SUM);
+  if (drop_cnt && tot_all != hist_total) atomicOr(err, ERR_COUNT);
+  st[ST_T1] = T1;
+  st[ST_TGE] = tge;
+  st[ST_TEQ] = teq;
+  st[ST_NEEDEQ] = need_eq;
+  if (drop_cnt) drop_cnt[unit] = (int32_t)(tot_all - (uint32_t)kb);
+}
+
+// Merge unit with at most FAST_ROWS slots: row r of the register file is slot
+// r; thread t holds merged positions 4t .. 4t+3 of every slot.
+__device__ __forceinline__ void thresh_fast_merge(FastSmem& L, int64_t unit, const SlotGeom& g, int32_t kb,
+                                                  int32_t smax, const float* __restrict__ V,
+                                                  const uint32_t* __restrict__ cnt, uint32_t T1, uint32_t need1,
+                                                  uint32_t cnt1, uint32_t* st, uint32_t* __restrict__ pre_all,
+                                                  uint32_t* __restrict__ pre_ge, uint32_t* __restrict__ pre_eq,
+                                                  int32_t* __restrict__ drop_cnt, uint32_t* err, uint32_t hist_total) {
+  const int t = threadIdx.x, lane = lane_id(), wv = wave_id();
+  const int ns = g.nslots;
+  const f4v* __restrict__ V4 = reinterpret_cast<const f4v*>(V);
+  uint32_t c[FAST_ROWS];
+  f4v v[FAST_ROWS];
+#pragma unroll
+  for (int r = 0; r < FAST_ROWS; ++r) {
+    c[r] = 0u;
+    v[r] = f4v{0.f, 0.f, 0.f, 0.f};
+    if (r < ns) {
+      c[r] = cnt[r];
+      v[r] = V4[r * (MERGE_TILE / 4) + t];
+    }
+  }
+  uint32_t key[FAST_ROWS][4];
+#pragma unroll
+  for (int r = 0; r < FAST_ROWS; ++r) {
+    const uint32_t cr = min(c[r], (uint32_t)MERGE_TILE);
+#pragma unroll
+    for (int q = 0; q < 4; ++q) key[r][q] = (uint32_t)(4 * t + q) < cr ? mag_key(v[r][q]) : KEY_NONE;
+    if (t == r) L.pref[r] = cr;
+  }
+  auto visit = [&](auto f) {
+#pragma unroll
+    for (int r = 0; r < FAST_ROWS; ++r)
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+        if ((key[r][q] >> D1_SHIFT) == T1) f(key[r][q]);
+  };
+  uint32_t tge, teq, need_eq;
+  resolve_low_digits(T1, need1, cnt1, L.u.c.h, L.scratch, err, visit, tge, teq, need_eq);
+  if (t < FAST_ROWS) {
+    L.u.c.cg[t] = 0u;
+    L.u.c.ce[t] = 0u;
+  }
+  __syncthreads();
+#pragma unroll
+  for (int r = 0; r < FAST_ROWS; ++r) {
+    if (r < ns) {
+      uint32_t ng = 0, ne = 0;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        ng += popc64(__ballot(key[r][q] != KEY_NONE && key[r][q] >= tge));
+        ne += popc64(__ballot(need_eq != 0u && key[r][q] == teq));
+      }
+      if (lane == 0) {
+        if (ng) atomicAdd(&L.u.c.cg[r], ng);
+        if (ne) atomicAdd(&L.u.c.ce[r], ne);
+      }
+    }
+  }
+  __syncthreads();
+  if (wv == 0) {   // exclusive prefixes over the unit's (at most 16) slots
+    const uint32_t a = lane < ns ? L.pref[lane] : 0u;
+    const uint32_t gg = lane < ns ? L.u.c.cg[lane] : 0u;
+    const uint32_t ee = lane < ns ? L.u.c.ce[lane] : 0u;
+    const uint32_t ai = wave_incl_scan(a), gi = wave_incl_scan(gg), ei = wave_incl_scan(ee);
+    const int64_t o = unit * smax;
+    if (lane < ns) {
+      pre_all[o + lane] = ai - a;
+      pre_ge[o + lane] = gi - gg;
+      pre_eq[o + lane] = ei - ee;
+    }
+    if (lane == WAVE - 1) finish_unit(st, T1, tge, teq, need_eq, ai, gi, ei, kb, drop_cnt, unit, err, hist_total);
+  }
+}
+
+// Block top-k unit with at most FAST_SLOTS slots.  Its threshold-bin entries
+// are numbered in slot order, f = 0 .. total-1 (pref[s] = first entry of slot
+// s, pref[ns] = total), and taken in chunks of FAST_CAP0 entries, entry
+// chunk + r 1024 + t in register r of thread t (coalesced loads).  Chunk 0
+// stays in registers; the entry -> slot map of chunk 0 is built in LDS (each
+// non-empty slot marks its first entry, then a max-scan fills the gaps).  A
+// bin larger than one chunk re-reads the other chunks per pass, finding each
+// entry's slot by binary search.
+
+// The largest s in [0, ns) with pref[s] <= f (f < pref[ns]).
+__device__ __forceinline__ int slot_of_entry(const uint32_t* pref, int ns, uint32_t f) {
+  int lo = 0, hi = ns;
+  while (hi - lo > 1) {
+    const int mid = (lo + hi) >> 1;
+    if (pref[mid] <= f) lo = mid;
+    else hi = mid;
+  }
+  return lo;
+}
+
+// Exclusive prefix maximum of one value per thread over the workgroup
+// (0 for thread 0).  `scratch` needs blockDim/64 + 1 words.  Contains barriers.
+__device__ __forceinline__ uint32_t block_excl_max(uint32_t v, uint32_t* scratch) {
+  const int nw = blockDim.x / WAVE, lane = lane_id();
+  uint32_t incl = v;
+#pragma unroll
+  for (int d = 1; d < WAVE; d <<= 1) {
+    const uint32_t o = __shfl_up(incl, d, WAVE);
+    if (lane >= d) incl = max(incl, o);
+  }
+  uint32_t excl = __shfl_up(incl, 1, WAVE);
+  if (lane == 0) excl = 0u;
+  if (lane == WAVE - 1) scratch[wave_id()] = incl;
+  __syncthreads();
+  uint32_t carry = 0;
+  for (int i = 0; i < wave_id(); ++i) carry = max(carry, scratch[i]);
+  __syncthreads();
+  (void)nw;
+  return max(carry, excl);
+}
+
+// Entries of chunks after the first: fn(key, slot) for entries
+// c0 + r 1024 + t, r < FAST_R0, in batches of 8 loads in flight; the slot of
+// each entry by binary search.
+template <typename F>
+__device__ __forceinline__ void visit_bin_chunk(const uint32_t* __restrict__ K, const uint32_t* pref, int ns,
+                                                int64_t ss, uint32_t c0, uint32_t total, F fn) {
+  constexpr int B = 8;
+  for (int r0 = 0; r0 < FAST_R0; r0 += B) {
+    uint32_t key[B], sl[B];
+#pragma unroll
+    for (int r = 0; r < B; ++r) {
+      const uint32_t f = c0 + (uint32_t)((r0 + r) * 1024) + threadIdx.x;
+      key[r] = KEY_NONE;
+      sl[r] = 0u;
+      if (f < total) {
+        sl[r] = (uint32_t)slot_of_entry(pref, ns, f);
+        key[r] = K[(int64_t)sl[r] * ss + (f - pref[sl[r]])];
+      }
+    }
+#pragma unroll
+    for (int r = 0; r < B; ++r)
+      if (key[r] != KEY_NONE) fn(key[r], sl[r]);
+  }
+}
+
+__device__ __forceinline__ void thresh_fast_topk(FastSmem& L, int64_t unit, const SlotGeom& g, int32_t kb,
+                                                 int32_t smax, const uint32_t* __restrict__ K,
+                                                 const uint32_t* __restrict__ cnt, const uint32_t* __restrict__ nbn,
+                                                 uint32_t T1, uint32_t need1, uint32_t cnt1, uint32_t* st,
+                                                 uint32_t* __restrict__ pre_all, uint32_t* __restrict__ pre_ge,
+                                                 uint32_t* __restrict__ pre_eq, uint32_t* err) {
+  constexpr int NT = 1024, PS = FAST_SLOTS / NT;   // thread t owns slots PS t .. PS t + PS - 1
+  constexpr int MW = FAST_CAP0 / 2 / NT;           // slot-map words (two 16-bit ids) per thread
+  static_assert(FAST_SLOTS <= 65536, "slot ids are 16-bit");
+  const int t = threadIdx.x;
+  const int ns = g.nslots;
+  uint32_t nb[PS];
+  {
+    uint32_t ca0[PS];
+#pragma unroll
+    for (int u = 0; u < PS; ++u) {
+      const int s = PS * t + u;
+      ca0[u] = 0u;
+      nb[u] = 0u;
+      if (s < ns) {
+        ca0[u] = cnt[s];
+        nb[u] = nbn[s];
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < PS; ++u) {
+      const int s = PS * t + u;
+      const uint32_t cap = s < ns ? (uint32_t)min((int64_t)g.ss, g.len - (int64_t)s * g.ss) : 0u;
+      nb[u] = min(nb[u], min(ca0[u], cap));
+    }
+  }
+  uint32_t sb = 0;
+#pragma unroll
+  for (int u = 0; u < PS; ++u) sb += nb[u];
+  // zero the slot map of chunk 0 while the scan runs
+  uint32_t* smw = reinterpret_cast<uint32_t*>(L.u.slotid);
+#pragma unroll
+  for (int q = 0; q < MW; ++q) smw[q * NT + t] = 0u;
+  uint32_t total;
+  uint32_t run = block_excl_scan(sb, L.scratch, &total);   // has barriers: the map is zero after it
+  if (total != cnt1 && t == 0) atomicOr(err, ERR_COUNT);
+  const uint32_t m = min(total, (uint32_t)FAST_CAP0);
+#pragma unroll
+  for (int u = 0; u < PS; ++u) {
+    const int s = PS * t + u;
+    if (s < ns) {
+      L.pref[s] = run;
+      if (nb[u] != 0u && run < m) L.u.slotid[run] = (uint16_t)s;   // first entry of a non-empty slot
+    }
+    run += nb[u];
+  }
+  if (t == 0) L.pref[ns] = total;
+  __syncthreads();
+  // fill forward: slot of entry f = the last slot head at or before f
+  {
+    uint32_t wv[MW / 2 * 2];
+    uint32_t mx = 0u;
+#pragma unroll
+    for (int q = 0; q < MW; ++q) {
+      wv[q] = smw[MW * t + q];
+      mx = max(mx, max(wv[q] & 0xFFFFu, wv[q] >> 16));
+    }
+    uint32_t run_max = block_excl_max(mx, L.scratch);
+#pragma unroll
+    for (int q = 0; q < MW; ++q) {
+      const uint32_t lo = max(run_max, wv[q] & 0xFFFFu);
+      const uint32_t hi = max(lo, wv[q] >> 16);
+      run_max = hi;
+      smw[MW * t + q] = lo | (hi << 16);
+    }
+  }
+  __syncthreads();
+  const uint32_t nchunks = (total + FAST_CAP0 - 1) / FAST_CAP0;
+  uint32_t rk[FAST_R0], rs[FAST_R0 / 2];
+#pragma unroll
+  for (int r = 0; r < FAST_R0; ++r) {
+    const uint32_t f = (uint32_t)(r * NT + t);
+    uint32_t key = KEY_NONE, sl = 0u;
+    if (f < m) {
+      sl = L.u.slotid[f];
+      key = K[(int64_t)sl * g.ss + (f - L.pref[sl])];
+    }
+    rk[r] = key;
+    if (r & 1) rs[r / 2] |= sl << 16;
+    else rs[r / 2] = sl;
+  }
+  __syncthreads();   // the slot map is dead from here (its LDS holds the histograms next)
+  auto visit = [&](auto fn) {
+#pragma unroll
+    for (int r = 0; r < FAST_R0; ++r)
+      if ((rk[r] >> D1_SHIFT) == T1) fn(rk[r]);
+    for (uint32_t c = 1; c < nchunks; ++c)
+      visit_bin_chunk(K, L.pref, ns, g.ss, c * FAST_CAP0, total, [&](uint32_t key, uint32_t) {
+        if ((key >> D1_SHIFT) == T1) fn(key);
+      });
+  };
+  uint32_t tge, teq, need_eq;
+  resolve_low_digits(T1, need1, cnt1, L.u.c.h, L.scratch, err, visit, tge, teq, need_eq);
+  for (int i = t; i < ns; i += NT) {
+    L.u.c.cg[i] = 0u;
+    L.u.c.ce[i] = 0u;
+  }
+  __syncthreads();
+  auto count1 = [&](uint32_t key, uint32_t si) {
+    if (key >= tge) atomicAdd(&L.u.c.cg[si], 1u);
+    else if (need_eq != 0u && key == teq) atomicAdd(&L.u.c.ce[si], 1u);
+  };
+#pragma unroll
+  for (int r = 0; r < FAST_R0; ++r)
+    if (rk[r] != KEY_NONE) count1(rk[r], (r & 1) ? (rs[r / 2] >> 16) : (rs[r / 2] & 0xFFFFu));
+  for (uint32_t c = 1; c < nchunks; ++c) visit_bin_chunk(K, L.pref, ns, g.ss, c * FAST_CAP0, total, count1);
+  __syncthreads();
+  uint32_t sa = 0, sg = 0, se = 0, ca[PS], gq[PS], eq[PS];
+#pragma unroll
+  for (int u = 0; u < PS; ++u) {
+    const int s = PS * t + u;
+    ca[u] = s < ns ? cnt[s] : 0u;
+  }
+#pragma unroll
+  for (int u = 0; u < PS; ++u) {
+    const int s = PS * t + u;
+    const uint32_t cap = s < ns ? (uint32_t)min((int64_t)g.ss, g.len - (int64_t)s * g.ss) : 0u;
+    ca[u] = min(ca[u], cap);
+    const uint32_t nbu = s < ns ? L.pref[s + 1] - L.pref[s] : 0u;   // bin entries of the slot (<= ca)
+    gq[u] = s < ns ? ca[u] - nbu + L.u.c.cg[s] : 0u;                 // entries above the bin are all selected
+    eq[u] = s < ns ? L.u.c.ce[s] : 0u;
+    sa += ca[u];
+    sg += gq[u];
+    se += eq[u];
+  }
+  uint32_t ta, tg, te;
+  uint32_t xa = block_excl_scan(sa, L.scratch, &ta);
+  uint32_t xg = block_excl_scan(sg, L.scratch, &tg);
+  uint32_t xe = block_excl_scan(se, L.scratch, &te);
+  const int64_t o = unit * smax;
+#pragma unroll
+  for (int u = 0; u < PS; ++u) {
+    const int s = PS * t + u;
+    if (s < ns) {
+      pre_all[o + s] = xa;
+      pre_ge[o + s] = xg;
+      pre_eq[o + s] = xe;
+    }
+    xa += ca[u];
+    xg += gq[u];
+    xe += eq[u];
+  }
+  if (t == 0) finish_unit(st, T1, tge, teq, need_eq, ta, tg, te, kb, nullptr, unit, err, 0u);
+}
+
 template <int mode>
 __global__ __launch_bounds__(1024) void k_thresh(int64_t n, int32_t P, int32_t kb, int32_t smax,
-                                                 int lps, const uint32_t* __restrict__ hist1,
+                                                 int lps, uint32_t* __restrict__ hist1,
                                                  const float* __restrict__ U_val, uint32_t* __restrict__ state,
                                                  const uint32_t* __restrict__ slot_cnt,
                                                  const uint32_t* __restrict__ slot_nbin,
@@ -443,7 +832,8 @@ __global__ __launch_bounds__(1024) void k_thresh(int64_t n, int32_t P, int32_t k
                                                  uint32_t* __restrict__ pre_all, uint32_t* __restrict__ pre_ge,
                                                  uint32_t* __restrict__ pre_eq, int32_t* __restrict__ drop_cnt,
                                                  uint32_t* __restrict__ err) {
-  __shared__ ThreshSmem L;
+  __shared__ ThreshLds S;
+  ThreshSmem& L = S.g;
   constexpr int NT = 1024;
   const int64_t unit = blockIdx.x;
   uint32_t* st = state + unit * ST_WORDS;
@@ -458,17 +848,33 @@ __global__ __launch_bounds__(1024) void k_thresh(int64_t n, int32_t P, int32_t k
 
   // ---- level 1
   uint32_t T1, need1, cnt1;
+  uint32_t hist_total = 0;
   if constexpr (mode == 1) {
-    g2lds<NB1 / NT>(L.h, hist1 + unit * NB1, NB1);
+    uint32_t* __restrict__ H = hist1 + unit * NB1;
+    g2lds<NB1 / NT>(L.h, H, NB1);
+#pragma unroll
+    for (int q = 0; q < NB1 / NT; ++q) H[q * NT + threadIdx.x] = 0u;   // histograms rest at zero
     __syncthreads();
     uint32_t above1;
-    block_select_desc(L.h, NB1, (uint32_t)kb, L.scratch, &T1, &above1, &cnt1, &ok);
+    block_select_desc(L.h, NB1, (uint32_t)kb, L.scratch, &T1, &above1, &cnt1, &ok, &hist_total);
     if (!ok && threadIdx.x == 0) atomicOr(err, ERR_COUNT);
     need1 = ok ? (uint32_t)kb - above1 : 0u;
   } else {
     T1 = st[ST_T1];
     need1 = st[ST_NEED1];
     cnt1 = st[ST_CNT1];
+  }
+  if constexpr (mode == 1) {
+    if (g.nslots <= FAST_ROWS) {
+      thresh_fast_merge(S.f, unit, g, kb, smax, V, cnt, T1, need1, cnt1, st, pre_all, pre_ge, pre_eq, drop_cnt,
+                        err, hist_total);
+      return;
+    }
+  } else {
+    if (g.nslots <= FAST_SLOTS) {
+      thresh_fast_topk(S.f, unit, g, kb, smax, K, cnt, nbn, T1, need1, cnt1, st, pre_all, pre_ge, pre_eq, err);
+      return;
+    }
   }
   const bool cached = cnt1 <= (uint32_t)THRESH_CACHE && (mode == 0 || g.nslots <= SLOT_LDS);
 
@@ -639,7 +1045,10 @@ __global__ __launch_bounds__(1024) void k_thresh(int64_t n, int32_t P, int32_t k
     st[ST_TGE] = tge;
     st[ST_TEQ] = teq;
     st[ST_NEEDEQ] = need_eq;
-    if (mode == 1) drop_cnt[unit] = (int32_t)(run_all - (uint32_t)kb);
+    if (mode == 1) {
+      drop_cnt[unit] = (int32_t)(run_all - (uint32_t)kb);
+      if (run_all != hist_total) atomicOr(err, ERR_COUNT);
+    }
   }
 }
 
@@ -897,7 +1306,7 @@ __global__ __launch_bounds__(MERGE_THREADS) void k_merge(
   uint32_t tot;
   uint32_t pos = block_excl_scan(cnt, scratch, &tot);
   if (threadIdx.x == 0) slot_cnt[pair * tiles_per_pair + tile] = tot;
-  const int64_t ubase = pair * (int64_t)L2 + Q0;
+  const int64_t ubase = pair * (int64_t)tiles_per_pair * MERGE_TILE + Q0;
 #pragma unroll
   for (int k = 0; k < MERGE_PER_THREAD; ++k) {
     if (eok[k]) {
@@ -1064,9 +1473,9 @@ hipError_t launch_hist1(const float* acc, int64_t ld_acc, int32_t nworkers, int6
   return hipGetLastError();
 }
 
-hipError_t launch_select1(const uint32_t* hist1, uint32_t* state, int64_t nunits, uint32_t need,
+hipError_t launch_select1(uint32_t* hist1, uint32_t* state, int64_t nunits, int64_t n, int32_t P, uint32_t need,
                           uint32_t* err, hipStream_t s) {
-  hipLaunchKernelGGL(k_select1, dim3((unsigned)nunits), dim3(1024), 0, s, hist1, state, need, err);
+  hipLaunchKernelGGL(k_select1, dim3((unsigned)nunits), dim3(1024), 0, s, hist1, state, n, P, need, err);
   return hipGetLastError();
 }
 
@@ -1081,7 +1490,7 @@ hipError_t launch_collect(const float* acc, int64_t ld_acc, int32_t nworkers, in
 }
 
 hipError_t launch_thresh(int mode, int64_t nunits, int64_t n, int32_t P, int32_t kb, int32_t smax, int lps,
-                         const uint32_t* hist1, const float* U_val, uint32_t* state, const uint32_t* slot_cnt,
+                         uint32_t* hist1, const float* U_val, uint32_t* state, const uint32_t* slot_cnt,
                          const uint32_t* slot_nbin, const uint32_t* bin_key, uint32_t* pre_all, uint32_t* pre_ge,
                          uint32_t* pre_eq, int32_t* drop_cnt, uint32_t* err, hipStream_t s) {
   if (mode == 0)

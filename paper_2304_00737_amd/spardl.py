@@ -35,6 +35,8 @@ _lib.spardl_srs_plan.argtypes = [_i32, _p, _p]
 _lib.spardl_srs_plan.restype = ctypes.c_int
 _lib.spardl_workspace_bytes.argtypes = [_i32, _i32, _i64, _i32]
 _lib.spardl_workspace_bytes.restype = _sz
+_lib.spardl_workspace_init.argtypes = [_i32, _i32, _i64, _i32, _p, _sz, _p]
+_lib.spardl_workspace_init.restype = ctypes.c_int
 _lib.spardl_residual_add.argtypes = [_p, _i64, _p, _i64, _i32, _i64, _i32, _p, _sz, _p]
 _lib.spardl_block_topk.argtypes = [_p, _i64, _i32, _i64, _i32, _i32, _i32, _p, _p, _p, _p, _sz, _p]
 _lib.spardl_sparse_merge_topk.argtypes = [_p, _p, _i32, _i64, _i32, _i32, _p, _p, _p, _p, _sz, _p]
@@ -91,6 +93,18 @@ def srs_plan(P: int):
 
 def workspace_bytes(nworkers: int, P: int, n: int, k_blk: int) -> int:
     return int(_lib.spardl_workspace_bytes(nworkers, P, n, k_blk))
+
+
+def workspace_init(ws, nworkers: int, P: int, n: int, k_blk: int, *, stream=None) -> None:
+    _check("workspace_init", _lib.spardl_workspace_init(nworkers, P, n, k_blk, _ptr(ws),
+                                                        ws.numel() * ws.element_size(), _stream(stream)))
+
+
+def workspace(nworkers: int, P: int, n: int, k_blk: int, device="cuda", *, stream=None):
+    """A prepared workspace (uint8 device tensor) for calls with these sizes."""
+    ws = torch.empty(workspace_bytes(nworkers, P, n, k_blk), dtype=torch.uint8, device=device)
+    workspace_init(ws, nworkers, P, n, k_blk, stream=stream)
+    return ws
 
 
 def residual_add(acc, grad, nworkers: int, n: int, P: int = 0, ws=None, *, ld_acc=None, ld_grad=None,
@@ -158,7 +172,7 @@ class SparDLStep:
         self.drop_val = [torch.empty((P, m, k_blk), dtype=torch.float32, device=dev) for m in self.bags]
         self.drop_cnt = [torch.empty((P, m), dtype=torch.int32, device=dev) for m in self.bags]
         self.dense = torch.empty(n, dtype=torch.float32, device=dev)
-        self.ws = torch.empty(workspace_bytes(P, P, n, k_blk), dtype=torch.uint8, device=dev)
+        self.ws = workspace(P, P, n, k_blk, device=dev)
 
     def residual_add(self, grad, stream=None):
         if self.fused:

@@ -98,6 +98,19 @@ def test_argument_errors_enqueue_nothing():
                                  sz(1 << 30), null) == EINVAL
     assert lib.spardl_block_topk(p, i64(100), i32(1), i64(100), i32(4), i32(3), i32(0), p, p, null, p,
                                  sz(64), null) == ECAP
+    # workspace_init: NULL, misaligned, too small, bad sizes
+    lib.spardl_workspace_init.argtypes = [i32, i32, i64, i32, ctypes.c_void_p, sz, ctypes.c_void_p]
+    assert lib.spardl_workspace_init(i32(1), i32(4), i64(100), i32(3), null, sz(1 << 30), null) == EINVAL
+    assert lib.spardl_workspace_init(i32(1), i32(4), i64(100), i32(3), ctypes.c_void_p(0x1010), sz(1 << 30),
+                                     null) == EINVAL
+    assert lib.spardl_workspace_init(i32(1), i32(4), i64(100), i32(3), p, sz(64), null) == ECAP
+    assert lib.spardl_workspace_init(i32(5), i32(4), i64(100), i32(3), p, sz(1 << 30), null) == EINVAL
+    # a workspace that is not 256-byte aligned
+    q = ctypes.c_void_p(0x1010)
+    assert lib.spardl_block_topk(p, i64(100), i32(1), i64(100), i32(4), i32(3), i32(0), p, p, null, q,
+                                 sz(1 << 30), null) == EINVAL
+    assert lib.spardl_sparse_merge_topk(p, p, i32(6), i64(600), i32(3), i32(1), p, p, p, q, sz(1 << 30),
+                                        null) == EINVAL
     # merge: P < 2, round out of range, small workspace
     assert lib.spardl_sparse_merge_topk(p, p, i32(1), i64(100), i32(3), i32(1), p, p, p, p, sz(1 << 30), null) == EINVAL
     assert lib.spardl_sparse_merge_topk(p, p, i32(6), i64(600), i32(3), i32(4), p, p, p, p, sz(1 << 30), null) == EINVAL

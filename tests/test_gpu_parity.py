@@ -51,7 +51,7 @@ def test_residual_add(P, n, ld, hist):
     a_d, g_d = _dev(acc), _dev(grad)
     ws = None
     if hist:
-        ws = torch.empty(spardl.workspace_bytes(P, P, n, 1), dtype=torch.uint8, device="cuda")
+        ws = spardl.workspace(P, P, n, 1)
     spardl.residual_add(a_d, g_d, P, n, P if hist else 0, ws, ld_acc=ld, ld_grad=ld)
     want = acc.copy()
     want[:, :n] = so.residual_add(acc[:, :n], grad[:, :n])
@@ -73,6 +73,8 @@ TOPK_CASES = [
     (8, 300000, 400, "ties"),
     (16, 1 << 18, 100, "normal"),
     (3, 100003, 33334, "dyadic"),
+    (2, 200000, 1000, "const"),        # a 100000-entry threshold bin: several register chunks
+    (4, 400000, 5000, "ties"),
 ]
 
 
@@ -104,11 +106,12 @@ def test_block_topk_subset_rows():
     P, n, kb = 6, 60000, 77
     acc = _rows("ties", P, n, 5)
     a_d = _dev(acc)
-    ws = torch.empty(spardl.workspace_bytes(1, P, n, kb), dtype=torch.uint8, device="cuda")
+    ws = spardl.workspace(1, P, n, kb)
     sp_i = torch.empty((P, P, kb), dtype=torch.int32, device="cuda")
     sp_v = torch.empty((P, P, kb), dtype=torch.float32, device="cuda")
     for w in range(P):
         spardl.block_topk(a_d[w], 1, n, P, kb, sp_i[w], sp_v[w], None, ws)
+    assert spardl.ws_error(ws) == 0
     bounds = so.block_bounds(n, P)
     si, sv = sp_i.cpu().numpy(), sp_v.cpu().numpy()
     for w in range(P):
@@ -146,7 +149,7 @@ def test_merge_rounds(P, kb, overlap, kind):
     idx, val = _random_state(P, n, kb, overlap, kind, 1000 + P + kb)
     sp_i, sp_v = _dev(idx), _dev(val)
     l, dist, bags = spardl.srs_plan(P)
-    ws = torch.empty(spardl.workspace_bytes(P, P, n, kb), dtype=torch.uint8, device="cuda")
+    ws = spardl.workspace(P, P, n, kb)
     sched = so.srs_schedule(P)
     assert [s.distance for s in sched] == dist
     for step in sched:
@@ -242,6 +245,24 @@ def test_deterministic():
                     snap.append(di[w, t, :dc[w, t]].tobytes() + dv[w, t, :dc[w, t]].tobytes())
         outs.append(snap)
     assert outs[0] == outs[1]
+
+
+def test_histogram_misuse_is_flagged():
+    """Two residual adds into one workspace without the top-k that consumes
+    the histogram double-count it; the next top-k must flag the inconsistent
+    total in the (sticky) error word, and workspace_init must clear it."""
+    P, n, kb = 4, 40000, 50
+    st = spardl.SparDLStep(P, n, kb)
+    grad = _dev(_rows("normal", P, n, 77))
+    st.residual_add(grad)
+    st.residual_add(grad)
+    st.block_topk()
+    assert spardl.ws_error(st.ws) & spardl.WS_ERR_COUNT
+    spardl.workspace_init(st.ws, P, P, n, kb)
+    assert spardl.ws_error(st.ws) == 0
+    st.residual_add(grad)
+    st.block_topk()
+    assert spardl.ws_error(st.ws) == 0
 
 
 def test_invalid_arguments_raise():
