@@ -58,11 +58,29 @@ __host__ __device__ __forceinline__ int64_t blk_start(int64_t b, int64_t n, int6
   return (b * n) / P;
 }
 
-__device__ __forceinline__ int64_t block_of(int64_t x, int64_t n, int64_t P) {
-  int64_t b = (x * P) / n;
-  while (b + 1 < P && blk_start(b + 1, n, P) <= x) ++b;
-  while (b > 0 && blk_start(b, n, P) > x) --b;
-  return b;
+// The P blocks of a row of n < 2^31 elements, block b = [start(b), start(b+1))
+// with start(b) = floor(b n / P).  With q = n / P and r = n % P supplied by the
+// host, start(b) = b q + floor(b r / P) takes 32-bit arithmetic only when
+// P < 2^16 (b r < P^2 < 2^32); kernels index everything in 32 bits so that no
+// 64-bit division (a long scalar sequence per wave) precedes their loads.
+struct Blocks {
+  uint32_t n, P, q, r;
+  __device__ __forceinline__ uint32_t start(uint32_t b) const {
+    if (P < 65536u) return b * q + (b * r) / P;
+    return (uint32_t)(((uint64_t)b * n) / P);
+  }
+  // block containing element x < n
+  __device__ __forceinline__ uint32_t of(uint32_t x) const {
+    uint32_t b = x / q;   // q >= 1; start(b) >= b q, so this never undershoots
+    if (b > P - 1u) b = P - 1u;
+    while (b > 0u && start(b) > x) --b;
+    while (b + 1u < P && start(b + 1u) <= x) ++b;
+    return b;
+  }
+};
+
+inline Blocks make_blocks(int64_t n, int32_t P) {
+  return Blocks{(uint32_t)n, (uint32_t)P, (uint32_t)(n / P), (uint32_t)(n % P)};
 }
 
 __device__ __forceinline__ int lane_id() { return threadIdx.x & (WAVE - 1); }

@@ -19,6 +19,8 @@
 #include "common.hpp"
 #include "launch.hpp"
 
+#include <algorithm>
+
 namespace spardl {
 
 typedef float f4v __attribute__((ext_vector_type(4)));
@@ -41,6 +43,16 @@ __global__ __launch_bounds__(256) void k_fill(FillRanges r) {
   }
 }
 
+// Adds the non-zero bins of an LDS histogram of NB1 bins into a global one.
+// Consecutive lanes take consecutive bins, so one wave's atomics fall on a
+// few cache lines (a lane-strided split multiplies the L2 atomic requests).
+__device__ __forceinline__ void flush_hist(const uint32_t* h, uint32_t* __restrict__ H) {
+  for (int i = threadIdx.x; i < NB1; i += blockDim.x) {
+    const uint32_t c = h[i];
+    if (c) atomicAdd(&H[i], c);
+  }
+}
+
 // ============================================================================ a1: residual add
 // One workgroup = one tile of ADD_TILE elements of one block of one row.
 // With HIST, every sum's level-1 digit is counted in an LDS histogram that is
@@ -49,26 +61,25 @@ __global__ __launch_bounds__(256) void k_fill(FillRanges r) {
 template <int VEC, bool HIST>
 __global__ __launch_bounds__(256) void k_residual_add(float* __restrict__ acc, int64_t ld_acc,
                                                       const float* __restrict__ grad, int64_t ld_grad,
-                                                      int64_t n, int32_t P, int32_t G,
-                                                      uint32_t* __restrict__ hist1) {
-  __shared__ uint32_t h[HIST ? NB1 : 1];
-  const int g = blockIdx.x % G;
-  const int64_t wb = blockIdx.x / G;
-  const int64_t b = wb % P, w = wb / P;
-  const int64_t s = blk_start(b, n, P), e = blk_start(b + 1, n, P);
-  const int64_t t0 = s + (int64_t)g * ADD_TILE;
+                                                      Blocks B, uint32_t G, uint32_t* __restrict__ hist1) {
+  __shared__ __align__(16) uint32_t h[HIST ? NB1 : 4];
+  const uint32_t g = blockIdx.x % G;
+  const uint32_t wb = blockIdx.x / G;
+  const uint32_t b = wb % B.P, w = wb / B.P;
+  const uint32_t s = B.start(b), e = B.start(b + 1u);
+  const uint32_t t0 = s + g * (uint32_t)ADD_TILE;
   if (t0 >= e) return;
   if (HIST) {
-    for (int i = threadIdx.x; i < NB1; i += 256) h[i] = 0u;
+    for (int i = threadIdx.x; i < NB1 / 4; i += 256) reinterpret_cast<uint4*>(h)[i] = make_uint4(0u, 0u, 0u, 0u);
     __syncthreads();
   }
-  float* __restrict__ A = acc + w * ld_acc;
-  const float* __restrict__ Gr = grad + w * ld_grad;
+  float* __restrict__ A = acc + (int64_t)w * ld_acc;
+  const float* __restrict__ Gr = grad + (int64_t)w * ld_grad;
   if (VEC == 4) {
     f4v a[ADD_F4], gg[ADD_F4];
 #pragma unroll
     for (int j = 0; j < ADD_F4; ++j) {
-      const int64_t off = t0 + ((int64_t)j * 256 + threadIdx.x) * 4;
+      const uint32_t off = t0 + (j * 256u + threadIdx.x) * 4u;
       if (off < e) {
         a[j] = *reinterpret_cast<const f4v*>(A + off);
         gg[j] = __builtin_nontemporal_load(reinterpret_cast<const f4v*>(Gr + off));
@@ -76,7 +87,7 @@ __global__ __launch_bounds__(256) void k_residual_add(float* __restrict__ acc, i
     }
 #pragma unroll
     for (int j = 0; j < ADD_F4; ++j) {
-      const int64_t off = t0 + ((int64_t)j * 256 + threadIdx.x) * 4;
+      const uint32_t off = t0 + (j * 256u + threadIdx.x) * 4u;
       if (off < e) {
         f4v r;
         r.x = a[j].x + gg[j].x;
@@ -95,7 +106,7 @@ __global__ __launch_bounds__(256) void k_residual_add(float* __restrict__ acc, i
   } else {
 #pragma unroll
     for (int j = 0; j < ADD_F4 * 4; ++j) {
-      const int64_t off = t0 + (int64_t)j * 256 + threadIdx.x;
+      const uint32_t off = t0 + j * 256u + threadIdx.x;
       if (off < e) {
         const float r = A[off] + Gr[off];
         A[off] = r;
@@ -105,32 +116,29 @@ __global__ __launch_bounds__(256) void k_residual_add(float* __restrict__ acc, i
   }
   if (HIST) {
     __syncthreads();
-    uint32_t* __restrict__ H = hist1 + (wb * HCOPIES + blockIdx.x % HCOPIES) * NB1;
-    for (int i = threadIdx.x; i < NB1; i += 256) {
-      const uint32_t c = h[i];
-      if (c) atomicAdd(&H[i], c);
-    }
+    uint32_t* __restrict__ H = hist1 + ((int64_t)wb * HCOPIES + blockIdx.x % HCOPIES) * NB1;
+    flush_hist(h, H);
   }
 }
 
 // Level-1 histogram only (block_topk without a fused residual add).
 template <int VEC>
-__global__ __launch_bounds__(256) void k_hist1(const float* __restrict__ acc, int64_t ld_acc, int64_t n,
-                                               int32_t P, int32_t G, uint32_t* __restrict__ hist1) {
-  __shared__ uint32_t h[NB1];
-  const int g = blockIdx.x % G;
-  const int64_t wb = blockIdx.x / G;
-  const int64_t b = wb % P, w = wb / P;
-  const int64_t s = blk_start(b, n, P), e = blk_start(b + 1, n, P);
-  const int64_t t0 = s + (int64_t)g * ADD_TILE;
+__global__ __launch_bounds__(256) void k_hist1(const float* __restrict__ acc, int64_t ld_acc, Blocks B,
+                                               uint32_t G, uint32_t* __restrict__ hist1) {
+  __shared__ __align__(16) uint32_t h[NB1];
+  const uint32_t g = blockIdx.x % G;
+  const uint32_t wb = blockIdx.x / G;
+  const uint32_t b = wb % B.P, w = wb / B.P;
+  const uint32_t s = B.start(b), e = B.start(b + 1u);
+  const uint32_t t0 = s + g * (uint32_t)ADD_TILE;
   if (t0 >= e) return;
-  for (int i = threadIdx.x; i < NB1; i += 256) h[i] = 0u;
+  for (int i = threadIdx.x; i < NB1 / 4; i += 256) reinterpret_cast<uint4*>(h)[i] = make_uint4(0u, 0u, 0u, 0u);
   __syncthreads();
-  const float* __restrict__ A = acc + w * ld_acc;
+  const float* __restrict__ A = acc + (int64_t)w * ld_acc;
   if (VEC == 4) {
 #pragma unroll
     for (int j = 0; j < ADD_F4; ++j) {
-      const int64_t off = t0 + ((int64_t)j * 256 + threadIdx.x) * 4;
+      const uint32_t off = t0 + (j * 256u + threadIdx.x) * 4u;
       if (off < e) {
         const f4v a = *reinterpret_cast<const f4v*>(A + off);
         atomicAdd(&h[mag_key(a.x) >> D1_SHIFT], 1u);
@@ -142,16 +150,13 @@ __global__ __launch_bounds__(256) void k_hist1(const float* __restrict__ acc, in
   } else {
 #pragma unroll
     for (int j = 0; j < ADD_F4 * 4; ++j) {
-      const int64_t off = t0 + (int64_t)j * 256 + threadIdx.x;
+      const uint32_t off = t0 + j * 256u + threadIdx.x;
       if (off < e) atomicAdd(&h[mag_key(A[off]) >> D1_SHIFT], 1u);
     }
   }
   __syncthreads();
-  uint32_t* __restrict__ H = hist1 + (wb * HCOPIES + blockIdx.x % HCOPIES) * NB1;
-  for (int i = threadIdx.x; i < NB1; i += 256) {
-    const uint32_t c = h[i];
-    if (c) atomicAdd(&H[i], c);
-  }
+  uint32_t* __restrict__ H = hist1 + ((int64_t)wb * HCOPIES + blockIdx.x % HCOPIES) * NB1;
+  flush_hist(h, H);
 }
 
 // ============================================================================ level-1 select
@@ -160,7 +165,7 @@ __global__ __launch_bounds__(256) void k_hist1(const float* __restrict__ acc, in
 // workspace keeps its histograms at zero between steps), and their total
 // must equal the block length.
 __global__ __launch_bounds__(1024) void k_select1(uint32_t* __restrict__ hist1, uint32_t* __restrict__ state,
-                                                  int64_t n, int32_t P, uint32_t need,
+                                                  Blocks B, uint32_t need,
                                                   uint32_t* __restrict__ err) {
   constexpr int NT = 1024, PER = NB1 / NT;
   __shared__ uint32_t h[NB1];
@@ -186,9 +191,9 @@ __global__ __launch_bounds__(1024) void k_select1(uint32_t* __restrict__ hist1, 
   uint32_t T, above, cnt, ok, total;
   block_select_desc(h, NB1, need, scratch, &T, &above, &cnt, &ok, &total);
   if (threadIdx.x == 0) {
-    const int64_t b = u % P;
+    const uint32_t b = (uint32_t)u % B.P;
     uint32_t* st = state + u * ST_WORDS;
-    if (!ok || (int64_t)total != blk_start(b + 1, n, P) - blk_start(b, n, P)) atomicOr(err, ERR_COUNT);
+    if (!ok || total != B.start(b + 1u) - B.start(b)) atomicOr(err, ERR_COUNT);
     st[ST_T1] = T;
     st[ST_ABOVE1] = above;
     st[ST_NEED1] = ok ? need - above : 0u;
@@ -212,18 +217,18 @@ struct SlotGeom {
   int32_t nslots;  // slots of this unit
 };
 
-__device__ __forceinline__ SlotGeom slot_geom(int mode, int64_t unit, int64_t n, int64_t P, int64_t kb) {
+__device__ __forceinline__ SlotGeom slot_geom(int mode, uint32_t unit, const Blocks& B, int64_t kb) {
   SlotGeom g;
   if (mode == 0) {
-    const int64_t b = unit % P, w = unit / P;
-    const int64_t s = blk_start(b, n, P), e = blk_start(b + 1, n, P);
-    g.base = w * n + s;
+    const uint32_t b = unit % B.P, w = unit / B.P;
+    const uint32_t s = B.start(b), e = B.start(b + 1u);
+    g.base = (int64_t)w * B.n + s;
     g.len = e - s;
     g.ss = SLOT;
     g.nslots = (int32_t)((e - s + SLOT - 1) / SLOT);
   } else {
     g.nslots = (int32_t)((2 * kb + MERGE_TILE - 1) / MERGE_TILE);
-    g.base = unit * g.nslots * MERGE_TILE;   // whole slots per unit: float4-aligned, full last slot
+    g.base = (int64_t)unit * g.nslots * MERGE_TILE;   // whole slots per unit: float4-aligned, full last slot
     g.len = 2 * kb;
     g.ss = MERGE_TILE;
   }
@@ -232,111 +237,132 @@ __device__ __forceinline__ SlotGeom slot_geom(int mode, int64_t unit, int64_t n,
 
 // ============================================================================ a3: candidates
 // One workgroup per slot of SLOT elements: keeps the entries whose key lies
-// at or above the level-1 threshold bin, in index order -- element order is
-// (register j, thread, component c) -- and the keys of the entries inside the
-// threshold bin.  No atomics and no waiting on other workgroups.
+// at or above the level-1 threshold bin, in index order, and the keys of the
+// entries inside the threshold bin.  Thread t owns the SLOT/256 consecutive
+// elements starting at SLOT/256 * t, so index order is thread order: one
+// wave scan of the packed per-thread counts (candidates | bin entries << 16)
+// and one barrier give every thread its write offsets.  No atomics and no
+// waiting on other workgroups.
+// Candidates of a slot are staged in LDS and written out with coalesced
+// stores when they fit COLLECT_STAGE entries (the usual case: about 1 % of a
+// slot); a slot with more writes them directly.
+constexpr int COLLECT_STAGE = 1024;
+
+struct CollectSmem {
+  int32_t si[COLLECT_STAGE];
+  float sv[COLLECT_STAGE];
+  uint32_t sk[COLLECT_STAGE];
+  uint32_t wtot[4];
+};
+
+template <int VEC, bool FULL>
+__device__ __forceinline__ void collect_slot(const float* __restrict__ A, uint32_t nvalid, int32_t pos0,
+                                             const uint32_t* __restrict__ t1_word, CollectSmem& L,
+                                             uint32_t* cnt_out, uint32_t* nbin_out, int32_t* __restrict__ CI,
+                                             float* __restrict__ CV, uint32_t* __restrict__ BK) {
+  constexpr int PT = SLOT / 256;
+  const int lane = lane_id(), wv = wave_id();
+  const uint32_t my0 = threadIdx.x * PT;
+  float v[PT];
+  if (VEC == 4) {
+#pragma unroll
+    for (int q = 0; q < PT / 4; ++q) {
+      f4v x = {0.f, 0.f, 0.f, 0.f};
+      if (FULL || my0 + 4 * q < nvalid) x = *reinterpret_cast<const f4v*>(A + my0 + 4 * q);
+      v[4 * q + 0] = x.x;
+      v[4 * q + 1] = x.y;
+      v[4 * q + 2] = x.z;
+      v[4 * q + 3] = x.w;
+    }
+  } else {
+#pragma unroll
+    for (int i = 0; i < PT; ++i) v[i] = (FULL || my0 + i < nvalid) ? A[my0 + i] : 0.f;
+  }
+  // the threshold bin is read only now, so its latency overlaps the data loads
+  __builtin_amdgcn_sched_barrier(0);
+  const uint32_t T1 = *t1_word;
+  const uint32_t tlo = T1 << D1_SHIFT;
+  const uint32_t thi = tlo + (1u << D1_SHIFT);   // T1 < 4096, so this fits in 32 bits
+  uint32_t tc = 0, tb = 0;
+#pragma unroll
+  for (int i = 0; i < PT; ++i) {
+    const uint32_t key = mag_key(v[i]);
+    const bool c = (FULL || my0 + i < nvalid) && key >= tlo;
+    tc += c ? 1u : 0u;
+    tb += (c && key < thi) ? 1u : 0u;
+  }
+  const uint32_t packed = tc | (tb << 16);   // a slot holds at most SLOT < 2^16 of each
+  const uint32_t incl = wave_incl_scan(packed);
+  if (lane == WAVE - 1) L.wtot[wv] = incl;
+  __syncthreads();
+  uint32_t base = 0, tot = 0;
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    const uint32_t x = L.wtot[k];
+    base += k < wv ? x : 0u;
+    tot += x;
+  }
+  const uint32_t ncand = tot & 0xFFFFu, nbin = tot >> 16;
+  if (threadIdx.x == 255) {
+    *cnt_out = ncand;
+    *nbin_out = nbin;
+  }
+  const uint32_t ex = base + incl - packed;
+  uint32_t pc = ex & 0xFFFFu, pb = ex >> 16;
+  const bool staged = ncand <= (uint32_t)COLLECT_STAGE;   // uniform
+  int32_t* __restrict__ oI = staged ? L.si : CI;
+  float* __restrict__ oV = staged ? L.sv : CV;
+  uint32_t* __restrict__ oK = staged ? L.sk : BK;
+  if (tc != 0u) {
+#pragma unroll
+    for (int i = 0; i < PT; ++i) {
+      const uint32_t key = mag_key(v[i]);
+      if ((FULL || my0 + i < nvalid) && key >= tlo) {
+        oI[pc] = pos0 + (int32_t)(my0 + i);
+        oV[pc] = v[i];
+        ++pc;
+        if (key < thi) {
+          oK[pb] = key;
+          ++pb;
+        }
+      }
+    }
+  }
+  if (staged) {
+    __syncthreads();
+    for (uint32_t j = threadIdx.x; j < ncand; j += 256) {
+      CI[j] = L.si[j];
+      CV[j] = L.sv[j];
+    }
+    for (uint32_t j = threadIdx.x; j < nbin; j += 256) BK[j] = L.sk[j];
+  }
+}
+
 template <int VEC>
-__global__ __launch_bounds__(256) void k_collect(const float* __restrict__ acc, int64_t ld_acc,
-                                                 int64_t n, int32_t P, int32_t smax,
-                                                 const uint32_t* __restrict__ state,
+__global__ __launch_bounds__(256) void k_collect(const float* __restrict__ acc, int64_t ld_acc, Blocks B,
+                                                 uint32_t smax, const uint32_t* __restrict__ state,
                                                  uint32_t* __restrict__ slot_cnt, uint32_t* __restrict__ slot_nbin,
                                                  int32_t* __restrict__ cand_idx, float* __restrict__ cand_val,
                                                  uint32_t* __restrict__ bin_key) {
-  constexpr int NJ = VEC == 4 ? SLOT / 1024 : SLOT / 256;   // register rows per thread
-  constexpr int NC = VEC;                                   // components per row
-  constexpr int NW = 4;
-  __shared__ uint32_t cc[NJ * NW], cb[NJ * NW];
-  __shared__ uint32_t tot[2];
-  const int64_t unit = blockIdx.x / smax;
-  const int32_t slot = (int32_t)(blockIdx.x % smax);
-  const int64_t b = unit % P, w = unit / P;
-  const int64_t s = blk_start(b, n, P), e = blk_start(b + 1, n, P);
-  const int64_t t0 = s + (int64_t)slot * SLOT;
+  __shared__ CollectSmem L;
+  const uint32_t unit = blockIdx.x / smax;
+  const uint32_t slot = blockIdx.x % smax;
+  const uint32_t b = unit % B.P, w = unit / B.P;
+  const uint32_t s = B.start(b), e = B.start(b + 1u);
+  const uint32_t t0 = s + slot * (uint32_t)SLOT;
   if (t0 >= e) return;
-  const uint32_t T1 = state[unit * ST_WORDS + ST_T1];
-  const uint32_t tlo = T1 << D1_SHIFT;
-  const int lane = lane_id(), wv = wave_id();
-  const float* __restrict__ A = acc + w * ld_acc;
-  const uint64_t lt = __lanemask_lt();
-
-  float v[NJ * NC];
-  auto pos_of = [&](int j, int c) -> int64_t {
-    return VEC == 4 ? t0 + ((int64_t)j * 256 + threadIdx.x) * 4 + c : t0 + (int64_t)j * 256 + threadIdx.x;
-  };
-#pragma unroll
-  for (int j = 0; j < NJ; ++j) {
-    if (VEC == 4) {
-      f4v q = {0.f, 0.f, 0.f, 0.f};
-      if (pos_of(j, 0) < e) q = *reinterpret_cast<const f4v*>(A + pos_of(j, 0));
-      v[4 * j + 0] = q.x;
-      v[4 * j + 1] = q.y;
-      v[4 * j + 2] = q.z;
-      v[4 * j + 3] = q.w;
-    } else {
-      v[j] = pos_of(j, 0) < e ? A[pos_of(j, 0)] : 0.f;
-    }
-  }
-#pragma unroll
-  for (int j = 0; j < NJ; ++j) {
-    uint32_t nc = 0, nb = 0;
-#pragma unroll
-    for (int c = 0; c < NC; ++c) {
-      const uint32_t key = mag_key(v[j * NC + c]);
-      const bool valid = pos_of(j, c) < e;
-      nc += popc64(__ballot(valid && key >= tlo));
-      nb += popc64(__ballot(valid && (key >> D1_SHIFT) == T1));
-    }
-    if (lane == 0) {
-      cc[j * NW + wv] = nc;
-      cb[j * NW + wv] = nb;
-    }
-  }
-  __syncthreads();
-  if (wv == 0) {   // exclusive scans over (j, wave) in j-major order
-    const uint32_t x = lane < NJ * NW ? cc[lane] : 0u, y = lane < NJ * NW ? cb[lane] : 0u;
-    const uint32_t xi = wave_incl_scan(x), yi = wave_incl_scan(y);
-    if (lane < NJ * NW) {
-      cc[lane] = xi - x;
-      cb[lane] = yi - y;
-    }
-    if (lane == WAVE - 1) {
-      tot[0] = xi;
-      tot[1] = yi;
-    }
-  }
-  __syncthreads();
-  const int64_t si = unit * smax + slot;
-  if (threadIdx.x == 0) {
-    slot_cnt[si] = tot[0];
-    slot_nbin[si] = tot[1];
-  }
-  const int64_t cbase = w * n + t0;
-#pragma unroll
-  for (int j = 0; j < NJ; ++j) {
-    bool pc_[NC], pb_[NC];
-    uint32_t pc = cc[j * NW + wv], pb = cb[j * NW + wv];
-#pragma unroll
-    for (int c = 0; c < NC; ++c) {
-      const uint32_t key = mag_key(v[j * NC + c]);
-      const bool valid = pos_of(j, c) < e;
-      pc_[c] = valid && key >= tlo;
-      pb_[c] = valid && (key >> D1_SHIFT) == T1;
-      pc += popc64(__ballot(pc_[c]) & lt);
-      pb += popc64(__ballot(pb_[c]) & lt);
-    }
-#pragma unroll
-    for (int c = 0; c < NC; ++c) {
-      if (pc_[c]) {
-        cand_idx[cbase + pc] = (int32_t)pos_of(j, c);
-        cand_val[cbase + pc] = v[j * NC + c];
-        ++pc;
-      }
-      if (pb_[c]) {
-        bin_key[cbase + pb] = mag_key(v[j * NC + c]);
-        ++pb;
-      }
-    }
-  }
+  const uint32_t rem = e - t0;   // entries of this slot inside the block, clamped in 32 bits
+  const uint32_t nvalid = rem < (uint32_t)SLOT ? rem : (uint32_t)SLOT;
+  const float* __restrict__ A = acc + (int64_t)w * ld_acc + t0;
+  const int64_t cbase = (int64_t)w * B.n + t0;
+  const int64_t si = (int64_t)unit * smax + slot;
+  const uint32_t* t1_word = state + (int64_t)unit * ST_WORDS + ST_T1;
+  if (nvalid == (uint32_t)SLOT)
+    collect_slot<VEC, true>(A, nvalid, (int32_t)t0, t1_word, L, slot_cnt + si, slot_nbin + si,
+                            cand_idx + cbase, cand_val + cbase, bin_key + cbase);
+  else
+    collect_slot<VEC, false>(A, nvalid, (int32_t)t0, t1_word, L, slot_cnt + si, slot_nbin + si,
+                             cand_idx + cbase, cand_val + cbase, bin_key + cbase);
 }
 
 // ============================================================================ exact threshold
@@ -823,7 +849,7 @@ __device__ __forceinline__ void thresh_fast_topk(FastSmem& L, int64_t unit, cons
 }
 
 template <int mode>
-__global__ __launch_bounds__(1024) void k_thresh(int64_t n, int32_t P, int32_t kb, int32_t smax,
+__global__ __launch_bounds__(1024) void k_thresh(Blocks B, int32_t kb, int32_t smax,
                                                  int lps, uint32_t* __restrict__ hist1,
                                                  const float* __restrict__ U_val, uint32_t* __restrict__ state,
                                                  const uint32_t* __restrict__ slot_cnt,
@@ -837,7 +863,7 @@ __global__ __launch_bounds__(1024) void k_thresh(int64_t n, int32_t P, int32_t k
   constexpr int NT = 1024;
   const int64_t unit = blockIdx.x;
   uint32_t* st = state + unit * ST_WORDS;
-  const SlotGeom g = slot_geom(mode, unit, n, P, kb);
+  const SlotGeom g = slot_geom(mode, (uint32_t)unit, B, kb);
   const uint32_t* __restrict__ cnt = slot_cnt + unit * smax;
   const uint32_t* __restrict__ nbn = slot_nbin + unit * smax;
   const uint32_t* __restrict__ K = bin_key + g.base;
@@ -1064,7 +1090,7 @@ __global__ __launch_bounds__(1024) void k_thresh(int64_t n, int32_t P, int32_t k
 // selected -> sp[w][b] in place, the rest -> the step's drop lists.
 template <int MODE>
 __global__ __launch_bounds__(256) void k_emit(
-    const int32_t* __restrict__ cand_idx, const float* __restrict__ cand_val, int64_t n, int32_t P,
+    const int32_t* __restrict__ cand_idx, const float* __restrict__ cand_val, Blocks B,
     int32_t kb, int32_t m, int32_t smax, int32_t G, int32_t gmax, const uint32_t* __restrict__ state,
     const uint32_t* __restrict__ slot_cnt, const uint32_t* __restrict__ pre_all,
     const uint32_t* __restrict__ pre_ge, const uint32_t* __restrict__ pre_eq, int32_t* __restrict__ out_idx,
@@ -1074,13 +1100,13 @@ __global__ __launch_bounds__(256) void k_emit(
   __shared__ uint32_t pre[EMIT_GROUP_TK + 1];
   __shared__ uint32_t cge[NJ * NWV], ceq[NJ * NWV];
   __shared__ uint32_t sh[2];
-  const int64_t unit = blockIdx.x / gmax;
-  const int32_t grp = (int32_t)(blockIdx.x % gmax);
-  const SlotGeom g = slot_geom(MODE, unit, n, P, kb);
+  const uint32_t unit = blockIdx.x / (uint32_t)gmax;
+  const int32_t grp = (int32_t)(blockIdx.x % (uint32_t)gmax);
+  const SlotGeom g = slot_geom(MODE, unit, B, kb);
   const int32_t s_lo = grp * G;
   if (s_lo >= g.nslots) return;
   const int32_t ns = min(G, g.nslots - s_lo);
-  const uint32_t* __restrict__ cnt = slot_cnt + unit * smax;
+  const uint32_t* __restrict__ cnt = slot_cnt + (int64_t)unit * smax;
   const int lane = lane_id(), wv = wave_id();
   if (wv == 0) {   // exclusive prefix of the group's slot counts
     const uint32_t c = lane < ns ? min(cnt[s_lo + lane], (uint32_t)g.ss) : 0u;
@@ -1090,9 +1116,9 @@ __global__ __launch_bounds__(256) void k_emit(
   __syncthreads();
   const uint32_t E = pre[ns];
   if (E == 0) return;
-  const uint32_t* st = state + unit * ST_WORDS;
+  const uint32_t* st = state + (int64_t)unit * ST_WORDS;
   const uint32_t tge = st[ST_TGE], teq = st[ST_TEQ], need_eq = st[ST_NEEDEQ];
-  const int64_t si = unit * smax + s_lo;
+  const int64_t si = (int64_t)unit * smax + s_lo;
   const uint32_t all_before = pre_all[si];
   uint32_t run_g = pre_ge[si], run_e = pre_eq[si];
   auto addr = [&](uint32_t p) -> int64_t {   // entry p of the group (index order) -> address
@@ -1104,10 +1130,10 @@ __global__ __launch_bounds__(256) void k_emit(
   };
   int64_t o;
   if (MODE == 0) {
-    o = unit * kb;
+    o = (int64_t)unit * kb;
   } else {
-    const int64_t w = unit / m, t = unit % m, b = (w + t) % P;
-    o = (w * P + b) * kb;
+    const uint32_t w = unit / (uint32_t)m, t = unit % (uint32_t)m, b = (w + t) % B.P;
+    o = ((int64_t)w * B.P + b) * kb;
   }
   const uint64_t lt = __lanemask_lt();
   for (uint32_t c0 = 0; c0 < E; c0 += EMIT_CHUNK) {
@@ -1169,8 +1195,8 @@ __global__ __launch_bounds__(256) void k_emit(
         } else if (MODE == 1) {
           const uint32_t dpos = all_before + p - sel_before;
           if (dpos < (uint32_t)kb) {
-            drop_idx[unit * kb + dpos] = ix[j];
-            drop_val[unit * kb + dpos] = vx[j];
+            drop_idx[(int64_t)unit * kb + dpos] = ix[j];
+            drop_val[(int64_t)unit * kb + dpos] = vx[j];
           } else {
             atomicOr(err, ERR_COUNT_DROP);
           }
@@ -1197,17 +1223,18 @@ __global__ __launch_bounds__(MERGE_THREADS) void k_merge(
   // held entries a0-1 .. a1 at [0, nh + 2), received b0 .. b1 at [nh + 2, nh + nr + 3)
   __shared__ int32_t cI[MERGE_TILE + 3];
   __shared__ float cV[MERGE_TILE + 3];
-  __shared__ uint32_t hist[NB1];
+  __shared__ __align__(16) uint32_t hist[NB1];
   __shared__ uint32_t scratch[16];
-  const int64_t pair = blockIdx.x / tiles_per_pair;
-  const int32_t tile = (int32_t)(blockIdx.x % tiles_per_pair);
-  const int64_t w = pair / m, t = pair % m, b = (w + t) % P, src = (w - d + P) % P;
-  const int32_t* __restrict__ Hi = sp_idx + (w * P + b) * kb;
-  const float* __restrict__ Hv = sp_val + (w * P + b) * kb;
-  const int32_t* __restrict__ Ri = sp_idx + (src * P + b) * kb;
-  const float* __restrict__ Rv = sp_val + (src * P + b) * kb;
+  const uint32_t pair = blockIdx.x / (uint32_t)tiles_per_pair;
+  const int32_t tile = (int32_t)(blockIdx.x % (uint32_t)tiles_per_pair);
+  const uint32_t uP = (uint32_t)P;
+  const uint32_t w = pair / (uint32_t)m, t = pair % (uint32_t)m, b = (w + t) % uP, src = (w + uP - (uint32_t)d) % uP;
+  const int32_t* __restrict__ Hi = sp_idx + ((int64_t)w * P + b) * kb;
+  const float* __restrict__ Hv = sp_val + ((int64_t)w * P + b) * kb;
+  const int32_t* __restrict__ Ri = sp_idx + ((int64_t)src * P + b) * kb;
+  const float* __restrict__ Rv = sp_val + ((int64_t)src * P + b) * kb;
   const int32_t L2 = 2 * kb;
-  for (int i = threadIdx.x; i < NB1; i += blockDim.x) hist[i] = 0u;
+  for (int i = threadIdx.x; i < NB1 / 4; i += blockDim.x) reinterpret_cast<uint4*>(hist)[i] = make_uint4(0u, 0u, 0u, 0u);
   const int32_t Q0 = tile * MERGE_TILE;
   const int32_t Q1 = min(Q0 + MERGE_TILE, L2);
   // split(q) = number of held entries among the first q merged positions:
@@ -1305,8 +1332,8 @@ __global__ __launch_bounds__(MERGE_THREADS) void k_merge(
   }
   uint32_t tot;
   uint32_t pos = block_excl_scan(cnt, scratch, &tot);
-  if (threadIdx.x == 0) slot_cnt[pair * tiles_per_pair + tile] = tot;
-  const int64_t ubase = pair * (int64_t)tiles_per_pair * MERGE_TILE + Q0;
+  if (threadIdx.x == 0) slot_cnt[(int64_t)pair * tiles_per_pair + tile] = tot;
+  const int64_t ubase = (int64_t)pair * tiles_per_pair * MERGE_TILE + Q0;
 #pragma unroll
   for (int k = 0; k < MERGE_PER_THREAD; ++k) {
     if (eok[k]) {
@@ -1316,11 +1343,7 @@ __global__ __launch_bounds__(MERGE_THREADS) void k_merge(
     }
   }
   __syncthreads();
-  uint32_t* __restrict__ H = hist1 + pair * NB1;
-  for (int i = threadIdx.x; i < NB1; i += blockDim.x) {
-    const uint32_t c = hist[i];
-    if (c) atomicAdd(&H[i], c);
-  }
+  flush_hist(hist, hist1 + (int64_t)pair * NB1);
 }
 
 // ============================================================================ a5: all-gather + densify
@@ -1329,17 +1352,18 @@ __global__ __launch_bounds__(MERGE_THREADS) void k_merge(
 // the index-sorted final blocks sp[b][b]), then streamed out.
 template <int VEC>
 __global__ __launch_bounds__(256) void k_densify(const int32_t* __restrict__ sp_idx,
-                                                 const float* __restrict__ sp_val, int32_t P, int64_t n,
+                                                 const float* __restrict__ sp_val, Blocks B,
                                                  int32_t kb, float* __restrict__ dense) {
   __shared__ float tileb[DENSE_TILE];
   __shared__ uint32_t cnt[8];
+  const int64_t n = B.n;
   const int64_t t0 = (int64_t)blockIdx.x * DENSE_TILE;
   const int64_t t1 = min(t0 + DENSE_TILE, n);
   for (int i = threadIdx.x; i < DENSE_TILE; i += blockDim.x) tileb[i] = 0.f;
-  const int64_t blo = block_of(t0, n, P), bhi = block_of(t1 - 1, n, P);
-  for (int64_t b = blo; b <= bhi; ++b) {
-    const int32_t* Fi = sp_idx + (b * P + b) * kb;
-    const float* Fv = sp_val + (b * P + b) * kb;
+  const uint32_t blo = B.of((uint32_t)t0), bhi = B.of((uint32_t)(t1 - 1));
+  for (uint32_t b = blo; b <= bhi; ++b) {
+    const int32_t* Fi = sp_idx + ((int64_t)b * B.P + b) * kb;
+    const float* Fv = sp_val + ((int64_t)b * B.P + b) * kb;
     const int32_t jlo = wg_lower_bound(Fi, kb, t0, cnt);
     const int32_t jhi = wg_lower_bound(Fi, kb, t1, cnt);
     for (int32_t j = jlo + (int32_t)threadIdx.x; j < jhi; j += blockDim.x) {
@@ -1367,17 +1391,18 @@ __global__ __launch_bounds__(256) void k_densify(const int32_t* __restrict__ sp_
 // ============================================================================ a6: residual collection
 // Membership bitmap of the final index set I, one 32-bit word per 32 indices,
 // built tile by tile without atomics on global memory.
-__global__ __launch_bounds__(256) void k_bitmap(const int32_t* __restrict__ sp_idx, int32_t P, int64_t n,
+__global__ __launch_bounds__(256) void k_bitmap(const int32_t* __restrict__ sp_idx, Blocks B,
                                                 int32_t kb, uint32_t* __restrict__ bm) {
   constexpr int WORDS = DENSE_TILE / 32;
   __shared__ uint32_t words[WORDS];
   __shared__ uint32_t cnt[8];
+  const int64_t n = B.n;
   const int64_t t0 = (int64_t)blockIdx.x * DENSE_TILE;
   const int64_t t1 = min(t0 + DENSE_TILE, n);
   for (int i = threadIdx.x; i < WORDS; i += blockDim.x) words[i] = 0u;
-  const int64_t blo = block_of(t0, n, P), bhi = block_of(t1 - 1, n, P);
-  for (int64_t b = blo; b <= bhi; ++b) {
-    const int32_t* Fi = sp_idx + (b * P + b) * kb;
+  const uint32_t blo = B.of((uint32_t)t0), bhi = B.of((uint32_t)(t1 - 1));
+  for (uint32_t b = blo; b <= bhi; ++b) {
+    const int32_t* Fi = sp_idx + ((int64_t)b * B.P + b) * kb;
     const int32_t jlo = wg_lower_bound(Fi, kb, t0, cnt);
     const int32_t jhi = wg_lower_bound(Fi, kb, t1, cnt);
     for (int32_t j = jlo + (int32_t)threadIdx.x; j < jhi; j += blockDim.x) {
@@ -1398,35 +1423,39 @@ __device__ __forceinline__ bool in_final(const uint32_t* __restrict__ bm, int32_
 }
 
 // acc[w][x] = 0 where worker w selected x locally and x is a final index.
-__global__ __launch_bounds__(256) void k_grc_zero(float* __restrict__ acc, int64_t ld_acc, int32_t P,
-                                                  int64_t n, int32_t kb, const int32_t* __restrict__ local_idx,
+// Grid: x over the worker's P k_blk local indices, y over workers.
+__global__ __launch_bounds__(256) void k_grc_zero(float* __restrict__ acc, int64_t ld_acc, uint32_t P, uint32_t n,
+                                                  uint32_t kb, const int32_t* __restrict__ local_idx,
                                                   const uint32_t* __restrict__ bm) {
-  const int64_t total = (int64_t)P * P * kb;
-  const int64_t per_w = (int64_t)P * kb;
-  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < total;
-       i += (int64_t)gridDim.x * blockDim.x) {
-    const int32_t x = local_idx[i];
-    if (x >= 0 && x < n && in_final(bm, x)) acc[(i / per_w) * ld_acc + x] = 0.0f;
+  const uint32_t per_w = P * kb;   // <= n < 2^31
+  for (uint32_t w = blockIdx.y; w < P; w += gridDim.y) {
+    const int32_t* __restrict__ L = local_idx + (int64_t)w * per_w;
+    float* __restrict__ A = acc + (int64_t)w * ld_acc;
+    for (uint32_t i = blockIdx.x * 256u + threadIdx.x; i < per_w; i += gridDim.x * 256u) {
+      const int32_t x = L[i];
+      if (x >= 0 && (uint32_t)x < n && in_final(bm, x)) A[x] = 0.0f;
+    }
   }
 }
 
 // acc[w][x] += v for the drops (x, v) of one step with x a final index.
-// Within one step a worker drops a given index at most once.
-__global__ __launch_bounds__(256) void k_grc_drops(float* __restrict__ acc, int64_t ld_acc, int64_t n, int32_t m,
-                                                   int32_t kb, int32_t npairs,
+// Within one step a worker drops a given index at most once.  Grid: x over a
+// pair's drop list, y over pairs (w, t); pair p belongs to worker p / m.
+__global__ __launch_bounds__(256) void k_grc_drops(float* __restrict__ acc, int64_t ld_acc, uint32_t n, uint32_t m,
+                                                   uint32_t kb, uint32_t npairs,
                                                    const int32_t* __restrict__ drop_idx,
                                                    const float* __restrict__ drop_val,
                                                    const int32_t* __restrict__ drop_cnt,
                                                    const uint32_t* __restrict__ bm) {
-  const int64_t total = (int64_t)npairs * kb;
-  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < total;
-       i += (int64_t)gridDim.x * blockDim.x) {
-    const int64_t pair = i / kb, j = i % kb;
-    if (j >= drop_cnt[pair]) continue;
-    const int32_t x = drop_idx[i];
-    if (x >= 0 && x < n && in_final(bm, x)) {
-      float* p = acc + (pair / m) * ld_acc + x;
-      *p = *p + drop_val[i];
+  for (uint32_t pair = blockIdx.y; pair < npairs; pair += gridDim.y) {
+    const int32_t c = drop_cnt[pair];
+    const uint32_t cnt = c < 0 ? 0u : min((uint32_t)c, kb);
+    const int32_t* __restrict__ Di = drop_idx + (int64_t)pair * kb;
+    const float* __restrict__ Dv = drop_val + (int64_t)pair * kb;
+    float* __restrict__ A = acc + (int64_t)(pair / m) * ld_acc;
+    for (uint32_t j = blockIdx.x * 256u + threadIdx.x; j < cnt; j += gridDim.x * 256u) {
+      const int32_t x = Di[j];
+      if (x >= 0 && (uint32_t)x < n && in_final(bm, x)) A[x] = A[x] + Dv[j];
     }
   }
 }
@@ -1453,12 +1482,14 @@ hipError_t launch_residual_add(float* acc, int64_t ld_acc, const float* grad, in
   const int64_t maxlen = (n + PP - 1) / PP;
   const int32_t G = (int32_t)((maxlen + ADD_TILE - 1) / ADD_TILE);
   const dim3 grid((unsigned)((int64_t)nworkers * PP * G));
+  const Blocks B = make_blocks(n, PP);
+  const uint32_t uG = (uint32_t)G;
   if (hist1) {
-    if (vec4) hipLaunchKernelGGL((k_residual_add<4, true>), grid, dim3(256), 0, s, acc, ld_acc, grad, ld_grad, n, PP, G, hist1);
-    else hipLaunchKernelGGL((k_residual_add<1, true>), grid, dim3(256), 0, s, acc, ld_acc, grad, ld_grad, n, PP, G, hist1);
+    if (vec4) hipLaunchKernelGGL((k_residual_add<4, true>), grid, dim3(256), 0, s, acc, ld_acc, grad, ld_grad, B, uG, hist1);
+    else hipLaunchKernelGGL((k_residual_add<1, true>), grid, dim3(256), 0, s, acc, ld_acc, grad, ld_grad, B, uG, hist1);
   } else {
-    if (vec4) hipLaunchKernelGGL((k_residual_add<4, false>), grid, dim3(256), 0, s, acc, ld_acc, grad, ld_grad, n, PP, G, hist1);
-    else hipLaunchKernelGGL((k_residual_add<1, false>), grid, dim3(256), 0, s, acc, ld_acc, grad, ld_grad, n, PP, G, hist1);
+    if (vec4) hipLaunchKernelGGL((k_residual_add<4, false>), grid, dim3(256), 0, s, acc, ld_acc, grad, ld_grad, B, uG, hist1);
+    else hipLaunchKernelGGL((k_residual_add<1, false>), grid, dim3(256), 0, s, acc, ld_acc, grad, ld_grad, B, uG, hist1);
   }
   return hipGetLastError();
 }
@@ -1468,14 +1499,15 @@ hipError_t launch_hist1(const float* acc, int64_t ld_acc, int32_t nworkers, int6
   const int64_t maxlen = (n + P - 1) / P;
   const int32_t G = (int32_t)((maxlen + ADD_TILE - 1) / ADD_TILE);
   const dim3 grid((unsigned)((int64_t)nworkers * P * G));
-  if (vec4) hipLaunchKernelGGL(k_hist1<4>, grid, dim3(256), 0, s, acc, ld_acc, n, P, G, hist1);
-  else hipLaunchKernelGGL(k_hist1<1>, grid, dim3(256), 0, s, acc, ld_acc, n, P, G, hist1);
+  const Blocks B = make_blocks(n, P);
+  if (vec4) hipLaunchKernelGGL(k_hist1<4>, grid, dim3(256), 0, s, acc, ld_acc, B, (uint32_t)G, hist1);
+  else hipLaunchKernelGGL(k_hist1<1>, grid, dim3(256), 0, s, acc, ld_acc, B, (uint32_t)G, hist1);
   return hipGetLastError();
 }
 
 hipError_t launch_select1(uint32_t* hist1, uint32_t* state, int64_t nunits, int64_t n, int32_t P, uint32_t need,
                           uint32_t* err, hipStream_t s) {
-  hipLaunchKernelGGL(k_select1, dim3((unsigned)nunits), dim3(1024), 0, s, hist1, state, n, P, need, err);
+  hipLaunchKernelGGL(k_select1, dim3((unsigned)nunits), dim3(1024), 0, s, hist1, state, make_blocks(n, P), need, err);
   return hipGetLastError();
 }
 
@@ -1484,8 +1516,9 @@ hipError_t launch_collect(const float* acc, int64_t ld_acc, int32_t nworkers, in
                           uint32_t* slot_nbin, int32_t* cand_idx, float* cand_val, uint32_t* bin_key,
                           hipStream_t s) {
   const dim3 grid((unsigned)((int64_t)nworkers * P * smax));
-  if (vec4) hipLaunchKernelGGL(k_collect<4>, grid, dim3(256), 0, s, acc, ld_acc, n, P, smax, state, slot_cnt, slot_nbin, cand_idx, cand_val, bin_key);
-  else hipLaunchKernelGGL(k_collect<1>, grid, dim3(256), 0, s, acc, ld_acc, n, P, smax, state, slot_cnt, slot_nbin, cand_idx, cand_val, bin_key);
+  const Blocks B = make_blocks(n, P);
+  if (vec4) hipLaunchKernelGGL(k_collect<4>, grid, dim3(256), 0, s, acc, ld_acc, B, (uint32_t)smax, state, slot_cnt, slot_nbin, cand_idx, cand_val, bin_key);
+  else hipLaunchKernelGGL(k_collect<1>, grid, dim3(256), 0, s, acc, ld_acc, B, (uint32_t)smax, state, slot_cnt, slot_nbin, cand_idx, cand_val, bin_key);
   return hipGetLastError();
 }
 
@@ -1494,10 +1527,10 @@ hipError_t launch_thresh(int mode, int64_t nunits, int64_t n, int32_t P, int32_t
                          const uint32_t* slot_nbin, const uint32_t* bin_key, uint32_t* pre_all, uint32_t* pre_ge,
                          uint32_t* pre_eq, int32_t* drop_cnt, uint32_t* err, hipStream_t s) {
   if (mode == 0)
-    hipLaunchKernelGGL(k_thresh<0>, dim3((unsigned)nunits), dim3(1024), 0, s, n, P, kb, smax, lps, hist1, U_val,
+    hipLaunchKernelGGL(k_thresh<0>, dim3((unsigned)nunits), dim3(1024), 0, s, make_blocks(n, P), kb, smax, lps, hist1, U_val,
                        state, slot_cnt, slot_nbin, bin_key, pre_all, pre_ge, pre_eq, drop_cnt, err);
   else
-    hipLaunchKernelGGL(k_thresh<1>, dim3((unsigned)nunits), dim3(1024), 0, s, n, P, kb, smax, lps, hist1, U_val,
+    hipLaunchKernelGGL(k_thresh<1>, dim3((unsigned)nunits), dim3(1024), 0, s, make_blocks(n, P), kb, smax, lps, hist1, U_val,
                        state, slot_cnt, slot_nbin, bin_key, pre_all, pre_ge, pre_eq, drop_cnt, err);
   return hipGetLastError();
 }
@@ -1509,9 +1542,9 @@ hipError_t launch_emit(int mode, const int32_t* cand_idx, const float* cand_val,
                        int32_t* local_idx, int32_t* drop_idx, float* drop_val, uint32_t* err, hipStream_t s) {
   const dim3 grid((unsigned)(nunits * gmax));
   if (mode == 0)
-    hipLaunchKernelGGL(k_emit<0>, grid, dim3(256), 0, s, cand_idx, cand_val, n, P, kb, m, smax, G, gmax, state, slot_cnt, pre_all, pre_ge, pre_eq, out_idx, out_val, local_idx, drop_idx, drop_val, err);
+    hipLaunchKernelGGL(k_emit<0>, grid, dim3(256), 0, s, cand_idx, cand_val, make_blocks(n, P), kb, m, smax, G, gmax, state, slot_cnt, pre_all, pre_ge, pre_eq, out_idx, out_val, local_idx, drop_idx, drop_val, err);
   else
-    hipLaunchKernelGGL(k_emit<1>, grid, dim3(256), 0, s, cand_idx, cand_val, n, P, kb, m, smax, G, gmax, state, slot_cnt, pre_all, pre_ge, pre_eq, out_idx, out_val, local_idx, drop_idx, drop_val, err);
+    hipLaunchKernelGGL(k_emit<1>, grid, dim3(256), 0, s, cand_idx, cand_val, make_blocks(n, P), kb, m, smax, G, gmax, state, slot_cnt, pre_all, pre_ge, pre_eq, out_idx, out_val, local_idx, drop_idx, drop_val, err);
   return hipGetLastError();
 }
 
@@ -1526,28 +1559,31 @@ hipError_t launch_merge(const int32_t* sp_idx, const float* sp_val, int32_t P, i
 hipError_t launch_densify(const int32_t* sp_idx, const float* sp_val, int32_t P, int64_t n, int32_t kb,
                           float* dense, bool vec4, hipStream_t s) {
   const dim3 grid((unsigned)((n + DENSE_TILE - 1) / DENSE_TILE));
-  if (vec4) hipLaunchKernelGGL(k_densify<4>, grid, dim3(256), 0, s, sp_idx, sp_val, P, n, kb, dense);
-  else hipLaunchKernelGGL(k_densify<1>, grid, dim3(256), 0, s, sp_idx, sp_val, P, n, kb, dense);
+  const Blocks B = make_blocks(n, P);
+  if (vec4) hipLaunchKernelGGL(k_densify<4>, grid, dim3(256), 0, s, sp_idx, sp_val, B, kb, dense);
+  else hipLaunchKernelGGL(k_densify<1>, grid, dim3(256), 0, s, sp_idx, sp_val, B, kb, dense);
   return hipGetLastError();
 }
 
 hipError_t launch_bitmap(const int32_t* sp_idx, int32_t P, int64_t n, int32_t kb, uint32_t* bm,
                          hipStream_t s) {
   const dim3 grid((unsigned)((n + DENSE_TILE - 1) / DENSE_TILE));
-  hipLaunchKernelGGL(k_bitmap, grid, dim3(256), 0, s, sp_idx, P, n, kb, bm);
+  hipLaunchKernelGGL(k_bitmap, grid, dim3(256), 0, s, sp_idx, make_blocks(n, P), kb, bm);
   return hipGetLastError();
 }
 
 hipError_t launch_grc_zero(float* acc, int64_t ld_acc, int32_t P, int64_t n, int32_t kb, const int32_t* local_idx,
                            const uint32_t* bm, hipStream_t s) {
-  hipLaunchKernelGGL(k_grc_zero, dim3(grid_for((int64_t)P * P * kb, 256, 8192)), dim3(256), 0, s, acc, ld_acc, P, n, kb, local_idx, bm);
+  const dim3 grid(grid_for((int64_t)P * kb, 256, 1024), (unsigned)std::min<int32_t>(P, 65535));
+  hipLaunchKernelGGL(k_grc_zero, grid, dim3(256), 0, s, acc, ld_acc, (uint32_t)P, (uint32_t)n, (uint32_t)kb, local_idx, bm);
   return hipGetLastError();
 }
 
 hipError_t launch_grc_drops(float* acc, int64_t ld_acc, int64_t n, int32_t m, int32_t kb, int32_t npairs,
                             const int32_t* drop_idx, const float* drop_val, const int32_t* drop_cnt,
                             const uint32_t* bm, hipStream_t s) {
-  hipLaunchKernelGGL(k_grc_drops, dim3(grid_for((int64_t)npairs * kb, 256, 8192)), dim3(256), 0, s, acc, ld_acc, n, m, kb, npairs, drop_idx, drop_val, drop_cnt, bm);
+  const dim3 grid(grid_for(kb, 256, 1024), (unsigned)std::min<int32_t>(npairs, 65535));
+  hipLaunchKernelGGL(k_grc_drops, grid, dim3(256), 0, s, acc, ld_acc, (uint32_t)n, (uint32_t)m, (uint32_t)kb, (uint32_t)npairs, drop_idx, drop_val, drop_cnt, bm);
   return hipGetLastError();
 }
 
