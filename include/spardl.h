@@ -66,9 +66,10 @@ enum {
 #define SPARDL_WS_ERR_LOOKBACK 1u  /* reserved (no kernel waits on another workgroup) */
 #define SPARDL_WS_ERR_COUNT 2u     /* a selection's counts are inconsistent */
 
-/* Flag for spardl_block_topk: the level-1 |v| histograms of acc are already in
- * ws, written by the immediately preceding spardl_residual_add call with the
- * same acc, ld_acc, nworkers, n, P and ws (fused pass; saves one read of acc). */
+/* Flag for spardl_block_topk: the level-1 |v| histograms (and speculative
+ * candidates) of acc are already in ws, written by the immediately preceding
+ * spardl_residual_add call with the same acc, ld_acc, nworkers, n, P, k_blk,
+ * ws and ws_bytes (fused pass; saves one or two reads of acc). */
 #define SPARDL_TOPK_HIST_READY 1
 
 /* Static text for a status code. */
@@ -103,15 +104,19 @@ int spardl_workspace_init(int32_t nworkers, int32_t P, int64_t n, int32_t k_blk,
  *   acc[w*ld_acc + x] = acc[w*ld_acc + x] + grad[w*ld_grad + x]
  * for w < nworkers, x < n, in place.  acc then holds A = G + xi, which also
  * serves as the copy that Algorithm 1 keeps for residual collection.
- * If P > 0 and ws != NULL, the same pass also records, for each of the P
- * blocks of each row, the level-1 |v| histogram that spardl_block_topk needs
- * (pass it SPARDL_TOPK_HIST_READY; that call consumes and clears it, so call
- * it before the next residual add with this ws).  P = 0 (ws ignored) is a
- * plain add.
+ * If P > 0 and ws != NULL, the same pass also prepares the block top-k that
+ * must follow with the same acc, nworkers, n, P, k_blk, ws and ws_bytes and
+ * SPARDL_TOPK_HIST_READY: it records each block's level-1 |v| histogram
+ * (that call consumes and clears it) and, from a block's second step on, the
+ * entries at or above a floor just below the block's previous threshold, so
+ * that the top-k need not read acc again when the floor held.  P = 0 (k_blk
+ * and ws ignored) is a plain add.
  * Errors: EINVAL for NULL acc/grad, nworkers < 1, n < 1 or n >= 2^31,
- * ld < n, P < 0, P > n; ECAPACITY if P > 0 and ws is too small. */
+ * ld < n, P < 0, P > n, and with ws: nworkers > P, misaligned ws or k_blk
+ * out of [1, floor(n / P)]; ECAPACITY if ws is smaller than
+ * spardl_workspace_bytes(nworkers, P, n, k_blk). */
 int spardl_residual_add(float* acc, int64_t ld_acc, const float* grad, int64_t ld_grad,
-                        int32_t nworkers, int64_t n, int32_t P, void* ws, size_t ws_bytes,
+                        int32_t nworkers, int64_t n, int32_t P, int32_t k_blk, void* ws, size_t ws_bytes,
                         hipStream_t stream);
 
 /* Block-wise top-k (Sec. III-B: every worker sparsifies each of its P blocks

@@ -37,10 +37,10 @@ inline int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 // takes the rest of ws, split into three equal arrays (candidate index,
 // candidate value, threshold-bin key).
 struct Layout {
-  size_t err = 0, bitmap = 0, hist1 = 0, state = 0, slot_cnt = 0, slot_nbin = 0, pre_all = 0, pre_ge = 0,
-         pre_eq = 0;
+  size_t err = 0, bitmap = 0, hist1 = 0, spec_t1 = 0, spec_used = 0, spec_cnt = 0, state = 0, slot_cnt = 0,
+         slot_nbin = 0, pre_all = 0, pre_ge = 0, pre_eq = 0;
   size_t fixed_end = 0;
-  int64_t units = 0, tiles_tk = 0, groups_tk = 0, tiles_mg = 0, slot_n = 0, pairs_max = 0;
+  int64_t units = 0, tiles_tk = 0, groups_tk = 0, tiles_mg = 0, slot_n = 0, pairs_max = 0, add_tiles = 0;
 };
 
 Layout make_layout(int32_t P, int64_t n, int32_t kb) {
@@ -60,6 +60,15 @@ Layout make_layout(int32_t P, int64_t n, int32_t kb) {
   off += align256((size_t)ceil_div(n, 32) * 4);
   L.hist1 = off;
   off += align256((size_t)L.units * HCOPIES * NB1 * 4);
+  // speculative candidates of the fused residual add: per (worker, block) the
+  // previous threshold bin + 1 (0: none) and the floor used; per add tile the count
+  L.add_tiles = ceil_div(maxlen, ADD_TILE);
+  L.spec_t1 = off;
+  off += align256((size_t)P * P * 4);
+  L.spec_used = off;
+  off += align256((size_t)P * P * 4);
+  L.spec_cnt = off;
+  off += align256((size_t)P * P * L.add_tiles * 4);
   L.state = off;
   off += align256((size_t)L.units * ST_WORDS * 4);
   L.slot_cnt = off;
@@ -80,7 +89,8 @@ inline size_t cand_bytes(int64_t entries) { return 3 * align256((size_t)entries 
 
 struct Ws {
   char* base;
-  uint32_t *err, *bitmap, *hist1, *state, *slot_cnt, *slot_nbin, *pre_all, *pre_ge, *pre_eq;
+  uint32_t *err, *bitmap, *hist1, *spec_t1, *spec_used, *spec_cnt, *state, *slot_cnt, *slot_nbin, *pre_all, *pre_ge,
+      *pre_eq;
   int32_t* cand_idx;
   float* cand_val;
   uint32_t* bin_key;
@@ -93,6 +103,9 @@ Ws carve(void* ws, size_t ws_bytes, const Layout& L) {
   w.err = at(L.err);
   w.bitmap = at(L.bitmap);
   w.hist1 = at(L.hist1);
+  w.spec_t1 = at(L.spec_t1);
+  w.spec_used = at(L.spec_used);
+  w.spec_cnt = at(L.spec_cnt);
   w.state = at(L.state);
   w.slot_cnt = at(L.slot_cnt);
   w.slot_nbin = at(L.slot_nbin);
@@ -180,28 +193,37 @@ int spardl_workspace_init(int32_t nworkers, int32_t P, int64_t n, int32_t k_blk,
   if (ws_bytes < need) return SPARDL_ECAPACITY;
   const Layout L = make_layout(P, n, k_blk);
   Ws w = carve(ws, ws_bytes, L);
-  SPARDL_TRY(launch_fill(Fill().add(w.err, 64).add(w.hist1, L.units * HCOPIES * NB1).r, stream));
+  SPARDL_TRY(launch_fill(Fill().add(w.err, 64).add(w.hist1, L.units * HCOPIES * NB1).add(w.spec_t1, (int64_t)P * P).r,
+                         stream));
   return SPARDL_OK;
 }
 
 int spardl_residual_add(float* acc, int64_t ld_acc, const float* grad, int64_t ld_grad,
-                        int32_t nworkers, int64_t n, int32_t P, void* ws, size_t ws_bytes,
+                        int32_t nworkers, int64_t n, int32_t P, int32_t k_blk, void* ws, size_t ws_bytes,
                         hipStream_t stream) {
   if (!acc || !grad || nworkers < 1 || n < 1 || n > kMaxN || ld_acc < n || ld_grad < n || P < 0 ||
       P > n)
     return SPARDL_EINVAL;
   if (P == 0 || ws == nullptr) {
     const bool v4 = aligned16(acc) && aligned16(grad) && ld_acc % 4 == 0 && ld_grad % 4 == 0 && n % 4 == 0;
-    SPARDL_TRY(launch_residual_add(acc, ld_acc, grad, ld_grad, nworkers, n, 1, v4, nullptr, stream));
+    SPARDL_TRY(launch_residual_add(acc, ld_acc, grad, ld_grad, nworkers, n, 1, v4, AddSpec{}, stream));
     return SPARDL_OK;
   }
-  if (nworkers > P || ws_misaligned(ws)) return SPARDL_EINVAL;
-  // Only the level-1 histogram region is used; its offset and size depend on (P, n).
-  const Layout L = make_layout(P, n, 1);
-  if (ws_bytes < L.state) return SPARDL_ECAPACITY;
+  if (nworkers > P || ws_misaligned(ws) || !sizes_ok(P, n, k_blk)) return SPARDL_EINVAL;
+  const size_t need = spardl_workspace_bytes(nworkers, P, n, k_blk);
+  if (need == 0) return SPARDL_EINVAL;
+  if (ws_bytes < need) return SPARDL_ECAPACITY;
+  const Layout L = make_layout(P, n, k_blk);
   Ws w = carve(ws, ws_bytes, L);
   const bool v4 = aligned16(acc) && aligned16(grad) && ld_acc % 4 == 0 && ld_grad % 4 == 0 && blocks_vec4(n, P);
-  SPARDL_TRY(launch_residual_add(acc, ld_acc, grad, ld_grad, nworkers, n, P, v4, w.hist1, stream));
+  AddSpec sp;
+  sp.hist1 = w.hist1;
+  sp.spec_t1 = w.spec_t1;
+  sp.spec_used = w.spec_used;
+  sp.spec_cnt = w.spec_cnt;
+  sp.cand_idx = w.cand_idx;
+  sp.cand_val = w.cand_val;
+  SPARDL_TRY(launch_residual_add(acc, ld_acc, grad, ld_grad, nworkers, n, P, v4, sp, stream));
   return SPARDL_OK;
 }
 
@@ -223,9 +245,11 @@ int spardl_block_topk(const float* acc, int64_t ld_acc, int32_t nworkers, int64_
     SPARDL_TRY(launch_fill(Fill().add(w.hist1, units * HCOPIES * NB1).r, stream));
     SPARDL_TRY(launch_hist1(acc, ld_acc, nworkers, n, P, v4, w.hist1, stream));
   }
-  SPARDL_TRY(launch_select1(w.hist1, w.state, units, n, P, (uint32_t)k_blk, w.err, stream));
-  SPARDL_TRY(launch_collect(acc, ld_acc, nworkers, n, P, v4, smax, w.state, w.slot_cnt, w.slot_nbin,
-                            w.cand_idx, w.cand_val, w.bin_key, stream));
+  const bool spec = (flags & SPARDL_TOPK_HIST_READY) != 0;   // candidates of the fused add may be used
+  SPARDL_TRY(launch_select1(w.hist1, w.state, units, n, P, (uint32_t)k_blk, w.spec_t1, w.spec_used, spec, w.err,
+                            stream));
+  SPARDL_TRY(launch_collect(acc, ld_acc, nworkers, n, P, v4, smax, w.state, w.spec_cnt, (int32_t)L.add_tiles,
+                            w.slot_cnt, w.slot_nbin, w.cand_idx, w.cand_val, w.bin_key, stream));
   SPARDL_TRY(launch_thresh(0, units, n, P, k_blk, smax, 1, nullptr, w.cand_val, w.state, w.slot_cnt, w.slot_nbin,
                            w.bin_key, w.pre_all, w.pre_ge, w.pre_eq, nullptr, w.err, stream));
   SPARDL_TRY(launch_emit(0, w.cand_idx, w.cand_val, units, n, P, k_blk, 1, smax, EMIT_GROUP_TK, gmax, w.state,

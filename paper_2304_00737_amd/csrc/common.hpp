@@ -43,6 +43,7 @@ enum : int {
   ST_TGE = 4,       // every candidate with key >= ST_TGE is selected
   ST_TEQ = 5,       // ... and the first ST_NEEDEQ (by index) with key == ST_TEQ
   ST_NEEDEQ = 6,
+  ST_SPECOK = 7,    // block top-k: the fused add's speculative candidates cover the threshold bin
   ST_WORDS = 16
 };
 

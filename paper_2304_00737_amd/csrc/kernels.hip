@@ -58,11 +58,27 @@ __device__ __forceinline__ void flush_hist(const uint32_t* h, uint32_t* __restri
 // With HIST, every sum's level-1 digit is counted in an LDS histogram that is
 // flushed (non-zero bins only) into the block's global one.  The gradient is
 // read once, so it is loaded non-temporally.
+//
+// The float4 path with HIST also writes speculative candidates for the block
+// top-k that follows: every sum whose key is at or above a floor two level-1
+// bins below the block's previous threshold bin (nothing on a block's first
+// step), in index order at the tile's own span of the candidate arrays, with
+// the count per tile.  The exact threshold bin found from this pass's
+// histogram decides whether the floor was low enough; if not, the top-k reads
+// the block again.  Thread t owns the 8 consecutive elements at 8 t.
+constexpr uint32_t SPEC_MARGIN = 2;     // level-1 bins between the previous threshold bin and the floor
+constexpr uint32_t SPEC_NONE = 0xFFFFFFFFu;
+constexpr int ADD_STAGE = 512;          // speculative candidates staged in LDS per tile
+
 template <int VEC, bool HIST>
 __global__ __launch_bounds__(256) void k_residual_add(float* __restrict__ acc, int64_t ld_acc,
                                                       const float* __restrict__ grad, int64_t ld_grad,
-                                                      Blocks B, uint32_t G, uint32_t* __restrict__ hist1) {
+                                                      Blocks B, uint32_t G, AddSpec sp) {
+  constexpr bool SPEC = HIST && VEC == 4;
   __shared__ __align__(16) uint32_t h[HIST ? NB1 : 4];
+  __shared__ int32_t s_idx[SPEC ? ADD_STAGE : 1];
+  __shared__ float s_val[SPEC ? ADD_STAGE : 1];
+  __shared__ uint32_t wtot[4];
   const uint32_t g = blockIdx.x % G;
   const uint32_t wb = blockIdx.x / G;
   const uint32_t b = wb % B.P, w = wb / B.P;
@@ -76,30 +92,88 @@ __global__ __launch_bounds__(256) void k_residual_add(float* __restrict__ acc, i
   float* __restrict__ A = acc + (int64_t)w * ld_acc;
   const float* __restrict__ Gr = grad + (int64_t)w * ld_grad;
   if (VEC == 4) {
-    f4v a[ADD_F4], gg[ADD_F4];
+    static_assert(ADD_TILE == 256 * 8, "eight elements per thread");
+    const uint32_t my0 = t0 + threadIdx.x * 8u;
+    f4v a[2], gg[2];
 #pragma unroll
-    for (int j = 0; j < ADD_F4; ++j) {
-      const uint32_t off = t0 + (j * 256u + threadIdx.x) * 4u;
-      if (off < e) {
-        a[j] = *reinterpret_cast<const f4v*>(A + off);
-        gg[j] = __builtin_nontemporal_load(reinterpret_cast<const f4v*>(Gr + off));
+    for (int j = 0; j < 2; ++j) {
+      if (my0 + 4u * j < e) {
+        a[j] = *reinterpret_cast<const f4v*>(A + my0 + 4u * j);
+        gg[j] = __builtin_nontemporal_load(reinterpret_cast<const f4v*>(Gr + my0 + 4u * j));
       }
     }
+    uint32_t F = SPEC_NONE;
+    if (SPEC) {
+      const uint32_t sw = sp.spec_t1[wb];
+      if (sw != 0u) {
+        const uint32_t T1p = sw - 1u;
+        F = T1p > SPEC_MARGIN ? (T1p - SPEC_MARGIN) << D1_SHIFT : 0u;
+      }
+      if (g == 0u && threadIdx.x == 0) sp.spec_used[wb] = F;
+    }
+    float r[8];
+    uint32_t nc = 0;
 #pragma unroll
-    for (int j = 0; j < ADD_F4; ++j) {
-      const uint32_t off = t0 + (j * 256u + threadIdx.x) * 4u;
-      if (off < e) {
-        f4v r;
-        r.x = a[j].x + gg[j].x;
-        r.y = a[j].y + gg[j].y;
-        r.z = a[j].z + gg[j].z;
-        r.w = a[j].w + gg[j].w;
-        *reinterpret_cast<f4v*>(A + off) = r;
+    for (int j = 0; j < 2; ++j) {
+      if (my0 + 4u * j < e) {
+        f4v q;
+        q.x = a[j].x + gg[j].x;
+        q.y = a[j].y + gg[j].y;
+        q.z = a[j].z + gg[j].z;
+        q.w = a[j].w + gg[j].w;
+        *reinterpret_cast<f4v*>(A + my0 + 4u * j) = q;
+        r[4 * j + 0] = q.x;
+        r[4 * j + 1] = q.y;
+        r[4 * j + 2] = q.z;
+        r[4 * j + 3] = q.w;
         if (HIST) {
-          atomicAdd(&h[mag_key(r.x) >> D1_SHIFT], 1u);
-          atomicAdd(&h[mag_key(r.y) >> D1_SHIFT], 1u);
-          atomicAdd(&h[mag_key(r.z) >> D1_SHIFT], 1u);
-          atomicAdd(&h[mag_key(r.w) >> D1_SHIFT], 1u);
+#pragma unroll
+          for (int c = 0; c < 4; ++c) {
+            const uint32_t key = mag_key(r[4 * j + c]);
+            atomicAdd(&h[key >> D1_SHIFT], 1u);
+            nc += key >= F ? 1u : 0u;
+          }
+        }
+      } else {
+#pragma unroll
+        for (int c = 0; c < 4; ++c) r[4 * j + c] = 0.f;
+      }
+    }
+    if (SPEC) {
+      // index-ordered compaction of the candidates (keys >= F) of the tile
+      const int lane = lane_id(), wv = wave_id();
+      const uint32_t incl = wave_incl_scan(nc);
+      if (lane == WAVE - 1) wtot[wv] = incl;
+      __syncthreads();
+      uint32_t base = 0, tot = 0;
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        const uint32_t x = wtot[k];
+        base += k < wv ? x : 0u;
+        tot += x;
+      }
+      const bool staged = tot <= (uint32_t)ADD_STAGE;   // uniform
+      int32_t* __restrict__ CI = sp.cand_idx + (int64_t)w * B.n + t0;
+      float* __restrict__ CV = sp.cand_val + (int64_t)w * B.n + t0;
+      int32_t* __restrict__ oI = staged ? s_idx : CI;
+      float* __restrict__ oV = staged ? s_val : CV;
+      uint32_t pos = base + incl - nc;
+      if (nc != 0u) {
+#pragma unroll
+        for (int k = 0; k < 8; ++k) {
+          if (my0 + (uint32_t)k < e && mag_key(r[k]) >= F) {
+            oI[pos] = (int32_t)(my0 + k);
+            oV[pos] = r[k];
+            ++pos;
+          }
+        }
+      }
+      if (threadIdx.x == 0) sp.spec_cnt[(int64_t)wb * G + g] = tot;
+      if (staged) {
+        __syncthreads();
+        for (uint32_t k = threadIdx.x; k < tot; k += 256) {
+          CI[k] = s_idx[k];
+          CV[k] = s_val[k];
         }
       }
     }
@@ -113,10 +187,11 @@ __global__ __launch_bounds__(256) void k_residual_add(float* __restrict__ acc, i
         if (HIST) atomicAdd(&h[mag_key(r) >> D1_SHIFT], 1u);
       }
     }
+    if (HIST && g == 0u && threadIdx.x == 0) sp.spec_used[wb] = SPEC_NONE;   // no candidates on this path
   }
   if (HIST) {
     __syncthreads();
-    uint32_t* __restrict__ H = hist1 + ((int64_t)wb * HCOPIES + blockIdx.x % HCOPIES) * NB1;
+    uint32_t* __restrict__ H = sp.hist1 + ((int64_t)wb * HCOPIES + blockIdx.x % HCOPIES) * NB1;
     flush_hist(h, H);
   }
 }
@@ -165,7 +240,8 @@ __global__ __launch_bounds__(256) void k_hist1(const float* __restrict__ acc, in
 // workspace keeps its histograms at zero between steps), and their total
 // must equal the block length.
 __global__ __launch_bounds__(1024) void k_select1(uint32_t* __restrict__ hist1, uint32_t* __restrict__ state,
-                                                  Blocks B, uint32_t need,
+                                                  Blocks B, uint32_t need, uint32_t* __restrict__ spec_t1,
+                                                  const uint32_t* __restrict__ spec_used, int spec,
                                                   uint32_t* __restrict__ err) {
   constexpr int NT = 1024, PER = NB1 / NT;
   __shared__ uint32_t h[NB1];
@@ -194,6 +270,10 @@ __global__ __launch_bounds__(1024) void k_select1(uint32_t* __restrict__ hist1, 
     const uint32_t b = (uint32_t)u % B.P;
     uint32_t* st = state + u * ST_WORDS;
     if (!ok || total != B.start(b + 1u) - B.start(b)) atomicOr(err, ERR_COUNT);
+    // the fused add's speculative candidates hold every key >= its floor, so
+    // they are usable when the floor is at or below the threshold bin
+    st[ST_SPECOK] = (spec && ok && spec_used[u] <= (T << D1_SHIFT)) ? 1u : 0u;
+    spec_t1[u] = ok ? T + 1u : 0u;
     st[ST_T1] = T;
     st[ST_ABOVE1] = above;
     st[ST_NEED1] = ok ? need - above : 0u;
@@ -253,6 +333,8 @@ struct CollectSmem {
   float sv[COLLECT_STAGE];
   uint32_t sk[COLLECT_STAGE];
   uint32_t wtot[4];
+  uint32_t ck[SLOT / 256 * 4 + 1];   // speculative path: kept entries per (register, wave), then their prefix
+  uint32_t cb[SLOT / 256 * 4 + 1];   // ... and threshold-bin entries
 };
 
 template <int VEC, bool FULL>
@@ -338,31 +420,113 @@ __device__ __forceinline__ void collect_slot(const float* __restrict__ A, uint32
   }
 }
 
+// A slot whose candidates the fused residual add already wrote (every key at
+// or above its floor; per add tile, in index order at the tile's span) is
+// filtered by one wave: the entries at or above the level-1 threshold bin are
+// compacted in place in index order (the first tile's list, then the
+// second's) and the bin keys stored.  Each chunk is loaded into registers
+// before any of its writes, and a compacted position never exceeds the
+// storage position of an entry not yet read, so no barrier is needed.
+static_assert(SLOT == 2 * ADD_TILE, "a slot holds two residual-add tiles");
+constexpr int RC_R = 4;   // entries per lane per chunk
+__device__ __forceinline__ void recollect_wave(uint32_t c0, uint32_t c1, uint32_t tlo, uint32_t thi,
+                                               uint32_t* cnt_out, uint32_t* nbin_out, int32_t* __restrict__ CI,
+                                               float* __restrict__ CV, uint32_t* __restrict__ BK) {
+  const int lane = lane_id();
+  const uint64_t lt = __lanemask_lt();
+  const uint32_t tot = c0 + c1;
+  uint32_t kept = 0, nbin = 0;
+  for (uint32_t e0 = 0; e0 < tot; e0 += WAVE * RC_R) {
+    int32_t ix[RC_R];
+    float vx[RC_R];
+#pragma unroll
+    for (int r = 0; r < RC_R; ++r) {
+      const uint32_t e = e0 + r * WAVE + lane;
+      ix[r] = 0;
+      vx[r] = 0.f;
+      if (e < tot) {
+        const uint32_t src = e < c0 ? e : (uint32_t)ADD_TILE + (e - c0);
+        ix[r] = CI[src];
+        vx[r] = CV[src];
+      }
+    }
+#pragma unroll
+    for (int r = 0; r < RC_R; ++r) {
+      const uint32_t e = e0 + r * WAVE + lane;
+      const uint32_t key = mag_key(vx[r]);
+      const bool k = e < tot && key >= tlo;
+      const bool bk = k && key < thi;
+      const uint64_t mk = __ballot(k), mb = __ballot(bk);
+      if (k) {
+        const uint32_t pos = kept + popc64(mk & lt);
+        CI[pos] = ix[r];
+        CV[pos] = vx[r];
+      }
+      if (bk) BK[nbin + popc64(mb & lt)] = key;
+      kept += popc64(mk);
+      nbin += popc64(mb);
+    }
+  }
+  if (lane == 0) {
+    *cnt_out = kept;
+    *nbin_out = nbin;
+  }
+}
+
+// One workgroup per COLLECT_GROUP consecutive slots of one (worker, block).
+// With the fused add's candidates usable, wave k filters slot k of the group;
+// otherwise the workgroup collects the group's slots from acc one by one.
+constexpr int COLLECT_GROUP = 4;
 template <int VEC>
 __global__ __launch_bounds__(256) void k_collect(const float* __restrict__ acc, int64_t ld_acc, Blocks B,
-                                                 uint32_t smax, const uint32_t* __restrict__ state,
+                                                 uint32_t smax, uint32_t gq, const uint32_t* __restrict__ state,
+                                                 const uint32_t* __restrict__ spec_cnt, uint32_t add_tiles,
                                                  uint32_t* __restrict__ slot_cnt, uint32_t* __restrict__ slot_nbin,
                                                  int32_t* __restrict__ cand_idx, float* __restrict__ cand_val,
                                                  uint32_t* __restrict__ bin_key) {
   __shared__ CollectSmem L;
-  const uint32_t unit = blockIdx.x / smax;
-  const uint32_t slot = blockIdx.x % smax;
+  const uint32_t unit = blockIdx.x / gq;
+  const uint32_t slot0 = (blockIdx.x % gq) * (uint32_t)COLLECT_GROUP;
   const uint32_t b = unit % B.P, w = unit / B.P;
   const uint32_t s = B.start(b), e = B.start(b + 1u);
-  const uint32_t t0 = s + slot * (uint32_t)SLOT;
-  if (t0 >= e) return;
-  const uint32_t rem = e - t0;   // entries of this slot inside the block, clamped in 32 bits
-  const uint32_t nvalid = rem < (uint32_t)SLOT ? rem : (uint32_t)SLOT;
-  const float* __restrict__ A = acc + (int64_t)w * ld_acc + t0;
-  const int64_t cbase = (int64_t)w * B.n + t0;
-  const int64_t si = (int64_t)unit * smax + slot;
-  const uint32_t* t1_word = state + (int64_t)unit * ST_WORDS + ST_T1;
-  if (nvalid == (uint32_t)SLOT)
-    collect_slot<VEC, true>(A, nvalid, (int32_t)t0, t1_word, L, slot_cnt + si, slot_nbin + si,
-                            cand_idx + cbase, cand_val + cbase, bin_key + cbase);
-  else
-    collect_slot<VEC, false>(A, nvalid, (int32_t)t0, t1_word, L, slot_cnt + si, slot_nbin + si,
-                             cand_idx + cbase, cand_val + cbase, bin_key + cbase);
+  if (s + slot0 * (uint32_t)SLOT >= e) return;
+  const uint32_t* st = state + (int64_t)unit * ST_WORDS;
+  const uint32_t specok = st[ST_SPECOK];
+  const uint32_t T1 = st[ST_T1];
+  if (specok != 0u) {
+    const uint32_t slot = slot0 + (uint32_t)wave_id();
+    const uint32_t t0 = s + slot * (uint32_t)SLOT;
+    if (slot >= smax || t0 >= e) return;
+    const uint32_t tlo = T1 << D1_SHIFT, thi = tlo + (1u << D1_SHIFT);
+    const int64_t tile0 = (int64_t)unit * add_tiles + (int64_t)slot * (SLOT / ADD_TILE);
+    // counts are clamped to the tiles' lengths inside the block, so reads stay in the slot
+    const uint32_t len0 = min(e - t0, (uint32_t)ADD_TILE);
+    const uint32_t len1 = t0 + (uint32_t)ADD_TILE < e ? min(e - t0 - (uint32_t)ADD_TILE, (uint32_t)ADD_TILE) : 0u;
+    const uint32_t c0 = min(spec_cnt[tile0], len0);
+    const uint32_t c1 = len1 != 0u ? min(spec_cnt[tile0 + 1], len1) : 0u;
+    const int64_t cbase = (int64_t)w * B.n + t0;
+    const int64_t si = (int64_t)unit * smax + slot;
+    recollect_wave(c0, c1, tlo, thi, slot_cnt + si, slot_nbin + si, cand_idx + cbase, cand_val + cbase,
+                   bin_key + cbase);
+    return;
+  }
+  for (int k = 0; k < COLLECT_GROUP; ++k) {
+    const uint32_t slot = slot0 + (uint32_t)k;
+    const uint32_t t0 = s + slot * (uint32_t)SLOT;
+    if (slot >= smax || t0 >= e) break;   // uniform
+    if (k > 0) __syncthreads();           // LDS reuse
+    const uint32_t rem = e - t0;          // entries of this slot inside the block, clamped in 32 bits
+    const uint32_t nvalid = rem < (uint32_t)SLOT ? rem : (uint32_t)SLOT;
+    const float* __restrict__ A = acc + (int64_t)w * ld_acc + t0;
+    const int64_t cbase = (int64_t)w * B.n + t0;
+    const int64_t si = (int64_t)unit * smax + slot;
+    if (nvalid == (uint32_t)SLOT)
+      collect_slot<VEC, true>(A, nvalid, (int32_t)t0, st + ST_T1, L, slot_cnt + si, slot_nbin + si,
+                              cand_idx + cbase, cand_val + cbase, bin_key + cbase);
+    else
+      collect_slot<VEC, false>(A, nvalid, (int32_t)t0, st + ST_T1, L, slot_cnt + si, slot_nbin + si,
+                               cand_idx + cbase, cand_val + cbase, bin_key + cbase);
+  }
 }
 
 // ============================================================================ exact threshold
@@ -1476,20 +1640,21 @@ hipError_t launch_fill(const FillRanges& r, hipStream_t s) {
 }
 
 hipError_t launch_residual_add(float* acc, int64_t ld_acc, const float* grad, int64_t ld_grad,
-                               int32_t nworkers, int64_t n, int32_t P, bool vec4, uint32_t* hist1,
+                               int32_t nworkers, int64_t n, int32_t P, bool vec4, const AddSpec& sp,
                                hipStream_t s) {
-  const int32_t PP = hist1 ? P : 1;
+  const bool hist = sp.hist1 != nullptr;
+  const int32_t PP = hist ? P : 1;
   const int64_t maxlen = (n + PP - 1) / PP;
   const int32_t G = (int32_t)((maxlen + ADD_TILE - 1) / ADD_TILE);
   const dim3 grid((unsigned)((int64_t)nworkers * PP * G));
   const Blocks B = make_blocks(n, PP);
   const uint32_t uG = (uint32_t)G;
-  if (hist1) {
-    if (vec4) hipLaunchKernelGGL((k_residual_add<4, true>), grid, dim3(256), 0, s, acc, ld_acc, grad, ld_grad, B, uG, hist1);
-    else hipLaunchKernelGGL((k_residual_add<1, true>), grid, dim3(256), 0, s, acc, ld_acc, grad, ld_grad, B, uG, hist1);
+  if (hist) {
+    if (vec4) hipLaunchKernelGGL((k_residual_add<4, true>), grid, dim3(256), 0, s, acc, ld_acc, grad, ld_grad, B, uG, sp);
+    else hipLaunchKernelGGL((k_residual_add<1, true>), grid, dim3(256), 0, s, acc, ld_acc, grad, ld_grad, B, uG, sp);
   } else {
-    if (vec4) hipLaunchKernelGGL((k_residual_add<4, false>), grid, dim3(256), 0, s, acc, ld_acc, grad, ld_grad, B, uG, hist1);
-    else hipLaunchKernelGGL((k_residual_add<1, false>), grid, dim3(256), 0, s, acc, ld_acc, grad, ld_grad, B, uG, hist1);
+    if (vec4) hipLaunchKernelGGL((k_residual_add<4, false>), grid, dim3(256), 0, s, acc, ld_acc, grad, ld_grad, B, uG, sp);
+    else hipLaunchKernelGGL((k_residual_add<1, false>), grid, dim3(256), 0, s, acc, ld_acc, grad, ld_grad, B, uG, sp);
   }
   return hipGetLastError();
 }
@@ -1506,19 +1671,21 @@ hipError_t launch_hist1(const float* acc, int64_t ld_acc, int32_t nworkers, int6
 }
 
 hipError_t launch_select1(uint32_t* hist1, uint32_t* state, int64_t nunits, int64_t n, int32_t P, uint32_t need,
-                          uint32_t* err, hipStream_t s) {
-  hipLaunchKernelGGL(k_select1, dim3((unsigned)nunits), dim3(1024), 0, s, hist1, state, make_blocks(n, P), need, err);
+                          uint32_t* spec_t1, const uint32_t* spec_used, bool spec, uint32_t* err, hipStream_t s) {
+  hipLaunchKernelGGL(k_select1, dim3((unsigned)nunits), dim3(1024), 0, s, hist1, state, make_blocks(n, P), need,
+                     spec_t1, spec_used, spec ? 1 : 0, err);
   return hipGetLastError();
 }
 
 hipError_t launch_collect(const float* acc, int64_t ld_acc, int32_t nworkers, int64_t n, int32_t P,
-                          bool vec4, int32_t smax, const uint32_t* state, uint32_t* slot_cnt,
-                          uint32_t* slot_nbin, int32_t* cand_idx, float* cand_val, uint32_t* bin_key,
-                          hipStream_t s) {
-  const dim3 grid((unsigned)((int64_t)nworkers * P * smax));
+                          bool vec4, int32_t smax, const uint32_t* state, const uint32_t* spec_cnt,
+                          int32_t add_tiles, uint32_t* slot_cnt, uint32_t* slot_nbin, int32_t* cand_idx,
+                          float* cand_val, uint32_t* bin_key, hipStream_t s) {
+  const uint32_t gq = (uint32_t)((smax + COLLECT_GROUP - 1) / COLLECT_GROUP);
+  const dim3 grid((unsigned)((int64_t)nworkers * P * gq));
   const Blocks B = make_blocks(n, P);
-  if (vec4) hipLaunchKernelGGL(k_collect<4>, grid, dim3(256), 0, s, acc, ld_acc, B, (uint32_t)smax, state, slot_cnt, slot_nbin, cand_idx, cand_val, bin_key);
-  else hipLaunchKernelGGL(k_collect<1>, grid, dim3(256), 0, s, acc, ld_acc, B, (uint32_t)smax, state, slot_cnt, slot_nbin, cand_idx, cand_val, bin_key);
+  if (vec4) hipLaunchKernelGGL(k_collect<4>, grid, dim3(256), 0, s, acc, ld_acc, B, (uint32_t)smax, gq, state, spec_cnt, (uint32_t)add_tiles, slot_cnt, slot_nbin, cand_idx, cand_val, bin_key);
+  else hipLaunchKernelGGL(k_collect<1>, grid, dim3(256), 0, s, acc, ld_acc, B, (uint32_t)smax, gq, state, spec_cnt, (uint32_t)add_tiles, slot_cnt, slot_nbin, cand_idx, cand_val, bin_key);
   return hipGetLastError();
 }
 

@@ -13,18 +13,28 @@ struct FillRanges {
   int count;
 };
 
+// Workspace arrays of the fused residual add (all null: plain add).
+struct AddSpec {
+  uint32_t* hist1 = nullptr;       // level-1 histograms, HCOPIES per (worker, block)
+  const uint32_t* spec_t1 = nullptr;  // previous threshold bin + 1 per (worker, block), 0 = none
+  uint32_t* spec_used = nullptr;   // floor used for the speculative candidates per (worker, block)
+  uint32_t* spec_cnt = nullptr;    // speculative candidates per add tile
+  int32_t* cand_idx = nullptr;     // candidate index / value arrays (row-sized)
+  float* cand_val = nullptr;
+};
+
 hipError_t launch_fill(const FillRanges& r, hipStream_t s);
 hipError_t launch_residual_add(float* acc, int64_t ld_acc, const float* grad, int64_t ld_grad,
-                               int32_t nworkers, int64_t n, int32_t P, bool vec4, uint32_t* hist1,
+                               int32_t nworkers, int64_t n, int32_t P, bool vec4, const AddSpec& sp,
                                hipStream_t s);
 hipError_t launch_hist1(const float* acc, int64_t ld_acc, int32_t nworkers, int64_t n, int32_t P,
                         bool vec4, uint32_t* hist1, hipStream_t s);
 hipError_t launch_select1(uint32_t* hist1, uint32_t* state, int64_t nunits, int64_t n, int32_t P, uint32_t need,
-                          uint32_t* err, hipStream_t s);
+                          uint32_t* spec_t1, const uint32_t* spec_used, bool spec, uint32_t* err, hipStream_t s);
 hipError_t launch_collect(const float* acc, int64_t ld_acc, int32_t nworkers, int64_t n, int32_t P,
-                          bool vec4, int32_t smax, const uint32_t* state, uint32_t* slot_cnt,
-                          uint32_t* slot_nbin, int32_t* cand_idx, float* cand_val, uint32_t* bin_key,
-                          hipStream_t s);
+                          bool vec4, int32_t smax, const uint32_t* state, const uint32_t* spec_cnt,
+                          int32_t add_tiles, uint32_t* slot_cnt, uint32_t* slot_nbin, int32_t* cand_idx,
+                          float* cand_val, uint32_t* bin_key, hipStream_t s);
 hipError_t launch_thresh(int mode, int64_t nunits, int64_t n, int32_t P, int32_t kb, int32_t smax, int lps,
                          uint32_t* hist1, const float* U_val, uint32_t* state, const uint32_t* slot_cnt,
                          const uint32_t* slot_nbin, const uint32_t* bin_key, uint32_t* pre_all, uint32_t* pre_ge,

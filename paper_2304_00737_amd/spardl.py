@@ -37,7 +37,7 @@ _lib.spardl_workspace_bytes.argtypes = [_i32, _i32, _i64, _i32]
 _lib.spardl_workspace_bytes.restype = _sz
 _lib.spardl_workspace_init.argtypes = [_i32, _i32, _i64, _i32, _p, _sz, _p]
 _lib.spardl_workspace_init.restype = ctypes.c_int
-_lib.spardl_residual_add.argtypes = [_p, _i64, _p, _i64, _i32, _i64, _i32, _p, _sz, _p]
+_lib.spardl_residual_add.argtypes = [_p, _i64, _p, _i64, _i32, _i64, _i32, _i32, _p, _sz, _p]
 _lib.spardl_block_topk.argtypes = [_p, _i64, _i32, _i64, _i32, _i32, _i32, _p, _p, _p, _p, _sz, _p]
 _lib.spardl_sparse_merge_topk.argtypes = [_p, _p, _i32, _i64, _i32, _i32, _p, _p, _p, _p, _sz, _p]
 _lib.spardl_allgather_densify.argtypes = [_p, _p, _i32, _i64, _i32, _p, _p]
@@ -107,13 +107,13 @@ def workspace(nworkers: int, P: int, n: int, k_blk: int, device="cuda", *, strea
     return ws
 
 
-def residual_add(acc, grad, nworkers: int, n: int, P: int = 0, ws=None, *, ld_acc=None, ld_grad=None,
-                 stream=None) -> None:
+def residual_add(acc, grad, nworkers: int, n: int, P: int = 0, ws=None, k_blk: int = 0, *, ld_acc=None,
+                 ld_grad=None, stream=None) -> None:
     ld_acc = _ld(acc, n) if ld_acc is None else ld_acc
     ld_grad = _ld(grad, n) if ld_grad is None else ld_grad
     ws_bytes = ws.numel() * ws.element_size() if ws is not None else 0
     _check("residual_add", _lib.spardl_residual_add(_ptr(acc), ld_acc, _ptr(grad), ld_grad, nworkers, n, P,
-                                                    _ptr(ws), ws_bytes, _stream(stream)))
+                                                    k_blk, _ptr(ws), ws_bytes, _stream(stream)))
 
 
 def block_topk(acc, nworkers: int, n: int, P: int, k_blk: int, sp_idx, sp_val, local_idx=None, ws=None,
@@ -176,7 +176,7 @@ class SparDLStep:
 
     def residual_add(self, grad, stream=None):
         if self.fused:
-            residual_add(self.acc, grad, self.P, self.n, self.P, self.ws, stream=stream)
+            residual_add(self.acc, grad, self.P, self.n, self.P, self.ws, self.k_blk, stream=stream)
         else:
             residual_add(self.acc, grad, self.P, self.n, 0, None, stream=stream)
 

@@ -6,6 +6,7 @@ from __future__ import annotations
 import sys
 
 import numpy as np
+import torch
 
 from oracle import spardl_oracle as so
 
@@ -80,3 +81,42 @@ def compare_step(st, res, P: int, n: int, kb: int, blocks=None, acc_host=None) -
         for b in blocks:
             got = st.acc[w, bounds[b]:bounds[b + 1]].cpu().numpy()
             assert_bits_equal(got, res.residual[(w, b)], f"residual w={w} b={b}")
+
+
+def ws_layout(P: int, n: int, kb: int, ws_bytes: int) -> dict:
+    """Byte offsets of the workspace arrays, mirroring the library's layout
+    (kept in step with it by tests/test_abi_cpu.py::test_ws_layout_mirror)."""
+    al = lambda x: (x + 255) & ~255
+    l = 0
+    while (1 << l) < P:
+        l += 1
+    bags = [P - (1 << (l - 1)) if i == 1 else (1 << (l - i)) for i in range(1, l + 1)]
+    mmax = max(bags) if bags else 0
+    maxlen = -(-n // P)
+    pairs_max = P * mmax
+    units = max(P * P, pairs_max)
+    tiles_tk = -(-maxlen // 4096)
+    tiles_mg = -(-2 * kb // 4096)
+    add_tiles = -(-maxlen // 2048)
+    slot_n = max(P * P * tiles_tk, pairs_max * tiles_mg)
+    L, off = {}, 256
+    L["bitmap"] = off; off += al(-(-n // 32) * 4)
+    L["hist1"] = off; off += al(units * 16 * 4096 * 4)
+    L["spec_t1"] = off; off += al(P * P * 4)
+    L["spec_used"] = off; off += al(P * P * 4)
+    L["spec_cnt"] = off; off += al(P * P * add_tiles * 4)
+    L["state"] = off; off += al(units * 16 * 4)
+    for k in ("slot_cnt", "slot_nbin", "pre_all", "pre_ge", "pre_eq"):
+        L[k] = off; off += al(slot_n * 4)
+    L["fixed_end"] = off
+    L["cand_entries"] = max(P * n, pairs_max * tiles_mg * 4096)
+    q = ((ws_bytes - off) // 3) & ~255
+    L["cand_idx"], L["cand_val"], L["bin_key"] = off, off + q, off + 2 * q
+    return L
+
+
+def ws_spec_ok(st) -> list:
+    """Per (worker, block): did the last block top-k use the fused add's candidates?"""
+    L = ws_layout(st.P, st.n, st.k_blk, st.ws.numel())
+    words = st.ws[L["state"]:L["state"] + st.P * st.P * 16 * 4].view(torch.int32).cpu().numpy()
+    return [bool(words[u * 16 + 7]) for u in range(st.P * st.P)]

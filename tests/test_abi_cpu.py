@@ -85,10 +85,17 @@ def test_argument_errors_enqueue_nothing():
     i64, i32, sz = ctypes.c_int64, ctypes.c_int32, ctypes.c_size_t
     EINVAL, ECAP = -1, -2
     # residual_add: NULL acc, ld < n, P > n
-    assert lib.spardl_residual_add(null, i64(10), p, i64(10), i32(1), i64(10), i32(0), null, sz(0), null) == EINVAL
-    assert lib.spardl_residual_add(p, i64(9), p, i64(10), i32(1), i64(10), i32(0), null, sz(0), null) == EINVAL
-    assert lib.spardl_residual_add(p, i64(10), p, i64(10), i32(1), i64(10), i32(11), p, sz(1 << 20), null) == EINVAL
-    assert lib.spardl_residual_add(p, i64(100), p, i64(100), i32(2), i64(100), i32(4), p, sz(16), null) == ECAP
+    assert lib.spardl_residual_add(null, i64(10), p, i64(10), i32(1), i64(10), i32(0), i32(0), null, sz(0),
+                                   null) == EINVAL
+    assert lib.spardl_residual_add(p, i64(9), p, i64(10), i32(1), i64(10), i32(0), i32(0), null, sz(0),
+                                   null) == EINVAL
+    assert lib.spardl_residual_add(p, i64(10), p, i64(10), i32(1), i64(10), i32(11), i32(1), p, sz(1 << 20),
+                                   null) == EINVAL
+    assert lib.spardl_residual_add(p, i64(100), p, i64(100), i32(2), i64(100), i32(4), i32(3), p, sz(16),
+                                   null) == ECAP
+    # with ws: k_blk outside [1, n / P]
+    assert lib.spardl_residual_add(p, i64(100), p, i64(100), i32(2), i64(100), i32(4), i32(26), p, sz(1 << 30),
+                                   null) == EINVAL
     # block_topk: k_blk too large, flags unknown, nworkers > P, small workspace
     assert lib.spardl_block_topk(p, i64(100), i32(1), i64(100), i32(4), i32(26), i32(0), p, p, null, p,
                                  sz(1 << 30), null) == EINVAL
@@ -127,3 +134,15 @@ def test_argument_errors_enqueue_nothing():
                                        sz(1 << 30), null) == EINVAL
     for s in (0, -1, -2, -3, 7):
         assert lib.spardl_strerror(s)
+
+
+def test_ws_layout_mirror():
+    """The GPU tests read workspace words through a Python mirror of the
+    layout; its total must equal the library's workspace size."""
+    from tests.gpu_util import ws_layout
+    lib = _lib()
+    al = lambda x: (x + 255) & ~255
+    for P, n, kb in [(1, 5000, 7), (4, 1 << 20, 2622), (5, 6000, 1200), (8, 25_600_000, 32_000), (16, 65536, 41),
+                     (12, 60000, 50), (3, 100003, 33334)]:
+        L = ws_layout(P, n, kb, 0)
+        assert L["fixed_end"] + 3 * al(L["cand_entries"] * 4) == lib.spardl_workspace_bytes(P, P, n, kb), (P, n, kb)

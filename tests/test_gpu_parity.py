@@ -11,7 +11,7 @@ import pytest
 
 from oracle import spardl_oracle as so
 from tests.conftest import gpu_available
-from tests.gpu_util import assert_bits_equal, assert_idx_equal, check_ws, compare_step, log
+from tests.gpu_util import assert_bits_equal, assert_idx_equal, check_ws, compare_step, log, ws_spec_ok
 
 pytestmark = pytest.mark.gpu
 
@@ -52,7 +52,7 @@ def test_residual_add(P, n, ld, hist):
     ws = None
     if hist:
         ws = spardl.workspace(P, P, n, 1)
-    spardl.residual_add(a_d, g_d, P, n, P if hist else 0, ws, ld_acc=ld, ld_grad=ld)
+    spardl.residual_add(a_d, g_d, P, n, P if hist else 0, ws, 1 if hist else 0, ld_acc=ld, ld_grad=ld)
     want = acc.copy()
     want[:, :n] = so.residual_add(acc[:, :n], grad[:, :n])
     assert_bits_equal(a_d.cpu().numpy(), want, "acc after residual add")
@@ -245,6 +245,36 @@ def test_deterministic():
                     snap.append(di[w, t, :dc[w, t]].tobytes() + dv[w, t, :dc[w, t]].tobytes())
         outs.append(snap)
     assert outs[0] == outs[1]
+
+
+def test_step_speculation_fallback():
+    """The fused residual add writes candidates above a floor just below each
+    block's previous threshold.  A much smaller gradient after a large one
+    drops the threshold below that floor, so the top-k must read the block
+    again; rising thresholds use the fused candidates.  Both paths must match
+    the oracle bit for bit, and both must actually run."""
+    P, n, kb = 4, 200000, 300
+    st = spardl.SparDLStep(P, n, kb)
+    acc = np.zeros((P, n), np.float32)
+    bounds = so.block_bounds(n, P)
+    rng = np.random.default_rng(77)
+    used = []
+    for t, scale in enumerate([1.0, 1e-4, 1.0, 1.0]):
+        grad = (_rows("normal", P, n, 500 + t) * np.float32(scale)).astype(np.float32)
+        if t == 0:   # k_blk huge entries per block: the top-k takes them, and the next threshold is far lower
+            for w in range(P):
+                for b in range(P):
+                    pos = bounds[b] + rng.choice(bounds[b + 1] - bounds[b], kb, replace=False)
+                    grad[w, pos] = np.float32(1000.0) * np.sign(grad[w, pos] + np.float32(0.5))
+        log(f"speculation step {t + 1}: gradient scale {scale}")
+        st.step(_dev(grad))
+        check_ws(st)
+        used.append(ws_spec_ok(st))
+        res = so.spardl_step([acc[w] for w in range(P)], [grad[w] for w in range(P)], P, n, kb)
+        compare_step(st, res, P, n, kb)
+    assert not any(used[0]), "no speculation is possible on the first step"
+    assert not all(used[1]), "a falling threshold must fall back to re-reading the block"
+    assert all(used[3]), "rising thresholds use the fused candidates"
 
 
 def test_histogram_misuse_is_flagged():
