@@ -67,7 +67,7 @@ Layout make_layout(int32_t P, int64_t n, int32_t kb) {
   off += align256((size_t)P * P * 4);
   L.spec_used = off;
   off += align256((size_t)P * P * 4);
-  L.spec_cnt = off;
+  L.spec_cnt = off;   // per add tile
   off += align256((size_t)P * P * L.add_tiles * 4);
   L.state = off;
   off += align256((size_t)L.units * ST_WORDS * 4);
@@ -246,8 +246,8 @@ int spardl_block_topk(const float* acc, int64_t ld_acc, int32_t nworkers, int64_
     SPARDL_TRY(launch_hist1(acc, ld_acc, nworkers, n, P, v4, w.hist1, stream));
   }
   const bool spec = (flags & SPARDL_TOPK_HIST_READY) != 0;   // candidates of the fused add may be used
-  SPARDL_TRY(launch_select1(w.hist1, w.state, units, n, P, (uint32_t)k_blk, w.spec_t1, w.spec_used, spec, w.err,
-                            stream));
+  SPARDL_TRY(launch_select1(w.hist1, w.state, units, n, P, (uint32_t)k_blk, w.spec_t1, w.spec_used, spec, acc,
+                            ld_acc, v4, w.err, stream));
   SPARDL_TRY(launch_collect(acc, ld_acc, nworkers, n, P, v4, smax, w.state, w.spec_cnt, (int32_t)L.add_tiles,
                             w.slot_cnt, w.slot_nbin, w.cand_idx, w.cand_val, w.bin_key, stream));
   SPARDL_TRY(launch_thresh(0, units, n, P, k_blk, smax, 1, nullptr, w.cand_val, w.state, w.slot_cnt, w.slot_nbin,

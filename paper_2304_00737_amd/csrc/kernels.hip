@@ -66,9 +66,22 @@ __device__ __forceinline__ void flush_hist(const uint32_t* h, uint32_t* __restri
 // the count per tile.  The exact threshold bin found from this pass's
 // histogram decides whether the floor was low enough; if not, the top-k reads
 // the block again.  Thread t owns the 8 consecutive elements at 8 t.
+//
+// From a block's second step on, the histogram counts only keys at or above
+// a lower floor (two binades further down): the threshold lies there unless it
+// fell by more than that since the previous step, and then the level-1 select
+// rebuilds the block's full histogram itself.
 constexpr uint32_t SPEC_MARGIN = 2;     // level-1 bins between the previous threshold bin and the floor
+constexpr uint32_t HIST_MARGIN = 32;    // further level-1 bins below the candidate floor kept in the histogram
 constexpr uint32_t SPEC_NONE = 0xFFFFFFFFu;
 constexpr int ADD_STAGE = 512;          // speculative candidates staged in LDS per tile
+
+// Histogram floor (a key) for a candidate floor F (SPEC_NONE: histogram everything).
+__device__ __forceinline__ uint32_t hist_floor(uint32_t F) {
+  if (F == SPEC_NONE) return 0u;
+  const uint32_t fb = F >> D1_SHIFT;
+  return fb > HIST_MARGIN ? (fb - HIST_MARGIN) << D1_SHIFT : 0u;
+}
 
 template <int VEC, bool HIST>
 __global__ __launch_bounds__(256) void k_residual_add(float* __restrict__ acc, int64_t ld_acc,
@@ -111,6 +124,7 @@ __global__ __launch_bounds__(256) void k_residual_add(float* __restrict__ acc, i
       }
       if (g == 0u && threadIdx.x == 0) sp.spec_used[wb] = F;
     }
+    const uint32_t FH = hist_floor(F);
     float r[8];
     uint32_t nc = 0;
 #pragma unroll
@@ -130,7 +144,7 @@ __global__ __launch_bounds__(256) void k_residual_add(float* __restrict__ acc, i
 #pragma unroll
           for (int c = 0; c < 4; ++c) {
             const uint32_t key = mag_key(r[4 * j + c]);
-            atomicAdd(&h[key >> D1_SHIFT], 1u);
+            if (key >= FH) atomicAdd(&h[key >> D1_SHIFT], 1u);
             nc += key >= F ? 1u : 0u;
           }
         }
@@ -237,11 +251,15 @@ __global__ __launch_bounds__(256) void k_hist1(const float* __restrict__ acc, in
 // ============================================================================ level-1 select
 // The block's histogram is the sum of its HCOPIES copies; every load is in
 // flight before the first add.  The copies are cleared once read (the
-// workspace keeps its histograms at zero between steps), and their total
-// must equal the block length.
+// workspace keeps its histograms at zero between steps).  A histogram of the
+// fused add covers keys at or above hist_floor(its candidate floor) (a bin
+// boundary), which decides the select exactly whenever the threshold bin lies
+// there; otherwise the workgroup rebuilds the block's full histogram from acc.
+// A full histogram must hold exactly the block's entries.
 __global__ __launch_bounds__(1024) void k_select1(uint32_t* __restrict__ hist1, uint32_t* __restrict__ state,
                                                   Blocks B, uint32_t need, uint32_t* __restrict__ spec_t1,
                                                   const uint32_t* __restrict__ spec_used, int spec,
+                                                  const float* __restrict__ acc, int64_t ld_acc, int vec4,
                                                   uint32_t* __restrict__ err) {
   constexpr int NT = 1024, PER = NB1 / NT;
   __shared__ uint32_t h[NB1];
@@ -263,16 +281,51 @@ __global__ __launch_bounds__(1024) void k_select1(uint32_t* __restrict__ hist1, 
     }
     h[q * NT + threadIdx.x] = c;
   }
+  const uint32_t used = spec ? spec_used[u] : SPEC_NONE;
+  const uint32_t FH = hist_floor(used);
   __syncthreads();
   uint32_t T, above, cnt, ok, total;
   block_select_desc(h, NB1, need, scratch, &T, &above, &cnt, &ok, &total);
+  const uint32_t b = (uint32_t)u % B.P, w = (uint32_t)u / B.P;
+  const uint32_t s = B.start(b), e = B.start(b + 1u);
+  bool full = FH == 0u;
+  if (!ok && !full) {   // the threshold fell below the histogram's floor: count the whole block
+    for (int i = threadIdx.x; i < NB1; i += NT) h[i] = 0u;
+    __syncthreads();
+    const float* __restrict__ A = acc + (int64_t)w * ld_acc;
+    if (vec4) {
+      for (uint32_t x0 = s + threadIdx.x * 4u; x0 < e; x0 += NT * 4u * 4u) {
+        f4v v[4];
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+          const uint32_t x = x0 + (uint32_t)k * NT * 4u;
+          if (x < e) v[k] = *reinterpret_cast<const f4v*>(A + x);
+        }
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+          const uint32_t x = x0 + (uint32_t)k * NT * 4u;
+          if (x < e) {
+            atomicAdd(&h[mag_key(v[k].x) >> D1_SHIFT], 1u);
+            atomicAdd(&h[mag_key(v[k].y) >> D1_SHIFT], 1u);
+            atomicAdd(&h[mag_key(v[k].z) >> D1_SHIFT], 1u);
+            atomicAdd(&h[mag_key(v[k].w) >> D1_SHIFT], 1u);
+          }
+        }
+      }
+    } else {
+      for (uint32_t x = s + threadIdx.x; x < e; x += NT) atomicAdd(&h[mag_key(A[x]) >> D1_SHIFT], 1u);
+    }
+    __syncthreads();
+    block_select_desc(h, NB1, need, scratch, &T, &above, &cnt, &ok, &total);
+    full = true;
+  }
   if (threadIdx.x == 0) {
-    const uint32_t b = (uint32_t)u % B.P;
     uint32_t* st = state + u * ST_WORDS;
-    if (!ok || total != B.start(b + 1u) - B.start(b)) atomicOr(err, ERR_COUNT);
+    const uint32_t len = e - s;
+    if (!ok || (full ? total != len : total > len)) atomicOr(err, ERR_COUNT);
     // the fused add's speculative candidates hold every key >= its floor, so
     // they are usable when the floor is at or below the threshold bin
-    st[ST_SPECOK] = (spec && ok && spec_used[u] <= (T << D1_SHIFT)) ? 1u : 0u;
+    st[ST_SPECOK] = (spec && ok && used <= (T << D1_SHIFT)) ? 1u : 0u;
     spec_t1[u] = ok ? T + 1u : 0u;
     st[ST_T1] = T;
     st[ST_ABOVE1] = above;
@@ -1671,9 +1724,10 @@ hipError_t launch_hist1(const float* acc, int64_t ld_acc, int32_t nworkers, int6
 }
 
 hipError_t launch_select1(uint32_t* hist1, uint32_t* state, int64_t nunits, int64_t n, int32_t P, uint32_t need,
-                          uint32_t* spec_t1, const uint32_t* spec_used, bool spec, uint32_t* err, hipStream_t s) {
+                          uint32_t* spec_t1, const uint32_t* spec_used, bool spec, const float* acc, int64_t ld_acc,
+                          bool vec4, uint32_t* err, hipStream_t s) {
   hipLaunchKernelGGL(k_select1, dim3((unsigned)nunits), dim3(1024), 0, s, hist1, state, make_blocks(n, P), need,
-                     spec_t1, spec_used, spec ? 1 : 0, err);
+                     spec_t1, spec_used, spec ? 1 : 0, acc, ld_acc, vec4 ? 1 : 0, err);
   return hipGetLastError();
 }
 

@@ -30,7 +30,8 @@ hipError_t launch_residual_add(float* acc, int64_t ld_acc, const float* grad, in
 hipError_t launch_hist1(const float* acc, int64_t ld_acc, int32_t nworkers, int64_t n, int32_t P,
                         bool vec4, uint32_t* hist1, hipStream_t s);
 hipError_t launch_select1(uint32_t* hist1, uint32_t* state, int64_t nunits, int64_t n, int32_t P, uint32_t need,
-                          uint32_t* spec_t1, const uint32_t* spec_used, bool spec, uint32_t* err, hipStream_t s);
+                          uint32_t* spec_t1, const uint32_t* spec_used, bool spec, const float* acc, int64_t ld_acc,
+                          bool vec4, uint32_t* err, hipStream_t s);
 hipError_t launch_collect(const float* acc, int64_t ld_acc, int32_t nworkers, int64_t n, int32_t P,
                           bool vec4, int32_t smax, const uint32_t* state, const uint32_t* spec_cnt,
                           int32_t add_tiles, uint32_t* slot_cnt, uint32_t* slot_nbin, int32_t* cand_idx,
