@@ -32,8 +32,8 @@
  *  - ws is scratch device memory of at least spardl_workspace_bytes(...)
  *    bytes, 256-byte aligned (EINVAL otherwise), prepared once by
  *    spardl_workspace_init before its first use.  Between calls it keeps its
- *    level-1 histograms at zero: the call that consumes a histogram clears it,
- *    so no call spends a memset on them.  The first 4 bytes of ws hold an
+ *    level-1 histograms and the final-index bitmap at zero (the call that
+ *    uses one clears it again), so no call spends a memset on them.  The first 4 bytes of ws hold an
  *    error word that spardl_workspace_init clears and that kernels OR bits
  *    into if an internal check fails (see SPARDL_WS_ERR_*); it stays set until
  *    the next spardl_workspace_init.  Read it after the stream completes.
@@ -90,8 +90,9 @@ int spardl_srs_plan(int32_t P, int32_t* distance, int32_t* bag_blocks);
  * passed to spardl_block_topk / spardl_residual_add).  0 on invalid sizes. */
 size_t spardl_workspace_bytes(int32_t nworkers, int32_t P, int64_t n, int32_t k_blk);
 
-/* Prepares ws for calls with these sizes: clears the error word and the
- * level-1 histograms (one small fill kernel on `stream`).  Call it once after
+/* Prepares ws for calls with these sizes: clears the error word, the
+ * level-1 histograms, the final-index bitmap and the record of previous
+ * thresholds (one fill kernel on `stream`).  Call it once after
  * allocating ws, and again after any call left an error bit set.
  * Errors: EINVAL for NULL or misaligned ws or invalid sizes (as
  * spardl_workspace_bytes); ECAPACITY if ws_bytes is below

@@ -193,7 +193,12 @@ int spardl_workspace_init(int32_t nworkers, int32_t P, int64_t n, int32_t k_blk,
   if (ws_bytes < need) return SPARDL_ECAPACITY;
   const Layout L = make_layout(P, n, k_blk);
   Ws w = carve(ws, ws_bytes, L);
-  SPARDL_TRY(launch_fill(Fill().add(w.err, 64).add(w.hist1, L.units * HCOPIES * NB1).add(w.spec_t1, (int64_t)P * P).r,
+  SPARDL_TRY(launch_fill(Fill()
+                             .add(w.err, 64)
+                             .add(w.bitmap, ceil_div(n, 32))
+                             .add(w.hist1, L.units * HCOPIES * NB1)
+                             .add(w.spec_t1, (int64_t)P * P)
+                             .r,
                          stream));
   return SPARDL_OK;
 }
@@ -304,13 +309,15 @@ int spardl_residual_collect(float* acc, int64_t ld_acc, int32_t P, int64_t n, in
   const Layout L = make_layout(P, n, k_blk);
   if (ws_bytes < L.hist1) return SPARDL_ECAPACITY;
   Ws w = carve(ws, ws_bytes, L);
-  SPARDL_TRY(launch_bitmap(sp_idx, P, n, k_blk, w.bitmap, stream));
+  // the membership bitmap rests at zero between calls: mark I, update, clear
+  SPARDL_TRY(launch_bm_mark(sp_idx, P, n, k_blk, w.bitmap, true, stream));
   SPARDL_TRY(launch_grc_zero(acc, ld_acc, P, n, k_blk, local_idx, w.bitmap, stream));
   for (int32_t i = 1; i <= l; ++i) {
     const int32_t m = bag_of(P, l, i);
     SPARDL_TRY(launch_grc_drops(acc, ld_acc, n, m, k_blk, P * m, drop_idx[i - 1], drop_val[i - 1],
                                 drop_cnt[i - 1], w.bitmap, stream));
   }
+  SPARDL_TRY(launch_bm_mark(sp_idx, P, n, k_blk, w.bitmap, false, stream));
   return SPARDL_OK;
 }
 

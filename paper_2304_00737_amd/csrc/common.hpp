@@ -237,6 +237,62 @@ __device__ __forceinline__ int32_t wg_partition_point(int32_t lo, int32_t hi, Pr
   return lo;
 }
 
+// Two independent partition points found together: every round tests
+// blockDim points of each range, so both searches share their rounds of loads
+// and barriers.  `cnt` needs 2 (blockDim/64) words of LDS.
+template <typename Pred0, typename Pred1>
+__device__ __forceinline__ void wg_partition_point2(int32_t lo0, int32_t hi0, Pred0 pred0, int32_t lo1, int32_t hi1,
+                                                    Pred1 pred1, uint32_t* cnt, int32_t* r0, int32_t* r1) {
+  const int nt = blockDim.x;
+  const int nw = nt / WAVE;
+  auto probe = [&](int32_t lo, int32_t hi, int32_t* p, bool* active) {
+    const int32_t S = hi - lo;
+    if (S <= nt) {
+      *p = lo + (int32_t)threadIdx.x;
+      *active = (int32_t)threadIdx.x < S;
+    } else {
+      *p = lo + (int32_t)(((int64_t)S * (threadIdx.x + 1)) / (nt + 1));
+      *active = true;
+    }
+  };
+  auto narrow = [&](int32_t* lo, int32_t* hi, int32_t c) {
+    const int32_t S = *hi - *lo;
+    if (S <= nt) {
+      *lo += c;
+      *hi = *lo;
+    } else {
+      const int32_t new_lo = c == 0 ? *lo : *lo + (int32_t)(((int64_t)S * c) / (nt + 1)) + 1;
+      const int32_t new_hi = c == nt ? *hi : *lo + (int32_t)(((int64_t)S * (c + 1)) / (nt + 1));
+      *lo = new_lo;
+      *hi = new_hi;
+    }
+  };
+  while (hi0 > lo0 || hi1 > lo1) {
+    int32_t p0 = 0, p1 = 0;
+    bool a0 = false, a1 = false;
+    if (hi0 > lo0) probe(lo0, hi0, &p0, &a0);
+    if (hi1 > lo1) probe(lo1, hi1, &p1, &a1);
+    const bool t0 = a0 && pred0(p0);
+    const bool t1 = a1 && pred1(p1);
+    const uint64_t m0 = __ballot(t0), m1 = __ballot(t1);
+    if (lane_id() == 0) {
+      cnt[wave_id()] = popc64(m0);
+      cnt[nw + wave_id()] = popc64(m1);
+    }
+    __syncthreads();
+    int32_t c0 = 0, c1 = 0;
+    for (int i = 0; i < nw; ++i) {
+      c0 += (int32_t)cnt[i];
+      c1 += (int32_t)cnt[nw + i];
+    }
+    __syncthreads();
+    if (hi0 > lo0) narrow(&lo0, &hi0, c0);
+    if (hi1 > lo1) narrow(&lo1, &hi1, c1);
+  }
+  *r0 = lo0;
+  *r1 = lo1;
+}
+
 // First position j in [0, len) with a[j] >= x (len if none); a sorted ascending.
 __device__ __forceinline__ int32_t wg_lower_bound(const int32_t* __restrict__ a, int32_t len, int64_t x,
                                                   uint32_t* cnt) {

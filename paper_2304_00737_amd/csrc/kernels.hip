@@ -1441,7 +1441,7 @@ __global__ __launch_bounds__(MERGE_THREADS) void k_merge(
   __shared__ int32_t cI[MERGE_TILE + 3];
   __shared__ float cV[MERGE_TILE + 3];
   __shared__ __align__(16) uint32_t hist[NB1];
-  __shared__ uint32_t scratch[16];
+  __shared__ uint32_t scratch[2 * (MERGE_THREADS / WAVE) + 1];
   const uint32_t pair = blockIdx.x / (uint32_t)tiles_per_pair;
   const int32_t tile = (int32_t)(blockIdx.x % (uint32_t)tiles_per_pair);
   const uint32_t uP = (uint32_t)P;
@@ -1456,13 +1456,12 @@ __global__ __launch_bounds__(MERGE_THREADS) void k_merge(
   const int32_t Q1 = min(Q0 + MERGE_TILE, L2);
   // split(q) = number of held entries among the first q merged positions:
   // the first a in [max(0, q-kb), min(q, kb)) whose held entry does not go
-  // before received entry q-a-1 (held goes first on equal indices).
-  auto split = [&](int32_t q) {
-    return wg_partition_point(max(0, q - kb), min(q, kb),
-                              [&](int32_t a) { return Hi[a] <= Ri[q - a - 1]; }, scratch);
-  };
-  const int32_t a0 = split(Q0);
-  const int32_t a1 = split(Q1);
+  // before received entry q-a-1 (held goes first on equal indices).  The
+  // tile's two splits are searched together.
+  int32_t a0, a1;
+  wg_partition_point2(max(0, Q0 - kb), min(Q0, kb), [&](int32_t a) { return Hi[a] <= Ri[Q0 - a - 1]; },
+                      max(0, Q1 - kb), min(Q1, kb), [&](int32_t a) { return Hi[a] <= Ri[Q1 - a - 1]; }, scratch,
+                      &a0, &a1);
   const int32_t b0 = Q0 - a0, b1 = Q1 - a1;
   const int32_t nh = a1 - a0, nr = b1 - b0;
   int32_t* hI = cI;
@@ -1547,19 +1546,25 @@ __global__ __launch_bounds__(MERGE_THREADS) void k_merge(
       }
     }
   }
+  // the scan's barriers put every thread past its merge loop, so the tile is
+  // staged in the (now free) input buffer and written out coalesced
   uint32_t tot;
   uint32_t pos = block_excl_scan(cnt, scratch, &tot);
   if (threadIdx.x == 0) slot_cnt[(int64_t)pair * tiles_per_pair + tile] = tot;
-  const int64_t ubase = (int64_t)pair * tiles_per_pair * MERGE_TILE + Q0;
 #pragma unroll
   for (int k = 0; k < MERGE_PER_THREAD; ++k) {
     if (eok[k]) {
-      U_idx[ubase + pos] = ei[k];
-      U_val[ubase + pos] = ev[k];
+      cI[pos] = ei[k];
+      cV[pos] = ev[k];
       ++pos;
     }
   }
   __syncthreads();
+  const int64_t ubase = (int64_t)pair * tiles_per_pair * MERGE_TILE + Q0;
+  for (uint32_t k = threadIdx.x; k < tot; k += blockDim.x) {
+    U_idx[ubase + k] = cI[k];
+    U_val[ubase + k] = cV[k];
+  }
   flush_hist(hist, hist1 + (int64_t)pair * NB1);
 }
 
@@ -1606,32 +1611,21 @@ __global__ __launch_bounds__(256) void k_densify(const int32_t* __restrict__ sp_
 }
 
 // ============================================================================ a6: residual collection
-// Membership bitmap of the final index set I, one 32-bit word per 32 indices,
-// built tile by tile without atomics on global memory.
-__global__ __launch_bounds__(256) void k_bitmap(const int32_t* __restrict__ sp_idx, Blocks B,
-                                                int32_t kb, uint32_t* __restrict__ bm) {
-  constexpr int WORDS = DENSE_TILE / 32;
-  __shared__ uint32_t words[WORDS];
-  __shared__ uint32_t cnt[8];
-  const int64_t n = B.n;
-  const int64_t t0 = (int64_t)blockIdx.x * DENSE_TILE;
-  const int64_t t1 = min(t0 + DENSE_TILE, n);
-  for (int i = threadIdx.x; i < WORDS; i += blockDim.x) words[i] = 0u;
-  const uint32_t blo = B.of((uint32_t)t0), bhi = B.of((uint32_t)(t1 - 1));
-  for (uint32_t b = blo; b <= bhi; ++b) {
-    const int32_t* Fi = sp_idx + ((int64_t)b * B.P + b) * kb;
-    const int32_t jlo = wg_lower_bound(Fi, kb, t0, cnt);
-    const int32_t jhi = wg_lower_bound(Fi, kb, t1, cnt);
-    for (int32_t j = jlo + (int32_t)threadIdx.x; j < jhi; j += blockDim.x) {
-      const int64_t r = (int64_t)Fi[j] - t0;
-      if (r >= 0 && r < DENSE_TILE) atomicOr(&words[r >> 5], 1u << (r & 31));
+// Membership bitmap of the final index set I, one bit per index.  The
+// workspace keeps it at zero between steps: one thread per final entry sets
+// its bit before the residual updates and clears the word afterwards.
+__global__ __launch_bounds__(256) void k_bm_mark(const int32_t* __restrict__ sp_idx, uint32_t P, uint32_t n,
+                                                 uint32_t kb, uint32_t* __restrict__ bm, int set) {
+  const uint32_t per_b = kb;
+  for (uint32_t b = blockIdx.y; b < P; b += gridDim.y) {
+    const int32_t* __restrict__ F = sp_idx + ((int64_t)b * P + b) * kb;
+    for (uint32_t j = blockIdx.x * 256u + threadIdx.x; j < per_b; j += gridDim.x * 256u) {
+      const int32_t x = F[j];
+      if (x >= 0 && (uint32_t)x < n) {
+        if (set) atomicOr(&bm[(uint32_t)x >> 5], 1u << ((uint32_t)x & 31u));
+        else bm[(uint32_t)x >> 5] = 0u;
+      }
     }
-  }
-  __syncthreads();
-  const int64_t nw = (n + 31) / 32;
-  for (int i = threadIdx.x; i < WORDS; i += blockDim.x) {
-    const int64_t wi = t0 / 32 + i;
-    if (wi < nw) bm[wi] = words[i];
   }
 }
 
@@ -1786,10 +1780,10 @@ hipError_t launch_densify(const int32_t* sp_idx, const float* sp_val, int32_t P,
   return hipGetLastError();
 }
 
-hipError_t launch_bitmap(const int32_t* sp_idx, int32_t P, int64_t n, int32_t kb, uint32_t* bm,
-                         hipStream_t s) {
-  const dim3 grid((unsigned)((n + DENSE_TILE - 1) / DENSE_TILE));
-  hipLaunchKernelGGL(k_bitmap, grid, dim3(256), 0, s, sp_idx, make_blocks(n, P), kb, bm);
+hipError_t launch_bm_mark(const int32_t* sp_idx, int32_t P, int64_t n, int32_t kb, uint32_t* bm, bool set,
+                          hipStream_t s) {
+  const dim3 grid(grid_for(kb, 256, 1024), (unsigned)std::min<int32_t>(P, 65535));
+  hipLaunchKernelGGL(k_bm_mark, grid, dim3(256), 0, s, sp_idx, (uint32_t)P, (uint32_t)n, (uint32_t)kb, bm, set ? 1 : 0);
   return hipGetLastError();
 }
 
