@@ -40,7 +40,7 @@ struct Layout {
   size_t err = 0, bitmap = 0, hist1 = 0, spec_t1 = 0, spec_used = 0, spec_cnt = 0, state = 0, slot_cnt = 0,
          slot_nbin = 0, pre_all = 0, pre_ge = 0, pre_eq = 0;
   size_t fixed_end = 0;
-  int64_t units = 0, tiles_tk = 0, groups_tk = 0, tiles_mg = 0, slot_n = 0, pairs_max = 0, add_tiles = 0;
+  int64_t units = 0, tiles_tk = 0, tiles_mg = 0, slot_n = 0, pairs_max = 0, add_tiles = 0;
 };
 
 Layout make_layout(int32_t P, int64_t n, int32_t kb) {
@@ -52,7 +52,6 @@ Layout make_layout(int32_t P, int64_t n, int32_t kb) {
   L.pairs_max = (int64_t)P * mmax;
   L.units = std::max<int64_t>((int64_t)P * P, L.pairs_max);
   L.tiles_tk = ceil_div(maxlen, SLOT);
-  L.groups_tk = ceil_div(L.tiles_tk, EMIT_GROUP_TK);
   L.tiles_mg = ceil_div(2ll * kb, MERGE_TILE);
   L.slot_n = std::max<int64_t>((int64_t)P * P * L.tiles_tk, L.pairs_max * L.tiles_mg);
   size_t off = 256;
@@ -245,7 +244,7 @@ int spardl_block_topk(const float* acc, int64_t ld_acc, int32_t nworkers, int64_
   Ws w = carve(ws, ws_bytes, L);
   const int64_t units = (int64_t)nworkers * P;
   const bool v4 = aligned16(acc) && ld_acc % 4 == 0 && blocks_vec4(n, P);
-  const int32_t smax = (int32_t)L.tiles_tk, gmax = (int32_t)L.groups_tk;
+  const int32_t smax = (int32_t)L.tiles_tk;
   if (!(flags & SPARDL_TOPK_HIST_READY)) {
     SPARDL_TRY(launch_fill(Fill().add(w.hist1, units * HCOPIES * NB1).r, stream));
     SPARDL_TRY(launch_hist1(acc, ld_acc, nworkers, n, P, v4, w.hist1, stream));
@@ -257,9 +256,8 @@ int spardl_block_topk(const float* acc, int64_t ld_acc, int32_t nworkers, int64_
                             w.slot_cnt, w.slot_nbin, w.cand_idx, w.cand_val, w.bin_key, stream));
   SPARDL_TRY(launch_thresh(0, units, n, P, k_blk, smax, 1, nullptr, w.cand_val, w.state, w.slot_cnt, w.slot_nbin,
                            w.bin_key, w.pre_all, w.pre_ge, w.pre_eq, nullptr, w.err, stream));
-  SPARDL_TRY(launch_emit(0, w.cand_idx, w.cand_val, units, n, P, k_blk, 1, smax, EMIT_GROUP_TK, gmax, w.state,
-                         w.slot_cnt, w.pre_all, w.pre_ge, w.pre_eq, sp_idx, sp_val, local_idx, nullptr, nullptr,
-                         w.err, stream));
+  SPARDL_TRY(launch_emit(0, w.cand_idx, w.cand_val, units, n, P, k_blk, 1, smax, w.state, w.slot_cnt, w.pre_all,
+                         w.pre_ge, w.pre_eq, sp_idx, sp_val, local_idx, nullptr, nullptr, w.err, stream));
   return SPARDL_OK;
 }
 
@@ -282,9 +280,8 @@ int spardl_sparse_merge_topk(int32_t* sp_idx, float* sp_val, int32_t P, int64_t 
                           stream));
   SPARDL_TRY(launch_thresh(1, pairs, n, P, k_blk, smax, 1, w.hist1, w.cand_val, w.state, w.slot_cnt, w.slot_nbin,
                            w.bin_key, w.pre_all, w.pre_ge, w.pre_eq, drop_cnt, w.err, stream));
-  SPARDL_TRY(launch_emit(1, w.cand_idx, w.cand_val, pairs, n, P, k_blk, m, smax, 1, smax, w.state, w.slot_cnt,
-                         w.pre_all, w.pre_ge, w.pre_eq, sp_idx, sp_val, nullptr, drop_idx, drop_val, w.err,
-                         stream));
+  SPARDL_TRY(launch_emit(1, w.cand_idx, w.cand_val, pairs, n, P, k_blk, m, smax, w.state, w.slot_cnt, w.pre_all,
+                         w.pre_ge, w.pre_eq, sp_idx, sp_val, nullptr, drop_idx, drop_val, w.err, stream));
   return SPARDL_OK;
 }
 

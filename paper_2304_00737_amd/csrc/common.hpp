@@ -23,9 +23,6 @@ constexpr int WAVE = 64;
 constexpr int ADD_F4 = 2;                        // float4 per lane per array in the residual add
 constexpr int ADD_TILE = 256 * ADD_F4 * 4;       // elements per residual-add workgroup
 constexpr int SLOT = 4096;                       // elements per candidate slot (one collect workgroup)
-constexpr int EMIT_GROUP_TK = 16;                // slots per emit workgroup, block top-k
-constexpr int EMIT_J = 16;                       // entries per thread per emit chunk
-constexpr int EMIT_CHUNK = 256 * EMIT_J;
 constexpr int MERGE_THREADS = 256;
 constexpr int MERGE_PER_THREAD = 16;
 constexpr int MERGE_TILE = MERGE_THREADS * MERGE_PER_THREAD;   // merged positions per workgroup

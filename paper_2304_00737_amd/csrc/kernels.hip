@@ -1296,55 +1296,43 @@ __global__ __launch_bounds__(1024) void k_thresh(Blocks B, int32_t kb, int32_t s
 }
 
 // ============================================================================ ordered emit
-// One workgroup per group of G consecutive slots.  An entry is selected if its
-// key is >= TGE, or equals TEQ and fewer than NEEDEQ equal keys precede it, so
-// the number of selected entries before an entry is
+// An entry is selected if its key is >= TGE, or equals TEQ and fewer than
+// NEEDEQ equal keys precede it, so the number of selected entries before an
+// entry is
 //   (#ge before it) + min(#eq before it, NEEDEQ),
-// with the counts before the group taken from the per-slot prefixes.
-// Unselected entries of a merge go to the drop list at
-// (#entries before) - (#selected before).
-// MODE 0 (block top-k): selected -> sp (and local_idx).  MODE 1 (merge):
-// selected -> sp[w][b] in place, the rest -> the step's drop lists.
+// with the counts before the slot taken from the per-slot prefixes of the
+// threshold stage and those inside it from wave ballots.  Unselected entries
+// of a merge go to the drop list at (#entries before) - (#selected before).
+// MODE 0 (block top-k): few candidates per slot, one wave per slot, no LDS
+// and no barrier; selected -> sp (and local_idx).  MODE 1 (merge): slots are
+// full merge tiles, so a workgroup takes one slot and each wave a quarter of
+// it, the counts of the quarters before it exchanged through LDS; selected ->
+// sp[w][b] in place, the rest -> the step's drop lists.
+constexpr int EMIT_R = 4;   // entries per lane per chunk
 template <int MODE>
 __global__ __launch_bounds__(256) void k_emit(
     const int32_t* __restrict__ cand_idx, const float* __restrict__ cand_val, Blocks B,
-    int32_t kb, int32_t m, int32_t smax, int32_t G, int32_t gmax, const uint32_t* __restrict__ state,
+    int32_t kb, int32_t m, int32_t smax, uint32_t gq, const uint32_t* __restrict__ state,
     const uint32_t* __restrict__ slot_cnt, const uint32_t* __restrict__ pre_all,
     const uint32_t* __restrict__ pre_ge, const uint32_t* __restrict__ pre_eq, int32_t* __restrict__ out_idx,
     float* __restrict__ out_val, int32_t* __restrict__ local_idx, int32_t* __restrict__ drop_idx,
     float* __restrict__ drop_val, uint32_t* __restrict__ err) {
-  constexpr int NT = 256, NWV = NT / WAVE, NJ = EMIT_J;
-  __shared__ uint32_t pre[EMIT_GROUP_TK + 1];
-  __shared__ uint32_t cge[NJ * NWV], ceq[NJ * NWV];
-  __shared__ uint32_t sh[2];
-  const uint32_t unit = blockIdx.x / (uint32_t)gmax;
-  const int32_t grp = (int32_t)(blockIdx.x % (uint32_t)gmax);
+  constexpr int NPART = MODE == 0 ? 1 : 4;   // waves sharing one slot
+  const uint32_t unit = blockIdx.x / gq;
+  const int wv = wave_id();
+  const int32_t slot = NPART == 1 ? (int32_t)((blockIdx.x % gq) * 4u + (uint32_t)wv) : (int32_t)(blockIdx.x % gq);
   const SlotGeom g = slot_geom(MODE, unit, B, kb);
-  const int32_t s_lo = grp * G;
-  if (s_lo >= g.nslots) return;
-  const int32_t ns = min(G, g.nslots - s_lo);
-  const uint32_t* __restrict__ cnt = slot_cnt + (int64_t)unit * smax;
-  const int lane = lane_id(), wv = wave_id();
-  if (wv == 0) {   // exclusive prefix of the group's slot counts
-    const uint32_t c = lane < ns ? min(cnt[s_lo + lane], (uint32_t)g.ss) : 0u;
-    const uint32_t ci = wave_incl_scan(c);
-    if (lane <= ns) pre[lane] = ci - c;
-  }
-  __syncthreads();
-  const uint32_t E = pre[ns];
-  if (E == 0) return;
+  if (slot >= g.nslots) return;   // uniform over the workgroup when NPART > 1
+  const int lane = lane_id();
+  const uint64_t lt = __lanemask_lt();
+  const int64_t si = (int64_t)unit * smax + slot;
   const uint32_t* st = state + (int64_t)unit * ST_WORDS;
-  const uint32_t tge = st[ST_TGE], teq = st[ST_TEQ], need_eq = st[ST_NEEDEQ];
-  const int64_t si = (int64_t)unit * smax + s_lo;
+  // independent loads: the slot's count and prefixes, the unit's threshold
+  const uint32_t cnt = min(slot_cnt[si], (uint32_t)g.ss);
   const uint32_t all_before = pre_all[si];
   uint32_t run_g = pre_ge[si], run_e = pre_eq[si];
-  auto addr = [&](uint32_t p) -> int64_t {   // entry p of the group (index order) -> address
-    int32_t lo = 0;
-#pragma unroll
-    for (int step = EMIT_GROUP_TK / 2; step >= 1; step >>= 1)
-      if (lo + step < ns && pre[lo + step] <= p) lo += step;
-    return g.base + (int64_t)(s_lo + lo) * g.ss + (p - pre[lo]);
-  };
+  const uint32_t tge = st[ST_TGE], teq = st[ST_TEQ], need_eq = st[ST_NEEDEQ];
+  const int64_t base = g.base + (int64_t)slot * g.ss;
   int64_t o;
   if (MODE == 0) {
     o = (int64_t)unit * kb;
@@ -1352,77 +1340,76 @@ __global__ __launch_bounds__(256) void k_emit(
     const uint32_t w = unit / (uint32_t)m, t = unit % (uint32_t)m, b = (w + t) % B.P;
     o = ((int64_t)w * B.P + b) * kb;
   }
-  const uint64_t lt = __lanemask_lt();
-  for (uint32_t c0 = 0; c0 < E; c0 += EMIT_CHUNK) {
-    int32_t ix[NJ];
-    float vx[NJ];
-    uint64_t mg[NJ], me[NJ];
-#pragma unroll
-    for (int j = 0; j < NJ; ++j) {
-      const uint32_t p = c0 + j * NT + threadIdx.x;
-      ix[j] = -1;
-      vx[j] = 0.f;
-      if (p < E) {
-        const int64_t a = addr(p);
-        ix[j] = cand_idx[a];
-        vx[j] = cand_val[a];
-      }
+  uint32_t p_lo = 0, p_hi = cnt;
+  if constexpr (NPART > 1) {
+    // this wave's quarter of the slot; add the ge / eq counts of the quarters before it
+    __shared__ uint32_t part_cnt[2 * NPART];
+    const uint32_t qlen = ((uint32_t)g.ss + NPART - 1) / NPART;
+    p_lo = min(cnt, (uint32_t)wv * qlen);
+    p_hi = min(cnt, p_lo + qlen);
+    uint32_t cg = 0, ce = 0;
+    for (uint32_t p0 = p_lo; p0 < p_hi; p0 += WAVE) {   // wave-uniform trip count
+      const uint32_t p = p0 + lane;
+      const uint32_t key = p < p_hi ? mag_key(cand_val[base + p]) : 0u;
+      cg += popc64(__ballot(p < p_hi && key >= tge));
+      ce += popc64(__ballot(p < p_hi && need_eq != 0u && key == teq));
     }
-#pragma unroll
-    for (int j = 0; j < NJ; ++j) {
-      const uint32_t p = c0 + j * NT + threadIdx.x;
-      const uint32_t key = mag_key(vx[j]);
-      mg[j] = __ballot(p < E && key >= tge);
-      me[j] = __ballot(p < E && need_eq != 0u && key == teq);
-      if (lane == 0) {
-        cge[j * NWV + wv] = popc64(mg[j]);
-        ceq[j * NWV + wv] = popc64(me[j]);
-      }
+    if (lane == 0) {
+      part_cnt[2 * wv] = cg;
+      part_cnt[2 * wv + 1] = ce;
     }
     __syncthreads();
-    if (wv == 0) {   // exclusive scan over (j, wave) in j-major order: one entry per lane
-      const uint32_t gv = cge[lane], ev = ceq[lane];
-      const uint32_t gi = wave_incl_scan(gv), ei = wave_incl_scan(ev);
-      cge[lane] = gi - gv;
-      ceq[lane] = ei - ev;
-      if (lane == WAVE - 1) {
-        sh[0] = gi;
-        sh[1] = ei;
+    for (int k = 0; k < wv; ++k) {
+      run_g += part_cnt[2 * k];
+      run_e += part_cnt[2 * k + 1];
+    }
+  }
+  for (uint32_t e0 = p_lo; e0 < p_hi; e0 += WAVE * EMIT_R) {
+    int32_t ix[EMIT_R];
+    float vx[EMIT_R];
+#pragma unroll
+    for (int r = 0; r < EMIT_R; ++r) {
+      const uint32_t p = e0 + r * WAVE + lane;
+      ix[r] = -1;
+      vx[r] = 0.f;
+      if (p < p_hi) {
+        ix[r] = cand_idx[base + p];
+        vx[r] = cand_val[base + p];
       }
     }
-    __syncthreads();
 #pragma unroll
-    for (int j = 0; j < NJ; ++j) {
-      const uint32_t p = c0 + j * NT + threadIdx.x;
-      if (p < E) {
-        const uint32_t ge_pre = run_g + cge[j * NWV + wv] + popc64(mg[j] & lt);
-        const uint32_t eq_pre = run_e + ceq[j * NWV + wv] + popc64(me[j] & lt);
-        const bool is_ge = (mg[j] >> lane) & 1ull;
-        const bool is_eq = (me[j] >> lane) & 1ull;
+    for (int r = 0; r < EMIT_R; ++r) {
+      const uint32_t p = e0 + r * WAVE + lane;
+      const uint32_t key = mag_key(vx[r]);
+      const bool is_ge = p < p_hi && key >= tge;
+      const bool is_eq = p < p_hi && need_eq != 0u && key == teq;
+      const uint64_t mg = __ballot(is_ge), me = __ballot(is_eq);
+      if (p < p_hi) {
+        const uint32_t ge_pre = run_g + popc64(mg & lt);
+        const uint32_t eq_pre = run_e + popc64(me & lt);
         const uint32_t sel_before = ge_pre + (eq_pre < need_eq ? eq_pre : need_eq);
         const bool sel = is_ge || (is_eq && eq_pre < need_eq);
         if (sel) {
           if (sel_before < (uint32_t)kb) {
-            out_idx[o + sel_before] = ix[j];
-            out_val[o + sel_before] = vx[j];
-            if (MODE == 0 && local_idx) local_idx[o + sel_before] = ix[j];
+            out_idx[o + sel_before] = ix[r];
+            out_val[o + sel_before] = vx[r];
+            if (MODE == 0 && local_idx) local_idx[o + sel_before] = ix[r];
           } else {
             atomicOr(err, ERR_COUNT_POS);
           }
         } else if (MODE == 1) {
           const uint32_t dpos = all_before + p - sel_before;
           if (dpos < (uint32_t)kb) {
-            drop_idx[(int64_t)unit * kb + dpos] = ix[j];
-            drop_val[(int64_t)unit * kb + dpos] = vx[j];
+            drop_idx[(int64_t)unit * kb + dpos] = ix[r];
+            drop_val[(int64_t)unit * kb + dpos] = vx[r];
           } else {
             atomicOr(err, ERR_COUNT_DROP);
           }
         }
       }
+      run_g += popc64(mg);
+      run_e += popc64(me);
     }
-    run_g += sh[0];
-    run_e += sh[1];
-    __syncthreads();
   }
 }
 
@@ -1751,15 +1738,18 @@ hipError_t launch_thresh(int mode, int64_t nunits, int64_t n, int32_t P, int32_t
 }
 
 hipError_t launch_emit(int mode, const int32_t* cand_idx, const float* cand_val, int64_t nunits, int64_t n,
-                       int32_t P, int32_t kb, int32_t m, int32_t smax, int32_t G, int32_t gmax,
-                       const uint32_t* state, const uint32_t* slot_cnt, const uint32_t* pre_all,
-                       const uint32_t* pre_ge, const uint32_t* pre_eq, int32_t* out_idx, float* out_val,
-                       int32_t* local_idx, int32_t* drop_idx, float* drop_val, uint32_t* err, hipStream_t s) {
-  const dim3 grid((unsigned)(nunits * gmax));
+                       int32_t P, int32_t kb, int32_t m, int32_t smax, const uint32_t* state,
+                       const uint32_t* slot_cnt, const uint32_t* pre_all, const uint32_t* pre_ge,
+                       const uint32_t* pre_eq, int32_t* out_idx, float* out_val, int32_t* local_idx,
+                       int32_t* drop_idx, float* drop_val, uint32_t* err, hipStream_t s) {
+  // block top-k: four slots (one per wave) per workgroup; merge: one slot per workgroup
+  const uint32_t gq = mode == 0 ? (uint32_t)((smax + 3) / 4) : (uint32_t)smax;
+  const dim3 grid((unsigned)(nunits * gq));
+  const Blocks B = make_blocks(n, P);
   if (mode == 0)
-    hipLaunchKernelGGL(k_emit<0>, grid, dim3(256), 0, s, cand_idx, cand_val, make_blocks(n, P), kb, m, smax, G, gmax, state, slot_cnt, pre_all, pre_ge, pre_eq, out_idx, out_val, local_idx, drop_idx, drop_val, err);
+    hipLaunchKernelGGL(k_emit<0>, grid, dim3(256), 0, s, cand_idx, cand_val, B, kb, m, smax, gq, state, slot_cnt, pre_all, pre_ge, pre_eq, out_idx, out_val, local_idx, drop_idx, drop_val, err);
   else
-    hipLaunchKernelGGL(k_emit<1>, grid, dim3(256), 0, s, cand_idx, cand_val, make_blocks(n, P), kb, m, smax, G, gmax, state, slot_cnt, pre_all, pre_ge, pre_eq, out_idx, out_val, local_idx, drop_idx, drop_val, err);
+    hipLaunchKernelGGL(k_emit<1>, grid, dim3(256), 0, s, cand_idx, cand_val, B, kb, m, smax, gq, state, slot_cnt, pre_all, pre_ge, pre_eq, out_idx, out_val, local_idx, drop_idx, drop_val, err);
   return hipGetLastError();
 }
 

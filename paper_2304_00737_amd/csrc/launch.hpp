@@ -41,10 +41,10 @@ hipError_t launch_thresh(int mode, int64_t nunits, int64_t n, int32_t P, int32_t
                          const uint32_t* slot_nbin, const uint32_t* bin_key, uint32_t* pre_all, uint32_t* pre_ge,
                          uint32_t* pre_eq, int32_t* drop_cnt, uint32_t* err, hipStream_t s);
 hipError_t launch_emit(int mode, const int32_t* cand_idx, const float* cand_val, int64_t nunits, int64_t n,
-                       int32_t P, int32_t kb, int32_t m, int32_t smax, int32_t G, int32_t gmax,
-                       const uint32_t* state, const uint32_t* slot_cnt, const uint32_t* pre_all,
-                       const uint32_t* pre_ge, const uint32_t* pre_eq, int32_t* out_idx, float* out_val,
-                       int32_t* local_idx, int32_t* drop_idx, float* drop_val, uint32_t* err, hipStream_t s);
+                       int32_t P, int32_t kb, int32_t m, int32_t smax, const uint32_t* state,
+                       const uint32_t* slot_cnt, const uint32_t* pre_all, const uint32_t* pre_ge,
+                       const uint32_t* pre_eq, int32_t* out_idx, float* out_val, int32_t* local_idx,
+                       int32_t* drop_idx, float* drop_val, uint32_t* err, hipStream_t s);
 hipError_t launch_merge(const int32_t* sp_idx, const float* sp_val, int32_t P, int32_t kb, int32_t d, int32_t m,
                         int32_t tiles_per_pair, uint32_t* hist1, uint32_t* slot_cnt, int32_t* U_idx,
                         float* U_val, hipStream_t s);
