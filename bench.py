@@ -213,13 +213,14 @@ def main() -> int:
     alg = {
         "residual_add": 12.0 * P * n,                              # read G, read xi, write A
         "block_topk": 4.0 * P * n + 12.0 * P * P * kb,             # read A; write idx, val, local idx
-        "allgather_densify": 4.0 * n + 8.0 * P * kb,               # write u; read the final blocks
+        "allgather_densify": 4.0 * n + n / 8.0 + 8.0 * P * kb,     # write u and the bitmap of I; read the final blocks
     }
     for i, pc in enumerate(pairs, start=1):
         alg[f"merge_step{i}"] = 32.0 * pc * kb                     # read held + received, write kept + dropped
     drops_total = float(sum(int(d.sum()) for d in dc))
-    # read local idx, final idx, drop lists; read+write touched residual entries (upper bound)
-    alg["residual_collect"] = 4.0 * P * P * kb + 4.0 * P * kb + 8.0 * drops_total + 8.0 * (P * P * kb + drops_total)
+    # read local idx and drop lists; read+write touched residual entries (upper bound); the
+    # membership lookups hit the bitmap of I that densify wrote (n/8 bytes, cache resident)
+    alg["residual_collect"] = 4.0 * P * P * kb + 8.0 * drops_total + 8.0 * (P * P * kb + drops_total)
     dominant = max(calls, key=lambda c: per_call_ms[c])
     dom_ms = add_ms if dominant == "residual_add" else per_call_ms[dominant]
     achieved = alg[dominant] / (dom_ms * 1e-3) / 1e9

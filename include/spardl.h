@@ -156,10 +156,15 @@ int spardl_sparse_merge_topk(int32_t* sp_idx, float* sp_val, int32_t P, int64_t 
  * one device is the identity.  Writes the dense update once:
  *   dense[x] = value of x in the final block containing x, if x is there;
  *   dense[x] = +0.0f otherwise;     for x < n.
- * Errors: EINVAL for NULL pointers, P < 1, n < P, n >= 2^31, k_blk out of
- * [1, floor(n/P)]. */
+ * member (optional, may be NULL; 4-byte aligned, ceil(n/32) words, caller
+ * owned) receives the membership bitmap of the final index set I: bit
+ * (x & 31) of word (x >> 5) is 1 iff x is in I; every word is written, bits
+ * at or above n are 0.  spardl_residual_collect can take it in place of
+ * building I itself.
+ * Errors: EINVAL for NULL sp/dense, misaligned member, P < 1, n < P,
+ * n >= 2^31, k_blk out of [1, floor(n/P)]. */
 int spardl_allgather_densify(const int32_t* sp_idx, const float* sp_val, int32_t P, int64_t n,
-                             int32_t k_blk, float* dense, hipStream_t stream);
+                             int32_t k_blk, float* dense, uint32_t* member, hipStream_t stream);
 
 /* Global residual collection (Sec. III-C, Algorithm 1).  Let I be the set of
  * indices in the final blocks sp[b][b], b < P.  For every worker w < P (row w
@@ -170,13 +175,19 @@ int spardl_allgather_densify(const int32_t* sp_idx, const float* sp_val, int32_t
  *                              x in I, steps 1..l in that order;
  *   other entries keep A_w    (local and end-procedure residuals).
  * The result is xi^t_w, the residual for the next iteration.
+ * I is read from member when it is given (the bitmap spardl_allgather_densify
+ * wrote for the same final blocks; sp_idx and ws are then unused and may be
+ * NULL), else built from sp_idx in the workspace's bitmap, which is left at
+ * zero again.
  * drop_idx/drop_val/drop_cnt are HOST arrays of l DEVICE pointers (element
  * i-1 = the buffers passed to spardl_sparse_merge_topk for step i); they may
  * be NULL when P = 1.
- * Errors: EINVAL for NULL pointers, P < 1, n < P, n >= 2^31, ld_acc < n,
- * k_blk out of [1, floor(n/P)]; ECAPACITY if ws is too small. */
+ * Errors: EINVAL for NULL acc/local_idx, NULL sp_idx or ws (or a ws not
+ * 256-byte aligned) without member, misaligned member, P < 1, n < P,
+ * n >= 2^31, ld_acc < n, k_blk out of [1, floor(n/P)]; ECAPACITY if ws is
+ * too small. */
 int spardl_residual_collect(float* acc, int64_t ld_acc, int32_t P, int64_t n, int32_t k_blk,
-                            const int32_t* local_idx, const int32_t* sp_idx,
+                            const int32_t* local_idx, const int32_t* sp_idx, const uint32_t* member,
                             const int32_t* const* drop_idx, const float* const* drop_val,
                             const int32_t* const* drop_cnt, void* ws, size_t ws_bytes,
                             hipStream_t stream);

@@ -286,35 +286,41 @@ int spardl_sparse_merge_topk(int32_t* sp_idx, float* sp_val, int32_t P, int64_t 
 }
 
 int spardl_allgather_densify(const int32_t* sp_idx, const float* sp_val, int32_t P, int64_t n,
-                             int32_t k_blk, float* dense, hipStream_t stream) {
+                             int32_t k_blk, float* dense, uint32_t* member, hipStream_t stream) {
   if (!sp_idx || !sp_val || !dense || !sizes_ok(P, n, k_blk)) return SPARDL_EINVAL;
-  SPARDL_TRY(launch_densify(sp_idx, sp_val, P, n, k_blk, dense, aligned16(dense), stream));
+  if (member && (reinterpret_cast<uintptr_t>(member) & 3u)) return SPARDL_EINVAL;
+  SPARDL_TRY(launch_densify(sp_idx, sp_val, P, n, k_blk, dense, member, aligned16(dense), stream));
   return SPARDL_OK;
 }
 
 int spardl_residual_collect(float* acc, int64_t ld_acc, int32_t P, int64_t n, int32_t k_blk,
-                            const int32_t* local_idx, const int32_t* sp_idx,
+                            const int32_t* local_idx, const int32_t* sp_idx, const uint32_t* member,
                             const int32_t* const* drop_idx, const float* const* drop_val,
                             const int32_t* const* drop_cnt, void* ws, size_t ws_bytes,
                             hipStream_t stream) {
-  if (!acc || !local_idx || !sp_idx || !ws || ws_misaligned(ws) || !sizes_ok(P, n, k_blk) || ld_acc < n)
+  if (!acc || !local_idx || !sizes_ok(P, n, k_blk) || ld_acc < n) return SPARDL_EINVAL;
+  if (member ? (reinterpret_cast<uintptr_t>(member) & 3u) != 0u : (!sp_idx || !ws || ws_misaligned(ws)))
     return SPARDL_EINVAL;
   const int32_t l = steps_of(P);
   if (l > 0 && (!drop_idx || !drop_val || !drop_cnt)) return SPARDL_EINVAL;
   for (int32_t i = 0; i < l; ++i)
     if (!drop_idx[i] || !drop_val[i] || !drop_cnt[i]) return SPARDL_EINVAL;
-  const Layout L = make_layout(P, n, k_blk);
-  if (ws_bytes < L.hist1) return SPARDL_ECAPACITY;
-  Ws w = carve(ws, ws_bytes, L);
-  // the membership bitmap rests at zero between calls: mark I, update, clear
-  SPARDL_TRY(launch_bm_mark(sp_idx, P, n, k_blk, w.bitmap, true, stream));
-  SPARDL_TRY(launch_grc_zero(acc, ld_acc, P, n, k_blk, local_idx, w.bitmap, stream));
+  uint32_t* bm = nullptr;
+  if (!member) {
+    const Layout L = make_layout(P, n, k_blk);
+    if (ws_bytes < L.hist1) return SPARDL_ECAPACITY;
+    bm = carve(ws, ws_bytes, L).bitmap;
+    // the workspace bitmap rests at zero between calls: mark I, update, clear
+    SPARDL_TRY(launch_bm_mark(sp_idx, P, n, k_blk, bm, true, stream));
+  }
+  const uint32_t* in_I = member ? member : bm;
+  SPARDL_TRY(launch_grc_zero(acc, ld_acc, P, n, k_blk, local_idx, in_I, stream));
   for (int32_t i = 1; i <= l; ++i) {
     const int32_t m = bag_of(P, l, i);
     SPARDL_TRY(launch_grc_drops(acc, ld_acc, n, m, k_blk, P * m, drop_idx[i - 1], drop_val[i - 1],
-                                drop_cnt[i - 1], w.bitmap, stream));
+                                drop_cnt[i - 1], in_I, stream));
   }
-  SPARDL_TRY(launch_bm_mark(sp_idx, P, n, k_blk, w.bitmap, false, stream));
+  if (!member) SPARDL_TRY(launch_bm_mark(sp_idx, P, n, k_blk, bm, false, stream));
   return SPARDL_OK;
 }
 

@@ -1557,30 +1557,44 @@ __global__ __launch_bounds__(MERGE_THREADS) void k_merge(
 
 // ============================================================================ a5: all-gather + densify
 // Tile [t0, t0 + DENSE_TILE) of the output is assembled in LDS: zeros, then
-// the final entries whose index falls in the tile (found by binary search in
-// the index-sorted final blocks sp[b][b]), then streamed out.
+// the final entries whose index falls in the tile (both ends found by one
+// joint binary search in the index-sorted final blocks sp[b][b]), then
+// streamed out.  With `member`, the tile's words of the membership bitmap of
+// the final index set I are written as well (bit x & 31 of word x >> 5 set
+// iff x is in I), every word of [0, ceil(n/32)) exactly once.
 template <int VEC>
 __global__ __launch_bounds__(256) void k_densify(const int32_t* __restrict__ sp_idx,
                                                  const float* __restrict__ sp_val, Blocks B,
-                                                 int32_t kb, float* __restrict__ dense) {
+                                                 int32_t kb, float* __restrict__ dense,
+                                                 uint32_t* __restrict__ member) {
+  static_assert(DENSE_TILE % 32 == 0 && DENSE_TILE / 32 <= 256, "one bitmap word per thread");
   __shared__ float tileb[DENSE_TILE];
+  __shared__ uint32_t bits[DENSE_TILE / 32];
   __shared__ uint32_t cnt[8];
   const int64_t n = B.n;
   const int64_t t0 = (int64_t)blockIdx.x * DENSE_TILE;
   const int64_t t1 = min(t0 + DENSE_TILE, n);
   for (int i = threadIdx.x; i < DENSE_TILE; i += blockDim.x) tileb[i] = 0.f;
+  if (threadIdx.x < DENSE_TILE / 32) bits[threadIdx.x] = 0u;
   const uint32_t blo = B.of((uint32_t)t0), bhi = B.of((uint32_t)(t1 - 1));
   for (uint32_t b = blo; b <= bhi; ++b) {
     const int32_t* Fi = sp_idx + ((int64_t)b * B.P + b) * kb;
     const float* Fv = sp_val + ((int64_t)b * B.P + b) * kb;
-    const int32_t jlo = wg_lower_bound(Fi, kb, t0, cnt);
-    const int32_t jhi = wg_lower_bound(Fi, kb, t1, cnt);
+    int32_t jlo, jhi;   // both ends of the tile's entries, searched together
+    wg_partition_point2(
+        0, kb, [&](int32_t p) { return (int64_t)Fi[p] < t0; }, 0, kb,
+        [&](int32_t p) { return (int64_t)Fi[p] < t1; }, cnt, &jlo, &jhi);
     for (int32_t j = jlo + (int32_t)threadIdx.x; j < jhi; j += blockDim.x) {
       const int64_t r = (int64_t)Fi[j] - t0;
-      if (r >= 0 && r < DENSE_TILE) tileb[r] = Fv[j];
+      if (r >= 0 && r < DENSE_TILE) {
+        tileb[r] = Fv[j];
+        if (member) atomicOr(&bits[r >> 5], 1u << (r & 31));
+      }
     }
   }
   __syncthreads();
+  if (member && threadIdx.x < DENSE_TILE / 32 && t0 + 32 * (int64_t)threadIdx.x < t1)
+    member[(t0 >> 5) + threadIdx.x] = bits[threadIdx.x];
   if (VEC == 4) {
     for (int i = threadIdx.x * 4; i < DENSE_TILE; i += blockDim.x * 4) {
       const int64_t x = t0 + i;
@@ -1762,11 +1776,11 @@ hipError_t launch_merge(const int32_t* sp_idx, const float* sp_val, int32_t P, i
 }
 
 hipError_t launch_densify(const int32_t* sp_idx, const float* sp_val, int32_t P, int64_t n, int32_t kb,
-                          float* dense, bool vec4, hipStream_t s) {
+                          float* dense, uint32_t* member, bool vec4, hipStream_t s) {
   const dim3 grid((unsigned)((n + DENSE_TILE - 1) / DENSE_TILE));
   const Blocks B = make_blocks(n, P);
-  if (vec4) hipLaunchKernelGGL(k_densify<4>, grid, dim3(256), 0, s, sp_idx, sp_val, B, kb, dense);
-  else hipLaunchKernelGGL(k_densify<1>, grid, dim3(256), 0, s, sp_idx, sp_val, B, kb, dense);
+  if (vec4) hipLaunchKernelGGL(k_densify<4>, grid, dim3(256), 0, s, sp_idx, sp_val, B, kb, dense, member);
+  else hipLaunchKernelGGL(k_densify<1>, grid, dim3(256), 0, s, sp_idx, sp_val, B, kb, dense, member);
   return hipGetLastError();
 }
 

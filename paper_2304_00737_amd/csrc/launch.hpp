@@ -49,7 +49,7 @@ hipError_t launch_merge(const int32_t* sp_idx, const float* sp_val, int32_t P, i
                         int32_t tiles_per_pair, uint32_t* hist1, uint32_t* slot_cnt, int32_t* U_idx,
                         float* U_val, hipStream_t s);
 hipError_t launch_densify(const int32_t* sp_idx, const float* sp_val, int32_t P, int64_t n, int32_t kb,
-                          float* dense, bool vec4, hipStream_t s);
+                          float* dense, uint32_t* member, bool vec4, hipStream_t s);
 hipError_t launch_bm_mark(const int32_t* sp_idx, int32_t P, int64_t n, int32_t kb, uint32_t* bm, bool set,
                           hipStream_t s);
 hipError_t launch_grc_zero(float* acc, int64_t ld_acc, int32_t P, int64_t n, int32_t kb, const int32_t* local_idx,

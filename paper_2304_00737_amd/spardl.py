@@ -40,8 +40,8 @@ _lib.spardl_workspace_init.restype = ctypes.c_int
 _lib.spardl_residual_add.argtypes = [_p, _i64, _p, _i64, _i32, _i64, _i32, _i32, _p, _sz, _p]
 _lib.spardl_block_topk.argtypes = [_p, _i64, _i32, _i64, _i32, _i32, _i32, _p, _p, _p, _p, _sz, _p]
 _lib.spardl_sparse_merge_topk.argtypes = [_p, _p, _i32, _i64, _i32, _i32, _p, _p, _p, _p, _sz, _p]
-_lib.spardl_allgather_densify.argtypes = [_p, _p, _i32, _i64, _i32, _p, _p]
-_lib.spardl_residual_collect.argtypes = [_p, _i64, _i32, _i64, _i32, _p, _p, _p, _p, _p, _p, _sz, _p]
+_lib.spardl_allgather_densify.argtypes = [_p, _p, _i32, _i64, _i32, _p, _p, _p]
+_lib.spardl_residual_collect.argtypes = [_p, _i64, _i32, _i64, _i32, _p, _p, _p, _p, _p, _p, _p, _sz, _p]
 for _f in ("residual_add", "block_topk", "sparse_merge_topk", "allgather_densify", "residual_collect"):
     getattr(_lib, "spardl_" + _f).restype = ctypes.c_int
 
@@ -131,20 +131,28 @@ def sparse_merge_topk(sp_idx, sp_val, P: int, n: int, k_blk: int, round: int, dr
         _ptr(ws), ws.numel() * ws.element_size(), _stream(stream)))
 
 
-def allgather_densify(sp_idx, sp_val, P: int, n: int, k_blk: int, dense, *, stream=None) -> None:
+def member_words(n: int) -> int:
+    """Words of the membership bitmap of the final index set."""
+    return (n + 31) // 32
+
+
+def allgather_densify(sp_idx, sp_val, P: int, n: int, k_blk: int, dense, member=None, *, stream=None) -> None:
+    """member: optional int32 tensor of member_words(n) words, receives the bitmap of I."""
     _check("allgather_densify", _lib.spardl_allgather_densify(_ptr(sp_idx), _ptr(sp_val), P, n, k_blk,
-                                                              _ptr(dense), _stream(stream)))
+                                                              _ptr(dense), _ptr(member), _stream(stream)))
 
 
 def residual_collect(acc, P: int, n: int, k_blk: int, local_idx, sp_idx, drop_idx, drop_val, drop_cnt, ws,
-                     *, ld_acc=None, stream=None) -> None:
-    """drop_idx / drop_val / drop_cnt: sequences of l tensors (one per step)."""
+                     member=None, *, ld_acc=None, stream=None) -> None:
+    """drop_idx / drop_val / drop_cnt: sequences of l tensors (one per step).
+    member: the bitmap allgather_densify wrote (then sp_idx and ws may be None)."""
     ld_acc = _ld(acc, n) if ld_acc is None else ld_acc
     l = len(drop_idx)
     arr = lambda ts: (ctypes.c_void_p * max(l, 1))(*[_ptr(t) for t in ts]) if l else None
+    ws_bytes = 0 if ws is None else ws.numel() * ws.element_size()
     _check("residual_collect", _lib.spardl_residual_collect(
-        _ptr(acc), ld_acc, P, n, k_blk, _ptr(local_idx), _ptr(sp_idx), arr(drop_idx), arr(drop_val),
-        arr(drop_cnt), _ptr(ws), ws.numel() * ws.element_size(), _stream(stream)))
+        _ptr(acc), ld_acc, P, n, k_blk, _ptr(local_idx), _ptr(sp_idx), _ptr(member), arr(drop_idx),
+        arr(drop_val), arr(drop_cnt), _ptr(ws), ws_bytes, _stream(stream)))
 
 
 def ws_error(ws) -> int:
@@ -172,6 +180,7 @@ class SparDLStep:
         self.drop_val = [torch.empty((P, m, k_blk), dtype=torch.float32, device=dev) for m in self.bags]
         self.drop_cnt = [torch.empty((P, m), dtype=torch.int32, device=dev) for m in self.bags]
         self.dense = torch.empty(n, dtype=torch.float32, device=dev)
+        self.member = torch.empty(member_words(n), dtype=torch.int32, device=dev)
         self.ws = workspace(P, P, n, k_blk, device=dev)
 
     def residual_add(self, grad, stream=None):
@@ -189,11 +198,13 @@ class SparDLStep:
                           self.drop_val[i - 1], self.drop_cnt[i - 1], self.ws, stream=stream)
 
     def densify(self, stream=None):
-        allgather_densify(self.sp_idx, self.sp_val, self.P, self.n, self.k_blk, self.dense, stream=stream)
+        allgather_densify(self.sp_idx, self.sp_val, self.P, self.n, self.k_blk, self.dense,
+                          self.member if self.fused else None, stream=stream)
 
     def collect(self, stream=None):
         residual_collect(self.acc, self.P, self.n, self.k_blk, self.local_idx, self.sp_idx, self.drop_idx,
-                         self.drop_val, self.drop_cnt, self.ws, stream=stream)
+                         self.drop_val, self.drop_cnt, self.ws, self.member if self.fused else None,
+                         stream=stream)
 
     def step(self, grad, stream=None):
         self.residual_add(grad, stream)

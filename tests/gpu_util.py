@@ -81,6 +81,14 @@ def compare_step(st, res, P: int, n: int, kb: int, blocks=None, acc_host=None) -
         for b in blocks:
             got = st.acc[w, bounds[b]:bounds[b + 1]].cpu().numpy()
             assert_bits_equal(got, res.residual[(w, b)], f"residual w={w} b={b}")
+    if getattr(st, "fused", False):   # densify also wrote the membership bitmap of I
+        words = st.member.cpu().numpy()
+        bits = np.unpackbits(words.view(np.uint8), bitorder="little").astype(bool)
+        assert not bits[n:].any(), "member bits at or above n"
+        for b in blocks:
+            want = np.zeros(bounds[b + 1] - bounds[b], bool)
+            want[np.asarray(res.final[b][0], np.int64) - bounds[b]] = True
+            assert np.array_equal(bits[bounds[b]:bounds[b + 1]], want), f"member bits block {b}"
 
 
 def ws_layout(P: int, n: int, kb: int, ws_bytes: int) -> dict:

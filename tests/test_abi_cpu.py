@@ -123,15 +123,26 @@ def test_argument_errors_enqueue_nothing():
     assert lib.spardl_sparse_merge_topk(p, p, i32(6), i64(600), i32(3), i32(4), p, p, p, p, sz(1 << 30), null) == EINVAL
     assert lib.spardl_sparse_merge_topk(p, p, i32(6), i64(600), i32(3), i32(0), p, p, p, p, sz(1 << 30), null) == EINVAL
     assert lib.spardl_sparse_merge_topk(p, p, i32(6), i64(600), i32(3), i32(1), p, p, p, p, sz(64), null) == ECAP
-    # densify: n < P, NULL output
-    assert lib.spardl_allgather_densify(p, p, i32(8), i64(7), i32(1), p, null) == EINVAL
-    assert lib.spardl_allgather_densify(p, p, i32(2), i64(8), i32(1), null, null) == EINVAL
+    # densify: n < P, NULL output, misaligned member bitmap
+    assert lib.spardl_allgather_densify(p, p, i32(8), i64(7), i32(1), p, null, null) == EINVAL
+    assert lib.spardl_allgather_densify(p, p, i32(2), i64(8), i32(1), null, null, null) == EINVAL
+    assert lib.spardl_allgather_densify(p, p, i32(2), i64(8), i32(1), p, ctypes.c_void_p(0x1002), null) == EINVAL
     # residual_collect: missing per-step drop arrays for P > 1
-    assert lib.spardl_residual_collect(p, i64(100), i32(4), i64(100), i32(3), p, p, null, null, null, p,
+    assert lib.spardl_residual_collect(p, i64(100), i32(4), i64(100), i32(3), p, p, null, null, null, null, p,
                                        sz(1 << 30), null) == EINVAL
     arr = (ctypes.c_void_p * 2)(0x1000, 0)
-    assert lib.spardl_residual_collect(p, i64(100), i32(4), i64(100), i32(3), p, p, arr, arr, arr, p,
+    assert lib.spardl_residual_collect(p, i64(100), i32(4), i64(100), i32(3), p, p, null, arr, arr, arr, p,
                                        sz(1 << 30), null) == EINVAL
+    # residual_collect: without a member bitmap, sp_idx and an aligned ws are required
+    ok3 = (ctypes.c_void_p * 2)(0x1000, 0x1000)
+    assert lib.spardl_residual_collect(p, i64(100), i32(4), i64(100), i32(3), p, null, null, ok3, ok3, ok3, p,
+                                       sz(1 << 30), null) == EINVAL
+    assert lib.spardl_residual_collect(p, i64(100), i32(4), i64(100), i32(3), p, p, null, ok3, ok3, ok3, null,
+                                       sz(1 << 30), null) == EINVAL
+    assert lib.spardl_residual_collect(p, i64(100), i32(4), i64(100), i32(3), p, p, null, ok3, ok3, ok3, q,
+                                       sz(1 << 30), null) == EINVAL
+    assert lib.spardl_residual_collect(p, i64(100), i32(4), i64(100), i32(3), p, p, ctypes.c_void_p(0x1001),
+                                       ok3, ok3, ok3, null, sz(0), null) == EINVAL
     for s in (0, -1, -2, -3, 7):
         assert lib.spardl_strerror(s)
 

@@ -213,6 +213,21 @@ def test_step(P, n, kb, kind, steps):
         compare_step(st, res, P, n, kb)
 
 
+@pytest.mark.parametrize("P,n,kb,kind,steps", [STEP_CASES[i] for i in (1, 4, 6, 8)])
+def test_step_unfused(P, n, kb, kind, steps):
+    """Residual add without histogram, block top-k that counts the block
+    itself and residual collection that builds I in the workspace."""
+    log(f"step unfused P={P} n={n} kb={kb} kind={kind} steps={steps}")
+    st = spardl.SparDLStep(P, n, kb, fused=False)
+    acc = np.zeros((P, n), np.float32)
+    for t in range(steps):
+        grad = _rows(kind, P, n, 100 * t + P + 1)
+        st.step(_dev(grad))
+        check_ws(st)
+        res = so.spardl_step([acc[w] for w in range(P)], [grad[w] for w in range(P)], P, n, kb)
+        compare_step(st, res, P, n, kb)
+
+
 def test_cfg1_full():
     wl = W.config(1)
     P, n, kb = wl.P, wl.n, wl.k_blk
