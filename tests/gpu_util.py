@@ -109,7 +109,7 @@ def ws_layout(P: int, n: int, kb: int, ws_bytes: int) -> dict:
     slot_n = max(P * P * tiles_tk, pairs_max * tiles_mg)
     L, off = {}, 256
     L["bitmap"] = off; off += al(-(-n // 32) * 4)
-    L["hist1"] = off; off += al(units * 16 * 4096 * 4)
+    L["hist1"] = off; off += al(units * 4 * 4096 * 4)     # 4 level-1 histogram copies per unit
     L["spec_t1"] = off; off += al(P * P * 4)
     L["spec_used"] = off; off += al(P * P * 4)
     L["spec_cnt"] = off; off += al(P * P * add_tiles * 4)
