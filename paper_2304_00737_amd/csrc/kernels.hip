@@ -481,7 +481,7 @@ __device__ __forceinline__ void collect_slot(const float* __restrict__ A, uint32
 // before any of its writes, and a compacted position never exceeds the
 // storage position of an entry not yet read, so no barrier is needed.
 static_assert(SLOT == 2 * ADD_TILE, "a slot holds two residual-add tiles");
-constexpr int RC_R = 4;   // entries per lane per chunk
+constexpr int RC_R = 16;  // entries per lane per chunk (a crowded slot holds up to 4096)
 __device__ __forceinline__ void recollect_wave(uint32_t c0, uint32_t c1, uint32_t tlo, uint32_t thi,
                                                uint32_t* cnt_out, uint32_t* nbin_out, int32_t* __restrict__ CI,
                                                float* __restrict__ CV, uint32_t* __restrict__ BK) {
@@ -529,9 +529,11 @@ __device__ __forceinline__ void recollect_wave(uint32_t c0, uint32_t c1, uint32_
 // One workgroup per COLLECT_GROUP consecutive slots of one (worker, block).
 // With the fused add's candidates usable, wave k filters slot k of the group;
 // otherwise the workgroup collects the group's slots from acc one by one.
+// Candidates crowd into the slots of large-scale segments, so one slot per
+// wave keeps the longest wave short; 64 registers let 8 waves share a SIMD.
 constexpr int COLLECT_GROUP = 4;
 template <int VEC>
-__global__ __launch_bounds__(256) void k_collect(const float* __restrict__ acc, int64_t ld_acc, Blocks B,
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(8, 8))) void k_collect(const float* __restrict__ acc, int64_t ld_acc, Blocks B,
                                                  uint32_t smax, uint32_t gq, const uint32_t* __restrict__ state,
                                                  const uint32_t* __restrict__ spec_cnt, uint32_t add_tiles,
                                                  uint32_t* __restrict__ slot_cnt, uint32_t* __restrict__ slot_nbin,
@@ -547,20 +549,22 @@ __global__ __launch_bounds__(256) void k_collect(const float* __restrict__ acc, 
   const uint32_t specok = st[ST_SPECOK];
   const uint32_t T1 = st[ST_T1];
   if (specok != 0u) {
-    const uint32_t slot = slot0 + (uint32_t)wave_id();
-    const uint32_t t0 = s + slot * (uint32_t)SLOT;
-    if (slot >= smax || t0 >= e) return;
     const uint32_t tlo = T1 << D1_SHIFT, thi = tlo + (1u << D1_SHIFT);
-    const int64_t tile0 = (int64_t)unit * add_tiles + (int64_t)slot * (SLOT / ADD_TILE);
-    // counts are clamped to the tiles' lengths inside the block, so reads stay in the slot
-    const uint32_t len0 = min(e - t0, (uint32_t)ADD_TILE);
-    const uint32_t len1 = t0 + (uint32_t)ADD_TILE < e ? min(e - t0 - (uint32_t)ADD_TILE, (uint32_t)ADD_TILE) : 0u;
-    const uint32_t c0 = min(spec_cnt[tile0], len0);
-    const uint32_t c1 = len1 != 0u ? min(spec_cnt[tile0 + 1], len1) : 0u;
-    const int64_t cbase = (int64_t)w * B.n + t0;
-    const int64_t si = (int64_t)unit * smax + slot;
-    recollect_wave(c0, c1, tlo, thi, slot_cnt + si, slot_nbin + si, cand_idx + cbase, cand_val + cbase,
-                   bin_key + cbase);
+    {
+      const uint32_t slot = slot0 + (uint32_t)wave_id();
+      const uint32_t t0 = s + slot * (uint32_t)SLOT;
+      if (slot >= smax || t0 >= e) return;
+      const int64_t tile0 = (int64_t)unit * add_tiles + (int64_t)slot * (SLOT / ADD_TILE);
+      // counts are clamped to the tiles' lengths inside the block, so reads stay in the slot
+      const uint32_t len0 = min(e - t0, (uint32_t)ADD_TILE);
+      const uint32_t len1 = t0 + (uint32_t)ADD_TILE < e ? min(e - t0 - (uint32_t)ADD_TILE, (uint32_t)ADD_TILE) : 0u;
+      const uint32_t c0 = min(spec_cnt[tile0], len0);
+      const uint32_t c1 = len1 != 0u ? min(spec_cnt[tile0 + 1], len1) : 0u;
+      const int64_t cbase = (int64_t)w * B.n + t0;
+      const int64_t si = (int64_t)unit * smax + slot;
+      recollect_wave(c0, c1, tlo, thi, slot_cnt + si, slot_nbin + si, cand_idx + cbase, cand_val + cbase,
+                     bin_key + cbase);
+    }
     return;
   }
   for (int k = 0; k < COLLECT_GROUP; ++k) {
@@ -695,10 +699,16 @@ constexpr int FAST_ROWS = 16;                    // merge: slots per unit, one f
 constexpr uint32_t KEY_NONE = 0xFFFFFFFFu;       // marks a register that holds no entry (keys are 31-bit)
 static_assert(MERGE_TILE == 4 * 1024, "a merge slot is one float4 per thread of the threshold kernel");
 
+// The slot map of chunk 0 holds two 16-bit slot ids per word, with one pad
+// word after every 16 so that a thread walking its 16 consecutive words hits
+// 16 different banks as its neighbours do.
+__device__ __forceinline__ uint32_t map_word(uint32_t w) { return w + (w >> 4); }
+__device__ __forceinline__ uint32_t map_half(uint32_t f) { return 2u * map_word(f >> 1) + (f & 1u); }
+
 struct FastSmem {
   uint32_t pref[FAST_SLOTS + 1];   // block top-k: exclusive prefix of bin entries per slot; merge: slot counts
   union {
-    uint16_t slotid[FAST_CAP0];    // block top-k: slot of each entry of chunk 0 (used before the histograms)
+    uint16_t slotid[FAST_CAP0 + FAST_CAP0 / 16];   // block top-k: slot of each entry of chunk 0, padded
     struct {
       uint32_t h[NB1];
       uint32_t cg[FAST_SLOTS];     // per-slot count of selected-by-key (>= TGE) bin entries
@@ -952,7 +962,7 @@ __device__ __forceinline__ void thresh_fast_topk(FastSmem& L, int64_t unit, cons
   // zero the slot map of chunk 0 while the scan runs
   uint32_t* smw = reinterpret_cast<uint32_t*>(L.u.slotid);
 #pragma unroll
-  for (int q = 0; q < MW; ++q) smw[q * NT + t] = 0u;
+  for (int q = 0; q < MW; ++q) smw[map_word(q * NT + t)] = 0u;
   uint32_t total;
   uint32_t run = block_excl_scan(sb, L.scratch, &total);   // has barriers: the map is zero after it
   if (total != cnt1 && t == 0) atomicOr(err, ERR_COUNT);
@@ -962,7 +972,7 @@ __device__ __forceinline__ void thresh_fast_topk(FastSmem& L, int64_t unit, cons
     const int s = PS * t + u;
     if (s < ns) {
       L.pref[s] = run;
-      if (nb[u] != 0u && run < m) L.u.slotid[run] = (uint16_t)s;   // first entry of a non-empty slot
+      if (nb[u] != 0u && run < m) L.u.slotid[map_half(run)] = (uint16_t)s;   // first entry of a non-empty slot
     }
     run += nb[u];
   }
@@ -974,7 +984,7 @@ __device__ __forceinline__ void thresh_fast_topk(FastSmem& L, int64_t unit, cons
     uint32_t mx = 0u;
 #pragma unroll
     for (int q = 0; q < MW; ++q) {
-      wv[q] = smw[MW * t + q];
+      wv[q] = smw[map_word(MW * t + q)];
       mx = max(mx, max(wv[q] & 0xFFFFu, wv[q] >> 16));
     }
     uint32_t run_max = block_excl_max(mx, L.scratch);
@@ -983,7 +993,7 @@ __device__ __forceinline__ void thresh_fast_topk(FastSmem& L, int64_t unit, cons
       const uint32_t lo = max(run_max, wv[q] & 0xFFFFu);
       const uint32_t hi = max(lo, wv[q] >> 16);
       run_max = hi;
-      smw[MW * t + q] = lo | (hi << 16);
+      smw[map_word(MW * t + q)] = lo | (hi << 16);
     }
   }
   __syncthreads();
@@ -994,7 +1004,7 @@ __device__ __forceinline__ void thresh_fast_topk(FastSmem& L, int64_t unit, cons
     const uint32_t f = (uint32_t)(r * NT + t);
     uint32_t key = KEY_NONE, sl = 0u;
     if (f < m) {
-      sl = L.u.slotid[f];
+      sl = L.u.slotid[map_half(f)];
       key = K[(int64_t)sl * g.ss + (f - L.pref[sl])];
     }
     rk[r] = key;
@@ -1308,7 +1318,7 @@ __global__ __launch_bounds__(1024) void k_thresh(Blocks B, int32_t kb, int32_t s
 // full merge tiles, so a workgroup takes one slot and each wave a quarter of
 // it, the counts of the quarters before it exchanged through LDS; selected ->
 // sp[w][b] in place, the rest -> the step's drop lists.
-constexpr int EMIT_R = 4;   // entries per lane per chunk
+constexpr int EMIT_R = 16;  // entries per lane per chunk (a crowded slot holds up to 4096)
 template <int MODE>
 __global__ __launch_bounds__(256) void k_emit(
     const int32_t* __restrict__ cand_idx, const float* __restrict__ cand_val, Blocks B,
