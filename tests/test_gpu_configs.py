@@ -23,8 +23,8 @@ if gpu_available():
     from paper_2304_00737_amd import workloads as W
 
 
-def _run(cfg_id, blocks):
-    wl = W.config(cfg_id)
+def _run(cfg_id, blocks, wl=None):
+    wl = W.config(cfg_id) if wl is None else wl
     P, n, kb = wl.P, wl.n, wl.k_blk
     log(f"workload {cfg_id}: {wl.describe()} sampled blocks={blocks}")
     bounds = so.block_bounds(n, P)
@@ -60,3 +60,17 @@ def test_workload3_vgg16_sized_sampled():
 
 def test_workload4_bert_sized_sampled():
     _run(4, [2, 15])
+
+
+@pytest.mark.parametrize("density", [(1, 100), (1, 10000)])
+def test_long_blocks_general_threshold_paths(density):
+    """Blocks of 35M elements: more candidate slots (8545) than the threshold
+    kernel keeps resident, so the block top-k takes the general path (cached
+    bin at 0.01 %, re-read from memory at 1 %); at 1 % the merge union spans 171
+    slots, more than the register-resident merge path holds, so the merge
+    threshold takes its general path too."""
+    n = 70_000_000
+    lens, sc = W._segments_loguniform(90, 40, n, 2 ** 9, 2 ** 22, 1e-5, 1e-1)
+    wl = W.Workload(90, f"long blocks P=2 n=70M rho={density[0]}/{density[1]}", 2, n, density, 2, "normal", lens, sc)
+    assert -(-(n // 2) // 4096) > 8192
+    _run(None, None, wl)
