@@ -13,6 +13,7 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 SPARDL_SO = os.path.join(PKG, "libspardl.so")
 GRADGEN_SO = os.path.join(PKG, "workloads", "libgradgen.so")
+GRADGEN_DEV_SO = os.path.join(PKG, "workloads", "libgradgen_dev.so")
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
@@ -44,6 +45,14 @@ def build_gradgen(verbose: bool = True) -> str:
     return GRADGEN_SO
 
 
+def build_gradgen_dev(verbose: bool = True) -> str:
+    src = os.path.join(PKG, "workloads", "gradgen_dev.hip")
+    tmp = GRADGEN_DEV_SO + ".tmp"
+    _run([HIPCC, *HIP_FLAGS, src, "-o", tmp], verbose)
+    os.replace(tmp, GRADGEN_DEV_SO)
+    return GRADGEN_DEV_SO
+
+
 def build_spardl(verbose: bool = True) -> str:
     srcs = [os.path.join(CSRC, f) for f in ("api.hip", "kernels.hip")]
     tmp = SPARDL_SO + ".tmp"
@@ -56,6 +65,7 @@ def build_all(verbose: bool = True) -> None:
     if shutil.which("gcc") is None:
         raise RuntimeError("gcc not found")
     build_gradgen(verbose)
+    build_gradgen_dev(verbose)
     build_spardl(verbose)
 
 

@@ -168,8 +168,12 @@ class SparDLStep:
     sp[b, b]), local_idx the local selections and drop_* the per-step drops.
     """
 
-    def __init__(self, P: int, n: int, k_blk: int, device="cuda", fused: bool = True):
+    def __init__(self, P: int, n: int, k_blk: int, device="cuda", fused: bool = True, rows_per_call: int = 0):
+        """rows_per_call: workers per residual-add / block top-k call (0: all P).
+        The workspace is sized for that many rows, so a model too large for a
+        P-row workspace runs its workers a few at a time."""
         self.P, self.n, self.k_blk, self.fused = P, n, k_blk, fused
+        self.rows = P if rows_per_call <= 0 else min(rows_per_call, P)
         dev = torch.device(device)
         self.acc = torch.zeros((P, n), dtype=torch.float32, device=dev)
         self.sp_idx = torch.empty((P, P, k_blk), dtype=torch.int32, device=dev)
@@ -181,17 +185,34 @@ class SparDLStep:
         self.drop_cnt = [torch.empty((P, m), dtype=torch.int32, device=dev) for m in self.bags]
         self.dense = torch.empty(n, dtype=torch.float32, device=dev)
         self.member = torch.empty(member_words(n), dtype=torch.int32, device=dev)
-        self.ws = workspace(P, P, n, k_blk, device=dev)
+        self.ws = workspace(self.rows, P, n, k_blk, device=dev)
+
+    def residual_add_rows(self, w0: int, grad_rows, stream=None):
+        """Rows w0 .. w0 + len(grad_rows) - 1 (at most rows_per_call)."""
+        r = grad_rows.shape[0]
+        acc = self.acc[w0:w0 + r]
+        if self.fused:
+            residual_add(acc, grad_rows, r, self.n, self.P, self.ws, self.k_blk, stream=stream)
+        else:
+            residual_add(acc, grad_rows, r, self.n, 0, None, stream=stream)
+
+    def block_topk_rows(self, w0: int, r: int, stream=None):
+        s = slice(w0, w0 + r)
+        block_topk(self.acc[s], r, self.n, self.P, self.k_blk, self.sp_idx[s], self.sp_val[s], self.local_idx[s],
+                   self.ws, TOPK_HIST_READY if self.fused else 0, stream=stream)
 
     def residual_add(self, grad, stream=None):
-        if self.fused:
-            residual_add(self.acc, grad, self.P, self.n, self.P, self.ws, self.k_blk, stream=stream)
-        else:
-            residual_add(self.acc, grad, self.P, self.n, 0, None, stream=stream)
+        self._all_rows()
+        self.residual_add_rows(0, grad, stream)
 
     def block_topk(self, stream=None):
-        block_topk(self.acc, self.P, self.n, self.P, self.k_blk, self.sp_idx, self.sp_val, self.local_idx,
-                   self.ws, TOPK_HIST_READY if self.fused else 0, stream=stream)
+        self._all_rows()
+        self.block_topk_rows(0, self.P, stream)
+
+    def _all_rows(self):
+        if self.rows != self.P:
+            raise ValueError("a workspace for fewer rows than P: alternate residual_add_rows and "
+                             "block_topk_rows per worker group (step() does)")
 
     def merge_round(self, i: int, stream=None):
         sparse_merge_topk(self.sp_idx, self.sp_val, self.P, self.n, self.k_blk, i, self.drop_idx[i - 1],
@@ -206,10 +227,21 @@ class SparDLStep:
                          self.drop_val, self.drop_cnt, self.ws, self.member if self.fused else None,
                          stream=stream)
 
-    def step(self, grad, stream=None):
-        self.residual_add(grad, stream)
-        self.block_topk(stream)
+    def finish(self, stream=None):
+        """The SRS steps, the decode and the residual collection, after every
+        worker's residual add and block top-k."""
         for i in range(1, self.l + 1):
             self.merge_round(i, stream)
         self.densify(stream)
         self.collect(stream)
+
+    def step(self, grad, stream=None):
+        if self.rows == self.P:
+            self.residual_add(grad, stream)
+            self.block_topk(stream)
+        else:   # a worker group's add and top-k share the workspace, so they alternate
+            for w0 in range(0, self.P, self.rows):
+                r = min(self.rows, self.P - w0)
+                self.residual_add_rows(w0, grad[w0:w0 + r], stream)
+                self.block_topk_rows(w0, r, stream)
+        self.finish(stream)

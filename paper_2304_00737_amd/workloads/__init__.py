@@ -172,6 +172,48 @@ def fill(out: np.ndarray, wl: Workload, step: int, worker: int, x0: int = 0) -> 
     return out
 
 
+DEV_LIB_PATH = os.path.join(_HERE, "libgradgen_dev.so")
+_dev_lib = None
+
+
+def _load_dev():
+    global _dev_lib
+    if _dev_lib is None:
+        if not os.path.exists(DEV_LIB_PATH):
+            raise ImportError(f"{DEV_LIB_PATH} is not built; run __graft_entry__.build()")
+        lib = ctypes.CDLL(DEV_LIB_PATH)
+        lib.gg_fill_device.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_int64, ctypes.c_uint64,
+                                       ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int,
+                                       ctypes.c_double, ctypes.c_void_p]
+        lib.gg_fill_device.restype = ctypes.c_int
+        _dev_lib = lib
+    return _dev_lib
+
+
+class DeviceGenerator:
+    """The same generator on the GPU: fills device memory with the bits fill()
+    gives on the host (input plumbing; torch is imported only here)."""
+
+    def __init__(self, wl: Workload, device="cuda"):
+        import torch
+        self.wl = wl
+        self.starts = torch.tensor(np.asarray(wl.seg_start, dtype=np.int64), device=device)
+        self.scales = torch.tensor(np.asarray(wl.seg_scale, dtype=np.float64), device=device)
+        self.lib = _load_dev()
+
+    def fill(self, out, step: int, worker: int, x0: int = 0, stream=None) -> None:
+        """out: contiguous float32 CUDA tensor; element j <- element x0 + j of the gradient."""
+        import torch
+        assert out.dtype == torch.float32 and out.is_contiguous() and out.is_cuda
+        s = (stream or torch.cuda.current_stream()).cuda_stream
+        wl = self.wl
+        rc = self.lib.gg_fill_device(out.data_ptr(), out.numel(), x0, stream_key(wl.cfg_id, step, worker),
+                                     DIST_CODE[wl.dist], self.starts.data_ptr(), self.scales.data_ptr(),
+                                     len(wl.seg_len), float(wl.zero_prob), s)
+        if rc != 0:
+            raise RuntimeError(f"gg_fill_device failed: {rc}")
+
+
 def gradient(wl: Workload, step: int, worker: int, x0: int = 0, count: int | None = None) -> np.ndarray:
     count = wl.n - x0 if count is None else count
     return fill(np.empty(count, dtype=np.float32), wl, step, worker, x0)

@@ -228,6 +228,20 @@ def test_step_unfused(P, n, kb, kind, steps):
         compare_step(st, res, P, n, kb)
 
 
+@pytest.mark.parametrize("P,n,kb,rows", [(8, 50000, 100, 1), (7, 70001, 501, 3), (5, 10007, 3, 2)])
+def test_step_rows_per_call(P, n, kb, rows):
+    """Workers a few at a time (a workspace for `rows` rows): the same step."""
+    log(f"step rows_per_call={rows} P={P} n={n} kb={kb}")
+    st = spardl.SparDLStep(P, n, kb, rows_per_call=rows)
+    acc = np.zeros((P, n), np.float32)
+    for t in range(3):
+        grad = _rows("normal", P, n, 300 * t + P)
+        st.step(_dev(grad))
+        check_ws(st)
+        res = so.spardl_step([acc[w] for w in range(P)], [grad[w] for w in range(P)], P, n, kb)
+        compare_step(st, res, P, n, kb)
+
+
 def test_cfg1_full():
     wl = W.config(1)
     P, n, kb = wl.P, wl.n, wl.k_blk
