@@ -1,0 +1,91 @@
+"""Digests of one sampled block of the GPT-2-XL-sized workload (P = 32,
+n = 1.5e9, 0.1 %, 2 steps with the residual carried).
+
+The oracle needs minutes per step on one block index of this workload, too
+long to run beside the GPU test, so this committed script runs it once
+(oracle and host input generator only) and stores SHA-256 digests of every
+output on that block index; the GPU test hashes its own outputs the same way.
+Every block index of every output depends only on that block index of the
+inputs, so one index exercises every kernel at full size.
+
+    python tests/golden/workload5_digest.py     # writes workload5_block17.json
+"""
+
+import hashlib
+import json
+import os
+import sys
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.dirname(os.path.dirname(os.path.abspath(__file__))))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+BLOCK = 17
+OUT = os.path.join(os.path.dirname(os.path.abspath(__file__)), f"workload5_block{BLOCK}.json")
+
+
+def _h(*arrays) -> hashlib.sha256:
+    h = hashlib.sha256()
+    for a in arrays:
+        h.update(np.ascontiguousarray(a).tobytes())
+    return h
+
+
+def step_digests(P, block, bags, sp, local, drops, dense, residual) -> dict:
+    """sp(w), local(w), residual(w): arrays for worker w on the block (sp a pair
+    (idx, val)); drops(i, w): (idx, val) of worker w's drops of the block at
+    step i; dense: the decoded update on the block.  Indices are hashed as
+    little-endian int32 and values as float32 bits, workers in order."""
+    hs, hl, hd, hr = hashlib.sha256(), hashlib.sha256(), hashlib.sha256(), hashlib.sha256()
+    for w in range(P):
+        i_, v_ = sp(w)
+        hs.update(np.asarray(i_, "<i4").tobytes())
+        hs.update(np.asarray(v_, "<f4").tobytes())
+        hl.update(np.asarray(local(w), "<i4").tobytes())
+        hr.update(np.asarray(residual(w), "<f4").tobytes())
+    for i, m in enumerate(bags, start=1):
+        for w in range(P):
+            for t in range(m):
+                if (w + t) % P != block:
+                    continue
+                i_, v_ = drops(i, w)
+                hd.update(np.array([i, w, len(i_)], "<i4").tobytes())
+                hd.update(np.asarray(i_, "<i4").tobytes())
+                hd.update(np.asarray(v_, "<f4").tobytes())
+    return {"sp": hs.hexdigest(), "local": hl.hexdigest(), "drops": hd.hexdigest(),
+            "dense": _h(np.asarray(dense, "<f4")).hexdigest(), "residual": hr.hexdigest()}
+
+
+def main() -> None:
+    from oracle import spardl_oracle as so
+    from paper_2304_00737_amd import workloads as W
+    wl = W.config(5)
+    P, n, kb = wl.P, wl.n, wl.k_blk
+    b = BLOCK
+    bounds = so.block_bounds(n, P)
+    L = bounds[b + 1] - bounds[b]
+    acc = [{b: np.zeros(L, np.float32)} for _ in range(P)]
+    out = {"workload": wl.name, "block": b, "block_range": [int(bounds[b]), int(bounds[b + 1])],
+           "k_per_block": kb, "steps": []}
+    for t in range(1, wl.steps + 1):
+        grad = []
+        for w in range(P):
+            h = np.empty(L, np.float32)
+            W.fill(h, wl, t, w, x0=bounds[b])
+            grad.append({b: h})
+        print(f"step {t}: inputs generated", flush=True)
+        res = so.spardl_step(acc, grad, P, n, kb, blocks=[b])
+        print(f"step {t}: oracle done", flush=True)
+        bags = [len(step.received_bag[0]) for step in so.srs_schedule(P)]
+        d = step_digests(P, b, bags, lambda w: res.S[(w, b)], lambda w: res.local[(w, b)][0],
+                         lambda i, w: res.drops[(i, w, b)], res.dense[b], lambda w: res.residual[(w, b)])
+        out["steps"].append(d)
+    with open(OUT, "w") as f:
+        json.dump(out, f, indent=1)
+    print("wrote", OUT)
+
+
+if __name__ == "__main__":
+    main()

@@ -74,3 +74,66 @@ def test_long_blocks_general_threshold_paths(density):
     wl = W.Workload(90, f"long blocks P=2 n=70M rho={density[0]}/{density[1]}", 2, n, density, 2, "normal", lens, sc)
     assert -(-(n // 2) // 4096) > 8192
     _run(None, None, wl)
+
+
+def test_workload5_gpt2xl_sized_block17():
+    """P = 32, n = 1.5e9, 0.1 %, 2 steps: the residual rows alone take 192 GB,
+    so the workers' gradients are generated on the GPU one at a time and each
+    worker's residual add and block top-k run on a one-row workspace.  Block
+    index 17 of every output is hashed and compared with the digests the
+    oracle produced (tests/golden/workload5_digest.py)."""
+    import json
+    import os
+    from tests.golden.workload5_digest import BLOCK, OUT, step_digests
+
+    gold = json.load(open(OUT))
+    wl = W.config(5)
+    P, n, kb = wl.P, wl.n, wl.k_blk
+    b = BLOCK
+    bounds = so.block_bounds(n, P)
+    lo, hi = bounds[b], bounds[b + 1]
+    assert gold["block_range"] == [lo, hi] and gold["k_per_block"] == kb
+    log(f"workload 5: {wl.describe()} block {b}")
+    torch.cuda.empty_cache()   # about 224 GB of HBM below; drop what earlier tests left cached
+    st = spardl.SparDLStep(P, n, kb, rows_per_call=1)
+    gen = W.DeviceGenerator(wl)
+    g = torch.empty((1, n), dtype=torch.float32, device="cuda")
+    for t in range(1, wl.steps + 1):
+        for w in range(P):
+            gen.fill(g[0], t, w)
+            st.residual_add_rows(w, g)
+            st.block_topk_rows(w, 1)
+        st.finish()
+        torch.cuda.synchronize()
+        check_ws(st)
+        log(f"  step {t}: GPU done, hashing block {b}")
+        sp_i = st.sp_idx[:, b].cpu().numpy()
+        sp_v = st.sp_val[:, b].cpu().numpy()
+        loc = st.local_idx[:, b].cpu().numpy()
+        dr = [(di.cpu().numpy(), dv.cpu().numpy(), dc.cpu().numpy())
+              for di, dv, dc in zip(st.drop_idx, st.drop_val, st.drop_cnt)]
+
+        def drops(i, w):
+            di, dv, dc = dr[i - 1]
+            t_ = (b - w) % P
+            c = int(dc[w, t_])
+            return di[w, t_, :c], dv[w, t_, :c]
+
+        dense = st.dense[lo:hi].cpu().numpy()
+        resid = st.acc[:, lo:hi].cpu().numpy()
+        got = step_digests(P, b, st.bags, lambda w: (sp_i[w], sp_v[w]), lambda w: loc[w], drops, dense,
+                           lambda w: resid[w])
+        want = gold["steps"][t - 1]
+        for key in want:
+            assert got[key] == want[key], f"step {t}: {key} digest differs"
+        # the membership bitmap on the block matches the final block's indices
+        words = st.member[lo // 32:(hi + 31) // 32 + 1].cpu().numpy()
+        bits = np.unpackbits(words.view(np.uint8), bitorder="little").astype(bool)
+        base = (lo // 32) * 32
+        want_bits = np.zeros(hi - lo, bool)
+        want_bits[sp_i[b] - lo] = True
+        assert np.array_equal(bits[lo - base:hi - base], want_bits), f"step {t}: membership bits"
+        log(f"  step {t}: digests match")
+        del sp_i, sp_v, loc, dr, dense, resid
+    del st, g, gen
+    torch.cuda.empty_cache()
