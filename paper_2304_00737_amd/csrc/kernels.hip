@@ -828,18 +828,31 @@ __device__ __forceinline__ void thresh_fast_merge(FastSmem& L, int64_t unit, con
     L.u.c.ce[t] = 0u;
   }
   __syncthreads();
+  // ties at the threshold key are rare: without them only the >= count is needed
+  if (need_eq == 0u) {
 #pragma unroll
-  for (int r = 0; r < FAST_ROWS; ++r) {
-    if (r < ns) {
-      uint32_t ng = 0, ne = 0;
+    for (int r = 0; r < FAST_ROWS; ++r) {
+      if (r < ns) {
+        uint32_t ng = 0;
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        ng += popc64(__ballot(key[r][q] != KEY_NONE && key[r][q] >= tge));
-        ne += popc64(__ballot(need_eq != 0u && key[r][q] == teq));
+        for (int q = 0; q < 4; ++q) ng += popc64(__ballot(key[r][q] != KEY_NONE && key[r][q] >= tge));
+        if (lane == 0 && ng) atomicAdd(&L.u.c.cg[r], ng);
       }
-      if (lane == 0) {
-        if (ng) atomicAdd(&L.u.c.cg[r], ng);
-        if (ne) atomicAdd(&L.u.c.ce[r], ne);
+    }
+  } else {
+#pragma unroll
+    for (int r = 0; r < FAST_ROWS; ++r) {
+      if (r < ns) {
+        uint32_t ng = 0, ne = 0;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          ng += popc64(__ballot(key[r][q] != KEY_NONE && key[r][q] >= tge));
+          ne += popc64(__ballot(key[r][q] == teq));
+        }
+        if (lane == 0) {
+          if (ng) atomicAdd(&L.u.c.cg[r], ng);
+          if (ne) atomicAdd(&L.u.c.ce[r], ne);
+        }
       }
     }
   }
