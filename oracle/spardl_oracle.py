@@ -19,6 +19,10 @@ What is computed, and where the paper defines it (SparDL, arXiv 2304.00737):
 * final All-Gather of the P reduced blocks and decode to a dense update
   (end of Sec. III-B; Sec. II for All-Gather semantics).
 * global residual collection (Sec. III-C, Algorithm 1).
+* the lazy-sparsification variant of the transmission ("Optimization for
+  SRS", Sec. III-B) with Algorithm 1's residual: held blocks stay dense,
+  received entries are added into them, and a block is sparsified only when
+  it is about to be sent (spardl_step_lazy; its own readings sit above it).
 
 Readings taken where the paper is silent or ambiguous (each one is listed in
 the design notes of the repository):
@@ -341,4 +345,112 @@ def spardl_step(acc, grad, P: int, n: int, k: int, blocks=None) -> SparDLStepRes
                                          res.final[b][0], in_order)
             res.residual[(w, b)] = xi
             _block_of(acc[w], b, bounds)[...] = xi
+    return res
+
+
+# ----------------------------------------------------------------------------
+# Lazy sparsification ("Optimization for SRS", Sec. III-B; Algorithm 1)
+# ----------------------------------------------------------------------------
+#
+# Readings taken for this variant (each one is listed in the design notes):
+#
+# * a worker keeps every block it holds dense (A plus what it has received);
+#   "the blocks transmitted next" at step i are the blocks of the bag sent at
+#   step i, and they are sparsified right before that step's transmission;
+#   the reserved block is sparsified after the last step.  So each worker
+#   sparsifies each block exactly once.
+# * summation adds each received entry into the receiver's dense block at its
+#   index (one fp32 add, held + received); no re-selection follows it.
+# * xi_b = G_b - g_b is an fp32 subtraction of a block that is zero off the
+#   selection: G_b[x] off it (bits unchanged, -0.0 included), +0.0 on it.
+# * I_b are the indexes of the final block b that the All-Gather delivers
+#   (worker b's selection of its reserved block); the new residual of worker w
+#   on block b is the copy of A taken before transmission, replaced on I_b by
+#   worker w's xi_b.
+
+
+@dataclass
+class LazyStepResult:
+    """Everything one lazy oracle step produces, keyed by worker w and block b."""
+
+    bounds: list
+    blocks: list
+    sel: dict = field(default_factory=dict)       # (w, b) -> (idx, val): g_b as worker w selected it
+    sent_at: dict = field(default_factory=dict)   # (w, b) -> step at which w sent b; 0 = reserved
+    final: dict = field(default_factory=dict)     # b -> (idx, val) = sel[(b, b)]
+    dense: dict = field(default_factory=dict)     # b -> dense update on block b
+    residual: dict = field(default_factory=dict)  # (w, b) -> new residual on block b
+
+
+def sparsify_with_residual(G_block: np.ndarray, base: int, k: int):
+    """Top-k of one dense block and xi = G - g (Algorithm 1, sparsification
+    and the residual line after it).  g is the selection written out densely
+    (zeros elsewhere) and subtracted in fp32."""
+    idx, val = local_sparsify(G_block, base, k)
+    g = np.zeros(len(G_block), dtype=np.float32)
+    g[idx - base] = val
+    xi = (np.asarray(G_block, dtype=np.float32) - g).astype(np.float32)
+    return idx, val, xi
+
+
+def add_received(G_block: np.ndarray, base: int, idx, val) -> None:
+    """Summation of a received sparse block into a dense held block (Sec. III-B,
+    Algorithm 1 "transmission and summation"): one fp32 add per received index."""
+    pos = np.asarray(idx, dtype=np.int64) - base
+    G_block[pos] = G_block[pos] + np.asarray(val, dtype=np.float32)
+
+
+def spardl_step_lazy(acc, grad, P: int, n: int, k: int, blocks=None) -> LazyStepResult:
+    """One SparDL synchronisation (d = 1) with lazy sparsification: Algorithm 1
+    as written, with the sparsification timing of "Optimization for SRS"
+    (Sec. III-B).
+
+    acc[w], grad[w]: as for spardl_step.  The new residual is written back into
+    acc on the listed blocks.
+    """
+    bounds = block_bounds(n, P)
+    blocks = list(range(P)) if blocks is None else sorted(blocks)
+    wanted = set(blocks)
+    res = LazyStepResult(bounds=bounds, blocks=blocks)
+    # residual add, partition into blocks, and the copy of the result
+    G, G_copy = {}, {}
+    for w in range(P):
+        for b in blocks:
+            G[(w, b)] = residual_add(_block_of(acc[w], b, bounds), _block_of(grad[w], b, bounds))
+            G_copy[(w, b)] = G[(w, b)].copy()
+    xi = {}
+    held = [set(range(P)) for _ in range(P)]
+    for step in srs_schedule(P):
+        # sparsify every block about to be sent, then send it
+        for w in range(P):
+            for b in step.sent_bag[w]:
+                assert b in held[w], "a sent block must still be held"
+                held[w].discard(b)
+                if b in wanted:
+                    idx, val, xi[(w, b)] = sparsify_with_residual(G[(w, b)], bounds[b], k)
+                    res.sel[(w, b)] = (idx, val)
+                    res.sent_at[(w, b)] = step.i
+        # transmission and summation into the receivers' dense blocks
+        for w in range(P):
+            src = step.source[w]
+            for b in step.received_bag[w]:
+                assert b in held[w], "Theorem 1 violated"
+                if b not in wanted:
+                    continue
+                add_received(G[(w, b)], bounds[b], *res.sel[(src, b)])
+    for w in range(P):
+        assert held[w] == {w}, "after l steps worker w holds only block w"
+        if w in wanted:
+            idx, val, xi[(w, w)] = sparsify_with_residual(G[(w, w)], bounds[w], k)
+            res.sel[(w, w)] = (idx, val)
+            res.sent_at[(w, w)] = 0
+    res.final = {b: res.sel[(b, b)] for b in blocks}
+    res.dense = allgather_densify(res.final, bounds, blocks)
+    for w in range(P):
+        for b in blocks:
+            new = G_copy[(w, b)].copy()
+            pos = res.final[b][0] - bounds[b]
+            new[pos] = xi[(w, b)][pos]
+            res.residual[(w, b)] = new
+            _block_of(acc[w], b, bounds)[...] = new
     return res

@@ -91,3 +91,54 @@ def bf_step(acc_rows, grad_rows, P: int, k: int):
             row.append(ledger.get(x, F32(0.0)) if x in I else A[w][x])
         new_res.append(row)
     return u, new_res, final, drops, local
+
+
+def bf_step_lazy(acc_rows, grad_rows, P: int, k: int):
+    """Lazy sparsification (Sec. III-B "Optimization for SRS", Algorithm 1):
+    dense per-worker rows, each block sparsified once, right before it is sent
+    (or at the end for the reserved block).
+
+    Returns (dense u, new residual rows, final dicts per block, selections
+    {(w, b): dict}).  The residual is built from a per-worker record of what
+    the worker still held (unsent) at each index when it gave the block up.
+    """
+    n = len(acc_rows[0])
+    s = [b * n // P for b in range(P + 1)]
+    A = [[F32(F32(acc_rows[w][x]) + F32(grad_rows[w][x])) for x in range(n)] for w in range(P)]
+    cur = [list(row) for row in A]          # the dense blocks each worker works on
+    l = 0
+    while (1 << l) < P:
+        l += 1
+    sel = {}
+    left_behind = [dict() for _ in range(P)]   # x -> value w kept back when it sparsified x's block
+
+    def sparsify(w, b):
+        block = {x: cur[w][x] for x in range(s[b], s[b + 1])}
+        kept = bf_topk(block, k)
+        sel[(w, b)] = kept
+        for x, v in block.items():
+            left_behind[w][x] = F32(0.0) if x in kept else v
+        return kept
+
+    for i in range(1, l + 1):
+        dist = 1 << (l - i)
+        lo, hi = 1 << (l - i), min(1 << (l - i + 1), P)
+        inbox = {}
+        for w in range(P):
+            inbox[(w + dist) % P] = [(b, dict(sparsify(w, b))) for b in ((w + t) % P for t in range(lo, hi))]
+        for r in range(P):
+            for b, msg in inbox[r]:
+                for x, v in msg.items():
+                    cur[r][x] = F32(cur[r][x] + v)
+    for w in range(P):
+        sparsify(w, w)
+
+    final = {b: sel[(b, b)] for b in range(P)}
+    u = [F32(0.0)] * n
+    I = set()
+    for b in range(P):
+        for x, v in final[b].items():
+            u[x] = v
+            I.add(x)
+    new_res = [[left_behind[w][x] if x in I else A[w][x] for x in range(n)] for w in range(P)]
+    return u, new_res, final, sel
