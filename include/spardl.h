@@ -192,6 +192,70 @@ int spardl_residual_collect(float* acc, int64_t ld_acc, int32_t P, int64_t n, in
                             const int32_t* const* drop_cnt, void* ws, size_t ws_bytes,
                             hipStream_t stream);
 
+/* ---------------------------------------------------------------------------
+ * Lazy sparsification (Sec. III-B "Optimization for SRS"; Algorithm 1).
+ * Held blocks stay dense: a worker sparsifies a block only right before it
+ * sends it (and its reserved block after the last step), and a receiver adds
+ * the received entries into its dense row.  One step, for P workers whose
+ * rows are acc[w*ld_acc ...] (A_w after a plain spardl_residual_add), is:
+ *   for round = 1..l: spardl_lazy_topk(round) on every worker, then
+ *                     spardl_lazy_receive(round);
+ *   spardl_lazy_topk(0) on every worker;
+ *   spardl_allgather_densify(sp, ..., member);      (final block b = sp[b][b])
+ *   spardl_lazy_residual_collect(..., member, saved).
+ * Every worker selects every block once, so sp[w][b] (layout as for
+ * spardl_block_topk) ends holding all P x P selections.
+ * ------------------------------------------------------------------------- */
+
+/* Block top-k of the blocks that workers w0 .. w0 + nworkers - 1 sparsify at
+ * SRS step `round`: for round in [1, l] the bag they send at that step,
+ * blocks b = (w + 2^(l-round) + t) mod P for t < bag_blocks of the step (see
+ * spardl_srs_plan); for round 0 the reserved block b = w.  acc points at row
+ * w0 (row w is acc + (w - w0)*ld_acc) and sp_idx/sp_val at sp[w0]:
+ *   sp_idx/sp_val[((w - w0)*P + b)*k_blk + j], j < k_blk = the top-k_blk
+ *   entries of block b of row w, sorted by ascending index (order as for
+ *   spardl_block_topk).
+ * Other blocks of sp are not written.  ws: a workspace for nworkers rows
+ * (spardl_workspace_bytes(nworkers, P, n, k_blk)), prepared once.
+ * Errors: EINVAL for NULL acc/sp/ws, misaligned ws, nworkers < 1, w0 < 0,
+ * w0 + nworkers > P, P < 1, n < P, n >= 2^31, ld_acc < n, k_blk outside
+ * [1, floor(n/P)], round outside [0, l]; ECAPACITY if ws is too small. */
+int spardl_lazy_topk(const float* acc, int64_t ld_acc, int32_t w0, int32_t nworkers, int64_t n, int32_t P,
+                     int32_t k_blk, int32_t round, int32_t* sp_idx, float* sp_val, void* ws, size_t ws_bytes,
+                     hipStream_t stream);
+
+/* Transmission and summation of SRS step `round` in [1, l] (Algorithm 1),
+ * all P workers at once.  With d = 2^(l-round) and m = bag_blocks of the
+ * step, worker w sent sp[w][b], b = (w + d + t) mod P, t < m, to worker
+ * r = (w + d) mod P, which adds each entry into its dense row:
+ *   saved[(w*P + b)*k_blk + j] = acc[r][x];  acc[r][x] = acc[r][x] + v
+ * for (x, v) = entry j of sp[w][b].  saved (device, P*P*k_blk floats, caller
+ * owned, same layout as sp) keeps what was overwritten for
+ * spardl_lazy_residual_collect; each (w, b) is sent at exactly one step, so
+ * one buffer serves all steps.  Entries whose index lies outside block b are
+ * skipped.  Steps must run in order 1..l, each after spardl_lazy_topk of the
+ * same round on every worker.
+ * Errors: EINVAL for NULL pointers, P < 2 (no steps), n < P, n >= 2^31,
+ * ld_acc < n, k_blk outside [1, floor(n/P)], round outside [1, l]. */
+int spardl_lazy_receive(float* acc, int64_t ld_acc, int32_t P, int64_t n, int32_t k_blk, int32_t round,
+                        const int32_t* sp_idx, const float* sp_val, float* saved, hipStream_t stream);
+
+/* Residual collection of the lazy step (Algorithm 1: "Replace part of
+ * G_copy at indexes I_i with xi_i").  With I the final index set given by
+ * member (the bitmap spardl_allgather_densify wrote), for every worker w:
+ *   acc[w][x] = 0.0f       for x in I that w selected (x in sp[w][b], any b);
+ *   acc[w][x] = A_w[x]     for x not in I that w received at some step (the
+ *                          value saved before the first receipt);
+ *   other entries keep acc: A_w off I, and on I what w held but did not send.
+ * The result is xi^t_w.  saved: the buffer spardl_lazy_receive filled (may
+ * be NULL when P = 1).
+ * Errors: EINVAL for NULL acc/sp_idx/member, misaligned member, NULL saved
+ * with P > 1, P < 1, n < P, n >= 2^31, ld_acc < n, k_blk outside
+ * [1, floor(n/P)]. */
+int spardl_lazy_residual_collect(float* acc, int64_t ld_acc, int32_t P, int64_t n, int32_t k_blk,
+                                 const int32_t* sp_idx, const uint32_t* member, const float* saved,
+                                 hipStream_t stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -153,6 +153,32 @@ struct Fill {
     if ((expr) != hipSuccess) return SPARDL_EDEVICE; \
   } while (0)
 
+// The block top-k pipeline over `units` selection units: level-1 histogram
+// (unless the fused add made it), level-1 select, candidates, exact
+// threshold, emit into sp[row][b].  With `spec` the fused add's speculative
+// candidates may be used; without it the previous-threshold hint is only
+// kept for the all-blocks map (the fused add of the next step reads it).
+int topk_units(const float* acc, int64_t ld_acc, int64_t units, const Units& U, int64_t n, int32_t P, int32_t k_blk,
+               bool make_hist, bool spec, int32_t* sp_idx, float* sp_val, int32_t* local_idx, const Ws& w,
+               const Layout& L, hipStream_t stream) {
+  const bool v4 = aligned16(acc) && ld_acc % 4 == 0 && blocks_vec4(n, P);
+  const int32_t smax = (int32_t)L.tiles_tk;
+  if (make_hist) {
+    SPARDL_TRY(launch_fill(Fill().add(w.hist1, units * HCOPIES * NB1).r, stream));
+    SPARDL_TRY(launch_hist1(acc, ld_acc, units, U, n, P, v4, w.hist1, stream));
+  }
+  uint32_t* hint = U.rel ? nullptr : w.spec_t1;
+  SPARDL_TRY(launch_select1(w.hist1, w.state, units, U, n, P, (uint32_t)k_blk, hint, w.spec_used, spec, acc, ld_acc,
+                            v4, w.err, stream));
+  SPARDL_TRY(launch_collect(acc, ld_acc, units, U, n, P, v4, smax, w.state, w.spec_cnt, (int32_t)L.add_tiles,
+                            w.slot_cnt, w.slot_nbin, w.cand_idx, w.cand_val, w.bin_key, stream));
+  SPARDL_TRY(launch_thresh(0, units, U, n, P, k_blk, smax, 1, nullptr, w.cand_val, w.state, w.slot_cnt,
+                           w.slot_nbin, w.bin_key, w.pre_all, w.pre_ge, w.pre_eq, nullptr, w.err, stream));
+  SPARDL_TRY(launch_emit(0, w.cand_idx, w.cand_val, units, U, n, P, k_blk, 1, smax, w.state, w.slot_cnt,
+                         w.pre_all, w.pre_ge, w.pre_eq, sp_idx, sp_val, local_idx, nullptr, nullptr, w.err, stream));
+  return SPARDL_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -242,23 +268,9 @@ int spardl_block_topk(const float* acc, int64_t ld_acc, int32_t nworkers, int64_
   if (ws_bytes < need) return SPARDL_ECAPACITY;
   const Layout L = make_layout(P, n, k_blk);
   Ws w = carve(ws, ws_bytes, L);
-  const int64_t units = (int64_t)nworkers * P;
-  const bool v4 = aligned16(acc) && ld_acc % 4 == 0 && blocks_vec4(n, P);
-  const int32_t smax = (int32_t)L.tiles_tk;
-  if (!(flags & SPARDL_TOPK_HIST_READY)) {
-    SPARDL_TRY(launch_fill(Fill().add(w.hist1, units * HCOPIES * NB1).r, stream));
-    SPARDL_TRY(launch_hist1(acc, ld_acc, nworkers, n, P, v4, w.hist1, stream));
-  }
   const bool spec = (flags & SPARDL_TOPK_HIST_READY) != 0;   // candidates of the fused add may be used
-  SPARDL_TRY(launch_select1(w.hist1, w.state, units, n, P, (uint32_t)k_blk, w.spec_t1, w.spec_used, spec, acc,
-                            ld_acc, v4, w.err, stream));
-  SPARDL_TRY(launch_collect(acc, ld_acc, nworkers, n, P, v4, smax, w.state, w.spec_cnt, (int32_t)L.add_tiles,
-                            w.slot_cnt, w.slot_nbin, w.cand_idx, w.cand_val, w.bin_key, stream));
-  SPARDL_TRY(launch_thresh(0, units, n, P, k_blk, smax, 1, nullptr, w.cand_val, w.state, w.slot_cnt, w.slot_nbin,
-                           w.bin_key, w.pre_all, w.pre_ge, w.pre_eq, nullptr, w.err, stream));
-  SPARDL_TRY(launch_emit(0, w.cand_idx, w.cand_val, units, n, P, k_blk, 1, smax, w.state, w.slot_cnt, w.pre_all,
-                         w.pre_ge, w.pre_eq, sp_idx, sp_val, local_idx, nullptr, nullptr, w.err, stream));
-  return SPARDL_OK;
+  return topk_units(acc, ld_acc, (int64_t)nworkers * P, all_blocks(P), n, P, k_blk, !spec, spec, sp_idx, sp_val,
+                    local_idx, w, L, stream);
 }
 
 int spardl_sparse_merge_topk(int32_t* sp_idx, float* sp_val, int32_t P, int64_t n, int32_t k_blk,
@@ -278,9 +290,9 @@ int spardl_sparse_merge_topk(int32_t* sp_idx, float* sp_val, int32_t P, int64_t 
   const int32_t smax = (int32_t)L.tiles_mg;
   SPARDL_TRY(launch_merge(sp_idx, sp_val, P, k_blk, d, m, smax, w.hist1, w.slot_cnt, w.cand_idx, w.cand_val,
                           stream));
-  SPARDL_TRY(launch_thresh(1, pairs, n, P, k_blk, smax, 1, w.hist1, w.cand_val, w.state, w.slot_cnt, w.slot_nbin,
+  SPARDL_TRY(launch_thresh(1, pairs, all_blocks(P), n, P, k_blk, smax, 1, w.hist1, w.cand_val, w.state, w.slot_cnt, w.slot_nbin,
                            w.bin_key, w.pre_all, w.pre_ge, w.pre_eq, drop_cnt, w.err, stream));
-  SPARDL_TRY(launch_emit(1, w.cand_idx, w.cand_val, pairs, n, P, k_blk, m, smax, w.state, w.slot_cnt, w.pre_all,
+  SPARDL_TRY(launch_emit(1, w.cand_idx, w.cand_val, pairs, all_blocks(P), n, P, k_blk, m, smax, w.state, w.slot_cnt, w.pre_all,
                          w.pre_ge, w.pre_eq, sp_idx, sp_val, nullptr, drop_idx, drop_val, w.err, stream));
   return SPARDL_OK;
 }
@@ -321,6 +333,53 @@ int spardl_residual_collect(float* acc, int64_t ld_acc, int32_t P, int64_t n, in
                                 drop_cnt[i - 1], in_I, stream));
   }
   if (!member) SPARDL_TRY(launch_bm_mark(sp_idx, P, n, k_blk, bm, false, stream));
+  return SPARDL_OK;
+}
+
+int spardl_lazy_topk(const float* acc, int64_t ld_acc, int32_t w0, int32_t nworkers, int64_t n, int32_t P,
+                     int32_t k_blk, int32_t round, int32_t* sp_idx, float* sp_val, void* ws, size_t ws_bytes,
+                     hipStream_t stream) {
+  if (!acc || !sp_idx || !sp_val || !ws || ws_misaligned(ws) || nworkers < 1 || w0 < 0 || w0 > P - nworkers ||
+      !sizes_ok(P, n, k_blk) || ld_acc < n)
+    return SPARDL_EINVAL;
+  const int32_t l = steps_of(P);
+  if (round < 0 || round > l) return SPARDL_EINVAL;
+  const size_t need = spardl_workspace_bytes(nworkers, P, n, k_blk);
+  if (need == 0) return SPARDL_EINVAL;
+  if (ws_bytes < need) return SPARDL_ECAPACITY;
+  const Layout L = make_layout(P, n, k_blk);
+  Ws w = carve(ws, ws_bytes, L);
+  // round r >= 1: the bag sent at step r, blocks (w + 2^(l-r) + t) mod P, t < m_r; round 0: block w
+  const Units U{round ? (uint32_t)bag_of(P, l, round) : 1u, round ? (uint32_t)(1 << (l - round)) : 0u, 1u,
+                (uint32_t)w0};
+  return topk_units(acc, ld_acc, (int64_t)nworkers * U.m, U, n, P, k_blk, true, false, sp_idx, sp_val, nullptr, w, L,
+                    stream);
+}
+
+int spardl_lazy_receive(float* acc, int64_t ld_acc, int32_t P, int64_t n, int32_t k_blk, int32_t round,
+                        const int32_t* sp_idx, const float* sp_val, float* saved, hipStream_t stream) {
+  if (!acc || !sp_idx || !sp_val || !saved || !sizes_ok(P, n, k_blk) || ld_acc < n) return SPARDL_EINVAL;
+  const int32_t l = steps_of(P);
+  if (round < 1 || round > l) return SPARDL_EINVAL;
+  SPARDL_TRY(launch_lazy_step(acc, ld_acc, P, n, k_blk, 1 << (l - round), bag_of(P, l, round), sp_idx, sp_val, saved,
+                              nullptr, false, stream));
+  return SPARDL_OK;
+}
+
+int spardl_lazy_residual_collect(float* acc, int64_t ld_acc, int32_t P, int64_t n, int32_t k_blk,
+                                 const int32_t* sp_idx, const uint32_t* member, const float* saved,
+                                 hipStream_t stream) {
+  if (!acc || !sp_idx || !member || (reinterpret_cast<uintptr_t>(member) & 3u) || !sizes_ok(P, n, k_blk) ||
+      ld_acc < n)
+    return SPARDL_EINVAL;
+  const int32_t l = steps_of(P);
+  if (l > 0 && !saved) return SPARDL_EINVAL;
+  // selected and final -> 0 (every (w, b) pair of sp is a selection of worker w)
+  SPARDL_TRY(launch_grc_zero(acc, ld_acc, P, n, k_blk, sp_idx, member, stream));
+  // received and not final -> the value before the first receipt
+  for (int32_t i = l; i >= 1; --i)
+    SPARDL_TRY(launch_lazy_step(acc, ld_acc, P, n, k_blk, 1 << (l - i), bag_of(P, l, i), sp_idx, nullptr, const_cast<float*>(saved),
+                                member, true, stream));
   return SPARDL_OK;
 }
 

@@ -81,6 +81,22 @@ inline Blocks make_blocks(int64_t n, int32_t P) {
   return Blocks{(uint32_t)n, (uint32_t)P, (uint32_t)(n / P), (uint32_t)(n % P)};
 }
 
+// Selection units of a block top-k call over rows (workers) w0, w0 + 1, ...:
+// unit u selects in row u / m the block (d + u % m + (rel ? w : 0)) mod P,
+// w = w0 + u / m being the worker.  All blocks of all rows: m = P, d = 0,
+// rel = 0, so unit = row * P + block.  The bag a worker sends at one SRS step:
+// m = bag size, d = distance, rel = 1.
+struct Units {
+  uint32_t m, d, rel, w0;
+  __device__ __forceinline__ void decode(uint32_t u, uint32_t P, uint32_t* row, uint32_t* b) const {
+    const uint32_t r = u / m;
+    *row = r;
+    *b = (d + (u - r * m) + (rel ? w0 + r : 0u)) % P;
+  }
+};
+
+inline Units all_blocks(int32_t P) { return Units{(uint32_t)P, 0u, 0u, 0u}; }
+
 __device__ __forceinline__ int lane_id() { return threadIdx.x & (WAVE - 1); }
 __device__ __forceinline__ int wave_id() { return threadIdx.x / WAVE; }
 

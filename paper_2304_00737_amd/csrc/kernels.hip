@@ -212,12 +212,13 @@ __global__ __launch_bounds__(256) void k_residual_add(float* __restrict__ acc, i
 
 // Level-1 histogram only (block_topk without a fused residual add).
 template <int VEC>
-__global__ __launch_bounds__(256) void k_hist1(const float* __restrict__ acc, int64_t ld_acc, Blocks B,
+__global__ __launch_bounds__(256) void k_hist1(const float* __restrict__ acc, int64_t ld_acc, Blocks B, Units U,
                                                uint32_t G, uint32_t* __restrict__ hist1) {
   __shared__ __align__(16) uint32_t h[NB1];
   const uint32_t g = blockIdx.x % G;
-  const uint32_t wb = blockIdx.x / G;
-  const uint32_t b = wb % B.P, w = wb / B.P;
+  const uint32_t wb = blockIdx.x / G;   // unit
+  uint32_t w, b;
+  U.decode(wb, B.P, &w, &b);
   const uint32_t s = B.start(b), e = B.start(b + 1u);
   const uint32_t t0 = s + g * (uint32_t)ADD_TILE;
   if (t0 >= e) return;
@@ -257,7 +258,7 @@ __global__ __launch_bounds__(256) void k_hist1(const float* __restrict__ acc, in
 // there; otherwise the workgroup rebuilds the block's full histogram from acc.
 // A full histogram must hold exactly the block's entries.
 __global__ __launch_bounds__(1024) void k_select1(uint32_t* __restrict__ hist1, uint32_t* __restrict__ state,
-                                                  Blocks B, uint32_t need, uint32_t* __restrict__ spec_t1,
+                                                  Blocks B, Units U, uint32_t need, uint32_t* __restrict__ spec_t1,
                                                   const uint32_t* __restrict__ spec_used, int spec,
                                                   const float* __restrict__ acc, int64_t ld_acc, int vec4,
                                                   uint32_t* __restrict__ err) {
@@ -286,7 +287,8 @@ __global__ __launch_bounds__(1024) void k_select1(uint32_t* __restrict__ hist1, 
   __syncthreads();
   uint32_t T, above, cnt, ok, total;
   block_select_desc(h, NB1, need, scratch, &T, &above, &cnt, &ok, &total);
-  const uint32_t b = (uint32_t)u % B.P, w = (uint32_t)u / B.P;
+  uint32_t w, b;
+  U.decode((uint32_t)u, B.P, &w, &b);
   const uint32_t s = B.start(b), e = B.start(b + 1u);
   bool full = FH == 0u;
   if (!ok && !full) {   // the threshold fell below the histogram's floor: count the whole block
@@ -326,7 +328,7 @@ __global__ __launch_bounds__(1024) void k_select1(uint32_t* __restrict__ hist1, 
     // the fused add's speculative candidates hold every key >= its floor, so
     // they are usable when the floor is at or below the threshold bin
     st[ST_SPECOK] = (spec && ok && used <= (T << D1_SHIFT)) ? 1u : 0u;
-    spec_t1[u] = ok ? T + 1u : 0u;
+    if (spec_t1) spec_t1[u] = ok ? T + 1u : 0u;
     st[ST_T1] = T;
     st[ST_ABOVE1] = above;
     st[ST_NEED1] = ok ? need - above : 0u;
@@ -350,10 +352,12 @@ struct SlotGeom {
   int32_t nslots;  // slots of this unit
 };
 
-__device__ __forceinline__ SlotGeom slot_geom(int mode, uint32_t unit, const Blocks& B, int64_t kb) {
+__device__ __forceinline__ SlotGeom slot_geom(int mode, uint32_t unit, const Blocks& B, const Units& U,
+                                              int64_t kb) {
   SlotGeom g;
   if (mode == 0) {
-    const uint32_t b = unit % B.P, w = unit / B.P;
+    uint32_t w, b;   // w: the unit's row within the call
+    U.decode(unit, B.P, &w, &b);
     const uint32_t s = B.start(b), e = B.start(b + 1u);
     g.base = (int64_t)w * B.n + s;
     g.len = e - s;
@@ -533,7 +537,7 @@ __device__ __forceinline__ void recollect_wave(uint32_t c0, uint32_t c1, uint32_
 // wave keeps the longest wave short; 64 registers let 8 waves share a SIMD.
 constexpr int COLLECT_GROUP = 4;
 template <int VEC>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(8, 8))) void k_collect(const float* __restrict__ acc, int64_t ld_acc, Blocks B,
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(8, 8))) void k_collect(const float* __restrict__ acc, int64_t ld_acc, Blocks B, Units U,
                                                  uint32_t smax, uint32_t gq, const uint32_t* __restrict__ state,
                                                  const uint32_t* __restrict__ spec_cnt, uint32_t add_tiles,
                                                  uint32_t* __restrict__ slot_cnt, uint32_t* __restrict__ slot_nbin,
@@ -542,7 +546,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(8, 8))) voi
   __shared__ CollectSmem L;
   const uint32_t unit = blockIdx.x / gq;
   const uint32_t slot0 = (blockIdx.x % gq) * (uint32_t)COLLECT_GROUP;
-  const uint32_t b = unit % B.P, w = unit / B.P;
+  uint32_t w, b;
+  U.decode(unit, B.P, &w, &b);
   const uint32_t s = B.start(b), e = B.start(b + 1u);
   if (s + slot0 * (uint32_t)SLOT >= e) return;
   const uint32_t* st = state + (int64_t)unit * ST_WORDS;
@@ -1089,7 +1094,7 @@ __device__ __forceinline__ void thresh_fast_topk(FastSmem& L, int64_t unit, cons
 }
 
 template <int mode>
-__global__ __launch_bounds__(1024) void k_thresh(Blocks B, int32_t kb, int32_t smax,
+__global__ __launch_bounds__(1024) void k_thresh(Blocks B, Units U, int32_t kb, int32_t smax,
                                                  int lps, uint32_t* __restrict__ hist1,
                                                  const float* __restrict__ U_val, uint32_t* __restrict__ state,
                                                  const uint32_t* __restrict__ slot_cnt,
@@ -1103,7 +1108,7 @@ __global__ __launch_bounds__(1024) void k_thresh(Blocks B, int32_t kb, int32_t s
   constexpr int NT = 1024;
   const int64_t unit = blockIdx.x;
   uint32_t* st = state + unit * ST_WORDS;
-  const SlotGeom g = slot_geom(mode, (uint32_t)unit, B, kb);
+  const SlotGeom g = slot_geom(mode, (uint32_t)unit, B, U, kb);
   const uint32_t* __restrict__ cnt = slot_cnt + unit * smax;
   const uint32_t* __restrict__ nbn = slot_nbin + unit * smax;
   const uint32_t* __restrict__ K = bin_key + g.base;
@@ -1334,7 +1339,7 @@ __global__ __launch_bounds__(1024) void k_thresh(Blocks B, int32_t kb, int32_t s
 constexpr int EMIT_R = 16;  // entries per lane per chunk (a crowded slot holds up to 4096)
 template <int MODE>
 __global__ __launch_bounds__(256) void k_emit(
-    const int32_t* __restrict__ cand_idx, const float* __restrict__ cand_val, Blocks B,
+    const int32_t* __restrict__ cand_idx, const float* __restrict__ cand_val, Blocks B, Units U,
     int32_t kb, int32_t m, int32_t smax, uint32_t gq, const uint32_t* __restrict__ state,
     const uint32_t* __restrict__ slot_cnt, const uint32_t* __restrict__ pre_all,
     const uint32_t* __restrict__ pre_ge, const uint32_t* __restrict__ pre_eq, int32_t* __restrict__ out_idx,
@@ -1344,7 +1349,7 @@ __global__ __launch_bounds__(256) void k_emit(
   const uint32_t unit = blockIdx.x / gq;
   const int wv = wave_id();
   const int32_t slot = NPART == 1 ? (int32_t)((blockIdx.x % gq) * 4u + (uint32_t)wv) : (int32_t)(blockIdx.x % gq);
-  const SlotGeom g = slot_geom(MODE, unit, B, kb);
+  const SlotGeom g = slot_geom(MODE, unit, B, U, kb);
   if (slot >= g.nslots) return;   // uniform over the workgroup when NPART > 1
   const int lane = lane_id();
   const uint64_t lt = __lanemask_lt();
@@ -1358,7 +1363,9 @@ __global__ __launch_bounds__(256) void k_emit(
   const int64_t base = g.base + (int64_t)slot * g.ss;
   int64_t o;
   if (MODE == 0) {
-    o = (int64_t)unit * kb;
+    uint32_t w, b;
+    U.decode(unit, B.P, &w, &b);
+    o = ((int64_t)w * B.P + b) * kb;
   } else {
     const uint32_t w = unit / (uint32_t)m, t = unit % (uint32_t)m, b = (w + t) % B.P;
     o = ((int64_t)w * B.P + b) * kb;
@@ -1699,6 +1706,43 @@ __global__ __launch_bounds__(256) void k_grc_drops(float* __restrict__ acc, int6
   }
 }
 
+// ============================================================================ lazy summation
+// One SRS step of the lazy variant (Sec. III-B "Optimization for SRS",
+// Algorithm 1): worker w sent sp[w][b], b = (w + d + t) mod P for t < m, to
+// worker r = (w + d) mod P.
+//  restore = 0: r adds every entry into its dense row, first saving the
+//               value there into saved[w][b] at the entry's position;
+//  restore = 1: r puts the saved value back where the index is not a final
+//               index (bm); run over the steps in reverse order, so the value
+//               before the first receipt is what stays.
+// Within one step each (receiver, block) has one sender whose indices are
+// distinct, so no two threads touch one element.  Entries outside their block
+// are skipped.  Grid: x over a block's k_blk entries, y over pairs (w, t).
+__global__ __launch_bounds__(256) void k_lazy_step(float* __restrict__ acc, int64_t ld_acc, Blocks B, uint32_t kb,
+                                                   uint32_t d, uint32_t m, const int32_t* __restrict__ sp_idx,
+                                                   const float* __restrict__ sp_val, float* __restrict__ saved,
+                                                   const uint32_t* __restrict__ bm, int restore) {
+  const uint32_t npairs = B.P * m;
+  for (uint32_t pair = blockIdx.y; pair < npairs; pair += gridDim.y) {
+    const uint32_t w = pair / m, t = pair - w * m;
+    const uint32_t r = (w + d) % B.P, b = (w + d + t) % B.P;
+    const uint32_t s = B.start(b), e = B.start(b + 1u);
+    const int64_t o = ((int64_t)w * B.P + b) * kb;
+    float* __restrict__ A = acc + (int64_t)r * ld_acc;
+    for (uint32_t j = blockIdx.x * 256u + threadIdx.x; j < kb; j += gridDim.x * 256u) {
+      const int32_t x = sp_idx[o + j];
+      if (x < (int32_t)s || x >= (int32_t)e) continue;
+      if (restore) {
+        if (!in_final(bm, x)) A[x] = saved[o + j];
+      } else {
+        const float old = A[x];
+        saved[o + j] = old;
+        A[x] = old + sp_val[o + j];
+      }
+    }
+  }
+}
+
 // ============================================================================ launchers
 static inline unsigned grid_for(int64_t work, int per_block, unsigned cap) {
   int64_t g = (work + per_block - 1) / per_block;
@@ -1734,52 +1778,52 @@ hipError_t launch_residual_add(float* acc, int64_t ld_acc, const float* grad, in
   return hipGetLastError();
 }
 
-hipError_t launch_hist1(const float* acc, int64_t ld_acc, int32_t nworkers, int64_t n, int32_t P,
+hipError_t launch_hist1(const float* acc, int64_t ld_acc, int64_t nunits, const Units& U, int64_t n, int32_t P,
                         bool vec4, uint32_t* hist1, hipStream_t s) {
   const int64_t maxlen = (n + P - 1) / P;
   const int32_t G = (int32_t)((maxlen + ADD_TILE - 1) / ADD_TILE);
-  const dim3 grid((unsigned)((int64_t)nworkers * P * G));
+  const dim3 grid((unsigned)(nunits * G));
   const Blocks B = make_blocks(n, P);
-  if (vec4) hipLaunchKernelGGL(k_hist1<4>, grid, dim3(256), 0, s, acc, ld_acc, B, (uint32_t)G, hist1);
-  else hipLaunchKernelGGL(k_hist1<1>, grid, dim3(256), 0, s, acc, ld_acc, B, (uint32_t)G, hist1);
+  if (vec4) hipLaunchKernelGGL(k_hist1<4>, grid, dim3(256), 0, s, acc, ld_acc, B, U, (uint32_t)G, hist1);
+  else hipLaunchKernelGGL(k_hist1<1>, grid, dim3(256), 0, s, acc, ld_acc, B, U, (uint32_t)G, hist1);
   return hipGetLastError();
 }
 
-hipError_t launch_select1(uint32_t* hist1, uint32_t* state, int64_t nunits, int64_t n, int32_t P, uint32_t need,
-                          uint32_t* spec_t1, const uint32_t* spec_used, bool spec, const float* acc, int64_t ld_acc,
-                          bool vec4, uint32_t* err, hipStream_t s) {
-  hipLaunchKernelGGL(k_select1, dim3((unsigned)nunits), dim3(1024), 0, s, hist1, state, make_blocks(n, P), need,
+hipError_t launch_select1(uint32_t* hist1, uint32_t* state, int64_t nunits, const Units& U, int64_t n, int32_t P,
+                          uint32_t need, uint32_t* spec_t1, const uint32_t* spec_used, bool spec, const float* acc,
+                          int64_t ld_acc, bool vec4, uint32_t* err, hipStream_t s) {
+  hipLaunchKernelGGL(k_select1, dim3((unsigned)nunits), dim3(1024), 0, s, hist1, state, make_blocks(n, P), U, need,
                      spec_t1, spec_used, spec ? 1 : 0, acc, ld_acc, vec4 ? 1 : 0, err);
   return hipGetLastError();
 }
 
-hipError_t launch_collect(const float* acc, int64_t ld_acc, int32_t nworkers, int64_t n, int32_t P,
+hipError_t launch_collect(const float* acc, int64_t ld_acc, int64_t nunits, const Units& U, int64_t n, int32_t P,
                           bool vec4, int32_t smax, const uint32_t* state, const uint32_t* spec_cnt,
                           int32_t add_tiles, uint32_t* slot_cnt, uint32_t* slot_nbin, int32_t* cand_idx,
                           float* cand_val, uint32_t* bin_key, hipStream_t s) {
   const uint32_t gq = (uint32_t)((smax + COLLECT_GROUP - 1) / COLLECT_GROUP);
-  const dim3 grid((unsigned)((int64_t)nworkers * P * gq));
+  const dim3 grid((unsigned)(nunits * gq));
   const Blocks B = make_blocks(n, P);
-  if (vec4) hipLaunchKernelGGL(k_collect<4>, grid, dim3(256), 0, s, acc, ld_acc, B, (uint32_t)smax, gq, state, spec_cnt, (uint32_t)add_tiles, slot_cnt, slot_nbin, cand_idx, cand_val, bin_key);
-  else hipLaunchKernelGGL(k_collect<1>, grid, dim3(256), 0, s, acc, ld_acc, B, (uint32_t)smax, gq, state, spec_cnt, (uint32_t)add_tiles, slot_cnt, slot_nbin, cand_idx, cand_val, bin_key);
+  if (vec4) hipLaunchKernelGGL(k_collect<4>, grid, dim3(256), 0, s, acc, ld_acc, B, U, (uint32_t)smax, gq, state, spec_cnt, (uint32_t)add_tiles, slot_cnt, slot_nbin, cand_idx, cand_val, bin_key);
+  else hipLaunchKernelGGL(k_collect<1>, grid, dim3(256), 0, s, acc, ld_acc, B, U, (uint32_t)smax, gq, state, spec_cnt, (uint32_t)add_tiles, slot_cnt, slot_nbin, cand_idx, cand_val, bin_key);
   return hipGetLastError();
 }
 
-hipError_t launch_thresh(int mode, int64_t nunits, int64_t n, int32_t P, int32_t kb, int32_t smax, int lps,
-                         uint32_t* hist1, const float* U_val, uint32_t* state, const uint32_t* slot_cnt,
+hipError_t launch_thresh(int mode, int64_t nunits, const Units& U, int64_t n, int32_t P, int32_t kb, int32_t smax,
+                         int lps, uint32_t* hist1, const float* U_val, uint32_t* state, const uint32_t* slot_cnt,
                          const uint32_t* slot_nbin, const uint32_t* bin_key, uint32_t* pre_all, uint32_t* pre_ge,
                          uint32_t* pre_eq, int32_t* drop_cnt, uint32_t* err, hipStream_t s) {
   if (mode == 0)
-    hipLaunchKernelGGL(k_thresh<0>, dim3((unsigned)nunits), dim3(1024), 0, s, make_blocks(n, P), kb, smax, lps, hist1, U_val,
+    hipLaunchKernelGGL(k_thresh<0>, dim3((unsigned)nunits), dim3(1024), 0, s, make_blocks(n, P), U, kb, smax, lps, hist1, U_val,
                        state, slot_cnt, slot_nbin, bin_key, pre_all, pre_ge, pre_eq, drop_cnt, err);
   else
-    hipLaunchKernelGGL(k_thresh<1>, dim3((unsigned)nunits), dim3(1024), 0, s, make_blocks(n, P), kb, smax, lps, hist1, U_val,
+    hipLaunchKernelGGL(k_thresh<1>, dim3((unsigned)nunits), dim3(1024), 0, s, make_blocks(n, P), U, kb, smax, lps, hist1, U_val,
                        state, slot_cnt, slot_nbin, bin_key, pre_all, pre_ge, pre_eq, drop_cnt, err);
   return hipGetLastError();
 }
 
-hipError_t launch_emit(int mode, const int32_t* cand_idx, const float* cand_val, int64_t nunits, int64_t n,
-                       int32_t P, int32_t kb, int32_t m, int32_t smax, const uint32_t* state,
+hipError_t launch_emit(int mode, const int32_t* cand_idx, const float* cand_val, int64_t nunits, const Units& U,
+                       int64_t n, int32_t P, int32_t kb, int32_t m, int32_t smax, const uint32_t* state,
                        const uint32_t* slot_cnt, const uint32_t* pre_all, const uint32_t* pre_ge,
                        const uint32_t* pre_eq, int32_t* out_idx, float* out_val, int32_t* local_idx,
                        int32_t* drop_idx, float* drop_val, uint32_t* err, hipStream_t s) {
@@ -1788,9 +1832,9 @@ hipError_t launch_emit(int mode, const int32_t* cand_idx, const float* cand_val,
   const dim3 grid((unsigned)(nunits * gq));
   const Blocks B = make_blocks(n, P);
   if (mode == 0)
-    hipLaunchKernelGGL(k_emit<0>, grid, dim3(256), 0, s, cand_idx, cand_val, B, kb, m, smax, gq, state, slot_cnt, pre_all, pre_ge, pre_eq, out_idx, out_val, local_idx, drop_idx, drop_val, err);
+    hipLaunchKernelGGL(k_emit<0>, grid, dim3(256), 0, s, cand_idx, cand_val, B, U, kb, m, smax, gq, state, slot_cnt, pre_all, pre_ge, pre_eq, out_idx, out_val, local_idx, drop_idx, drop_val, err);
   else
-    hipLaunchKernelGGL(k_emit<1>, grid, dim3(256), 0, s, cand_idx, cand_val, B, kb, m, smax, gq, state, slot_cnt, pre_all, pre_ge, pre_eq, out_idx, out_val, local_idx, drop_idx, drop_val, err);
+    hipLaunchKernelGGL(k_emit<1>, grid, dim3(256), 0, s, cand_idx, cand_val, B, U, kb, m, smax, gq, state, slot_cnt, pre_all, pre_ge, pre_eq, out_idx, out_val, local_idx, drop_idx, drop_val, err);
   return hipGetLastError();
 }
 
@@ -1822,6 +1866,15 @@ hipError_t launch_grc_zero(float* acc, int64_t ld_acc, int32_t P, int64_t n, int
                            const uint32_t* bm, hipStream_t s) {
   const dim3 grid(grid_for((int64_t)P * kb, 256, 1024), (unsigned)std::min<int32_t>(P, 65535));
   hipLaunchKernelGGL(k_grc_zero, grid, dim3(256), 0, s, acc, ld_acc, (uint32_t)P, (uint32_t)n, (uint32_t)kb, local_idx, bm);
+  return hipGetLastError();
+}
+
+hipError_t launch_lazy_step(float* acc, int64_t ld_acc, int32_t P, int64_t n, int32_t kb, int32_t d, int32_t m,
+                            const int32_t* sp_idx, const float* sp_val, float* saved, const uint32_t* bm,
+                            bool restore, hipStream_t s) {
+  const dim3 grid(grid_for(kb, 256, 1024), (unsigned)std::min<int64_t>((int64_t)P * m, 65535));
+  hipLaunchKernelGGL(k_lazy_step, grid, dim3(256), 0, s, acc, ld_acc, make_blocks(n, P), (uint32_t)kb, (uint32_t)d,
+                     (uint32_t)m, sp_idx, sp_val, saved, bm, restore ? 1 : 0);
   return hipGetLastError();
 }
 

@@ -4,6 +4,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "common.hpp"
+
 namespace spardl {
 
 constexpr int FILL_MAX = 8;
@@ -27,21 +29,22 @@ hipError_t launch_fill(const FillRanges& r, hipStream_t s);
 hipError_t launch_residual_add(float* acc, int64_t ld_acc, const float* grad, int64_t ld_grad,
                                int32_t nworkers, int64_t n, int32_t P, bool vec4, const AddSpec& sp,
                                hipStream_t s);
-hipError_t launch_hist1(const float* acc, int64_t ld_acc, int32_t nworkers, int64_t n, int32_t P,
+// Block top-k stages over nunits selection units (Units in common.hpp).
+hipError_t launch_hist1(const float* acc, int64_t ld_acc, int64_t nunits, const Units& U, int64_t n, int32_t P,
                         bool vec4, uint32_t* hist1, hipStream_t s);
-hipError_t launch_select1(uint32_t* hist1, uint32_t* state, int64_t nunits, int64_t n, int32_t P, uint32_t need,
-                          uint32_t* spec_t1, const uint32_t* spec_used, bool spec, const float* acc, int64_t ld_acc,
-                          bool vec4, uint32_t* err, hipStream_t s);
-hipError_t launch_collect(const float* acc, int64_t ld_acc, int32_t nworkers, int64_t n, int32_t P,
+hipError_t launch_select1(uint32_t* hist1, uint32_t* state, int64_t nunits, const Units& U, int64_t n, int32_t P,
+                          uint32_t need, uint32_t* spec_t1, const uint32_t* spec_used, bool spec, const float* acc,
+                          int64_t ld_acc, bool vec4, uint32_t* err, hipStream_t s);
+hipError_t launch_collect(const float* acc, int64_t ld_acc, int64_t nunits, const Units& U, int64_t n, int32_t P,
                           bool vec4, int32_t smax, const uint32_t* state, const uint32_t* spec_cnt,
                           int32_t add_tiles, uint32_t* slot_cnt, uint32_t* slot_nbin, int32_t* cand_idx,
                           float* cand_val, uint32_t* bin_key, hipStream_t s);
-hipError_t launch_thresh(int mode, int64_t nunits, int64_t n, int32_t P, int32_t kb, int32_t smax, int lps,
-                         uint32_t* hist1, const float* U_val, uint32_t* state, const uint32_t* slot_cnt,
+hipError_t launch_thresh(int mode, int64_t nunits, const Units& U, int64_t n, int32_t P, int32_t kb, int32_t smax,
+                         int lps, uint32_t* hist1, const float* U_val, uint32_t* state, const uint32_t* slot_cnt,
                          const uint32_t* slot_nbin, const uint32_t* bin_key, uint32_t* pre_all, uint32_t* pre_ge,
                          uint32_t* pre_eq, int32_t* drop_cnt, uint32_t* err, hipStream_t s);
-hipError_t launch_emit(int mode, const int32_t* cand_idx, const float* cand_val, int64_t nunits, int64_t n,
-                       int32_t P, int32_t kb, int32_t m, int32_t smax, const uint32_t* state,
+hipError_t launch_emit(int mode, const int32_t* cand_idx, const float* cand_val, int64_t nunits, const Units& U,
+                       int64_t n, int32_t P, int32_t kb, int32_t m, int32_t smax, const uint32_t* state,
                        const uint32_t* slot_cnt, const uint32_t* pre_all, const uint32_t* pre_ge,
                        const uint32_t* pre_eq, int32_t* out_idx, float* out_val, int32_t* local_idx,
                        int32_t* drop_idx, float* drop_val, uint32_t* err, hipStream_t s);
@@ -54,6 +57,9 @@ hipError_t launch_bm_mark(const int32_t* sp_idx, int32_t P, int64_t n, int32_t k
                           hipStream_t s);
 hipError_t launch_grc_zero(float* acc, int64_t ld_acc, int32_t P, int64_t n, int32_t kb, const int32_t* local_idx,
                            const uint32_t* bm, hipStream_t s);
+hipError_t launch_lazy_step(float* acc, int64_t ld_acc, int32_t P, int64_t n, int32_t kb, int32_t d, int32_t m,
+                            const int32_t* sp_idx, const float* sp_val, float* saved, const uint32_t* bm,
+                            bool restore, hipStream_t s);
 hipError_t launch_grc_drops(float* acc, int64_t ld_acc, int64_t n, int32_t m, int32_t kb, int32_t npairs,
                             const int32_t* drop_idx, const float* drop_val, const int32_t* drop_cnt,
                             const uint32_t* bm, hipStream_t s);

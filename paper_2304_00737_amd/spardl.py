@@ -42,7 +42,11 @@ _lib.spardl_block_topk.argtypes = [_p, _i64, _i32, _i64, _i32, _i32, _i32, _p, _
 _lib.spardl_sparse_merge_topk.argtypes = [_p, _p, _i32, _i64, _i32, _i32, _p, _p, _p, _p, _sz, _p]
 _lib.spardl_allgather_densify.argtypes = [_p, _p, _i32, _i64, _i32, _p, _p, _p]
 _lib.spardl_residual_collect.argtypes = [_p, _i64, _i32, _i64, _i32, _p, _p, _p, _p, _p, _p, _p, _sz, _p]
-for _f in ("residual_add", "block_topk", "sparse_merge_topk", "allgather_densify", "residual_collect"):
+_lib.spardl_lazy_topk.argtypes = [_p, _i64, _i32, _i32, _i64, _i32, _i32, _i32, _p, _p, _p, _sz, _p]
+_lib.spardl_lazy_receive.argtypes = [_p, _i64, _i32, _i64, _i32, _i32, _p, _p, _p, _p]
+_lib.spardl_lazy_residual_collect.argtypes = [_p, _i64, _i32, _i64, _i32, _p, _p, _p, _p]
+for _f in ("residual_add", "block_topk", "sparse_merge_topk", "allgather_densify", "residual_collect",
+           "lazy_topk", "lazy_receive", "lazy_residual_collect"):
     getattr(_lib, "spardl_" + _f).restype = ctypes.c_int
 
 
@@ -155,6 +159,29 @@ def residual_collect(acc, P: int, n: int, k_blk: int, local_idx, sp_idx, drop_id
         arr(drop_val), arr(drop_cnt), _ptr(ws), ws_bytes, _stream(stream)))
 
 
+def lazy_topk(acc, w0: int, nworkers: int, n: int, P: int, k_blk: int, round: int, sp_idx, sp_val, ws, *,
+              ld_acc=None, stream=None) -> None:
+    """acc: rows w0 .. w0 + nworkers - 1; sp_idx/sp_val: sp[w0:w0 + nworkers]."""
+    ld_acc = _ld(acc, n) if ld_acc is None else ld_acc
+    _check("lazy_topk", _lib.spardl_lazy_topk(_ptr(acc), ld_acc, w0, nworkers, n, P, k_blk, round, _ptr(sp_idx),
+                                              _ptr(sp_val), _ptr(ws), ws.numel() * ws.element_size(),
+                                              _stream(stream)))
+
+
+def lazy_receive(acc, P: int, n: int, k_blk: int, round: int, sp_idx, sp_val, saved, *, ld_acc=None,
+                 stream=None) -> None:
+    ld_acc = _ld(acc, n) if ld_acc is None else ld_acc
+    _check("lazy_receive", _lib.spardl_lazy_receive(_ptr(acc), ld_acc, P, n, k_blk, round, _ptr(sp_idx),
+                                                    _ptr(sp_val), _ptr(saved), _stream(stream)))
+
+
+def lazy_residual_collect(acc, P: int, n: int, k_blk: int, sp_idx, member, saved, *, ld_acc=None,
+                          stream=None) -> None:
+    ld_acc = _ld(acc, n) if ld_acc is None else ld_acc
+    _check("lazy_residual_collect", _lib.spardl_lazy_residual_collect(
+        _ptr(acc), ld_acc, P, n, k_blk, _ptr(sp_idx), _ptr(member), _ptr(saved), _stream(stream)))
+
+
 def ws_error(ws) -> int:
     """Error word at the start of a workspace (synchronises the current stream)."""
     return int(ws[:4].view(torch.int32).cpu().item())
@@ -244,4 +271,64 @@ class SparDLStep:
                 r = min(self.rows, self.P - w0)
                 self.residual_add_rows(w0, grad[w0:w0 + r], stream)
                 self.block_topk_rows(w0, r, stream)
+        self.finish(stream)
+
+
+class SparDLLazyStep:
+    """Buffers for P simulated workers and one lazy-sparsification step
+    (Sec. III-B "Optimization for SRS", Algorithm 1) through the C ABI.
+
+    acc[P, n] holds the residual between steps (and the workers' dense blocks
+    during a step).  After step(grad): dense holds the global update, member
+    the bitmap of its index set, sp_idx/sp_val[w, b] worker w's selection of
+    block b (final block b in sp[b, b]), saved what the receipts overwrote.
+    """
+
+    def __init__(self, P: int, n: int, k_blk: int, device="cuda", rows_per_call: int = 0):
+        self.P, self.n, self.k_blk = P, n, k_blk
+        self.rows = P if rows_per_call <= 0 else min(rows_per_call, P)
+        dev = torch.device(device)
+        self.acc = torch.zeros((P, n), dtype=torch.float32, device=dev)
+        self.sp_idx = torch.empty((P, P, k_blk), dtype=torch.int32, device=dev)
+        self.sp_val = torch.empty((P, P, k_blk), dtype=torch.float32, device=dev)
+        self.saved = torch.empty((P, P, k_blk), dtype=torch.float32, device=dev)
+        self.l, self.distance, self.bags = srs_plan(P)
+        self.dense = torch.empty(n, dtype=torch.float32, device=dev)
+        self.member = torch.empty(member_words(n), dtype=torch.int32, device=dev)
+        self.ws = workspace(self.rows, P, n, k_blk, device=dev)
+
+    def residual_add_rows(self, w0: int, grad_rows, stream=None):
+        r = grad_rows.shape[0]
+        residual_add(self.acc[w0:w0 + r], grad_rows, r, self.n, 0, None, stream=stream)
+
+    def topk_round(self, i: int, stream=None):
+        """Every worker's selection for step i (0: the reserved blocks)."""
+        for w0 in range(0, self.P, self.rows):
+            r = min(self.rows, self.P - w0)
+            s = slice(w0, w0 + r)
+            lazy_topk(self.acc[s], w0, r, self.n, self.P, self.k_blk, i, self.sp_idx[s], self.sp_val[s], self.ws,
+                      stream=stream)
+
+    def receive(self, i: int, stream=None):
+        lazy_receive(self.acc, self.P, self.n, self.k_blk, i, self.sp_idx, self.sp_val, self.saved, stream=stream)
+
+    def densify(self, stream=None):
+        allgather_densify(self.sp_idx, self.sp_val, self.P, self.n, self.k_blk, self.dense, self.member,
+                          stream=stream)
+
+    def collect(self, stream=None):
+        lazy_residual_collect(self.acc, self.P, self.n, self.k_blk, self.sp_idx, self.member,
+                              self.saved if self.l else None, stream=stream)
+
+    def finish(self, stream=None):
+        """Everything after the residual add of every worker."""
+        for i in range(1, self.l + 1):
+            self.topk_round(i, stream)
+            self.receive(i, stream)
+        self.topk_round(0, stream)
+        self.densify(stream)
+        self.collect(stream)
+
+    def step(self, grad, stream=None):
+        self.residual_add_rows(0, grad, stream)
         self.finish(stream)

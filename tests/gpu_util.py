@@ -128,3 +128,31 @@ def ws_spec_ok(st) -> list:
     L = ws_layout(st.P, st.n, st.k_blk, st.ws.numel())
     words = st.ws[L["state"]:L["state"] + st.P * st.P * 16 * 4].view(torch.int32).cpu().numpy()
     return [bool(words[u * 16 + 7]) for u in range(st.P * st.P)]
+
+
+def compare_lazy_step(st, res, P: int, n: int, kb: int, blocks=None) -> None:
+    """Compare the GPU state after one lazy step with an oracle LazyStepResult:
+    every worker's selection of every listed block, the dense update, the
+    membership bitmap of I and the new residuals, bit for bit."""
+    blocks = list(range(P)) if blocks is None else list(blocks)
+    bounds = so.block_bounds(n, P)
+    sp_idx = st.sp_idx[:, blocks].cpu().numpy()
+    sp_val = st.sp_val[:, blocks].cpu().numpy()
+    for w in range(P):
+        for j, b in enumerate(blocks):
+            si, sv = res.sel[(w, b)]
+            assert_idx_equal(sp_idx[w, j], si, f"selection w={w} b={b} (sent at step {res.sent_at[(w, b)]})")
+            assert_bits_equal(sp_val[w, j], sv, f"selection value w={w} b={b}")
+    words = st.member.cpu().numpy()
+    mbits = np.unpackbits(words.view(np.uint8), bitorder="little").astype(bool)
+    assert not mbits[n:].any(), "member bits at or above n"
+    for b in blocks:
+        got = st.dense[bounds[b]:bounds[b + 1]].cpu().numpy()
+        assert_bits_equal(got, res.dense[b], f"dense block {b}")
+        want = np.zeros(bounds[b + 1] - bounds[b], bool)
+        want[np.asarray(res.final[b][0], np.int64) - bounds[b]] = True
+        assert np.array_equal(mbits[bounds[b]:bounds[b + 1]], want), f"member bits block {b}"
+    for w in range(P):
+        for b in blocks:
+            got = st.acc[w, bounds[b]:bounds[b + 1]].cpu().numpy()
+            assert_bits_equal(got, res.residual[(w, b)], f"residual w={w} b={b}")

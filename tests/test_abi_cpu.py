@@ -143,6 +143,30 @@ def test_argument_errors_enqueue_nothing():
                                        sz(1 << 30), null) == EINVAL
     assert lib.spardl_residual_collect(p, i64(100), i32(4), i64(100), i32(3), p, p, ctypes.c_void_p(0x1001),
                                        ok3, ok3, ok3, null, sz(0), null) == EINVAL
+    # lazy_topk (P = 4, l = 2): round outside [0, l], rows outside [0, P), ld < n, small or misaligned ws
+    big = sz(1 << 30)
+    lt = lambda ld, w0, nw, rnd, ws, wsz: lib.spardl_lazy_topk(p, i64(ld), i32(w0), i32(nw), i64(100), i32(4),
+                                                               i32(3), i32(rnd), p, p, ws, wsz, null)
+    assert lt(100, 0, 1, 3, p, big) == EINVAL
+    assert lt(100, 0, 1, -1, p, big) == EINVAL
+    assert lt(100, 3, 2, 1, p, big) == EINVAL
+    assert lt(100, -1, 1, 1, p, big) == EINVAL
+    assert lt(100, 0, 0, 1, p, big) == EINVAL
+    assert lt(99, 0, 1, 1, p, big) == EINVAL
+    assert lt(100, 0, 1, 1, q, big) == EINVAL
+    assert lt(100, 0, 1, 1, null, big) == EINVAL
+    assert lt(100, 0, 1, 1, p, sz(64)) == ECAP
+    # lazy_receive: P = 1 has no steps; round outside [1, l]; NULL saved
+    assert lib.spardl_lazy_receive(p, i64(100), i32(1), i64(100), i32(3), i32(1), p, p, p, null) == EINVAL
+    assert lib.spardl_lazy_receive(p, i64(100), i32(4), i64(100), i32(3), i32(0), p, p, p, null) == EINVAL
+    assert lib.spardl_lazy_receive(p, i64(100), i32(4), i64(100), i32(3), i32(3), p, p, p, null) == EINVAL
+    assert lib.spardl_lazy_receive(p, i64(100), i32(4), i64(100), i32(3), i32(1), p, p, null, null) == EINVAL
+    # lazy_residual_collect: NULL or misaligned member, NULL saved with P > 1, k_blk too large
+    assert lib.spardl_lazy_residual_collect(p, i64(100), i32(4), i64(100), i32(3), p, null, p, null) == EINVAL
+    assert lib.spardl_lazy_residual_collect(p, i64(100), i32(4), i64(100), i32(3), p, ctypes.c_void_p(0x1002), p,
+                                            null) == EINVAL
+    assert lib.spardl_lazy_residual_collect(p, i64(100), i32(4), i64(100), i32(3), p, p, null, null) == EINVAL
+    assert lib.spardl_lazy_residual_collect(p, i64(100), i32(4), i64(100), i32(26), p, p, p, null) == EINVAL
     for s in (0, -1, -2, -3, 7):
         assert lib.spardl_strerror(s)
 

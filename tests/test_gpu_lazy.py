@@ -1,0 +1,133 @@
+"""Bit-exact parity of the lazy-sparsification step (Sec. III-B "Optimization
+for SRS", Algorithm 1) through the C ABI with the CPU oracle's
+spardl_step_lazy: every worker's selection of every block, the dense update,
+the membership bitmap of the final index set and the new residuals, over
+several consecutive steps (the residual is carried)."""
+
+import numpy as np
+import pytest
+
+from oracle import spardl_oracle as so
+from tests.conftest import gpu_available
+from tests.gpu_util import assert_bits_equal, assert_idx_equal, check_ws, compare_lazy_step, log
+from tests.test_gpu_parity import STEP_CASES
+
+pytestmark = pytest.mark.gpu
+
+if gpu_available():
+    import torch
+    from paper_2304_00737_amd import spardl
+    from paper_2304_00737_amd import workloads as W
+
+
+def _dev(a):
+    return torch.from_numpy(np.ascontiguousarray(a)).cuda()
+
+
+def _run(P, n, kb, kind, steps, rows=0, seed=0):
+    st = spardl.SparDLLazyStep(P, n, kb, rows_per_call=rows)
+    acc = np.zeros((P, n), np.float32)
+    for t in range(steps):
+        grad = W.small_rows(kind, P, n, 100 * t + P + seed)
+        st.step(_dev(grad))
+        check_ws(st)
+        res = so.spardl_step_lazy([acc[w] for w in range(P)], [grad[w] for w in range(P)], P, n, kb)
+        compare_lazy_step(st, res, P, n, kb)
+
+
+@pytest.mark.parametrize("P,n,kb,kind,steps", STEP_CASES)
+def test_lazy_step(P, n, kb, kind, steps):
+    log(f"lazy step P={P} n={n} kb={kb} kind={kind} steps={steps}")
+    _run(P, n, kb, kind, steps)
+
+
+@pytest.mark.parametrize("P,n,kb,rows", [(8, 50000, 100, 1), (7, 70001, 501, 3), (5, 10007, 3, 2)])
+def test_lazy_rows_per_call(P, n, kb, rows):
+    """A workspace for `rows` workers: each round's selections run a few
+    workers at a time."""
+    log(f"lazy step rows_per_call={rows} P={P} n={n} kb={kb}")
+    _run(P, n, kb, "normal", 3, rows=rows, seed=7)
+
+
+@pytest.mark.parametrize("P,w0,nw", [(8, 0, 8), (8, 3, 2), (5, 4, 1), (6, 1, 4)])
+def test_lazy_topk_rounds_alone(P, w0, nw):
+    """One selection call per round on rows w0 .. w0 + nw - 1: exactly the
+    blocks of the round's bag (or the reserved block) are written, each the
+    local top-k of that block; every other entry of sp is left alone."""
+    n, kb = 30011, 37
+    log(f"lazy topk rounds P={P} w0={w0} nw={nw}")
+    acc = W.small_rows("normal", P, n, 55 + P)
+    acc_d = _dev(acc)
+    bounds = so.block_bounds(n, P)
+    ws = spardl.workspace(nw, P, n, kb)
+    for rnd in range(so.num_steps(P) + 1):
+        sp_i = torch.full((P, P, kb), -7, dtype=torch.int32, device="cuda")
+        sp_v = torch.full((P, P, kb), 3.5, dtype=torch.float32, device="cuda")
+        s = slice(w0, w0 + nw)
+        spardl.lazy_topk(acc_d[s], w0, nw, n, P, kb, rnd, sp_i[s], sp_v[s], ws)
+        torch.cuda.synchronize()
+        assert spardl.ws_error(ws) == 0
+        gi, gv = sp_i.cpu().numpy(), sp_v.cpu().numpy()
+        for w in range(P):
+            if rnd == 0:
+                mine = {w}
+            else:
+                mine = set(so.srs_schedule(P)[rnd - 1].sent_bag[w])
+            for b in range(P):
+                if w0 <= w < w0 + nw and b in mine:
+                    li, lv = so.local_sparsify(acc[w, bounds[b]:bounds[b + 1]], bounds[b], kb)
+                    assert_idx_equal(gi[w, b], li, f"round {rnd} w={w} b={b}")
+                    assert_bits_equal(gv[w, b], lv, f"round {rnd} w={w} b={b}")
+                else:
+                    assert (gi[w, b] == -7).all() and (gv[w, b] == 3.5).all(), f"round {rnd} wrote w={w} b={b}"
+
+
+def test_lazy_workload1_full():
+    wl = W.config(1)
+    P, n, kb = wl.P, wl.n, wl.k_blk
+    log(f"lazy cfg1 {wl.describe()}")
+    st = spardl.SparDLLazyStep(P, n, kb)
+    acc = np.zeros((P, n), np.float32)
+    for t in range(1, wl.steps + 1):
+        grad = np.stack([W.gradient(wl, t, w) for w in range(P)])
+        st.step(_dev(grad))
+        check_ws(st)
+        res = so.spardl_step_lazy([acc[w] for w in range(P)], [grad[w] for w in range(P)], P, n, kb)
+        compare_lazy_step(st, res, P, n, kb)
+
+
+def _run_config(cfg_id, blocks):
+    """A full-size workload in the configuration the benchmark uses; the
+    oracle recomputes the listed block indices (blocks never exchange data)."""
+    wl = W.config(cfg_id)
+    P, n, kb = wl.P, wl.n, wl.k_blk
+    log(f"lazy workload {cfg_id}: {wl.describe()} blocks={blocks}")
+    bounds = so.block_bounds(n, P)
+    blocks = list(range(P)) if blocks is None else blocks
+    st = spardl.SparDLLazyStep(P, n, kb)
+    grad_d = torch.empty((P, n), dtype=torch.float32, device="cuda")
+    host = torch.empty(n, dtype=torch.float32).pin_memory()
+    acc = [{b: np.zeros(bounds[b + 1] - bounds[b], np.float32) for b in blocks} for _ in range(P)]
+    for t in range(1, wl.steps + 1):
+        grad = [dict() for _ in range(P)]
+        for w in range(P):
+            W.fill(host.numpy(), wl, t, w)
+            grad_d[w].copy_(host)
+            torch.cuda.synchronize()
+            for b in blocks:
+                grad[w][b] = host.numpy()[bounds[b]:bounds[b + 1]].copy()
+        st.step(grad_d)
+        torch.cuda.synchronize()
+        check_ws(st)
+        log(f"  step {t}: GPU done, oracle on {len(blocks)} block indices")
+        res = so.spardl_step_lazy(acc, grad, P, n, kb, blocks=blocks)
+        compare_lazy_step(st, res, P, n, kb, blocks=blocks)
+        log(f"  step {t}: bit-exact")
+
+
+def test_lazy_workload2_resnet50_sized_full():
+    _run_config(2, None)
+
+
+def test_lazy_workload4_bert_sized_sampled():
+    _run_config(4, [2, 15])
