@@ -62,7 +62,7 @@ def _traffic_from_profiles(kernel: str, src_hash: str, units_per_launch: float):
     return k.get("bytes_per_launch")
 
 
-def cpu_baseline(wl, max_seconds: float = 25.0):
+def cpu_baseline(wl, max_seconds: float = 25.0, lazy: bool = False):
     """The oracle, as it stands, on a bounded sample of the same workload:
     whole block indices of one step (blocks never interact, so a block index
     is a self-contained unit of the step)."""
@@ -78,7 +78,7 @@ def cpu_baseline(wl, max_seconds: float = 25.0):
         acc = [{b: np.zeros(bounds[b + 1] - bounds[b], np.float32)} for _ in range(P)]
         grad = [{b: W.gradient(wl, 1, w, bounds[b], bounds[b + 1] - bounds[b])} for w in range(P)]
         t0 = time.perf_counter()
-        so.spardl_step(acc, grad, P, n, kb, blocks=[b])
+        (so.spardl_step_lazy if lazy else so.spardl_step)(acc, grad, P, n, kb, blocks=[b])
         elapsed += time.perf_counter() - t0
         done_elems += P * (bounds[b + 1] - bounds[b])
         blocks.append(b)
@@ -95,6 +95,9 @@ def main() -> int:
     ap.add_argument("--steps", type=int, default=30)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", type=int, default=2, help="synthetic workload id (1-5)")
+    ap.add_argument("--variant", choices=("eager", "lazy"), default="eager",
+                    help="eager: re-select after every merge (the hot path); lazy: sparsify a block only "
+                         "when it is sent (Sec. III-B, Optimization for SRS)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--calib-copy", action="store_true",
                     help="first run one untimed device-to-device copy of CALIB_BYTES (a reference "
@@ -116,6 +119,7 @@ def main() -> int:
     P, n, kb = wl.P, wl.n, wl.k_blk
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
+    lazy = args.variant == "lazy"
     if 4.0 * P * n * (wl.steps + 1) > PER_WORKER_BYTES:
         return run_per_worker(args, wl, dev)
 
@@ -139,16 +143,27 @@ def main() -> int:
         torch.cuda.synchronize()
         del src, dst
 
-    st = spardl.SparDLStep(P, n, kb, device=dev)
     stream = torch.cuda.current_stream()
+    if lazy:
+        st = spardl.SparDLLazyStep(P, n, kb, device=dev)
+        calls = ["residual_add"] + [c for i in range(1, st.l + 1) for c in (f"topk_step{i}", f"receive_step{i}")] + \
+                ["topk_reserved", "allgather_densify", "residual_collect"]
 
-    calls = ["residual_add", "block_topk"] + [f"merge_step{i}" for i in range(1, st.l + 1)] + \
-            ["allgather_densify", "residual_collect"]
+        def call_fns(j):
+            g = grads[j % len(grads)]
+            fns = [lambda: st.residual_add_rows(0, g)]
+            for i in range(1, st.l + 1):
+                fns += [lambda i=i: st.topk_round(i), lambda i=i: st.receive(i)]
+            return fns + [lambda: st.topk_round(0), st.densify, st.collect]
+    else:
+        st = spardl.SparDLStep(P, n, kb, device=dev)
+        calls = ["residual_add", "block_topk"] + [f"merge_step{i}" for i in range(1, st.l + 1)] + \
+                ["allgather_densify", "residual_collect"]
 
-    def call_fns(j):
-        g = grads[j % len(grads)]
-        return [lambda: st.residual_add(g), st.block_topk] + \
-               [(lambda i=i: st.merge_round(i)) for i in range(1, st.l + 1)] + [st.densify, st.collect]
+        def call_fns(j):
+            g = grads[j % len(grads)]
+            return [lambda: st.residual_add(g), st.block_topk] + \
+                   [(lambda i=i: st.merge_round(i)) for i in range(1, st.l + 1)] + [st.densify, st.collect]
 
     def ev():
         return torch.cuda.Event(enable_timing=True)
@@ -173,7 +188,7 @@ def main() -> int:
     assert spardl.ws_error(st.ws) == 0
     total_ms = start.elapsed_time(end)
     ms_per_step = total_ms / args.steps
-    dc = [t.cpu().numpy() for t in st.drop_cnt]          # drops of the last timed step
+    dc = [] if lazy else [t.cpu().numpy() for t in st.drop_cnt]   # drops of the last timed step
 
     # ---- per-call attribution (untimed for `value`): events around every call.
     # An event record costs a fixed marker overhead on the stream; it is
@@ -200,9 +215,13 @@ def main() -> int:
     k_mid = [(ev(), ev()) for _ in range(args.steps)]
     for j in range(args.steps):
         k_mid[j][0].record(stream)
-        st.residual_add(g0)
-        k_mid[j][1].record(stream)
-        st.block_topk()
+        if lazy:
+            st.residual_add_rows(0, g0)
+            k_mid[j][1].record(stream)
+        else:
+            st.residual_add(g0)
+            k_mid[j][1].record(stream)
+            st.block_topk()
     torch.cuda.synchronize()
     add_ms = sum(a.elapsed_time(b) for a, b in k_mid) / args.steps - marker_ms
     assert spardl.ws_error(st.ws) == 0
@@ -214,25 +233,37 @@ def main() -> int:
     pairs = [P * m for m in st.bags]
     alg = {
         "residual_add": 12.0 * P * n,                              # read G, read xi, write A
-        "block_topk": 4.0 * P * n + 12.0 * P * P * kb,             # read A; write idx, val, local idx
         "allgather_densify": 4.0 * n + n / 8.0 + 8.0 * P * kb,     # write u and the bitmap of I; read the final blocks
     }
-    for i, pc in enumerate(pairs, start=1):
-        alg[f"merge_step{i}"] = 32.0 * pc * kb                     # read held + received, write kept + dropped
-    drops_total = float(sum(int(d.sum()) for d in dc))
-    # read local idx and drop lists; read+write touched residual entries (upper bound); the
-    # membership lookups hit the bitmap of I that densify wrote (n/8 bytes, cache resident)
-    alg["residual_collect"] = 4.0 * P * P * kb + 8.0 * drops_total + 8.0 * (P * P * kb + drops_total)
+    if lazy:
+        blk = n / P
+        for i, pc in enumerate(pairs, start=1):
+            alg[f"topk_step{i}"] = 4.0 * pc * blk + 8.0 * pc * kb  # read the sent blocks; write idx, val
+            alg[f"receive_step{i}"] = 20.0 * pc * kb               # read idx, val; read, save and write acc
+        alg["topk_reserved"] = 4.0 * P * blk + 8.0 * P * kb
+        # read every selection; zero the selected final entries (upper bound: all); restore the
+        # received entries off I (read idx and saved value, write; upper bound: all)
+        alg["residual_collect"] = 8.0 * P * P * kb + 12.0 * sum(pairs) * kb
+    else:
+        alg["block_topk"] = 4.0 * P * n + 12.0 * P * P * kb        # read A; write idx, val, local idx
+        for i, pc in enumerate(pairs, start=1):
+            alg[f"merge_step{i}"] = 32.0 * pc * kb                 # read held + received, write kept + dropped
+        drops_total = float(sum(int(d.sum()) for d in dc))
+        # read local idx and drop lists; read+write touched residual entries (upper bound); the
+        # membership lookups hit the bitmap of I that densify wrote (n/8 bytes, cache resident)
+        alg["residual_collect"] = 4.0 * P * P * kb + 8.0 * drops_total + 8.0 * (P * P * kb + drops_total)
     dominant = max(calls, key=lambda c: per_call_ms[c])
     dom_ms = add_ms if dominant == "residual_add" else per_call_ms[dominant]
     achieved = alg[dominant] / (dom_ms * 1e-3) / 1e9
     src_hash = _kernel_src_hash()
-    traffic = _traffic_from_profiles(dominant, src_hash, 1.0)
+    # the stored counter readings are of the fused add (eager variant)
+    traffic = None if lazy else _traffic_from_profiles(dominant, src_hash, 1.0)
     core_bytes = sum(v for k, v in alg.items() if k != "allgather_densify")
     full_bytes = sum(alg.values())
 
     out = {
-        "metric": "gradient elements/sec per full SparDL step (P=8 virtual); % of HBM peak",
+        "metric": ("gradient elements/sec per full SparDL step, lazy sparsification (P=8 virtual); % of HBM peak"
+                   if lazy else "gradient elements/sec per full SparDL step (P=8 virtual); % of HBM peak"),
         "value": value,
         "unit": "elements/s",
         "n_gpus": 1,
@@ -246,7 +277,7 @@ def main() -> int:
         "data": "synthetic",
         "config": {"workload": wl.name, "P": P, "n_per_worker": n, "density": f"{wl.density[0]}/{wl.density[1]}",
                    "k_per_block": kb, "gradient_batches": wl.steps, "residual": "carried across steps",
-                   "segments": len(wl.seg_len), "seed": W.SEED_BASE},
+                   "segments": len(wl.seg_len), "seed": W.SEED_BASE, "variant": args.variant},
         "roofline": {"bound": "hbm", "kernel": "k_residual_add" if dominant == "residual_add" else dominant,
                      "achieved": achieved, "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS, "traffic": traffic,
@@ -260,7 +291,7 @@ def main() -> int:
         "kernel_src": src_hash,
     }
     if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(wl)
+        out["cpu_baseline"] = cpu_baseline(wl, lazy=lazy)
     print(json.dumps(out), flush=True)
     return 0
 
@@ -282,7 +313,11 @@ def run_per_worker(args, wl, dev) -> int:
     from paper_2304_00737_amd import workloads as W
 
     P, n, kb = wl.P, wl.n, wl.k_blk
-    st = spardl.SparDLStep(P, n, kb, device=dev, rows_per_call=1)
+    lazy = args.variant == "lazy"
+    if lazy:
+        st = spardl.SparDLLazyStep(P, n, kb, device=dev, rows_per_call=1)
+    else:
+        st = spardl.SparDLStep(P, n, kb, device=dev, rows_per_call=1)
     gen = W.DeviceGenerator(wl, device=dev)
     g = torch.empty((1, n), dtype=torch.float32, device=dev)
     stream = torch.cuda.current_stream()
@@ -306,7 +341,8 @@ def run_per_worker(args, wl, dev) -> int:
             e[0].record(stream)
             st.residual_add_rows(w, g)
             e[1].record(stream)
-            st.block_topk_rows(w, 1)
+            if not lazy:   # the lazy variant selects inside finish(), round by round
+                st.block_topk_rows(w, 1)
             e[2].record(stream)
             marks.append(e)
         f = (ev(), ev())
@@ -316,7 +352,7 @@ def run_per_worker(args, wl, dev) -> int:
         torch.cuda.synchronize()
         assert spardl.ws_error(st.ws) == 0
         add = sum(a.elapsed_time(b) for a, b, _ in marks) - P * marker_ms
-        topk = sum(b.elapsed_time(c) for _, b, c in marks) - P * marker_ms
+        topk = 0.0 if lazy else sum(b.elapsed_time(c) for _, b, c in marks) - P * marker_ms
         tail = f[0].elapsed_time(f[1]) - marker_ms
         return add, topk, tail
 
@@ -335,7 +371,8 @@ def run_per_worker(args, wl, dev) -> int:
     achieved = alg_add / (add_launch_ms * 1e-3) / 1e9
     full = 16.0 * P * n + 4.0 * n + n / 8.0 + 12.0 * P * P * kb
     out = {
-        "metric": "gradient elements/sec per full SparDL step (P=8 virtual); % of HBM peak",
+        "metric": ("gradient elements/sec per full SparDL step, lazy sparsification (P=8 virtual); % of HBM peak"
+                   if lazy else "gradient elements/sec per full SparDL step (P=8 virtual); % of HBM peak"),
         "value": P * n / (ms_per_step * 1e-3),
         "unit": "elements/s",
         "n_gpus": 1,
@@ -349,7 +386,7 @@ def run_per_worker(args, wl, dev) -> int:
         "data": "synthetic",
         "config": {"workload": wl.name, "P": P, "n_per_worker": n, "density": f"{wl.density[0]}/{wl.density[1]}",
                    "k_per_block": kb, "gradient_batches": wl.steps, "residual": "carried across steps",
-                   "segments": len(wl.seg_len), "seed": W.SEED_BASE,
+                   "segments": len(wl.seg_len), "seed": W.SEED_BASE, "variant": args.variant,
                    "timing": "sum of event-timed hot calls; each worker's gradient generated on the GPU "
                              "between them (one-row workspace)"},
         "roofline": {"bound": "hbm", "kernel": "k_residual_add", "achieved": achieved, "peak": HBM_PEAK_GBS,
@@ -357,8 +394,9 @@ def run_per_worker(args, wl, dev) -> int:
                      "alg_bytes_per_launch": alg_add, "avg_launch_ms": add_launch_ms},
         "step_roofline": {"alg_bytes_full": full, "achieved_full_GBs": full / (ms_per_step * 1e-3) / 1e9,
                           "frac_full": full / (ms_per_step * 1e-3) / 1e9 / HBM_PEAK_GBS},
-        "per_call_ms": {"residual_add_all_workers": add_ms, "block_topk_all_workers": topk_ms,
-                        "srs_densify_collect": tail_ms},
+        "per_call_ms": ({"residual_add_all_workers": add_ms, "rounds_densify_collect": tail_ms} if lazy else
+                        {"residual_add_all_workers": add_ms, "block_topk_all_workers": topk_ms,
+                         "srs_densify_collect": tail_ms}),
         "event_marker_ms": marker_ms,
         "wall_s": time.time() - t0,
         "kernel_src": _kernel_src_hash(),

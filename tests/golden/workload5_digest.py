@@ -8,7 +8,8 @@ output on that block index; the GPU test hashes its own outputs the same way.
 Every block index of every output depends only on that block index of the
 inputs, so one index exercises every kernel at full size.
 
-    python tests/golden/workload5_digest.py     # writes workload5_block17.json
+    python tests/golden/workload5_digest.py          # writes workload5_block17.json
+    python tests/golden/workload5_digest.py --lazy   # lazy sparsification: workload5_block17_lazy.json
 """
 
 import hashlib
@@ -24,6 +25,7 @@ if ROOT not in sys.path:
 
 BLOCK = 17
 OUT = os.path.join(os.path.dirname(os.path.abspath(__file__)), f"workload5_block{BLOCK}.json")
+OUT_LAZY = os.path.join(os.path.dirname(os.path.abspath(__file__)), f"workload5_block{BLOCK}_lazy.json")
 
 
 def _h(*arrays) -> hashlib.sha256:
@@ -58,7 +60,20 @@ def step_digests(P, block, bags, sp, local, drops, dense, residual) -> dict:
             "dense": _h(np.asarray(dense, "<f4")).hexdigest(), "residual": hr.hexdigest()}
 
 
+def lazy_step_digests(P, sel, dense, residual) -> dict:
+    """sel(w): worker w's selection (idx, val) of the block; residual(w): its
+    new residual on the block; dense: the decoded update on the block."""
+    hs, hr = hashlib.sha256(), hashlib.sha256()
+    for w in range(P):
+        i_, v_ = sel(w)
+        hs.update(np.asarray(i_, "<i4").tobytes())
+        hs.update(np.asarray(v_, "<f4").tobytes())
+        hr.update(np.asarray(residual(w), "<f4").tobytes())
+    return {"sel": hs.hexdigest(), "dense": _h(np.asarray(dense, "<f4")).hexdigest(), "residual": hr.hexdigest()}
+
+
 def main() -> None:
+    lazy = "--lazy" in sys.argv[1:]
     from oracle import spardl_oracle as so
     from paper_2304_00737_amd import workloads as W
     wl = W.config(5)
@@ -76,15 +91,24 @@ def main() -> None:
             W.fill(h, wl, t, w, x0=bounds[b])
             grad.append({b: h})
         print(f"step {t}: inputs generated", flush=True)
-        res = so.spardl_step(acc, grad, P, n, kb, blocks=[b])
-        print(f"step {t}: oracle done", flush=True)
-        bags = [len(step.received_bag[0]) for step in so.srs_schedule(P)]
-        d = step_digests(P, b, bags, lambda w: res.S[(w, b)], lambda w: res.local[(w, b)][0],
-                         lambda i, w: res.drops[(i, w, b)], res.dense[b], lambda w: res.residual[(w, b)])
+        if lazy:
+            res = so.spardl_step_lazy(acc, grad, P, n, kb, blocks=[b])
+            print(f"step {t}: oracle done", flush=True)
+            d = lazy_step_digests(P, lambda w: res.sel[(w, b)], res.dense[b], lambda w: res.residual[(w, b)])
+        else:
+            res = so.spardl_step(acc, grad, P, n, kb, blocks=[b])
+            print(f"step {t}: oracle done", flush=True)
+            bags = [len(step.received_bag[0]) for step in so.srs_schedule(P)]
+            d = step_digests(P, b, bags, lambda w: res.S[(w, b)], lambda w: res.local[(w, b)][0],
+                             lambda i, w: res.drops[(i, w, b)], res.dense[b], lambda w: res.residual[(w, b)])
         out["steps"].append(d)
-    with open(OUT, "w") as f:
+        del res, grad
+    path = OUT_LAZY if lazy else OUT
+    if lazy:
+        out["variant"] = "lazy sparsification"
+    with open(path, "w") as f:
         json.dump(out, f, indent=1)
-    print("wrote", OUT)
+    print("wrote", path)
 
 
 if __name__ == "__main__":

@@ -131,3 +131,48 @@ def test_lazy_workload2_resnet50_sized_full():
 
 def test_lazy_workload4_bert_sized_sampled():
     _run_config(4, [2, 15])
+
+
+def test_lazy_workload5_gpt2xl_sized_block17():
+    """P = 32, n = 1.5e9, 0.1 %, 2 steps: gradients generated on the GPU one
+    worker at a time, each worker's selections run on a one-row workspace.
+    Block index 17 of every output is hashed and compared with the digests
+    the oracle produced (tests/golden/workload5_digest.py --lazy)."""
+    import json
+    import os
+    from tests.golden.workload5_digest import BLOCK, OUT_LAZY, lazy_step_digests
+
+    if not os.path.exists(OUT_LAZY):
+        pytest.skip("lazy digests not generated")
+    gold = json.load(open(OUT_LAZY))
+    wl = W.config(5)
+    P, n, kb = wl.P, wl.n, wl.k_blk
+    b = BLOCK
+    bounds = so.block_bounds(n, P)
+    lo, hi = bounds[b], bounds[b + 1]
+    assert gold["block_range"] == [lo, hi] and gold["k_per_block"] == kb
+    log(f"lazy workload 5: {wl.describe()} block {b}")
+    torch.cuda.empty_cache()
+    st = spardl.SparDLLazyStep(P, n, kb, rows_per_call=1)
+    gen = W.DeviceGenerator(wl)
+    g = torch.empty((1, n), dtype=torch.float32, device="cuda")
+    for t in range(1, wl.steps + 1):
+        for w in range(P):
+            gen.fill(g[0], t, w)
+            st.residual_add_rows(w, g)
+        st.finish()
+        torch.cuda.synchronize()
+        check_ws(st)
+        log(f"  step {t}: GPU done, hashing block {b}")
+        sp_i = st.sp_idx[:, b].cpu().numpy()
+        sp_v = st.sp_val[:, b].cpu().numpy()
+        dense = st.dense[lo:hi].cpu().numpy()
+        resid = st.acc[:, lo:hi].cpu().numpy()
+        got = lazy_step_digests(P, lambda w: (sp_i[w], sp_v[w]), dense, lambda w: resid[w])
+        want = gold["steps"][t - 1]
+        for key in want:
+            assert got[key] == want[key], f"step {t}: {key} digest differs"
+        log(f"  step {t}: digests match")
+        del sp_i, sp_v, dense, resid
+    del st, g, gen
+    torch.cuda.empty_cache()
