@@ -454,3 +454,116 @@ def spardl_step_lazy(acc, grad, P: int, n: int, k: int, blocks=None) -> LazyStep
             res.residual[(w, b)] = new
             _block_of(acc[w], b, bounds)[...] = new
     return res
+
+
+# ----------------------------------------------------------------------------
+# Spar-All-Gather across teams, recursive form (R-SAG; Sec. III-D, case "d is
+# a power of 2")
+# ----------------------------------------------------------------------------
+#
+# Readings taken for this part (each one is listed in the design notes):
+#
+# * team tau holds the consecutive workers tau Q .. tau Q + Q - 1, Q = P / d;
+#   the worker at position q of its team runs SRS with its team (Q blocks of
+#   the gradient, block b = [floor(b n / Q), floor((b+1) n / Q)), k_blk = L
+#   entries per block) and ends holding block q.
+# * at R-SAG step t (0-based, t < log2 d) team X exchanges with team X xor 2^t,
+#   the partner at distance 2^t that is its own partner (recursive doubling);
+#   the two workers at position q exchange block q, each adds the other's
+#   entries by index (held + received, one fp32 add, the same on both sides)
+#   and keeps the top L.
+# * both sides drop the same entries.  At step t the two merged blocks are each
+#   already held by 2^t workers (recursive doubling), so 2^(t+1) workers compute
+#   the identical merge and drop the identical entries; each takes the share
+#   2^-(t+1) of every dropped value into its residual (an exact fp32
+#   multiplication by a power of two).  At the first step that is the half per
+#   side that the paper states; after it, taking a half at every worker would
+#   collect 2^t times what was dropped, so the share follows the paper's own
+#   rule for B-SAG instead (1 / the number of workers holding the same copy).
+#   Like the in-procedure drops of SRS these count at the final indices only,
+#   after the SRS drops, in step order (elsewhere every worker keeps its own A).
+
+
+def rsag_partner(X: int, t: int) -> int:
+    """Team exchanging with team X at R-SAG step t (recursive doubling)."""
+    return X ^ (1 << t)
+
+
+@dataclass
+class SagStepResult:
+    """One step with d teams; blocks are the Q = P / d blocks of a worker."""
+
+    bounds: list
+    blocks: list
+    local: dict = field(default_factory=dict)      # (w, b) -> (idx, val) after local top-L
+    S: dict = field(default_factory=dict)          # (w, b) -> (idx, val) after SRS and SAG
+    drops: dict = field(default_factory=dict)      # (i, w, b) -> (idx, val): SRS drops inside w's team
+    sag_drops: dict = field(default_factory=dict)  # (t, w) -> (idx, val): what w's pair dropped of block w % Q
+    final: dict = field(default_factory=dict)      # b -> (idx, val)
+    dense: dict = field(default_factory=dict)
+    residual: dict = field(default_factory=dict)
+
+
+def sag_share(vals, t: int) -> np.ndarray:
+    """A worker's share of the values its pair dropped at R-SAG step t: one
+    fp32 multiplication by 2^-(t+1) (exact unless the result is subnormal)."""
+    return (np.asarray(vals, dtype=np.float32) * np.float32(2.0 ** -(t + 1))).astype(np.float32)
+
+
+def spardl_step_rsag(acc, grad, P: int, n: int, L: int, d: int, blocks=None) -> SagStepResult:
+    """One SparDL synchronisation with d teams joined by R-SAG (Sec. III-D):
+    SRS inside every team, log2 d recursive-doubling exchanges across teams
+    with top-L after each, then the All-Gather inside the team; global
+    residual collection over all three kinds of drops.
+
+    L is the per-block count L(k, d, P) = d k / P.  acc / grad as for
+    spardl_step, with the Q = P / d team blocks as the block structure.
+    """
+    assert d >= 1 and d & (d - 1) == 0 and P % d == 0, "R-SAG needs a power-of-two d dividing P"
+    Q = P // d
+    bounds = block_bounds(n, Q)
+    blocks = list(range(Q)) if blocks is None else sorted(blocks)
+    res = SagStepResult(bounds=bounds, blocks=blocks)
+    A = {}
+    for w in range(P):
+        for b in blocks:
+            A[(w, b)] = residual_add(_block_of(acc[w], b, bounds), _block_of(grad[w], b, bounds))
+            res.local[(w, b)] = local_sparsify(A[(w, b)], bounds[b], L)
+            res.S[(w, b)] = res.local[(w, b)]
+    # SRS inside each team, on the team's own numbering
+    for tau in range(d):
+        Sq = {(q, b): res.S[(tau * Q + q, b)] for q in range(Q) for b in blocks}
+        dr = spar_reduce_scatter(Sq, Q, L, blocks)
+        for (q, b), v in Sq.items():
+            res.S[(tau * Q + q, b)] = v
+        for (i, q, b), v in dr.items():
+            res.drops[(i, tau * Q + q, b)] = v
+    # R-SAG across teams
+    steps = d.bit_length() - 1
+    for t in range(steps):
+        for X in range(d):
+            Y = rsag_partner(X, t)
+            if Y < X:
+                continue
+            for q in blocks:
+                wx, wy = X * Q + q, Y * Q + q
+                hi, hv = res.S[(wx, q)]
+                ri, rv = res.S[(wy, q)]
+                ki, kv, di, dv = merge_and_resparsify(hi, hv, ri, rv, L)
+                res.S[(wx, q)] = res.S[(wy, q)] = (ki, kv)
+                res.sag_drops[(t, wx)] = res.sag_drops[(t, wy)] = (di, dv)
+    for q in blocks:
+        for X in range(1, d):
+            assert np.array_equal(res.S[(X * Q + q, q)][0], res.S[(q, q)][0]), "teams disagree"
+        res.final[q] = res.S[(q, q)]
+    res.dense = allgather_densify(res.final, bounds, blocks)
+    l = num_steps(Q)
+    for w in range(P):
+        for b in blocks:
+            in_order = [res.drops[(i, w, b)] for i in range(1, l + 1) if (i, w, b) in res.drops]
+            if b == w % Q:
+                in_order += [(res.sag_drops[(t, w)][0], sag_share(res.sag_drops[(t, w)][1], t)) for t in range(steps)]
+            xi = global_residual_collect(A[(w, b)], bounds[b], res.local[(w, b)][0], res.final[b][0], in_order)
+            res.residual[(w, b)] = xi
+            _block_of(acc[w], b, bounds)[...] = xi
+    return res

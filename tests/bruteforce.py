@@ -142,3 +142,81 @@ def bf_step_lazy(acc_rows, grad_rows, P: int, k: int):
             I.add(x)
     new_res = [[left_behind[w][x] if x in I else A[w][x] for x in range(n)] for w in range(P)]
     return u, new_res, final, sel
+
+
+def bf_step_rsag(acc_rows, grad_rows, P: int, L: int, d: int):
+    """d teams of Q = P / d consecutive workers: SRS inside each team over Q
+    blocks, then recursive doubling across teams (partner team X xor 2^t) with
+    top-L after each exchange; every worker records the drops of its merge and
+    takes 1 / (workers that made the same merge) = 2^-(t+1) of each into its
+    residual (Sec. III-D).
+
+    Returns (dense u, new residual rows, final dicts per block).
+    """
+    n = len(acc_rows[0])
+    Q = P // d
+    s = [b * n // Q for b in range(Q + 1)]
+    A = [[F32(F32(acc_rows[w][x]) + F32(grad_rows[w][x])) for x in range(n)] for w in range(P)]
+    state, local, ledger_drops = {}, {}, [dict() for _ in range(P)]   # x -> list of drop values, in order
+    for w in range(P):
+        for b in range(Q):
+            state[(w, b)] = bf_topk({x: A[w][x] for x in range(s[b], s[b + 1])}, L)
+            local[(w, b)] = dict(state[(w, b)])
+    l = 0
+    while (1 << l) < Q:
+        l += 1
+    for i in range(1, l + 1):
+        dist = 1 << (l - i)
+        lo, hi = 1 << (l - i), min(1 << (l - i + 1), Q)
+        for tau in range(d):
+            inbox = {}
+            for q in range(Q):
+                dst = (q + dist) % Q
+                inbox[dst] = [(b, dict(state[(tau * Q + q, b)])) for b in ((q + t) % Q for t in range(lo, hi))]
+            for r in range(Q):
+                w = tau * Q + r
+                for b, msg in inbox[r]:
+                    merged = bf_merge(state[(w, b)], msg)
+                    kept = bf_topk(merged, L)
+                    state[(w, b)] = kept
+                    for x, v in merged.items():
+                        if x not in kept:
+                            ledger_drops[w].setdefault(x, []).append(v)
+    t = 0
+    while (1 << t) < d:
+        new = {}
+        for w in range(P):
+            X, q = divmod(w, Q)
+            partner = (X ^ (1 << t)) * Q + q
+            merged = bf_merge(state[(w, q)], state[(partner, q)])
+            new[w] = (bf_topk(merged, L), merged)
+        for w in range(P):
+            kept, merged = new[w]
+            state[(w, w % Q)] = kept
+            for x, v in merged.items():
+                if x not in kept:
+                    ledger_drops[w].setdefault(x, []).append(F32(v * F32(1.0 / (2 << t))))
+        t += 1
+    final = {b: state[(b, b)] for b in range(Q)}
+    for w in range(P):
+        assert state[(w, w % Q)] == final[w % Q]
+    u = [F32(0.0)] * n
+    I = set()
+    for b in range(Q):
+        for x, v in final[b].items():
+            u[x] = v
+            I.add(x)
+    new_res = []
+    for w in range(P):
+        row = []
+        for x in range(n):
+            if x not in I:
+                row.append(A[w][x])
+                continue
+            b = next(bb for bb in range(Q) if s[bb] <= x < s[bb + 1])
+            r = F32(0.0) if x in local[(w, b)] else A[w][x]
+            for v in ledger_drops[w].get(x, []):
+                r = F32(r + v)
+            row.append(r)
+        new_res.append(row)
+    return u, new_res, final
