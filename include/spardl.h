@@ -256,6 +256,60 @@ int spardl_lazy_residual_collect(float* acc, int64_t ld_acc, int32_t P, int64_t 
                                  const int32_t* sp_idx, const uint32_t* member, const float* saved,
                                  hipStream_t stream);
 
+/* ---------------------------------------------------------------------------
+ * Spar-All-Gather across d teams, recursive form (R-SAG; Sec. III-D, d a
+ * power of 2).  P workers form d teams of Q = P / d consecutive workers
+ * (team tau = workers tau*Q .. tau*Q + Q - 1).  Each team runs the d = 1
+ * calls above on its own rows with Q in place of P and k_blk = L(k, d, P) =
+ * d k / P: its rows of acc, its Q x Q x k_blk slice of sp (rows tau*Q ..),
+ * its own workspace.  After the team's SRS the worker at position q holds
+ * block q in sp[tau*Q + q][q].  Then, for t = 0 .. log2(d) - 1:
+ *   spardl_rsag_merge_topk(t);
+ * then the final blocks are sp[q][q], q < Q (any team): decode them with
+ * spardl_allgather_densify(sp, P = Q, ..., member) and collect residuals per
+ * team with spardl_residual_collect(..., member), then
+ * spardl_rsag_residual(..., member).  sp below is the whole P x Q x k_blk
+ * array (row w = worker w, Q blocks per row).
+ * ------------------------------------------------------------------------- */
+
+/* Workspace of spardl_rsag_merge_topk (separate from the teams' workspaces):
+ * 256-byte aligned device memory of this many bytes, prepared once by
+ * spardl_rsag_workspace_init (it rests at zero between calls, except the
+ * error word).  0 on invalid sizes: P < 2, d < 2, d not a power of 2, d not
+ * dividing P, n < Q, n >= 2^31, k_blk outside [1, floor(n / Q)]. */
+size_t spardl_rsag_workspace_bytes(int32_t P, int32_t d, int64_t n, int32_t k_blk);
+int spardl_rsag_workspace_init(int32_t P, int32_t d, int64_t n, int32_t k_blk, void* ws, size_t ws_bytes,
+                               hipStream_t stream);
+
+/* R-SAG exchange t in [0, log2 d) (Sec. III-D): team X and team X xor 2^t
+ * exchange, for every position q < Q, the block q their workers hold; both
+ * add the other's entries by index (held + received) and keep the top k_blk,
+ * so both hold the same block.  Pair p < (d/2)*Q is (j, q) = (p / Q, p % Q),
+ * X = j with a 0 bit inserted at bit t, Y = X + 2^t:
+ *   sp[X*Q + q][q] and sp[Y*Q + q][q] <- the kept entries (sorted by index);
+ *   drop_idx/drop_val[p*k_blk + j], j < drop_cnt[p] <- the dropped ones.
+ * Errors: EINVAL for NULL pointers, misaligned ws, invalid sizes (see
+ * spardl_rsag_workspace_bytes), t outside [0, log2 d); ECAPACITY if ws is
+ * smaller than spardl_rsag_workspace_bytes. */
+int spardl_rsag_merge_topk(int32_t* sp_idx, float* sp_val, int32_t P, int32_t d, int64_t n, int32_t k_blk,
+                           int32_t t, int32_t* drop_idx, float* drop_val, int32_t* drop_cnt, void* ws,
+                           size_t ws_bytes, hipStream_t stream);
+
+/* Residual share of the R-SAG drops (Sec. III-D): 2^(t+1) workers made the
+ * identical merge at exchange t, so each adds 2^-(t+1) of every value its
+ * pair dropped, at final indices only:
+ *   acc[w][x] = acc[w][x] + 2^-(t+1) * v   for w in {X*Q + q, Y*Q + q} of
+ *   pair p, every drop (x, v) of p with x in I (member), t = 0, 1, ... in
+ *   that order.
+ * Run after the teams' spardl_residual_collect.  drop_idx/drop_val/drop_cnt
+ * are HOST arrays of log2(d) DEVICE pointers (element t = the buffers of
+ * exchange t).
+ * Errors: EINVAL for NULL pointers, misaligned member, invalid sizes,
+ * ld_acc < n. */
+int spardl_rsag_residual(float* acc, int64_t ld_acc, int32_t P, int32_t d, int64_t n, int32_t k_blk,
+                         const uint32_t* member, const int32_t* const* drop_idx, const float* const* drop_val,
+                         const int32_t* const* drop_cnt, hipStream_t stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -86,6 +86,41 @@ Layout make_layout(int32_t P, int64_t n, int32_t kb) {
 
 inline size_t cand_bytes(int64_t entries) { return 3 * align256((size_t)entries * 4); }
 
+// Workspace of the R-SAG exchanges (npairs merges of two k_blk blocks): the
+// error word, one level-1 histogram and the selection state per pair, per-slot
+// counts and prefixes, then the merged candidates.
+Layout make_pair_layout(int64_t npairs, int32_t kb) {
+  Layout L;
+  L.pairs_max = npairs;
+  L.units = npairs;
+  L.tiles_mg = ceil_div(2ll * kb, MERGE_TILE);
+  L.slot_n = npairs * L.tiles_mg;
+  size_t off = 256;
+  L.hist1 = off;
+  off += align256((size_t)npairs * NB1 * 4);
+  L.state = off;
+  off += align256((size_t)npairs * ST_WORDS * 4);
+  L.slot_cnt = off;
+  off += align256((size_t)L.slot_n * 4);
+  L.slot_nbin = off;
+  off += align256((size_t)L.slot_n * 4);
+  L.pre_all = off;
+  off += align256((size_t)L.slot_n * 4);
+  L.pre_ge = off;
+  off += align256((size_t)L.slot_n * 4);
+  L.pre_eq = off;
+  off += align256((size_t)L.slot_n * 4);
+  L.fixed_end = off;
+  return L;
+}
+
+
+inline int32_t log2_exact(int32_t d) {
+  int32_t t = 0;
+  while ((1 << t) < d) ++t;
+  return t;
+}
+
 struct Ws {
   char* base;
   uint32_t *err, *bitmap, *hist1, *spec_t1, *spec_used, *spec_cnt, *state, *slot_cnt, *slot_nbin, *pre_all, *pre_ge,
@@ -136,6 +171,12 @@ bool sizes_ok(int32_t P, int64_t n, int32_t kb) {
   return true;
 }
 
+// d a power of two dividing P, and k_blk valid for blocks of a team of P / d
+bool rsag_sizes_ok(int32_t P, int32_t d, int64_t n, int32_t kb) {
+  if (P < 2 || d < 2 || (d & (d - 1)) || P % d) return false;
+  return sizes_ok(P / d, n, kb);
+}
+
 struct Fill {
   FillRanges r{};
   Fill& add(void* p, int64_t words) {
@@ -174,7 +215,7 @@ int topk_units(const float* acc, int64_t ld_acc, int64_t units, const Units& U, 
                             w.slot_cnt, w.slot_nbin, w.cand_idx, w.cand_val, w.bin_key, stream));
   SPARDL_TRY(launch_thresh(0, units, U, n, P, k_blk, smax, 1, nullptr, w.cand_val, w.state, w.slot_cnt,
                            w.slot_nbin, w.bin_key, w.pre_all, w.pre_ge, w.pre_eq, nullptr, w.err, stream));
-  SPARDL_TRY(launch_emit(0, w.cand_idx, w.cand_val, units, U, n, P, k_blk, 1, smax, w.state, w.slot_cnt,
+  SPARDL_TRY(launch_emit(0, w.cand_idx, w.cand_val, units, U, n, P, k_blk, Pairs{}, smax, w.state, w.slot_cnt,
                          w.pre_all, w.pre_ge, w.pre_eq, sp_idx, sp_val, local_idx, nullptr, nullptr, w.err, stream));
   return SPARDL_OK;
 }
@@ -288,11 +329,12 @@ int spardl_sparse_merge_topk(int32_t* sp_idx, float* sp_val, int32_t P, int64_t 
   const int32_t m = bag_of(P, l, round);
   const int64_t pairs = (int64_t)P * m;
   const int32_t smax = (int32_t)L.tiles_mg;
-  SPARDL_TRY(launch_merge(sp_idx, sp_val, P, k_blk, d, m, smax, w.hist1, w.slot_cnt, w.cand_idx, w.cand_val,
+  const Pairs PM = srs_pairs(P, m, d);
+  SPARDL_TRY(launch_merge(sp_idx, sp_val, PM, pairs, k_blk, smax, w.hist1, w.slot_cnt, w.cand_idx, w.cand_val,
                           stream));
   SPARDL_TRY(launch_thresh(1, pairs, all_blocks(P), n, P, k_blk, smax, 1, w.hist1, w.cand_val, w.state, w.slot_cnt, w.slot_nbin,
                            w.bin_key, w.pre_all, w.pre_ge, w.pre_eq, drop_cnt, w.err, stream));
-  SPARDL_TRY(launch_emit(1, w.cand_idx, w.cand_val, pairs, all_blocks(P), n, P, k_blk, m, smax, w.state, w.slot_cnt, w.pre_all,
+  SPARDL_TRY(launch_emit(1, w.cand_idx, w.cand_val, pairs, all_blocks(P), n, P, k_blk, PM, smax, w.state, w.slot_cnt, w.pre_all,
                          w.pre_ge, w.pre_eq, sp_idx, sp_val, nullptr, drop_idx, drop_val, w.err, stream));
   return SPARDL_OK;
 }
@@ -380,6 +422,67 @@ int spardl_lazy_residual_collect(float* acc, int64_t ld_acc, int32_t P, int64_t 
   for (int32_t i = l; i >= 1; --i)
     SPARDL_TRY(launch_lazy_step(acc, ld_acc, P, n, k_blk, 1 << (l - i), bag_of(P, l, i), sp_idx, nullptr, const_cast<float*>(saved),
                                 member, true, stream));
+  return SPARDL_OK;
+}
+
+size_t spardl_rsag_workspace_bytes(int32_t P, int32_t d, int64_t n, int32_t k_blk) {
+  if (!rsag_sizes_ok(P, d, n, k_blk)) return 0;
+  const int64_t npairs = (int64_t)(d / 2) * (P / d);
+  const Layout L = make_pair_layout(npairs, k_blk);
+  return L.fixed_end + cand_bytes(npairs * L.tiles_mg * MERGE_TILE);
+}
+
+int spardl_rsag_workspace_init(int32_t P, int32_t d, int64_t n, int32_t k_blk, void* ws, size_t ws_bytes,
+                               hipStream_t stream) {
+  if (!ws || ws_misaligned(ws)) return SPARDL_EINVAL;
+  const size_t need = spardl_rsag_workspace_bytes(P, d, n, k_blk);
+  if (need == 0) return SPARDL_EINVAL;
+  if (ws_bytes < need) return SPARDL_ECAPACITY;
+  const int64_t npairs = (int64_t)(d / 2) * (P / d);
+  const Layout L = make_pair_layout(npairs, k_blk);
+  Ws w = carve(ws, ws_bytes, L);
+  SPARDL_TRY(launch_fill(Fill().add(w.err, 64).add(w.hist1, npairs * NB1).r, stream));
+  return SPARDL_OK;
+}
+
+int spardl_rsag_merge_topk(int32_t* sp_idx, float* sp_val, int32_t P, int32_t d, int64_t n, int32_t k_blk,
+                           int32_t t, int32_t* drop_idx, float* drop_val, int32_t* drop_cnt, void* ws,
+                           size_t ws_bytes, hipStream_t stream) {
+  if (!sp_idx || !sp_val || !drop_idx || !drop_val || !drop_cnt || !ws || ws_misaligned(ws) ||
+      !rsag_sizes_ok(P, d, n, k_blk))
+    return SPARDL_EINVAL;
+  if (t < 0 || t >= log2_exact(d)) return SPARDL_EINVAL;
+  const int32_t Q = P / d;
+  const int64_t npairs = (int64_t)(d / 2) * Q;
+  const Layout L = make_pair_layout(npairs, k_blk);
+  if (ws_bytes < spardl_rsag_workspace_bytes(P, d, n, k_blk)) return SPARDL_ECAPACITY;
+  Ws w = carve(ws, ws_bytes, L);
+  const Pairs PM = rsag_pairs(Q, t);
+  const int32_t smax = (int32_t)L.tiles_mg;
+  SPARDL_TRY(launch_merge(sp_idx, sp_val, PM, npairs, k_blk, smax, w.hist1, w.slot_cnt, w.cand_idx, w.cand_val,
+                          stream));
+  SPARDL_TRY(launch_thresh(1, npairs, all_blocks(Q), n, Q, k_blk, smax, 1, w.hist1, w.cand_val, w.state,
+                           w.slot_cnt, w.slot_nbin, w.bin_key, w.pre_all, w.pre_ge, w.pre_eq, drop_cnt, w.err,
+                           stream));
+  SPARDL_TRY(launch_emit(1, w.cand_idx, w.cand_val, npairs, all_blocks(Q), n, Q, k_blk, PM, smax, w.state,
+                         w.slot_cnt, w.pre_all, w.pre_ge, w.pre_eq, sp_idx, sp_val, nullptr, drop_idx, drop_val,
+                         w.err, stream));
+  return SPARDL_OK;
+}
+
+int spardl_rsag_residual(float* acc, int64_t ld_acc, int32_t P, int32_t d, int64_t n, int32_t k_blk,
+                         const uint32_t* member, const int32_t* const* drop_idx, const float* const* drop_val,
+                         const int32_t* const* drop_cnt, hipStream_t stream) {
+  if (!acc || !member || (reinterpret_cast<uintptr_t>(member) & 3u) || !rsag_sizes_ok(P, d, n, k_blk) ||
+      ld_acc < n || !drop_idx || !drop_val || !drop_cnt)
+    return SPARDL_EINVAL;
+  const int32_t steps = log2_exact(d);
+  for (int32_t t = 0; t < steps; ++t)
+    if (!drop_idx[t] || !drop_val[t] || !drop_cnt[t]) return SPARDL_EINVAL;
+  const int32_t Q = P / d;
+  for (int32_t t = 0; t < steps; ++t)
+    SPARDL_TRY(launch_grc_sag_drops(acc, ld_acc, n, Q, t, k_blk, (d / 2) * Q, drop_idx[t], drop_val[t], drop_cnt[t],
+                                    member, stream));
   return SPARDL_OK;
 }
 

@@ -97,6 +97,39 @@ struct Units {
 
 inline Units all_blocks(int32_t P) { return Units{(uint32_t)P, 0u, 0u, 0u}; }
 
+// Pairs of one merge call.  Pair p adds the received block into the held
+// block (both named by their block number row * nb + b in sp) and keeps the
+// top k_blk in the held block and, if `both`, in the received one too.
+//  SRS step (kind 0, nb = P workers): pair p = (w, t), held = sp[w][b],
+//    received = sp[(w - dist) mod P][b], b = (w + t) mod P, t < m.
+//  R-SAG exchange t (kind 1, nb = Q): pair p = (j, q); team X = j with a 0
+//    bit inserted at bit t, team Y = X + 2^t; held = sp[X Q + q][q],
+//    received = sp[Y Q + q][q], and both keep the result.
+struct Pairs {
+  uint32_t kind, nb, m, dist, t;
+  __device__ __forceinline__ void decode(uint32_t p, int64_t* held, int64_t* recv, bool* both) const {
+    if (kind == 0u) {
+      const uint32_t w = p / m, tt = p - w * m;
+      const uint32_t b = (w + tt) % nb, src = (w + nb - dist) % nb;
+      *held = (int64_t)w * nb + b;
+      *recv = (int64_t)src * nb + b;
+      *both = false;
+    } else {
+      const uint32_t j = p / nb, q = p - j * nb;
+      const uint32_t lowmask = (1u << t) - 1u;
+      const uint32_t X = ((j & ~lowmask) << 1) | (j & lowmask), Y = X | (1u << t);
+      *held = (int64_t)(X * nb + q) * nb + q;
+      *recv = (int64_t)(Y * nb + q) * nb + q;
+      *both = true;
+    }
+  }
+};
+
+inline Pairs srs_pairs(int32_t P, int32_t m, int32_t dist) {
+  return Pairs{0u, (uint32_t)P, (uint32_t)m, (uint32_t)dist, 0u};
+}
+inline Pairs rsag_pairs(int32_t Q, int32_t t) { return Pairs{1u, (uint32_t)Q, 0u, 0u, (uint32_t)t}; }
+
 __device__ __forceinline__ int lane_id() { return threadIdx.x & (WAVE - 1); }
 __device__ __forceinline__ int wave_id() { return threadIdx.x / WAVE; }
 

@@ -1339,8 +1339,8 @@ __global__ __launch_bounds__(1024) void k_thresh(Blocks B, Units U, int32_t kb, 
 constexpr int EMIT_R = 16;  // entries per lane per chunk (a crowded slot holds up to 4096)
 template <int MODE>
 __global__ __launch_bounds__(256) void k_emit(
-    const int32_t* __restrict__ cand_idx, const float* __restrict__ cand_val, Blocks B, Units U,
-    int32_t kb, int32_t m, int32_t smax, uint32_t gq, const uint32_t* __restrict__ state,
+    const int32_t* __restrict__ cand_idx, const float* __restrict__ cand_val, Blocks B, Units U, Pairs PM,
+    int32_t kb, int32_t smax, uint32_t gq, const uint32_t* __restrict__ state,
     const uint32_t* __restrict__ slot_cnt, const uint32_t* __restrict__ pre_all,
     const uint32_t* __restrict__ pre_ge, const uint32_t* __restrict__ pre_eq, int32_t* __restrict__ out_idx,
     float* __restrict__ out_val, int32_t* __restrict__ local_idx, int32_t* __restrict__ drop_idx,
@@ -1361,14 +1361,17 @@ __global__ __launch_bounds__(256) void k_emit(
   uint32_t run_g = pre_ge[si], run_e = pre_eq[si];
   const uint32_t tge = st[ST_TGE], teq = st[ST_TEQ], need_eq = st[ST_NEEDEQ];
   const int64_t base = g.base + (int64_t)slot * g.ss;
-  int64_t o;
+  int64_t o, o2 = -1;   // output block(s); o2: the other side of an R-SAG exchange
   if (MODE == 0) {
     uint32_t w, b;
     U.decode(unit, B.P, &w, &b);
     o = ((int64_t)w * B.P + b) * kb;
   } else {
-    const uint32_t w = unit / (uint32_t)m, t = unit % (uint32_t)m, b = (w + t) % B.P;
-    o = ((int64_t)w * B.P + b) * kb;
+    int64_t hb, rb;
+    bool both;
+    PM.decode(unit, &hb, &rb, &both);
+    o = hb * kb;
+    if (both) o2 = rb * kb;
   }
   uint32_t p_lo = 0, p_hi = cnt;
   if constexpr (NPART > 1) {
@@ -1423,6 +1426,10 @@ __global__ __launch_bounds__(256) void k_emit(
           if (sel_before < (uint32_t)kb) {
             out_idx[o + sel_before] = ix[r];
             out_val[o + sel_before] = vx[r];
+            if (MODE == 1 && o2 >= 0) {
+              out_idx[o2 + sel_before] = ix[r];
+              out_val[o2 + sel_before] = vx[r];
+            }
             if (MODE == 0 && local_idx) local_idx[o + sel_before] = ix[r];
           } else {
             atomicOr(err, ERR_COUNT_POS);
@@ -1444,15 +1451,16 @@ __global__ __launch_bounds__(256) void k_emit(
 }
 
 // ============================================================================ a4: merge-path index sum
-// Pair (w, t): held = sp[w][b], received = sp[(w - d) mod P][b], b = (w+t) mod P.
+// Pair p (Pairs in common.hpp): held block + received block, e.g. for an SRS
+// step held = sp[w][b], received = sp[(w - d) mod P][b], b = (w+t) mod P.
 // The merged sequence orders by index with the held entry first on equal
 // indices; the held entry then emits held + received and the received entry
 // leaves a hole.  Tile = MERGE_TILE merged positions; its hole-free part is
 // written densely into the tile's slot, and the level-1 histogram of the
 // union is accumulated for the selection.
 __global__ __launch_bounds__(MERGE_THREADS) void k_merge(
-    const int32_t* __restrict__ sp_idx, const float* __restrict__ sp_val, int32_t P, int32_t kb,
-    int32_t d, int32_t m, int32_t tiles_per_pair, uint32_t* __restrict__ hist1,
+    const int32_t* __restrict__ sp_idx, const float* __restrict__ sp_val, Pairs PM, int32_t kb,
+    int32_t tiles_per_pair, uint32_t* __restrict__ hist1,
     uint32_t* __restrict__ slot_cnt, int32_t* __restrict__ U_idx, float* __restrict__ U_val) {
   // held entries a0-1 .. a1 at [0, nh + 2), received b0 .. b1 at [nh + 2, nh + nr + 3)
   __shared__ int32_t cI[MERGE_TILE + 3];
@@ -1461,12 +1469,13 @@ __global__ __launch_bounds__(MERGE_THREADS) void k_merge(
   __shared__ uint32_t scratch[2 * (MERGE_THREADS / WAVE) + 1];
   const uint32_t pair = blockIdx.x / (uint32_t)tiles_per_pair;
   const int32_t tile = (int32_t)(blockIdx.x % (uint32_t)tiles_per_pair);
-  const uint32_t uP = (uint32_t)P;
-  const uint32_t w = pair / (uint32_t)m, t = pair % (uint32_t)m, b = (w + t) % uP, src = (w + uP - (uint32_t)d) % uP;
-  const int32_t* __restrict__ Hi = sp_idx + ((int64_t)w * P + b) * kb;
-  const float* __restrict__ Hv = sp_val + ((int64_t)w * P + b) * kb;
-  const int32_t* __restrict__ Ri = sp_idx + ((int64_t)src * P + b) * kb;
-  const float* __restrict__ Rv = sp_val + ((int64_t)src * P + b) * kb;
+  int64_t hb, rb;
+  bool both;
+  PM.decode(pair, &hb, &rb, &both);
+  const int32_t* __restrict__ Hi = sp_idx + hb * kb;
+  const float* __restrict__ Hv = sp_val + hb * kb;
+  const int32_t* __restrict__ Ri = sp_idx + rb * kb;
+  const float* __restrict__ Rv = sp_val + rb * kb;
   const int32_t L2 = 2 * kb;
   for (int i = threadIdx.x; i < NB1 / 4; i += blockDim.x) reinterpret_cast<uint4*>(hist)[i] = make_uint4(0u, 0u, 0u, 0u);
   const int32_t Q0 = tile * MERGE_TILE;
@@ -1706,6 +1715,37 @@ __global__ __launch_bounds__(256) void k_grc_drops(float* __restrict__ acc, int6
   }
 }
 
+// acc[w][x] += share * v for the drops (x, v) of R-SAG exchange t with x a
+// final index, on both workers of each pair (they made the same merge;
+// share = 2^-(t+1), the product exact unless it is subnormal).  Grid: x over
+// a pair's drop list, y over pairs, numbered as in the exchange.
+__global__ __launch_bounds__(256) void k_grc_sag_drops(float* __restrict__ acc, int64_t ld_acc, uint32_t n,
+                                                       uint32_t Q, uint32_t t, uint32_t kb, uint32_t npairs,
+                                                       const int32_t* __restrict__ drop_idx,
+                                                       const float* __restrict__ drop_val,
+                                                       const int32_t* __restrict__ drop_cnt,
+                                                       const uint32_t* __restrict__ bm, float share) {
+  for (uint32_t pair = blockIdx.y; pair < npairs; pair += gridDim.y) {
+    const int32_t c = drop_cnt[pair];
+    const uint32_t cnt = c < 0 ? 0u : min((uint32_t)c, kb);
+    const uint32_t j = pair / Q, q = pair - j * Q;
+    const uint32_t lowmask = (1u << t) - 1u;
+    const uint32_t X = ((j & ~lowmask) << 1) | (j & lowmask), Y = X | (1u << t);
+    const int32_t* __restrict__ Di = drop_idx + (int64_t)pair * kb;
+    const float* __restrict__ Dv = drop_val + (int64_t)pair * kb;
+    float* __restrict__ AX = acc + (int64_t)(X * Q + q) * ld_acc;
+    float* __restrict__ AY = acc + (int64_t)(Y * Q + q) * ld_acc;
+    for (uint32_t j2 = blockIdx.x * 256u + threadIdx.x; j2 < cnt; j2 += gridDim.x * 256u) {
+      const int32_t x = Di[j2];
+      if (x >= 0 && (uint32_t)x < n && in_final(bm, x)) {
+        const float v = Dv[j2] * share;
+        AX[x] = AX[x] + v;
+        AY[x] = AY[x] + v;
+      }
+    }
+  }
+}
+
 // ============================================================================ lazy summation
 // One SRS step of the lazy variant (Sec. III-B "Optimization for SRS",
 // Algorithm 1): worker w sent sp[w][b], b = (w + d + t) mod P for t < m, to
@@ -1823,7 +1863,7 @@ hipError_t launch_thresh(int mode, int64_t nunits, const Units& U, int64_t n, in
 }
 
 hipError_t launch_emit(int mode, const int32_t* cand_idx, const float* cand_val, int64_t nunits, const Units& U,
-                       int64_t n, int32_t P, int32_t kb, int32_t m, int32_t smax, const uint32_t* state,
+                       int64_t n, int32_t P, int32_t kb, const Pairs& PM, int32_t smax, const uint32_t* state,
                        const uint32_t* slot_cnt, const uint32_t* pre_all, const uint32_t* pre_ge,
                        const uint32_t* pre_eq, int32_t* out_idx, float* out_val, int32_t* local_idx,
                        int32_t* drop_idx, float* drop_val, uint32_t* err, hipStream_t s) {
@@ -1832,17 +1872,17 @@ hipError_t launch_emit(int mode, const int32_t* cand_idx, const float* cand_val,
   const dim3 grid((unsigned)(nunits * gq));
   const Blocks B = make_blocks(n, P);
   if (mode == 0)
-    hipLaunchKernelGGL(k_emit<0>, grid, dim3(256), 0, s, cand_idx, cand_val, B, U, kb, m, smax, gq, state, slot_cnt, pre_all, pre_ge, pre_eq, out_idx, out_val, local_idx, drop_idx, drop_val, err);
+    hipLaunchKernelGGL(k_emit<0>, grid, dim3(256), 0, s, cand_idx, cand_val, B, U, PM, kb, smax, gq, state, slot_cnt, pre_all, pre_ge, pre_eq, out_idx, out_val, local_idx, drop_idx, drop_val, err);
   else
-    hipLaunchKernelGGL(k_emit<1>, grid, dim3(256), 0, s, cand_idx, cand_val, B, U, kb, m, smax, gq, state, slot_cnt, pre_all, pre_ge, pre_eq, out_idx, out_val, local_idx, drop_idx, drop_val, err);
+    hipLaunchKernelGGL(k_emit<1>, grid, dim3(256), 0, s, cand_idx, cand_val, B, U, PM, kb, smax, gq, state, slot_cnt, pre_all, pre_ge, pre_eq, out_idx, out_val, local_idx, drop_idx, drop_val, err);
   return hipGetLastError();
 }
 
-hipError_t launch_merge(const int32_t* sp_idx, const float* sp_val, int32_t P, int32_t kb, int32_t d, int32_t m,
+hipError_t launch_merge(const int32_t* sp_idx, const float* sp_val, const Pairs& PM, int64_t npairs, int32_t kb,
                         int32_t tiles_per_pair, uint32_t* hist1, uint32_t* slot_cnt, int32_t* U_idx,
                         float* U_val, hipStream_t s) {
-  const dim3 grid((unsigned)((int64_t)P * m * tiles_per_pair));
-  hipLaunchKernelGGL(k_merge, grid, dim3(MERGE_THREADS), 0, s, sp_idx, sp_val, P, kb, d, m, tiles_per_pair, hist1, slot_cnt, U_idx, U_val);
+  const dim3 grid((unsigned)(npairs * tiles_per_pair));
+  hipLaunchKernelGGL(k_merge, grid, dim3(MERGE_THREADS), 0, s, sp_idx, sp_val, PM, kb, tiles_per_pair, hist1, slot_cnt, U_idx, U_val);
   return hipGetLastError();
 }
 
@@ -1866,6 +1906,15 @@ hipError_t launch_grc_zero(float* acc, int64_t ld_acc, int32_t P, int64_t n, int
                            const uint32_t* bm, hipStream_t s) {
   const dim3 grid(grid_for((int64_t)P * kb, 256, 1024), (unsigned)std::min<int32_t>(P, 65535));
   hipLaunchKernelGGL(k_grc_zero, grid, dim3(256), 0, s, acc, ld_acc, (uint32_t)P, (uint32_t)n, (uint32_t)kb, local_idx, bm);
+  return hipGetLastError();
+}
+
+hipError_t launch_grc_sag_drops(float* acc, int64_t ld_acc, int64_t n, int32_t Q, int32_t t, int32_t kb,
+                                int32_t npairs, const int32_t* drop_idx, const float* drop_val,
+                                const int32_t* drop_cnt, const uint32_t* bm, hipStream_t s) {
+  const dim3 grid(grid_for(kb, 256, 1024), (unsigned)std::min<int32_t>(npairs, 65535));
+  hipLaunchKernelGGL(k_grc_sag_drops, grid, dim3(256), 0, s, acc, ld_acc, (uint32_t)n, (uint32_t)Q, (uint32_t)t,
+                     (uint32_t)kb, (uint32_t)npairs, drop_idx, drop_val, drop_cnt, bm, 1.0f / (float)(2 << t));
   return hipGetLastError();
 }
 

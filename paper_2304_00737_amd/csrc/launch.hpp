@@ -44,11 +44,11 @@ hipError_t launch_thresh(int mode, int64_t nunits, const Units& U, int64_t n, in
                          const uint32_t* slot_nbin, const uint32_t* bin_key, uint32_t* pre_all, uint32_t* pre_ge,
                          uint32_t* pre_eq, int32_t* drop_cnt, uint32_t* err, hipStream_t s);
 hipError_t launch_emit(int mode, const int32_t* cand_idx, const float* cand_val, int64_t nunits, const Units& U,
-                       int64_t n, int32_t P, int32_t kb, int32_t m, int32_t smax, const uint32_t* state,
+                       int64_t n, int32_t P, int32_t kb, const Pairs& PM, int32_t smax, const uint32_t* state,
                        const uint32_t* slot_cnt, const uint32_t* pre_all, const uint32_t* pre_ge,
                        const uint32_t* pre_eq, int32_t* out_idx, float* out_val, int32_t* local_idx,
                        int32_t* drop_idx, float* drop_val, uint32_t* err, hipStream_t s);
-hipError_t launch_merge(const int32_t* sp_idx, const float* sp_val, int32_t P, int32_t kb, int32_t d, int32_t m,
+hipError_t launch_merge(const int32_t* sp_idx, const float* sp_val, const Pairs& PM, int64_t npairs, int32_t kb,
                         int32_t tiles_per_pair, uint32_t* hist1, uint32_t* slot_cnt, int32_t* U_idx,
                         float* U_val, hipStream_t s);
 hipError_t launch_densify(const int32_t* sp_idx, const float* sp_val, int32_t P, int64_t n, int32_t kb,
@@ -57,6 +57,9 @@ hipError_t launch_bm_mark(const int32_t* sp_idx, int32_t P, int64_t n, int32_t k
                           hipStream_t s);
 hipError_t launch_grc_zero(float* acc, int64_t ld_acc, int32_t P, int64_t n, int32_t kb, const int32_t* local_idx,
                            const uint32_t* bm, hipStream_t s);
+hipError_t launch_grc_sag_drops(float* acc, int64_t ld_acc, int64_t n, int32_t Q, int32_t t, int32_t kb,
+                                int32_t npairs, const int32_t* drop_idx, const float* drop_val,
+                                const int32_t* drop_cnt, const uint32_t* bm, hipStream_t s);
 hipError_t launch_lazy_step(float* acc, int64_t ld_acc, int32_t P, int64_t n, int32_t kb, int32_t d, int32_t m,
                             const int32_t* sp_idx, const float* sp_val, float* saved, const uint32_t* bm,
                             bool restore, hipStream_t s);

@@ -45,8 +45,14 @@ _lib.spardl_residual_collect.argtypes = [_p, _i64, _i32, _i64, _i32, _p, _p, _p,
 _lib.spardl_lazy_topk.argtypes = [_p, _i64, _i32, _i32, _i64, _i32, _i32, _i32, _p, _p, _p, _sz, _p]
 _lib.spardl_lazy_receive.argtypes = [_p, _i64, _i32, _i64, _i32, _i32, _p, _p, _p, _p]
 _lib.spardl_lazy_residual_collect.argtypes = [_p, _i64, _i32, _i64, _i32, _p, _p, _p, _p]
+_lib.spardl_rsag_workspace_bytes.argtypes = [_i32, _i32, _i64, _i32]
+_lib.spardl_rsag_workspace_bytes.restype = _sz
+_lib.spardl_rsag_workspace_init.argtypes = [_i32, _i32, _i64, _i32, _p, _sz, _p]
+_lib.spardl_rsag_merge_topk.argtypes = [_p, _p, _i32, _i32, _i64, _i32, _i32, _p, _p, _p, _p, _sz, _p]
+_lib.spardl_rsag_residual.argtypes = [_p, _i64, _i32, _i32, _i64, _i32, _p, _p, _p, _p, _p]
 for _f in ("residual_add", "block_topk", "sparse_merge_topk", "allgather_densify", "residual_collect",
-           "lazy_topk", "lazy_receive", "lazy_residual_collect"):
+           "lazy_topk", "lazy_receive", "lazy_residual_collect", "rsag_workspace_init", "rsag_merge_topk",
+           "rsag_residual"):
     getattr(_lib, "spardl_" + _f).restype = ctypes.c_int
 
 
@@ -180,6 +186,34 @@ def lazy_residual_collect(acc, P: int, n: int, k_blk: int, sp_idx, member, saved
     ld_acc = _ld(acc, n) if ld_acc is None else ld_acc
     _check("lazy_residual_collect", _lib.spardl_lazy_residual_collect(
         _ptr(acc), ld_acc, P, n, k_blk, _ptr(sp_idx), _ptr(member), _ptr(saved), _stream(stream)))
+
+
+def rsag_workspace(P: int, d: int, n: int, k_blk: int, device="cuda", *, stream=None):
+    """A prepared workspace for spardl_rsag_merge_topk with these sizes."""
+    nbytes = int(_lib.spardl_rsag_workspace_bytes(P, d, n, k_blk))
+    if nbytes == 0:
+        raise SpardlError("rsag_workspace_bytes", EINVAL)
+    ws = torch.empty(nbytes, dtype=torch.uint8, device=device)
+    _check("rsag_workspace_init", _lib.spardl_rsag_workspace_init(P, d, n, k_blk, _ptr(ws), nbytes, _stream(stream)))
+    return ws
+
+
+def rsag_merge_topk(sp_idx, sp_val, P: int, d: int, n: int, k_blk: int, t: int, drop_idx, drop_val, drop_cnt, ws,
+                    *, stream=None) -> None:
+    _check("rsag_merge_topk", _lib.spardl_rsag_merge_topk(
+        _ptr(sp_idx), _ptr(sp_val), P, d, n, k_blk, t, _ptr(drop_idx), _ptr(drop_val), _ptr(drop_cnt), _ptr(ws),
+        ws.numel() * ws.element_size(), _stream(stream)))
+
+
+def rsag_residual(acc, P: int, d: int, n: int, k_blk: int, member, drop_idx, drop_val, drop_cnt, *, ld_acc=None,
+                  stream=None) -> None:
+    """drop_*: sequences of log2(d) tensors (one per exchange)."""
+    ld_acc = _ld(acc, n) if ld_acc is None else ld_acc
+    steps = len(drop_idx)
+    arr = lambda ts: (ctypes.c_void_p * max(steps, 1))(*[_ptr(t) for t in ts])
+    _check("rsag_residual", _lib.spardl_rsag_residual(_ptr(acc), ld_acc, P, d, n, k_blk, _ptr(member),
+                                                      arr(drop_idx), arr(drop_val), arr(drop_cnt),
+                                                      _stream(stream)))
 
 
 def ws_error(ws) -> int:
@@ -332,3 +366,87 @@ class SparDLLazyStep:
     def step(self, grad, stream=None):
         self.residual_add_rows(0, grad, stream)
         self.finish(stream)
+
+
+class SparDLSagStep:
+    """P simulated workers in d teams of Q = P / d joined by R-SAG (Sec. III-D,
+    d a power of 2), one synchronisation step through the C ABI.
+
+    k_blk is L(k, d, P) = d k / P, the entries per block of a team's Q blocks.
+    After step(grad): dense / member as for SparDLStep; sp_idx/sp_val[w, b]
+    the state of worker w's block b (final block q in sp[q, q] of every
+    team); drop_*[i - 1][w] the SRS drops of worker w at step i inside its
+    team; sag_*[t][p] what pair p dropped at exchange t.
+    """
+
+    def __init__(self, P: int, d: int, n: int, k_blk: int, device="cuda", fused: bool = True):
+        if d < 2 or d & (d - 1) or P % d:
+            raise ValueError("R-SAG needs a power-of-two d >= 2 dividing P")
+        self.P, self.d, self.Q, self.n, self.k_blk, self.fused = P, d, P // d, n, k_blk, fused
+        Q = self.Q
+        dev = torch.device(device)
+        self.acc = torch.zeros((P, n), dtype=torch.float32, device=dev)
+        self.sp_idx = torch.empty((P, Q, k_blk), dtype=torch.int32, device=dev)
+        self.sp_val = torch.empty((P, Q, k_blk), dtype=torch.float32, device=dev)
+        self.local_idx = torch.empty((P, Q, k_blk), dtype=torch.int32, device=dev)
+        self.l, self.distance, self.bags = srs_plan(Q)
+        self.drop_idx = [torch.empty((P, m, k_blk), dtype=torch.int32, device=dev) for m in self.bags]
+        self.drop_val = [torch.empty((P, m, k_blk), dtype=torch.float32, device=dev) for m in self.bags]
+        self.drop_cnt = [torch.empty((P, m), dtype=torch.int32, device=dev) for m in self.bags]
+        self.steps = d.bit_length() - 1
+        npairs = (d // 2) * Q
+        self.sag_idx = [torch.empty((npairs, k_blk), dtype=torch.int32, device=dev) for _ in range(self.steps)]
+        self.sag_val = [torch.empty((npairs, k_blk), dtype=torch.float32, device=dev) for _ in range(self.steps)]
+        self.sag_cnt = [torch.empty(npairs, dtype=torch.int32, device=dev) for _ in range(self.steps)]
+        self.dense = torch.empty(n, dtype=torch.float32, device=dev)
+        self.member = torch.empty(member_words(n), dtype=torch.int32, device=dev)
+        self.ws_team = [workspace(Q, Q, n, k_blk, device=dev) for _ in range(d)]
+        self.ws_sag = rsag_workspace(P, d, n, k_blk, device=dev)
+
+    def _rows(self, tau):
+        return slice(tau * self.Q, (tau + 1) * self.Q)
+
+    def add_and_select(self, grad, stream=None):
+        Q, n, L = self.Q, self.n, self.k_blk
+        for tau in range(self.d):
+            r, ws = self._rows(tau), self.ws_team[tau]
+            if self.fused:
+                residual_add(self.acc[r], grad[r], Q, n, Q, ws, L, stream=stream)
+            else:
+                residual_add(self.acc[r], grad[r], Q, n, 0, None, stream=stream)
+            block_topk(self.acc[r], Q, n, Q, L, self.sp_idx[r], self.sp_val[r], self.local_idx[r], ws,
+                       TOPK_HIST_READY if self.fused else 0, stream=stream)
+
+    def team_srs(self, stream=None):
+        for tau in range(self.d):
+            r = self._rows(tau)
+            for i in range(1, self.l + 1):
+                sparse_merge_topk(self.sp_idx[r], self.sp_val[r], self.Q, self.n, self.k_blk, i,
+                                  self.drop_idx[i - 1][r], self.drop_val[i - 1][r], self.drop_cnt[i - 1][r],
+                                  self.ws_team[tau], stream=stream)
+
+    def exchanges(self, stream=None):
+        for t in range(self.steps):
+            rsag_merge_topk(self.sp_idx, self.sp_val, self.P, self.d, self.n, self.k_blk, t, self.sag_idx[t],
+                            self.sag_val[t], self.sag_cnt[t], self.ws_sag, stream=stream)
+
+    def densify(self, stream=None):
+        Q = self.Q
+        allgather_densify(self.sp_idx[:Q], self.sp_val[:Q], Q, self.n, self.k_blk, self.dense, self.member,
+                          stream=stream)
+
+    def collect(self, stream=None):
+        for tau in range(self.d):
+            r = self._rows(tau)
+            residual_collect(self.acc[r], self.Q, self.n, self.k_blk, self.local_idx[r], self.sp_idx[r],
+                             [t[r] for t in self.drop_idx], [t[r] for t in self.drop_val],
+                             [t[r] for t in self.drop_cnt], self.ws_team[tau], self.member, stream=stream)
+        rsag_residual(self.acc, self.P, self.d, self.n, self.k_blk, self.member, self.sag_idx, self.sag_val,
+                      self.sag_cnt, stream=stream)
+
+    def step(self, grad, stream=None):
+        self.add_and_select(grad, stream)
+        self.team_srs(stream)
+        self.exchanges(stream)
+        self.densify(stream)
+        self.collect(stream)

@@ -156,3 +156,59 @@ def compare_lazy_step(st, res, P: int, n: int, kb: int, blocks=None) -> None:
         for b in blocks:
             got = st.acc[w, bounds[b]:bounds[b + 1]].cpu().numpy()
             assert_bits_equal(got, res.residual[(w, b)], f"residual w={w} b={b}")
+
+
+def compare_sag_step(st, res, blocks=None) -> None:
+    """Compare the GPU state after one R-SAG step with an oracle SagStepResult:
+    local selections, the sparse state of every block, the SRS drops inside
+    every team, the drops of every exchange, the dense update, the bitmap of I
+    and the residuals, bit for bit."""
+    P, d, Q, n = st.P, st.d, st.Q, st.n
+    blocks = list(range(Q)) if blocks is None else list(blocks)
+    bounds = so.block_bounds(n, Q)
+    sp_idx, sp_val = st.sp_idx.cpu().numpy(), st.sp_val.cpu().numpy()
+    local = st.local_idx.cpu().numpy()
+    for w in range(P):
+        for b in blocks:
+            assert_idx_equal(local[w, b], res.local[(w, b)][0], f"local_idx w={w} b={b}")
+            si, sv = res.S[(w, b)]
+            assert_idx_equal(sp_idx[w, b], si, f"sp_idx w={w} b={b}")
+            assert_bits_equal(sp_val[w, b], sv, f"sp_val w={w} b={b}")
+    for i, m in enumerate(st.bags, start=1):
+        di, dv, dc = (x[i - 1].cpu().numpy() for x in (st.drop_idx, st.drop_val, st.drop_cnt))
+        for w in range(P):
+            q = w % Q
+            for t in range(m):
+                b = (q + t) % Q
+                if b not in blocks:
+                    continue
+                oi, ov = res.drops[(i, w, b)]
+                c = int(dc[w, t])
+                assert c == len(oi), f"team drop count step {i} w={w} b={b}"
+                assert_idx_equal(di[w, t, :c], oi, f"team drop idx step {i} w={w} b={b}")
+                assert_bits_equal(dv[w, t, :c], ov, f"team drop val step {i} w={w} b={b}")
+    for t in range(st.steps):
+        si, sv, sc = (x[t].cpu().numpy() for x in (st.sag_idx, st.sag_val, st.sag_cnt))
+        for p in range(len(sc)):
+            j, q = divmod(p, Q)
+            if q not in blocks:
+                continue
+            low = j & ((1 << t) - 1)
+            X = ((j >> t) << (t + 1)) | low
+            oi, ov = res.sag_drops[(t, X * Q + q)]
+            c = int(sc[p])
+            assert c == len(oi), f"exchange {t} drop count pair {p}"
+            assert_idx_equal(si[p, :c], oi, f"exchange {t} drop idx pair {p}")
+            assert_bits_equal(sv[p, :c], ov, f"exchange {t} drop val pair {p}")
+    words = st.member.cpu().numpy()
+    mbits = np.unpackbits(words.view(np.uint8), bitorder="little").astype(bool)
+    assert not mbits[n:].any(), "member bits at or above n"
+    for b in blocks:
+        assert_bits_equal(st.dense[bounds[b]:bounds[b + 1]].cpu().numpy(), res.dense[b], f"dense block {b}")
+        want = np.zeros(bounds[b + 1] - bounds[b], bool)
+        want[np.asarray(res.final[b][0], np.int64) - bounds[b]] = True
+        assert np.array_equal(mbits[bounds[b]:bounds[b + 1]], want), f"member bits block {b}"
+    for w in range(P):
+        for b in blocks:
+            got = st.acc[w, bounds[b]:bounds[b + 1]].cpu().numpy()
+            assert_bits_equal(got, res.residual[(w, b)], f"residual w={w} b={b}")

@@ -167,6 +167,32 @@ def test_argument_errors_enqueue_nothing():
                                             null) == EINVAL
     assert lib.spardl_lazy_residual_collect(p, i64(100), i32(4), i64(100), i32(3), p, p, null, null) == EINVAL
     assert lib.spardl_lazy_residual_collect(p, i64(100), i32(4), i64(100), i32(26), p, p, p, null) == EINVAL
+    # R-SAG: d not a power of 2 or not dividing P, t out of range, small workspace, missing drop arrays
+    lib.spardl_rsag_workspace_bytes.argtypes = [i32, i32, i64, i32]
+    lib.spardl_rsag_workspace_bytes.restype = sz
+    assert lib.spardl_rsag_workspace_bytes(i32(12), i32(3), i64(1200), i32(5)) == 0
+    assert lib.spardl_rsag_workspace_bytes(i32(12), i32(8), i64(1200), i32(5)) == 0
+    assert lib.spardl_rsag_workspace_bytes(i32(8), i32(1), i64(1200), i32(5)) == 0
+    assert lib.spardl_rsag_workspace_bytes(i32(8), i32(4), i64(1200), i32(601)) == 0
+    assert lib.spardl_rsag_workspace_bytes(i32(8), i32(4), i64(1200), i32(600)) > 0
+    rm = lambda t, ws, wsz: lib.spardl_rsag_merge_topk(p, p, i32(8), i32(4), i64(1200), i32(5), i32(t), p, p, p,
+                                                       ws, wsz, null)
+    assert rm(2, p, big) == EINVAL
+    assert rm(-1, p, big) == EINVAL
+    assert rm(0, q, big) == EINVAL
+    assert rm(0, p, sz(64)) == ECAP
+    assert lib.spardl_rsag_merge_topk(p, p, i32(8), i32(3), i64(1200), i32(5), i32(0), p, p, p, p, big,
+                                      null) == EINVAL
+    one = (ctypes.c_void_p * 2)(0x1000, 0)
+    assert lib.spardl_rsag_residual(p, i64(1200), i32(8), i32(4), i64(1200), i32(5), p, one, one, one,
+                                    null) == EINVAL
+    assert lib.spardl_rsag_residual(p, i64(1200), i32(8), i32(4), i64(1200), i32(5), null, ok3, ok3, ok3,
+                                    null) == EINVAL
+    assert lib.spardl_rsag_residual(p, i64(1199), i32(8), i32(4), i64(1200), i32(5), p, ok3, ok3, ok3,
+                                    null) == EINVAL
+    lib.spardl_rsag_workspace_init.argtypes = [i32, i32, i64, i32, ctypes.c_void_p, sz, ctypes.c_void_p]
+    assert lib.spardl_rsag_workspace_init(i32(8), i32(4), i64(1200), i32(5), q, big, null) == EINVAL
+    assert lib.spardl_rsag_workspace_init(i32(8), i32(4), i64(1200), i32(5), p, sz(64), null) == ECAP
     for s in (0, -1, -2, -3, 7):
         assert lib.spardl_strerror(s)
 
