@@ -567,3 +567,146 @@ def spardl_step_rsag(acc, grad, P: int, n: int, L: int, d: int, blocks=None) -> 
             res.residual[(w, b)] = xi
             _block_of(acc[w], b, bounds)[...] = xi
     return res
+
+
+# ----------------------------------------------------------------------------
+# Spar-All-Gather across teams, Bruck form (B-SAG; Sec. III-D, case "d is not
+# a power of 2") and the compression-ratio controller (Algorithm 2)
+# ----------------------------------------------------------------------------
+#
+# Readings taken for this part (each one is listed in the design notes):
+#
+# * teams and the SRS inside them as for R-SAG; any d >= 2 dividing P.
+# * every worker keeps the top h of the block it holds after SRS (h is the
+#   controller's count for that block); what it drops is its own in-procedure
+#   residual, collected in full.
+# * the Bruck All-Gather hands every holder of block q the d top-h blocks; each
+#   sums them by index in team order (((team 0 + team 1) + team 2) + ...), so
+#   every team gets the same bits.  N_q is the number of distinct indices.
+# * if N_q > L the holders keep the top L, otherwise all N_q stay.  The paper
+#   gives each of the d holders 1/d of what this last selection drops; under
+#   Algorithm 1's collection that share never reaches a residual (a dropped
+#   index is not a final index, and off the final indices every worker keeps
+#   its own A, which already accounts for the dropped values), so it is not
+#   applied.  The same holds for the drops of R-SAG's last exchange.
+# * Algorithm 2 runs per block q (all holders see the same N_q): state (h,
+#   step, flag) in double precision, h = k/P = L/d, step = 0.01 (d - 1) L / d,
+#   flag = false, and N = 0 before the first step.  At each step: if
+#   (N > L) xor (step > 0) then (if flag: step = 2 step, flag = false; else
+#   flag = true) else step = -step / 2, flag = false; h = h + step, clamped to
+#   [L/d, L] (the range the paper gives for h); the count used is
+#   floor(h + 1/2), clamped to [1, L].  N is then this step's N_q.
+
+
+class HController:
+    """Algorithm 2 for one block: the top-h count of each step."""
+
+    def __init__(self, L: int, d: int):
+        self.L, self.d = L, d
+        self.lo = L / d
+        self.h = self.lo
+        self.step = 0.01 * (d - 1) * L / d
+        self.flag = False
+        self.N = 0
+
+    def next_count(self) -> int:
+        if (self.N > self.L) != (self.step > 0):
+            if self.flag:
+                self.step = self.step * 2.0
+                self.flag = False
+            else:
+                self.flag = True
+        else:
+            self.step = -self.step * 0.5
+            self.flag = False
+        self.h = min(max(self.h + self.step, self.lo), float(self.L))
+        return min(max(int(np.floor(self.h + 0.5)), 1), self.L)
+
+    def observe(self, N: int) -> None:
+        self.N = int(N)
+
+
+@dataclass
+class BsagStepResult:
+    """One B-SAG step; blocks are the Q = P / d blocks of a worker."""
+
+    bounds: list
+    blocks: list
+    h: dict = field(default_factory=dict)          # b -> top-h count used
+    local: dict = field(default_factory=dict)      # (w, b) -> (idx, val) after local top-L
+    S: dict = field(default_factory=dict)          # (w, b) -> (idx, val) after SRS
+    drops: dict = field(default_factory=dict)      # (i, w, b) -> SRS drops inside w's team
+    kept_h: dict = field(default_factory=dict)     # w -> (idx, val): top-h of the block w holds
+    drop_h: dict = field(default_factory=dict)     # w -> (idx, val): the rest of it
+    union: dict = field(default_factory=dict)      # b -> (idx, val): team-order sum of the top-h blocks
+    final_drops: dict = field(default_factory=dict)  # b -> (idx, val) dropped by the final top-L
+    final: dict = field(default_factory=dict)      # b -> (idx, val)
+    dense: dict = field(default_factory=dict)
+    residual: dict = field(default_factory=dict)
+
+
+def select_top(idx, val, c: int):
+    """Keep the top c of a sparse list (order of Sec. II / reading 4): returns
+    (kept_idx, kept_val, dropped_idx, dropped_val), both by ascending index."""
+    idx = np.asarray(idx, dtype=np.int64)
+    val = np.asarray(val, dtype=np.float32)
+    keep = top_k(idx, val, c)
+    mask = np.zeros(len(idx), dtype=bool)
+    mask[keep] = True
+    return idx[mask], val[mask], idx[~mask], val[~mask]
+
+
+def spardl_step_bsag(acc, grad, P: int, n: int, L: int, d: int, ctrl: dict, blocks=None) -> BsagStepResult:
+    """One SparDL synchronisation with d teams joined by B-SAG (Sec. III-D):
+    SRS inside every team, top-h, Bruck All-Gather across teams and summation,
+    top-L, All-Gather inside the team; global residual collection over every
+    kind of drop.  ctrl: {b: HController} carried across steps (created on
+    first use)."""
+    assert d >= 2 and P % d == 0
+    Q = P // d
+    bounds = block_bounds(n, Q)
+    blocks = list(range(Q)) if blocks is None else sorted(blocks)
+    res = BsagStepResult(bounds=bounds, blocks=blocks)
+    A = {}
+    for w in range(P):
+        for b in blocks:
+            A[(w, b)] = residual_add(_block_of(acc[w], b, bounds), _block_of(grad[w], b, bounds))
+            res.local[(w, b)] = local_sparsify(A[(w, b)], bounds[b], L)
+            res.S[(w, b)] = res.local[(w, b)]
+    for tau in range(d):
+        Sq = {(q, b): res.S[(tau * Q + q, b)] for q in range(Q) for b in blocks}
+        dr = spar_reduce_scatter(Sq, Q, L, blocks)
+        for (q, b), v in Sq.items():
+            res.S[(tau * Q + q, b)] = v
+        for (i, q, b), v in dr.items():
+            res.drops[(i, tau * Q + q, b)] = v
+    for q in blocks:
+        c = ctrl.setdefault(q, HController(L, d)).next_count()
+        res.h[q] = c
+        for tau in range(d):
+            w = tau * Q + q
+            ki, kv, di, dv = select_top(*res.S[(w, q)], c)
+            res.kept_h[w] = (ki, kv)
+            res.drop_h[w] = (di, dv)
+        ui, uv = res.kept_h[q]
+        for tau in range(1, d):
+            ui, uv = index_sum(ui, uv, *res.kept_h[tau * Q + q])
+        res.union[q] = (ui, uv)
+        ctrl[q].observe(len(ui))
+        if len(ui) > L:
+            ki, kv, di, dv = select_top(ui, uv, L)
+        else:
+            ki, kv, di, dv = ui, uv, ui[:0], uv[:0]
+        res.final[q] = (ki, kv)
+        res.final_drops[q] = (di, dv)
+    res.dense = allgather_densify(res.final, bounds, blocks)
+    l = num_steps(Q)
+    for w in range(P):
+        for b in blocks:
+            in_order = [res.drops[(i, w, b)] for i in range(1, l + 1) if (i, w, b) in res.drops]
+            if b == w % Q:
+                in_order.append(res.drop_h[w])
+            xi = global_residual_collect(A[(w, b)], bounds[b], res.local[(w, b)][0], res.final[b][0], in_order)
+            res.residual[(w, b)] = xi
+            _block_of(acc[w], b, bounds)[...] = xi
+    return res

@@ -220,3 +220,103 @@ def bf_step_rsag(acc_rows, grad_rows, P: int, L: int, d: int):
             row.append(r)
         new_res.append(row)
     return u, new_res, final
+
+
+class BfController:
+    """Algorithm 2 restated: returns the top-h count for the next step."""
+
+    def __init__(self, L, d):
+        self.L, self.d = L, d
+        self.state = {"h": L / d, "step": 0.01 * (d - 1) * L / d, "flag": False, "N": 0}
+
+    def count(self):
+        s = self.state
+        too_many = s["N"] > self.L
+        rising = s["step"] > 0
+        if too_many == rising:          # the xor is false: turn round, halve
+            s["step"] = -s["step"] * 0.5
+            s["flag"] = False
+        elif s["flag"]:                 # second step the same way in a row: double
+            s["step"] = s["step"] * 2.0
+            s["flag"] = False
+        else:
+            s["flag"] = True
+        s["h"] = min(max(s["h"] + s["step"], self.L / self.d), float(self.L))
+        c = int(s["h"] + 0.5)
+        return min(max(c, 1), self.L)
+
+
+def bf_step_bsag(acc_rows, grad_rows, P: int, L: int, d: int, ctrls: dict):
+    """d teams of Q = P / d consecutive workers: SRS inside each team, top-h of
+    each held block, all-gather across teams summed in team order, top-L when
+    more than L indices result (Sec. III-D, Algorithm 2 for h).
+
+    Returns (dense u, new residual rows, final dicts per block, counts h per
+    block, union sizes per block).
+    """
+    n = len(acc_rows[0])
+    Q = P // d
+    s = [b * n // Q for b in range(Q + 1)]
+    A = [[F32(F32(acc_rows[w][x]) + F32(grad_rows[w][x])) for x in range(n)] for w in range(P)]
+    state, local, ledger = {}, {}, [dict() for _ in range(P)]
+    for w in range(P):
+        for b in range(Q):
+            state[(w, b)] = bf_topk({x: A[w][x] for x in range(s[b], s[b + 1])}, L)
+            local[(w, b)] = dict(state[(w, b)])
+    l = 0
+    while (1 << l) < Q:
+        l += 1
+    for i in range(1, l + 1):
+        dist = 1 << (l - i)
+        lo, hi = 1 << (l - i), min(1 << (l - i + 1), Q)
+        for tau in range(d):
+            inbox = {}
+            for q in range(Q):
+                inbox[(q + dist) % Q] = [(b, dict(state[(tau * Q + q, b)])) for b in ((q + t) % Q for t in range(lo, hi))]
+            for r in range(Q):
+                w = tau * Q + r
+                for b, msg in inbox[r]:
+                    merged = bf_merge(state[(w, b)], msg)
+                    kept = bf_topk(merged, L)
+                    state[(w, b)] = kept
+                    for x, v in merged.items():
+                        if x not in kept:
+                            ledger[w].setdefault(x, []).append(v)
+    final, hs, Ns = {}, {}, {}
+    for q in range(Q):
+        c = ctrls.setdefault(q, BfController(L, d)).count()
+        hs[q] = c
+        gathered = []
+        for tau in range(d):
+            w = tau * Q + q
+            top = bf_topk(state[(w, q)], c)
+            for x, v in state[(w, q)].items():
+                if x not in top:
+                    ledger[w].setdefault(x, []).append(v)
+            gathered.append(top)
+        total = dict(gathered[0])
+        for g in gathered[1:]:
+            total = bf_merge(total, g)
+        Ns[q] = len(total)
+        ctrls[q].state["N"] = len(total)
+        final[q] = bf_topk(total, L)
+    u = [F32(0.0)] * n
+    I = set()
+    for q in range(Q):
+        for x, v in final[q].items():
+            u[x] = v
+            I.add(x)
+    new_res = []
+    for w in range(P):
+        row = []
+        for x in range(n):
+            if x not in I:
+                row.append(A[w][x])
+                continue
+            b = next(bb for bb in range(Q) if s[bb] <= x < s[bb + 1])
+            r = F32(0.0) if x in local[(w, b)] else A[w][x]
+            for v in ledger[w].get(x, []):
+                r = F32(r + v)
+            row.append(r)
+        new_res.append(row)
+    return u, new_res, final, hs, Ns
