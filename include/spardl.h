@@ -310,6 +310,58 @@ int spardl_rsag_residual(float* acc, int64_t ld_acc, int32_t P, int32_t d, int64
                          const uint32_t* member, const int32_t* const* drop_idx, const float* const* drop_val,
                          const int32_t* const* drop_cnt, hipStream_t stream);
 
+/* ---------------------------------------------------------------------------
+ * Spar-All-Gather across d teams, Bruck form (B-SAG; Sec. III-D, any d >= 2
+ * dividing P) with the compression-ratio controller of Algorithm 2.  Teams,
+ * their SRS and sp (P x Q x k_blk, k_blk = L = d k / P) as for R-SAG.  After
+ * the teams' SRS:
+ *   spardl_bsag_exchange(...);   final block q in sp[q][q], padded
+ *   spardl_allgather_densify(sp, P = Q, ..., member);
+ *   spardl_residual_collect(...) per team (with member), then
+ *   spardl_bsag_residual(..., member).
+ * ------------------------------------------------------------------------- */
+
+/* Workspace of spardl_bsag_exchange: 256-byte aligned, this many bytes,
+ * prepared once by spardl_bsag_workspace_init, which also sets Algorithm 2's
+ * initial state for every block (h = L/d, step = 0.01 (d-1) L / d, flag
+ * false, no previous count).  The workspace carries that state from step to
+ * step.  0 on invalid sizes: P < 2, d < 2, d not dividing P, n < Q,
+ * n >= 2^31, k_blk outside [1, floor(n / Q)]. */
+size_t spardl_bsag_workspace_bytes(int32_t P, int32_t d, int64_t n, int32_t k_blk);
+int spardl_bsag_workspace_init(int32_t P, int32_t d, int64_t n, int32_t k_blk, void* ws, size_t ws_bytes,
+                               hipStream_t stream);
+
+/* One B-SAG exchange (Sec. III-D; Algorithm 2), for every block q < Q:
+ *  1. Algorithm 2 updates block q's state from the previous union size and
+ *     gives the count h_q (in [1, k_blk]);
+ *  2. every holder w = tau*Q + q keeps the top h_q of sp[w][q]; the other
+ *     k_blk - h_q entries go to drop_idx/drop_val[w*k_blk + j],
+ *     j < drop_cnt[w], sorted by index (its own residual);
+ *  3. the d kept lists are summed by index in team order (the result of the
+ *     Bruck All-Gather, the same on every holder); N_q = its size;
+ *  4. sp[q][q] (team 0's holder) <- the top k_blk of that sum, or all of it
+ *     when N_q <= k_blk, sorted by index and padded to k_blk entries with
+ *     index INT32_MAX, value 0 (spardl_allgather_densify and the residual
+ *     calls skip such entries).
+ * info (optional, device, 2*Q int32): info[q] = h_q, info[Q + q] = N_q.
+ * Errors: EINVAL for NULL pointers, misaligned ws, invalid sizes (see
+ * spardl_bsag_workspace_bytes); ECAPACITY if ws is too small. */
+int spardl_bsag_exchange(int32_t* sp_idx, float* sp_val, int32_t P, int32_t d, int64_t n, int32_t k_blk,
+                         int32_t* drop_idx, float* drop_val, int32_t* drop_cnt, int32_t* info, void* ws,
+                         size_t ws_bytes, hipStream_t stream);
+
+/* Residual share of the top-h drops: every worker w adds its own drops
+ * (drop_idx/drop_val/drop_cnt of spardl_bsag_exchange) at final indices:
+ *   acc[w][x] = acc[w][x] + v   for every drop (x, v) of w with x in I.
+ * Run after the teams' spardl_residual_collect.  The final selection's drops
+ * need no share: none of their indices is final, and off I every worker
+ * keeps its own A.
+ * Errors: EINVAL for NULL pointers, misaligned member, invalid sizes,
+ * ld_acc < n. */
+int spardl_bsag_residual(float* acc, int64_t ld_acc, int32_t P, int32_t d, int64_t n, int32_t k_blk,
+                         const uint32_t* member, const int32_t* drop_idx, const float* drop_val,
+                         const int32_t* drop_cnt, hipStream_t stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -177,6 +177,48 @@ bool rsag_sizes_ok(int32_t P, int32_t d, int64_t n, int32_t kb) {
   return sizes_ok(P / d, n, kb);
 }
 
+// any d >= 2 dividing P, k_blk valid for blocks of a team of P / d
+bool bsag_sizes_ok(int32_t P, int32_t d, int64_t n, int32_t kb) {
+  if (P < 2 || d < 2 || P % d) return false;
+  return sizes_ok(P / d, n, kb);
+}
+
+// Workspace of the B-SAG exchange.
+struct BsagLayout {
+  size_t H, S, F, N, cnt, bm, kept_i, kept_v, U_i, U_v, fd_i, fd_v, fd_cnt, scratch, end;
+  uint32_t W;
+};
+
+BsagLayout make_bsag_layout(int32_t P, int32_t d, int64_t n, int32_t kb) {
+  BsagLayout L;
+  const int64_t Q = P / d;
+  const int64_t maxlen = (n + Q - 1) / Q;
+  L.W = (uint32_t)((maxlen + 31) / 32);
+  const int64_t cap = (int64_t)d * kb;
+  size_t off = 256;   // error word
+  auto take = [&](size_t bytes) {
+    const size_t at = off;
+    off += (bytes + 255) & ~(size_t)255;
+    return at;
+  };
+  L.H = take((size_t)Q * 8);
+  L.S = take((size_t)Q * 8);
+  L.F = take((size_t)Q * 4);
+  L.N = take((size_t)Q * 4);
+  L.cnt = take((size_t)Q * 4);
+  L.bm = take((size_t)Q * L.W * 4);
+  L.kept_i = take((size_t)P * kb * 4);
+  L.kept_v = take((size_t)P * kb * 4);
+  L.U_i = take((size_t)Q * cap * 4);
+  L.U_v = take((size_t)Q * cap * 4);
+  L.fd_i = take((size_t)Q * cap * 4);
+  L.fd_v = take((size_t)Q * cap * 4);
+  L.fd_cnt = take((size_t)Q * 4);
+  L.scratch = take((size_t)n * 4);
+  L.end = off;
+  return L;
+}
+
 struct Fill {
   FillRanges r{};
   Fill& add(void* p, int64_t words) {
@@ -483,6 +525,80 @@ int spardl_rsag_residual(float* acc, int64_t ld_acc, int32_t P, int32_t d, int64
   for (int32_t t = 0; t < steps; ++t)
     SPARDL_TRY(launch_grc_sag_drops(acc, ld_acc, n, Q, t, k_blk, (d / 2) * Q, drop_idx[t], drop_val[t], drop_cnt[t],
                                     member, stream));
+  return SPARDL_OK;
+}
+
+size_t spardl_bsag_workspace_bytes(int32_t P, int32_t d, int64_t n, int32_t k_blk) {
+  if (!bsag_sizes_ok(P, d, n, k_blk)) return 0;
+  return make_bsag_layout(P, d, n, k_blk).end;
+}
+
+int spardl_bsag_workspace_init(int32_t P, int32_t d, int64_t n, int32_t k_blk, void* ws, size_t ws_bytes,
+                               hipStream_t stream) {
+  if (!ws || ws_misaligned(ws)) return SPARDL_EINVAL;
+  const size_t need = spardl_bsag_workspace_bytes(P, d, n, k_blk);
+  if (need == 0) return SPARDL_EINVAL;
+  if (ws_bytes < need) return SPARDL_ECAPACITY;
+  const BsagLayout L = make_bsag_layout(P, d, n, k_blk);
+  char* base = (char*)ws;
+  const int32_t Q = P / d;
+  SPARDL_TRY(launch_fill(Fill().add(base, 64).add(base + L.bm, (int64_t)Q * L.W).r, stream));
+  // Algorithm 2's initial state: h = k/P = L/d, step = 0.01 (d - 1) L / d, flag false, N = 0
+  const double h0 = (double)k_blk / (double)d;
+  const double step0 = 0.01 * (d - 1) * k_blk / d;
+  SPARDL_TRY(launch_bsag_init(Q, h0, step0, (double*)(base + L.H), (double*)(base + L.S), (uint32_t*)(base + L.F),
+                              (uint32_t*)(base + L.N), stream));
+  return SPARDL_OK;
+}
+
+int spardl_bsag_exchange(int32_t* sp_idx, float* sp_val, int32_t P, int32_t d, int64_t n, int32_t k_blk,
+                         int32_t* drop_idx, float* drop_val, int32_t* drop_cnt, int32_t* info, void* ws,
+                         size_t ws_bytes, hipStream_t stream) {
+  if (!sp_idx || !sp_val || !drop_idx || !drop_val || !drop_cnt || !ws || ws_misaligned(ws) ||
+      !bsag_sizes_ok(P, d, n, k_blk))
+    return SPARDL_EINVAL;
+  if (ws_bytes < spardl_bsag_workspace_bytes(P, d, n, k_blk)) return SPARDL_ECAPACITY;
+  const BsagLayout L = make_bsag_layout(P, d, n, k_blk);
+  char* base = (char*)ws;
+  BsagArgs a;
+  a.sp_idx = sp_idx;
+  a.sp_val = sp_val;
+  a.Q = P / d;
+  a.d = d;
+  a.kb = k_blk;
+  a.n = n;
+  a.H = (double*)(base + L.H);
+  a.S = (double*)(base + L.S);
+  a.F = (uint32_t*)(base + L.F);
+  a.N = (uint32_t*)(base + L.N);
+  a.cnt = (uint32_t*)(base + L.cnt);
+  a.kept_i = (int32_t*)(base + L.kept_i);
+  a.kept_v = (float*)(base + L.kept_v);
+  a.drop_i = drop_idx;
+  a.drop_v = drop_val;
+  a.drop_cnt = drop_cnt;
+  a.scratch = (float*)(base + L.scratch);
+  a.bm = (uint32_t*)(base + L.bm);
+  a.W = L.W;
+  a.U_i = (int32_t*)(base + L.U_i);
+  a.U_v = (float*)(base + L.U_v);
+  a.fd_i = (int32_t*)(base + L.fd_i);
+  a.fd_v = (float*)(base + L.fd_v);
+  a.fd_cnt = (int32_t*)(base + L.fd_cnt);
+  a.info = info;
+  a.err = (uint32_t*)base;
+  SPARDL_TRY(launch_bsag_exchange(a, stream));
+  return SPARDL_OK;
+}
+
+int spardl_bsag_residual(float* acc, int64_t ld_acc, int32_t P, int32_t d, int64_t n, int32_t k_blk,
+                         const uint32_t* member, const int32_t* drop_idx, const float* drop_val,
+                         const int32_t* drop_cnt, hipStream_t stream) {
+  if (!acc || !member || (reinterpret_cast<uintptr_t>(member) & 3u) || !bsag_sizes_ok(P, d, n, k_blk) ||
+      ld_acc < n || !drop_idx || !drop_val || !drop_cnt)
+    return SPARDL_EINVAL;
+  // worker w's top-h drops: pairs of one entry each (m = 1), pair w = row w
+  SPARDL_TRY(launch_grc_drops(acc, ld_acc, n, 1, k_blk, P, drop_idx, drop_val, drop_cnt, member, stream));
   return SPARDL_OK;
 }
 

@@ -1746,6 +1746,246 @@ __global__ __launch_bounds__(256) void k_grc_sag_drops(float* __restrict__ acc, 
   }
 }
 
+// ============================================================================ B-SAG
+// Spar-All-Gather across d teams, Bruck form, and its compression-ratio
+// controller (Sec. III-D, Algorithm 2).  Per block q of a team's Q blocks the
+// workspace keeps the controller state (h, step, flag in double precision, the
+// last union size N) and the count used at this step.
+
+// Algorithm 2, one thread per block: update step and h from the last N, keep
+// h in [L/d, L], count = floor(h + 1/2) clamped to [1, L].
+__global__ __launch_bounds__(64) void k_bsag_control(uint32_t Q, uint32_t L, uint32_t d, double* __restrict__ H,
+                                                     double* __restrict__ S, uint32_t* __restrict__ F,
+                                                     const uint32_t* __restrict__ N, uint32_t* __restrict__ cnt) {
+  for (uint32_t q = blockIdx.x * 64u + threadIdx.x; q < Q; q += gridDim.x * 64u) {
+    double h = H[q], step = S[q];
+    uint32_t flag = F[q];
+    const bool too_many = N[q] > L;
+    if (too_many != (step > 0.0)) {
+      if (flag) {
+        step = step * 2.0;
+        flag = 0u;
+      } else {
+        flag = 1u;
+      }
+    } else {
+      step = -step * 0.5;
+      flag = 0u;
+    }
+    const double lo = (double)L / (double)d;
+    h = h + step;
+    h = h < lo ? lo : h;
+    h = h > (double)L ? (double)L : h;
+    double c = floor(h + 0.5);
+    c = c < 1.0 ? 1.0 : c;
+    c = c > (double)L ? (double)L : c;
+    H[q] = h;
+    S[q] = step;
+    F[q] = flag;
+    cnt[q] = (uint32_t)c;
+  }
+}
+
+__global__ __launch_bounds__(64) void k_bsag_init(uint32_t Q, double h0, double step0, double* __restrict__ H,
+                                                  double* __restrict__ S, uint32_t* __restrict__ F,
+                                                  uint32_t* __restrict__ N) {
+  for (uint32_t q = blockIdx.x * 64u + threadIdx.x; q < Q; q += gridDim.x * 64u) {
+    H[q] = h0;
+    S[q] = step0;
+    F[q] = 0u;
+    N[q] = 0u;
+  }
+}
+
+// Keep the top c of one sparse list sorted by index (the order of every
+// selection: larger |v| bits first, then the lower index), by the exact
+// three-level radix select of the merge threshold, then write the kept
+// entries in index order to K (and sentinels -- index INT32_MAX, value 0 --
+// from c up to `pad`), the rest in index order to D.  One workgroup of 1024
+// threads; the list is read five times (it is small and stays in L2).
+struct SelSmem {
+  uint32_t h[NB1];
+  uint32_t scratch[32];
+};
+
+__device__ void select_list(const int32_t* __restrict__ Ii, const float* __restrict__ Iv, uint32_t len,
+                            uint32_t c, int32_t* __restrict__ Ki, float* __restrict__ Kv, uint32_t pad,
+                            int32_t* __restrict__ Di, float* __restrict__ Dv, int32_t* dcnt, uint32_t* err,
+                            SelSmem& S) {
+  constexpr uint32_t NT = 1024;
+  if (c >= len) {
+    for (uint32_t j = threadIdx.x; j < len; j += NT) {
+      Ki[j] = Ii[j];
+      Kv[j] = Iv[j];
+    }
+    for (uint32_t j = len + threadIdx.x; j < pad; j += NT) {
+      Ki[j] = INT32_MAX;
+      Kv[j] = 0.f;
+    }
+    if (threadIdx.x == 0 && dcnt) *dcnt = 0;
+    return;
+  }
+  for (uint32_t i = threadIdx.x; i < NB1; i += NT) S.h[i] = 0u;
+  __syncthreads();
+  for (uint32_t j = threadIdx.x; j < len; j += NT) atomicAdd(&S.h[mag_key(Iv[j]) >> D1_SHIFT], 1u);
+  __syncthreads();
+  uint32_t T1, above1, cnt1, ok;
+  block_select_desc(S.h, NB1, c, S.scratch, &T1, &above1, &cnt1, &ok);
+  if (!ok) {
+    if (threadIdx.x == 0) atomicOr(err, ERR_COUNT);
+    return;
+  }
+  uint32_t tge, teq, need_eq;
+  resolve_low_digits(T1, c - above1, cnt1, S.h, S.scratch, err,
+                     [&](auto f) {
+                       for (uint32_t j = threadIdx.x; j < len; j += NT) {
+                         const uint32_t key = mag_key(Iv[j]);
+                         if ((key >> D1_SHIFT) == T1) f(key);
+                       }
+                     },
+                     tge, teq, need_eq);
+  // thread t owns the consecutive entries [t per, (t + 1) per): counts, scan, emit
+  const uint32_t per = (len + NT - 1) / NT;
+  const uint32_t j0 = min(len, threadIdx.x * per), j1 = min(len, j0 + per);
+  uint32_t ng = 0, ne = 0;
+  __syncthreads();   // the scans below reuse scratch
+  for (uint32_t j = j0; j < j1; ++j) {
+    const uint32_t key = mag_key(Iv[j]);
+    ng += key >= tge;
+    ne += need_eq != 0u && key == teq;
+  }
+  uint32_t tot_g, tot_e;
+  uint32_t rg = block_excl_scan(ng, S.scratch, &tot_g);
+  uint32_t re = block_excl_scan(ne, S.scratch, &tot_e);
+  if (threadIdx.x == 0 && tot_g + min(tot_e, need_eq) != c) atomicOr(err, ERR_COUNT_SUM);
+  for (uint32_t j = j0; j < j1; ++j) {
+    const int32_t x = Ii[j];
+    const float v = Iv[j];
+    const uint32_t key = mag_key(v);
+    const bool is_g = key >= tge, is_e = need_eq != 0u && key == teq;
+    const uint32_t before = rg + min(re, need_eq);
+    if (is_g || (is_e && re < need_eq)) {
+      if (before < c) {
+        Ki[before] = x;
+        Kv[before] = v;
+      }
+    } else if (j - before < len - c) {
+      Di[j - before] = x;
+      Dv[j - before] = v;
+    }
+    rg += is_g;
+    re += is_e;
+  }
+  for (uint32_t j = c + threadIdx.x; j < pad; j += NT) {
+    Ki[j] = INT32_MAX;
+    Kv[j] = 0.f;
+  }
+  if (threadIdx.x == 0 && dcnt) *dcnt = (int32_t)(len - c);
+}
+
+// Top-h of the block every worker holds after its team's SRS: worker w =
+// tau Q + q holds sp[w][q]; keeps cnt[q] entries in kept[w], drops the rest
+// to drop[w] (k_blk entries per worker).  One workgroup per worker.
+__global__ __launch_bounds__(1024) void k_bsag_toph(const int32_t* __restrict__ sp_idx,
+                                                    const float* __restrict__ sp_val, uint32_t Q, uint32_t kb,
+                                                    const uint32_t* __restrict__ cnt, int32_t* __restrict__ kept_i,
+                                                    float* __restrict__ kept_v, int32_t* __restrict__ drop_i,
+                                                    float* __restrict__ drop_v, int32_t* __restrict__ drop_cnt,
+                                                    uint32_t* __restrict__ err) {
+  __shared__ SelSmem S;
+  const uint32_t w = blockIdx.x, q = w % Q;
+  const int64_t in = ((int64_t)w * Q + q) * kb, o = (int64_t)w * kb;
+  const uint32_t c = min(cnt[q], kb);
+  select_list(sp_idx + in, sp_val + in, kb, c, kept_i + o, kept_v + o, 0u, drop_i + o, drop_v + o, drop_cnt + w,
+              err, S);
+}
+
+// The Bruck All-Gather's result summed in team order, for block q: the d
+// kept lists of the holders of q are scattered one team after the other into
+// a dense row (first occurrence stores, later ones add) with a bitmap of the
+// occupied indices, which the compaction then walks in index order (and
+// clears).  One workgroup per block; bm gives block q the words
+// [q W, (q + 1) W), W = ceil(max block length / 32).
+__global__ __launch_bounds__(1024) void k_bsag_union(const int32_t* __restrict__ kept_i,
+                                                     const float* __restrict__ kept_v, Blocks B, uint32_t d,
+                                                     uint32_t kb, const uint32_t* __restrict__ cnt,
+                                                     float* __restrict__ scratch, uint32_t* __restrict__ bm,
+                                                     uint32_t W, int32_t* __restrict__ U_i, float* __restrict__ U_v,
+                                                     uint32_t* __restrict__ N, int32_t* __restrict__ info,
+                                                     uint32_t* __restrict__ err) {
+  constexpr uint32_t NT = 1024;
+  __shared__ uint32_t sc[32];
+  const uint32_t q = blockIdx.x, Q = B.P;
+  const uint32_t s = B.start(q), e = B.start(q + 1u);
+  const uint32_t c = min(cnt[q], kb);
+  uint32_t* __restrict__ M = bm + (int64_t)q * W;
+  for (uint32_t tau = 0; tau < d; ++tau) {
+    const int64_t o = ((int64_t)tau * Q + q) * kb;
+    for (uint32_t j = threadIdx.x; j < c; j += NT) {
+      const int32_t x = kept_i[o + j];
+      if (x < (int32_t)s || x >= (int32_t)e) continue;
+      const uint32_t r = (uint32_t)x - s, bit = 1u << (r & 31u);
+      const float v = kept_v[o + j];
+      // the atomic's old word says whether an earlier team brought this index
+      if (atomicOr(&M[r >> 5], bit) & bit) scratch[x] = scratch[x] + v;
+      else scratch[x] = v;
+    }
+    __syncthreads();   // a later team's entry for the same index must see this one
+  }
+  const uint32_t words = (e - s + 31u) >> 5;
+  const uint32_t per = (words + NT - 1) / NT;
+  const uint32_t w0 = min(words, threadIdx.x * per), w1 = min(words, w0 + per);
+  // the words were written by atomics (performed in L2): read them past L1
+  auto word = [&](uint32_t i) { return __hip_atomic_load(&M[i], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT); };
+  uint32_t mine = 0;
+  for (uint32_t i = w0; i < w1; ++i) mine += __popc(word(i));
+  uint32_t tot;
+  uint32_t pos = block_excl_scan(mine, sc, &tot);
+  const uint32_t cap = d * kb;
+  int32_t* __restrict__ Ui = U_i + (int64_t)q * cap;
+  float* __restrict__ Uv = U_v + (int64_t)q * cap;
+  for (uint32_t i = w0; i < w1; ++i) {
+    uint32_t m = word(i);
+    if (m == 0u) continue;
+    M[i] = 0u;
+    while (m) {
+      const uint32_t b = __ffs(m) - 1u;
+      m &= m - 1u;
+      const int32_t x = (int32_t)(s + 32u * i + b);
+      if (pos < cap) {
+        Ui[pos] = x;
+        Uv[pos] = scratch[x];
+      }
+      ++pos;
+    }
+  }
+  if (threadIdx.x == 0) {
+    if (tot > cap) atomicOr(err, ERR_COUNT);
+    N[q] = tot;
+    if (info) {
+      info[q] = (int32_t)c;
+      info[Q + q] = (int32_t)tot;
+    }
+  }
+}
+
+// Final top-L of each block's union (all of it when it has at most L
+// entries), into sp[q][q] padded to k_blk with sentinels; the dropped entries
+// to fdrop[q].  One workgroup per block.
+__global__ __launch_bounds__(1024) void k_bsag_final(const int32_t* __restrict__ U_i, const float* __restrict__ U_v,
+                                                     const uint32_t* __restrict__ N, uint32_t Q, uint32_t d,
+                                                     uint32_t kb, int32_t* __restrict__ sp_idx,
+                                                     float* __restrict__ sp_val, int32_t* __restrict__ fd_i,
+                                                     float* __restrict__ fd_v, int32_t* __restrict__ fd_cnt,
+                                                     uint32_t* __restrict__ err) {
+  __shared__ SelSmem S;
+  const uint32_t q = blockIdx.x;
+  const uint32_t cap = d * kb;
+  const uint32_t len = min(N[q], cap);
+  const int64_t in = (int64_t)q * cap, o = ((int64_t)q * Q + q) * kb;
+  select_list(U_i + in, U_v + in, len, kb, sp_idx + o, sp_val + o, kb, fd_i + in, fd_v + in, fd_cnt + q, err, S);
+}
+
 // ============================================================================ lazy summation
 // One SRS step of the lazy variant (Sec. III-B "Optimization for SRS",
 // Algorithm 1): worker w sent sp[w][b], b = (w + d + t) mod P for t < m, to
@@ -1915,6 +2155,25 @@ hipError_t launch_grc_sag_drops(float* acc, int64_t ld_acc, int64_t n, int32_t Q
   const dim3 grid(grid_for(kb, 256, 1024), (unsigned)std::min<int32_t>(npairs, 65535));
   hipLaunchKernelGGL(k_grc_sag_drops, grid, dim3(256), 0, s, acc, ld_acc, (uint32_t)n, (uint32_t)Q, (uint32_t)t,
                      (uint32_t)kb, (uint32_t)npairs, drop_idx, drop_val, drop_cnt, bm, 1.0f / (float)(2 << t));
+  return hipGetLastError();
+}
+
+hipError_t launch_bsag_init(int32_t Q, double h0, double step0, double* H, double* S, uint32_t* F, uint32_t* N,
+                            hipStream_t s) {
+  hipLaunchKernelGGL(k_bsag_init, dim3(grid_for(Q, 64, 1024)), dim3(64), 0, s, (uint32_t)Q, h0, step0, H, S, F, N);
+  return hipGetLastError();
+}
+
+hipError_t launch_bsag_exchange(const BsagArgs& a, hipStream_t s) {
+  const uint32_t Q = (uint32_t)a.Q, d = (uint32_t)a.d, kb = (uint32_t)a.kb;
+  hipLaunchKernelGGL(k_bsag_control, dim3(grid_for(Q, 64, 1024)), dim3(64), 0, s, Q, kb, d, a.H, a.S, a.F, a.N,
+                     a.cnt);
+  hipLaunchKernelGGL(k_bsag_toph, dim3(Q * d), dim3(1024), 0, s, a.sp_idx, a.sp_val, Q, kb, a.cnt, a.kept_i,
+                     a.kept_v, a.drop_i, a.drop_v, a.drop_cnt, a.err);
+  hipLaunchKernelGGL(k_bsag_union, dim3(Q), dim3(1024), 0, s, a.kept_i, a.kept_v, make_blocks(a.n, a.Q), d, kb,
+                     a.cnt, a.scratch, a.bm, a.W, a.U_i, a.U_v, a.N, a.info, a.err);
+  hipLaunchKernelGGL(k_bsag_final, dim3(Q), dim3(1024), 0, s, a.U_i, a.U_v, a.N, Q, d, kb, a.sp_idx, a.sp_val,
+                     a.fd_i, a.fd_v, a.fd_cnt, a.err);
   return hipGetLastError();
 }
 

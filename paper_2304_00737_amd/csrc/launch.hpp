@@ -60,6 +60,33 @@ hipError_t launch_grc_zero(float* acc, int64_t ld_acc, int32_t P, int64_t n, int
 hipError_t launch_grc_sag_drops(float* acc, int64_t ld_acc, int64_t n, int32_t Q, int32_t t, int32_t kb,
                                 int32_t npairs, const int32_t* drop_idx, const float* drop_val,
                                 const int32_t* drop_cnt, const uint32_t* bm, hipStream_t s);
+// Device arrays of one B-SAG exchange (kernels.hip, B-SAG section).
+struct BsagArgs {
+  int32_t* sp_idx;
+  float* sp_val;
+  int32_t Q, d, kb;
+  int64_t n;
+  double *H, *S;            // controller h and step per block
+  uint32_t *F, *N, *cnt;    // controller flag, last union size, count in use
+  int32_t* kept_i;          // top-h of every worker's held block (P x kb)
+  float* kept_v;
+  int32_t* drop_i;          // the rest (caller's arrays, P x kb, counts P)
+  float* drop_v;
+  int32_t* drop_cnt;
+  float* scratch;           // n floats
+  uint32_t* bm;             // Q x W words, at zero between calls
+  uint32_t W;
+  int32_t* U_i;             // team-order sums (Q x d kb)
+  float* U_v;
+  int32_t* fd_i;            // final drops (Q x d kb, counts Q)
+  float* fd_v;
+  int32_t* fd_cnt;
+  int32_t* info;            // optional: count used and union size per block
+  uint32_t* err;
+};
+hipError_t launch_bsag_init(int32_t Q, double h0, double step0, double* H, double* S, uint32_t* F, uint32_t* N,
+                            hipStream_t s);
+hipError_t launch_bsag_exchange(const BsagArgs& a, hipStream_t s);
 hipError_t launch_lazy_step(float* acc, int64_t ld_acc, int32_t P, int64_t n, int32_t kb, int32_t d, int32_t m,
                             const int32_t* sp_idx, const float* sp_val, float* saved, const uint32_t* bm,
                             bool restore, hipStream_t s);

@@ -50,9 +50,14 @@ _lib.spardl_rsag_workspace_bytes.restype = _sz
 _lib.spardl_rsag_workspace_init.argtypes = [_i32, _i32, _i64, _i32, _p, _sz, _p]
 _lib.spardl_rsag_merge_topk.argtypes = [_p, _p, _i32, _i32, _i64, _i32, _i32, _p, _p, _p, _p, _sz, _p]
 _lib.spardl_rsag_residual.argtypes = [_p, _i64, _i32, _i32, _i64, _i32, _p, _p, _p, _p, _p]
+_lib.spardl_bsag_workspace_bytes.argtypes = [_i32, _i32, _i64, _i32]
+_lib.spardl_bsag_workspace_bytes.restype = _sz
+_lib.spardl_bsag_workspace_init.argtypes = [_i32, _i32, _i64, _i32, _p, _sz, _p]
+_lib.spardl_bsag_exchange.argtypes = [_p, _p, _i32, _i32, _i64, _i32, _p, _p, _p, _p, _p, _sz, _p]
+_lib.spardl_bsag_residual.argtypes = [_p, _i64, _i32, _i32, _i64, _i32, _p, _p, _p, _p, _p]
 for _f in ("residual_add", "block_topk", "sparse_merge_topk", "allgather_densify", "residual_collect",
            "lazy_topk", "lazy_receive", "lazy_residual_collect", "rsag_workspace_init", "rsag_merge_topk",
-           "rsag_residual"):
+           "rsag_residual", "bsag_workspace_init", "bsag_exchange", "bsag_residual"):
     getattr(_lib, "spardl_" + _f).restype = ctypes.c_int
 
 
@@ -216,6 +221,31 @@ def rsag_residual(acc, P: int, d: int, n: int, k_blk: int, member, drop_idx, dro
                                                       _stream(stream)))
 
 
+def bsag_workspace(P: int, d: int, n: int, k_blk: int, device="cuda", *, stream=None):
+    """A prepared workspace for spardl_bsag_exchange (it carries Algorithm 2's state)."""
+    nbytes = int(_lib.spardl_bsag_workspace_bytes(P, d, n, k_blk))
+    if nbytes == 0:
+        raise SpardlError("bsag_workspace_bytes", EINVAL)
+    ws = torch.empty(nbytes, dtype=torch.uint8, device=device)
+    _check("bsag_workspace_init", _lib.spardl_bsag_workspace_init(P, d, n, k_blk, _ptr(ws), nbytes, _stream(stream)))
+    return ws
+
+
+def bsag_exchange(sp_idx, sp_val, P: int, d: int, n: int, k_blk: int, drop_idx, drop_val, drop_cnt, ws, info=None,
+                  *, stream=None) -> None:
+    _check("bsag_exchange", _lib.spardl_bsag_exchange(
+        _ptr(sp_idx), _ptr(sp_val), P, d, n, k_blk, _ptr(drop_idx), _ptr(drop_val), _ptr(drop_cnt), _ptr(info),
+        _ptr(ws), ws.numel() * ws.element_size(), _stream(stream)))
+
+
+def bsag_residual(acc, P: int, d: int, n: int, k_blk: int, member, drop_idx, drop_val, drop_cnt, *, ld_acc=None,
+                  stream=None) -> None:
+    ld_acc = _ld(acc, n) if ld_acc is None else ld_acc
+    _check("bsag_residual", _lib.spardl_bsag_residual(_ptr(acc), ld_acc, P, d, n, k_blk, _ptr(member),
+                                                      _ptr(drop_idx), _ptr(drop_val), _ptr(drop_cnt),
+                                                      _stream(stream)))
+
+
 def ws_error(ws) -> int:
     """Error word at the start of a workspace (synchronises the current stream)."""
     return int(ws[:4].view(torch.int32).cpu().item())
@@ -370,7 +400,8 @@ class SparDLLazyStep:
 
 class SparDLSagStep:
     """P simulated workers in d teams of Q = P / d joined by R-SAG (Sec. III-D,
-    d a power of 2), one synchronisation step through the C ABI.
+    d a power of 2) or, with bruck=True, by B-SAG (any d dividing P, top-h
+    counts from Algorithm 2), one synchronisation step through the C ABI.
 
     k_blk is L(k, d, P) = d k / P, the entries per block of a team's Q blocks.
     After step(grad): dense / member as for SparDLStep; sp_idx/sp_val[w, b]
@@ -379,10 +410,11 @@ class SparDLSagStep:
     team; sag_*[t][p] what pair p dropped at exchange t.
     """
 
-    def __init__(self, P: int, d: int, n: int, k_blk: int, device="cuda", fused: bool = True):
-        if d < 2 or d & (d - 1) or P % d:
-            raise ValueError("R-SAG needs a power-of-two d >= 2 dividing P")
+    def __init__(self, P: int, d: int, n: int, k_blk: int, device="cuda", fused: bool = True, bruck: bool = False):
+        if d < 2 or P % d or (not bruck and d & (d - 1)):
+            raise ValueError("d >= 2 must divide P (and be a power of two for R-SAG)")
         self.P, self.d, self.Q, self.n, self.k_blk, self.fused = P, d, P // d, n, k_blk, fused
+        self.bruck = bruck
         Q = self.Q
         dev = torch.device(device)
         self.acc = torch.zeros((P, n), dtype=torch.float32, device=dev)
@@ -393,15 +425,23 @@ class SparDLSagStep:
         self.drop_idx = [torch.empty((P, m, k_blk), dtype=torch.int32, device=dev) for m in self.bags]
         self.drop_val = [torch.empty((P, m, k_blk), dtype=torch.float32, device=dev) for m in self.bags]
         self.drop_cnt = [torch.empty((P, m), dtype=torch.int32, device=dev) for m in self.bags]
-        self.steps = d.bit_length() - 1
-        npairs = (d // 2) * Q
-        self.sag_idx = [torch.empty((npairs, k_blk), dtype=torch.int32, device=dev) for _ in range(self.steps)]
-        self.sag_val = [torch.empty((npairs, k_blk), dtype=torch.float32, device=dev) for _ in range(self.steps)]
-        self.sag_cnt = [torch.empty(npairs, dtype=torch.int32, device=dev) for _ in range(self.steps)]
         self.dense = torch.empty(n, dtype=torch.float32, device=dev)
         self.member = torch.empty(member_words(n), dtype=torch.int32, device=dev)
         self.ws_team = [workspace(Q, Q, n, k_blk, device=dev) for _ in range(d)]
-        self.ws_sag = rsag_workspace(P, d, n, k_blk, device=dev)
+        if bruck:
+            self.steps = 1
+            self.toph_idx = torch.empty((P, k_blk), dtype=torch.int32, device=dev)
+            self.toph_val = torch.empty((P, k_blk), dtype=torch.float32, device=dev)
+            self.toph_cnt = torch.empty(P, dtype=torch.int32, device=dev)
+            self.info = torch.empty(2 * Q, dtype=torch.int32, device=dev)
+            self.ws_sag = bsag_workspace(P, d, n, k_blk, device=dev)
+        else:
+            self.steps = d.bit_length() - 1
+            npairs = (d // 2) * Q
+            self.sag_idx = [torch.empty((npairs, k_blk), dtype=torch.int32, device=dev) for _ in range(self.steps)]
+            self.sag_val = [torch.empty((npairs, k_blk), dtype=torch.float32, device=dev) for _ in range(self.steps)]
+            self.sag_cnt = [torch.empty(npairs, dtype=torch.int32, device=dev) for _ in range(self.steps)]
+            self.ws_sag = rsag_workspace(P, d, n, k_blk, device=dev)
 
     def _rows(self, tau):
         return slice(tau * self.Q, (tau + 1) * self.Q)
@@ -426,6 +466,10 @@ class SparDLSagStep:
                                   self.ws_team[tau], stream=stream)
 
     def exchanges(self, stream=None):
+        if self.bruck:
+            bsag_exchange(self.sp_idx, self.sp_val, self.P, self.d, self.n, self.k_blk, self.toph_idx,
+                          self.toph_val, self.toph_cnt, self.ws_sag, self.info, stream=stream)
+            return
         for t in range(self.steps):
             rsag_merge_topk(self.sp_idx, self.sp_val, self.P, self.d, self.n, self.k_blk, t, self.sag_idx[t],
                             self.sag_val[t], self.sag_cnt[t], self.ws_sag, stream=stream)
@@ -441,8 +485,12 @@ class SparDLSagStep:
             residual_collect(self.acc[r], self.Q, self.n, self.k_blk, self.local_idx[r], self.sp_idx[r],
                              [t[r] for t in self.drop_idx], [t[r] for t in self.drop_val],
                              [t[r] for t in self.drop_cnt], self.ws_team[tau], self.member, stream=stream)
-        rsag_residual(self.acc, self.P, self.d, self.n, self.k_blk, self.member, self.sag_idx, self.sag_val,
-                      self.sag_cnt, stream=stream)
+        if self.bruck:
+            bsag_residual(self.acc, self.P, self.d, self.n, self.k_blk, self.member, self.toph_idx, self.toph_val,
+                          self.toph_cnt, stream=stream)
+        else:
+            rsag_residual(self.acc, self.P, self.d, self.n, self.k_blk, self.member, self.sag_idx, self.sag_val,
+                          self.sag_cnt, stream=stream)
 
     def step(self, grad, stream=None):
         self.add_and_select(grad, stream)

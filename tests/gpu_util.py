@@ -212,3 +212,67 @@ def compare_sag_step(st, res, blocks=None) -> None:
         for b in blocks:
             got = st.acc[w, bounds[b]:bounds[b + 1]].cpu().numpy()
             assert_bits_equal(got, res.residual[(w, b)], f"residual w={w} b={b}")
+
+
+def compare_bsag_step(st, res, blocks=None) -> None:
+    """Compare the GPU state after one B-SAG step with an oracle BsagStepResult:
+    local selections, every worker's block state after its team's SRS, the
+    SRS drops, the controller's counts and union sizes, every worker's top-h
+    drops, the final blocks (sentinel-padded in sp[q][q]), the dense update,
+    the bitmap of I and the residuals, bit for bit."""
+    P, d, Q, n, L = st.P, st.d, st.Q, st.n, st.k_blk
+    blocks = list(range(Q)) if blocks is None else list(blocks)
+    bounds = so.block_bounds(n, Q)
+    sp_idx, sp_val = st.sp_idx.cpu().numpy(), st.sp_val.cpu().numpy()
+    local = st.local_idx.cpu().numpy()
+    for w in range(P):
+        for b in blocks:
+            assert_idx_equal(local[w, b], res.local[(w, b)][0], f"local_idx w={w} b={b}")
+            if w == b:           # team 0's holder of block b: the final block
+                fi, fv = res.final[b]
+                c = len(fi)
+                assert_idx_equal(sp_idx[w, b, :c], fi, f"final idx block {b}")
+                assert_bits_equal(sp_val[w, b, :c], fv, f"final val block {b}")
+                assert (sp_idx[w, b, c:] == np.iinfo(np.int32).max).all(), f"final padding block {b}"
+                assert (sp_val[w, b, c:] == 0).all(), f"final padding values block {b}"
+                continue
+            si, sv = res.S[(w, b)]
+            assert_idx_equal(sp_idx[w, b], si, f"sp_idx w={w} b={b}")
+            assert_bits_equal(sp_val[w, b], sv, f"sp_val w={w} b={b}")
+    for i, m in enumerate(st.bags, start=1):
+        di, dv, dc = (x[i - 1].cpu().numpy() for x in (st.drop_idx, st.drop_val, st.drop_cnt))
+        for w in range(P):
+            q = w % Q
+            for t in range(m):
+                b = (q + t) % Q
+                if b not in blocks:
+                    continue
+                oi, ov = res.drops[(i, w, b)]
+                c = int(dc[w, t])
+                assert c == len(oi), f"team drop count step {i} w={w} b={b}"
+                assert_idx_equal(di[w, t, :c], oi, f"team drop idx step {i} w={w} b={b}")
+                assert_bits_equal(dv[w, t, :c], ov, f"team drop val step {i} w={w} b={b}")
+    info = st.info.cpu().numpy()
+    th_i, th_v, th_c = st.toph_idx.cpu().numpy(), st.toph_val.cpu().numpy(), st.toph_cnt.cpu().numpy()
+    for q in blocks:
+        assert int(info[q]) == res.h[q], f"top-h count block {q}: {int(info[q])} vs {res.h[q]}"
+        assert int(info[Q + q]) == len(res.union[q][0]), f"union size block {q}"
+        for tau in range(d):
+            w = tau * Q + q
+            oi, ov = res.drop_h[w]
+            c = int(th_c[w])
+            assert c == len(oi), f"top-h drop count w={w}"
+            assert_idx_equal(th_i[w, :c], oi, f"top-h drop idx w={w}")
+            assert_bits_equal(th_v[w, :c], ov, f"top-h drop val w={w}")
+    words = st.member.cpu().numpy()
+    mbits = np.unpackbits(words.view(np.uint8), bitorder="little").astype(bool)
+    assert not mbits[n:].any(), "member bits at or above n"
+    for b in blocks:
+        assert_bits_equal(st.dense[bounds[b]:bounds[b + 1]].cpu().numpy(), res.dense[b], f"dense block {b}")
+        want = np.zeros(bounds[b + 1] - bounds[b], bool)
+        want[np.asarray(res.final[b][0], np.int64) - bounds[b]] = True
+        assert np.array_equal(mbits[bounds[b]:bounds[b + 1]], want), f"member bits block {b}"
+    for w in range(P):
+        for b in blocks:
+            got = st.acc[w, bounds[b]:bounds[b + 1]].cpu().numpy()
+            assert_bits_equal(got, res.residual[(w, b)], f"residual w={w} b={b}")

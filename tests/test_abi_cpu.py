@@ -193,6 +193,25 @@ def test_argument_errors_enqueue_nothing():
     lib.spardl_rsag_workspace_init.argtypes = [i32, i32, i64, i32, ctypes.c_void_p, sz, ctypes.c_void_p]
     assert lib.spardl_rsag_workspace_init(i32(8), i32(4), i64(1200), i32(5), q, big, null) == EINVAL
     assert lib.spardl_rsag_workspace_init(i32(8), i32(4), i64(1200), i32(5), p, sz(64), null) == ECAP
+    # B-SAG: d not dividing P, k_blk too large for a team block, small or misaligned workspace
+    lib.spardl_bsag_workspace_bytes.argtypes = [i32, i32, i64, i32]
+    lib.spardl_bsag_workspace_bytes.restype = sz
+    assert lib.spardl_bsag_workspace_bytes(i32(14), i32(4), i64(1400), i32(5)) == 0
+    assert lib.spardl_bsag_workspace_bytes(i32(14), i32(1), i64(1400), i32(5)) == 0
+    assert lib.spardl_bsag_workspace_bytes(i32(14), i32(7), i64(1400), i32(701)) == 0
+    assert lib.spardl_bsag_workspace_bytes(i32(14), i32(7), i64(1400), i32(700)) > 0
+    bx = lambda P_, d_, ws, wsz: lib.spardl_bsag_exchange(p, p, i32(P_), i32(d_), i64(1400), i32(5), p, p, p, null,
+                                                          ws, wsz, null)
+    assert bx(14, 4, p, big) == EINVAL
+    assert bx(14, 7, q, big) == EINVAL
+    assert bx(14, 7, p, sz(64)) == ECAP
+    assert lib.spardl_bsag_residual(p, i64(1400), i32(14), i32(7), i64(1400), i32(5), null, p, p, p,
+                                    null) == EINVAL
+    assert lib.spardl_bsag_residual(p, i64(1400), i32(14), i32(7), i64(1400), i32(5), p, null, p, p,
+                                    null) == EINVAL
+    lib.spardl_bsag_workspace_init.argtypes = [i32, i32, i64, i32, ctypes.c_void_p, sz, ctypes.c_void_p]
+    assert lib.spardl_bsag_workspace_init(i32(14), i32(7), i64(1400), i32(5), q, big, null) == EINVAL
+    assert lib.spardl_bsag_workspace_init(i32(14), i32(7), i64(1400), i32(5), p, sz(64), null) == ECAP
     for s in (0, -1, -2, -3, 7):
         assert lib.spardl_strerror(s)
 

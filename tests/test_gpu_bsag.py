@@ -1,0 +1,97 @@
+"""Bit-exact parity of SparDL with d teams joined by B-SAG (Sec. III-D, any d
+dividing P) and the h controller of Algorithm 2, through the C ABI, with the
+CPU oracle's spardl_step_bsag over consecutive steps (residual and
+controller state carried): SRS state and drops, the counts h and union sizes,
+the top-h drops, the final blocks, the dense update, the bitmap of I and the
+residuals."""
+
+import numpy as np
+import pytest
+
+from oracle import spardl_oracle as so
+from tests.conftest import gpu_available
+from tests.gpu_util import compare_bsag_step, log
+
+pytestmark = pytest.mark.gpu
+
+if gpu_available():
+    import torch
+    from paper_2304_00737_amd import spardl
+    from paper_2304_00737_amd import workloads as W
+
+
+def _dev(a):
+    return torch.from_numpy(np.ascontiguousarray(a)).cuda()
+
+
+def _check(st):
+    assert spardl.ws_error(st.ws_sag) == 0
+    for ws in st.ws_team:
+        assert spardl.ws_error(ws) == 0
+
+
+CASES = [
+    # P, d, n, L, kind, steps, fused
+    (2, 2, 4000, 300, "normal", 4, True),
+    (6, 3, 9000, 500, "normal", 5, True),
+    (6, 2, 6001, 40, "ties", 3, True),
+    (9, 3, 30000, 1000, "normal", 4, False),
+    (8, 4, 20000, 700, "dyadic", 3, True),
+    (10, 5, 12345, 1, "normal", 2, True),
+    (12, 3, 40000, 2000, "ties", 3, True),
+    (14, 7, 70000, 3000, "normal", 5, True),
+    (5, 5, 2000, 2000, "dyadic", 2, True),    # Q = 1, L = the whole row: nothing is lost
+    (4, 2, 3000, 7, "const", 2, True),
+    (6, 3, 6000, 11, "zeros", 2, False),
+]
+
+
+@pytest.mark.parametrize("P,d,n,L,kind,steps,fused", CASES)
+def test_bsag_step(P, d, n, L, kind, steps, fused):
+    log(f"bsag step P={P} d={d} n={n} L={L} kind={kind} steps={steps} fused={fused}")
+    st = spardl.SparDLSagStep(P, d, n, L, fused=fused, bruck=True)
+    acc = np.zeros((P, n), np.float32)
+    ctrl = {}
+    hs = set()
+    for t in range(steps):
+        grad = W.small_rows(kind, P, n, 100 * t + 7 * P + d)
+        st.step(_dev(grad))
+        torch.cuda.synchronize()
+        _check(st)
+        res = so.spardl_step_bsag([acc[w] for w in range(P)], [grad[w] for w in range(P)], P, n, L, d, ctrl)
+        compare_bsag_step(st, res)
+        hs.add(tuple(res.h.values()))
+    log(f"  counts over the steps: {sorted(hs)}")
+
+
+def test_bsag_p14_d7_sized():
+    """The paper's best B-SAG case, P = 14 workers in d = 7 teams, on 14M
+    parameters at 1 % (L = d k / P = 70000); the oracle recomputes block 1."""
+    P, d, n = 14, 7, 14_000_000
+    k = n // 100
+    L = d * k // P
+    wl = W.config(2)
+    log(f"bsag P={P} d={d} n={n} L={L}")
+    Q = P // d
+    blocks = [1]
+    bounds = so.block_bounds(n, Q)
+    st = spardl.SparDLSagStep(P, d, n, L, bruck=True)
+    grad_d = torch.empty((P, n), dtype=torch.float32, device="cuda")
+    host = np.empty(n, np.float32)
+    acc = [{b: np.zeros(bounds[b + 1] - bounds[b], np.float32) for b in blocks} for _ in range(P)]
+    ctrl = {}
+    for t in range(1, 4):
+        grad = [dict() for _ in range(P)]
+        for w in range(P):
+            W.fill(host, wl, t, w % wl.P, x0=w * 1000)
+            grad_d[w].copy_(torch.from_numpy(host))
+            for b in blocks:
+                grad[w][b] = host[bounds[b]:bounds[b + 1]].copy()
+        torch.cuda.synchronize()
+        st.step(grad_d)
+        torch.cuda.synchronize()
+        _check(st)
+        log(f"  step {t}: GPU done, oracle on block {blocks}")
+        res = so.spardl_step_bsag(acc, grad, P, n, L, d, ctrl, blocks=blocks)
+        compare_bsag_step(st, res, blocks=blocks)
+        log(f"  step {t}: bit-exact (h = {res.h}, N = {[len(res.union[q][0]) for q in blocks]})")
