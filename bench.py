@@ -89,6 +89,19 @@ def cpu_baseline(wl, max_seconds: float = 25.0, lazy: bool = False):
                       f"({done_elems} gradient elements, {elapsed:.1f} s; numpy, single thread)"}
 
 
+def ws_check(st) -> None:
+    from paper_2304_00737_amd import spardl
+    for ws in [getattr(st, "ws", None), getattr(st, "ws_sag", None)] + list(getattr(st, "ws_team", [])):
+        if ws is not None:
+            assert spardl.ws_error(ws) == 0
+
+
+def rsag_exchange(st, t: int) -> None:
+    from paper_2304_00737_amd import spardl
+    spardl.rsag_merge_topk(st.sp_idx, st.sp_val, st.P, st.d, st.n, st.k_blk, t, st.sag_idx[t], st.sag_val[t],
+                           st.sag_cnt[t], st.ws_sag)
+
+
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -98,6 +111,11 @@ def main() -> int:
     ap.add_argument("--variant", choices=("eager", "lazy"), default="eager",
                     help="eager: re-select after every merge (the hot path); lazy: sparsify a block only "
                          "when it is sent (Sec. III-B, Optimization for SRS)")
+    ap.add_argument("--teams", type=int, default=1,
+                    help="d > 1: d teams of P/d workers joined by R-SAG (Sec. III-D; d a power of 2), "
+                         "L = d k / P entries per team block")
+    ap.add_argument("--bruck", action="store_true",
+                    help="with --teams d: join the teams by B-SAG (any d dividing P; Algorithm 2 sets h)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--calib-copy", action="store_true",
                     help="first run one untimed device-to-device copy of CALIB_BYTES (a reference "
@@ -120,6 +138,11 @@ def main() -> int:
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     lazy = args.variant == "lazy"
+    d = args.teams
+    if d > 1 and (lazy or P % d or (d & (d - 1) and not args.bruck)):
+        print(json.dumps({"error": "--teams needs a d dividing P (a power of two without --bruck), "
+                                   "with the eager variant"}))
+        return 2
     if 4.0 * P * n * (wl.steps + 1) > PER_WORKER_BYTES:
         return run_per_worker(args, wl, dev)
 
@@ -144,7 +167,24 @@ def main() -> int:
         del src, dst
 
     stream = torch.cuda.current_stream()
-    if lazy:
+    if d > 1:
+        L = d * wl.k_blk
+        st = spardl.SparDLSagStep(P, d, n, L, device=dev, bruck=args.bruck)
+        if args.bruck:
+            calls = ["add_and_block_topk", "team_srs", "bsag_exchange", "allgather_densify", "residual_collect"]
+
+            def call_fns(j):
+                g = grads[j % len(grads)]
+                return [lambda: st.add_and_select(g), st.team_srs, st.exchanges, st.densify, st.collect]
+        else:
+            calls = ["add_and_block_topk", "team_srs"] + [f"exchange{t}" for t in range(st.steps)] + \
+                    ["allgather_densify", "residual_collect"]
+
+            def call_fns(j):
+                g = grads[j % len(grads)]
+                return [lambda: st.add_and_select(g), st.team_srs] + \
+                       [(lambda t=t: rsag_exchange(st, t)) for t in range(st.steps)] + [st.densify, st.collect]
+    elif lazy:
         st = spardl.SparDLLazyStep(P, n, kb, device=dev)
         calls = ["residual_add"] + [c for i in range(1, st.l + 1) for c in (f"topk_step{i}", f"receive_step{i}")] + \
                 ["topk_reserved", "allgather_densify", "residual_collect"]
@@ -172,7 +212,7 @@ def main() -> int:
         for f in call_fns(j):
             f()
     torch.cuda.synchronize()
-    assert spardl.ws_error(st.ws) == 0
+    ws_check(st)
 
     # ---- timed region: K whole steps, one event pair around them
     start, end = ev(), ev()
@@ -185,10 +225,10 @@ def main() -> int:
     end.record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - wall0
-    assert spardl.ws_error(st.ws) == 0
+    ws_check(st)
     total_ms = start.elapsed_time(end)
     ms_per_step = total_ms / args.steps
-    dc = [] if lazy else [t.cpu().numpy() for t in st.drop_cnt]   # drops of the last timed step
+    dc = [] if lazy or d > 1 else [t.cpu().numpy() for t in st.drop_cnt]   # drops of the last timed step
 
     # ---- per-call attribution (untimed for `value`): events around every call.
     # An event record costs a fixed marker overhead on the stream; it is
@@ -204,7 +244,7 @@ def main() -> int:
         empty[j][0].record(stream)
         empty[j][1].record(stream)
     torch.cuda.synchronize()
-    assert spardl.ws_error(st.ws) == 0
+    ws_check(st)
     marker_ms = sum(a.elapsed_time(b) for a, b in empty) / args.steps
     per_call_ms = {c: max(sum(evs[j][ci][0].elapsed_time(evs[j][ci][1]) for j in range(args.steps))
                           / args.steps - marker_ms, 0.0) for ci, c in enumerate(calls)}
@@ -215,7 +255,10 @@ def main() -> int:
     k_mid = [(ev(), ev()) for _ in range(args.steps)]
     for j in range(args.steps):
         k_mid[j][0].record(stream)
-        if lazy:
+        if d > 1:
+            st.add_and_select(g0)
+            k_mid[j][1].record(stream)
+        elif lazy:
             st.residual_add_rows(0, g0)
             k_mid[j][1].record(stream)
         else:
@@ -224,7 +267,7 @@ def main() -> int:
             st.block_topk()
     torch.cuda.synchronize()
     add_ms = sum(a.elapsed_time(b) for a, b in k_mid) / args.steps - marker_ms
-    assert spardl.ws_error(st.ws) == 0
+    ws_check(st)
 
     elems = P * n
     value = elems / (ms_per_step * 1e-3)
@@ -235,7 +278,23 @@ def main() -> int:
         "residual_add": 12.0 * P * n,                              # read G, read xi, write A
         "allgather_densify": 4.0 * n + n / 8.0 + 8.0 * P * kb,     # write u and the bitmap of I; read the final blocks
     }
-    if lazy:
+    if d > 1:
+        Q, L = st.Q, st.k_blk
+        alg["add_and_block_topk"] = 16.0 * P * n + 12.0 * P * Q * L
+        alg["team_srs"] = sum(32.0 * P * m * L for m in st.bags)
+        if args.bruck:
+            # read every held block; write top-h and drops; the union reads the kept lists, writes and
+            # reads the scatter row and writes the sums; the final selection reads them and writes sp
+            alg["bsag_exchange"] = 16.0 * P * L + 8.0 * P * L + 16.0 * d * Q * L
+            alg["allgather_densify"] = 4.0 * n + n / 8.0 + 8.0 * Q * L
+            alg["residual_collect"] = 4.0 * P * Q * L + 8.0 * (P * Q * L) + 16.0 * P * L
+        else:
+            for t in range(st.steps):
+                alg[f"exchange{t}"] = 40.0 * (d // 2) * Q * L     # read both blocks; write both kept + the drops
+            alg["allgather_densify"] = 4.0 * n + n / 8.0 + 8.0 * Q * L
+            alg["residual_collect"] = 4.0 * P * Q * L + 8.0 * (P * Q * L) + 24.0 * st.steps * (d // 2) * Q * L
+        del alg["residual_add"]
+    elif lazy:
         blk = n / P
         for i, pc in enumerate(pairs, start=1):
             alg[f"topk_step{i}"] = 4.0 * pc * blk + 8.0 * pc * kb  # read the sent blocks; write idx, val
@@ -253,16 +312,19 @@ def main() -> int:
         # membership lookups hit the bitmap of I that densify wrote (n/8 bytes, cache resident)
         alg["residual_collect"] = 4.0 * P * P * kb + 8.0 * drops_total + 8.0 * (P * P * kb + drops_total)
     dominant = max(calls, key=lambda c: per_call_ms[c])
-    dom_ms = add_ms if dominant == "residual_add" else per_call_ms[dominant]
+    dom_ms = add_ms if dominant in ("residual_add", "add_and_block_topk") else per_call_ms[dominant]
     achieved = alg[dominant] / (dom_ms * 1e-3) / 1e9
     src_hash = _kernel_src_hash()
     # the stored counter readings are of the fused add (eager variant)
-    traffic = None if lazy else _traffic_from_profiles(dominant, src_hash, 1.0)
+    traffic = None if lazy or d > 1 else _traffic_from_profiles(dominant, src_hash, 1.0)
     core_bytes = sum(v for k, v in alg.items() if k != "allgather_densify")
     full_bytes = sum(alg.values())
 
     out = {
-        "metric": ("gradient elements/sec per full SparDL step, lazy sparsification (P=8 virtual); % of HBM peak"
+        "metric": (f"gradient elements/sec per full SparDL step, {'B' if args.bruck else 'R'}-SAG with d={d} teams "
+                   f"(P=8 virtual); % of HBM peak"
+                   if d > 1 else
+                   "gradient elements/sec per full SparDL step, lazy sparsification (P=8 virtual); % of HBM peak"
                    if lazy else "gradient elements/sec per full SparDL step (P=8 virtual); % of HBM peak"),
         "value": value,
         "unit": "elements/s",
@@ -277,7 +339,9 @@ def main() -> int:
         "data": "synthetic",
         "config": {"workload": wl.name, "P": P, "n_per_worker": n, "density": f"{wl.density[0]}/{wl.density[1]}",
                    "k_per_block": kb, "gradient_batches": wl.steps, "residual": "carried across steps",
-                   "segments": len(wl.seg_len), "seed": W.SEED_BASE, "variant": args.variant},
+                   "segments": len(wl.seg_len), "seed": W.SEED_BASE, "variant": args.variant, "teams": d,
+                   "team_join": ("B-SAG" if args.bruck else "R-SAG") if d > 1 else None,
+                   "L_per_team_block": st.k_blk if d > 1 else None},
         "roofline": {"bound": "hbm", "kernel": "k_residual_add" if dominant == "residual_add" else dominant,
                      "achieved": achieved, "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS, "traffic": traffic,
@@ -290,7 +354,7 @@ def main() -> int:
         "wall_s_timed": wall,
         "kernel_src": src_hash,
     }
-    if not args.no_cpu_baseline:
+    if not args.no_cpu_baseline and d == 1:
         out["cpu_baseline"] = cpu_baseline(wl, lazy=lazy)
     print(json.dumps(out), flush=True)
     return 0
@@ -313,6 +377,9 @@ def run_per_worker(args, wl, dev) -> int:
     from paper_2304_00737_amd import workloads as W
 
     P, n, kb = wl.P, wl.n, wl.k_blk
+    if args.teams > 1:
+        print(json.dumps({"error": "the per-worker run (workload 5) has no team variant"}))
+        return 2
     lazy = args.variant == "lazy"
     if lazy:
         st = spardl.SparDLLazyStep(P, n, kb, device=dev, rows_per_call=1)
@@ -350,7 +417,7 @@ def run_per_worker(args, wl, dev) -> int:
         st.finish()
         f[1].record(stream)
         torch.cuda.synchronize()
-        assert spardl.ws_error(st.ws) == 0
+        ws_check(st)
         add = sum(a.elapsed_time(b) for a, b, _ in marks) - P * marker_ms
         topk = 0.0 if lazy else sum(b.elapsed_time(c) for _, b, c in marks) - P * marker_ms
         tail = f[0].elapsed_time(f[1]) - marker_ms
