@@ -185,16 +185,17 @@ bool bsag_sizes_ok(int32_t P, int32_t d, int64_t n, int32_t kb) {
 
 // Workspace of the B-SAG exchange.
 struct BsagLayout {
-  size_t H, S, F, N, cnt, bm, kept_i, kept_v, U_i, U_v, fd_i, fd_v, fd_cnt, scratch, end;
-  uint32_t W;
+  size_t H, S, F, N, cnt, hist, lst, ccnt, tile_cnt, kept_i, kept_v, U_i, U_v, fd_i, fd_v, fd_cnt, end;
+  uint32_t ntile;
 };
 
 BsagLayout make_bsag_layout(int32_t P, int32_t d, int64_t n, int32_t kb) {
   BsagLayout L;
   const int64_t Q = P / d;
   const int64_t maxlen = (n + Q - 1) / Q;
-  L.W = (uint32_t)((maxlen + 31) / 32);
+  L.ntile = (uint32_t)ceil_div(maxlen, (int64_t)UNION_TILE);
   const int64_t cap = (int64_t)d * kb;
+  const int64_t nch = ceil_div(cap, (int64_t)LIST_CHUNK);
   size_t off = 256;   // error word
   auto take = [&](size_t bytes) {
     const size_t at = off;
@@ -206,7 +207,10 @@ BsagLayout make_bsag_layout(int32_t P, int32_t d, int64_t n, int32_t kb) {
   L.F = take((size_t)Q * 4);
   L.N = take((size_t)Q * 4);
   L.cnt = take((size_t)Q * 4);
-  L.bm = take((size_t)Q * L.W * 4);
+  L.hist = take((size_t)P * NB1 * 4);
+  L.lst = take((size_t)P * 4 * 4);
+  L.ccnt = take((size_t)P * nch * 2 * 4);
+  L.tile_cnt = take((size_t)Q * L.ntile * 4);
   L.kept_i = take((size_t)P * kb * 4);
   L.kept_v = take((size_t)P * kb * 4);
   L.U_i = take((size_t)Q * cap * 4);
@@ -214,7 +218,6 @@ BsagLayout make_bsag_layout(int32_t P, int32_t d, int64_t n, int32_t kb) {
   L.fd_i = take((size_t)Q * cap * 4);
   L.fd_v = take((size_t)Q * cap * 4);
   L.fd_cnt = take((size_t)Q * 4);
-  L.scratch = take((size_t)n * 4);
   L.end = off;
   return L;
 }
@@ -542,7 +545,7 @@ int spardl_bsag_workspace_init(int32_t P, int32_t d, int64_t n, int32_t k_blk, v
   const BsagLayout L = make_bsag_layout(P, d, n, k_blk);
   char* base = (char*)ws;
   const int32_t Q = P / d;
-  SPARDL_TRY(launch_fill(Fill().add(base, 64).add(base + L.bm, (int64_t)Q * L.W).r, stream));
+  SPARDL_TRY(launch_fill(Fill().add(base, 64).add(base + L.hist, (int64_t)P * NB1).r, stream));
   // Algorithm 2's initial state: h = k/P = L/d, step = 0.01 (d - 1) L / d, flag false, N = 0
   const double h0 = (double)k_blk / (double)d;
   const double step0 = 0.01 * (d - 1) * k_blk / d;
@@ -577,9 +580,11 @@ int spardl_bsag_exchange(int32_t* sp_idx, float* sp_val, int32_t P, int32_t d, i
   a.drop_i = drop_idx;
   a.drop_v = drop_val;
   a.drop_cnt = drop_cnt;
-  a.scratch = (float*)(base + L.scratch);
-  a.bm = (uint32_t*)(base + L.bm);
-  a.W = L.W;
+  a.hist = (uint32_t*)(base + L.hist);
+  a.lst = (uint32_t*)(base + L.lst);
+  a.ccnt = (uint32_t*)(base + L.ccnt);
+  a.tile_cnt = (uint32_t*)(base + L.tile_cnt);
+  a.ntile = L.ntile;
   a.U_i = (int32_t*)(base + L.U_i);
   a.U_v = (float*)(base + L.U_v);
   a.fd_i = (int32_t*)(base + L.fd_i);

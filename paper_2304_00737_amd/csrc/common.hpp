@@ -11,6 +11,8 @@ namespace spardl {
 // three digits: bits 30..19 (4096 bins), 18..8 (2048 bins), 7..0 (256 bins).
 constexpr int D1_SHIFT = 19;
 constexpr int NB1 = 4096;
+constexpr uint32_t LIST_CHUNK = 4096;    // list entries per workgroup of the B-SAG list selections
+constexpr uint32_t UNION_TILE = 16384;   // indices per workgroup of the B-SAG union
 constexpr int D2_SHIFT = 8;
 constexpr int NB2 = 2048;
 constexpr int NB3 = 256;

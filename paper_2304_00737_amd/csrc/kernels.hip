@@ -1797,193 +1797,305 @@ __global__ __launch_bounds__(64) void k_bsag_init(uint32_t Q, double h0, double 
   }
 }
 
-// Keep the top c of one sparse list sorted by index (the order of every
-// selection: larger |v| bits first, then the lower index), by the exact
-// three-level radix select of the merge threshold, then write the kept
-// entries in index order to K (and sentinels -- index INT32_MAX, value 0 --
-// from c up to `pad`), the rest in index order to D.  One workgroup of 1024
-// threads; the list is read five times (it is small and stays in L2).
-struct SelSmem {
-  uint32_t h[NB1];
-  uint32_t scratch[32];
+// ---- top-c selection of many sparse lists (each sorted by index), spread
+// over workgroups: a chunked level-1 histogram, one workgroup per list for
+// the threshold (levels 2-3 scan the list for the threshold bin's keys),
+// chunked counts, chunked emit in index order.  ListSel says where list i
+// lives, its length, how many entries it keeps and where the kept (and then
+// sentinels -- index INT32_MAX, value 0 -- up to `pad`) and dropped entries go.
+
+struct ListDesc {
+  const int32_t* ii;
+  const float* iv;
+  uint32_t len, c, pad;
+  int32_t* ki;
+  float* kv;
+  int32_t* di;
+  float* dv;
+  int32_t* dcnt;
 };
 
-__device__ void select_list(const int32_t* __restrict__ Ii, const float* __restrict__ Iv, uint32_t len,
-                            uint32_t c, int32_t* __restrict__ Ki, float* __restrict__ Kv, uint32_t pad,
-                            int32_t* __restrict__ Di, float* __restrict__ Dv, int32_t* dcnt, uint32_t* err,
-                            SelSmem& S) {
+struct ListSel {
+  uint32_t mode;       // 0: top-h of the held blocks, list = worker; 1: final top-L, list = block
+  uint32_t Q, kb, cap;  // cap = d k_blk
+  int32_t* sp_idx;
+  float* sp_val;
+  const uint32_t* cnt;  // top-h count per block
+  const uint32_t* N;    // union size per block
+  int32_t *kept_i, *drop_i, *U_i, *fd_i;
+  float *kept_v, *drop_v, *U_v, *fd_v;
+  int32_t *drop_cnt, *fd_cnt;
+  __device__ __forceinline__ ListDesc desc(uint32_t i) const {
+    ListDesc D;
+    if (mode == 0u) {
+      const uint32_t q = i % Q;
+      const int64_t in = ((int64_t)i * Q + q) * kb, o = (int64_t)i * kb;
+      D.ii = sp_idx + in;
+      D.iv = sp_val + in;
+      D.len = kb;
+      D.c = min(cnt[q], kb);
+      D.pad = 0u;
+      D.ki = kept_i + o;
+      D.kv = kept_v + o;
+      D.di = drop_i + o;
+      D.dv = drop_v + o;
+      D.dcnt = drop_cnt + i;
+    } else {
+      const int64_t in = (int64_t)i * cap, o = ((int64_t)i * Q + i) * kb;
+      D.ii = U_i + in;
+      D.iv = U_v + in;
+      D.len = min(N[i], cap);
+      D.c = kb;
+      D.pad = kb;
+      D.ki = sp_idx + o;
+      D.kv = sp_val + o;
+      D.di = fd_i + in;
+      D.dv = fd_v + in;
+      D.dcnt = fd_cnt + i;
+    }
+    return D;
+  }
+};
+
+__global__ __launch_bounds__(256) void k_lsel_hist(ListSel S, uint32_t nch, uint32_t* __restrict__ hist) {
+  __shared__ __align__(16) uint32_t h[NB1];
+  const uint32_t i = blockIdx.x / nch, k = blockIdx.x % nch;
+  const ListDesc D = S.desc(i);
+  const uint32_t j0 = k * LIST_CHUNK;
+  if (D.c >= D.len || j0 >= D.len) return;   // uniform: nothing to select, or no entries here
+  const uint32_t j1 = min(D.len, j0 + LIST_CHUNK);
+  for (int b = threadIdx.x; b < NB1; b += 256) h[b] = 0u;
+  __syncthreads();
+  for (uint32_t j = j0 + threadIdx.x; j < j1; j += 256u) atomicAdd(&h[mag_key(D.iv[j]) >> D1_SHIFT], 1u);
+  __syncthreads();
+  flush_hist(h, hist + (int64_t)i * NB1);
+}
+
+// st[4 i ..]: key bound tge, tie key teq, ties to keep need_eq, entries kept
+__global__ __launch_bounds__(1024) void k_lsel_level(ListSel S, uint32_t* __restrict__ hist,
+                                                     uint32_t* __restrict__ st, uint32_t* __restrict__ err) {
+  __shared__ uint32_t h[NB1];
+  __shared__ uint32_t scratch[32];
   constexpr uint32_t NT = 1024;
-  if (c >= len) {
-    for (uint32_t j = threadIdx.x; j < len; j += NT) {
-      Ki[j] = Ii[j];
-      Kv[j] = Iv[j];
+  const uint32_t i = blockIdx.x;
+  const ListDesc D = S.desc(i);
+  uint32_t tge = 0u, teq = 0u, need_eq = 0u;   // keep everything unless a selection is needed
+  if (D.c < D.len) {
+    uint32_t* __restrict__ H = hist + (int64_t)i * NB1;
+    for (uint32_t b = threadIdx.x; b < NB1; b += NT) {
+      h[b] = H[b];
+      H[b] = 0u;   // histograms rest at zero
     }
-    for (uint32_t j = len + threadIdx.x; j < pad; j += NT) {
-      Ki[j] = INT32_MAX;
-      Kv[j] = 0.f;
+    __syncthreads();
+    uint32_t T1, above1, cnt1, ok;
+    block_select_desc(h, NB1, D.c, scratch, &T1, &above1, &cnt1, &ok);
+    if (!ok) {
+      if (threadIdx.x == 0) atomicOr(err, ERR_COUNT);
+    } else {
+      resolve_low_digits(T1, D.c - above1, cnt1, h, scratch, err,
+                         [&](auto f) {
+                           for (uint32_t j = threadIdx.x; j < D.len; j += NT) {
+                             const uint32_t key = mag_key(D.iv[j]);
+                             if ((key >> D1_SHIFT) == T1) f(key);
+                           }
+                         },
+                         tge, teq, need_eq);
     }
-    if (threadIdx.x == 0 && dcnt) *dcnt = 0;
-    return;
   }
-  for (uint32_t i = threadIdx.x; i < NB1; i += NT) S.h[i] = 0u;
-  __syncthreads();
-  for (uint32_t j = threadIdx.x; j < len; j += NT) atomicAdd(&S.h[mag_key(Iv[j]) >> D1_SHIFT], 1u);
-  __syncthreads();
-  uint32_t T1, above1, cnt1, ok;
-  block_select_desc(S.h, NB1, c, S.scratch, &T1, &above1, &cnt1, &ok);
-  if (!ok) {
-    if (threadIdx.x == 0) atomicOr(err, ERR_COUNT);
-    return;
+  if (threadIdx.x == 0) {
+    st[4 * i + 0] = tge;
+    st[4 * i + 1] = teq;
+    st[4 * i + 2] = need_eq;
+    st[4 * i + 3] = min(D.c, D.len);
   }
-  uint32_t tge, teq, need_eq;
-  resolve_low_digits(T1, c - above1, cnt1, S.h, S.scratch, err,
-                     [&](auto f) {
-                       for (uint32_t j = threadIdx.x; j < len; j += NT) {
-                         const uint32_t key = mag_key(Iv[j]);
-                         if ((key >> D1_SHIFT) == T1) f(key);
-                       }
-                     },
-                     tge, teq, need_eq);
-  // thread t owns the consecutive entries [t per, (t + 1) per): counts, scan, emit
-  const uint32_t per = (len + NT - 1) / NT;
-  const uint32_t j0 = min(len, threadIdx.x * per), j1 = min(len, j0 + per);
+}
+
+__device__ __forceinline__ uint32_t block_sum256(uint32_t v, uint32_t* sc) {
+  uint32_t tot;
+  block_excl_scan(v, sc, &tot);
+  return tot;
+}
+
+// per chunk: entries with key >= tge, and with key == teq (when ties are to be split)
+__global__ __launch_bounds__(256) void k_lsel_count(ListSel S, uint32_t nch, const uint32_t* __restrict__ st,
+                                                    uint32_t* __restrict__ ccnt) {
+  __shared__ uint32_t sc[8];
+  const uint32_t i = blockIdx.x / nch, k = blockIdx.x % nch;
+  const ListDesc D = S.desc(i);
+  const uint32_t tge = st[4 * i], teq = st[4 * i + 1], need_eq = st[4 * i + 2];
+  const uint32_t j0 = k * LIST_CHUNK, j1 = min(D.len, j0 + LIST_CHUNK);
   uint32_t ng = 0, ne = 0;
-  __syncthreads();   // the scans below reuse scratch
-  for (uint32_t j = j0; j < j1; ++j) {
-    const uint32_t key = mag_key(Iv[j]);
+  for (uint32_t j = j0 + threadIdx.x; j < j1; j += 256u) {
+    const uint32_t key = mag_key(D.iv[j]);
     ng += key >= tge;
     ne += need_eq != 0u && key == teq;
   }
-  uint32_t tot_g, tot_e;
-  uint32_t rg = block_excl_scan(ng, S.scratch, &tot_g);
-  uint32_t re = block_excl_scan(ne, S.scratch, &tot_e);
-  if (threadIdx.x == 0 && tot_g + min(tot_e, need_eq) != c) atomicOr(err, ERR_COUNT_SUM);
-  for (uint32_t j = j0; j < j1; ++j) {
-    const int32_t x = Ii[j];
-    const float v = Iv[j];
+  ng = block_sum256(ng, sc);
+  ne = block_sum256(ne, sc);
+  if (threadIdx.x == 0) {
+    ccnt[2 * ((int64_t)i * nch + k)] = ng;
+    ccnt[2 * ((int64_t)i * nch + k) + 1] = ne;
+  }
+}
+
+// per chunk: kept entries to K in index order, the rest to D; chunk 0 also
+// writes the sentinels and the drop count
+__global__ __launch_bounds__(256) void k_lsel_emit(ListSel S, uint32_t nch, const uint32_t* __restrict__ st,
+                                                   const uint32_t* __restrict__ ccnt, uint32_t* __restrict__ err) {
+  constexpr uint32_t PT = LIST_CHUNK / 256;   // consecutive entries per thread
+  __shared__ uint32_t sc[8];
+  const uint32_t i = blockIdx.x / nch, k = blockIdx.x % nch;
+  const ListDesc D = S.desc(i);
+  const uint32_t tge = st[4 * i], teq = st[4 * i + 1], need_eq = st[4 * i + 2], keep = st[4 * i + 3];
+  if (k == 0) {
+    for (uint32_t j = keep + threadIdx.x; j < D.pad; j += 256u) {
+      D.ki[j] = INT32_MAX;
+      D.kv[j] = 0.f;
+    }
+    if (threadIdx.x == 0) *D.dcnt = (int32_t)(D.len - keep);
+  }
+  const uint32_t j0 = k * LIST_CHUNK;
+  if (j0 >= D.len) return;   // uniform
+  // selected and tied entries of the chunks before this one
+  uint32_t pg = 0, pe = 0;
+  for (uint32_t k2 = threadIdx.x; k2 < k; k2 += 256u) {
+    pg += ccnt[2 * ((int64_t)i * nch + k2)];
+    pe += ccnt[2 * ((int64_t)i * nch + k2) + 1];
+  }
+  pg = block_sum256(pg, sc);
+  pe = block_sum256(pe, sc);
+  const uint32_t a = min(D.len, j0 + threadIdx.x * PT), b = min(D.len, a + PT);
+  uint32_t ng = 0, ne = 0;
+  for (uint32_t j = a; j < b; ++j) {
+    const uint32_t key = mag_key(D.iv[j]);
+    ng += key >= tge;
+    ne += need_eq != 0u && key == teq;
+  }
+  uint32_t tg, te;
+  uint32_t rg = pg + block_excl_scan(ng, sc, &tg);
+  uint32_t re = pe + block_excl_scan(ne, sc, &te);
+  const uint32_t ndrop = D.len - keep;
+  for (uint32_t j = a; j < b; ++j) {
+    const int32_t x = D.ii[j];
+    const float v = D.iv[j];
     const uint32_t key = mag_key(v);
     const bool is_g = key >= tge, is_e = need_eq != 0u && key == teq;
     const uint32_t before = rg + min(re, need_eq);
     if (is_g || (is_e && re < need_eq)) {
-      if (before < c) {
-        Ki[before] = x;
-        Kv[before] = v;
+      if (before < keep) {
+        D.ki[before] = x;
+        D.kv[before] = v;
+      } else {
+        atomicOr(err, ERR_COUNT_POS);
       }
-    } else if (j - before < len - c) {
-      Di[j - before] = x;
-      Dv[j - before] = v;
+    } else if (j - before < ndrop) {
+      D.di[j - before] = x;
+      D.dv[j - before] = v;
+    } else {
+      atomicOr(err, ERR_COUNT_DROP);
     }
     rg += is_g;
     re += is_e;
   }
-  for (uint32_t j = c + threadIdx.x; j < pad; j += NT) {
-    Ki[j] = INT32_MAX;
-    Kv[j] = 0.f;
-  }
-  if (threadIdx.x == 0 && dcnt) *dcnt = (int32_t)(len - c);
 }
 
-// Top-h of the block every worker holds after its team's SRS: worker w =
-// tau Q + q holds sp[w][q]; keeps cnt[q] entries in kept[w], drops the rest
-// to drop[w] (k_blk entries per worker).  One workgroup per worker.
-__global__ __launch_bounds__(1024) void k_bsag_toph(const int32_t* __restrict__ sp_idx,
-                                                    const float* __restrict__ sp_val, uint32_t Q, uint32_t kb,
-                                                    const uint32_t* __restrict__ cnt, int32_t* __restrict__ kept_i,
-                                                    float* __restrict__ kept_v, int32_t* __restrict__ drop_i,
-                                                    float* __restrict__ drop_v, int32_t* __restrict__ drop_cnt,
-                                                    uint32_t* __restrict__ err) {
-  __shared__ SelSmem S;
-  const uint32_t w = blockIdx.x, q = w % Q;
-  const int64_t in = ((int64_t)w * Q + q) * kb, o = (int64_t)w * kb;
-  const uint32_t c = min(cnt[q], kb);
-  select_list(sp_idx + in, sp_val + in, kb, c, kept_i + o, kept_v + o, 0u, drop_i + o, drop_v + o, drop_cnt + w,
-              err, S);
-}
+// ---- the Bruck All-Gather's result summed in team order, for block q, in
+// tiles of UT indices: each workgroup takes the d kept lists' entries that
+// fall in its tile (binary searches in the index-sorted lists), adds them in
+// team order in LDS (first occurrence stores, later ones add; an LDS
+// occupancy bitmap tells which), and either counts the tile's distinct
+// indices (pass 1) or writes them in index order after the counts of the
+// tiles before it (pass 2).  Tile 0 of each block also records N_q.
+constexpr uint32_t UT = UNION_TILE;
 
-// The Bruck All-Gather's result summed in team order, for block q: the d
-// kept lists of the holders of q are scattered one team after the other into
-// a dense row (first occurrence stores, later ones add) with a bitmap of the
-// occupied indices, which the compaction then walks in index order (and
-// clears).  One workgroup per block; bm gives block q the words
-// [q W, (q + 1) W), W = ceil(max block length / 32).
+template <bool WRITE>
 __global__ __launch_bounds__(1024) void k_bsag_union(const int32_t* __restrict__ kept_i,
                                                      const float* __restrict__ kept_v, Blocks B, uint32_t d,
-                                                     uint32_t kb, const uint32_t* __restrict__ cnt,
-                                                     float* __restrict__ scratch, uint32_t* __restrict__ bm,
-                                                     uint32_t W, int32_t* __restrict__ U_i, float* __restrict__ U_v,
-                                                     uint32_t* __restrict__ N, int32_t* __restrict__ info,
-                                                     uint32_t* __restrict__ err) {
+                                                     uint32_t kb, const uint32_t* __restrict__ cnt, uint32_t ntile,
+                                                     uint32_t* __restrict__ tile_cnt, int32_t* __restrict__ U_i,
+                                                     float* __restrict__ U_v, uint32_t* __restrict__ N,
+                                                     int32_t* __restrict__ info, uint32_t* __restrict__ err) {
   constexpr uint32_t NT = 1024;
-  __shared__ uint32_t sc[32];
-  const uint32_t q = blockIdx.x, Q = B.P;
+  __shared__ float vals[WRITE ? UT : 1];
+  __shared__ uint32_t bits[UT / 32];
+  __shared__ uint32_t sc[24];
+  __shared__ uint32_t range[2];
+  const uint32_t q = blockIdx.x / ntile, tile = blockIdx.x % ntile, Q = B.P;
   const uint32_t s = B.start(q), e = B.start(q + 1u);
+  const uint32_t lo = s + tile * UT;
+  if (lo >= e) {   // uniform: a shorter block has fewer tiles
+    if (!WRITE && threadIdx.x == 0) tile_cnt[(int64_t)q * ntile + tile] = 0u;
+    return;
+  }
+  const uint32_t hi = min(e, lo + UT);
   const uint32_t c = min(cnt[q], kb);
-  uint32_t* __restrict__ M = bm + (int64_t)q * W;
+  for (uint32_t w = threadIdx.x; w < UT / 32; w += NT) bits[w] = 0u;
   for (uint32_t tau = 0; tau < d; ++tau) {
     const int64_t o = ((int64_t)tau * Q + q) * kb;
-    for (uint32_t j = threadIdx.x; j < c; j += NT) {
-      const int32_t x = kept_i[o + j];
-      if (x < (int32_t)s || x >= (int32_t)e) continue;
-      const uint32_t r = (uint32_t)x - s, bit = 1u << (r & 31u);
-      const float v = kept_v[o + j];
-      // the atomic's old word says whether an earlier team brought this index
-      if (atomicOr(&M[r >> 5], bit) & bit) scratch[x] = scratch[x] + v;
-      else scratch[x] = v;
-    }
-    __syncthreads();   // a later team's entry for the same index must see this one
-  }
-  const uint32_t words = (e - s + 31u) >> 5;
-  const uint32_t per = (words + NT - 1) / NT;
-  const uint32_t w0 = min(words, threadIdx.x * per), w1 = min(words, w0 + per);
-  // the words were written by atomics (performed in L2): read them past L1
-  auto word = [&](uint32_t i) { return __hip_atomic_load(&M[i], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT); };
-  uint32_t mine = 0;
-  for (uint32_t i = w0; i < w1; ++i) mine += __popc(word(i));
-  uint32_t tot;
-  uint32_t pos = block_excl_scan(mine, sc, &tot);
-  const uint32_t cap = d * kb;
-  int32_t* __restrict__ Ui = U_i + (int64_t)q * cap;
-  float* __restrict__ Uv = U_v + (int64_t)q * cap;
-  for (uint32_t i = w0; i < w1; ++i) {
-    uint32_t m = word(i);
-    if (m == 0u) continue;
-    M[i] = 0u;
-    while (m) {
-      const uint32_t b = __ffs(m) - 1u;
-      m &= m - 1u;
-      const int32_t x = (int32_t)(s + 32u * i + b);
-      if (pos < cap) {
-        Ui[pos] = x;
-        Uv[pos] = scratch[x];
+    if (threadIdx.x < 2) {   // first entry at or above lo (thread 0) and hi (thread 1)
+      const int32_t bound = (int32_t)(threadIdx.x == 0 ? lo : hi);
+      uint32_t l2 = 0, h2 = c;
+      while (l2 < h2) {
+        const uint32_t m = (l2 + h2) >> 1;
+        if (kept_i[o + m] < bound) l2 = m + 1;
+        else h2 = m;
       }
-      ++pos;
+      range[threadIdx.x] = l2;
     }
+    __syncthreads();   // also orders this team's additions after the previous team's
+    const uint32_t a = range[0], b = range[1];
+    for (uint32_t j = a + threadIdx.x; j < b; j += NT) {
+      const uint32_t r = (uint32_t)kept_i[o + j] - lo, bit = 1u << (r & 31u);
+      const uint32_t old = atomicOr(&bits[r >> 5], bit);
+      if (WRITE) {
+        const float v = kept_v[o + j];
+        vals[r] = (old & bit) ? vals[r] + v : v;
+      }
+    }
+    __syncthreads();
   }
-  if (threadIdx.x == 0) {
-    if (tot > cap) atomicOr(err, ERR_COUNT);
-    N[q] = tot;
+  const uint32_t words = (hi - lo + 31u) >> 5;
+  const uint32_t m0 = threadIdx.x < words ? bits[threadIdx.x] : 0u;   // words <= UT / 32 = 512 < NT
+  uint32_t tot;
+  uint32_t pos = block_excl_scan(__popc(m0), sc, &tot);
+  if (!WRITE) {
+    if (threadIdx.x == 0) tile_cnt[(int64_t)q * ntile + tile] = tot;
+    return;
+  }
+  // distinct indices of the tiles before this one (and of all tiles, for tile 0)
+  const uint32_t* __restrict__ tc = tile_cnt + (int64_t)q * ntile;
+  uint32_t before = 0, all = 0;
+  for (uint32_t t2 = threadIdx.x; t2 < ntile; t2 += NT) {
+    const uint32_t v = tc[t2];
+    before += t2 < tile ? v : 0u;
+    all += v;
+  }
+  uint32_t tmp;
+  block_excl_scan(before, sc, &tmp);
+  before = tmp;
+  block_excl_scan(all, sc, &tmp);
+  all = tmp;
+  const uint32_t cap = d * kb;
+  pos += before;
+  uint32_t m = m0;
+  while (m) {
+    const uint32_t bt = __ffs(m) - 1u;
+    m &= m - 1u;
+    const uint32_t r = 32u * threadIdx.x + bt;
+    if (pos < cap) {
+      U_i[(int64_t)q * cap + pos] = (int32_t)(lo + r);
+      U_v[(int64_t)q * cap + pos] = vals[r];
+    }
+    ++pos;
+  }
+  if (tile == 0 && threadIdx.x == 0) {
+    if (all > cap) atomicOr(err, ERR_COUNT);
+    N[q] = all;
     if (info) {
       info[q] = (int32_t)c;
-      info[Q + q] = (int32_t)tot;
+      info[Q + q] = (int32_t)all;
     }
   }
-}
-
-// Final top-L of each block's union (all of it when it has at most L
-// entries), into sp[q][q] padded to k_blk with sentinels; the dropped entries
-// to fdrop[q].  One workgroup per block.
-__global__ __launch_bounds__(1024) void k_bsag_final(const int32_t* __restrict__ U_i, const float* __restrict__ U_v,
-                                                     const uint32_t* __restrict__ N, uint32_t Q, uint32_t d,
-                                                     uint32_t kb, int32_t* __restrict__ sp_idx,
-                                                     float* __restrict__ sp_val, int32_t* __restrict__ fd_i,
-                                                     float* __restrict__ fd_v, int32_t* __restrict__ fd_cnt,
-                                                     uint32_t* __restrict__ err) {
-  __shared__ SelSmem S;
-  const uint32_t q = blockIdx.x;
-  const uint32_t cap = d * kb;
-  const uint32_t len = min(N[q], cap);
-  const int64_t in = (int64_t)q * cap, o = ((int64_t)q * Q + q) * kb;
-  select_list(U_i + in, U_v + in, len, kb, sp_idx + o, sp_val + o, kb, fd_i + in, fd_v + in, fd_cnt + q, err, S);
 }
 
 // ============================================================================ lazy summation
@@ -2165,15 +2277,47 @@ hipError_t launch_bsag_init(int32_t Q, double h0, double step0, double* H, doubl
 }
 
 hipError_t launch_bsag_exchange(const BsagArgs& a, hipStream_t s) {
-  const uint32_t Q = (uint32_t)a.Q, d = (uint32_t)a.d, kb = (uint32_t)a.kb;
+  const uint32_t Q = (uint32_t)a.Q, d = (uint32_t)a.d, kb = (uint32_t)a.kb, P = Q * d, cap = d * kb;
   hipLaunchKernelGGL(k_bsag_control, dim3(grid_for(Q, 64, 1024)), dim3(64), 0, s, Q, kb, d, a.H, a.S, a.F, a.N,
                      a.cnt);
-  hipLaunchKernelGGL(k_bsag_toph, dim3(Q * d), dim3(1024), 0, s, a.sp_idx, a.sp_val, Q, kb, a.cnt, a.kept_i,
-                     a.kept_v, a.drop_i, a.drop_v, a.drop_cnt, a.err);
-  hipLaunchKernelGGL(k_bsag_union, dim3(Q), dim3(1024), 0, s, a.kept_i, a.kept_v, make_blocks(a.n, a.Q), d, kb,
-                     a.cnt, a.scratch, a.bm, a.W, a.U_i, a.U_v, a.N, a.info, a.err);
-  hipLaunchKernelGGL(k_bsag_final, dim3(Q), dim3(1024), 0, s, a.U_i, a.U_v, a.N, Q, d, kb, a.sp_idx, a.sp_val,
-                     a.fd_i, a.fd_v, a.fd_cnt, a.err);
+  ListSel L{};
+  L.Q = Q;
+  L.kb = kb;
+  L.cap = cap;
+  L.sp_idx = a.sp_idx;
+  L.sp_val = a.sp_val;
+  L.cnt = a.cnt;
+  L.N = a.N;
+  L.kept_i = a.kept_i;
+  L.kept_v = a.kept_v;
+  L.drop_i = a.drop_i;
+  L.drop_v = a.drop_v;
+  L.drop_cnt = a.drop_cnt;
+  L.U_i = a.U_i;
+  L.U_v = a.U_v;
+  L.fd_i = a.fd_i;
+  L.fd_v = a.fd_v;
+  L.fd_cnt = a.fd_cnt;
+  // top-h of every held block: P lists of k_blk entries
+  L.mode = 0u;
+  const uint32_t nch0 = (kb + LIST_CHUNK - 1) / LIST_CHUNK;
+  hipLaunchKernelGGL(k_lsel_hist, dim3(P * nch0), dim3(256), 0, s, L, nch0, a.hist);
+  hipLaunchKernelGGL(k_lsel_level, dim3(P), dim3(1024), 0, s, L, a.hist, a.lst, a.err);
+  hipLaunchKernelGGL(k_lsel_count, dim3(P * nch0), dim3(256), 0, s, L, nch0, a.lst, a.ccnt);
+  hipLaunchKernelGGL(k_lsel_emit, dim3(P * nch0), dim3(256), 0, s, L, nch0, a.lst, a.ccnt, a.err);
+  // team-order sums, counted then written tile by tile
+  const Blocks B = make_blocks(a.n, a.Q);
+  hipLaunchKernelGGL(k_bsag_union<false>, dim3(Q * a.ntile), dim3(1024), 0, s, a.kept_i, a.kept_v, B, d, kb, a.cnt,
+                     a.ntile, a.tile_cnt, a.U_i, a.U_v, a.N, a.info, a.err);
+  hipLaunchKernelGGL(k_bsag_union<true>, dim3(Q * a.ntile), dim3(1024), 0, s, a.kept_i, a.kept_v, B, d, kb, a.cnt,
+                     a.ntile, a.tile_cnt, a.U_i, a.U_v, a.N, a.info, a.err);
+  // final top-L of every block: Q lists of up to d k_blk entries
+  L.mode = 1u;
+  const uint32_t nch1 = (cap + LIST_CHUNK - 1) / LIST_CHUNK;
+  hipLaunchKernelGGL(k_lsel_hist, dim3(Q * nch1), dim3(256), 0, s, L, nch1, a.hist);
+  hipLaunchKernelGGL(k_lsel_level, dim3(Q), dim3(1024), 0, s, L, a.hist, a.lst, a.err);
+  hipLaunchKernelGGL(k_lsel_count, dim3(Q * nch1), dim3(256), 0, s, L, nch1, a.lst, a.ccnt);
+  hipLaunchKernelGGL(k_lsel_emit, dim3(Q * nch1), dim3(256), 0, s, L, nch1, a.lst, a.ccnt, a.err);
   return hipGetLastError();
 }
 

@@ -73,9 +73,11 @@ struct BsagArgs {
   int32_t* drop_i;          // the rest (caller's arrays, P x kb, counts P)
   float* drop_v;
   int32_t* drop_cnt;
-  float* scratch;           // n floats
-  uint32_t* bm;             // Q x W words, at zero between calls
-  uint32_t W;
+  uint32_t* hist;           // level-1 histograms of the list selections (P x 4096, at zero between calls)
+  uint32_t* lst;            // per list: threshold words (P x 4)
+  uint32_t* ccnt;           // per list chunk: selected and tied counts
+  uint32_t* tile_cnt;       // per block tile of the union: distinct indices
+  uint32_t ntile;           // union tiles per block
   int32_t* U_i;             // team-order sums (Q x d kb)
   float* U_v;
   int32_t* fd_i;            // final drops (Q x d kb, counts Q)
