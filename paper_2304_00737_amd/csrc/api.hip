@@ -258,7 +258,9 @@ int topk_units(const float* acc, int64_t ld_acc, int64_t units, const Units& U, 
                             v4, w.err, stream));
   SPARDL_TRY(launch_collect(acc, ld_acc, units, U, n, P, v4, smax, w.state, w.spec_cnt, (int32_t)L.add_tiles,
                             w.slot_cnt, w.slot_nbin, w.cand_idx, w.cand_val, w.bin_key, stream));
-  SPARDL_TRY(launch_thresh(0, units, U, n, P, k_blk, smax, 1, nullptr, w.cand_val, w.state, w.slot_cnt,
+  // hist1: the staged threshold for long units builds its level-2/3 histograms in the units'
+  // level-1 histogram space, which the select has cleared
+  SPARDL_TRY(launch_thresh(0, units, U, n, P, k_blk, smax, 1, w.hist1, w.cand_val, w.state, w.slot_cnt,
                            w.slot_nbin, w.bin_key, w.pre_all, w.pre_ge, w.pre_eq, nullptr, w.err, stream));
   SPARDL_TRY(launch_emit(0, w.cand_idx, w.cand_val, units, U, n, P, k_blk, Pairs{}, smax, w.state, w.slot_cnt,
                          w.pre_all, w.pre_ge, w.pre_eq, sp_idx, sp_val, local_idx, nullptr, nullptr, w.err, stream));

@@ -43,6 +43,10 @@ enum : int {
   ST_TEQ = 5,       // ... and the first ST_NEEDEQ (by index) with key == ST_TEQ
   ST_NEEDEQ = 6,
   ST_SPECOK = 7,    // block top-k: the fused add's speculative candidates cover the threshold bin
+  ST_HTOT = 8,      // large-unit threshold: entries in the merge union's histogram
+  ST_PRE23 = 9,     // ... top 23 key bits fixed by level 2
+  ST_NEED2 = 10,    // ... entries still needed from that level-2 bin
+  ST_STAGE = 11,    // ... 2 while level 3 is still needed, else 0
   ST_WORDS = 16
 };
 

@@ -1323,6 +1323,275 @@ __global__ __launch_bounds__(1024) void k_thresh(Blocks B, Units U, int32_t kb, 
   }
 }
 
+// ============================================================================ exact threshold, large units
+// When units are few and long (a worker's blocks of a very long gradient, a
+// team's blocks, unions larger than the register-resident merge path holds),
+// one workgroup per unit leaves most of the GPU idle.  These kernels resolve
+// the same threshold in stages spread over slot groups:
+//   merge only: level-1 select on the union histogram (one workgroup per unit);
+//   level-2 histogram of the threshold bin's keys (slot groups; LDS, then
+//   atomics into the unit's level-1 histogram space, already cleared);
+//   level-2 select (one workgroup per unit); level-3 histogram; level-3 select;
+//   per-slot counts of selected-by-key and tied keys (slot groups);
+//   per-unit exclusive scans into pre_all / pre_ge / pre_eq.
+// They write exactly what k_thresh writes.
+constexpr int BIG_GROUP0 = 64;   // block top-k: slots per workgroup (a wave per slot in turn)
+
+// f(key, slot) for every threshold-bin entry of slots [s0, s1): block top-k:
+// the keys the collect stored, a wave per slot; merge: the union entries whose
+// key is in bin T1, the whole workgroup per slot.
+template <int mode, typename F>
+__device__ __forceinline__ void visit_bin_slots(const SlotGeom& g, int32_t s0, int32_t s1,
+                                                const uint32_t* __restrict__ K, const float* __restrict__ V,
+                                                const uint32_t* __restrict__ cnt, const uint32_t* __restrict__ nbn,
+                                                uint32_t T1, F f) {
+  if constexpr (mode == 0) {
+    const int nw = blockDim.x / WAVE;
+    for (int32_t slot = s0 + wave_id(); slot < s1; slot += nw) {
+      const int64_t room = g.len - (int64_t)slot * g.ss;   // entries of the region in this slot
+      const uint32_t nb = (uint32_t)min(min((int64_t)nbn[slot], (int64_t)g.ss), room);
+      const uint32_t* __restrict__ Ks = K + (int64_t)slot * g.ss;
+      for (uint32_t j = lane_id(); j < nb; j += WAVE) f(Ks[j], slot);
+    }
+  } else {
+    for (int32_t slot = s0; slot < s1; ++slot) {
+      const uint32_t c = min(cnt[slot], (uint32_t)g.ss);
+      const float* __restrict__ Vs = V + (int64_t)slot * g.ss;
+      for (uint32_t j = threadIdx.x; j < c; j += blockDim.x) {
+        const uint32_t key = mag_key(Vs[j]);
+        if ((key >> D1_SHIFT) == T1) f(key, slot);
+      }
+    }
+  }
+}
+
+struct BigArgs {
+  Blocks B;
+  Units U;
+  int32_t kb, smax, group;   // group: slots per workgroup of the slot-group kernels
+  int64_t hstride;           // words of level-1 histogram space per unit
+  uint32_t* hist1;
+  const float* U_val;
+  uint32_t* state;
+  const uint32_t *slot_cnt, *slot_nbin, *bin_key;
+  uint32_t *pre_all, *pre_ge, *pre_eq;
+  int32_t* drop_cnt;
+  uint32_t* err;
+};
+
+__global__ __launch_bounds__(1024) void k_big_level1(BigArgs a) {
+  __shared__ uint32_t h[NB1];
+  __shared__ uint32_t scratch[32];
+  constexpr int NT = 1024;
+  const int64_t unit = blockIdx.x;
+  uint32_t* H = a.hist1 + unit * a.hstride;
+  for (int i = threadIdx.x; i < NB1; i += NT) {
+    h[i] = H[i];
+    H[i] = 0u;   // histograms rest at zero
+  }
+  __syncthreads();
+  uint32_t T1, above1, cnt1, ok, total;
+  block_select_desc(h, NB1, (uint32_t)a.kb, scratch, &T1, &above1, &cnt1, &ok, &total);
+  if (threadIdx.x == 0) {
+    uint32_t* st = a.state + unit * ST_WORDS;
+    if (!ok) atomicOr(a.err, ERR_COUNT);
+    st[ST_T1] = T1;
+    st[ST_NEED1] = ok ? (uint32_t)a.kb - above1 : 0u;
+    st[ST_CNT1] = cnt1;
+    st[ST_HTOT] = total;
+  }
+}
+
+// LEVEL 2: histogram of key bits 8..18 of the bin-T1 keys; LEVEL 3: of bits
+// 0..7 of the keys whose top 23 bits are ST_PRE23
+template <int mode, int LEVEL>
+__global__ __launch_bounds__(256) void k_big_hist(BigArgs a, uint32_t ngroups) {
+  constexpr int NB = LEVEL == 2 ? NB2 : NB3;
+  __shared__ uint32_t h[NB];
+  const int64_t unit = blockIdx.x / ngroups;
+  const int32_t grp = (int32_t)(blockIdx.x % ngroups);
+  const uint32_t* st = a.state + unit * ST_WORDS;
+  const uint32_t T1 = st[ST_T1];
+  if (LEVEL == 2 ? st[ST_NEED1] == st[ST_CNT1] : st[ST_STAGE] != 2u) return;   // uniform: resolved already
+  const uint32_t pre23 = st[ST_PRE23];
+  const SlotGeom g = slot_geom(mode, (uint32_t)unit, a.B, a.U, a.kb);
+  const int32_t s0 = grp * a.group, s1 = min(g.nslots, s0 + a.group);
+  if (s0 >= s1) return;
+  for (int i = threadIdx.x; i < NB; i += blockDim.x) h[i] = 0u;
+  __syncthreads();
+  visit_bin_slots<mode>(g, s0, s1, a.bin_key + g.base, a.U_val + g.base, a.slot_cnt + unit * a.smax,
+                        a.slot_nbin + unit * a.smax, T1, [&](uint32_t key, int32_t) {
+                          if (LEVEL == 2) atomicAdd(&h[(key >> D2_SHIFT) & (NB2 - 1)], 1u);
+                          else if ((key >> D2_SHIFT) == pre23) atomicAdd(&h[key & (NB3 - 1)], 1u);
+                        });
+  __syncthreads();
+  uint32_t* H = a.hist1 + unit * a.hstride + (LEVEL == 2 ? 0 : NB2);
+  for (int i = threadIdx.x; i < NB; i += blockDim.x) {
+    const uint32_t c = h[i];
+    if (c) atomicAdd(&H[i], c);
+  }
+}
+
+template <int LEVEL>
+__global__ __launch_bounds__(1024) void k_big_select(BigArgs a) {
+  constexpr int NB = LEVEL == 2 ? NB2 : NB3;
+  __shared__ uint32_t h[NB];
+  __shared__ uint32_t scratch[32];
+  const int64_t unit = blockIdx.x;
+  uint32_t* st = a.state + unit * ST_WORDS;
+  const uint32_t T1 = st[ST_T1], need1 = st[ST_NEED1], cnt1 = st[ST_CNT1];
+  if (LEVEL == 2 && need1 == cnt1) {   // the whole bin is selected
+    if (threadIdx.x == 0) {
+      st[ST_TGE] = T1 << D1_SHIFT;
+      st[ST_TEQ] = 0u;
+      st[ST_NEEDEQ] = 0u;
+      st[ST_STAGE] = 0u;
+    }
+    return;
+  }
+  if (LEVEL == 3 && st[ST_STAGE] != 2u) return;
+  uint32_t* H = a.hist1 + unit * a.hstride + (LEVEL == 2 ? 0 : NB2);
+  for (int i = threadIdx.x; i < NB; i += blockDim.x) {
+    h[i] = H[i];
+    H[i] = 0u;
+  }
+  __syncthreads();
+  const uint32_t need = LEVEL == 2 ? need1 : st[ST_NEED2];
+  uint32_t T, above, cnt, ok;
+  block_select_desc(h, NB, need, scratch, &T, &above, &cnt, &ok);
+  if (threadIdx.x != 0) return;
+  if (!ok) atomicOr(a.err, ERR_COUNT_L23);
+  const uint32_t rest = need - above;
+  if (LEVEL == 2) {
+    const uint32_t pre23 = (T1 << (D1_SHIFT - D2_SHIFT)) | T;
+    st[ST_TGE] = pre23 << D2_SHIFT;
+    st[ST_TEQ] = 0u;
+    st[ST_NEEDEQ] = 0u;
+    st[ST_PRE23] = pre23;
+    st[ST_NEED2] = rest;
+    st[ST_STAGE] = (ok && rest != cnt) ? 2u : 0u;
+  } else {
+    const uint32_t key = (st[ST_PRE23] << D2_SHIFT) | T;
+    if (rest == cnt) {
+      st[ST_TGE] = key;
+    } else {
+      st[ST_TGE] = key + 1u;
+      st[ST_TEQ] = key;
+      st[ST_NEEDEQ] = rest;
+    }
+    st[ST_STAGE] = 0u;
+  }
+}
+
+// per slot: entries selected by key (>= TGE) into pre_ge, tied (== TEQ) into pre_eq
+template <int mode>
+__global__ __launch_bounds__(256) void k_big_count(BigArgs a, uint32_t ngroups) {
+  __shared__ uint32_t part[2 * 4];
+  const int64_t unit = blockIdx.x / ngroups;
+  const int32_t grp = (int32_t)(blockIdx.x % ngroups);
+  const uint32_t* st = a.state + unit * ST_WORDS;
+  const uint32_t T1 = st[ST_T1], tge = st[ST_TGE], teq = st[ST_TEQ], need_eq = st[ST_NEEDEQ];
+  const SlotGeom g = slot_geom(mode, (uint32_t)unit, a.B, a.U, a.kb);
+  const int32_t s0 = grp * a.group, s1 = min(g.nslots, s0 + a.group);
+  const uint32_t* __restrict__ cnt = a.slot_cnt + unit * a.smax;
+  const uint32_t* __restrict__ nbn = a.slot_nbin + unit * a.smax;
+  const int64_t o = unit * a.smax;
+  if constexpr (mode == 0) {
+    // a wave per slot: the entries above the bin are selected; count the bin's keys
+    const int nw = blockDim.x / WAVE;
+    for (int32_t slot = s0 + wave_id(); slot < s1; slot += nw) {
+      const int64_t room = g.len - (int64_t)slot * g.ss;
+      const uint32_t c = (uint32_t)min(min((int64_t)cnt[slot], (int64_t)g.ss), room);
+      const uint32_t nb = min(nbn[slot], c);
+      const uint32_t* __restrict__ Ks = a.bin_key + g.base + (int64_t)slot * g.ss;
+      uint32_t ge = 0, eq = 0;
+      for (uint32_t j = lane_id(); j < nb; j += WAVE) {
+        const uint32_t key = Ks[j];
+        ge += key >= tge;
+        eq += need_eq != 0u && key == teq;
+      }
+      ge = wave_sum(ge);
+      eq = wave_sum(eq);
+      if (lane_id() == 0) {
+        a.pre_ge[o + slot] = (c - nb) + ge;
+        a.pre_eq[o + slot] = eq;
+      }
+    }
+  } else {
+    (void)T1;
+    for (int32_t slot = s0; slot < s1; ++slot) {
+      const uint32_t c = min(cnt[slot], (uint32_t)g.ss);
+      const float* __restrict__ Vs = a.U_val + g.base + (int64_t)slot * g.ss;
+      uint32_t ge = 0, eq = 0;
+      for (uint32_t j = threadIdx.x; j < c; j += blockDim.x) {
+        const uint32_t key = mag_key(Vs[j]);
+        ge += key >= tge;
+        eq += need_eq != 0u && key == teq;
+      }
+      ge = wave_sum(ge);
+      eq = wave_sum(eq);
+      if (lane_id() == 0) {
+        part[2 * wave_id()] = ge;
+        part[2 * wave_id() + 1] = eq;
+      }
+      __syncthreads();
+      if (threadIdx.x == 0) {
+        uint32_t tg = 0, te = 0;
+        for (int w = 0; w < (int)(blockDim.x / WAVE); ++w) {
+          tg += part[2 * w];
+          te += part[2 * w + 1];
+        }
+        a.pre_ge[o + slot] = tg;
+        a.pre_eq[o + slot] = te;
+      }
+      __syncthreads();
+    }
+  }
+}
+
+// per unit: exclusive prefixes in slot order (in place over the counts), the
+// consistency checks and the merge's drop count
+template <int mode>
+__global__ __launch_bounds__(1024) void k_big_scan(BigArgs a) {
+  __shared__ uint32_t scratch[32];
+  constexpr uint32_t NT = 1024;
+  const int64_t unit = blockIdx.x;
+  uint32_t* st = a.state + unit * ST_WORDS;
+  const SlotGeom g = slot_geom(mode, (uint32_t)unit, a.B, a.U, a.kb);
+  const uint32_t ns = (uint32_t)g.nslots;
+  const uint32_t per = (ns + NT - 1) / NT;
+  const uint32_t i0 = min(ns, threadIdx.x * per), i1 = min(ns, i0 + per);
+  const int64_t o = unit * a.smax;
+  const uint32_t* __restrict__ cnt = a.slot_cnt + o;
+  uint32_t sa = 0, sg = 0, se = 0;
+  for (uint32_t i = i0; i < i1; ++i) {
+    sa += min(cnt[i], (uint32_t)g.ss);
+    sg += a.pre_ge[o + i];
+    se += a.pre_eq[o + i];
+  }
+  uint32_t ta, tg, te;
+  uint32_t xa = block_excl_scan(sa, scratch, &ta);
+  uint32_t xg = block_excl_scan(sg, scratch, &tg);
+  uint32_t xe = block_excl_scan(se, scratch, &te);
+  for (uint32_t i = i0; i < i1; ++i) {
+    const uint32_t ca = min(cnt[i], (uint32_t)g.ss), cg = a.pre_ge[o + i], ce = a.pre_eq[o + i];
+    a.pre_all[o + i] = xa;
+    a.pre_ge[o + i] = xg;
+    a.pre_eq[o + i] = xe;
+    xa += ca;
+    xg += cg;
+    xe += ce;
+  }
+  if (threadIdx.x == 0) {
+    const uint32_t need_eq = st[ST_NEEDEQ];
+    if (tg + (te < need_eq ? te : need_eq) != (uint32_t)a.kb) atomicOr(a.err, ERR_COUNT_SUM);
+    if (mode == 1) {
+      a.drop_cnt[unit] = (int32_t)(ta - (uint32_t)a.kb);
+      if (ta != st[ST_HTOT]) atomicOr(a.err, ERR_COUNT);
+    }
+  }
+}
+
 // ============================================================================ ordered emit
 // An entry is selected if its key is >= TGE, or equals TEQ and fewer than
 // NEEDEQ equal keys precede it, so the number of selected entries before an
@@ -2205,6 +2474,49 @@ hipError_t launch_thresh(int mode, int64_t nunits, const Units& U, int64_t n, in
                          int lps, uint32_t* hist1, const float* U_val, uint32_t* state, const uint32_t* slot_cnt,
                          const uint32_t* slot_nbin, const uint32_t* bin_key, uint32_t* pre_all, uint32_t* pre_ge,
                          uint32_t* pre_eq, int32_t* drop_cnt, uint32_t* err, hipStream_t s) {
+  // few long units: the staged threshold over slot groups (same results)
+  const bool big = mode == 0 ? (smax > FAST_SLOTS || (nunits < 32 && smax > 1024))
+                             : (2ll * kb > (int64_t)FAST_ROWS * MERGE_TILE);
+  if (big) {
+    if (!hist1) return hipErrorInvalidValue;   // the staged threshold needs the histogram space
+    BigArgs a;
+    a.B = make_blocks(n, P);
+    a.U = U;
+    a.kb = kb;
+    a.smax = smax;
+    a.group = mode == 0 ? BIG_GROUP0 : 1;
+    a.hstride = mode == 0 ? (int64_t)HCOPIES * NB1 : NB1;
+    a.hist1 = hist1;
+    a.U_val = U_val;
+    a.state = state;
+    a.slot_cnt = slot_cnt;
+    a.slot_nbin = slot_nbin;
+    a.bin_key = bin_key;
+    a.pre_all = pre_all;
+    a.pre_ge = pre_ge;
+    a.pre_eq = pre_eq;
+    a.drop_cnt = drop_cnt;
+    a.err = err;
+    const uint32_t ngroups = (uint32_t)((smax + a.group - 1) / a.group);
+    const dim3 gu((unsigned)nunits), gg((unsigned)(nunits * ngroups));
+    if (mode == 0) {
+      hipLaunchKernelGGL((k_big_hist<0, 2>), gg, dim3(256), 0, s, a, ngroups);
+      hipLaunchKernelGGL(k_big_select<2>, gu, dim3(1024), 0, s, a);
+      hipLaunchKernelGGL((k_big_hist<0, 3>), gg, dim3(256), 0, s, a, ngroups);
+      hipLaunchKernelGGL(k_big_select<3>, gu, dim3(1024), 0, s, a);
+      hipLaunchKernelGGL(k_big_count<0>, gg, dim3(256), 0, s, a, ngroups);
+      hipLaunchKernelGGL(k_big_scan<0>, gu, dim3(1024), 0, s, a);
+    } else {
+      hipLaunchKernelGGL(k_big_level1, gu, dim3(1024), 0, s, a);
+      hipLaunchKernelGGL((k_big_hist<1, 2>), gg, dim3(256), 0, s, a, ngroups);
+      hipLaunchKernelGGL(k_big_select<2>, gu, dim3(1024), 0, s, a);
+      hipLaunchKernelGGL((k_big_hist<1, 3>), gg, dim3(256), 0, s, a, ngroups);
+      hipLaunchKernelGGL(k_big_select<3>, gu, dim3(1024), 0, s, a);
+      hipLaunchKernelGGL(k_big_count<1>, gg, dim3(256), 0, s, a, ngroups);
+      hipLaunchKernelGGL(k_big_scan<1>, gu, dim3(1024), 0, s, a);
+    }
+    return hipGetLastError();
+  }
   if (mode == 0)
     hipLaunchKernelGGL(k_thresh<0>, dim3((unsigned)nunits), dim3(1024), 0, s, make_blocks(n, P), U, kb, smax, lps, hist1, U_val,
                        state, slot_cnt, slot_nbin, bin_key, pre_all, pre_ge, pre_eq, drop_cnt, err);
