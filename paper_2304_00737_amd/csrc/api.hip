@@ -260,7 +260,7 @@ int topk_units(const float* acc, int64_t ld_acc, int64_t units, const Units& U, 
                             w.slot_cnt, w.slot_nbin, w.cand_idx, w.cand_val, w.bin_key, stream));
   // hist1: the staged threshold for long units builds its level-2/3 histograms in the units'
   // level-1 histogram space, which the select has cleared
-  SPARDL_TRY(launch_thresh(0, units, U, n, P, k_blk, smax, 1, w.hist1, w.cand_val, w.state, w.slot_cnt,
+  SPARDL_TRY(launch_thresh(0, units, U, n, P, k_blk, smax, w.hist1, w.cand_val, w.state, w.slot_cnt,
                            w.slot_nbin, w.bin_key, w.pre_all, w.pre_ge, w.pre_eq, nullptr, w.err, stream));
   SPARDL_TRY(launch_emit(0, w.cand_idx, w.cand_val, units, U, n, P, k_blk, Pairs{}, smax, w.state, w.slot_cnt,
                          w.pre_all, w.pre_ge, w.pre_eq, sp_idx, sp_val, local_idx, nullptr, nullptr, w.err, stream));
@@ -379,7 +379,7 @@ int spardl_sparse_merge_topk(int32_t* sp_idx, float* sp_val, int32_t P, int64_t 
   const Pairs PM = srs_pairs(P, m, d);
   SPARDL_TRY(launch_merge(sp_idx, sp_val, PM, pairs, k_blk, smax, w.hist1, w.slot_cnt, w.cand_idx, w.cand_val,
                           stream));
-  SPARDL_TRY(launch_thresh(1, pairs, all_blocks(P), n, P, k_blk, smax, 1, w.hist1, w.cand_val, w.state, w.slot_cnt, w.slot_nbin,
+  SPARDL_TRY(launch_thresh(1, pairs, all_blocks(P), n, P, k_blk, smax, w.hist1, w.cand_val, w.state, w.slot_cnt, w.slot_nbin,
                            w.bin_key, w.pre_all, w.pre_ge, w.pre_eq, drop_cnt, w.err, stream));
   SPARDL_TRY(launch_emit(1, w.cand_idx, w.cand_val, pairs, all_blocks(P), n, P, k_blk, PM, smax, w.state, w.slot_cnt, w.pre_all,
                          w.pre_ge, w.pre_eq, sp_idx, sp_val, nullptr, drop_idx, drop_val, w.err, stream));
@@ -508,7 +508,7 @@ int spardl_rsag_merge_topk(int32_t* sp_idx, float* sp_val, int32_t P, int32_t d,
   const int32_t smax = (int32_t)L.tiles_mg;
   SPARDL_TRY(launch_merge(sp_idx, sp_val, PM, npairs, k_blk, smax, w.hist1, w.slot_cnt, w.cand_idx, w.cand_val,
                           stream));
-  SPARDL_TRY(launch_thresh(1, npairs, all_blocks(Q), n, Q, k_blk, smax, 1, w.hist1, w.cand_val, w.state,
+  SPARDL_TRY(launch_thresh(1, npairs, all_blocks(Q), n, Q, k_blk, smax, w.hist1, w.cand_val, w.state,
                            w.slot_cnt, w.slot_nbin, w.bin_key, w.pre_all, w.pre_ge, w.pre_eq, drop_cnt, w.err,
                            stream));
   SPARDL_TRY(launch_emit(1, w.cand_idx, w.cand_val, npairs, all_blocks(Q), n, Q, k_blk, PM, smax, w.state,

@@ -30,7 +30,6 @@ constexpr int MERGE_PER_THREAD = 16;
 constexpr int MERGE_TILE = MERGE_THREADS * MERGE_PER_THREAD;   // merged positions per workgroup
 constexpr int DENSE_TILE = 16384;
 constexpr int HCOPIES = 4;                       // level-1 histogram copies per block (spreads the flush atomics)
-constexpr int SLOT_LDS = 4096;                   // slots per chunk in the threshold kernel's per-slot pass
 
 // ---------------------------------------------------------------- state words
 // Per selection unit (a (worker, block) pair or a merge pair), 16 u32:

@@ -598,98 +598,15 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(8, 8))) voi
 //
 // Only the entries of the level-1 threshold bin need levels 2 and 3.  For a
 // dense block they were stored per slot by k_collect; for a merge they are
-// picked out of the union here (after the level-1 select on the union's
-// histogram, which is done here too).  When the bin fits (THRESH_CACHE
-// entries) its keys and slot numbers are gathered once into LDS and every
-// later step runs from LDS; otherwise each step re-reads global memory.
-constexpr int THRESH_CACHE = 8192;
-constexpr int GATHER_U = 8;    // loads in flight per lane in the gathers
-
+// picked out of the union (after the level-1 select on the union's histogram,
+// which is done here too).  This kernel takes units whose bin entries (block
+// top-k) or whole union (merge) fit its register-resident paths; longer units
+// take the staged threshold over slot groups below, which writes the same
+// results (launch_thresh chooses).
 struct ThreshSmem {
   uint32_t h[NB1];
-  uint32_t ck[THRESH_CACHE];   // cached key
-  uint32_t cs[THRESH_CACHE];   // cached slot
-  uint32_t cg[SLOT_LDS];       // per-slot count of selected-by-key (>= TGE)
-  uint32_t ce[SLOT_LDS];       // per-slot count of key == TEQ
   uint32_t scratch[24];
-  uint32_t ncache;
 };
-
-// Threshold-bin keys of a dense block, stored per slot: f(key, slot, valid),
-// called by every lane of a wave together (so f may use ballots).  lps
-// lanes per slot, each with up to GATHER_U loads in flight.
-template <typename F>
-__device__ __forceinline__ void visit_bin_keys(const uint32_t* __restrict__ K, const SlotGeom& g,
-                                               const uint32_t* __restrict__ nbin, int32_t s_begin,
-                                               int32_t s_end, int lps, F f) {
-  const int per_round = blockDim.x / lps;
-  const int sl = threadIdx.x / lps, li = threadIdx.x % lps;
-  for (int32_t s0 = s_begin; s0 < s_end; s0 += per_round) {
-    const int32_t slot = s0 + sl;
-    const bool live = slot < s_end;
-    const uint32_t* __restrict__ Ks = K + (int64_t)(live ? slot : s_begin) * g.ss;
-    // the slot's count and its first keys are loaded together (keys past the
-    // count are read from inside the slot and discarded)
-    const int64_t room = g.len - (int64_t)(live ? slot : s_begin) * g.ss;   // entries inside the region
-    const uint32_t cap = (uint32_t)min(min((int64_t)g.ss, room), (int64_t)GATHER_U * lps);
-    uint32_t key[GATHER_U];
-#pragma unroll
-    for (int u = 0; u < GATHER_U; ++u) {
-      const uint32_t k = u * lps + li;
-      key[u] = k < cap ? Ks[k] : 0u;
-    }
-    const uint32_t nb = live ? min(nbin[slot], (uint32_t)g.ss) : 0u;
-#pragma unroll
-    for (int u = 0; u < GATHER_U; ++u) {
-      const uint32_t k = u * lps + li;
-      f(key[u], slot, k < nb);
-    }
-    uint32_t wmax = nb;   // the wave continues as long as its longest slot needs
-#pragma unroll
-    for (int d = WAVE / 2; d > 0; d >>= 1) wmax = max(wmax, (uint32_t)__shfl_xor(wmax, d, WAVE));
-    for (uint32_t k0 = GATHER_U * lps; k0 < wmax; k0 += GATHER_U * lps) {
-#pragma unroll
-      for (int u = 0; u < GATHER_U; ++u) {
-        const uint32_t k = k0 + u * lps + li;
-        key[u] = k < nb ? Ks[k] : 0u;
-      }
-#pragma unroll
-      for (int u = 0; u < GATHER_U; ++u) {
-        const uint32_t k = k0 + u * lps + li;
-        f(key[u], slot, k < nb);
-      }
-    }
-  }
-}
-
-// Every entry of a merge union: f(key, slot, valid), called by all lanes
-// together (a wave's 64 positions always lie in one slot).  Values are loaded
-// together with the slot counts; positions past a slot's count are read from
-// inside the unit's region and discarded.
-template <typename F>
-__device__ __forceinline__ void visit_union(const float* __restrict__ V, const SlotGeom& g,
-                                            const uint32_t* __restrict__ cnt, int32_t s_begin, int32_t s_end,
-                                            F f) {
-  const int nt = blockDim.x;
-  const int64_t p_end = min((int64_t)s_end * g.ss, g.len);   // never read past the unit's region
-  for (int64_t p0 = (int64_t)s_begin * g.ss; p0 < p_end; p0 += (int64_t)GATHER_U * nt) {
-    float val[GATHER_U];
-    uint32_t c[GATHER_U];
-#pragma unroll
-    for (int u = 0; u < GATHER_U; ++u) {
-      const int64_t p = min(p0 + (int64_t)u * nt + threadIdx.x, p_end - 1);
-      val[u] = V[p];
-      c[u] = cnt[p / g.ss];
-    }
-#pragma unroll
-    for (int u = 0; u < GATHER_U; ++u) {
-      const int64_t p = p0 + (int64_t)u * nt + threadIdx.x;
-      const int32_t slot = (int32_t)(min(p, p_end - 1) / g.ss);
-      const bool valid = p < p_end && (uint32_t)(p - (int64_t)slot * g.ss) < min(c[u], (uint32_t)g.ss);
-      f(mag_key(val[u]), slot, valid);
-    }
-  }
-}
 
 // ---- resident fast paths
 // When a unit's threshold-bin entries (block top-k) or its whole union
@@ -1095,7 +1012,7 @@ __device__ __forceinline__ void thresh_fast_topk(FastSmem& L, int64_t unit, cons
 
 template <int mode>
 __global__ __launch_bounds__(1024) void k_thresh(Blocks B, Units U, int32_t kb, int32_t smax,
-                                                 int lps, uint32_t* __restrict__ hist1,
+                                                 uint32_t* __restrict__ hist1,
                                                  const float* __restrict__ U_val, uint32_t* __restrict__ state,
                                                  const uint32_t* __restrict__ slot_cnt,
                                                  const uint32_t* __restrict__ slot_nbin,
@@ -1113,8 +1030,6 @@ __global__ __launch_bounds__(1024) void k_thresh(Blocks B, Units U, int32_t kb, 
   const uint32_t* __restrict__ nbn = slot_nbin + unit * smax;
   const uint32_t* __restrict__ K = bin_key + g.base;
   const float* __restrict__ V = U_val + g.base;
-  const int lane = lane_id();
-  const uint64_t lt = __lanemask_lt();
   uint32_t ok;
 
   // ---- level 1
@@ -1147,180 +1062,7 @@ __global__ __launch_bounds__(1024) void k_thresh(Blocks B, Units U, int32_t kb, 
       return;
     }
   }
-  const bool cached = cnt1 <= (uint32_t)THRESH_CACHE && (mode == 0 || g.nslots <= SLOT_LDS);
-
-  // ---- gather the threshold bin into LDS (mode 1 also counts the above-bin entries per slot)
-  if (cached) {
-    if (threadIdx.x == 0) L.ncache = 0u;
-    for (int i = threadIdx.x; i < SLOT_LDS; i += NT) {
-      L.cg[i] = 0u;
-      L.ce[i] = 0u;
-    }
-    __syncthreads();
-    auto append = [&](bool take, uint32_t key, int32_t slot) {   // wave-aggregated LDS append
-      const uint64_t mk = __ballot(take);
-      if (mk == 0ull) return;
-      uint32_t base = 0;
-      if (lane == 0) base = atomicAdd(&L.ncache, popc64(mk));
-      base = __shfl(base, 0, WAVE);
-      if (take) {
-        const uint32_t q = base + popc64(mk & lt);
-        if (q < (uint32_t)THRESH_CACHE) {
-          L.ck[q] = key;
-          L.cs[q] = (uint32_t)slot;
-        }
-      }
-    };
-    if constexpr (mode == 0) {
-      visit_bin_keys(K, g, nbn, 0, g.nslots, lps,
-                     [&](uint32_t key, int32_t slot, bool valid) { append(valid, key, slot); });
-    } else {
-      visit_union(V, g, cnt, 0, g.nslots, [&](uint32_t key, int32_t slot, bool valid) {
-        const uint32_t d1 = key >> D1_SHIFT;
-        const uint64_t ma = __ballot(valid && d1 > T1);
-        if (lane == 0 && ma) atomicAdd(&L.cg[slot], popc64(ma));
-        append(valid && d1 == T1, key, slot);
-      });
-    }
-    __syncthreads();
-  }
-  const uint32_t ncache = cached ? min(L.ncache, (uint32_t)THRESH_CACHE) : 0u;
-  // every threshold-bin entry: from the cache, or from global memory
-  auto visit_bin = [&](auto f) {
-    if (cached) {
-      for (uint32_t i = threadIdx.x; i < ncache; i += NT) f(L.ck[i], (int32_t)L.cs[i]);
-    } else if constexpr (mode == 0) {
-      visit_bin_keys(K, g, nbn, 0, g.nslots, lps, [&](uint32_t key, int32_t slot, bool valid) {
-        if (valid) f(key, slot);
-      });
-    } else {
-      visit_union(V, g, cnt, 0, g.nslots, [&](uint32_t key, int32_t slot, bool valid) {
-        if (valid && (key >> D1_SHIFT) == T1) f(key, slot);
-      });
-    }
-  };
-
-  // ---- levels 2 and 3
-  uint32_t tge = T1 << D1_SHIFT, teq = 0u, need_eq = 0u;
-  if (need1 != cnt1) {
-    for (int i = threadIdx.x; i < NB2; i += NT) L.h[i] = 0u;
-    __syncthreads();
-    visit_bin([&](uint32_t key, int32_t) { atomicAdd(&L.h[(key >> D2_SHIFT) & (NB2 - 1)], 1u); });
-    __syncthreads();
-    uint32_t T2, above2, cnt2;
-    block_select_desc(L.h, NB2, need1, L.scratch, &T2, &above2, &cnt2, &ok);
-    if (!ok && threadIdx.x == 0) atomicOr(err, ERR_COUNT_L23);
-    const uint32_t need2 = need1 - above2;
-    const uint32_t pre23 = (T1 << (D1_SHIFT - D2_SHIFT)) | T2;   // top 23 bits of the key
-    tge = pre23 << D2_SHIFT;
-    if (ok && need2 != cnt2) {
-      for (int i = threadIdx.x; i < NB3; i += NT) L.h[i] = 0u;
-      __syncthreads();
-      visit_bin([&](uint32_t key, int32_t) {
-        if ((key >> D2_SHIFT) == pre23) atomicAdd(&L.h[key & (NB3 - 1)], 1u);
-      });
-      __syncthreads();
-      uint32_t T3, above3, cnt3;
-      block_select_desc(L.h, NB3, need2, L.scratch, &T3, &above3, &cnt3, &ok);
-      if (!ok && threadIdx.x == 0) atomicOr(err, ERR_COUNT_L23);
-      const uint32_t need3 = need2 - above3;
-      const uint32_t T = (pre23 << D2_SHIFT) | T3;
-      if (need3 == cnt3) {
-        tge = T;
-      } else {
-        tge = T + 1u;
-        teq = T;
-        need_eq = need3;
-      }
-    }
-  }
-
-  // ---- per-slot counts (>= TGE, == TEQ) and their exclusive prefixes, in slot chunks
-  uint32_t run_all = 0, run_ge = 0, run_eq = 0;
-  for (int32_t c0 = 0; c0 < g.nslots; c0 += SLOT_LDS) {
-    const int32_t nc = min(SLOT_LDS, g.nslots - c0);
-    const int32_t c1 = c0 + nc;
-    // start values: entries above the threshold bin are selected by key
-    if (!(mode == 1 && cached)) {
-      __syncthreads();
-      for (int i = threadIdx.x; i < SLOT_LDS; i += NT) {
-        uint32_t a = 0u;
-        if (mode == 0 && i < nc) {
-          const uint32_t c = min(cnt[c0 + i], (uint32_t)g.ss);
-          a = c - min(nbn[c0 + i], c);
-        }
-        L.cg[i] = a;
-        L.ce[i] = 0u;
-      }
-      __syncthreads();
-    }
-    if (mode == 1 && !cached) {
-      if constexpr (mode == 1) visit_union(V, g, cnt, c0, c1, [&](uint32_t key, int32_t slot, bool valid) {
-        const uint64_t mg = __ballot(valid && key >= tge);
-        const uint64_t me = __ballot(valid && need_eq != 0u && key == teq);
-        if (lane == 0) {
-          if (mg) atomicAdd(&L.cg[slot - c0], popc64(mg));
-          if (me) atomicAdd(&L.ce[slot - c0], popc64(me));
-        }
-      });
-    } else {
-      auto count_bin = [&](uint32_t key, int32_t slot) {
-        if (slot < c0 || slot >= c1) return;
-        if (key >= tge) atomicAdd(&L.cg[slot - c0], 1u);
-        else if (need_eq != 0u && key == teq) atomicAdd(&L.ce[slot - c0], 1u);
-      };
-      if (cached) {
-        for (uint32_t i = threadIdx.x; i < ncache; i += NT) count_bin(L.ck[i], (int32_t)L.cs[i]);
-      } else if constexpr (mode == 0) {
-        visit_bin_keys(K, g, nbn, c0, c1, lps, [&](uint32_t key, int32_t slot, bool valid) {
-          if (valid) count_bin(key, slot);
-        });
-      }
-    }
-    __syncthreads();
-    uint32_t a[4], gg[4], ee[4], sa = 0, sg = 0, se = 0;
-#pragma unroll
-    for (int k = 0; k < 4; ++k) {
-      const int i = 4 * threadIdx.x + k;
-      a[k] = i < nc ? min(cnt[c0 + i], (uint32_t)g.ss) : 0u;
-      gg[k] = i < nc ? L.cg[i] : 0u;
-      ee[k] = i < nc ? L.ce[i] : 0u;
-      sa += a[k];
-      sg += gg[k];
-      se += ee[k];
-    }
-    uint32_t ta, tg, te;
-    uint32_t xa = block_excl_scan(sa, L.scratch, &ta);
-    uint32_t xg = block_excl_scan(sg, L.scratch, &tg);
-    uint32_t xe = block_excl_scan(se, L.scratch, &te);
-    const int64_t o = unit * smax + c0;
-#pragma unroll
-    for (int k = 0; k < 4; ++k) {
-      const int i = 4 * threadIdx.x + k;
-      if (i < nc) {
-        pre_all[o + i] = run_all + xa;
-        pre_ge[o + i] = run_ge + xg;
-        pre_eq[o + i] = run_eq + xe;
-      }
-      xa += a[k];
-      xg += gg[k];
-      xe += ee[k];
-    }
-    run_all += ta;
-    run_ge += tg;
-    run_eq += te;
-  }
-  if (threadIdx.x == 0) {
-    if (run_ge + (run_eq < need_eq ? run_eq : need_eq) != (uint32_t)kb) atomicOr(err, ERR_COUNT_SUM);
-    st[ST_T1] = T1;
-    st[ST_TGE] = tge;
-    st[ST_TEQ] = teq;
-    st[ST_NEEDEQ] = need_eq;
-    if (mode == 1) {
-      drop_cnt[unit] = (int32_t)(run_all - (uint32_t)kb);
-      if (run_all != hist_total) atomicOr(err, ERR_COUNT);
-    }
-  }
+  if (threadIdx.x == 0) atomicOr(err, ERR_COUNT);   // longer units are routed to the staged threshold
 }
 
 // ============================================================================ exact threshold, large units
@@ -2471,7 +2213,7 @@ hipError_t launch_collect(const float* acc, int64_t ld_acc, int64_t nunits, cons
 }
 
 hipError_t launch_thresh(int mode, int64_t nunits, const Units& U, int64_t n, int32_t P, int32_t kb, int32_t smax,
-                         int lps, uint32_t* hist1, const float* U_val, uint32_t* state, const uint32_t* slot_cnt,
+                         uint32_t* hist1, const float* U_val, uint32_t* state, const uint32_t* slot_cnt,
                          const uint32_t* slot_nbin, const uint32_t* bin_key, uint32_t* pre_all, uint32_t* pre_ge,
                          uint32_t* pre_eq, int32_t* drop_cnt, uint32_t* err, hipStream_t s) {
   // few long units: the staged threshold over slot groups (same results)
@@ -2518,10 +2260,10 @@ hipError_t launch_thresh(int mode, int64_t nunits, const Units& U, int64_t n, in
     return hipGetLastError();
   }
   if (mode == 0)
-    hipLaunchKernelGGL(k_thresh<0>, dim3((unsigned)nunits), dim3(1024), 0, s, make_blocks(n, P), U, kb, smax, lps, hist1, U_val,
+    hipLaunchKernelGGL(k_thresh<0>, dim3((unsigned)nunits), dim3(1024), 0, s, make_blocks(n, P), U, kb, smax, hist1, U_val,
                        state, slot_cnt, slot_nbin, bin_key, pre_all, pre_ge, pre_eq, drop_cnt, err);
   else
-    hipLaunchKernelGGL(k_thresh<1>, dim3((unsigned)nunits), dim3(1024), 0, s, make_blocks(n, P), U, kb, smax, lps, hist1, U_val,
+    hipLaunchKernelGGL(k_thresh<1>, dim3((unsigned)nunits), dim3(1024), 0, s, make_blocks(n, P), U, kb, smax, hist1, U_val,
                        state, slot_cnt, slot_nbin, bin_key, pre_all, pre_ge, pre_eq, drop_cnt, err);
   return hipGetLastError();
 }

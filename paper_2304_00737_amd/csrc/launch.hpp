@@ -40,7 +40,7 @@ hipError_t launch_collect(const float* acc, int64_t ld_acc, int64_t nunits, cons
                           int32_t add_tiles, uint32_t* slot_cnt, uint32_t* slot_nbin, int32_t* cand_idx,
                           float* cand_val, uint32_t* bin_key, hipStream_t s);
 hipError_t launch_thresh(int mode, int64_t nunits, const Units& U, int64_t n, int32_t P, int32_t kb, int32_t smax,
-                         int lps, uint32_t* hist1, const float* U_val, uint32_t* state, const uint32_t* slot_cnt,
+                         uint32_t* hist1, const float* U_val, uint32_t* state, const uint32_t* slot_cnt,
                          const uint32_t* slot_nbin, const uint32_t* bin_key, uint32_t* pre_all, uint32_t* pre_ge,
                          uint32_t* pre_eq, int32_t* drop_cnt, uint32_t* err, hipStream_t s);
 hipError_t launch_emit(int mode, const int32_t* cand_idx, const float* cand_val, int64_t nunits, const Units& U,

@@ -64,11 +64,11 @@ def test_workload4_bert_sized_sampled():
 
 @pytest.mark.parametrize("density", [(1, 100), (1, 10000)])
 def test_long_blocks_general_threshold_paths(density):
-    """Blocks of 35M elements: more candidate slots (8545) than the threshold
-    kernel keeps resident, so the block top-k takes the general path (cached
-    bin at 0.01 %, re-read from memory at 1 %); at 1 % the merge union spans 171
-    slots, more than the register-resident merge path holds, so the merge
-    threshold takes its general path too."""
+    """Blocks of 35M elements: more candidate slots (8545) than the
+    one-workgroup threshold keeps resident, so the block top-k takes the staged
+    threshold over slot groups; at 1 % the merge union spans 171 slots, more
+    than the register-resident merge path holds, so the merge threshold is
+    staged too."""
     n = 70_000_000
     lens, sc = W._segments_loguniform(90, 40, n, 2 ** 9, 2 ** 22, 1e-5, 1e-1)
     wl = W.Workload(90, f"long blocks P=2 n=70M rho={density[0]}/{density[1]}", 2, n, density, 2, "normal", lens, sc)
