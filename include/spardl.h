@@ -197,7 +197,7 @@ int spardl_residual_collect(float* acc, int64_t ld_acc, int32_t P, int64_t n, in
  * Held blocks stay dense: a worker sparsifies a block only right before it
  * sends it (and its reserved block after the last step), and a receiver adds
  * the received entries into its dense row.  One step, for P workers whose
- * rows are acc[w*ld_acc ...] (A_w after a plain spardl_residual_add), is:
+ * rows are acc[w*ld_acc ...] (A_w after spardl_residual_add), is:
  *   for round = 1..l: spardl_lazy_topk(round) on every worker, then
  *                     spardl_lazy_receive(round);
  *   spardl_lazy_topk(0) on every worker;
@@ -205,6 +205,12 @@ int spardl_residual_collect(float* acc, int64_t ld_acc, int32_t P, int64_t n, in
  *   spardl_lazy_residual_collect(..., member, saved).
  * Every worker selects every block once, so sp[w][b] (layout as for
  * spardl_block_topk) ends holding all P x P selections.
+ * Fused form (all P rows in one workspace): the residual add with the
+ * workspace (as for spardl_block_topk), every spardl_lazy_topk with
+ * SPARDL_TOPK_HIST_READY and every spardl_lazy_receive with the workspace,
+ * which keeps the add's histograms exact through the receipts; a selection
+ * then reads its block at most once, not at all while it is unchanged since
+ * the add.  Plain form: a plain add, flags 0, receipts without a workspace.
  * ------------------------------------------------------------------------- */
 
 /* Block top-k of the blocks that workers w0 .. w0 + nworkers - 1 sparsify at
@@ -217,12 +223,15 @@ int spardl_residual_collect(float* acc, int64_t ld_acc, int32_t P, int64_t n, in
  *   spardl_block_topk).
  * Other blocks of sp are not written.  ws: a workspace for nworkers rows
  * (spardl_workspace_bytes(nworkers, P, n, k_blk)), prepared once.
+ * flags: 0, or SPARDL_TOPK_HIST_READY in the fused form (then w0 = 0 and
+ * nworkers = P).
  * Errors: EINVAL for NULL acc/sp/ws, misaligned ws, nworkers < 1, w0 < 0,
  * w0 + nworkers > P, P < 1, n < P, n >= 2^31, ld_acc < n, k_blk outside
- * [1, floor(n/P)], round outside [0, l]; ECAPACITY if ws is too small. */
+ * [1, floor(n/P)], round outside [0, l], unknown flags, HIST_READY with a
+ * row subset; ECAPACITY if ws is too small. */
 int spardl_lazy_topk(const float* acc, int64_t ld_acc, int32_t w0, int32_t nworkers, int64_t n, int32_t P,
-                     int32_t k_blk, int32_t round, int32_t* sp_idx, float* sp_val, void* ws, size_t ws_bytes,
-                     hipStream_t stream);
+                     int32_t k_blk, int32_t round, int32_t flags, int32_t* sp_idx, float* sp_val, void* ws,
+                     size_t ws_bytes, hipStream_t stream);
 
 /* Transmission and summation of SRS step `round` in [1, l] (Algorithm 1),
  * all P workers at once.  With d = 2^(l-round) and m = bag_blocks of the
@@ -234,11 +243,16 @@ int spardl_lazy_topk(const float* acc, int64_t ld_acc, int32_t w0, int32_t nwork
  * spardl_lazy_residual_collect; each (w, b) is sent at exactly one step, so
  * one buffer serves all steps.  Entries whose index lies outside block b are
  * skipped.  Steps must run in order 1..l, each after spardl_lazy_topk of the
- * same round on every worker.
+ * same round on every worker.  ws (optional): the fused form's workspace for
+ * all P rows; the receipt then updates the receiving block's histogram and
+ * marks the block as changed since the add.
  * Errors: EINVAL for NULL pointers, P < 2 (no steps), n < P, n >= 2^31,
- * ld_acc < n, k_blk outside [1, floor(n/P)], round outside [1, l]. */
+ * ld_acc < n, k_blk outside [1, floor(n/P)], round outside [1, l], a
+ * misaligned ws; ECAPACITY if ws is smaller than
+ * spardl_workspace_bytes(P, P, n, k_blk). */
 int spardl_lazy_receive(float* acc, int64_t ld_acc, int32_t P, int64_t n, int32_t k_blk, int32_t round,
-                        const int32_t* sp_idx, const float* sp_val, float* saved, hipStream_t stream);
+                        const int32_t* sp_idx, const float* sp_val, float* saved, void* ws, size_t ws_bytes,
+                        hipStream_t stream);
 
 /* Residual collection of the lazy step (Algorithm 1: "Replace part of
  * G_copy at indexes I_i with xi_i").  With I the final index set given by

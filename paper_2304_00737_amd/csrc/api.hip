@@ -253,7 +253,9 @@ int topk_units(const float* acc, int64_t ld_acc, int64_t units, const Units& U, 
     SPARDL_TRY(launch_fill(Fill().add(w.hist1, units * HCOPIES * NB1).r, stream));
     SPARDL_TRY(launch_hist1(acc, ld_acc, units, U, n, P, v4, w.hist1, stream));
   }
-  uint32_t* hint = U.rel ? nullptr : w.spec_t1;
+  // the previous-threshold hint feeds the next fused add: kept unless this is a
+  // lazy selection that did not start from a fused add
+  uint32_t* hint = (U.rel && !spec) ? nullptr : w.spec_t1;
   SPARDL_TRY(launch_select1(w.hist1, w.state, units, U, n, P, (uint32_t)k_blk, hint, w.spec_used, spec, acc, ld_acc,
                             v4, w.err, stream));
   SPARDL_TRY(launch_collect(acc, ld_acc, units, U, n, P, v4, smax, w.state, w.spec_cnt, (int32_t)L.add_tiles,
@@ -426,11 +428,13 @@ int spardl_residual_collect(float* acc, int64_t ld_acc, int32_t P, int64_t n, in
 }
 
 int spardl_lazy_topk(const float* acc, int64_t ld_acc, int32_t w0, int32_t nworkers, int64_t n, int32_t P,
-                     int32_t k_blk, int32_t round, int32_t* sp_idx, float* sp_val, void* ws, size_t ws_bytes,
-                     hipStream_t stream) {
+                     int32_t k_blk, int32_t round, int32_t flags, int32_t* sp_idx, float* sp_val, void* ws,
+                     size_t ws_bytes, hipStream_t stream) {
   if (!acc || !sp_idx || !sp_val || !ws || ws_misaligned(ws) || nworkers < 1 || w0 < 0 || w0 > P - nworkers ||
-      !sizes_ok(P, n, k_blk) || ld_acc < n)
+      !sizes_ok(P, n, k_blk) || ld_acc < n || (flags & ~SPARDL_TOPK_HIST_READY))
     return SPARDL_EINVAL;
+  const bool fused = (flags & SPARDL_TOPK_HIST_READY) != 0;
+  if (fused && (w0 != 0 || nworkers != P)) return SPARDL_EINVAL;   // the fused add's arrays cover all P rows
   const int32_t l = steps_of(P);
   if (round < 0 || round > l) return SPARDL_EINVAL;
   const size_t need = spardl_workspace_bytes(nworkers, P, n, k_blk);
@@ -441,17 +445,28 @@ int spardl_lazy_topk(const float* acc, int64_t ld_acc, int32_t w0, int32_t nwork
   // round r >= 1: the bag sent at step r, blocks (w + 2^(l-r) + t) mod P, t < m_r; round 0: block w
   const Units U{round ? (uint32_t)bag_of(P, l, round) : 1u, round ? (uint32_t)(1 << (l - round)) : 0u, 1u,
                 (uint32_t)w0};
-  return topk_units(acc, ld_acc, (int64_t)nworkers * U.m, U, n, P, k_blk, true, false, sp_idx, sp_val, nullptr, w, L,
-                    stream);
+  return topk_units(acc, ld_acc, (int64_t)nworkers * U.m, U, n, P, k_blk, !fused, fused, sp_idx, sp_val, nullptr, w,
+                    L, stream);
 }
 
 int spardl_lazy_receive(float* acc, int64_t ld_acc, int32_t P, int64_t n, int32_t k_blk, int32_t round,
-                        const int32_t* sp_idx, const float* sp_val, float* saved, hipStream_t stream) {
+                        const int32_t* sp_idx, const float* sp_val, float* saved, void* ws, size_t ws_bytes,
+                        hipStream_t stream) {
   if (!acc || !sp_idx || !sp_val || !saved || !sizes_ok(P, n, k_blk) || ld_acc < n) return SPARDL_EINVAL;
   const int32_t l = steps_of(P);
   if (round < 1 || round > l) return SPARDL_EINVAL;
+  uint32_t *hist1 = nullptr, *spec_used = nullptr;
+  if (ws) {   // keep the fused add's histograms exact through the receipts
+    if (ws_misaligned(ws)) return SPARDL_EINVAL;
+    const size_t need = spardl_workspace_bytes(P, P, n, k_blk);
+    if (ws_bytes < need) return SPARDL_ECAPACITY;
+    const Layout L = make_layout(P, n, k_blk);
+    Ws w = carve(ws, ws_bytes, L);
+    hist1 = w.hist1;
+    spec_used = w.spec_used;
+  }
   SPARDL_TRY(launch_lazy_step(acc, ld_acc, P, n, k_blk, 1 << (l - round), bag_of(P, l, round), sp_idx, sp_val, saved,
-                              nullptr, false, stream));
+                              nullptr, false, hist1, spec_used, stream));
   return SPARDL_OK;
 }
 
@@ -467,8 +482,8 @@ int spardl_lazy_residual_collect(float* acc, int64_t ld_acc, int32_t P, int64_t 
   SPARDL_TRY(launch_grc_zero(acc, ld_acc, P, n, k_blk, sp_idx, member, stream));
   // received and not final -> the value before the first receipt
   for (int32_t i = l; i >= 1; --i)
-    SPARDL_TRY(launch_lazy_step(acc, ld_acc, P, n, k_blk, 1 << (l - i), bag_of(P, l, i), sp_idx, nullptr, const_cast<float*>(saved),
-                                member, true, stream));
+    SPARDL_TRY(launch_lazy_step(acc, ld_acc, P, n, k_blk, 1 << (l - i), bag_of(P, l, i), sp_idx, nullptr,
+                                const_cast<float*>(saved), member, true, nullptr, nullptr, stream));
   return SPARDL_OK;
 }
 

@@ -98,6 +98,14 @@ struct Units {
     *row = r;
     *b = (d + (u - r * m) + (rel ? w0 + r : 0u)) % P;
   }
+  // row * P + block: where the unit's per-block arrays live (histograms,
+  // speculation words, selection state, slot counts), the same place for
+  // every map, so a selection finds what the fused add left for its block
+  __device__ __forceinline__ uint32_t canon(uint32_t u, uint32_t P) const {
+    uint32_t r, b;
+    decode(u, P, &r, &b);
+    return r * P + b;
+  }
 };
 
 inline Units all_blocks(int32_t P) { return Units{(uint32_t)P, 0u, 0u, 0u}; }

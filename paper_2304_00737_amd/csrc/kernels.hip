@@ -74,11 +74,13 @@ __device__ __forceinline__ void flush_hist(const uint32_t* h, uint32_t* __restri
 constexpr uint32_t SPEC_MARGIN = 2;     // level-1 bins between the previous threshold bin and the floor
 constexpr uint32_t HIST_MARGIN = 32;    // further level-1 bins below the candidate floor kept in the histogram
 constexpr uint32_t SPEC_NONE = 0xFFFFFFFFu;
+constexpr uint32_t SPEC_DIRTY = 0x80000000u;   // set on spec_used: entries changed since the add, candidates stale
 constexpr int ADD_STAGE = 512;          // speculative candidates staged in LDS per tile
 
 // Histogram floor (a key) for a candidate floor F (SPEC_NONE: histogram everything).
 __device__ __forceinline__ uint32_t hist_floor(uint32_t F) {
   if (F == SPEC_NONE) return 0u;
+  F &= ~SPEC_DIRTY;
   const uint32_t fb = F >> D1_SHIFT;
   return fb > HIST_MARGIN ? (fb - HIST_MARGIN) << D1_SHIFT : 0u;
 }
@@ -135,7 +137,7 @@ __global__ __launch_bounds__(256) void k_residual_add(float* __restrict__ acc, i
         q.y = a[j].y + gg[j].y;
         q.z = a[j].z + gg[j].z;
         q.w = a[j].w + gg[j].w;
-        *reinterpret_cast<f4v*>(A + my0 + 4u * j) = q;
+        __builtin_nontemporal_store(q, reinterpret_cast<f4v*>(A + my0 + 4u * j));   // re-read only next step
         r[4 * j + 0] = q.x;
         r[4 * j + 1] = q.y;
         r[4 * j + 2] = q.z;
@@ -216,9 +218,9 @@ __global__ __launch_bounds__(256) void k_hist1(const float* __restrict__ acc, in
                                                uint32_t G, uint32_t* __restrict__ hist1) {
   __shared__ __align__(16) uint32_t h[NB1];
   const uint32_t g = blockIdx.x % G;
-  const uint32_t wb = blockIdx.x / G;   // unit
   uint32_t w, b;
-  U.decode(wb, B.P, &w, &b);
+  U.decode(blockIdx.x / G, B.P, &w, &b);
+  const uint32_t wb = w * B.P + b;   // the block's histogram
   const uint32_t s = B.start(b), e = B.start(b + 1u);
   const uint32_t t0 = s + g * (uint32_t)ADD_TILE;
   if (t0 >= e) return;
@@ -265,7 +267,9 @@ __global__ __launch_bounds__(1024) void k_select1(uint32_t* __restrict__ hist1, 
   constexpr int NT = 1024, PER = NB1 / NT;
   __shared__ uint32_t h[NB1];
   __shared__ uint32_t scratch[24];
-  const int64_t u = blockIdx.x;
+  uint32_t w, b;
+  U.decode(blockIdx.x, B.P, &w, &b);
+  const int64_t u = (int64_t)w * B.P + b;   // the block's arrays
   uint32_t* __restrict__ H = hist1 + u * HCOPIES * NB1;
   uint32_t r[PER][HCOPIES];
 #pragma unroll
@@ -287,8 +291,6 @@ __global__ __launch_bounds__(1024) void k_select1(uint32_t* __restrict__ hist1, 
   __syncthreads();
   uint32_t T, above, cnt, ok, total;
   block_select_desc(h, NB1, need, scratch, &T, &above, &cnt, &ok, &total);
-  uint32_t w, b;
-  U.decode((uint32_t)u, B.P, &w, &b);
   const uint32_t s = B.start(b), e = B.start(b + 1u);
   bool full = FH == 0u;
   if (!ok && !full) {   // the threshold fell below the histogram's floor: count the whole block
@@ -544,10 +546,10 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(8, 8))) voi
                                                  int32_t* __restrict__ cand_idx, float* __restrict__ cand_val,
                                                  uint32_t* __restrict__ bin_key) {
   __shared__ CollectSmem L;
-  const uint32_t unit = blockIdx.x / gq;
   const uint32_t slot0 = (blockIdx.x % gq) * (uint32_t)COLLECT_GROUP;
   uint32_t w, b;
-  U.decode(unit, B.P, &w, &b);
+  U.decode(blockIdx.x / gq, B.P, &w, &b);
+  const uint32_t unit = w * B.P + b;   // the block's arrays
   const uint32_t s = B.start(b), e = B.start(b + 1u);
   if (s + slot0 * (uint32_t)SLOT >= e) return;
   const uint32_t* st = state + (int64_t)unit * ST_WORDS;
@@ -1023,9 +1025,10 @@ __global__ __launch_bounds__(1024) void k_thresh(Blocks B, Units U, int32_t kb, 
   __shared__ ThreshLds S;
   ThreshSmem& L = S.g;
   constexpr int NT = 1024;
-  const int64_t unit = blockIdx.x;
+  const int64_t cunit = blockIdx.x;
+  const SlotGeom g = slot_geom(mode, (uint32_t)cunit, B, U, kb);
+  const int64_t unit = mode == 0 ? (int64_t)U.canon((uint32_t)cunit, B.P) : cunit;   // the unit's arrays
   uint32_t* st = state + unit * ST_WORDS;
-  const SlotGeom g = slot_geom(mode, (uint32_t)unit, B, U, kb);
   const uint32_t* __restrict__ cnt = slot_cnt + unit * smax;
   const uint32_t* __restrict__ nbn = slot_nbin + unit * smax;
   const uint32_t* __restrict__ K = bin_key + g.base;
@@ -1079,6 +1082,8 @@ __global__ __launch_bounds__(1024) void k_thresh(Blocks B, Units U, int32_t kb, 
 // They write exactly what k_thresh writes.
 constexpr int BIG_GROUP0 = 64;   // block top-k: slots per workgroup (a wave per slot in turn)
 
+
+
 // f(key, slot) for every threshold-bin entry of slots [s0, s1): block top-k:
 // the keys the collect stored, a wave per slot; merge: the union entries whose
 // key is in bin T1, the whole workgroup per slot.
@@ -1110,6 +1115,7 @@ __device__ __forceinline__ void visit_bin_slots(const SlotGeom& g, int32_t s0, i
 struct BigArgs {
   Blocks B;
   Units U;
+  int mode;
   int32_t kb, smax, group;   // group: slots per workgroup of the slot-group kernels
   int64_t hstride;           // words of level-1 histogram space per unit
   uint32_t* hist1;
@@ -1121,12 +1127,19 @@ struct BigArgs {
   uint32_t* err;
 };
 
+// where a unit's arrays live: block top-k units at row * P + block (as for
+// k_thresh), merge pairs at their own number
+__device__ __forceinline__ int64_t big_unit(const BigArgs& a, int64_t unit) {
+  return a.mode == 0 ? (int64_t)a.U.canon((uint32_t)unit, a.B.P) : unit;
+}
+
 __global__ __launch_bounds__(1024) void k_big_level1(BigArgs a) {
   __shared__ uint32_t h[NB1];
   __shared__ uint32_t scratch[32];
   constexpr int NT = 1024;
   const int64_t unit = blockIdx.x;
-  uint32_t* H = a.hist1 + unit * a.hstride;
+  const int64_t ua = big_unit(a, unit);
+  uint32_t* H = a.hist1 + ua * a.hstride;
   for (int i = threadIdx.x; i < NB1; i += NT) {
     h[i] = H[i];
     H[i] = 0u;   // histograms rest at zero
@@ -1135,7 +1148,7 @@ __global__ __launch_bounds__(1024) void k_big_level1(BigArgs a) {
   uint32_t T1, above1, cnt1, ok, total;
   block_select_desc(h, NB1, (uint32_t)a.kb, scratch, &T1, &above1, &cnt1, &ok, &total);
   if (threadIdx.x == 0) {
-    uint32_t* st = a.state + unit * ST_WORDS;
+    uint32_t* st = a.state + ua * ST_WORDS;
     if (!ok) atomicOr(a.err, ERR_COUNT);
     st[ST_T1] = T1;
     st[ST_NEED1] = ok ? (uint32_t)a.kb - above1 : 0u;
@@ -1151,8 +1164,9 @@ __global__ __launch_bounds__(256) void k_big_hist(BigArgs a, uint32_t ngroups) {
   constexpr int NB = LEVEL == 2 ? NB2 : NB3;
   __shared__ uint32_t h[NB];
   const int64_t unit = blockIdx.x / ngroups;
+  const int64_t ua = big_unit(a, unit);
   const int32_t grp = (int32_t)(blockIdx.x % ngroups);
-  const uint32_t* st = a.state + unit * ST_WORDS;
+  const uint32_t* st = a.state + ua * ST_WORDS;
   const uint32_t T1 = st[ST_T1];
   if (LEVEL == 2 ? st[ST_NEED1] == st[ST_CNT1] : st[ST_STAGE] != 2u) return;   // uniform: resolved already
   const uint32_t pre23 = st[ST_PRE23];
@@ -1161,13 +1175,13 @@ __global__ __launch_bounds__(256) void k_big_hist(BigArgs a, uint32_t ngroups) {
   if (s0 >= s1) return;
   for (int i = threadIdx.x; i < NB; i += blockDim.x) h[i] = 0u;
   __syncthreads();
-  visit_bin_slots<mode>(g, s0, s1, a.bin_key + g.base, a.U_val + g.base, a.slot_cnt + unit * a.smax,
-                        a.slot_nbin + unit * a.smax, T1, [&](uint32_t key, int32_t) {
+  visit_bin_slots<mode>(g, s0, s1, a.bin_key + g.base, a.U_val + g.base, a.slot_cnt + ua * a.smax,
+                        a.slot_nbin + ua * a.smax, T1, [&](uint32_t key, int32_t) {
                           if (LEVEL == 2) atomicAdd(&h[(key >> D2_SHIFT) & (NB2 - 1)], 1u);
                           else if ((key >> D2_SHIFT) == pre23) atomicAdd(&h[key & (NB3 - 1)], 1u);
                         });
   __syncthreads();
-  uint32_t* H = a.hist1 + unit * a.hstride + (LEVEL == 2 ? 0 : NB2);
+  uint32_t* H = a.hist1 + ua * a.hstride + (LEVEL == 2 ? 0 : NB2);
   for (int i = threadIdx.x; i < NB; i += blockDim.x) {
     const uint32_t c = h[i];
     if (c) atomicAdd(&H[i], c);
@@ -1180,7 +1194,8 @@ __global__ __launch_bounds__(1024) void k_big_select(BigArgs a) {
   __shared__ uint32_t h[NB];
   __shared__ uint32_t scratch[32];
   const int64_t unit = blockIdx.x;
-  uint32_t* st = a.state + unit * ST_WORDS;
+  const int64_t ua = big_unit(a, unit);
+  uint32_t* st = a.state + ua * ST_WORDS;
   const uint32_t T1 = st[ST_T1], need1 = st[ST_NEED1], cnt1 = st[ST_CNT1];
   if (LEVEL == 2 && need1 == cnt1) {   // the whole bin is selected
     if (threadIdx.x == 0) {
@@ -1192,7 +1207,7 @@ __global__ __launch_bounds__(1024) void k_big_select(BigArgs a) {
     return;
   }
   if (LEVEL == 3 && st[ST_STAGE] != 2u) return;
-  uint32_t* H = a.hist1 + unit * a.hstride + (LEVEL == 2 ? 0 : NB2);
+  uint32_t* H = a.hist1 + ua * a.hstride + (LEVEL == 2 ? 0 : NB2);
   for (int i = threadIdx.x; i < NB; i += blockDim.x) {
     h[i] = H[i];
     H[i] = 0u;
@@ -1230,14 +1245,15 @@ template <int mode>
 __global__ __launch_bounds__(256) void k_big_count(BigArgs a, uint32_t ngroups) {
   __shared__ uint32_t part[2 * 4];
   const int64_t unit = blockIdx.x / ngroups;
+  const int64_t ua = big_unit(a, unit);
   const int32_t grp = (int32_t)(blockIdx.x % ngroups);
-  const uint32_t* st = a.state + unit * ST_WORDS;
+  const uint32_t* st = a.state + ua * ST_WORDS;
   const uint32_t T1 = st[ST_T1], tge = st[ST_TGE], teq = st[ST_TEQ], need_eq = st[ST_NEEDEQ];
   const SlotGeom g = slot_geom(mode, (uint32_t)unit, a.B, a.U, a.kb);
   const int32_t s0 = grp * a.group, s1 = min(g.nslots, s0 + a.group);
-  const uint32_t* __restrict__ cnt = a.slot_cnt + unit * a.smax;
-  const uint32_t* __restrict__ nbn = a.slot_nbin + unit * a.smax;
-  const int64_t o = unit * a.smax;
+  const uint32_t* __restrict__ cnt = a.slot_cnt + ua * a.smax;
+  const uint32_t* __restrict__ nbn = a.slot_nbin + ua * a.smax;
+  const int64_t o = ua * a.smax;
   if constexpr (mode == 0) {
     // a wave per slot: the entries above the bin are selected; count the bin's keys
     const int nw = blockDim.x / WAVE;
@@ -1298,12 +1314,13 @@ __global__ __launch_bounds__(1024) void k_big_scan(BigArgs a) {
   __shared__ uint32_t scratch[32];
   constexpr uint32_t NT = 1024;
   const int64_t unit = blockIdx.x;
-  uint32_t* st = a.state + unit * ST_WORDS;
+  const int64_t ua = big_unit(a, unit);
+  uint32_t* st = a.state + ua * ST_WORDS;
   const SlotGeom g = slot_geom(mode, (uint32_t)unit, a.B, a.U, a.kb);
   const uint32_t ns = (uint32_t)g.nslots;
   const uint32_t per = (ns + NT - 1) / NT;
   const uint32_t i0 = min(ns, threadIdx.x * per), i1 = min(ns, i0 + per);
-  const int64_t o = unit * a.smax;
+  const int64_t o = ua * a.smax;
   const uint32_t* __restrict__ cnt = a.slot_cnt + o;
   uint32_t sa = 0, sg = 0, se = 0;
   for (uint32_t i = i0; i < i1; ++i) {
@@ -1364,8 +1381,9 @@ __global__ __launch_bounds__(256) void k_emit(
   if (slot >= g.nslots) return;   // uniform over the workgroup when NPART > 1
   const int lane = lane_id();
   const uint64_t lt = __lanemask_lt();
-  const int64_t si = (int64_t)unit * smax + slot;
-  const uint32_t* st = state + (int64_t)unit * ST_WORDS;
+  const uint32_t au = MODE == 0 ? U.canon(unit, B.P) : unit;   // the unit's arrays
+  const int64_t si = (int64_t)au * smax + slot;
+  const uint32_t* st = state + (int64_t)au * ST_WORDS;
   // independent loads: the slot's count and prefixes, the unit's threshold
   const uint32_t cnt = min(slot_cnt[si], (uint32_t)g.ss);
   const uint32_t all_before = pre_all[si];
@@ -2120,11 +2138,22 @@ __global__ __launch_bounds__(1024) void k_bsag_union(const int32_t* __restrict__
 //               before the first receipt is what stays.
 // Within one step each (receiver, block) has one sender whose indices are
 // distinct, so no two threads touch one element.  Entries outside their block
-// are skipped.  Grid: x over a block's k_blk entries, y over pairs (w, t).
+// are skipped.  With hist1 (receive only), the receiver block's level-1
+// histogram left by the fused add is kept exact -- the old key's bin loses
+// the entry, the new key's bin gains it, both only at or above the add's
+// histogram floor, as deltas gathered in LDS per workgroup and added bin by
+// bin -- and the block is marked in spec_used, since its speculative
+// candidates no longer hold its values.  Grid: x over chunks of a block's
+// k_blk entries (LAZY_CHUNK per workgroup with hist1, else 256 per sweep),
+// y over pairs (w, t).
+constexpr uint32_t LAZY_CHUNK = 4096;
+
 __global__ __launch_bounds__(256) void k_lazy_step(float* __restrict__ acc, int64_t ld_acc, Blocks B, uint32_t kb,
                                                    uint32_t d, uint32_t m, const int32_t* __restrict__ sp_idx,
                                                    const float* __restrict__ sp_val, float* __restrict__ saved,
-                                                   const uint32_t* __restrict__ bm, int restore) {
+                                                   const uint32_t* __restrict__ bm, int restore,
+                                                   uint32_t* __restrict__ hist1, uint32_t* __restrict__ spec_used) {
+  __shared__ uint32_t dh[NB1];   // histogram deltas (receive with hist1)
   const uint32_t npairs = B.P * m;
   for (uint32_t pair = blockIdx.y; pair < npairs; pair += gridDim.y) {
     const uint32_t w = pair / m, t = pair - w * m;
@@ -2132,6 +2161,34 @@ __global__ __launch_bounds__(256) void k_lazy_step(float* __restrict__ acc, int6
     const uint32_t s = B.start(b), e = B.start(b + 1u);
     const int64_t o = ((int64_t)w * B.P + b) * kb;
     float* __restrict__ A = acc + (int64_t)r * ld_acc;
+    if (hist1) {   // uniform
+      const int64_t cu = (int64_t)r * B.P + b;   // the receiver block's arrays
+      const uint32_t FH = hist_floor(spec_used[cu]);
+      const uint32_t j0 = blockIdx.x * LAZY_CHUNK;
+      if (j0 >= kb) continue;
+      if (blockIdx.x == 0 && threadIdx.x == 0) atomicOr(&spec_used[cu], SPEC_DIRTY);
+      for (int i = threadIdx.x; i < NB1; i += 256) dh[i] = 0u;
+      __syncthreads();
+      for (uint32_t j = j0 + threadIdx.x; j < min(kb, j0 + LAZY_CHUNK); j += 256u) {
+        const int32_t x = sp_idx[o + j];
+        if (x < (int32_t)s || x >= (int32_t)e) continue;
+        const float old = A[x];
+        const float nv = old + sp_val[o + j];
+        saved[o + j] = old;
+        A[x] = nv;
+        const uint32_t k0 = mag_key(old), k1 = mag_key(nv);
+        if (k0 >= FH) atomicSub(&dh[k0 >> D1_SHIFT], 1u);
+        if (k1 >= FH) atomicAdd(&dh[k1 >> D1_SHIFT], 1u);
+      }
+      __syncthreads();
+      uint32_t* __restrict__ H = hist1 + (cu * HCOPIES + (blockIdx.x % HCOPIES)) * NB1;
+      for (int i = threadIdx.x; i < NB1; i += 256) {
+        const uint32_t c = dh[i];   // a signed delta, added modulo 2^32
+        if (c) atomicAdd(&H[i], c);
+      }
+      __syncthreads();   // dh is cleared for the next pair
+      continue;
+    }
     for (uint32_t j = blockIdx.x * 256u + threadIdx.x; j < kb; j += gridDim.x * 256u) {
       const int32_t x = sp_idx[o + j];
       if (x < (int32_t)s || x >= (int32_t)e) continue;
@@ -2224,6 +2281,7 @@ hipError_t launch_thresh(int mode, int64_t nunits, const Units& U, int64_t n, in
     BigArgs a;
     a.B = make_blocks(n, P);
     a.U = U;
+    a.mode = mode;
     a.kb = kb;
     a.smax = smax;
     a.group = mode == 0 ? BIG_GROUP0 : 1;
@@ -2377,10 +2435,11 @@ hipError_t launch_bsag_exchange(const BsagArgs& a, hipStream_t s) {
 
 hipError_t launch_lazy_step(float* acc, int64_t ld_acc, int32_t P, int64_t n, int32_t kb, int32_t d, int32_t m,
                             const int32_t* sp_idx, const float* sp_val, float* saved, const uint32_t* bm,
-                            bool restore, hipStream_t s) {
-  const dim3 grid(grid_for(kb, 256, 1024), (unsigned)std::min<int64_t>((int64_t)P * m, 65535));
+                            bool restore, uint32_t* hist1, uint32_t* spec_used, hipStream_t s) {
+  const unsigned gx = hist1 ? (unsigned)((kb + LAZY_CHUNK - 1) / LAZY_CHUNK) : grid_for(kb, 256, 1024);
+  const dim3 grid(gx, (unsigned)std::min<int64_t>((int64_t)P * m, 65535));
   hipLaunchKernelGGL(k_lazy_step, grid, dim3(256), 0, s, acc, ld_acc, make_blocks(n, P), (uint32_t)kb, (uint32_t)d,
-                     (uint32_t)m, sp_idx, sp_val, saved, bm, restore ? 1 : 0);
+                     (uint32_t)m, sp_idx, sp_val, saved, bm, restore ? 1 : 0, hist1, spec_used);
   return hipGetLastError();
 }
 

@@ -91,7 +91,7 @@ hipError_t launch_bsag_init(int32_t Q, double h0, double step0, double* H, doubl
 hipError_t launch_bsag_exchange(const BsagArgs& a, hipStream_t s);
 hipError_t launch_lazy_step(float* acc, int64_t ld_acc, int32_t P, int64_t n, int32_t kb, int32_t d, int32_t m,
                             const int32_t* sp_idx, const float* sp_val, float* saved, const uint32_t* bm,
-                            bool restore, hipStream_t s);
+                            bool restore, uint32_t* hist1, uint32_t* spec_used, hipStream_t s);
 hipError_t launch_grc_drops(float* acc, int64_t ld_acc, int64_t n, int32_t m, int32_t kb, int32_t npairs,
                             const int32_t* drop_idx, const float* drop_val, const int32_t* drop_cnt,
                             const uint32_t* bm, hipStream_t s);

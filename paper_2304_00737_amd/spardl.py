@@ -42,8 +42,8 @@ _lib.spardl_block_topk.argtypes = [_p, _i64, _i32, _i64, _i32, _i32, _i32, _p, _
 _lib.spardl_sparse_merge_topk.argtypes = [_p, _p, _i32, _i64, _i32, _i32, _p, _p, _p, _p, _sz, _p]
 _lib.spardl_allgather_densify.argtypes = [_p, _p, _i32, _i64, _i32, _p, _p, _p]
 _lib.spardl_residual_collect.argtypes = [_p, _i64, _i32, _i64, _i32, _p, _p, _p, _p, _p, _p, _p, _sz, _p]
-_lib.spardl_lazy_topk.argtypes = [_p, _i64, _i32, _i32, _i64, _i32, _i32, _i32, _p, _p, _p, _sz, _p]
-_lib.spardl_lazy_receive.argtypes = [_p, _i64, _i32, _i64, _i32, _i32, _p, _p, _p, _p]
+_lib.spardl_lazy_topk.argtypes = [_p, _i64, _i32, _i32, _i64, _i32, _i32, _i32, _i32, _p, _p, _p, _sz, _p]
+_lib.spardl_lazy_receive.argtypes = [_p, _i64, _i32, _i64, _i32, _i32, _p, _p, _p, _p, _sz, _p]
 _lib.spardl_lazy_residual_collect.argtypes = [_p, _i64, _i32, _i64, _i32, _p, _p, _p, _p]
 _lib.spardl_rsag_workspace_bytes.argtypes = [_i32, _i32, _i64, _i32]
 _lib.spardl_rsag_workspace_bytes.restype = _sz
@@ -170,20 +170,23 @@ def residual_collect(acc, P: int, n: int, k_blk: int, local_idx, sp_idx, drop_id
         arr(drop_val), arr(drop_cnt), _ptr(ws), ws_bytes, _stream(stream)))
 
 
-def lazy_topk(acc, w0: int, nworkers: int, n: int, P: int, k_blk: int, round: int, sp_idx, sp_val, ws, *,
-              ld_acc=None, stream=None) -> None:
+def lazy_topk(acc, w0: int, nworkers: int, n: int, P: int, k_blk: int, round: int, sp_idx, sp_val, ws,
+              flags: int = 0, *, ld_acc=None, stream=None) -> None:
     """acc: rows w0 .. w0 + nworkers - 1; sp_idx/sp_val: sp[w0:w0 + nworkers]."""
     ld_acc = _ld(acc, n) if ld_acc is None else ld_acc
-    _check("lazy_topk", _lib.spardl_lazy_topk(_ptr(acc), ld_acc, w0, nworkers, n, P, k_blk, round, _ptr(sp_idx),
-                                              _ptr(sp_val), _ptr(ws), ws.numel() * ws.element_size(),
+    _check("lazy_topk", _lib.spardl_lazy_topk(_ptr(acc), ld_acc, w0, nworkers, n, P, k_blk, round, flags,
+                                              _ptr(sp_idx), _ptr(sp_val), _ptr(ws), ws.numel() * ws.element_size(),
                                               _stream(stream)))
 
 
-def lazy_receive(acc, P: int, n: int, k_blk: int, round: int, sp_idx, sp_val, saved, *, ld_acc=None,
+def lazy_receive(acc, P: int, n: int, k_blk: int, round: int, sp_idx, sp_val, saved, ws=None, *, ld_acc=None,
                  stream=None) -> None:
+    """ws: the fused form's workspace (keeps the add's histograms exact), or None."""
     ld_acc = _ld(acc, n) if ld_acc is None else ld_acc
+    ws_bytes = 0 if ws is None else ws.numel() * ws.element_size()
     _check("lazy_receive", _lib.spardl_lazy_receive(_ptr(acc), ld_acc, P, n, k_blk, round, _ptr(sp_idx),
-                                                    _ptr(sp_val), _ptr(saved), _stream(stream)))
+                                                    _ptr(sp_val), _ptr(saved), _ptr(ws), ws_bytes,
+                                                    _stream(stream)))
 
 
 def lazy_residual_collect(acc, P: int, n: int, k_blk: int, sp_idx, member, saved, *, ld_acc=None,
@@ -348,9 +351,13 @@ class SparDLLazyStep:
     block b (final block b in sp[b, b]), saved what the receipts overwrote.
     """
 
-    def __init__(self, P: int, n: int, k_blk: int, device="cuda", rows_per_call: int = 0):
+    def __init__(self, P: int, n: int, k_blk: int, device="cuda", rows_per_call: int = 0, fused: bool = True):
+        """fused: the add prepares every block's selection and the receipts keep
+        it exact (needs all P rows in one workspace, so rows_per_call < P
+        runs the plain form)."""
         self.P, self.n, self.k_blk = P, n, k_blk
         self.rows = P if rows_per_call <= 0 else min(rows_per_call, P)
+        self.fused = fused and self.rows == P
         dev = torch.device(device)
         self.acc = torch.zeros((P, n), dtype=torch.float32, device=dev)
         self.sp_idx = torch.empty((P, P, k_blk), dtype=torch.int32, device=dev)
@@ -363,18 +370,25 @@ class SparDLLazyStep:
 
     def residual_add_rows(self, w0: int, grad_rows, stream=None):
         r = grad_rows.shape[0]
-        residual_add(self.acc[w0:w0 + r], grad_rows, r, self.n, 0, None, stream=stream)
+        if self.fused:
+            if w0 != 0 or r != self.P:
+                raise ValueError("the fused lazy step adds all P rows in one call")
+            residual_add(self.acc, grad_rows, r, self.n, self.P, self.ws, self.k_blk, stream=stream)
+        else:
+            residual_add(self.acc[w0:w0 + r], grad_rows, r, self.n, 0, None, stream=stream)
 
     def topk_round(self, i: int, stream=None):
         """Every worker's selection for step i (0: the reserved blocks)."""
+        flags = TOPK_HIST_READY if self.fused else 0
         for w0 in range(0, self.P, self.rows):
             r = min(self.rows, self.P - w0)
             s = slice(w0, w0 + r)
             lazy_topk(self.acc[s], w0, r, self.n, self.P, self.k_blk, i, self.sp_idx[s], self.sp_val[s], self.ws,
-                      stream=stream)
+                      flags, stream=stream)
 
     def receive(self, i: int, stream=None):
-        lazy_receive(self.acc, self.P, self.n, self.k_blk, i, self.sp_idx, self.sp_val, self.saved, stream=stream)
+        lazy_receive(self.acc, self.P, self.n, self.k_blk, i, self.sp_idx, self.sp_val, self.saved,
+                     self.ws if self.fused else None, stream=stream)
 
     def densify(self, stream=None):
         allgather_densify(self.sp_idx, self.sp_val, self.P, self.n, self.k_blk, self.dense, self.member,

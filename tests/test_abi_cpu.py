@@ -145,8 +145,8 @@ def test_argument_errors_enqueue_nothing():
                                        ok3, ok3, ok3, null, sz(0), null) == EINVAL
     # lazy_topk (P = 4, l = 2): round outside [0, l], rows outside [0, P), ld < n, small or misaligned ws
     big = sz(1 << 30)
-    lt = lambda ld, w0, nw, rnd, ws, wsz: lib.spardl_lazy_topk(p, i64(ld), i32(w0), i32(nw), i64(100), i32(4),
-                                                               i32(3), i32(rnd), p, p, ws, wsz, null)
+    lt = lambda ld, w0, nw, rnd, ws, wsz, fl=0: lib.spardl_lazy_topk(p, i64(ld), i32(w0), i32(nw), i64(100), i32(4),
+                                                                     i32(3), i32(rnd), i32(fl), p, p, ws, wsz, null)
     assert lt(100, 0, 1, 3, p, big) == EINVAL
     assert lt(100, 0, 1, -1, p, big) == EINVAL
     assert lt(100, 3, 2, 1, p, big) == EINVAL
@@ -156,11 +156,17 @@ def test_argument_errors_enqueue_nothing():
     assert lt(100, 0, 1, 1, q, big) == EINVAL
     assert lt(100, 0, 1, 1, null, big) == EINVAL
     assert lt(100, 0, 1, 1, p, sz(64)) == ECAP
+    assert lt(100, 0, 4, 1, p, big, 2) == EINVAL        # unknown flag
+    assert lt(100, 1, 2, 1, p, big, 1) == EINVAL        # fused form on a row subset
     # lazy_receive: P = 1 has no steps; round outside [1, l]; NULL saved
-    assert lib.spardl_lazy_receive(p, i64(100), i32(1), i64(100), i32(3), i32(1), p, p, p, null) == EINVAL
-    assert lib.spardl_lazy_receive(p, i64(100), i32(4), i64(100), i32(3), i32(0), p, p, p, null) == EINVAL
-    assert lib.spardl_lazy_receive(p, i64(100), i32(4), i64(100), i32(3), i32(3), p, p, p, null) == EINVAL
-    assert lib.spardl_lazy_receive(p, i64(100), i32(4), i64(100), i32(3), i32(1), p, p, null, null) == EINVAL
+    lr = lambda P_, rnd, saved, ws, wsz: lib.spardl_lazy_receive(p, i64(100), i32(P_), i64(100), i32(3), i32(rnd), p,
+                                                                 p, saved, ws, wsz, null)
+    assert lr(1, 1, p, null, sz(0)) == EINVAL
+    assert lr(4, 0, p, null, sz(0)) == EINVAL
+    assert lr(4, 3, p, null, sz(0)) == EINVAL
+    assert lr(4, 1, null, null, sz(0)) == EINVAL
+    assert lr(4, 1, p, q, big) == EINVAL                # misaligned workspace
+    assert lr(4, 1, p, p, sz(64)) == ECAP               # workspace too small for the histograms
     # lazy_residual_collect: NULL or misaligned member, NULL saved with P > 1, k_blk too large
     assert lib.spardl_lazy_residual_collect(p, i64(100), i32(4), i64(100), i32(3), p, null, p, null) == EINVAL
     assert lib.spardl_lazy_residual_collect(p, i64(100), i32(4), i64(100), i32(3), p, ctypes.c_void_p(0x1002), p,

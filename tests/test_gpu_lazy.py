@@ -24,8 +24,8 @@ def _dev(a):
     return torch.from_numpy(np.ascontiguousarray(a)).cuda()
 
 
-def _run(P, n, kb, kind, steps, rows=0, seed=0):
-    st = spardl.SparDLLazyStep(P, n, kb, rows_per_call=rows)
+def _run(P, n, kb, kind, steps, rows=0, seed=0, fused=True):
+    st = spardl.SparDLLazyStep(P, n, kb, rows_per_call=rows, fused=fused)
     acc = np.zeros((P, n), np.float32)
     for t in range(steps):
         grad = W.small_rows(kind, P, n, 100 * t + P + seed)
@@ -37,8 +37,16 @@ def _run(P, n, kb, kind, steps, rows=0, seed=0):
 
 @pytest.mark.parametrize("P,n,kb,kind,steps", STEP_CASES)
 def test_lazy_step(P, n, kb, kind, steps):
+    """Fused form: the add's histograms, kept exact through the receipts."""
     log(f"lazy step P={P} n={n} kb={kb} kind={kind} steps={steps}")
-    _run(P, n, kb, kind, steps)
+    _run(P, n, kb, kind, steps + 1)
+
+
+@pytest.mark.parametrize("P,n,kb,kind,steps", [STEP_CASES[i] for i in (1, 4, 6, 7, 10)])
+def test_lazy_step_plain(P, n, kb, kind, steps):
+    """Plain form: plain add, every selection counts its blocks itself."""
+    log(f"lazy step (plain) P={P} n={n} kb={kb} kind={kind} steps={steps}")
+    _run(P, n, kb, kind, steps, seed=3, fused=False)
 
 
 @pytest.mark.parametrize("P,n,kb,rows", [(8, 50000, 100, 1), (7, 70001, 501, 3), (5, 10007, 3, 2)])
