@@ -286,6 +286,38 @@ int spardl_lazy_residual_collect(float* acc, int64_t ld_acc, int32_t P, int64_t 
  * array (row w = worker w, Q blocks per row).
  * ------------------------------------------------------------------------- */
 
+/* All d teams in one call (the same results as the calls above team by team,
+ * with fewer and larger launches): a workspace for P rows of Q = P / d blocks,
+ * 256-byte aligned, spardl_team_workspace_bytes(P, d, n, k_blk) bytes,
+ * prepared once by spardl_team_workspace_init.  0 on invalid sizes: P < 1,
+ * d < 1, d not dividing P, n < Q, n >= 2^31, k_blk outside [1, floor(n/Q)]. */
+size_t spardl_team_workspace_bytes(int32_t P, int32_t d, int64_t n, int32_t k_blk);
+int spardl_team_workspace_init(int32_t P, int32_t d, int64_t n, int32_t k_blk, void* ws, size_t ws_bytes,
+                               hipStream_t stream);
+
+/* spardl_residual_add (with the workspace) for all P rows, blocks of the
+ * team's Q-block partition.  Errors: EINVAL for NULL pointers, misaligned
+ * ws, invalid sizes, ld < n; ECAPACITY if ws is too small. */
+int spardl_team_residual_add(float* acc, int64_t ld_acc, const float* grad, int64_t ld_grad, int32_t P, int32_t d,
+                             int64_t n, int32_t k_blk, void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* spardl_block_topk for all P rows, Q blocks each: sp_idx/sp_val/local_idx
+ * [(w*Q + b)*k_blk + j].  flags: 0 or SPARDL_TOPK_HIST_READY (after
+ * spardl_team_residual_add with the same workspace).  Errors as for
+ * spardl_team_residual_add, plus unknown flags. */
+int spardl_team_block_topk(const float* acc, int64_t ld_acc, int32_t P, int32_t d, int64_t n, int32_t k_blk,
+                           int32_t flags, int32_t* sp_idx, float* sp_val, int32_t* local_idx, void* ws,
+                           size_t ws_bytes, hipStream_t stream);
+
+/* spardl_sparse_merge_topk step `round` in [1, ceil(log2 Q)] inside every
+ * team at once: pair (tau Q + w)*m + t merges block (w + t) mod Q of row
+ * tau Q + w with that block of row tau Q + (w - 2^(l-round)) mod Q; drops at
+ * drop_idx/drop_val[((tau Q + w)*m + t)*k_blk + j], j < drop_cnt[...].
+ * Errors as for spardl_team_residual_add, plus round out of range. */
+int spardl_team_merge_topk(int32_t* sp_idx, float* sp_val, int32_t P, int32_t d, int64_t n, int32_t k_blk,
+                           int32_t round, int32_t* drop_idx, float* drop_val, int32_t* drop_cnt, void* ws,
+                           size_t ws_bytes, hipStream_t stream);
+
 /* Workspace of spardl_rsag_merge_topk (separate from the teams' workspaces):
  * 256-byte aligned device memory of this many bytes, prepared once by
  * spardl_rsag_workspace_init (it rests at zero between calls, except the

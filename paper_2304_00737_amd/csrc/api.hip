@@ -43,17 +43,20 @@ struct Layout {
   int64_t units = 0, tiles_tk = 0, tiles_mg = 0, slot_n = 0, pairs_max = 0, add_tiles = 0;
 };
 
-Layout make_layout(int32_t P, int64_t n, int32_t kb) {
+// rows: rows of acc the calls cover (P, or all d teams' rows with P = Q
+// blocks per row); everything scales with rows x blocks.
+Layout make_layout(int32_t P, int64_t n, int32_t kb, int32_t rows = 0) {
   Layout L;
+  if (rows <= 0) rows = P;
   const int32_t l = steps_of(P);
   int64_t mmax = 0;   // largest bag over the steps (step 1 is not always the largest)
   for (int32_t i = 1; i <= l; ++i) mmax = std::max<int64_t>(mmax, bag_of(P, l, i));
   const int64_t maxlen = ceil_div(n, P);
-  L.pairs_max = (int64_t)P * mmax;
-  L.units = std::max<int64_t>((int64_t)P * P, L.pairs_max);
+  L.pairs_max = (int64_t)rows * mmax;
+  L.units = std::max<int64_t>((int64_t)rows * P, L.pairs_max);
   L.tiles_tk = ceil_div(maxlen, SLOT);
   L.tiles_mg = ceil_div(2ll * kb, MERGE_TILE);
-  L.slot_n = std::max<int64_t>((int64_t)P * P * L.tiles_tk, L.pairs_max * L.tiles_mg);
+  L.slot_n = std::max<int64_t>((int64_t)rows * P * L.tiles_tk, L.pairs_max * L.tiles_mg);
   size_t off = 256;
   L.bitmap = off;
   off += align256((size_t)ceil_div(n, 32) * 4);
@@ -63,11 +66,11 @@ Layout make_layout(int32_t P, int64_t n, int32_t kb) {
   // previous threshold bin + 1 (0: none) and the floor used; per add tile the count
   L.add_tiles = ceil_div(maxlen, ADD_TILE);
   L.spec_t1 = off;
-  off += align256((size_t)P * P * 4);
+  off += align256((size_t)rows * P * 4);
   L.spec_used = off;
-  off += align256((size_t)P * P * 4);
+  off += align256((size_t)rows * P * 4);
   L.spec_cnt = off;   // per add tile
-  off += align256((size_t)P * P * L.add_tiles * 4);
+  off += align256((size_t)rows * P * L.add_tiles * 4);
   L.state = off;
   off += align256((size_t)L.units * ST_WORDS * 4);
   L.slot_cnt = off;
@@ -267,6 +270,19 @@ int topk_units(const float* acc, int64_t ld_acc, int64_t units, const Units& U, 
   SPARDL_TRY(launch_emit(0, w.cand_idx, w.cand_val, units, U, n, P, k_blk, Pairs{}, smax, w.state, w.slot_cnt,
                          w.pre_all, w.pre_ge, w.pre_eq, sp_idx, sp_val, local_idx, nullptr, nullptr, w.err, stream));
   return SPARDL_OK;
+}
+
+// ---- all d teams in one call: P rows, Q = P / d blocks per row, SRS inside
+// each team on its own rows (the d = 1 calls above with rows = blocks = Q
+// give the same results team by team).
+bool team_sizes_ok(int32_t P, int32_t d, int64_t n, int32_t kb) {
+  return P >= 1 && d >= 1 && P % d == 0 && sizes_ok(P / d, n, kb);
+}
+size_t team_ws_bytes(int32_t P, int32_t d, int64_t n, int32_t kb) {
+  const int32_t Q = P / d;
+  const Layout L = make_layout(Q, n, kb, P);
+  const int64_t cand = std::max<int64_t>((int64_t)P * n, L.pairs_max * L.tiles_mg * MERGE_TILE);
+  return L.fixed_end + cand_bytes(cand);
 }
 
 }  // namespace
@@ -621,6 +637,90 @@ int spardl_bsag_residual(float* acc, int64_t ld_acc, int32_t P, int32_t d, int64
     return SPARDL_EINVAL;
   // worker w's top-h drops: pairs of one entry each (m = 1), pair w = row w
   SPARDL_TRY(launch_grc_drops(acc, ld_acc, n, 1, k_blk, P, drop_idx, drop_val, drop_cnt, member, stream));
+  return SPARDL_OK;
+}
+
+size_t spardl_team_workspace_bytes(int32_t P, int32_t d, int64_t n, int32_t k_blk) {
+  if (!team_sizes_ok(P, d, n, k_blk)) return 0;
+  return team_ws_bytes(P, d, n, k_blk);
+}
+
+int spardl_team_workspace_init(int32_t P, int32_t d, int64_t n, int32_t k_blk, void* ws, size_t ws_bytes,
+                               hipStream_t stream) {
+  if (!ws || ws_misaligned(ws) || !team_sizes_ok(P, d, n, k_blk)) return SPARDL_EINVAL;
+  if (ws_bytes < team_ws_bytes(P, d, n, k_blk)) return SPARDL_ECAPACITY;
+  const int32_t Q = P / d;
+  const Layout L = make_layout(Q, n, k_blk, P);
+  Ws w = carve(ws, ws_bytes, L);
+  SPARDL_TRY(launch_fill(Fill()
+                             .add(w.err, 64)
+                             .add(w.bitmap, ceil_div(n, 32))
+                             .add(w.hist1, L.units * HCOPIES * NB1)
+                             .add(w.spec_t1, (int64_t)P * Q)
+                             .r,
+                         stream));
+  return SPARDL_OK;
+}
+
+int spardl_team_residual_add(float* acc, int64_t ld_acc, const float* grad, int64_t ld_grad, int32_t P, int32_t d,
+                             int64_t n, int32_t k_blk, void* ws, size_t ws_bytes, hipStream_t stream) {
+  if (!acc || !grad || !ws || ws_misaligned(ws) || !team_sizes_ok(P, d, n, k_blk) || ld_acc < n || ld_grad < n)
+    return SPARDL_EINVAL;
+  if (ws_bytes < team_ws_bytes(P, d, n, k_blk)) return SPARDL_ECAPACITY;
+  const int32_t Q = P / d;
+  const Layout L = make_layout(Q, n, k_blk, P);
+  Ws w = carve(ws, ws_bytes, L);
+  const bool v4 = aligned16(acc) && aligned16(grad) && ld_acc % 4 == 0 && ld_grad % 4 == 0 && blocks_vec4(n, Q);
+  AddSpec sp;
+  sp.hist1 = w.hist1;
+  sp.spec_t1 = w.spec_t1;
+  sp.spec_used = w.spec_used;
+  sp.spec_cnt = w.spec_cnt;
+  sp.cand_idx = w.cand_idx;
+  sp.cand_val = w.cand_val;
+  SPARDL_TRY(launch_residual_add(acc, ld_acc, grad, ld_grad, P, n, Q, v4, sp, stream));
+  return SPARDL_OK;
+}
+
+int spardl_team_block_topk(const float* acc, int64_t ld_acc, int32_t P, int32_t d, int64_t n, int32_t k_blk,
+                           int32_t flags, int32_t* sp_idx, float* sp_val, int32_t* local_idx, void* ws,
+                           size_t ws_bytes, hipStream_t stream) {
+  if (!acc || !sp_idx || !sp_val || !ws || ws_misaligned(ws) || !team_sizes_ok(P, d, n, k_blk) || ld_acc < n ||
+      (flags & ~SPARDL_TOPK_HIST_READY))
+    return SPARDL_EINVAL;
+  if (ws_bytes < team_ws_bytes(P, d, n, k_blk)) return SPARDL_ECAPACITY;
+  const int32_t Q = P / d;
+  const Layout L = make_layout(Q, n, k_blk, P);
+  Ws w = carve(ws, ws_bytes, L);
+  const bool spec = (flags & SPARDL_TOPK_HIST_READY) != 0;
+  return topk_units(acc, ld_acc, (int64_t)P * Q, all_blocks(Q), n, Q, k_blk, !spec, spec, sp_idx, sp_val, local_idx,
+                    w, L, stream);
+}
+
+int spardl_team_merge_topk(int32_t* sp_idx, float* sp_val, int32_t P, int32_t d, int64_t n, int32_t k_blk,
+                           int32_t round, int32_t* drop_idx, float* drop_val, int32_t* drop_cnt, void* ws,
+                           size_t ws_bytes, hipStream_t stream) {
+  if (!sp_idx || !sp_val || !drop_idx || !drop_val || !drop_cnt || !ws || ws_misaligned(ws) ||
+      !team_sizes_ok(P, d, n, k_blk))
+    return SPARDL_EINVAL;
+  const int32_t Q = P / d;
+  const int32_t l = steps_of(Q);
+  if (round < 1 || round > l) return SPARDL_EINVAL;
+  if (ws_bytes < team_ws_bytes(P, d, n, k_blk)) return SPARDL_ECAPACITY;
+  const Layout L = make_layout(Q, n, k_blk, P);
+  Ws w = carve(ws, ws_bytes, L);
+  const int32_t dist = 1 << (l - round);
+  const int32_t m = bag_of(Q, l, round);
+  const int64_t pairs = (int64_t)P * m;
+  const int32_t smax = (int32_t)L.tiles_mg;
+  const Pairs PM = team_srs_pairs(Q, m, dist);
+  SPARDL_TRY(launch_merge(sp_idx, sp_val, PM, pairs, k_blk, smax, w.hist1, w.slot_cnt, w.cand_idx, w.cand_val,
+                          stream));
+  SPARDL_TRY(launch_thresh(1, pairs, all_blocks(Q), n, Q, k_blk, smax, w.hist1, w.cand_val, w.state, w.slot_cnt,
+                           w.slot_nbin, w.bin_key, w.pre_all, w.pre_ge, w.pre_eq, drop_cnt, w.err, stream));
+  SPARDL_TRY(launch_emit(1, w.cand_idx, w.cand_val, pairs, all_blocks(Q), n, Q, k_blk, PM, smax, w.state,
+                         w.slot_cnt, w.pre_all, w.pre_ge, w.pre_eq, sp_idx, sp_val, nullptr, drop_idx, drop_val,
+                         w.err, stream));
   return SPARDL_OK;
 }
 

@@ -118,14 +118,19 @@ inline Units all_blocks(int32_t P) { return Units{(uint32_t)P, 0u, 0u, 0u}; }
 //  R-SAG exchange t (kind 1, nb = Q): pair p = (j, q); team X = j with a 0
 //    bit inserted at bit t, team Y = X + 2^t; held = sp[X Q + q][q],
 //    received = sp[Y Q + q][q], and both keep the result.
+//  SRS step of every team at once (kind 2, nb = Q workers per team): pair
+//    p = tau Q m + (w, t) is the kind-0 pair (w, t) of team tau, on the
+//    team's rows tau Q .. tau Q + Q - 1.
 struct Pairs {
   uint32_t kind, nb, m, dist, t;
   __device__ __forceinline__ void decode(uint32_t p, int64_t* held, int64_t* recv, bool* both) const {
-    if (kind == 0u) {
+    if (kind != 1u) {
+      const uint32_t team = kind == 2u ? p / (nb * m) : 0u;
+      p -= team * nb * m;
       const uint32_t w = p / m, tt = p - w * m;
       const uint32_t b = (w + tt) % nb, src = (w + nb - dist) % nb;
-      *held = (int64_t)w * nb + b;
-      *recv = (int64_t)src * nb + b;
+      *held = (int64_t)(team * nb + w) * nb + b;
+      *recv = (int64_t)(team * nb + src) * nb + b;
       *both = false;
     } else {
       const uint32_t j = p / nb, q = p - j * nb;
@@ -142,6 +147,9 @@ inline Pairs srs_pairs(int32_t P, int32_t m, int32_t dist) {
   return Pairs{0u, (uint32_t)P, (uint32_t)m, (uint32_t)dist, 0u};
 }
 inline Pairs rsag_pairs(int32_t Q, int32_t t) { return Pairs{1u, (uint32_t)Q, 0u, 0u, (uint32_t)t}; }
+inline Pairs team_srs_pairs(int32_t Q, int32_t m, int32_t dist) {
+  return Pairs{2u, (uint32_t)Q, (uint32_t)m, (uint32_t)dist, 0u};
+}
 
 __device__ __forceinline__ int lane_id() { return threadIdx.x & (WAVE - 1); }
 __device__ __forceinline__ int wave_id() { return threadIdx.x / WAVE; }

@@ -50,6 +50,12 @@ _lib.spardl_rsag_workspace_bytes.restype = _sz
 _lib.spardl_rsag_workspace_init.argtypes = [_i32, _i32, _i64, _i32, _p, _sz, _p]
 _lib.spardl_rsag_merge_topk.argtypes = [_p, _p, _i32, _i32, _i64, _i32, _i32, _p, _p, _p, _p, _sz, _p]
 _lib.spardl_rsag_residual.argtypes = [_p, _i64, _i32, _i32, _i64, _i32, _p, _p, _p, _p, _p]
+_lib.spardl_team_workspace_bytes.argtypes = [_i32, _i32, _i64, _i32]
+_lib.spardl_team_workspace_bytes.restype = _sz
+_lib.spardl_team_workspace_init.argtypes = [_i32, _i32, _i64, _i32, _p, _sz, _p]
+_lib.spardl_team_residual_add.argtypes = [_p, _i64, _p, _i64, _i32, _i32, _i64, _i32, _p, _sz, _p]
+_lib.spardl_team_block_topk.argtypes = [_p, _i64, _i32, _i32, _i64, _i32, _i32, _p, _p, _p, _p, _sz, _p]
+_lib.spardl_team_merge_topk.argtypes = [_p, _p, _i32, _i32, _i64, _i32, _i32, _p, _p, _p, _p, _sz, _p]
 _lib.spardl_bsag_workspace_bytes.argtypes = [_i32, _i32, _i64, _i32]
 _lib.spardl_bsag_workspace_bytes.restype = _sz
 _lib.spardl_bsag_workspace_init.argtypes = [_i32, _i32, _i64, _i32, _p, _sz, _p]
@@ -57,7 +63,8 @@ _lib.spardl_bsag_exchange.argtypes = [_p, _p, _i32, _i32, _i64, _i32, _p, _p, _p
 _lib.spardl_bsag_residual.argtypes = [_p, _i64, _i32, _i32, _i64, _i32, _p, _p, _p, _p, _p]
 for _f in ("residual_add", "block_topk", "sparse_merge_topk", "allgather_densify", "residual_collect",
            "lazy_topk", "lazy_receive", "lazy_residual_collect", "rsag_workspace_init", "rsag_merge_topk",
-           "rsag_residual", "bsag_workspace_init", "bsag_exchange", "bsag_residual"):
+           "rsag_residual", "bsag_workspace_init", "bsag_exchange", "bsag_residual", "team_workspace_init",
+           "team_residual_add", "team_block_topk", "team_merge_topk"):
     getattr(_lib, "spardl_" + _f).restype = ctypes.c_int
 
 
@@ -222,6 +229,39 @@ def rsag_residual(acc, P: int, d: int, n: int, k_blk: int, member, drop_idx, dro
     _check("rsag_residual", _lib.spardl_rsag_residual(_ptr(acc), ld_acc, P, d, n, k_blk, _ptr(member),
                                                       arr(drop_idx), arr(drop_val), arr(drop_cnt),
                                                       _stream(stream)))
+
+
+def team_workspace(P: int, d: int, n: int, k_blk: int, device="cuda", *, stream=None):
+    """A prepared workspace for the team calls (all d teams at once)."""
+    nbytes = int(_lib.spardl_team_workspace_bytes(P, d, n, k_blk))
+    if nbytes == 0:
+        raise SpardlError("team_workspace_bytes", EINVAL)
+    ws = torch.empty(nbytes, dtype=torch.uint8, device=device)
+    _check("team_workspace_init", _lib.spardl_team_workspace_init(P, d, n, k_blk, _ptr(ws), nbytes, _stream(stream)))
+    return ws
+
+
+def _nb(ws) -> int:
+    return ws.numel() * ws.element_size()
+
+
+def team_residual_add(acc, grad, P: int, d: int, n: int, k_blk: int, ws, *, stream=None) -> None:
+    _check("team_residual_add", _lib.spardl_team_residual_add(_ptr(acc), _ld(acc, n), _ptr(grad), _ld(grad, n), P, d,
+                                                              n, k_blk, _ptr(ws), _nb(ws), _stream(stream)))
+
+
+def team_block_topk(acc, P: int, d: int, n: int, k_blk: int, sp_idx, sp_val, local_idx, ws, flags: int = 0, *,
+                    stream=None) -> None:
+    _check("team_block_topk", _lib.spardl_team_block_topk(_ptr(acc), _ld(acc, n), P, d, n, k_blk, flags,
+                                                          _ptr(sp_idx), _ptr(sp_val), _ptr(local_idx), _ptr(ws),
+                                                          _nb(ws), _stream(stream)))
+
+
+def team_merge_topk(sp_idx, sp_val, P: int, d: int, n: int, k_blk: int, round: int, drop_idx, drop_val, drop_cnt,
+                    ws, *, stream=None) -> None:
+    _check("team_merge_topk", _lib.spardl_team_merge_topk(_ptr(sp_idx), _ptr(sp_val), P, d, n, k_blk, round,
+                                                          _ptr(drop_idx), _ptr(drop_val), _ptr(drop_cnt), _ptr(ws),
+                                                          _nb(ws), _stream(stream)))
 
 
 def bsag_workspace(P: int, d: int, n: int, k_blk: int, device="cuda", *, stream=None):
@@ -424,11 +464,14 @@ class SparDLSagStep:
     team; sag_*[t][p] what pair p dropped at exchange t.
     """
 
-    def __init__(self, P: int, d: int, n: int, k_blk: int, device="cuda", fused: bool = True, bruck: bool = False):
+    def __init__(self, P: int, d: int, n: int, k_blk: int, device="cuda", fused: bool = True, bruck: bool = False,
+                 batched: bool = True):
+        """batched: the teams' add, top-k and SRS steps in one call each over
+        all P rows (otherwise team by team, each with its own workspace)."""
         if d < 2 or P % d or (not bruck and d & (d - 1)):
             raise ValueError("d >= 2 must divide P (and be a power of two for R-SAG)")
         self.P, self.d, self.Q, self.n, self.k_blk, self.fused = P, d, P // d, n, k_blk, fused
-        self.bruck = bruck
+        self.bruck, self.batched = bruck, batched
         Q = self.Q
         dev = torch.device(device)
         self.acc = torch.zeros((P, n), dtype=torch.float32, device=dev)
@@ -441,7 +484,11 @@ class SparDLSagStep:
         self.drop_cnt = [torch.empty((P, m), dtype=torch.int32, device=dev) for m in self.bags]
         self.dense = torch.empty(n, dtype=torch.float32, device=dev)
         self.member = torch.empty(member_words(n), dtype=torch.int32, device=dev)
-        self.ws_team = [workspace(Q, Q, n, k_blk, device=dev) for _ in range(d)]
+        if batched:
+            self.ws_all = team_workspace(P, d, n, k_blk, device=dev)
+            self.ws_team = [self.ws_all]    # (its error word is checked like the per-team ones)
+        else:
+            self.ws_team = [workspace(Q, Q, n, k_blk, device=dev) for _ in range(d)]
         if bruck:
             self.steps = 1
             self.toph_idx = torch.empty((P, k_blk), dtype=torch.int32, device=dev)
@@ -462,6 +509,14 @@ class SparDLSagStep:
 
     def add_and_select(self, grad, stream=None):
         Q, n, L = self.Q, self.n, self.k_blk
+        if self.batched:
+            if self.fused:
+                team_residual_add(self.acc, grad, self.P, self.d, n, L, self.ws_all, stream=stream)
+            else:
+                residual_add(self.acc, grad, self.P, n, 0, None, stream=stream)
+            team_block_topk(self.acc, self.P, self.d, n, L, self.sp_idx, self.sp_val, self.local_idx, self.ws_all,
+                            TOPK_HIST_READY if self.fused else 0, stream=stream)
+            return
         for tau in range(self.d):
             r, ws = self._rows(tau), self.ws_team[tau]
             if self.fused:
@@ -472,6 +527,11 @@ class SparDLSagStep:
                        TOPK_HIST_READY if self.fused else 0, stream=stream)
 
     def team_srs(self, stream=None):
+        if self.batched:
+            for i in range(1, self.l + 1):
+                team_merge_topk(self.sp_idx, self.sp_val, self.P, self.d, self.n, self.k_blk, i, self.drop_idx[i - 1],
+                                self.drop_val[i - 1], self.drop_cnt[i - 1], self.ws_all, stream=stream)
+            return
         for tau in range(self.d):
             r = self._rows(tau)
             for i in range(1, self.l + 1):
@@ -498,7 +558,7 @@ class SparDLSagStep:
             r = self._rows(tau)
             residual_collect(self.acc[r], self.Q, self.n, self.k_blk, self.local_idx[r], self.sp_idx[r],
                              [t[r] for t in self.drop_idx], [t[r] for t in self.drop_val],
-                             [t[r] for t in self.drop_cnt], self.ws_team[tau], self.member, stream=stream)
+                             [t[r] for t in self.drop_cnt], None, self.member, stream=stream)
         if self.bruck:
             bsag_residual(self.acc, self.P, self.d, self.n, self.k_blk, self.member, self.toph_idx, self.toph_val,
                           self.toph_cnt, stream=stream)

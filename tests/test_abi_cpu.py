@@ -218,6 +218,21 @@ def test_argument_errors_enqueue_nothing():
     lib.spardl_bsag_workspace_init.argtypes = [i32, i32, i64, i32, ctypes.c_void_p, sz, ctypes.c_void_p]
     assert lib.spardl_bsag_workspace_init(i32(14), i32(7), i64(1400), i32(5), q, big, null) == EINVAL
     assert lib.spardl_bsag_workspace_init(i32(14), i32(7), i64(1400), i32(5), p, sz(64), null) == ECAP
+    # team calls: d not dividing P, k_blk too large for a team block, round out of range, small workspace
+    lib.spardl_team_workspace_bytes.argtypes = [i32, i32, i64, i32]
+    lib.spardl_team_workspace_bytes.restype = sz
+    assert lib.spardl_team_workspace_bytes(i32(12), i32(5), i64(1200), i32(5)) == 0
+    assert lib.spardl_team_workspace_bytes(i32(12), i32(4), i64(1200), i32(401)) == 0
+    assert lib.spardl_team_workspace_bytes(i32(12), i32(4), i64(1200), i32(400)) > 0
+    tm = lambda rnd, wsz: lib.spardl_team_merge_topk(p, p, i32(12), i32(4), i64(1200), i32(5), i32(rnd), p, p, p, p,
+                                                     wsz, null)
+    assert tm(0, big) == EINVAL
+    assert tm(3, big) == EINVAL          # Q = 3: two steps
+    assert tm(1, sz(64)) == ECAP
+    assert lib.spardl_team_block_topk(p, i64(1200), i32(12), i32(4), i64(1200), i32(5), i32(2), p, p, null, p, big,
+                                      null) == EINVAL
+    assert lib.spardl_team_residual_add(p, i64(1199), p, i64(1200), i32(12), i32(4), i64(1200), i32(5), p, big,
+                                        null) == EINVAL
     for s in (0, -1, -2, -3, 7):
         assert lib.spardl_strerror(s)
 

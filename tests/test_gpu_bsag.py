@@ -46,10 +46,11 @@ CASES = [
 ]
 
 
-@pytest.mark.parametrize("P,d,n,L,kind,steps,fused", CASES)
-def test_bsag_step(P, d, n, L, kind, steps, fused):
-    log(f"bsag step P={P} d={d} n={n} L={L} kind={kind} steps={steps} fused={fused}")
-    st = spardl.SparDLSagStep(P, d, n, L, fused=fused, bruck=True)
+@pytest.mark.parametrize("P,d,n,L,kind,steps,fused,batched",
+                         [c + (True,) for c in CASES] + [CASES[i] + (False,) for i in (1, 7)])
+def test_bsag_step(P, d, n, L, kind, steps, fused, batched):
+    log(f"bsag step P={P} d={d} n={n} L={L} kind={kind} steps={steps} fused={fused} batched={batched}")
+    st = spardl.SparDLSagStep(P, d, n, L, fused=fused, bruck=True, batched=batched)
     acc = np.zeros((P, n), np.float32)
     ctrl = {}
     hs = set()

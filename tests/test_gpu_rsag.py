@@ -43,10 +43,13 @@ CASES = [
 ]
 
 
-@pytest.mark.parametrize("P,d,n,L,kind,steps,fused", CASES)
-def test_rsag_step(P, d, n, L, kind, steps, fused):
-    log(f"rsag step P={P} d={d} n={n} L={L} kind={kind} steps={steps} fused={fused}")
-    st = spardl.SparDLSagStep(P, d, n, L, fused=fused)
+@pytest.mark.parametrize("P,d,n,L,kind,steps,fused,batched",
+                         [c + (True,) for c in CASES] + [CASES[i] + (False,) for i in (3, 4, 6)])
+def test_rsag_step(P, d, n, L, kind, steps, fused, batched):
+    """batched: the teams' add, top-k and SRS steps over all P rows in one
+    call each; otherwise team by team."""
+    log(f"rsag step P={P} d={d} n={n} L={L} kind={kind} steps={steps} fused={fused} batched={batched}")
+    st = spardl.SparDLSagStep(P, d, n, L, fused=fused, batched=batched)
     acc = np.zeros((P, n), np.float32)
     for t in range(steps):
         grad = W.small_rows(kind, P, n, 100 * t + 13 * P + d)
