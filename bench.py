@@ -116,6 +116,8 @@ def main() -> int:
                          "L = d k / P entries per team block")
     ap.add_argument("--bruck", action="store_true",
                     help="with --teams d: join the teams by B-SAG (any d dividing P; Algorithm 2 sets h)")
+    ap.add_argument("--rows-per-call", type=int, default=0,
+                    help="workload 5: workers per residual-add / block top-k call (default PER_WORKER_ROWS)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--calib-copy", action="store_true",
                     help="first run one untimed device-to-device copy of CALIB_BYTES (a reference "
@@ -363,14 +365,20 @@ def main() -> int:
 # Above this many bytes of residual plus resident gradient batches the
 # workload runs one worker at a time (the GPT-2-XL-sized one: 192 GB of residual).
 PER_WORKER_BYTES = 200e9
+# workers per residual-add / block top-k call there (--rows-per-call): one row
+# of workspace (18 GB of candidates) and gradient (6 GB) beside the 192 GB
+# residual.  Two rows fit too (selection 1.9 ms faster per step) but the adds
+# over the larger footprint lose 2.3 ms.
+PER_WORKER_ROWS = 1
 
 
 def run_per_worker(args, wl, dev) -> int:
     """A workload whose gradients cannot all be resident beside the residual:
-    each worker's gradient is generated on the GPU (untimed), then its residual
-    add and block top-k run on a one-row workspace; the SRS steps, the decode
-    and the residual collection follow for all workers.  Step time = the sum
-    of the event-timed hot calls (marker cost removed)."""
+    the workers' gradients are generated on the GPU PER_WORKER_ROWS at a time
+    (untimed), then their residual add and block top-k run on a workspace for
+    that many rows; the SRS steps, the decode and the residual collection
+    follow for all workers.  Step time = the sum of the event-timed hot calls
+    (marker cost removed)."""
     import torch
 
     from paper_2304_00737_amd import spardl
@@ -381,12 +389,16 @@ def run_per_worker(args, wl, dev) -> int:
         print(json.dumps({"error": "the per-worker run (workload 5) has no team variant"}))
         return 2
     lazy = args.variant == "lazy"
+    R = args.rows_per_call if args.rows_per_call > 0 else PER_WORKER_ROWS
+    if P % R:
+        print(json.dumps({"error": f"--rows-per-call must divide P = {P}"}))
+        return 2
     if lazy:
-        st = spardl.SparDLLazyStep(P, n, kb, device=dev, rows_per_call=1)
+        st = spardl.SparDLLazyStep(P, n, kb, device=dev, rows_per_call=R)
     else:
-        st = spardl.SparDLStep(P, n, kb, device=dev, rows_per_call=1)
+        st = spardl.SparDLStep(P, n, kb, device=dev, rows_per_call=R)
     gen = W.DeviceGenerator(wl, device=dev)
-    g = torch.empty((1, n), dtype=torch.float32, device=dev)
+    g = torch.empty((R, n), dtype=torch.float32, device=dev)
     stream = torch.cuda.current_stream()
 
     def ev():
@@ -402,14 +414,15 @@ def run_per_worker(args, wl, dev) -> int:
     def one_step(j):
         t = j % wl.steps + 1
         marks = []
-        for w in range(P):
-            gen.fill(g[0], t, w)
+        for w0 in range(0, P, R):
+            for r in range(R):
+                gen.fill(g[r], t, w0 + r)
             e = (ev(), ev(), ev())
             e[0].record(stream)
-            st.residual_add_rows(w, g)
+            st.residual_add_rows(w0, g)
             e[1].record(stream)
             if not lazy:   # the lazy variant selects inside finish(), round by round
-                st.block_topk_rows(w, 1)
+                st.block_topk_rows(w0, R)
             e[2].record(stream)
             marks.append(e)
         f = (ev(), ev())
@@ -418,8 +431,8 @@ def run_per_worker(args, wl, dev) -> int:
         f[1].record(stream)
         torch.cuda.synchronize()
         ws_check(st)
-        add = sum(a.elapsed_time(b) for a, b, _ in marks) - P * marker_ms
-        topk = 0.0 if lazy else sum(b.elapsed_time(c) for _, b, c in marks) - P * marker_ms
+        add = sum(a.elapsed_time(b) for a, b, _ in marks) - len(marks) * marker_ms
+        topk = 0.0 if lazy else sum(b.elapsed_time(c) for _, b, c in marks) - len(marks) * marker_ms
         tail = f[0].elapsed_time(f[1]) - marker_ms
         return add, topk, tail
 
@@ -433,8 +446,8 @@ def run_per_worker(args, wl, dev) -> int:
     topk_ms = sum(r[1] for r in res) / steps
     tail_ms = sum(r[2] for r in res) / steps
     ms_per_step = add_ms + topk_ms + tail_ms
-    add_launch_ms = add_ms / P
-    alg_add = 12.0 * n
+    add_launch_ms = add_ms / (P // R)
+    alg_add = 12.0 * R * n
     achieved = alg_add / (add_launch_ms * 1e-3) / 1e9
     full = 16.0 * P * n + 4.0 * n + n / 8.0 + 12.0 * P * P * kb
     out = {
@@ -454,8 +467,8 @@ def run_per_worker(args, wl, dev) -> int:
         "config": {"workload": wl.name, "P": P, "n_per_worker": n, "density": f"{wl.density[0]}/{wl.density[1]}",
                    "k_per_block": kb, "gradient_batches": wl.steps, "residual": "carried across steps",
                    "segments": len(wl.seg_len), "seed": W.SEED_BASE, "variant": args.variant,
-                   "timing": "sum of event-timed hot calls; each worker's gradient generated on the GPU "
-                             "between them (one-row workspace)"},
+                   "timing": "sum of event-timed hot calls; the workers' gradients generated on the GPU "
+                             f"between them, {R} rows per call ({R}-row workspace)"},
         "roofline": {"bound": "hbm", "kernel": "k_residual_add", "achieved": achieved, "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS, "traffic": None,
                      "alg_bytes_per_launch": alg_add, "avg_launch_ms": add_launch_ms},

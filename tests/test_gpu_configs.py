@@ -95,14 +95,16 @@ def test_workload5_gpt2xl_sized_block17():
     assert gold["block_range"] == [lo, hi] and gold["k_per_block"] == kb
     log(f"workload 5: {wl.describe()} block {b}")
     torch.cuda.empty_cache()   # about 224 GB of HBM below; drop what earlier tests left cached
-    st = spardl.SparDLStep(P, n, kb, rows_per_call=1)
+    R = 1   # workers per call, as bench.py runs this workload
+    st = spardl.SparDLStep(P, n, kb, rows_per_call=R)
     gen = W.DeviceGenerator(wl)
-    g = torch.empty((1, n), dtype=torch.float32, device="cuda")
+    g = torch.empty((R, n), dtype=torch.float32, device="cuda")
     for t in range(1, wl.steps + 1):
-        for w in range(P):
-            gen.fill(g[0], t, w)
-            st.residual_add_rows(w, g)
-            st.block_topk_rows(w, 1)
+        for w0 in range(0, P, R):
+            for r in range(R):
+                gen.fill(g[r], t, w0 + r)
+            st.residual_add_rows(w0, g)
+            st.block_topk_rows(w0, R)
         st.finish()
         torch.cuda.synchronize()
         check_ws(st)
