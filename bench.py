@@ -47,9 +47,9 @@ def _kernel_src_hash() -> str:
     return h.hexdigest()[:16]
 
 
-def _traffic_from_profiles(kernel: str, src_hash: str, units_per_launch: float):
+def _traffic_from_profiles(kernel: str, src_hash: str, workload: str):
     """HBM bytes per launch from committed rocprofv3 counter runs, if they were
-    taken on the current kernel source; otherwise None."""
+    taken on the current kernel source and on this workload; otherwise None."""
     path = os.path.join(ROOT, "profiles", "traffic.json")
     try:
         with open(path) as fh:
@@ -57,7 +57,7 @@ def _traffic_from_profiles(kernel: str, src_hash: str, units_per_launch: float):
     except (OSError, ValueError):
         return None
     k = rec.get("kernels", {}).get(kernel)
-    if not k or rec.get("src_hash") != src_hash:
+    if not k or rec.get("src_hash") != src_hash or rec.get("workload") != workload:
         return None
     return k.get("bytes_per_launch")
 
@@ -318,7 +318,7 @@ def main() -> int:
     achieved = alg[dominant] / (dom_ms * 1e-3) / 1e9
     src_hash = _kernel_src_hash()
     # the stored counter readings are of the fused add (eager variant)
-    traffic = None if lazy or d > 1 else _traffic_from_profiles(dominant, src_hash, 1.0)
+    traffic = None if lazy or d > 1 else _traffic_from_profiles(dominant, src_hash, wl.name)
     core_bytes = sum(v for k, v in alg.items() if k != "allgather_densify")
     full_bytes = sum(alg.values())
 
