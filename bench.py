@@ -29,21 +29,14 @@ CALIB_BYTES = 1 << 30   # bytes read (and written) by the calibration copy
 
 
 def _kernel_src_hash() -> str:
-    """Hash of the residual-add kernel's source (its section of kernels.hip,
-    its launcher and the shared header), to tell whether stored counter
-    readings still describe the kernel being timed."""
+    """Hash of the residual-add kernel's source (its file, with its launcher,
+    and the headers it includes), to tell whether stored counter readings
+    still describe the kernel being timed."""
     csrc = os.path.join(ROOT, "paper_2304_00737_amd", "csrc")
-    with open(os.path.join(csrc, "kernels.hip")) as fh:
-        k = fh.read()
-    a = k.index("// ============================================================================ a1: residual add")
-    b = k.index("// ============================================================================", a + 10)
-    c = k.index("hipError_t launch_residual_add(")
-    d = k.index("hipError_t launch_hist1(")
     h = hashlib.sha256()
-    h.update(k[a:b].encode())
-    h.update(k[c:d].encode())
-    with open(os.path.join(csrc, "common.hpp"), "rb") as fh:
-        h.update(fh.read())
+    for f in ("kernels_add.hip", "device.hpp", "common.hpp"):
+        with open(os.path.join(csrc, f), "rb") as fh:
+            h.update(fh.read())
     return h.hexdigest()[:16]
 
 

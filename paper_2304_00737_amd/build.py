@@ -17,6 +17,9 @@ GRADGEN_DEV_SO = os.path.join(PKG, "workloads", "libgradgen_dev.so")
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
+# sources of libspardl.so (csrc/): the entry points, then the kernels by stage
+KERNEL_SOURCES = ("api.hip", "kernels_add.hip", "kernels_select.hip", "kernels_merge.hip", "kernels_decode.hip", "kernels_variants.hip")
+
 HIP_FLAGS = [
     "--offload-arch=gfx950",
     "-O3",
@@ -54,7 +57,7 @@ def build_gradgen_dev(verbose: bool = True) -> str:
 
 
 def build_spardl(verbose: bool = True) -> str:
-    srcs = [os.path.join(CSRC, f) for f in ("api.hip", "kernels.hip")]
+    srcs = [os.path.join(CSRC, f) for f in KERNEL_SOURCES]
     tmp = SPARDL_SO + ".tmp"
     _run([HIPCC, *HIP_FLAGS, "-I", os.path.join(ROOT, "include"), *srcs, "-o", tmp], verbose)
     os.replace(tmp, SPARDL_SO)

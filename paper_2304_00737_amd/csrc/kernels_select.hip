@@ -1,9 +1,6 @@
-// SparDL per-worker hot path kernels for gfx950 (CDNA4, wave64).
-//
-// Paper: SparDL (arXiv 2304.00737).  Residual add: Sec. III-B / Algorithm 1.
-// Block top-k: Sec. III-B with top-k of Sec. II.  Spar-Reduce-Scatter step:
-// Sec. III-B "Transmission with sparsification".  All-Gather + decode: end of
-// Sec. III-B.  Global residual collection: Sec. III-C / Algorithm 1.
+// Exact top-k selection of the SparDL per-worker hot path for gfx950 (CDNA4,
+// wave64): block top-k (Sec. III-B, top-k of Sec. II) and the selection of a
+// Spar-Reduce-Scatter merge (Sec. III-B "Transmission with sparsification").
 //
 // Exact top-k is a radix select on the 31-bit magnitude key in three digits
 // (12/11/8 bits).  Dense blocks: the level-1 histogram is built while
@@ -11,245 +8,16 @@
 // entries at or above the level-1 threshold bin as candidates in per-tile
 // slots (index order inside a slot) and the threshold-bin keys beside them;
 // the last two digits are resolved on those keys only; an ordered emit writes
-// the selection.  Merges of two sorted sparse blocks use merge-path tiles and
-// feed the same threshold and emit stages.  No workgroup ever waits on
-// another, and no floating-point atomics are used anywhere, so every result
-// is bit-reproducible.
+// the selection.  Merges feed the same threshold and emit stages.  No
+// workgroup ever waits on another, and no floating-point atomics are used, so
+// every result is bit-reproducible.
 
-#include "common.hpp"
+#include "device.hpp"
 #include "launch.hpp"
 
 #include <algorithm>
 
 namespace spardl {
-
-typedef float f4v __attribute__((ext_vector_type(4)));
-
-// ============================================================================ fill
-// Zero up to FILL_MAX word ranges in one launch (counters, histograms and
-// look-back status words are cleared this way; no memset nodes are used).
-__global__ __launch_bounds__(256) void k_fill(FillRanges r) {
-  int64_t total = 0;
-  for (int k = 0; k < r.count; ++k) total += r.len[k];
-  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
-  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < total; i += stride) {
-    int64_t j = i;
-    int k = 0;
-    while (j >= r.len[k]) {
-      j -= r.len[k];
-      ++k;
-    }
-    r.ptr[k][j] = 0u;
-  }
-}
-
-// Adds the non-zero bins of an LDS histogram of NB1 bins into a global one.
-// Consecutive lanes take consecutive bins, so one wave's atomics fall on a
-// few cache lines (a lane-strided split multiplies the L2 atomic requests).
-__device__ __forceinline__ void flush_hist(const uint32_t* h, uint32_t* __restrict__ H) {
-  for (int i = threadIdx.x; i < NB1; i += blockDim.x) {
-    const uint32_t c = h[i];
-    if (c) atomicAdd(&H[i], c);
-  }
-}
-
-// ============================================================================ a1: residual add
-// One workgroup = one tile of ADD_TILE elements of one block of one row.
-// With HIST, every sum's level-1 digit is counted in an LDS histogram that is
-// flushed (non-zero bins only) into the block's global one.  The gradient is
-// read once, so it is loaded non-temporally.
-//
-// The float4 path with HIST also writes speculative candidates for the block
-// top-k that follows: every sum whose key is at or above a floor two level-1
-// bins below the block's previous threshold bin (nothing on a block's first
-// step), in index order at the tile's own span of the candidate arrays, with
-// the count per tile.  The exact threshold bin found from this pass's
-// histogram decides whether the floor was low enough; if not, the top-k reads
-// the block again.  Thread t owns the 8 consecutive elements at 8 t.
-//
-// From a block's second step on, the histogram counts only keys at or above
-// a lower floor (two binades further down): the threshold lies there unless it
-// fell by more than that since the previous step, and then the level-1 select
-// rebuilds the block's full histogram itself.
-constexpr uint32_t SPEC_MARGIN = 2;     // level-1 bins between the previous threshold bin and the floor
-constexpr uint32_t HIST_MARGIN = 32;    // further level-1 bins below the candidate floor kept in the histogram
-constexpr uint32_t SPEC_NONE = 0xFFFFFFFFu;
-constexpr uint32_t SPEC_DIRTY = 0x80000000u;   // set on spec_used: entries changed since the add, candidates stale
-constexpr int ADD_STAGE = 512;          // speculative candidates staged in LDS per tile
-
-// Histogram floor (a key) for a candidate floor F (SPEC_NONE: histogram everything).
-__device__ __forceinline__ uint32_t hist_floor(uint32_t F) {
-  if (F == SPEC_NONE) return 0u;
-  F &= ~SPEC_DIRTY;
-  const uint32_t fb = F >> D1_SHIFT;
-  return fb > HIST_MARGIN ? (fb - HIST_MARGIN) << D1_SHIFT : 0u;
-}
-
-template <int VEC, bool HIST>
-__global__ __launch_bounds__(256) void k_residual_add(float* __restrict__ acc, int64_t ld_acc,
-                                                      const float* __restrict__ grad, int64_t ld_grad,
-                                                      Blocks B, uint32_t G, AddSpec sp) {
-  constexpr bool SPEC = HIST && VEC == 4;
-  __shared__ __align__(16) uint32_t h[HIST ? NB1 : 4];
-  __shared__ int32_t s_idx[SPEC ? ADD_STAGE : 1];
-  __shared__ float s_val[SPEC ? ADD_STAGE : 1];
-  __shared__ uint32_t wtot[4];
-  const uint32_t g = blockIdx.x % G;
-  const uint32_t wb = blockIdx.x / G;
-  const uint32_t b = wb % B.P, w = wb / B.P;
-  const uint32_t s = B.start(b), e = B.start(b + 1u);
-  const uint32_t t0 = s + g * (uint32_t)ADD_TILE;
-  if (t0 >= e) return;
-  if (HIST) {
-    for (int i = threadIdx.x; i < NB1 / 4; i += 256) reinterpret_cast<uint4*>(h)[i] = make_uint4(0u, 0u, 0u, 0u);
-    __syncthreads();
-  }
-  float* __restrict__ A = acc + (int64_t)w * ld_acc;
-  const float* __restrict__ Gr = grad + (int64_t)w * ld_grad;
-  if (VEC == 4) {
-    static_assert(ADD_TILE == 256 * 8, "eight elements per thread");
-    const uint32_t my0 = t0 + threadIdx.x * 8u;
-    f4v a[2], gg[2];
-#pragma unroll
-    for (int j = 0; j < 2; ++j) {
-      if (my0 + 4u * j < e) {
-        a[j] = *reinterpret_cast<const f4v*>(A + my0 + 4u * j);
-        gg[j] = __builtin_nontemporal_load(reinterpret_cast<const f4v*>(Gr + my0 + 4u * j));
-      }
-    }
-    uint32_t F = SPEC_NONE;
-    if (SPEC) {
-      const uint32_t sw = sp.spec_t1[wb];
-      if (sw != 0u) {
-        const uint32_t T1p = sw - 1u;
-        F = T1p > SPEC_MARGIN ? (T1p - SPEC_MARGIN) << D1_SHIFT : 0u;
-      }
-      if (g == 0u && threadIdx.x == 0) sp.spec_used[wb] = F;
-    }
-    const uint32_t FH = hist_floor(F);
-    float r[8];
-    uint32_t nc = 0;
-#pragma unroll
-    for (int j = 0; j < 2; ++j) {
-      if (my0 + 4u * j < e) {
-        f4v q;
-        q.x = a[j].x + gg[j].x;
-        q.y = a[j].y + gg[j].y;
-        q.z = a[j].z + gg[j].z;
-        q.w = a[j].w + gg[j].w;
-        __builtin_nontemporal_store(q, reinterpret_cast<f4v*>(A + my0 + 4u * j));   // re-read only next step
-        r[4 * j + 0] = q.x;
-        r[4 * j + 1] = q.y;
-        r[4 * j + 2] = q.z;
-        r[4 * j + 3] = q.w;
-        if (HIST) {
-#pragma unroll
-          for (int c = 0; c < 4; ++c) {
-            const uint32_t key = mag_key(r[4 * j + c]);
-            if (key >= FH) atomicAdd(&h[key >> D1_SHIFT], 1u);
-            nc += key >= F ? 1u : 0u;
-          }
-        }
-      } else {
-#pragma unroll
-        for (int c = 0; c < 4; ++c) r[4 * j + c] = 0.f;
-      }
-    }
-    if (SPEC) {
-      // index-ordered compaction of the candidates (keys >= F) of the tile
-      const int lane = lane_id(), wv = wave_id();
-      const uint32_t incl = wave_incl_scan(nc);
-      if (lane == WAVE - 1) wtot[wv] = incl;
-      __syncthreads();
-      uint32_t base = 0, tot = 0;
-#pragma unroll
-      for (int k = 0; k < 4; ++k) {
-        const uint32_t x = wtot[k];
-        base += k < wv ? x : 0u;
-        tot += x;
-      }
-      const bool staged = tot <= (uint32_t)ADD_STAGE;   // uniform
-      int32_t* __restrict__ CI = sp.cand_idx + (int64_t)w * B.n + t0;
-      float* __restrict__ CV = sp.cand_val + (int64_t)w * B.n + t0;
-      int32_t* __restrict__ oI = staged ? s_idx : CI;
-      float* __restrict__ oV = staged ? s_val : CV;
-      uint32_t pos = base + incl - nc;
-      if (nc != 0u) {
-#pragma unroll
-        for (int k = 0; k < 8; ++k) {
-          if (my0 + (uint32_t)k < e && mag_key(r[k]) >= F) {
-            oI[pos] = (int32_t)(my0 + k);
-            oV[pos] = r[k];
-            ++pos;
-          }
-        }
-      }
-      if (threadIdx.x == 0) sp.spec_cnt[(int64_t)wb * G + g] = tot;
-      if (staged) {
-        __syncthreads();
-        for (uint32_t k = threadIdx.x; k < tot; k += 256) {
-          CI[k] = s_idx[k];
-          CV[k] = s_val[k];
-        }
-      }
-    }
-  } else {
-#pragma unroll
-    for (int j = 0; j < ADD_F4 * 4; ++j) {
-      const uint32_t off = t0 + j * 256u + threadIdx.x;
-      if (off < e) {
-        const float r = A[off] + Gr[off];
-        A[off] = r;
-        if (HIST) atomicAdd(&h[mag_key(r) >> D1_SHIFT], 1u);
-      }
-    }
-    if (HIST && g == 0u && threadIdx.x == 0) sp.spec_used[wb] = SPEC_NONE;   // no candidates on this path
-  }
-  if (HIST) {
-    __syncthreads();
-    uint32_t* __restrict__ H = sp.hist1 + ((int64_t)wb * HCOPIES + blockIdx.x % HCOPIES) * NB1;
-    flush_hist(h, H);
-  }
-}
-
-// Level-1 histogram only (block_topk without a fused residual add).
-template <int VEC>
-__global__ __launch_bounds__(256) void k_hist1(const float* __restrict__ acc, int64_t ld_acc, Blocks B, Units U,
-                                               uint32_t G, uint32_t* __restrict__ hist1) {
-  __shared__ __align__(16) uint32_t h[NB1];
-  const uint32_t g = blockIdx.x % G;
-  uint32_t w, b;
-  U.decode(blockIdx.x / G, B.P, &w, &b);
-  const uint32_t wb = w * B.P + b;   // the block's histogram
-  const uint32_t s = B.start(b), e = B.start(b + 1u);
-  const uint32_t t0 = s + g * (uint32_t)ADD_TILE;
-  if (t0 >= e) return;
-  for (int i = threadIdx.x; i < NB1 / 4; i += 256) reinterpret_cast<uint4*>(h)[i] = make_uint4(0u, 0u, 0u, 0u);
-  __syncthreads();
-  const float* __restrict__ A = acc + (int64_t)w * ld_acc;
-  if (VEC == 4) {
-#pragma unroll
-    for (int j = 0; j < ADD_F4; ++j) {
-      const uint32_t off = t0 + (j * 256u + threadIdx.x) * 4u;
-      if (off < e) {
-        const f4v a = *reinterpret_cast<const f4v*>(A + off);
-        atomicAdd(&h[mag_key(a.x) >> D1_SHIFT], 1u);
-        atomicAdd(&h[mag_key(a.y) >> D1_SHIFT], 1u);
-        atomicAdd(&h[mag_key(a.z) >> D1_SHIFT], 1u);
-        atomicAdd(&h[mag_key(a.w) >> D1_SHIFT], 1u);
-      }
-    }
-  } else {
-#pragma unroll
-    for (int j = 0; j < ADD_F4 * 4; ++j) {
-      const uint32_t off = t0 + j * 256u + threadIdx.x;
-      if (off < e) atomicAdd(&h[mag_key(A[off]) >> D1_SHIFT], 1u);
-    }
-  }
-  __syncthreads();
-  uint32_t* __restrict__ H = hist1 + ((int64_t)wb * HCOPIES + blockIdx.x % HCOPIES) * NB1;
-  flush_hist(h, H);
-}
 
 // ============================================================================ level-1 select
 // The block's histogram is the sum of its HCOPIES copies; every load is in
@@ -646,55 +414,6 @@ union ThreshLds {
   ThreshSmem g;
   FastSmem f;
 };
-
-// Levels 2 and 3 over the threshold-bin keys: visit(f) calls f(key) for
-// every entry in bin T1.  Returns the threshold as (tge, teq, need_eq).
-template <typename Visit>
-__device__ __forceinline__ void resolve_low_digits(uint32_t T1, uint32_t need1, uint32_t cnt1, uint32_t* h,
-                                                   uint32_t* scratch, uint32_t* err, Visit visit, uint32_t& tge,
-                                                   uint32_t& teq, uint32_t& need_eq) {
-  constexpr int NT = 1024;
-  tge = T1 << D1_SHIFT;
-  teq = 0u;
-  need_eq = 0u;
-  if (need1 == cnt1) return;
-  __syncthreads();
-  for (int i = threadIdx.x; i < NB2; i += NT) h[i] = 0u;
-  __syncthreads();
-  visit([&](uint32_t key) { atomicAdd(&h[(key >> D2_SHIFT) & (NB2 - 1)], 1u); });
-  __syncthreads();
-  uint32_t T2, above2, cnt2, ok;
-  block_select_desc(h, NB2, need1, scratch, &T2, &above2, &cnt2, &ok);
-  if (!ok) {
-    if (threadIdx.x == 0) atomicOr(err, ERR_COUNT_L23);
-    return;
-  }
-  const uint32_t need2 = need1 - above2;
-  const uint32_t pre23 = (T1 << (D1_SHIFT - D2_SHIFT)) | T2;   // top 23 bits of the key
-  tge = pre23 << D2_SHIFT;
-  if (need2 == cnt2) return;
-  for (int i = threadIdx.x; i < NB3; i += NT) h[i] = 0u;
-  __syncthreads();
-  visit([&](uint32_t key) {
-    if ((key >> D2_SHIFT) == pre23) atomicAdd(&h[key & (NB3 - 1)], 1u);
-  });
-  __syncthreads();
-  uint32_t T3, above3, cnt3;
-  block_select_desc(h, NB3, need2, scratch, &T3, &above3, &cnt3, &ok);
-  if (!ok) {
-    if (threadIdx.x == 0) atomicOr(err, ERR_COUNT_L23);
-    return;
-  }
-  const uint32_t need3 = need2 - above3;
-  const uint32_t T = (pre23 << D2_SHIFT) | T3;
-  if (need3 == cnt3) {
-    tge = T;
-  } else {
-    tge = T + 1u;
-    teq = T;
-    need_eq = need3;
-  }
-}
 
 __device__ __forceinline__ void finish_unit(uint32_t* st, uint32_t T1, uint32_t tge, uint32_t teq, uint32_t need_eq,
                                             uint32_t tot_all, uint32_t tot_ge, uint32_t tot_eq, int32_t kb,
@@ -1479,776 +1198,7 @@ __global__ __launch_bounds__(256) void k_emit(
   }
 }
 
-// ============================================================================ a4: merge-path index sum
-// Pair p (Pairs in common.hpp): held block + received block, e.g. for an SRS
-// step held = sp[w][b], received = sp[(w - d) mod P][b], b = (w+t) mod P.
-// The merged sequence orders by index with the held entry first on equal
-// indices; the held entry then emits held + received and the received entry
-// leaves a hole.  Tile = MERGE_TILE merged positions; its hole-free part is
-// written densely into the tile's slot, and the level-1 histogram of the
-// union is accumulated for the selection.
-__global__ __launch_bounds__(MERGE_THREADS) void k_merge(
-    const int32_t* __restrict__ sp_idx, const float* __restrict__ sp_val, Pairs PM, int32_t kb,
-    int32_t tiles_per_pair, uint32_t* __restrict__ hist1,
-    uint32_t* __restrict__ slot_cnt, int32_t* __restrict__ U_idx, float* __restrict__ U_val) {
-  // held entries a0-1 .. a1 at [0, nh + 2), received b0 .. b1 at [nh + 2, nh + nr + 3)
-  __shared__ int32_t cI[MERGE_TILE + 3];
-  __shared__ float cV[MERGE_TILE + 3];
-  __shared__ __align__(16) uint32_t hist[NB1];
-  __shared__ uint32_t scratch[2 * (MERGE_THREADS / WAVE) + 1];
-  const uint32_t pair = blockIdx.x / (uint32_t)tiles_per_pair;
-  const int32_t tile = (int32_t)(blockIdx.x % (uint32_t)tiles_per_pair);
-  int64_t hb, rb;
-  bool both;
-  PM.decode(pair, &hb, &rb, &both);
-  const int32_t* __restrict__ Hi = sp_idx + hb * kb;
-  const float* __restrict__ Hv = sp_val + hb * kb;
-  const int32_t* __restrict__ Ri = sp_idx + rb * kb;
-  const float* __restrict__ Rv = sp_val + rb * kb;
-  const int32_t L2 = 2 * kb;
-  for (int i = threadIdx.x; i < NB1 / 4; i += blockDim.x) reinterpret_cast<uint4*>(hist)[i] = make_uint4(0u, 0u, 0u, 0u);
-  const int32_t Q0 = tile * MERGE_TILE;
-  const int32_t Q1 = min(Q0 + MERGE_TILE, L2);
-  // split(q) = number of held entries among the first q merged positions:
-  // the first a in [max(0, q-kb), min(q, kb)) whose held entry does not go
-  // before received entry q-a-1 (held goes first on equal indices).  The
-  // tile's two splits are searched together.
-  int32_t a0, a1;
-  wg_partition_point2(max(0, Q0 - kb), min(Q0, kb), [&](int32_t a) { return Hi[a] <= Ri[Q0 - a - 1]; },
-                      max(0, Q1 - kb), min(Q1, kb), [&](int32_t a) { return Hi[a] <= Ri[Q1 - a - 1]; }, scratch,
-                      &a0, &a1);
-  const int32_t b0 = Q0 - a0, b1 = Q1 - a1;
-  const int32_t nh = a1 - a0, nr = b1 - b0;
-  int32_t* hI = cI;
-  float* hV = cV;
-  int32_t* rI = cI + nh + 2;
-  float* rV = cV + nh + 2;
-  {
-    // hI[i] = held[a0 - 1 + i] (outside [0, kb): -1 before, INT_MAX after), i <= nh + 1;
-    // rI[i] = recv[b0 + i] (INT_MAX past the end), i <= nr.  All loads first.
-    constexpr int SU = (MERGE_TILE + 3 + MERGE_THREADS - 1) / MERGE_THREADS;
-    int32_t ti[SU];
-    float tv[SU];
-#pragma unroll
-    for (int u = 0; u < SU; ++u) {
-      const int i = threadIdx.x + u * MERGE_THREADS;   // position in the combined buffer
-      ti[u] = INT32_MAX;
-      tv[u] = 0.f;
-      if (i <= nh + 1) {
-        const int32_t gi = a0 - 1 + i;
-        if (gi < 0) ti[u] = -1;
-        else if (gi < kb) { ti[u] = Hi[gi]; tv[u] = Hv[gi]; }
-      } else if (i <= nh + 2 + nr) {
-        const int32_t gj = b0 + (i - nh - 2);
-        if (gj < kb) { ti[u] = Ri[gj]; tv[u] = Rv[gj]; }
-      }
-    }
-#pragma unroll
-    for (int u = 0; u < SU; ++u) {
-      const int i = threadIdx.x + u * MERGE_THREADS;
-      if (i <= nh + 2 + nr) {
-        cI[i] = ti[u];
-        cV[i] = tv[u];
-      }
-    }
-  }
-  __syncthreads();
-  // held(i) = hI[i - a0 + 1], recv(j) = rI[j - b0]
-  int32_t ei[MERGE_PER_THREAD];
-  float ev[MERGE_PER_THREAD];
-  bool eok[MERGE_PER_THREAD];
-  uint32_t cnt = 0;
-  const int32_t q_lo = Q0 + (int32_t)threadIdx.x * MERGE_PER_THREAD;
-  int32_t a = 0, bb = 0;
-  if (q_lo < Q1) {
-    int32_t lo = max(a0, a1 - (Q1 - q_lo)), hi = min(a1, a0 + (q_lo - Q0));
-    while (lo < hi) {
-      const int32_t mid = (lo + hi) >> 1;
-      if (hI[mid - a0 + 1] <= rI[q_lo - mid - 1 - b0]) lo = mid + 1;
-      else hi = mid;
-    }
-    a = lo;
-    bb = q_lo - a;
-  }
-#pragma unroll
-  for (int k = 0; k < MERGE_PER_THREAD; ++k) {
-    eok[k] = false;
-    ei[k] = 0;
-    ev[k] = 0.f;
-    if (q_lo + k < Q1) {
-      a = min(a, a1);     // only reachable with unsorted input; keeps LDS reads in range
-      bb = min(bb, b1);
-      const int32_t hx = hI[a - a0 + 1];
-      const int32_t rx = rI[bb - b0];
-      if (hx <= rx) {
-        float v = hV[a - a0 + 1];
-        if (rx == hx) v = v + rV[bb - b0];
-        ei[k] = hx;
-        ev[k] = v;
-        eok[k] = true;
-        ++a;
-      } else {
-        if (hI[a - a0] != rx) {
-          ei[k] = rx;
-          ev[k] = rV[bb - b0];
-          eok[k] = true;
-        }
-        ++bb;
-      }
-      if (eok[k]) {
-        ++cnt;
-        atomicAdd(&hist[mag_key(ev[k]) >> D1_SHIFT], 1u);
-      }
-    }
-  }
-  // the scan's barriers put every thread past its merge loop, so the tile is
-  // staged in the (now free) input buffer and written out coalesced
-  uint32_t tot;
-  uint32_t pos = block_excl_scan(cnt, scratch, &tot);
-  if (threadIdx.x == 0) slot_cnt[(int64_t)pair * tiles_per_pair + tile] = tot;
-#pragma unroll
-  for (int k = 0; k < MERGE_PER_THREAD; ++k) {
-    if (eok[k]) {
-      cI[pos] = ei[k];
-      cV[pos] = ev[k];
-      ++pos;
-    }
-  }
-  __syncthreads();
-  const int64_t ubase = (int64_t)pair * tiles_per_pair * MERGE_TILE + Q0;
-  for (uint32_t k = threadIdx.x; k < tot; k += blockDim.x) {
-    U_idx[ubase + k] = cI[k];
-    U_val[ubase + k] = cV[k];
-  }
-  flush_hist(hist, hist1 + (int64_t)pair * NB1);
-}
-
-// ============================================================================ a5: all-gather + densify
-// One workgroup per tile [t0, t0 + DENSE_TILE) of the output.  The tile's
-// zeros are stored first, straight to memory, so that the write stream does
-// not wait for anything; then the final entries whose index falls in the
-// tile are found (both ends by one joint binary search in the index-sorted
-// final blocks sp[b][b]) and stored over them after a barrier, whose
-// workgroup-scope ordering makes the entry the last write to its element.
-// With `member`, the tile's words of the membership bitmap of the final
-// index set I are written as well (bit x & 31 of word x >> 5 set iff x is in
-// I), every word of [0, ceil(n/32)) exactly once.
-template <int VEC>
-__global__ __launch_bounds__(256) void k_densify(const int32_t* __restrict__ sp_idx,
-                                                 const float* __restrict__ sp_val, Blocks B,
-                                                 int32_t kb, float* __restrict__ dense,
-                                                 uint32_t* __restrict__ member) {
-  static_assert(DENSE_TILE % 1024 == 0, "whole float4 rounds and bitmap words");
-  __shared__ uint32_t bits[DENSE_TILE / 32];
-  __shared__ uint32_t cnt[8];
-  const int64_t n = B.n;
-  const int64_t t0 = (int64_t)blockIdx.x * DENSE_TILE;
-  const int64_t t1 = min(t0 + DENSE_TILE, n);
-  if (VEC == 4) {
-    for (int i = threadIdx.x * 4; i < DENSE_TILE; i += blockDim.x * 4) {
-      const int64_t x = t0 + i;
-      if (x + 3 < t1) {
-        *reinterpret_cast<float4*>(dense + x) = make_float4(0.f, 0.f, 0.f, 0.f);
-      } else {
-        for (int c = 0; c < 4; ++c)
-          if (x + c < t1) dense[x + c] = 0.f;
-      }
-    }
-  } else {
-    for (int i = threadIdx.x; i < DENSE_TILE; i += blockDim.x)
-      if (t0 + i < t1) dense[t0 + i] = 0.f;
-  }
-  for (int i = threadIdx.x; i < DENSE_TILE / 32; i += blockDim.x) bits[i] = 0u;
-  const uint32_t blo = B.of((uint32_t)t0), bhi = B.of((uint32_t)(t1 - 1));
-  for (uint32_t b = blo; b <= bhi; ++b) {
-    const int32_t* Fi = sp_idx + ((int64_t)b * B.P + b) * kb;
-    const float* Fv = sp_val + ((int64_t)b * B.P + b) * kb;
-    int32_t lo, hi;
-    wg_partition_point2(
-        0, kb, [&](int32_t p) { return (int64_t)Fi[p] < t0; }, 0, kb,
-        [&](int32_t p) { return (int64_t)Fi[p] < t1; }, cnt, &lo, &hi);
-    if (b == blo) __syncthreads();   // uniform: the zero stores and the bitmap clear come first
-    for (int32_t j = lo + (int32_t)threadIdx.x; j < hi; j += blockDim.x) {
-      const int64_t r = (int64_t)Fi[j] - t0;
-      if (r >= 0 && r < t1 - t0) {
-        dense[t0 + r] = Fv[j];
-        if (member) atomicOr(&bits[r >> 5], 1u << (r & 31));
-      }
-    }
-  }
-  if (member) {
-    __syncthreads();
-    for (int i = threadIdx.x; i < DENSE_TILE / 32 && t0 + 32 * (int64_t)i < t1; i += blockDim.x)
-      member[(t0 >> 5) + i] = bits[i];
-  }
-}
-
-// ============================================================================ a6: residual collection
-// Membership bitmap of the final index set I, one bit per index.  The
-// workspace keeps it at zero between steps: one thread per final entry sets
-// its bit before the residual updates and clears the word afterwards.
-__global__ __launch_bounds__(256) void k_bm_mark(const int32_t* __restrict__ sp_idx, uint32_t P, uint32_t n,
-                                                 uint32_t kb, uint32_t* __restrict__ bm, int set) {
-  const uint32_t per_b = kb;
-  for (uint32_t b = blockIdx.y; b < P; b += gridDim.y) {
-    const int32_t* __restrict__ F = sp_idx + ((int64_t)b * P + b) * kb;
-    for (uint32_t j = blockIdx.x * 256u + threadIdx.x; j < per_b; j += gridDim.x * 256u) {
-      const int32_t x = F[j];
-      if (x >= 0 && (uint32_t)x < n) {
-        if (set) atomicOr(&bm[(uint32_t)x >> 5], 1u << ((uint32_t)x & 31u));
-        else bm[(uint32_t)x >> 5] = 0u;
-      }
-    }
-  }
-}
-
-__device__ __forceinline__ bool in_final(const uint32_t* __restrict__ bm, int32_t x) {
-  return (bm[x >> 5] >> (x & 31)) & 1u;
-}
-
-// acc[w][x] = 0 where worker w selected x locally and x is a final index.
-// Grid: x over the worker's P k_blk local indices, y over workers.
-__global__ __launch_bounds__(256) void k_grc_zero(float* __restrict__ acc, int64_t ld_acc, uint32_t P, uint32_t n,
-                                                  uint32_t kb, const int32_t* __restrict__ local_idx,
-                                                  const uint32_t* __restrict__ bm) {
-  const uint32_t per_w = P * kb;   // <= n < 2^31
-  for (uint32_t w = blockIdx.y; w < P; w += gridDim.y) {
-    const int32_t* __restrict__ L = local_idx + (int64_t)w * per_w;
-    float* __restrict__ A = acc + (int64_t)w * ld_acc;
-    for (uint32_t i = blockIdx.x * 256u + threadIdx.x; i < per_w; i += gridDim.x * 256u) {
-      const int32_t x = L[i];
-      if (x >= 0 && (uint32_t)x < n && in_final(bm, x)) A[x] = 0.0f;
-    }
-  }
-}
-
-// acc[w][x] += v for the drops (x, v) of one step with x a final index.
-// Within one step a worker drops a given index at most once.  Grid: x over a
-// pair's drop list, y over pairs (w, t); pair p belongs to worker p / m.
-__global__ __launch_bounds__(256) void k_grc_drops(float* __restrict__ acc, int64_t ld_acc, uint32_t n, uint32_t m,
-                                                   uint32_t kb, uint32_t npairs,
-                                                   const int32_t* __restrict__ drop_idx,
-                                                   const float* __restrict__ drop_val,
-                                                   const int32_t* __restrict__ drop_cnt,
-                                                   const uint32_t* __restrict__ bm) {
-  for (uint32_t pair = blockIdx.y; pair < npairs; pair += gridDim.y) {
-    const int32_t c = drop_cnt[pair];
-    const uint32_t cnt = c < 0 ? 0u : min((uint32_t)c, kb);
-    const int32_t* __restrict__ Di = drop_idx + (int64_t)pair * kb;
-    const float* __restrict__ Dv = drop_val + (int64_t)pair * kb;
-    float* __restrict__ A = acc + (int64_t)(pair / m) * ld_acc;
-    for (uint32_t j = blockIdx.x * 256u + threadIdx.x; j < cnt; j += gridDim.x * 256u) {
-      const int32_t x = Di[j];
-      if (x >= 0 && (uint32_t)x < n && in_final(bm, x)) A[x] = A[x] + Dv[j];
-    }
-  }
-}
-
-// acc[w][x] += share * v for the drops (x, v) of R-SAG exchange t with x a
-// final index, on both workers of each pair (they made the same merge;
-// share = 2^-(t+1), the product exact unless it is subnormal).  Grid: x over
-// a pair's drop list, y over pairs, numbered as in the exchange.
-__global__ __launch_bounds__(256) void k_grc_sag_drops(float* __restrict__ acc, int64_t ld_acc, uint32_t n,
-                                                       uint32_t Q, uint32_t t, uint32_t kb, uint32_t npairs,
-                                                       const int32_t* __restrict__ drop_idx,
-                                                       const float* __restrict__ drop_val,
-                                                       const int32_t* __restrict__ drop_cnt,
-                                                       const uint32_t* __restrict__ bm, float share) {
-  for (uint32_t pair = blockIdx.y; pair < npairs; pair += gridDim.y) {
-    const int32_t c = drop_cnt[pair];
-    const uint32_t cnt = c < 0 ? 0u : min((uint32_t)c, kb);
-    const uint32_t j = pair / Q, q = pair - j * Q;
-    const uint32_t lowmask = (1u << t) - 1u;
-    const uint32_t X = ((j & ~lowmask) << 1) | (j & lowmask), Y = X | (1u << t);
-    const int32_t* __restrict__ Di = drop_idx + (int64_t)pair * kb;
-    const float* __restrict__ Dv = drop_val + (int64_t)pair * kb;
-    float* __restrict__ AX = acc + (int64_t)(X * Q + q) * ld_acc;
-    float* __restrict__ AY = acc + (int64_t)(Y * Q + q) * ld_acc;
-    for (uint32_t j2 = blockIdx.x * 256u + threadIdx.x; j2 < cnt; j2 += gridDim.x * 256u) {
-      const int32_t x = Di[j2];
-      if (x >= 0 && (uint32_t)x < n && in_final(bm, x)) {
-        const float v = Dv[j2] * share;
-        AX[x] = AX[x] + v;
-        AY[x] = AY[x] + v;
-      }
-    }
-  }
-}
-
-// ============================================================================ B-SAG
-// Spar-All-Gather across d teams, Bruck form, and its compression-ratio
-// controller (Sec. III-D, Algorithm 2).  Per block q of a team's Q blocks the
-// workspace keeps the controller state (h, step, flag in double precision, the
-// last union size N) and the count used at this step.
-
-// Algorithm 2, one thread per block: update step and h from the last N, keep
-// h in [L/d, L], count = floor(h + 1/2) clamped to [1, L].
-__global__ __launch_bounds__(64) void k_bsag_control(uint32_t Q, uint32_t L, uint32_t d, double* __restrict__ H,
-                                                     double* __restrict__ S, uint32_t* __restrict__ F,
-                                                     const uint32_t* __restrict__ N, uint32_t* __restrict__ cnt) {
-  for (uint32_t q = blockIdx.x * 64u + threadIdx.x; q < Q; q += gridDim.x * 64u) {
-    double h = H[q], step = S[q];
-    uint32_t flag = F[q];
-    const bool too_many = N[q] > L;
-    if (too_many != (step > 0.0)) {
-      if (flag) {
-        step = step * 2.0;
-        flag = 0u;
-      } else {
-        flag = 1u;
-      }
-    } else {
-      step = -step * 0.5;
-      flag = 0u;
-    }
-    const double lo = (double)L / (double)d;
-    h = h + step;
-    h = h < lo ? lo : h;
-    h = h > (double)L ? (double)L : h;
-    double c = floor(h + 0.5);
-    c = c < 1.0 ? 1.0 : c;
-    c = c > (double)L ? (double)L : c;
-    H[q] = h;
-    S[q] = step;
-    F[q] = flag;
-    cnt[q] = (uint32_t)c;
-  }
-}
-
-__global__ __launch_bounds__(64) void k_bsag_init(uint32_t Q, double h0, double step0, double* __restrict__ H,
-                                                  double* __restrict__ S, uint32_t* __restrict__ F,
-                                                  uint32_t* __restrict__ N) {
-  for (uint32_t q = blockIdx.x * 64u + threadIdx.x; q < Q; q += gridDim.x * 64u) {
-    H[q] = h0;
-    S[q] = step0;
-    F[q] = 0u;
-    N[q] = 0u;
-  }
-}
-
-// ---- top-c selection of many sparse lists (each sorted by index), spread
-// over workgroups: a chunked level-1 histogram, one workgroup per list for
-// the threshold (levels 2-3 scan the list for the threshold bin's keys),
-// chunked counts, chunked emit in index order.  ListSel says where list i
-// lives, its length, how many entries it keeps and where the kept (and then
-// sentinels -- index INT32_MAX, value 0 -- up to `pad`) and dropped entries go.
-
-struct ListDesc {
-  const int32_t* ii;
-  const float* iv;
-  uint32_t len, c, pad;
-  int32_t* ki;
-  float* kv;
-  int32_t* di;
-  float* dv;
-  int32_t* dcnt;
-};
-
-struct ListSel {
-  uint32_t mode;       // 0: top-h of the held blocks, list = worker; 1: final top-L, list = block
-  uint32_t Q, kb, cap;  // cap = d k_blk
-  int32_t* sp_idx;
-  float* sp_val;
-  const uint32_t* cnt;  // top-h count per block
-  const uint32_t* N;    // union size per block
-  int32_t *kept_i, *drop_i, *U_i, *fd_i;
-  float *kept_v, *drop_v, *U_v, *fd_v;
-  int32_t *drop_cnt, *fd_cnt;
-  __device__ __forceinline__ ListDesc desc(uint32_t i) const {
-    ListDesc D;
-    if (mode == 0u) {
-      const uint32_t q = i % Q;
-      const int64_t in = ((int64_t)i * Q + q) * kb, o = (int64_t)i * kb;
-      D.ii = sp_idx + in;
-      D.iv = sp_val + in;
-      D.len = kb;
-      D.c = min(cnt[q], kb);
-      D.pad = 0u;
-      D.ki = kept_i + o;
-      D.kv = kept_v + o;
-      D.di = drop_i + o;
-      D.dv = drop_v + o;
-      D.dcnt = drop_cnt + i;
-    } else {
-      const int64_t in = (int64_t)i * cap, o = ((int64_t)i * Q + i) * kb;
-      D.ii = U_i + in;
-      D.iv = U_v + in;
-      D.len = min(N[i], cap);
-      D.c = kb;
-      D.pad = kb;
-      D.ki = sp_idx + o;
-      D.kv = sp_val + o;
-      D.di = fd_i + in;
-      D.dv = fd_v + in;
-      D.dcnt = fd_cnt + i;
-    }
-    return D;
-  }
-};
-
-__global__ __launch_bounds__(256) void k_lsel_hist(ListSel S, uint32_t nch, uint32_t* __restrict__ hist) {
-  __shared__ __align__(16) uint32_t h[NB1];
-  const uint32_t i = blockIdx.x / nch, k = blockIdx.x % nch;
-  const ListDesc D = S.desc(i);
-  const uint32_t j0 = k * LIST_CHUNK;
-  if (D.c >= D.len || j0 >= D.len) return;   // uniform: nothing to select, or no entries here
-  const uint32_t j1 = min(D.len, j0 + LIST_CHUNK);
-  for (int b = threadIdx.x; b < NB1; b += 256) h[b] = 0u;
-  __syncthreads();
-  for (uint32_t j = j0 + threadIdx.x; j < j1; j += 256u) atomicAdd(&h[mag_key(D.iv[j]) >> D1_SHIFT], 1u);
-  __syncthreads();
-  flush_hist(h, hist + (int64_t)i * NB1);
-}
-
-// st[4 i ..]: key bound tge, tie key teq, ties to keep need_eq, entries kept
-__global__ __launch_bounds__(1024) void k_lsel_level(ListSel S, uint32_t* __restrict__ hist,
-                                                     uint32_t* __restrict__ st, uint32_t* __restrict__ err) {
-  __shared__ uint32_t h[NB1];
-  __shared__ uint32_t scratch[32];
-  constexpr uint32_t NT = 1024;
-  const uint32_t i = blockIdx.x;
-  const ListDesc D = S.desc(i);
-  uint32_t tge = 0u, teq = 0u, need_eq = 0u;   // keep everything unless a selection is needed
-  if (D.c < D.len) {
-    uint32_t* __restrict__ H = hist + (int64_t)i * NB1;
-    for (uint32_t b = threadIdx.x; b < NB1; b += NT) {
-      h[b] = H[b];
-      H[b] = 0u;   // histograms rest at zero
-    }
-    __syncthreads();
-    uint32_t T1, above1, cnt1, ok;
-    block_select_desc(h, NB1, D.c, scratch, &T1, &above1, &cnt1, &ok);
-    if (!ok) {
-      if (threadIdx.x == 0) atomicOr(err, ERR_COUNT);
-    } else {
-      resolve_low_digits(T1, D.c - above1, cnt1, h, scratch, err,
-                         [&](auto f) {
-                           for (uint32_t j = threadIdx.x; j < D.len; j += NT) {
-                             const uint32_t key = mag_key(D.iv[j]);
-                             if ((key >> D1_SHIFT) == T1) f(key);
-                           }
-                         },
-                         tge, teq, need_eq);
-    }
-  }
-  if (threadIdx.x == 0) {
-    st[4 * i + 0] = tge;
-    st[4 * i + 1] = teq;
-    st[4 * i + 2] = need_eq;
-    st[4 * i + 3] = min(D.c, D.len);
-  }
-}
-
-__device__ __forceinline__ uint32_t block_sum256(uint32_t v, uint32_t* sc) {
-  uint32_t tot;
-  block_excl_scan(v, sc, &tot);
-  return tot;
-}
-
-// per chunk: entries with key >= tge, and with key == teq (when ties are to be split)
-__global__ __launch_bounds__(256) void k_lsel_count(ListSel S, uint32_t nch, const uint32_t* __restrict__ st,
-                                                    uint32_t* __restrict__ ccnt) {
-  __shared__ uint32_t sc[8];
-  const uint32_t i = blockIdx.x / nch, k = blockIdx.x % nch;
-  const ListDesc D = S.desc(i);
-  const uint32_t tge = st[4 * i], teq = st[4 * i + 1], need_eq = st[4 * i + 2];
-  const uint32_t j0 = k * LIST_CHUNK, j1 = min(D.len, j0 + LIST_CHUNK);
-  uint32_t ng = 0, ne = 0;
-  for (uint32_t j = j0 + threadIdx.x; j < j1; j += 256u) {
-    const uint32_t key = mag_key(D.iv[j]);
-    ng += key >= tge;
-    ne += need_eq != 0u && key == teq;
-  }
-  ng = block_sum256(ng, sc);
-  ne = block_sum256(ne, sc);
-  if (threadIdx.x == 0) {
-    ccnt[2 * ((int64_t)i * nch + k)] = ng;
-    ccnt[2 * ((int64_t)i * nch + k) + 1] = ne;
-  }
-}
-
-// per chunk: kept entries to K in index order, the rest to D; chunk 0 also
-// writes the sentinels and the drop count
-__global__ __launch_bounds__(256) void k_lsel_emit(ListSel S, uint32_t nch, const uint32_t* __restrict__ st,
-                                                   const uint32_t* __restrict__ ccnt, uint32_t* __restrict__ err) {
-  constexpr uint32_t PT = LIST_CHUNK / 256;   // consecutive entries per thread
-  __shared__ uint32_t sc[8];
-  const uint32_t i = blockIdx.x / nch, k = blockIdx.x % nch;
-  const ListDesc D = S.desc(i);
-  const uint32_t tge = st[4 * i], teq = st[4 * i + 1], need_eq = st[4 * i + 2], keep = st[4 * i + 3];
-  if (k == 0) {
-    for (uint32_t j = keep + threadIdx.x; j < D.pad; j += 256u) {
-      D.ki[j] = INT32_MAX;
-      D.kv[j] = 0.f;
-    }
-    if (threadIdx.x == 0) *D.dcnt = (int32_t)(D.len - keep);
-  }
-  const uint32_t j0 = k * LIST_CHUNK;
-  if (j0 >= D.len) return;   // uniform
-  // selected and tied entries of the chunks before this one
-  uint32_t pg = 0, pe = 0;
-  for (uint32_t k2 = threadIdx.x; k2 < k; k2 += 256u) {
-    pg += ccnt[2 * ((int64_t)i * nch + k2)];
-    pe += ccnt[2 * ((int64_t)i * nch + k2) + 1];
-  }
-  pg = block_sum256(pg, sc);
-  pe = block_sum256(pe, sc);
-  const uint32_t a = min(D.len, j0 + threadIdx.x * PT), b = min(D.len, a + PT);
-  uint32_t ng = 0, ne = 0;
-  for (uint32_t j = a; j < b; ++j) {
-    const uint32_t key = mag_key(D.iv[j]);
-    ng += key >= tge;
-    ne += need_eq != 0u && key == teq;
-  }
-  uint32_t tg, te;
-  uint32_t rg = pg + block_excl_scan(ng, sc, &tg);
-  uint32_t re = pe + block_excl_scan(ne, sc, &te);
-  const uint32_t ndrop = D.len - keep;
-  for (uint32_t j = a; j < b; ++j) {
-    const int32_t x = D.ii[j];
-    const float v = D.iv[j];
-    const uint32_t key = mag_key(v);
-    const bool is_g = key >= tge, is_e = need_eq != 0u && key == teq;
-    const uint32_t before = rg + min(re, need_eq);
-    if (is_g || (is_e && re < need_eq)) {
-      if (before < keep) {
-        D.ki[before] = x;
-        D.kv[before] = v;
-      } else {
-        atomicOr(err, ERR_COUNT_POS);
-      }
-    } else if (j - before < ndrop) {
-      D.di[j - before] = x;
-      D.dv[j - before] = v;
-    } else {
-      atomicOr(err, ERR_COUNT_DROP);
-    }
-    rg += is_g;
-    re += is_e;
-  }
-}
-
-// ---- the Bruck All-Gather's result summed in team order, for block q, in
-// tiles of UT indices: each workgroup takes the d kept lists' entries that
-// fall in its tile (binary searches in the index-sorted lists), adds them in
-// team order in LDS (first occurrence stores, later ones add; an LDS
-// occupancy bitmap tells which), and either counts the tile's distinct
-// indices (pass 1) or writes them in index order after the counts of the
-// tiles before it (pass 2).  Tile 0 of each block also records N_q.
-constexpr uint32_t UT = UNION_TILE;
-
-template <bool WRITE>
-__global__ __launch_bounds__(1024) void k_bsag_union(const int32_t* __restrict__ kept_i,
-                                                     const float* __restrict__ kept_v, Blocks B, uint32_t d,
-                                                     uint32_t kb, const uint32_t* __restrict__ cnt, uint32_t ntile,
-                                                     uint32_t* __restrict__ tile_cnt, int32_t* __restrict__ U_i,
-                                                     float* __restrict__ U_v, uint32_t* __restrict__ N,
-                                                     int32_t* __restrict__ info, uint32_t* __restrict__ err) {
-  constexpr uint32_t NT = 1024;
-  __shared__ float vals[WRITE ? UT : 1];
-  __shared__ uint32_t bits[UT / 32];
-  __shared__ uint32_t sc[24];
-  __shared__ uint32_t range[2];
-  const uint32_t q = blockIdx.x / ntile, tile = blockIdx.x % ntile, Q = B.P;
-  const uint32_t s = B.start(q), e = B.start(q + 1u);
-  const uint32_t lo = s + tile * UT;
-  if (lo >= e) {   // uniform: a shorter block has fewer tiles
-    if (!WRITE && threadIdx.x == 0) tile_cnt[(int64_t)q * ntile + tile] = 0u;
-    return;
-  }
-  const uint32_t hi = min(e, lo + UT);
-  const uint32_t c = min(cnt[q], kb);
-  for (uint32_t w = threadIdx.x; w < UT / 32; w += NT) bits[w] = 0u;
-  for (uint32_t tau = 0; tau < d; ++tau) {
-    const int64_t o = ((int64_t)tau * Q + q) * kb;
-    if (threadIdx.x < 2) {   // first entry at or above lo (thread 0) and hi (thread 1)
-      const int32_t bound = (int32_t)(threadIdx.x == 0 ? lo : hi);
-      uint32_t l2 = 0, h2 = c;
-      while (l2 < h2) {
-        const uint32_t m = (l2 + h2) >> 1;
-        if (kept_i[o + m] < bound) l2 = m + 1;
-        else h2 = m;
-      }
-      range[threadIdx.x] = l2;
-    }
-    __syncthreads();   // also orders this team's additions after the previous team's
-    const uint32_t a = range[0], b = range[1];
-    for (uint32_t j = a + threadIdx.x; j < b; j += NT) {
-      const uint32_t r = (uint32_t)kept_i[o + j] - lo, bit = 1u << (r & 31u);
-      const uint32_t old = atomicOr(&bits[r >> 5], bit);
-      if (WRITE) {
-        const float v = kept_v[o + j];
-        vals[r] = (old & bit) ? vals[r] + v : v;
-      }
-    }
-    __syncthreads();
-  }
-  const uint32_t words = (hi - lo + 31u) >> 5;
-  const uint32_t m0 = threadIdx.x < words ? bits[threadIdx.x] : 0u;   // words <= UT / 32 = 512 < NT
-  uint32_t tot;
-  uint32_t pos = block_excl_scan(__popc(m0), sc, &tot);
-  if (!WRITE) {
-    if (threadIdx.x == 0) tile_cnt[(int64_t)q * ntile + tile] = tot;
-    return;
-  }
-  // distinct indices of the tiles before this one (and of all tiles, for tile 0)
-  const uint32_t* __restrict__ tc = tile_cnt + (int64_t)q * ntile;
-  uint32_t before = 0, all = 0;
-  for (uint32_t t2 = threadIdx.x; t2 < ntile; t2 += NT) {
-    const uint32_t v = tc[t2];
-    before += t2 < tile ? v : 0u;
-    all += v;
-  }
-  uint32_t tmp;
-  block_excl_scan(before, sc, &tmp);
-  before = tmp;
-  block_excl_scan(all, sc, &tmp);
-  all = tmp;
-  const uint32_t cap = d * kb;
-  pos += before;
-  uint32_t m = m0;
-  while (m) {
-    const uint32_t bt = __ffs(m) - 1u;
-    m &= m - 1u;
-    const uint32_t r = 32u * threadIdx.x + bt;
-    if (pos < cap) {
-      U_i[(int64_t)q * cap + pos] = (int32_t)(lo + r);
-      U_v[(int64_t)q * cap + pos] = vals[r];
-    }
-    ++pos;
-  }
-  if (tile == 0 && threadIdx.x == 0) {
-    if (all > cap) atomicOr(err, ERR_COUNT);
-    N[q] = all;
-    if (info) {
-      info[q] = (int32_t)c;
-      info[Q + q] = (int32_t)all;
-    }
-  }
-}
-
-// ============================================================================ lazy summation
-// One SRS step of the lazy variant (Sec. III-B "Optimization for SRS",
-// Algorithm 1): worker w sent sp[w][b], b = (w + d + t) mod P for t < m, to
-// worker r = (w + d) mod P.
-//  restore = 0: r adds every entry into its dense row, first saving the
-//               value there into saved[w][b] at the entry's position;
-//  restore = 1: r puts the saved value back where the index is not a final
-//               index (bm); run over the steps in reverse order, so the value
-//               before the first receipt is what stays.
-// Within one step each (receiver, block) has one sender whose indices are
-// distinct, so no two threads touch one element.  Entries outside their block
-// are skipped.  With hist1 (receive only), the receiver block's level-1
-// histogram left by the fused add is kept exact -- the old key's bin loses
-// the entry, the new key's bin gains it, both only at or above the add's
-// histogram floor, as deltas gathered in LDS per workgroup and added bin by
-// bin -- and the block is marked in spec_used, since its speculative
-// candidates no longer hold its values.  Grid: x over chunks of a block's
-// k_blk entries (LAZY_CHUNK per workgroup with hist1, else 256 per sweep),
-// y over pairs (w, t).
-constexpr uint32_t LAZY_CHUNK = 4096;
-
-__global__ __launch_bounds__(256) void k_lazy_step(float* __restrict__ acc, int64_t ld_acc, Blocks B, uint32_t kb,
-                                                   uint32_t d, uint32_t m, const int32_t* __restrict__ sp_idx,
-                                                   const float* __restrict__ sp_val, float* __restrict__ saved,
-                                                   const uint32_t* __restrict__ bm, int restore,
-                                                   uint32_t* __restrict__ hist1, uint32_t* __restrict__ spec_used) {
-  __shared__ uint32_t dh[NB1];   // histogram deltas (receive with hist1)
-  const uint32_t npairs = B.P * m;
-  for (uint32_t pair = blockIdx.y; pair < npairs; pair += gridDim.y) {
-    const uint32_t w = pair / m, t = pair - w * m;
-    const uint32_t r = (w + d) % B.P, b = (w + d + t) % B.P;
-    const uint32_t s = B.start(b), e = B.start(b + 1u);
-    const int64_t o = ((int64_t)w * B.P + b) * kb;
-    float* __restrict__ A = acc + (int64_t)r * ld_acc;
-    if (hist1) {   // uniform
-      const int64_t cu = (int64_t)r * B.P + b;   // the receiver block's arrays
-      const uint32_t FH = hist_floor(spec_used[cu]);
-      const uint32_t j0 = blockIdx.x * LAZY_CHUNK;
-      if (j0 >= kb) continue;
-      if (blockIdx.x == 0 && threadIdx.x == 0) atomicOr(&spec_used[cu], SPEC_DIRTY);
-      for (int i = threadIdx.x; i < NB1; i += 256) dh[i] = 0u;
-      __syncthreads();
-      for (uint32_t j = j0 + threadIdx.x; j < min(kb, j0 + LAZY_CHUNK); j += 256u) {
-        const int32_t x = sp_idx[o + j];
-        if (x < (int32_t)s || x >= (int32_t)e) continue;
-        const float old = A[x];
-        const float nv = old + sp_val[o + j];
-        saved[o + j] = old;
-        A[x] = nv;
-        const uint32_t k0 = mag_key(old), k1 = mag_key(nv);
-        if (k0 >= FH) atomicSub(&dh[k0 >> D1_SHIFT], 1u);
-        if (k1 >= FH) atomicAdd(&dh[k1 >> D1_SHIFT], 1u);
-      }
-      __syncthreads();
-      uint32_t* __restrict__ H = hist1 + (cu * HCOPIES + (blockIdx.x % HCOPIES)) * NB1;
-      for (int i = threadIdx.x; i < NB1; i += 256) {
-        const uint32_t c = dh[i];   // a signed delta, added modulo 2^32
-        if (c) atomicAdd(&H[i], c);
-      }
-      __syncthreads();   // dh is cleared for the next pair
-      continue;
-    }
-    for (uint32_t j = blockIdx.x * 256u + threadIdx.x; j < kb; j += gridDim.x * 256u) {
-      const int32_t x = sp_idx[o + j];
-      if (x < (int32_t)s || x >= (int32_t)e) continue;
-      if (restore) {
-        if (!in_final(bm, x)) A[x] = saved[o + j];
-      } else {
-        const float old = A[x];
-        saved[o + j] = old;
-        A[x] = old + sp_val[o + j];
-      }
-    }
-  }
-}
-
 // ============================================================================ launchers
-static inline unsigned grid_for(int64_t work, int per_block, unsigned cap) {
-  int64_t g = (work + per_block - 1) / per_block;
-  if (g < 1) g = 1;
-  return (unsigned)(g > cap ? cap : g);
-}
-
-hipError_t launch_fill(const FillRanges& r, hipStream_t s) {
-  int64_t total = 0;
-  for (int k = 0; k < r.count; ++k) total += r.len[k];
-  if (total <= 0) return hipSuccess;
-  hipLaunchKernelGGL(k_fill, dim3(grid_for(total, 256, 4096)), dim3(256), 0, s, r);
-  return hipGetLastError();
-}
-
-hipError_t launch_residual_add(float* acc, int64_t ld_acc, const float* grad, int64_t ld_grad,
-                               int32_t nworkers, int64_t n, int32_t P, bool vec4, const AddSpec& sp,
-                               hipStream_t s) {
-  const bool hist = sp.hist1 != nullptr;
-  const int32_t PP = hist ? P : 1;
-  const int64_t maxlen = (n + PP - 1) / PP;
-  const int32_t G = (int32_t)((maxlen + ADD_TILE - 1) / ADD_TILE);
-  const dim3 grid((unsigned)((int64_t)nworkers * PP * G));
-  const Blocks B = make_blocks(n, PP);
-  const uint32_t uG = (uint32_t)G;
-  if (hist) {
-    if (vec4) hipLaunchKernelGGL((k_residual_add<4, true>), grid, dim3(256), 0, s, acc, ld_acc, grad, ld_grad, B, uG, sp);
-    else hipLaunchKernelGGL((k_residual_add<1, true>), grid, dim3(256), 0, s, acc, ld_acc, grad, ld_grad, B, uG, sp);
-  } else {
-    if (vec4) hipLaunchKernelGGL((k_residual_add<4, false>), grid, dim3(256), 0, s, acc, ld_acc, grad, ld_grad, B, uG, sp);
-    else hipLaunchKernelGGL((k_residual_add<1, false>), grid, dim3(256), 0, s, acc, ld_acc, grad, ld_grad, B, uG, sp);
-  }
-  return hipGetLastError();
-}
-
-hipError_t launch_hist1(const float* acc, int64_t ld_acc, int64_t nunits, const Units& U, int64_t n, int32_t P,
-                        bool vec4, uint32_t* hist1, hipStream_t s) {
-  const int64_t maxlen = (n + P - 1) / P;
-  const int32_t G = (int32_t)((maxlen + ADD_TILE - 1) / ADD_TILE);
-  const dim3 grid((unsigned)(nunits * G));
-  const Blocks B = make_blocks(n, P);
-  if (vec4) hipLaunchKernelGGL(k_hist1<4>, grid, dim3(256), 0, s, acc, ld_acc, B, U, (uint32_t)G, hist1);
-  else hipLaunchKernelGGL(k_hist1<1>, grid, dim3(256), 0, s, acc, ld_acc, B, U, (uint32_t)G, hist1);
-  return hipGetLastError();
-}
-
 hipError_t launch_select1(uint32_t* hist1, uint32_t* state, int64_t nunits, const Units& U, int64_t n, int32_t P,
                           uint32_t need, uint32_t* spec_t1, const uint32_t* spec_used, bool spec, const float* acc,
                           int64_t ld_acc, bool vec4, uint32_t* err, hipStream_t s) {
@@ -2339,115 +1289,6 @@ hipError_t launch_emit(int mode, const int32_t* cand_idx, const float* cand_val,
     hipLaunchKernelGGL(k_emit<0>, grid, dim3(256), 0, s, cand_idx, cand_val, B, U, PM, kb, smax, gq, state, slot_cnt, pre_all, pre_ge, pre_eq, out_idx, out_val, local_idx, drop_idx, drop_val, err);
   else
     hipLaunchKernelGGL(k_emit<1>, grid, dim3(256), 0, s, cand_idx, cand_val, B, U, PM, kb, smax, gq, state, slot_cnt, pre_all, pre_ge, pre_eq, out_idx, out_val, local_idx, drop_idx, drop_val, err);
-  return hipGetLastError();
-}
-
-hipError_t launch_merge(const int32_t* sp_idx, const float* sp_val, const Pairs& PM, int64_t npairs, int32_t kb,
-                        int32_t tiles_per_pair, uint32_t* hist1, uint32_t* slot_cnt, int32_t* U_idx,
-                        float* U_val, hipStream_t s) {
-  const dim3 grid((unsigned)(npairs * tiles_per_pair));
-  hipLaunchKernelGGL(k_merge, grid, dim3(MERGE_THREADS), 0, s, sp_idx, sp_val, PM, kb, tiles_per_pair, hist1, slot_cnt, U_idx, U_val);
-  return hipGetLastError();
-}
-
-hipError_t launch_densify(const int32_t* sp_idx, const float* sp_val, int32_t P, int64_t n, int32_t kb,
-                          float* dense, uint32_t* member, bool vec4, hipStream_t s) {
-  const dim3 grid((unsigned)((n + DENSE_TILE - 1) / DENSE_TILE));
-  const Blocks B = make_blocks(n, P);
-  if (vec4) hipLaunchKernelGGL(k_densify<4>, grid, dim3(256), 0, s, sp_idx, sp_val, B, kb, dense, member);
-  else hipLaunchKernelGGL(k_densify<1>, grid, dim3(256), 0, s, sp_idx, sp_val, B, kb, dense, member);
-  return hipGetLastError();
-}
-
-hipError_t launch_bm_mark(const int32_t* sp_idx, int32_t P, int64_t n, int32_t kb, uint32_t* bm, bool set,
-                          hipStream_t s) {
-  const dim3 grid(grid_for(kb, 256, 1024), (unsigned)std::min<int32_t>(P, 65535));
-  hipLaunchKernelGGL(k_bm_mark, grid, dim3(256), 0, s, sp_idx, (uint32_t)P, (uint32_t)n, (uint32_t)kb, bm, set ? 1 : 0);
-  return hipGetLastError();
-}
-
-hipError_t launch_grc_zero(float* acc, int64_t ld_acc, int32_t P, int64_t n, int32_t kb, const int32_t* local_idx,
-                           const uint32_t* bm, hipStream_t s) {
-  const dim3 grid(grid_for((int64_t)P * kb, 256, 1024), (unsigned)std::min<int32_t>(P, 65535));
-  hipLaunchKernelGGL(k_grc_zero, grid, dim3(256), 0, s, acc, ld_acc, (uint32_t)P, (uint32_t)n, (uint32_t)kb, local_idx, bm);
-  return hipGetLastError();
-}
-
-hipError_t launch_grc_sag_drops(float* acc, int64_t ld_acc, int64_t n, int32_t Q, int32_t t, int32_t kb,
-                                int32_t npairs, const int32_t* drop_idx, const float* drop_val,
-                                const int32_t* drop_cnt, const uint32_t* bm, hipStream_t s) {
-  const dim3 grid(grid_for(kb, 256, 1024), (unsigned)std::min<int32_t>(npairs, 65535));
-  hipLaunchKernelGGL(k_grc_sag_drops, grid, dim3(256), 0, s, acc, ld_acc, (uint32_t)n, (uint32_t)Q, (uint32_t)t,
-                     (uint32_t)kb, (uint32_t)npairs, drop_idx, drop_val, drop_cnt, bm, 1.0f / (float)(2 << t));
-  return hipGetLastError();
-}
-
-hipError_t launch_bsag_init(int32_t Q, double h0, double step0, double* H, double* S, uint32_t* F, uint32_t* N,
-                            hipStream_t s) {
-  hipLaunchKernelGGL(k_bsag_init, dim3(grid_for(Q, 64, 1024)), dim3(64), 0, s, (uint32_t)Q, h0, step0, H, S, F, N);
-  return hipGetLastError();
-}
-
-hipError_t launch_bsag_exchange(const BsagArgs& a, hipStream_t s) {
-  const uint32_t Q = (uint32_t)a.Q, d = (uint32_t)a.d, kb = (uint32_t)a.kb, P = Q * d, cap = d * kb;
-  hipLaunchKernelGGL(k_bsag_control, dim3(grid_for(Q, 64, 1024)), dim3(64), 0, s, Q, kb, d, a.H, a.S, a.F, a.N,
-                     a.cnt);
-  ListSel L{};
-  L.Q = Q;
-  L.kb = kb;
-  L.cap = cap;
-  L.sp_idx = a.sp_idx;
-  L.sp_val = a.sp_val;
-  L.cnt = a.cnt;
-  L.N = a.N;
-  L.kept_i = a.kept_i;
-  L.kept_v = a.kept_v;
-  L.drop_i = a.drop_i;
-  L.drop_v = a.drop_v;
-  L.drop_cnt = a.drop_cnt;
-  L.U_i = a.U_i;
-  L.U_v = a.U_v;
-  L.fd_i = a.fd_i;
-  L.fd_v = a.fd_v;
-  L.fd_cnt = a.fd_cnt;
-  // top-h of every held block: P lists of k_blk entries
-  L.mode = 0u;
-  const uint32_t nch0 = (kb + LIST_CHUNK - 1) / LIST_CHUNK;
-  hipLaunchKernelGGL(k_lsel_hist, dim3(P * nch0), dim3(256), 0, s, L, nch0, a.hist);
-  hipLaunchKernelGGL(k_lsel_level, dim3(P), dim3(1024), 0, s, L, a.hist, a.lst, a.err);
-  hipLaunchKernelGGL(k_lsel_count, dim3(P * nch0), dim3(256), 0, s, L, nch0, a.lst, a.ccnt);
-  hipLaunchKernelGGL(k_lsel_emit, dim3(P * nch0), dim3(256), 0, s, L, nch0, a.lst, a.ccnt, a.err);
-  // team-order sums, counted then written tile by tile
-  const Blocks B = make_blocks(a.n, a.Q);
-  hipLaunchKernelGGL(k_bsag_union<false>, dim3(Q * a.ntile), dim3(1024), 0, s, a.kept_i, a.kept_v, B, d, kb, a.cnt,
-                     a.ntile, a.tile_cnt, a.U_i, a.U_v, a.N, a.info, a.err);
-  hipLaunchKernelGGL(k_bsag_union<true>, dim3(Q * a.ntile), dim3(1024), 0, s, a.kept_i, a.kept_v, B, d, kb, a.cnt,
-                     a.ntile, a.tile_cnt, a.U_i, a.U_v, a.N, a.info, a.err);
-  // final top-L of every block: Q lists of up to d k_blk entries
-  L.mode = 1u;
-  const uint32_t nch1 = (cap + LIST_CHUNK - 1) / LIST_CHUNK;
-  hipLaunchKernelGGL(k_lsel_hist, dim3(Q * nch1), dim3(256), 0, s, L, nch1, a.hist);
-  hipLaunchKernelGGL(k_lsel_level, dim3(Q), dim3(1024), 0, s, L, a.hist, a.lst, a.err);
-  hipLaunchKernelGGL(k_lsel_count, dim3(Q * nch1), dim3(256), 0, s, L, nch1, a.lst, a.ccnt);
-  hipLaunchKernelGGL(k_lsel_emit, dim3(Q * nch1), dim3(256), 0, s, L, nch1, a.lst, a.ccnt, a.err);
-  return hipGetLastError();
-}
-
-hipError_t launch_lazy_step(float* acc, int64_t ld_acc, int32_t P, int64_t n, int32_t kb, int32_t d, int32_t m,
-                            const int32_t* sp_idx, const float* sp_val, float* saved, const uint32_t* bm,
-                            bool restore, uint32_t* hist1, uint32_t* spec_used, hipStream_t s) {
-  const unsigned gx = hist1 ? (unsigned)((kb + LAZY_CHUNK - 1) / LAZY_CHUNK) : grid_for(kb, 256, 1024);
-  const dim3 grid(gx, (unsigned)std::min<int64_t>((int64_t)P * m, 65535));
-  hipLaunchKernelGGL(k_lazy_step, grid, dim3(256), 0, s, acc, ld_acc, make_blocks(n, P), (uint32_t)kb, (uint32_t)d,
-                     (uint32_t)m, sp_idx, sp_val, saved, bm, restore ? 1 : 0, hist1, spec_used);
-  return hipGetLastError();
-}
-
-hipError_t launch_grc_drops(float* acc, int64_t ld_acc, int64_t n, int32_t m, int32_t kb, int32_t npairs,
-                            const int32_t* drop_idx, const float* drop_val, const int32_t* drop_cnt,
-                            const uint32_t* bm, hipStream_t s) {
-  const dim3 grid(grid_for(kb, 256, 1024), (unsigned)std::min<int32_t>(npairs, 65535));
-  hipLaunchKernelGGL(k_grc_drops, grid, dim3(256), 0, s, acc, ld_acc, (uint32_t)n, (uint32_t)m, (uint32_t)kb, (uint32_t)npairs, drop_idx, drop_val, drop_cnt, bm);
   return hipGetLastError();
 }
 

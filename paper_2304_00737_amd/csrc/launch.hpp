@@ -1,4 +1,4 @@
-// Host-side launchers of the kernels in kernels.hip (internal to libspardl).
+// Host-side launchers of the kernels in kernels_*.hip (internal to libspardl).
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -60,7 +60,7 @@ hipError_t launch_grc_zero(float* acc, int64_t ld_acc, int32_t P, int64_t n, int
 hipError_t launch_grc_sag_drops(float* acc, int64_t ld_acc, int64_t n, int32_t Q, int32_t t, int32_t kb,
                                 int32_t npairs, const int32_t* drop_idx, const float* drop_val,
                                 const int32_t* drop_cnt, const uint32_t* bm, hipStream_t s);
-// Device arrays of one B-SAG exchange (kernels.hip, B-SAG section).
+// Device arrays of one B-SAG exchange (kernels_variants.hip).
 struct BsagArgs {
   int32_t* sp_idx;
   float* sp_val;
