@@ -300,19 +300,74 @@ __device__ __forceinline__ void recollect_wave(uint32_t c0, uint32_t c1, uint32_
   }
 }
 
-// One workgroup per COLLECT_GROUP consecutive slots of one (worker, block).
-// With the fused add's candidates usable, wave k filters slot k of the group;
-// otherwise the workgroup collects the group's slots from acc one by one.
-// Candidates crowd into the slots of large-scale segments, so one slot per
-// wave keeps the longest wave short; 64 registers let 8 waves share a SIMD.
-constexpr int COLLECT_GROUP = 4;
-template <int VEC>
+// The same for a slot whose first R1 WAVE entries the caller loaded into
+// ix1 / vx1 (lane l holds entries r WAVE + l), so that the loads of several
+// slots are in flight together; later chunks of RC_R2 per lane.
+constexpr int RC_R2 = 8;
+template <int R1>
+__device__ __forceinline__ void recollect_wave_pre(uint32_t c0, uint32_t c1, uint32_t tlo, uint32_t thi,
+                                                   uint32_t* cnt_out, uint32_t* nbin_out, int32_t* __restrict__ CI,
+                                                   float* __restrict__ CV, uint32_t* __restrict__ BK,
+                                                   const int32_t (&ix1)[R1], const float (&vx1)[R1]) {
+  const int lane = lane_id();
+  const uint64_t lt = __lanemask_lt();
+  const uint32_t tot = c0 + c1;
+  uint32_t kept = 0, nbin = 0;
+  auto put = [&](uint32_t e, int32_t ix, float vx) {
+    const uint32_t key = mag_key(vx);
+    const bool k = e < tot && key >= tlo;
+    const bool bk = k && key < thi;
+    const uint64_t mk = __ballot(k), mb = __ballot(bk);
+    if (k) {
+      const uint32_t pos = kept + popc64(mk & lt);
+      CI[pos] = ix;
+      CV[pos] = vx;
+    }
+    if (bk) BK[nbin + popc64(mb & lt)] = key;
+    kept += popc64(mk);
+    nbin += popc64(mb);
+  };
+#pragma unroll
+  for (int r = 0; r < R1; ++r)
+    if ((uint32_t)(r * WAVE) < tot) put((uint32_t)(r * WAVE + lane), ix1[r], vx1[r]);
+  for (uint32_t e0 = (uint32_t)(R1 * WAVE); e0 < tot; e0 += WAVE * RC_R2) {
+    int32_t ix[RC_R2];
+    float vx[RC_R2];
+#pragma unroll
+    for (int r = 0; r < RC_R2; ++r) {
+      const uint32_t e = e0 + r * WAVE + lane;
+      ix[r] = 0;
+      vx[r] = 0.f;
+      if (e < tot) {
+        const uint32_t src = e < c0 ? e : (uint32_t)ADD_TILE + (e - c0);
+        ix[r] = CI[src];
+        vx[r] = CV[src];
+      }
+    }
+#pragma unroll
+    for (int r = 0; r < RC_R2; ++r) put(e0 + r * WAVE + lane, ix[r], vx[r]);
+  }
+  if (lane == 0) {
+    *cnt_out = kept;
+    *nbin_out = nbin;
+  }
+}
+
+// One workgroup per 4 SPW consecutive slots of one (worker, block).  With
+// the fused add's candidates usable, each wave filters SPW consecutive slots,
+// the counts and first entries of all of them loaded before any is filtered
+// (when a call has many sparse slots, one slot per wave leaves the wave
+// waiting on memory most of the time); otherwise the workgroup collects the
+// group's slots from acc one by one.  64 registers let 8 waves share a SIMD.
+constexpr int64_t MULTI_SLOT_MIN = 1 << 17;   // slots per call from which waves take 2 slots each
+template <int VEC, int SPW>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(8, 8))) void k_collect(const float* __restrict__ acc, int64_t ld_acc, Blocks B, Units U,
                                                  uint32_t smax, uint32_t gq, const uint32_t* __restrict__ state,
                                                  const uint32_t* __restrict__ spec_cnt, uint32_t add_tiles,
                                                  uint32_t* __restrict__ slot_cnt, uint32_t* __restrict__ slot_nbin,
                                                  int32_t* __restrict__ cand_idx, float* __restrict__ cand_val,
                                                  uint32_t* __restrict__ bin_key) {
+  constexpr int COLLECT_GROUP = 4 * SPW;     // slots per workgroup
   __shared__ CollectSmem L;
   const uint32_t slot0 = (blockIdx.x % gq) * (uint32_t)COLLECT_GROUP;
   uint32_t w, b;
@@ -321,11 +376,11 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(8, 8))) voi
   const uint32_t s = B.start(b), e = B.start(b + 1u);
   if (s + slot0 * (uint32_t)SLOT >= e) return;
   const uint32_t* st = state + (int64_t)unit * ST_WORDS;
-  const uint32_t specok = st[ST_SPECOK];
-  const uint32_t T1 = st[ST_T1];
-  if (specok != 0u) {
-    const uint32_t tlo = T1 << D1_SHIFT, thi = tlo + (1u << D1_SHIFT);
-    {
+  if constexpr (SPW == 1) {
+    const uint32_t specok = st[ST_SPECOK];
+    if (specok != 0u) {
+      const uint32_t T1 = st[ST_T1];
+      const uint32_t tlo = T1 << D1_SHIFT, thi = tlo + (1u << D1_SHIFT);
       const uint32_t slot = slot0 + (uint32_t)wave_id();
       const uint32_t t0 = s + slot * (uint32_t)SLOT;
       if (slot >= smax || t0 >= e) return;
@@ -339,8 +394,63 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(8, 8))) voi
       const int64_t si = (int64_t)unit * smax + slot;
       recollect_wave(c0, c1, tlo, thi, slot_cnt + si, slot_nbin + si, cand_idx + cbase, cand_val + cbase,
                      bin_key + cbase);
+      return;
     }
-    return;
+  } else {
+    // this wave's slots: their candidate counts are loaded beside the unit's
+    // state words (in bounds for any live slot)
+    constexpr int R1 = 4;   // first entries per lane of each slot
+    const uint32_t sw = slot0 + (uint32_t)wave_id() * (uint32_t)SPW;
+    uint32_t c0[SPW], c1[SPW];
+#pragma unroll
+    for (int j = 0; j < SPW; ++j) {
+      const uint32_t slot = sw + (uint32_t)j;
+      const uint32_t t0 = s + slot * (uint32_t)SLOT;
+      c0[j] = 0u;
+      c1[j] = 0u;
+      if (slot < smax && t0 < e) {
+        const int64_t tile0 = (int64_t)unit * add_tiles + (int64_t)slot * (SLOT / ADD_TILE);
+        const uint32_t len0 = min(e - t0, (uint32_t)ADD_TILE);
+        const uint32_t len1 = t0 + (uint32_t)ADD_TILE < e ? min(e - t0 - (uint32_t)ADD_TILE, (uint32_t)ADD_TILE) : 0u;
+        c0[j] = min(spec_cnt[tile0], len0);
+        c1[j] = len1 != 0u ? min(spec_cnt[tile0 + 1], len1) : 0u;
+      }
+    }
+    const uint32_t specok = st[ST_SPECOK];
+    const uint32_t T1 = st[ST_T1];
+    if (specok != 0u) {
+      const uint32_t tlo = T1 << D1_SHIFT, thi = tlo + (1u << D1_SHIFT);
+      const int lane = lane_id();
+      int32_t ix[SPW][R1];
+      float vx[SPW][R1];
+#pragma unroll
+      for (int j = 0; j < SPW; ++j) {
+        const uint32_t tot = c0[j] + c1[j];
+        const int64_t cbase = (int64_t)w * B.n + s + (sw + (uint32_t)j) * (uint32_t)SLOT;
+#pragma unroll
+        for (int r = 0; r < R1; ++r) {
+          const uint32_t q = (uint32_t)(r * WAVE + lane);
+          ix[j][r] = 0;
+          vx[j][r] = 0.f;
+          if (q < tot) {
+            const uint32_t src = q < c0[j] ? q : (uint32_t)ADD_TILE + (q - c0[j]);
+            ix[j][r] = cand_idx[cbase + src];
+            vx[j][r] = cand_val[cbase + src];
+          }
+        }
+      }
+#pragma unroll
+      for (int j = 0; j < SPW; ++j) {
+        const uint32_t slot = sw + (uint32_t)j;
+        const uint32_t t0 = s + slot * (uint32_t)SLOT;
+        if (slot >= smax || t0 >= e) break;   // wave-uniform; later slots are past the block too
+        const int64_t cbase = (int64_t)w * B.n + t0;
+        const int64_t si = (int64_t)unit * smax + slot;
+        recollect_wave_pre<R1>(c0[j], c1[j], tlo, thi, slot_cnt + si, slot_nbin + si, cand_idx + cbase,
+                               cand_val + cbase, bin_key + cbase, ix[j], vx[j]);
+      }
+      return;
+    }
   }
   for (int k = 0; k < COLLECT_GROUP; ++k) {
     const uint32_t slot = slot0 + (uint32_t)k;
@@ -1078,13 +1188,72 @@ __global__ __launch_bounds__(1024) void k_big_scan(BigArgs a) {
 // with the counts before the slot taken from the per-slot prefixes of the
 // threshold stage and those inside it from wave ballots.  Unselected entries
 // of a merge go to the drop list at (#entries before) - (#selected before).
-// MODE 0 (block top-k): few candidates per slot, one wave per slot, no LDS
-// and no barrier; selected -> sp (and local_idx).  MODE 1 (merge): slots are
-// full merge tiles, so a workgroup takes one slot and each wave a quarter of
-// it, the counts of the quarters before it exchanged through LDS; selected ->
-// sp[w][b] in place, the rest -> the step's drop lists.
-constexpr int EMIT_R = 16;  // entries per lane per chunk (a crowded slot holds up to 4096)
-template <int MODE>
+// MODE 0 (block top-k): few candidates per slot, one wave per slot, or SPW
+// consecutive slots per wave when the call has many slots (as the collect),
+// with the counts, prefixes and first entries of all of them loaded before
+// any is emitted; no LDS and no barrier; selected -> sp (and local_idx).
+// MODE 1 (merge): slots are full merge tiles, so a workgroup takes one slot
+// and each wave a quarter of it, the counts of the quarters before it
+// exchanged through LDS; selected -> sp[w][b] in place, the rest -> the
+// step's drop lists.
+constexpr int EMIT_R = 16;    // entries per lane per chunk (a crowded slot holds up to 4096)
+constexpr int EMIT_R1 = 4;    // block top-k, several slots per wave: first entries per lane of each slot
+constexpr int EMIT_R0 = 8;    // ... entries per lane per chunk after the first
+
+// Block top-k emit of one slot whose first R1 WAVE entries are in ix1 / vx1
+// (lane l holds entries r WAVE + l); run_g / run_e: the >= and == counts of
+// the unit's slots before this one.
+template <int R1>
+__device__ __forceinline__ void emit_topk_slot(uint32_t cnt, uint32_t run_g, uint32_t run_e, uint32_t tge,
+                                               uint32_t teq, uint32_t need_eq, int32_t kb,
+                                               const int32_t* __restrict__ CI, const float* __restrict__ CV,
+                                               const int32_t (&ix1)[R1], const float (&vx1)[R1],
+                                               int32_t* __restrict__ oI, float* __restrict__ oV,
+                                               int32_t* __restrict__ oL, uint32_t* __restrict__ err) {
+  const int lane = lane_id();
+  const uint64_t lt = __lanemask_lt();
+  auto put = [&](uint32_t p, int32_t ix, float vx) {
+    const uint32_t key = mag_key(vx);
+    const bool is_ge = p < cnt && key >= tge;
+    const bool is_eq = p < cnt && need_eq != 0u && key == teq;
+    const uint64_t mg = __ballot(is_ge), me = __ballot(is_eq);
+    const uint32_t ge_pre = run_g + popc64(mg & lt);
+    const uint32_t eq_pre = run_e + popc64(me & lt);
+    if (is_ge || (is_eq && eq_pre < need_eq)) {
+      const uint32_t sel_before = ge_pre + (eq_pre < need_eq ? eq_pre : need_eq);
+      if (sel_before < (uint32_t)kb) {
+        oI[sel_before] = ix;
+        oV[sel_before] = vx;
+        if (oL) oL[sel_before] = ix;
+      } else {
+        atomicOr(err, ERR_COUNT_POS);
+      }
+    }
+    run_g += popc64(mg);
+    run_e += popc64(me);
+  };
+#pragma unroll
+  for (int r = 0; r < R1; ++r)
+    if ((uint32_t)(r * WAVE) < cnt) put((uint32_t)(r * WAVE + lane), ix1[r], vx1[r]);
+  for (uint32_t e0 = (uint32_t)(R1 * WAVE); e0 < cnt; e0 += WAVE * EMIT_R0) {
+    int32_t ix[EMIT_R0];
+    float vx[EMIT_R0];
+#pragma unroll
+    for (int r = 0; r < EMIT_R0; ++r) {
+      const uint32_t p = e0 + r * WAVE + lane;
+      ix[r] = -1;
+      vx[r] = 0.f;
+      if (p < cnt) {
+        ix[r] = CI[p];
+        vx[r] = CV[p];
+      }
+    }
+#pragma unroll
+    for (int r = 0; r < EMIT_R0; ++r) put(e0 + r * WAVE + lane, ix[r], vx[r]);
+  }
+}
+
+template <int MODE, int SPW = 1>
 __global__ __launch_bounds__(256) void k_emit(
     const int32_t* __restrict__ cand_idx, const float* __restrict__ cand_val, Blocks B, Units U, Pairs PM,
     int32_t kb, int32_t smax, uint32_t gq, const uint32_t* __restrict__ state,
@@ -1092,108 +1261,204 @@ __global__ __launch_bounds__(256) void k_emit(
     const uint32_t* __restrict__ pre_ge, const uint32_t* __restrict__ pre_eq, int32_t* __restrict__ out_idx,
     float* __restrict__ out_val, int32_t* __restrict__ local_idx, int32_t* __restrict__ drop_idx,
     float* __restrict__ drop_val, uint32_t* __restrict__ err) {
-  constexpr int NPART = MODE == 0 ? 1 : 4;   // waves sharing one slot
   const uint32_t unit = blockIdx.x / gq;
   const int wv = wave_id();
-  const int32_t slot = NPART == 1 ? (int32_t)((blockIdx.x % gq) * 4u + (uint32_t)wv) : (int32_t)(blockIdx.x % gq);
-  const SlotGeom g = slot_geom(MODE, unit, B, U, kb);
-  if (slot >= g.nslots) return;   // uniform over the workgroup when NPART > 1
-  const int lane = lane_id();
-  const uint64_t lt = __lanemask_lt();
-  const uint32_t au = MODE == 0 ? U.canon(unit, B.P) : unit;   // the unit's arrays
-  const int64_t si = (int64_t)au * smax + slot;
-  const uint32_t* st = state + (int64_t)au * ST_WORDS;
-  // independent loads: the slot's count and prefixes, the unit's threshold
-  const uint32_t cnt = min(slot_cnt[si], (uint32_t)g.ss);
-  const uint32_t all_before = pre_all[si];
-  uint32_t run_g = pre_ge[si], run_e = pre_eq[si];
-  const uint32_t tge = st[ST_TGE], teq = st[ST_TEQ], need_eq = st[ST_NEEDEQ];
-  const int64_t base = g.base + (int64_t)slot * g.ss;
-  int64_t o, o2 = -1;   // output block(s); o2: the other side of an R-SAG exchange
-  if (MODE == 0) {
+  if constexpr (MODE == 0 && SPW == 1) {
+    const int32_t slot = (int32_t)((blockIdx.x % gq) * 4u + (uint32_t)wv);
+    const SlotGeom g = slot_geom(0, unit, B, U, kb);
+    if (slot >= g.nslots) return;
+    const int lane = lane_id();
+    const uint64_t lt = __lanemask_lt();
+    const uint32_t au = U.canon(unit, B.P);   // the unit's arrays
+    const int64_t si = (int64_t)au * smax + slot;
+    const uint32_t* st = state + (int64_t)au * ST_WORDS;
+    // independent loads: the slot's count and prefixes, the unit's threshold
+    const uint32_t cnt = min(slot_cnt[si], (uint32_t)g.ss);
+    uint32_t run_g = pre_ge[si], run_e = pre_eq[si];
+    const uint32_t tge = st[ST_TGE], teq = st[ST_TEQ], need_eq = st[ST_NEEDEQ];
+    const int64_t base = g.base + (int64_t)slot * g.ss;
     uint32_t w, b;
     U.decode(unit, B.P, &w, &b);
-    o = ((int64_t)w * B.P + b) * kb;
+    const int64_t o = ((int64_t)w * B.P + b) * kb;
+    for (uint32_t e0 = 0; e0 < cnt; e0 += WAVE * EMIT_R) {
+      int32_t ix[EMIT_R];
+      float vx[EMIT_R];
+#pragma unroll
+      for (int r = 0; r < EMIT_R; ++r) {
+        const uint32_t p = e0 + r * WAVE + lane;
+        ix[r] = -1;
+        vx[r] = 0.f;
+        if (p < cnt) {
+          ix[r] = cand_idx[base + p];
+          vx[r] = cand_val[base + p];
+        }
+      }
+#pragma unroll
+      for (int r = 0; r < EMIT_R; ++r) {
+        const uint32_t p = e0 + r * WAVE + lane;
+        const uint32_t key = mag_key(vx[r]);
+        const bool is_ge = p < cnt && key >= tge;
+        const bool is_eq = p < cnt && need_eq != 0u && key == teq;
+        const uint64_t mg = __ballot(is_ge), me = __ballot(is_eq);
+        if (p < cnt) {
+          const uint32_t ge_pre = run_g + popc64(mg & lt);
+          const uint32_t eq_pre = run_e + popc64(me & lt);
+          const uint32_t sel_before = ge_pre + (eq_pre < need_eq ? eq_pre : need_eq);
+          if (is_ge || (is_eq && eq_pre < need_eq)) {
+            if (sel_before < (uint32_t)kb) {
+              out_idx[o + sel_before] = ix[r];
+              out_val[o + sel_before] = vx[r];
+              if (local_idx) local_idx[o + sel_before] = ix[r];
+            } else {
+              atomicOr(err, ERR_COUNT_POS);
+            }
+          }
+        }
+        run_g += popc64(mg);
+        run_e += popc64(me);
+      }
+    }
+  } else if constexpr (MODE == 0) {
+    constexpr int R1 = EMIT_R1;
+    const int32_t sw = (int32_t)((blockIdx.x % gq) * (4u * SPW) + (uint32_t)wv * SPW);
+    const SlotGeom g = slot_geom(0, unit, B, U, kb);
+    if (sw >= g.nslots) return;
+    const int lane = lane_id();
+    const uint32_t au = U.canon(unit, B.P);   // the unit's arrays
+    const uint32_t* st = state + (int64_t)au * ST_WORDS;
+    // independent loads: every slot's count and prefixes, the unit's threshold
+    uint32_t cnt[SPW], rg[SPW], re[SPW];
+#pragma unroll
+    for (int j = 0; j < SPW; ++j) {
+      cnt[j] = 0u;
+      rg[j] = 0u;
+      re[j] = 0u;
+      if (sw + j < g.nslots) {
+        const int64_t si = (int64_t)au * smax + sw + j;
+        cnt[j] = min(slot_cnt[si], (uint32_t)g.ss);
+        rg[j] = pre_ge[si];
+        re[j] = pre_eq[si];
+      }
+    }
+    const uint32_t tge = st[ST_TGE], teq = st[ST_TEQ], need_eq = st[ST_NEEDEQ];
+    int32_t ix[SPW][R1];
+    float vx[SPW][R1];
+#pragma unroll
+    for (int j = 0; j < SPW; ++j) {
+      const int64_t base = g.base + (int64_t)(sw + j) * g.ss;
+#pragma unroll
+      for (int r = 0; r < R1; ++r) {
+        const uint32_t p = (uint32_t)(r * WAVE + lane);
+        ix[j][r] = -1;
+        vx[j][r] = 0.f;
+        if (p < cnt[j]) {
+          ix[j][r] = cand_idx[base + p];
+          vx[j][r] = cand_val[base + p];
+        }
+      }
+    }
+    uint32_t w, b;
+    U.decode(unit, B.P, &w, &b);
+    const int64_t o = ((int64_t)w * B.P + b) * kb;
+#pragma unroll
+    for (int j = 0; j < SPW; ++j) {
+      if (sw + j >= g.nslots) break;   // wave-uniform
+      const int64_t base = g.base + (int64_t)(sw + j) * g.ss;
+      emit_topk_slot<R1>(cnt[j], rg[j], re[j], tge, teq, need_eq, kb, cand_idx + base, cand_val + base, ix[j], vx[j],
+                     out_idx + o, out_val + o, local_idx ? local_idx + o : nullptr, err);
+    }
   } else {
+    constexpr int NPART = 4;   // waves sharing one slot
+    const int32_t slot = (int32_t)(blockIdx.x % gq);
+    const SlotGeom g = slot_geom(1, unit, B, U, kb);
+    if (slot >= g.nslots) return;   // uniform over the workgroup
+    const int lane = lane_id();
+    const uint64_t lt = __lanemask_lt();
+    const int64_t si = (int64_t)unit * smax + slot;
+    const uint32_t* st = state + (int64_t)unit * ST_WORDS;
+    // independent loads: the slot's count and prefixes, the unit's threshold
+    const uint32_t cnt = min(slot_cnt[si], (uint32_t)g.ss);
+    const uint32_t all_before = pre_all[si];
+    uint32_t run_g = pre_ge[si], run_e = pre_eq[si];
+    const uint32_t tge = st[ST_TGE], teq = st[ST_TEQ], need_eq = st[ST_NEEDEQ];
+    const int64_t base = g.base + (int64_t)slot * g.ss;
     int64_t hb, rb;
     bool both;
     PM.decode(unit, &hb, &rb, &both);
-    o = hb * kb;
-    if (both) o2 = rb * kb;
-  }
-  uint32_t p_lo = 0, p_hi = cnt;
-  if constexpr (NPART > 1) {
-    // this wave's quarter of the slot; add the ge / eq counts of the quarters before it
-    __shared__ uint32_t part_cnt[2 * NPART];
-    const uint32_t qlen = ((uint32_t)g.ss + NPART - 1) / NPART;
-    p_lo = min(cnt, (uint32_t)wv * qlen);
-    p_hi = min(cnt, p_lo + qlen);
-    uint32_t cg = 0, ce = 0;
-    for (uint32_t p0 = p_lo; p0 < p_hi; p0 += WAVE) {   // wave-uniform trip count
-      const uint32_t p = p0 + lane;
-      const uint32_t key = p < p_hi ? mag_key(cand_val[base + p]) : 0u;
-      cg += popc64(__ballot(p < p_hi && key >= tge));
-      ce += popc64(__ballot(p < p_hi && need_eq != 0u && key == teq));
-    }
-    if (lane == 0) {
-      part_cnt[2 * wv] = cg;
-      part_cnt[2 * wv + 1] = ce;
-    }
-    __syncthreads();
-    for (int k = 0; k < wv; ++k) {
-      run_g += part_cnt[2 * k];
-      run_e += part_cnt[2 * k + 1];
-    }
-  }
-  for (uint32_t e0 = p_lo; e0 < p_hi; e0 += WAVE * EMIT_R) {
-    int32_t ix[EMIT_R];
-    float vx[EMIT_R];
-#pragma unroll
-    for (int r = 0; r < EMIT_R; ++r) {
-      const uint32_t p = e0 + r * WAVE + lane;
-      ix[r] = -1;
-      vx[r] = 0.f;
-      if (p < p_hi) {
-        ix[r] = cand_idx[base + p];
-        vx[r] = cand_val[base + p];
+    const int64_t o = hb * kb, o2 = both ? rb * kb : -1;   // output block(s); o2: the other side of an R-SAG exchange
+    uint32_t p_lo = 0, p_hi = cnt;
+    {
+      // this wave's quarter of the slot; add the ge / eq counts of the quarters before it
+      __shared__ uint32_t part_cnt[2 * NPART];
+      const uint32_t qlen = ((uint32_t)g.ss + NPART - 1) / NPART;
+      p_lo = min(cnt, (uint32_t)wv * qlen);
+      p_hi = min(cnt, p_lo + qlen);
+      uint32_t cg = 0, ce = 0;
+      for (uint32_t p0 = p_lo; p0 < p_hi; p0 += WAVE) {   // wave-uniform trip count
+        const uint32_t p = p0 + lane;
+        const uint32_t key = p < p_hi ? mag_key(cand_val[base + p]) : 0u;
+        cg += popc64(__ballot(p < p_hi && key >= tge));
+        ce += popc64(__ballot(p < p_hi && need_eq != 0u && key == teq));
+      }
+      if (lane == 0) {
+        part_cnt[2 * wv] = cg;
+        part_cnt[2 * wv + 1] = ce;
+      }
+      __syncthreads();
+      for (int k = 0; k < wv; ++k) {
+        run_g += part_cnt[2 * k];
+        run_e += part_cnt[2 * k + 1];
       }
     }
+    for (uint32_t e0 = p_lo; e0 < p_hi; e0 += WAVE * EMIT_R) {
+      int32_t ix[EMIT_R];
+      float vx[EMIT_R];
 #pragma unroll
-    for (int r = 0; r < EMIT_R; ++r) {
-      const uint32_t p = e0 + r * WAVE + lane;
-      const uint32_t key = mag_key(vx[r]);
-      const bool is_ge = p < p_hi && key >= tge;
-      const bool is_eq = p < p_hi && need_eq != 0u && key == teq;
-      const uint64_t mg = __ballot(is_ge), me = __ballot(is_eq);
-      if (p < p_hi) {
-        const uint32_t ge_pre = run_g + popc64(mg & lt);
-        const uint32_t eq_pre = run_e + popc64(me & lt);
-        const uint32_t sel_before = ge_pre + (eq_pre < need_eq ? eq_pre : need_eq);
-        const bool sel = is_ge || (is_eq && eq_pre < need_eq);
-        if (sel) {
-          if (sel_before < (uint32_t)kb) {
-            out_idx[o + sel_before] = ix[r];
-            out_val[o + sel_before] = vx[r];
-            if (MODE == 1 && o2 >= 0) {
-              out_idx[o2 + sel_before] = ix[r];
-              out_val[o2 + sel_before] = vx[r];
-            }
-            if (MODE == 0 && local_idx) local_idx[o + sel_before] = ix[r];
-          } else {
-            atomicOr(err, ERR_COUNT_POS);
-          }
-        } else if (MODE == 1) {
-          const uint32_t dpos = all_before + p - sel_before;
-          if (dpos < (uint32_t)kb) {
-            drop_idx[(int64_t)unit * kb + dpos] = ix[r];
-            drop_val[(int64_t)unit * kb + dpos] = vx[r];
-          } else {
-            atomicOr(err, ERR_COUNT_DROP);
-          }
+      for (int r = 0; r < EMIT_R; ++r) {
+        const uint32_t p = e0 + r * WAVE + lane;
+        ix[r] = -1;
+        vx[r] = 0.f;
+        if (p < p_hi) {
+          ix[r] = cand_idx[base + p];
+          vx[r] = cand_val[base + p];
         }
       }
-      run_g += popc64(mg);
-      run_e += popc64(me);
+#pragma unroll
+      for (int r = 0; r < EMIT_R; ++r) {
+        const uint32_t p = e0 + r * WAVE + lane;
+        const uint32_t key = mag_key(vx[r]);
+        const bool is_ge = p < p_hi && key >= tge;
+        const bool is_eq = p < p_hi && need_eq != 0u && key == teq;
+        const uint64_t mg = __ballot(is_ge), me = __ballot(is_eq);
+        if (p < p_hi) {
+          const uint32_t ge_pre = run_g + popc64(mg & lt);
+          const uint32_t eq_pre = run_e + popc64(me & lt);
+          const uint32_t sel_before = ge_pre + (eq_pre < need_eq ? eq_pre : need_eq);
+          const bool sel = is_ge || (is_eq && eq_pre < need_eq);
+          if (sel) {
+            if (sel_before < (uint32_t)kb) {
+              out_idx[o + sel_before] = ix[r];
+              out_val[o + sel_before] = vx[r];
+              if (o2 >= 0) {
+                out_idx[o2 + sel_before] = ix[r];
+                out_val[o2 + sel_before] = vx[r];
+              }
+            } else {
+              atomicOr(err, ERR_COUNT_POS);
+            }
+          } else {
+            const uint32_t dpos = all_before + p - sel_before;
+            if (dpos < (uint32_t)kb) {
+              drop_idx[(int64_t)unit * kb + dpos] = ix[r];
+              drop_val[(int64_t)unit * kb + dpos] = vx[r];
+            } else {
+              atomicOr(err, ERR_COUNT_DROP);
+            }
+          }
+        }
+        run_g += popc64(mg);
+        run_e += popc64(me);
+      }
     }
   }
 }
@@ -1211,11 +1476,14 @@ hipError_t launch_collect(const float* acc, int64_t ld_acc, int64_t nunits, cons
                           bool vec4, int32_t smax, const uint32_t* state, const uint32_t* spec_cnt,
                           int32_t add_tiles, uint32_t* slot_cnt, uint32_t* slot_nbin, int32_t* cand_idx,
                           float* cand_val, uint32_t* bin_key, hipStream_t s) {
-  const uint32_t gq = (uint32_t)((smax + COLLECT_GROUP - 1) / COLLECT_GROUP);
+  // the speculative path exists for float4 rows only (the add writes no candidates otherwise)
+  const int spw = vec4 && nunits * smax >= MULTI_SLOT_MIN ? 2 : 1;
+  const uint32_t gq = (uint32_t)((smax + 4 * spw - 1) / (4 * spw));
   const dim3 grid((unsigned)(nunits * gq));
   const Blocks B = make_blocks(n, P);
-  if (vec4) hipLaunchKernelGGL(k_collect<4>, grid, dim3(256), 0, s, acc, ld_acc, B, U, (uint32_t)smax, gq, state, spec_cnt, (uint32_t)add_tiles, slot_cnt, slot_nbin, cand_idx, cand_val, bin_key);
-  else hipLaunchKernelGGL(k_collect<1>, grid, dim3(256), 0, s, acc, ld_acc, B, U, (uint32_t)smax, gq, state, spec_cnt, (uint32_t)add_tiles, slot_cnt, slot_nbin, cand_idx, cand_val, bin_key);
+  if (spw == 2) hipLaunchKernelGGL((k_collect<4, 2>), grid, dim3(256), 0, s, acc, ld_acc, B, U, (uint32_t)smax, gq, state, spec_cnt, (uint32_t)add_tiles, slot_cnt, slot_nbin, cand_idx, cand_val, bin_key);
+  else if (vec4) hipLaunchKernelGGL((k_collect<4, 1>), grid, dim3(256), 0, s, acc, ld_acc, B, U, (uint32_t)smax, gq, state, spec_cnt, (uint32_t)add_tiles, slot_cnt, slot_nbin, cand_idx, cand_val, bin_key);
+  else hipLaunchKernelGGL((k_collect<1, 1>), grid, dim3(256), 0, s, acc, ld_acc, B, U, (uint32_t)smax, gq, state, spec_cnt, (uint32_t)add_tiles, slot_cnt, slot_nbin, cand_idx, cand_val, bin_key);
   return hipGetLastError();
 }
 
@@ -1281,11 +1549,14 @@ hipError_t launch_emit(int mode, const int32_t* cand_idx, const float* cand_val,
                        const uint32_t* slot_cnt, const uint32_t* pre_all, const uint32_t* pre_ge,
                        const uint32_t* pre_eq, int32_t* out_idx, float* out_val, int32_t* local_idx,
                        int32_t* drop_idx, float* drop_val, uint32_t* err, hipStream_t s) {
-  // block top-k: four slots (one per wave) per workgroup; merge: one slot per workgroup
-  const uint32_t gq = mode == 0 ? (uint32_t)((smax + 3) / 4) : (uint32_t)smax;
+  // block top-k: 4 spw slots per workgroup (spw per wave); merge: one slot per workgroup
+  const int spw = mode == 0 && nunits * smax >= MULTI_SLOT_MIN ? 2 : 1;
+  const uint32_t gq = mode == 0 ? (uint32_t)((smax + 4 * spw - 1) / (4 * spw)) : (uint32_t)smax;
   const dim3 grid((unsigned)(nunits * gq));
   const Blocks B = make_blocks(n, P);
-  if (mode == 0)
+  if (mode == 0 && spw == 2)
+    hipLaunchKernelGGL((k_emit<0, 2>), grid, dim3(256), 0, s, cand_idx, cand_val, B, U, PM, kb, smax, gq, state, slot_cnt, pre_all, pre_ge, pre_eq, out_idx, out_val, local_idx, drop_idx, drop_val, err);
+  else if (mode == 0)
     hipLaunchKernelGGL(k_emit<0>, grid, dim3(256), 0, s, cand_idx, cand_val, B, U, PM, kb, smax, gq, state, slot_cnt, pre_all, pre_ge, pre_eq, out_idx, out_val, local_idx, drop_idx, drop_val, err);
   else
     hipLaunchKernelGGL(k_emit<1>, grid, dim3(256), 0, s, cand_idx, cand_val, B, U, PM, kb, smax, gq, state, slot_cnt, pre_all, pre_ge, pre_eq, out_idx, out_val, local_idx, drop_idx, drop_val, err);
