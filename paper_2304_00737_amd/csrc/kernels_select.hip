@@ -359,7 +359,9 @@ __device__ __forceinline__ void recollect_wave_pre(uint32_t c0, uint32_t c1, uin
 // (when a call has many sparse slots, one slot per wave leaves the wave
 // waiting on memory most of the time); otherwise the workgroup collects the
 // group's slots from acc one by one.  64 registers let 8 waves share a SIMD.
-constexpr int64_t MULTI_SLOT_MIN = 1 << 17;   // slots per call from which waves take 2 slots each
+// Slots per call from which the block top-k's collect and emit give each wave
+// 2 slots and its staged threshold takes 256 slots per workgroup.
+constexpr int64_t MULTI_SLOT_MIN = 1 << 17;
 template <int VEC, int SPW>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(8, 8))) void k_collect(const float* __restrict__ acc, int64_t ld_acc, Blocks B, Units U,
                                                  uint32_t smax, uint32_t gq, const uint32_t* __restrict__ state,
@@ -909,34 +911,81 @@ __global__ __launch_bounds__(1024) void k_thresh(Blocks B, Units U, int32_t kb, 
 //   per-slot counts of selected-by-key and tied keys (slot groups);
 //   per-unit exclusive scans into pre_all / pre_ge / pre_eq.
 // They write exactly what k_thresh writes.
-constexpr int BIG_GROUP0 = 64;   // block top-k: slots per workgroup (a wave per slot in turn)
+constexpr int BIG_THREADS = 256;  // threads of the slot-group kernels
+constexpr int BIG_R0 = 4;         // block top-k: bin entries per thread in flight
+// block top-k: slots per workgroup: 64, a wave per slot in turn, or, when the
+// call has at least MULTI_SLOT_MIN slots (sparse bins), 256, one per thread,
+// their bin entries walked as one flattened list
+constexpr int BIG_GROUP0 = 64;
+constexpr int BIG_GROUP0_MANY = BIG_THREADS;
 
-
-
-// f(key, slot) for every threshold-bin entry of slots [s0, s1): block top-k:
-// the keys the collect stored, a wave per slot; merge: the union entries whose
-// key is in bin T1, the whole workgroup per slot.
-template <int mode, typename F>
-__device__ __forceinline__ void visit_bin_slots(const SlotGeom& g, int32_t s0, int32_t s1,
-                                                const uint32_t* __restrict__ K, const float* __restrict__ V,
-                                                const uint32_t* __restrict__ cnt, const uint32_t* __restrict__ nbn,
-                                                uint32_t T1, F f) {
-  if constexpr (mode == 0) {
-    const int nw = blockDim.x / WAVE;
-    for (int32_t slot = s0 + wave_id(); slot < s1; slot += nw) {
-      const int64_t room = g.len - (int64_t)slot * g.ss;   // entries of the region in this slot
-      const uint32_t nb = (uint32_t)min(min((int64_t)nbn[slot], (int64_t)g.ss), room);
-      const uint32_t* __restrict__ Ks = K + (int64_t)slot * g.ss;
-      for (uint32_t j = lane_id(); j < nb; j += WAVE) f(Ks[j], slot);
-    }
-  } else {
-    for (int32_t slot = s0; slot < s1; ++slot) {
-      const uint32_t c = min(cnt[slot], (uint32_t)g.ss);
-      const float* __restrict__ Vs = V + (int64_t)slot * g.ss;
-      for (uint32_t j = threadIdx.x; j < c; j += blockDim.x) {
-        const uint32_t key = mag_key(Vs[j]);
-        if ((key >> D1_SHIFT) == T1) f(key, slot);
+// The bin entries of the block top-k slots s0 .. s0 + group - 1 (one per
+// thread; my_nb: the thread's slot's count, 0 for threads past them) taken as
+// one flattened list, so that every load of the group is in flight at once
+// instead of one slot's after another's: f(key, slot - s0) for each.  The
+// slot of entry e is the last one whose exclusive prefix is at most e.
+// Workgroups of BIG_THREADS threads; `pref` holds BIG_THREADS words of LDS,
+// `scratch` 5.  Contains barriers.
+template <typename F>
+__device__ __forceinline__ void visit_bin_group(const SlotGeom& g, int32_t s0, int32_t group,
+                                                const uint32_t* __restrict__ K, uint32_t my_nb, uint32_t* pref,
+                                                uint32_t* scratch, F f) {
+  uint32_t total;
+  pref[threadIdx.x] = block_excl_scan(my_nb, scratch, &total);
+  __syncthreads();
+  for (uint32_t e0 = 0; e0 < total; e0 += (uint32_t)(BIG_THREADS * BIG_R0)) {
+    uint32_t key[BIG_R0];
+    int32_t sl[BIG_R0];
+#pragma unroll
+    for (int r = 0; r < BIG_R0; ++r) {
+      const uint32_t e = e0 + (uint32_t)(r * BIG_THREADS) + threadIdx.x;
+      sl[r] = -1;
+      key[r] = 0u;
+      if (e < total) {
+        int32_t lo = 0, hi = group;   // threads past the group hold no entries
+        while (hi - lo > 1) {
+          const int32_t mid = (lo + hi) >> 1;
+          if (pref[mid] <= e) lo = mid;
+          else hi = mid;
+        }
+        sl[r] = lo;
+        key[r] = K[(int64_t)(s0 + lo) * g.ss + (e - pref[lo])];
       }
+    }
+#pragma unroll
+    for (int r = 0; r < BIG_R0; ++r)
+      if (sl[r] >= 0) f(key[r], sl[r]);
+  }
+}
+
+// f(key, slot) for every threshold-bin entry of the block top-k slots
+// [s0, s1), a wave per slot in turn (groups of BIG_GROUP0 slots, whose bins
+// are fuller: the flattened walk's searches cost more than they save there).
+template <typename F>
+__device__ __forceinline__ void visit_bin_slots_topk(const SlotGeom& g, int32_t s0, int32_t s1,
+                                                     const uint32_t* __restrict__ K,
+                                                     const uint32_t* __restrict__ nbn, F f) {
+  const int nw = blockDim.x / WAVE;
+  for (int32_t slot = s0 + wave_id(); slot < s1; slot += nw) {
+    const int64_t room = g.len - (int64_t)slot * g.ss;   // entries of the region in this slot
+    const uint32_t nb = (uint32_t)min(min((int64_t)nbn[slot], (int64_t)g.ss), room);
+    const uint32_t* __restrict__ Ks = K + (int64_t)slot * g.ss;
+    for (uint32_t j = lane_id(); j < nb; j += WAVE) f(Ks[j], slot);
+  }
+}
+
+// f(key, slot) for every threshold-bin entry of the merge slots [s0, s1):
+// the union entries whose key is in bin T1, the whole workgroup per slot.
+template <typename F>
+__device__ __forceinline__ void visit_bin_slots_merge(const SlotGeom& g, int32_t s0, int32_t s1,
+                                                      const float* __restrict__ V, const uint32_t* __restrict__ cnt,
+                                                      uint32_t T1, F f) {
+  for (int32_t slot = s0; slot < s1; ++slot) {
+    const uint32_t c = min(cnt[slot], (uint32_t)g.ss);
+    const float* __restrict__ Vs = V + (int64_t)slot * g.ss;
+    for (uint32_t j = threadIdx.x; j < c; j += blockDim.x) {
+      const uint32_t key = mag_key(Vs[j]);
+      if ((key >> D1_SHIFT) == T1) f(key, slot);
     }
   }
 }
@@ -1003,12 +1052,27 @@ __global__ __launch_bounds__(256) void k_big_hist(BigArgs a, uint32_t ngroups) {
   const int32_t s0 = grp * a.group, s1 = min(g.nslots, s0 + a.group);
   if (s0 >= s1) return;
   for (int i = threadIdx.x; i < NB; i += blockDim.x) h[i] = 0u;
-  __syncthreads();
-  visit_bin_slots<mode>(g, s0, s1, a.bin_key + g.base, a.U_val + g.base, a.slot_cnt + ua * a.smax,
-                        a.slot_nbin + ua * a.smax, T1, [&](uint32_t key, int32_t) {
-                          if (LEVEL == 2) atomicAdd(&h[(key >> D2_SHIFT) & (NB2 - 1)], 1u);
-                          else if ((key >> D2_SHIFT) == pre23) atomicAdd(&h[key & (NB3 - 1)], 1u);
-                        });
+  auto bump = [&](uint32_t key, int32_t) {
+    if (LEVEL == 2) atomicAdd(&h[(key >> D2_SHIFT) & (NB2 - 1)], 1u);
+    else if ((key >> D2_SHIFT) == pre23) atomicAdd(&h[key & (NB3 - 1)], 1u);
+  };
+  if (mode == 0 && a.group == BIG_GROUP0_MANY) {
+    __shared__ uint32_t pref[BIG_THREADS];
+    __shared__ uint32_t scratch[8];
+    const int32_t slot = s0 + (int32_t)threadIdx.x;
+    uint32_t nb = 0u;
+    if (slot < s1) {
+      const int64_t room = g.len - (int64_t)slot * g.ss;   // entries of the region in this slot
+      nb = (uint32_t)min(min((int64_t)a.slot_nbin[ua * a.smax + slot], (int64_t)g.ss), room);
+    }
+    visit_bin_group(g, s0, a.group, a.bin_key + g.base, nb, pref, scratch, bump);   // its first barrier orders the zeroing
+  } else if (mode == 0) {
+    __syncthreads();
+    visit_bin_slots_topk(g, s0, s1, a.bin_key + g.base, a.slot_nbin + ua * a.smax, bump);
+  } else {
+    __syncthreads();
+    visit_bin_slots_merge(g, s0, s1, a.U_val + g.base, a.slot_cnt + ua * a.smax, T1, bump);
+  }
   __syncthreads();
   uint32_t* H = a.hist1 + ua * a.hstride + (LEVEL == 2 ? 0 : NB2);
   for (int i = threadIdx.x; i < NB; i += blockDim.x) {
@@ -1083,7 +1147,7 @@ __global__ __launch_bounds__(256) void k_big_count(BigArgs a, uint32_t ngroups) 
   const uint32_t* __restrict__ cnt = a.slot_cnt + ua * a.smax;
   const uint32_t* __restrict__ nbn = a.slot_nbin + ua * a.smax;
   const int64_t o = ua * a.smax;
-  if constexpr (mode == 0) {
+  if (mode == 0 && a.group != BIG_GROUP0_MANY) {
     // a wave per slot: the entries above the bin are selected; count the bin's keys
     const int nw = blockDim.x / WAVE;
     for (int32_t slot = s0 + wave_id(); slot < s1; slot += nw) {
@@ -1103,6 +1167,30 @@ __global__ __launch_bounds__(256) void k_big_count(BigArgs a, uint32_t ngroups) 
         a.pre_ge[o + slot] = (c - nb) + ge;
         a.pre_eq[o + slot] = eq;
       }
+    }
+  } else if (mode == 0) {
+    // a thread per slot: the entries above the bin are selected; the bin's
+    // keys, flattened over the group, are counted into LDS per slot
+    __shared__ uint32_t pref[BIG_THREADS], sge[BIG_THREADS], seq[BIG_THREADS];
+    __shared__ uint32_t scratch[8];
+    if (s0 >= s1) return;   // uniform
+    const int32_t slot = s0 + (int32_t)threadIdx.x;
+    uint32_t c = 0u, nb = 0u;
+    if (slot < s1) {
+      const int64_t room = g.len - (int64_t)slot * g.ss;
+      c = (uint32_t)min(min((int64_t)cnt[slot], (int64_t)g.ss), room);
+      nb = min(nbn[slot], c);
+    }
+    sge[threadIdx.x] = 0u;
+    seq[threadIdx.x] = 0u;   // ordered before the visits by the scan's barriers
+    visit_bin_group(g, s0, a.group, a.bin_key + g.base, nb, pref, scratch, [&](uint32_t key, int32_t ls) {
+      if (key >= tge) atomicAdd(&sge[ls], 1u);
+      else if (need_eq != 0u && key == teq) atomicAdd(&seq[ls], 1u);
+    });
+    __syncthreads();
+    if (slot < s1) {
+      a.pre_ge[o + slot] = (c - nb) + sge[threadIdx.x];
+      a.pre_eq[o + slot] = seq[threadIdx.x];
     }
   } else {
     (void)T1;
@@ -1502,7 +1590,7 @@ hipError_t launch_thresh(int mode, int64_t nunits, const Units& U, int64_t n, in
     a.mode = mode;
     a.kb = kb;
     a.smax = smax;
-    a.group = mode == 0 ? BIG_GROUP0 : 1;
+    a.group = mode == 0 ? (nunits * smax >= MULTI_SLOT_MIN ? BIG_GROUP0_MANY : BIG_GROUP0) : 1;
     a.hstride = mode == 0 ? (int64_t)HCOPIES * NB1 : NB1;
     a.hist1 = hist1;
     a.U_val = U_val;
