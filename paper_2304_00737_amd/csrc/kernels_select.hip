@@ -540,27 +540,32 @@ __device__ __forceinline__ void finish_unit(uint32_t* st, uint32_t T1, uint32_t 
 }
 
 // Merge unit with at most FAST_ROWS slots: row r of the register file is slot
-// r; thread t holds merged positions 4t .. 4t+3 of every slot.
+// r; thread t holds merged positions 4t .. 4t+3 of every slot.  The caller
+// loads the union (fast_merge_load) before its level-1 select, so that the
+// loads overlap the select's barriers.
+__device__ __forceinline__ void fast_merge_load(const SlotGeom& g, const float* __restrict__ V,
+                                                const uint32_t* __restrict__ cnt, uint32_t (&c)[FAST_ROWS],
+                                                f4v (&v)[FAST_ROWS]) {
+  const f4v* __restrict__ V4 = reinterpret_cast<const f4v*>(V);
+#pragma unroll
+  for (int r = 0; r < FAST_ROWS; ++r) {
+    c[r] = 0u;
+    v[r] = f4v{0.f, 0.f, 0.f, 0.f};
+    if (r < g.nslots) {
+      c[r] = cnt[r];
+      v[r] = V4[r * (MERGE_TILE / 4) + threadIdx.x];
+    }
+  }
+}
+
 __device__ __forceinline__ void thresh_fast_merge(FastSmem& L, int64_t unit, const SlotGeom& g, int32_t kb,
-                                                  int32_t smax, const float* __restrict__ V,
-                                                  const uint32_t* __restrict__ cnt, uint32_t T1, uint32_t need1,
+                                                  int32_t smax, const uint32_t (&c)[FAST_ROWS],
+                                                  const f4v (&v)[FAST_ROWS], uint32_t T1, uint32_t need1,
                                                   uint32_t cnt1, uint32_t* st, uint32_t* __restrict__ pre_all,
                                                   uint32_t* __restrict__ pre_ge, uint32_t* __restrict__ pre_eq,
                                                   int32_t* __restrict__ drop_cnt, uint32_t* err, uint32_t hist_total) {
   const int t = threadIdx.x, lane = lane_id(), wv = wave_id();
   const int ns = g.nslots;
-  const f4v* __restrict__ V4 = reinterpret_cast<const f4v*>(V);
-  uint32_t c[FAST_ROWS];
-  f4v v[FAST_ROWS];
-#pragma unroll
-  for (int r = 0; r < FAST_ROWS; ++r) {
-    c[r] = 0u;
-    v[r] = f4v{0.f, 0.f, 0.f, 0.f};
-    if (r < ns) {
-      c[r] = cnt[r];
-      v[r] = V4[r * (MERGE_TILE / 4) + t];
-    }
-  }
   uint32_t key[FAST_ROWS][4];
 #pragma unroll
   for (int r = 0; r < FAST_ROWS; ++r) {
@@ -869,7 +874,10 @@ __global__ __launch_bounds__(1024) void k_thresh(Blocks B, Units U, int32_t kb, 
   // ---- level 1
   uint32_t T1, need1, cnt1;
   uint32_t hist_total = 0;
+  uint32_t mc[mode == 1 ? FAST_ROWS : 1];
+  f4v mv[mode == 1 ? FAST_ROWS : 1];
   if constexpr (mode == 1) {
+    if (g.nslots <= FAST_ROWS) fast_merge_load(g, V, cnt, mc, mv);   // uniform
     uint32_t* __restrict__ H = hist1 + unit * NB1;
     g2lds<NB1 / NT>(L.h, H, NB1);
 #pragma unroll
@@ -886,7 +894,7 @@ __global__ __launch_bounds__(1024) void k_thresh(Blocks B, Units U, int32_t kb, 
   }
   if constexpr (mode == 1) {
     if (g.nslots <= FAST_ROWS) {
-      thresh_fast_merge(S.f, unit, g, kb, smax, V, cnt, T1, need1, cnt1, st, pre_all, pre_ge, pre_eq, drop_cnt,
+      thresh_fast_merge(S.f, unit, g, kb, smax, mc, mv, T1, need1, cnt1, st, pre_all, pre_ge, pre_eq, drop_cnt,
                         err, hist_total);
       return;
     }
@@ -1474,17 +1482,30 @@ __global__ __launch_bounds__(256) void k_emit(
     bool both;
     PM.decode(unit, &hb, &rb, &both);
     const int64_t o = hb * kb, o2 = both ? rb * kb : -1;   // output block(s); o2: the other side of an R-SAG exchange
-    uint32_t p_lo = 0, p_hi = cnt;
+    // this wave's quarter of the slot, loaded once into registers (a quarter
+    // is one chunk); the ge / eq counts of the quarters before it through LDS
+    static_assert(MERGE_TILE == NPART * WAVE * EMIT_R, "a quarter of a merge slot is one chunk");
+    __shared__ uint32_t part_cnt[2 * NPART];
+    const uint32_t p_lo = min(cnt, (uint32_t)(wv * WAVE * EMIT_R));
+    const uint32_t p_hi = min(cnt, p_lo + (uint32_t)(WAVE * EMIT_R));
+    int32_t ix[EMIT_R];
+    float vx[EMIT_R];
+#pragma unroll
+    for (int r = 0; r < EMIT_R; ++r) {
+      const uint32_t p = p_lo + r * WAVE + lane;
+      ix[r] = -1;
+      vx[r] = 0.f;
+      if (p < p_hi) {
+        ix[r] = cand_idx[base + p];
+        vx[r] = cand_val[base + p];
+      }
+    }
     {
-      // this wave's quarter of the slot; add the ge / eq counts of the quarters before it
-      __shared__ uint32_t part_cnt[2 * NPART];
-      const uint32_t qlen = ((uint32_t)g.ss + NPART - 1) / NPART;
-      p_lo = min(cnt, (uint32_t)wv * qlen);
-      p_hi = min(cnt, p_lo + qlen);
       uint32_t cg = 0, ce = 0;
-      for (uint32_t p0 = p_lo; p0 < p_hi; p0 += WAVE) {   // wave-uniform trip count
-        const uint32_t p = p0 + lane;
-        const uint32_t key = p < p_hi ? mag_key(cand_val[base + p]) : 0u;
+#pragma unroll
+      for (int r = 0; r < EMIT_R; ++r) {
+        const uint32_t p = p_lo + r * WAVE + lane;
+        const uint32_t key = mag_key(vx[r]);
         cg += popc64(__ballot(p < p_hi && key >= tge));
         ce += popc64(__ballot(p < p_hi && need_eq != 0u && key == teq));
       }
@@ -1498,19 +1519,8 @@ __global__ __launch_bounds__(256) void k_emit(
         run_e += part_cnt[2 * k + 1];
       }
     }
-    for (uint32_t e0 = p_lo; e0 < p_hi; e0 += WAVE * EMIT_R) {
-      int32_t ix[EMIT_R];
-      float vx[EMIT_R];
-#pragma unroll
-      for (int r = 0; r < EMIT_R; ++r) {
-        const uint32_t p = e0 + r * WAVE + lane;
-        ix[r] = -1;
-        vx[r] = 0.f;
-        if (p < p_hi) {
-          ix[r] = cand_idx[base + p];
-          vx[r] = cand_val[base + p];
-        }
-      }
+    {
+      const uint32_t e0 = p_lo;
 #pragma unroll
       for (int r = 0; r < EMIT_R; ++r) {
         const uint32_t p = e0 + r * WAVE + lane;
