@@ -921,6 +921,7 @@ __global__ __launch_bounds__(1024) void k_thresh(Blocks B, Units U, int32_t kb, 
 // They write exactly what k_thresh writes.
 constexpr int BIG_THREADS = 256;  // threads of the slot-group kernels
 constexpr int BIG_R0 = 4;         // block top-k: bin entries per thread in flight
+constexpr int BIG_R1 = MERGE_TILE / BIG_THREADS;   // merge: union entries per thread in flight (a slot)
 // block top-k: slots per workgroup: 64, a wave per slot in turn, or, when the
 // call has at least MULTI_SLOT_MIN slots (sparse bins), 256, one per thread,
 // their bin entries walked as one flattened list
@@ -991,9 +992,18 @@ __device__ __forceinline__ void visit_bin_slots_merge(const SlotGeom& g, int32_t
   for (int32_t slot = s0; slot < s1; ++slot) {
     const uint32_t c = min(cnt[slot], (uint32_t)g.ss);
     const float* __restrict__ Vs = V + (int64_t)slot * g.ss;
-    for (uint32_t j = threadIdx.x; j < c; j += blockDim.x) {
-      const uint32_t key = mag_key(Vs[j]);
-      if ((key >> D1_SHIFT) == T1) f(key, slot);
+    for (uint32_t j0 = 0; j0 < c; j0 += BIG_THREADS * BIG_R1) {   // a merge slot is one chunk
+      float v[BIG_R1];
+#pragma unroll
+      for (int r = 0; r < BIG_R1; ++r) {
+        const uint32_t j = j0 + (uint32_t)(r * BIG_THREADS) + threadIdx.x;
+        v[r] = j < c ? Vs[j] : 0.f;
+      }
+#pragma unroll
+      for (int r = 0; r < BIG_R1; ++r) {
+        const uint32_t key = mag_key(v[r]);
+        if (j0 + (uint32_t)(r * BIG_THREADS) + threadIdx.x < c && (key >> D1_SHIFT) == T1) f(key, slot);
+      }
     }
   }
 }
@@ -1206,10 +1216,20 @@ __global__ __launch_bounds__(256) void k_big_count(BigArgs a, uint32_t ngroups) 
       const uint32_t c = min(cnt[slot], (uint32_t)g.ss);
       const float* __restrict__ Vs = a.U_val + g.base + (int64_t)slot * g.ss;
       uint32_t ge = 0, eq = 0;
-      for (uint32_t j = threadIdx.x; j < c; j += blockDim.x) {
-        const uint32_t key = mag_key(Vs[j]);
-        ge += key >= tge;
-        eq += need_eq != 0u && key == teq;
+      for (uint32_t j0 = 0; j0 < c; j0 += BIG_THREADS * BIG_R1) {   // a merge slot is one chunk
+        float v[BIG_R1];
+#pragma unroll
+        for (int r = 0; r < BIG_R1; ++r) {
+          const uint32_t j = j0 + (uint32_t)(r * BIG_THREADS) + threadIdx.x;
+          v[r] = j < c ? Vs[j] : 0.f;
+        }
+#pragma unroll
+        for (int r = 0; r < BIG_R1; ++r) {
+          const uint32_t key = mag_key(v[r]);
+          const bool in = j0 + (uint32_t)(r * BIG_THREADS) + threadIdx.x < c;
+          ge += in && key >= tge;
+          eq += in && need_eq != 0u && key == teq;
+        }
       }
       ge = wave_sum(ge);
       eq = wave_sum(eq);

@@ -135,6 +135,7 @@ __global__ __launch_bounds__(256) void k_lsel_hist(ListSel S, uint32_t nch, uint
 }
 
 // st[4 i ..]: key bound tge, tie key teq, ties to keep need_eq, entries kept
+constexpr int LSEL_R = 8;   // list entries per thread in flight in the threshold's scans
 __global__ __launch_bounds__(1024) void k_lsel_level(ListSel S, uint32_t* __restrict__ hist,
                                                      uint32_t* __restrict__ st, uint32_t* __restrict__ err) {
   __shared__ uint32_t h[NB1];
@@ -156,10 +157,19 @@ __global__ __launch_bounds__(1024) void k_lsel_level(ListSel S, uint32_t* __rest
       if (threadIdx.x == 0) atomicOr(err, ERR_COUNT);
     } else {
       resolve_low_digits(T1, D.c - above1, cnt1, h, scratch, err,
-                         [&](auto f) {
-                           for (uint32_t j = threadIdx.x; j < D.len; j += NT) {
-                             const uint32_t key = mag_key(D.iv[j]);
-                             if ((key >> D1_SHIFT) == T1) f(key);
+                         [&](auto f) {   // LSEL_R loads per thread in flight
+                           for (uint32_t j0 = 0; j0 < D.len; j0 += NT * LSEL_R) {
+                             float v[LSEL_R];
+#pragma unroll
+                             for (int r = 0; r < LSEL_R; ++r) {
+                               const uint32_t j = j0 + (uint32_t)r * NT + threadIdx.x;
+                               v[r] = j < D.len ? D.iv[j] : 0.f;
+                             }
+#pragma unroll
+                             for (int r = 0; r < LSEL_R; ++r) {
+                               const uint32_t key = mag_key(v[r]);
+                               if (j0 + (uint32_t)r * NT + threadIdx.x < D.len && (key >> D1_SHIFT) == T1) f(key);
+                             }
                            }
                          },
                          tge, teq, need_eq);
@@ -270,6 +280,30 @@ __global__ __launch_bounds__(256) void k_lsel_emit(ListSel S, uint32_t nch, cons
 // indices (pass 1) or writes them in index order after the counts of the
 // tiles before it (pass 2).  Tile 0 of each block also records N_q.
 constexpr uint32_t UT = UNION_TILE;
+constexpr uint32_t UNION_TEAMS = 8;   // teams whose ranges are searched together (two waves each)
+static_assert(2 * UNION_TEAMS <= 1024 / WAVE, "two waves of the union workgroup per team of a batch");
+
+// First position m in [0, len) with a[m] >= bound (len if none), a sorted
+// ascending; one wave, 64 probes per round (three rounds for 64000 entries).
+__device__ __forceinline__ uint32_t wave_lower_bound(const int32_t* __restrict__ a, uint32_t len, int32_t bound) {
+  const uint32_t lane = (uint32_t)lane_id();
+  uint32_t l = 0, h = len;   // the answer lies in [l, h]
+  while (h > l) {
+    const uint32_t S = h - l;
+    if (S <= (uint32_t)WAVE) {
+      l += (uint32_t)popc64(__ballot(lane < S && a[l + lane] < bound));
+      break;
+    }
+    // probe k at l + S (k + 1) / (WAVE + 1) < h; the true probes are a prefix
+    const uint32_t m = l + (uint32_t)(((uint64_t)S * (lane + 1u)) / (WAVE + 1u));
+    const uint32_t t = (uint32_t)popc64(__ballot(a[m] < bound));
+    const uint32_t nl = t == 0u ? l : l + (uint32_t)(((uint64_t)S * t) / (WAVE + 1u)) + 1u;
+    const uint32_t nh = t == (uint32_t)WAVE ? h : l + (uint32_t)(((uint64_t)S * (t + 1u)) / (WAVE + 1u));
+    l = nl;
+    h = nh;
+  }
+  return l;
+}
 
 template <bool WRITE>
 __global__ __launch_bounds__(1024) void k_bsag_union(const int32_t* __restrict__ kept_i,
@@ -282,7 +316,7 @@ __global__ __launch_bounds__(1024) void k_bsag_union(const int32_t* __restrict__
   __shared__ float vals[WRITE ? UT : 1];
   __shared__ uint32_t bits[UT / 32];
   __shared__ uint32_t sc[24];
-  __shared__ uint32_t range[2];
+  __shared__ uint32_t range[2 * UNION_TEAMS];
   const uint32_t q = blockIdx.x / ntile, tile = blockIdx.x % ntile, Q = B.P;
   const uint32_t s = B.start(q), e = B.start(q + 1u);
   const uint32_t lo = s + tile * UT;
@@ -293,29 +327,31 @@ __global__ __launch_bounds__(1024) void k_bsag_union(const int32_t* __restrict__
   const uint32_t hi = min(e, lo + UT);
   const uint32_t c = min(cnt[q], kb);
   for (uint32_t w = threadIdx.x; w < UT / 32; w += NT) bits[w] = 0u;
-  for (uint32_t tau = 0; tau < d; ++tau) {
-    const int64_t o = ((int64_t)tau * Q + q) * kb;
-    if (threadIdx.x < 2) {   // first entry at or above lo (thread 0) and hi (thread 1)
-      const int32_t bound = (int32_t)(threadIdx.x == 0 ? lo : hi);
-      uint32_t l2 = 0, h2 = c;
-      while (l2 < h2) {
-        const uint32_t m = (l2 + h2) >> 1;
-        if (kept_i[o + m] < bound) l2 = m + 1;
-        else h2 = m;
-      }
-      range[threadIdx.x] = l2;
+  for (uint32_t t0 = 0; t0 < d; t0 += UNION_TEAMS) {
+    const uint32_t nt = min(d - t0, UNION_TEAMS);
+    __syncthreads();   // the previous batch's ranges have been read
+    // the tile's range in each team's list: wave 2k finds the first entry of
+    // team t0 + k at or above lo, wave 2k + 1 the first at or above hi
+    const uint32_t sx = (uint32_t)wave_id();
+    if (sx < 2u * nt) {
+      const int64_t o = ((int64_t)(t0 + sx / 2u) * Q + q) * kb;
+      const uint32_t r = wave_lower_bound(kept_i + o, c, (int32_t)((sx & 1u) ? hi : lo));
+      if (lane_id() == 0) range[sx] = r;
     }
-    __syncthreads();   // also orders this team's additions after the previous team's
-    const uint32_t a = range[0], b = range[1];
-    for (uint32_t j = a + threadIdx.x; j < b; j += NT) {
-      const uint32_t r = (uint32_t)kept_i[o + j] - lo, bit = 1u << (r & 31u);
-      const uint32_t old = atomicOr(&bits[r >> 5], bit);
-      if (WRITE) {
-        const float v = kept_v[o + j];
-        vals[r] = (old & bit) ? vals[r] + v : v;
+    __syncthreads();   // also orders the zeroing above before the first additions
+    for (uint32_t k = 0; k < nt; ++k) {
+      const int64_t o = ((int64_t)(t0 + k) * Q + q) * kb;
+      const uint32_t a = range[2u * k], b = range[2u * k + 1u];
+      for (uint32_t j = a + threadIdx.x; j < b; j += NT) {
+        const uint32_t r = (uint32_t)kept_i[o + j] - lo, bit = 1u << (r & 31u);
+        const uint32_t old = atomicOr(&bits[r >> 5], bit);
+        if (WRITE) {
+          const float v = kept_v[o + j];
+          vals[r] = (old & bit) ? vals[r] + v : v;
+        }
       }
+      __syncthreads();   // this team's additions before the next team's
     }
-    __syncthreads();
   }
   const uint32_t words = (hi - lo + 31u) >> 5;
   const uint32_t m0 = threadIdx.x < words ? bits[threadIdx.x] : 0u;   // words <= UT / 32 = 512 < NT
