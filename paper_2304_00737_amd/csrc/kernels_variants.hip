@@ -417,13 +417,15 @@ __global__ __launch_bounds__(1024) void k_bsag_union(const int32_t* __restrict__
 // k_blk entries (LAZY_CHUNK per workgroup with hist1, else 256 per sweep),
 // y over pairs (w, t).
 constexpr uint32_t LAZY_CHUNK = 4096;
+constexpr int LAZY_R = LAZY_CHUNK / 256;   // entries per thread of a receipt chunk
 
+template <bool HIST>   // HIST: hist1 is given (receive only); the two forms get their own registers
 __global__ __launch_bounds__(256) void k_lazy_step(float* __restrict__ acc, int64_t ld_acc, Blocks B, uint32_t kb,
                                                    uint32_t d, uint32_t m, const int32_t* __restrict__ sp_idx,
                                                    const float* __restrict__ sp_val, float* __restrict__ saved,
                                                    const uint32_t* __restrict__ bm, int restore,
                                                    uint32_t* __restrict__ hist1, uint32_t* __restrict__ spec_used) {
-  __shared__ uint32_t dh[NB1];   // histogram deltas (receive with hist1)
+  __shared__ uint32_t dh[HIST ? NB1 : 1];   // histogram deltas
   const uint32_t npairs = B.P * m;
   for (uint32_t pair = blockIdx.y; pair < npairs; pair += gridDim.y) {
     const uint32_t w = pair / m, t = pair - w * m;
@@ -431,7 +433,7 @@ __global__ __launch_bounds__(256) void k_lazy_step(float* __restrict__ acc, int6
     const uint32_t s = B.start(b), e = B.start(b + 1u);
     const int64_t o = ((int64_t)w * B.P + b) * kb;
     float* __restrict__ A = acc + (int64_t)r * ld_acc;
-    if (hist1) {   // uniform
+    if constexpr (HIST) {
       const int64_t cu = (int64_t)r * B.P + b;   // the receiver block's arrays
       const uint32_t FH = hist_floor(spec_used[cu]);
       const uint32_t j0 = blockIdx.x * LAZY_CHUNK;
@@ -439,13 +441,35 @@ __global__ __launch_bounds__(256) void k_lazy_step(float* __restrict__ acc, int6
       if (blockIdx.x == 0 && threadIdx.x == 0) atomicOr(&spec_used[cu], SPEC_DIRTY);
       for (int i = threadIdx.x; i < NB1; i += 256) dh[i] = 0u;
       __syncthreads();
-      for (uint32_t j = j0 + threadIdx.x; j < min(kb, j0 + LAZY_CHUNK); j += 256u) {
-        const int32_t x = sp_idx[o + j];
-        if (x < (int32_t)s || x >= (int32_t)e) continue;
-        const float old = A[x];
-        const float nv = old + sp_val[o + j];
+      // the chunk's entries, then the values they land on, all loads in flight
+      // before any store (a pair's indices are distinct, so no entry's store
+      // meets another's load)
+      const uint32_t j1 = min(kb, j0 + LAZY_CHUNK);
+      int32_t xs[LAZY_R];
+      float vs[LAZY_R], olds[LAZY_R];
+#pragma unroll
+      for (int q = 0; q < LAZY_R; ++q) {
+        const uint32_t j = j0 + (uint32_t)q * 256u + threadIdx.x;
+        xs[q] = -1;
+        vs[q] = 0.f;
+        if (j < j1) {
+          xs[q] = sp_idx[o + j];
+          vs[q] = sp_val[o + j];
+        }
+      }
+#pragma unroll
+      for (int q = 0; q < LAZY_R; ++q) {
+        const bool in = xs[q] >= (int32_t)s && xs[q] < (int32_t)e;   // false for an empty lane (-1)
+        olds[q] = in ? A[xs[q]] : 0.f;
+      }
+#pragma unroll
+      for (int q = 0; q < LAZY_R; ++q) {
+        if (xs[q] < (int32_t)s || xs[q] >= (int32_t)e) continue;
+        const uint32_t j = j0 + (uint32_t)q * 256u + threadIdx.x;
+        const float old = olds[q];
+        const float nv = old + vs[q];
         saved[o + j] = old;
-        A[x] = nv;
+        A[xs[q]] = nv;
         const uint32_t k0 = mag_key(old), k1 = mag_key(nv);
         if (k0 >= FH) atomicSub(&dh[k0 >> D1_SHIFT], 1u);
         if (k1 >= FH) atomicAdd(&dh[k1 >> D1_SHIFT], 1u);
@@ -530,8 +554,12 @@ hipError_t launch_lazy_step(float* acc, int64_t ld_acc, int32_t P, int64_t n, in
                             bool restore, uint32_t* hist1, uint32_t* spec_used, hipStream_t s) {
   const unsigned gx = hist1 ? (unsigned)((kb + LAZY_CHUNK - 1) / LAZY_CHUNK) : grid_for(kb, 256, 1024);
   const dim3 grid(gx, (unsigned)std::min<int64_t>((int64_t)P * m, 65535));
-  hipLaunchKernelGGL(k_lazy_step, grid, dim3(256), 0, s, acc, ld_acc, make_blocks(n, P), (uint32_t)kb, (uint32_t)d,
-                     (uint32_t)m, sp_idx, sp_val, saved, bm, restore ? 1 : 0, hist1, spec_used);
+  if (hist1)
+    hipLaunchKernelGGL(k_lazy_step<true>, grid, dim3(256), 0, s, acc, ld_acc, make_blocks(n, P), (uint32_t)kb,
+                       (uint32_t)d, (uint32_t)m, sp_idx, sp_val, saved, bm, restore ? 1 : 0, hist1, spec_used);
+  else
+    hipLaunchKernelGGL(k_lazy_step<false>, grid, dim3(256), 0, s, acc, ld_acc, make_blocks(n, P), (uint32_t)kb,
+                       (uint32_t)d, (uint32_t)m, sp_idx, sp_val, saved, bm, restore ? 1 : 0, hist1, spec_used);
   return hipGetLastError();
 }
 
