@@ -1254,6 +1254,7 @@ __global__ __launch_bounds__(256) void k_big_count(BigArgs a, uint32_t ngroups) 
 
 // per unit: exclusive prefixes in slot order (in place over the counts), the
 // consistency checks and the merge's drop count
+constexpr int SCAN_R = 16;   // slots per thread the scan holds in registers (units of up to 16384 slots)
 template <int mode>
 __global__ __launch_bounds__(1024) void k_big_scan(BigArgs a) {
   __shared__ uint32_t scratch[32];
@@ -1268,23 +1269,60 @@ __global__ __launch_bounds__(1024) void k_big_scan(BigArgs a) {
   const int64_t o = ua * a.smax;
   const uint32_t* __restrict__ cnt = a.slot_cnt + o;
   uint32_t sa = 0, sg = 0, se = 0;
-  for (uint32_t i = i0; i < i1; ++i) {
-    sa += min(cnt[i], (uint32_t)g.ss);
-    sg += a.pre_ge[o + i];
-    se += a.pre_eq[o + i];
-  }
   uint32_t ta, tg, te;
-  uint32_t xa = block_excl_scan(sa, scratch, &ta);
-  uint32_t xg = block_excl_scan(sg, scratch, &tg);
-  uint32_t xe = block_excl_scan(se, scratch, &te);
-  for (uint32_t i = i0; i < i1; ++i) {
-    const uint32_t ca = min(cnt[i], (uint32_t)g.ss), cg = a.pre_ge[o + i], ce = a.pre_eq[o + i];
-    a.pre_all[o + i] = xa;
-    a.pre_ge[o + i] = xg;
-    a.pre_eq[o + i] = xe;
-    xa += ca;
-    xg += cg;
-    xe += ce;
+  if (per <= (uint32_t)SCAN_R) {   // uniform: the thread's slots held in registers, all loads in flight
+    uint32_t ca[SCAN_R], cg[SCAN_R], ce[SCAN_R];
+#pragma unroll
+    for (int r = 0; r < SCAN_R; ++r) {
+      const uint32_t i = i0 + (uint32_t)r;
+      ca[r] = 0u;
+      cg[r] = 0u;
+      ce[r] = 0u;
+      if (i < i1) {
+        ca[r] = min(cnt[i], (uint32_t)g.ss);
+        cg[r] = a.pre_ge[o + i];
+        ce[r] = a.pre_eq[o + i];
+      }
+    }
+#pragma unroll
+    for (int r = 0; r < SCAN_R; ++r) {
+      sa += ca[r];
+      sg += cg[r];
+      se += ce[r];
+    }
+    uint32_t xa = block_excl_scan(sa, scratch, &ta);
+    uint32_t xg = block_excl_scan(sg, scratch, &tg);
+    uint32_t xe = block_excl_scan(se, scratch, &te);
+#pragma unroll
+    for (int r = 0; r < SCAN_R; ++r) {
+      const uint32_t i = i0 + (uint32_t)r;
+      if (i < i1) {
+        a.pre_all[o + i] = xa;
+        a.pre_ge[o + i] = xg;
+        a.pre_eq[o + i] = xe;
+      }
+      xa += ca[r];
+      xg += cg[r];
+      xe += ce[r];
+    }
+  } else {
+    for (uint32_t i = i0; i < i1; ++i) {
+      sa += min(cnt[i], (uint32_t)g.ss);
+      sg += a.pre_ge[o + i];
+      se += a.pre_eq[o + i];
+    }
+    uint32_t xa = block_excl_scan(sa, scratch, &ta);
+    uint32_t xg = block_excl_scan(sg, scratch, &tg);
+    uint32_t xe = block_excl_scan(se, scratch, &te);
+    for (uint32_t i = i0; i < i1; ++i) {
+      const uint32_t ca = min(cnt[i], (uint32_t)g.ss), cg = a.pre_ge[o + i], ce = a.pre_eq[o + i];
+      a.pre_all[o + i] = xa;
+      a.pre_ge[o + i] = xg;
+      a.pre_eq[o + i] = xe;
+      xa += ca;
+      xg += cg;
+      xe += ce;
+    }
   }
   if (threadIdx.x == 0) {
     const uint32_t need_eq = st[ST_NEEDEQ];
