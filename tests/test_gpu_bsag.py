@@ -96,3 +96,39 @@ def test_bsag_p14_d7_sized():
         res = so.spardl_step_bsag(acc, grad, P, n, L, d, ctrl, blocks=blocks)
         compare_bsag_step(st, res, blocks=blocks)
         log(f"  step {t}: bit-exact (h = {res.h}, N = {[len(res.union[q][0]) for q in blocks]})")
+
+
+@pytest.mark.parametrize("d", [2, 4, 8])
+def test_bsag_resnet50_sized(d):
+    """The ResNet-50-sized workload (P = 8, n = 25.6M, 1 %) with d teams joined
+    by B-SAG, L = d k / P, in the configuration the benchmark runs (all teams
+    per call); the oracle recomputes two block indices of every output, with
+    the controller carried over three steps."""
+    wl = W.config(2)
+    P, n = wl.P, wl.n
+    Q = P // d
+    k = wl.k_blk * P
+    L = d * k // P
+    log(f"bsag {wl.describe()} d={d} L={L}")
+    blocks = [0, Q - 1] if Q > 1 else [0]
+    bounds = so.block_bounds(n, Q)
+    st = spardl.SparDLSagStep(P, d, n, L, bruck=True)
+    grad_d = torch.empty((P, n), dtype=torch.float32, device="cuda")
+    host = torch.empty(n, dtype=torch.float32).pin_memory()
+    acc = [{b: np.zeros(bounds[b + 1] - bounds[b], np.float32) for b in blocks} for _ in range(P)]
+    ctrl = {}
+    for t in range(1, wl.steps + 1):
+        grad = [dict() for _ in range(P)]
+        for w in range(P):
+            W.fill(host.numpy(), wl, t, w)
+            grad_d[w].copy_(host)
+            torch.cuda.synchronize()
+            for b in blocks:
+                grad[w][b] = host.numpy()[bounds[b]:bounds[b + 1]].copy()
+        st.step(grad_d)
+        torch.cuda.synchronize()
+        _check(st)
+        log(f"  step {t}: GPU done, oracle on block indices {blocks}")
+        res = so.spardl_step_bsag(acc, grad, P, n, L, d, ctrl, blocks=blocks)
+        compare_bsag_step(st, res, blocks=blocks)
+        log(f"  step {t}: bit-exact (h = {res.h})")
