@@ -274,11 +274,12 @@ __global__ __launch_bounds__(256) void k_lsel_emit(ListSel S, uint32_t nch, cons
 
 // ---- the Bruck All-Gather's result summed in team order, for block q, in
 // tiles of UT indices: each workgroup takes the d kept lists' entries that
-// fall in its tile (binary searches in the index-sorted lists), adds them in
-// team order in LDS (first occurrence stores, later ones add; an LDS
-// occupancy bitmap tells which), and either counts the tile's distinct
-// indices (pass 1) or writes them in index order after the counts of the
-// tiles before it (pass 2).  Tile 0 of each block also records N_q.
+// fall in its tile (found by wave searches in the index-sorted lists, all
+// teams' at once), adds them in team order in LDS (first occurrence stores,
+// later ones add; an LDS occupancy bitmap tells which), and either counts
+// the tile's distinct indices (pass 1) or writes them in index order after
+// the counts of the tiles before it (pass 2).  Tile 0 of each block also
+// records N_q.
 constexpr uint32_t UT = UNION_TILE;
 constexpr uint32_t UNION_TEAMS = 8;   // teams whose ranges are searched together (two waves each)
 static_assert(2 * UNION_TEAMS <= 1024 / WAVE, "two waves of the union workgroup per team of a batch");
