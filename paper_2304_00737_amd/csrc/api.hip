@@ -261,7 +261,7 @@ int topk_units(const float* acc, int64_t ld_acc, int64_t units, const Units& U, 
   uint32_t* hint = (U.rel && !spec) ? nullptr : w.spec_t1;
   SPARDL_TRY(launch_select1(w.hist1, w.state, units, U, n, P, (uint32_t)k_blk, hint, w.spec_used, spec, acc, ld_acc,
                             v4, w.err, stream));
-  SPARDL_TRY(launch_collect(acc, ld_acc, units, U, n, P, v4, smax, w.state, w.spec_cnt, (int32_t)L.add_tiles,
+  SPARDL_TRY(launch_collect(acc, ld_acc, units, U, n, P, k_blk, v4, smax, w.state, w.spec_cnt, (int32_t)L.add_tiles,
                             w.slot_cnt, w.slot_nbin, w.cand_idx, w.cand_val, w.bin_key, stream));
   // hist1: the staged threshold for long units builds its level-2/3 histograms in the units'
   // level-1 histogram space, which the select has cleared

@@ -358,12 +358,21 @@ __device__ __forceinline__ void recollect_wave_pre(uint32_t c0, uint32_t c1, uin
 // the counts and first entries of all of them loaded before any is filtered
 // (when a call has many sparse slots, one slot per wave leaves the wave
 // waiting on memory most of the time); otherwise the workgroup collects the
-// group's slots from acc one by one.  64 registers let 8 waves share a SIMD.
+// group's slots from acc one by one.  64 registers let 8 waves share a SIMD
+// (the 8-slot form, holding 8 slots' loads, takes up to 96 and 5 waves).
 // Slots per call from which the block top-k's collect and emit give each wave
 // 2 slots and its staged threshold takes 256 slots per workgroup.
 constexpr int64_t MULTI_SLOT_MIN = 1 << 17;
+// Slots per wave of the block top-k's collect and emit: 1; 2 from
+// MULTI_SLOT_MIN slots per call; 8 when, besides, a block keeps fewer than 8
+// entries per slot (its slots hold a few candidates each, so the loads of 8
+// slots are in flight for the cost of one).
+static inline int topk_slots_per_wave(int64_t nunits, int32_t smax, int32_t kb) {
+  if (nunits * smax < MULTI_SLOT_MIN) return 1;
+  return (int64_t)kb < 8ll * smax ? 8 : 2;
+}
 template <int VEC, int SPW>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(8, 8))) void k_collect(const float* __restrict__ acc, int64_t ld_acc, Blocks B, Units U,
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(SPW >= 8 ? 5 : 8, 8))) void k_collect(const float* __restrict__ acc, int64_t ld_acc, Blocks B, Units U,
                                                  uint32_t smax, uint32_t gq, const uint32_t* __restrict__ state,
                                                  const uint32_t* __restrict__ spec_cnt, uint32_t add_tiles,
                                                  uint32_t* __restrict__ slot_cnt, uint32_t* __restrict__ slot_nbin,
@@ -401,7 +410,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(8, 8))) voi
   } else {
     // this wave's slots: their candidate counts are loaded beside the unit's
     // state words (in bounds for any live slot)
-    constexpr int R1 = 4;   // first entries per lane of each slot
+    constexpr int R1 = SPW >= 8 ? 1 : 4;   // first entries per lane of each slot
     const uint32_t sw = slot0 + (uint32_t)wave_id() * (uint32_t)SPW;
     uint32_t c0[SPW], c1[SPW];
 #pragma unroll
@@ -1473,7 +1482,7 @@ __global__ __launch_bounds__(256) void k_emit(
       }
     }
   } else if constexpr (MODE == 0) {
-    constexpr int R1 = EMIT_R1;
+    constexpr int R1 = SPW >= 8 ? 1 : EMIT_R1;
     const int32_t sw = (int32_t)((blockIdx.x % gq) * (4u * SPW) + (uint32_t)wv * SPW);
     const SlotGeom g = slot_geom(0, unit, B, U, kb);
     if (sw >= g.nslots) return;
@@ -1629,15 +1638,16 @@ hipError_t launch_select1(uint32_t* hist1, uint32_t* state, int64_t nunits, cons
 }
 
 hipError_t launch_collect(const float* acc, int64_t ld_acc, int64_t nunits, const Units& U, int64_t n, int32_t P,
-                          bool vec4, int32_t smax, const uint32_t* state, const uint32_t* spec_cnt,
+                          int32_t kb, bool vec4, int32_t smax, const uint32_t* state, const uint32_t* spec_cnt,
                           int32_t add_tiles, uint32_t* slot_cnt, uint32_t* slot_nbin, int32_t* cand_idx,
                           float* cand_val, uint32_t* bin_key, hipStream_t s) {
   // the speculative path exists for float4 rows only (the add writes no candidates otherwise)
-  const int spw = vec4 && nunits * smax >= MULTI_SLOT_MIN ? 2 : 1;
+  const int spw = vec4 ? topk_slots_per_wave(nunits, smax, kb) : 1;
   const uint32_t gq = (uint32_t)((smax + 4 * spw - 1) / (4 * spw));
   const dim3 grid((unsigned)(nunits * gq));
   const Blocks B = make_blocks(n, P);
-  if (spw == 2) hipLaunchKernelGGL((k_collect<4, 2>), grid, dim3(256), 0, s, acc, ld_acc, B, U, (uint32_t)smax, gq, state, spec_cnt, (uint32_t)add_tiles, slot_cnt, slot_nbin, cand_idx, cand_val, bin_key);
+  if (spw == 8) hipLaunchKernelGGL((k_collect<4, 8>), grid, dim3(256), 0, s, acc, ld_acc, B, U, (uint32_t)smax, gq, state, spec_cnt, (uint32_t)add_tiles, slot_cnt, slot_nbin, cand_idx, cand_val, bin_key);
+  else if (spw == 2) hipLaunchKernelGGL((k_collect<4, 2>), grid, dim3(256), 0, s, acc, ld_acc, B, U, (uint32_t)smax, gq, state, spec_cnt, (uint32_t)add_tiles, slot_cnt, slot_nbin, cand_idx, cand_val, bin_key);
   else if (vec4) hipLaunchKernelGGL((k_collect<4, 1>), grid, dim3(256), 0, s, acc, ld_acc, B, U, (uint32_t)smax, gq, state, spec_cnt, (uint32_t)add_tiles, slot_cnt, slot_nbin, cand_idx, cand_val, bin_key);
   else hipLaunchKernelGGL((k_collect<1, 1>), grid, dim3(256), 0, s, acc, ld_acc, B, U, (uint32_t)smax, gq, state, spec_cnt, (uint32_t)add_tiles, slot_cnt, slot_nbin, cand_idx, cand_val, bin_key);
   return hipGetLastError();
@@ -1706,11 +1716,13 @@ hipError_t launch_emit(int mode, const int32_t* cand_idx, const float* cand_val,
                        const uint32_t* pre_eq, int32_t* out_idx, float* out_val, int32_t* local_idx,
                        int32_t* drop_idx, float* drop_val, uint32_t* err, hipStream_t s) {
   // block top-k: 4 spw slots per workgroup (spw per wave); merge: one slot per workgroup
-  const int spw = mode == 0 && nunits * smax >= MULTI_SLOT_MIN ? 2 : 1;
+  const int spw = mode == 0 ? topk_slots_per_wave(nunits, smax, kb) : 1;
   const uint32_t gq = mode == 0 ? (uint32_t)((smax + 4 * spw - 1) / (4 * spw)) : (uint32_t)smax;
   const dim3 grid((unsigned)(nunits * gq));
   const Blocks B = make_blocks(n, P);
-  if (mode == 0 && spw == 2)
+  if (mode == 0 && spw == 8)
+    hipLaunchKernelGGL((k_emit<0, 8>), grid, dim3(256), 0, s, cand_idx, cand_val, B, U, PM, kb, smax, gq, state, slot_cnt, pre_all, pre_ge, pre_eq, out_idx, out_val, local_idx, drop_idx, drop_val, err);
+  else if (mode == 0 && spw == 2)
     hipLaunchKernelGGL((k_emit<0, 2>), grid, dim3(256), 0, s, cand_idx, cand_val, B, U, PM, kb, smax, gq, state, slot_cnt, pre_all, pre_ge, pre_eq, out_idx, out_val, local_idx, drop_idx, drop_val, err);
   else if (mode == 0)
     hipLaunchKernelGGL(k_emit<0>, grid, dim3(256), 0, s, cand_idx, cand_val, B, U, PM, kb, smax, gq, state, slot_cnt, pre_all, pre_ge, pre_eq, out_idx, out_val, local_idx, drop_idx, drop_val, err);

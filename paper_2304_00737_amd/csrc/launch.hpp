@@ -36,7 +36,7 @@ hipError_t launch_select1(uint32_t* hist1, uint32_t* state, int64_t nunits, cons
                           uint32_t need, uint32_t* spec_t1, const uint32_t* spec_used, bool spec, const float* acc,
                           int64_t ld_acc, bool vec4, uint32_t* err, hipStream_t s);
 hipError_t launch_collect(const float* acc, int64_t ld_acc, int64_t nunits, const Units& U, int64_t n, int32_t P,
-                          bool vec4, int32_t smax, const uint32_t* state, const uint32_t* spec_cnt,
+                          int32_t kb, bool vec4, int32_t smax, const uint32_t* state, const uint32_t* spec_cnt,
                           int32_t add_tiles, uint32_t* slot_cnt, uint32_t* slot_nbin, int32_t* cand_idx,
                           float* cand_val, uint32_t* bin_key, hipStream_t s);
 hipError_t launch_thresh(int mode, int64_t nunits, const Units& U, int64_t n, int32_t P, int32_t kb, int32_t smax,

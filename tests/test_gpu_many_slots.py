@@ -1,6 +1,7 @@
 """Bit-exact block top-k of one worker's row when the call has at least 2^17
 candidate slots, the size from which the collect and the emit give each wave
-two slots and the staged threshold walks 256-slot groups as one list.
+two slots (eight when a block keeps fewer than 8 entries per slot) and the
+staged threshold walks 256-slot groups as one list.
 
 One row of 16 blocks of 33,588,228 elements (8201 slots each, the last one
 ragged; 16 units of that many slots take the staged threshold), tie-heavy
@@ -39,9 +40,19 @@ def _ties(n, seed):
     return v
 
 
-def test_block_topk_many_slots_one_row():
+def _normal(n, seed):
+    return np.random.default_rng(seed).standard_normal(n, dtype=np.float32)
+
+
+@pytest.mark.parametrize("kind,kb", [("ties", KB), ("normal", M // 1000)])
+def test_block_topk_many_slots_one_row(kind, kb):
+    """ties at 1 %: crowded slots, two slots per wave; N(0,1) at 0.1 %: about
+    ten candidates per slot and fewer than 8 kept entries per slot, so eight
+    slots per wave."""
     assert P * ((M + 4095) // 4096) >= 1 << 17
-    log(f"many-slot block top-k: one row, P={P}, block {M}, k_blk {KB}")
+    KB = kb
+    log(f"many-slot block top-k: one row, P={P}, block {M}, k_blk {KB}, {kind}")
+    gen = _ties if kind == "ties" else _normal
     acc = torch.zeros((1, N), dtype=torch.float32, device="cuda")
     ws = spardl.workspace(1, P, N, KB)
     sp_i = torch.empty((1, P, KB), dtype=torch.int32, device="cuda")
@@ -49,7 +60,7 @@ def test_block_topk_many_slots_one_row():
     li = torch.empty((1, P, KB), dtype=torch.int32, device="cuda")
     host = np.zeros(N, np.float32)
     for step in range(2):
-        g = _ties(N, 40 + step)
+        g = gen(N, 40 + step)
         spardl.residual_add(acc, torch.from_numpy(g).cuda().view(1, N), 1, N, P, ws, KB)
         spardl.block_topk(acc, 1, N, P, KB, sp_i, sp_v, li, ws, spardl.TOPK_HIST_READY)
         torch.cuda.synchronize()
