@@ -1279,41 +1279,46 @@ __global__ __launch_bounds__(1024) void k_big_scan(BigArgs a) {
   const uint32_t* __restrict__ cnt = a.slot_cnt + o;
   uint32_t sa = 0, sg = 0, se = 0;
   uint32_t ta, tg, te;
-  if (per <= (uint32_t)SCAN_R) {   // uniform: the thread's slots held in registers, all loads in flight
-    uint32_t ca[SCAN_R], cg[SCAN_R], ce[SCAN_R];
+  if (per <= (uint32_t)SCAN_R) {   // uniform
+    // the three arrays loaded coalesced (slot r NT + t in register r of
+    // thread t), all loads in flight; each array then goes through LDS so
+    // that thread t scans its contiguous slots [i0, i1) and the prefixes
+    // are stored coalesced again
+    __shared__ uint32_t buf[SCAN_R * NT];
+    uint32_t v[3][SCAN_R];
 #pragma unroll
     for (int r = 0; r < SCAN_R; ++r) {
-      const uint32_t i = i0 + (uint32_t)r;
-      ca[r] = 0u;
-      cg[r] = 0u;
-      ce[r] = 0u;
-      if (i < i1) {
-        ca[r] = min(cnt[i], (uint32_t)g.ss);
-        cg[r] = a.pre_ge[o + i];
-        ce[r] = a.pre_eq[o + i];
+      const uint32_t i = (uint32_t)r * NT + threadIdx.x;
+      v[0][r] = i < ns ? min(cnt[i], (uint32_t)g.ss) : 0u;
+      v[1][r] = i < ns ? a.pre_ge[o + i] : 0u;
+      v[2][r] = i < ns ? a.pre_eq[o + i] : 0u;
+    }
+    uint32_t* const outs[3] = {a.pre_all + o, a.pre_ge + o, a.pre_eq + o};
+    uint32_t tots[3];
+#pragma unroll
+    for (int q = 0; q < 3; ++q) {
+#pragma unroll
+      for (int r = 0; r < SCAN_R; ++r) buf[r * NT + threadIdx.x] = v[q][r];
+      __syncthreads();
+      uint32_t sum = 0;
+      for (uint32_t i = i0; i < i1; ++i) sum += buf[i];
+      uint32_t x = block_excl_scan(sum, scratch, &tots[q]);   // its barriers order the reads above
+      for (uint32_t i = i0; i < i1; ++i) {
+        const uint32_t c = buf[i];
+        buf[i] = x;
+        x += c;
       }
-    }
+      __syncthreads();
 #pragma unroll
-    for (int r = 0; r < SCAN_R; ++r) {
-      sa += ca[r];
-      sg += cg[r];
-      se += ce[r];
-    }
-    uint32_t xa = block_excl_scan(sa, scratch, &ta);
-    uint32_t xg = block_excl_scan(sg, scratch, &tg);
-    uint32_t xe = block_excl_scan(se, scratch, &te);
-#pragma unroll
-    for (int r = 0; r < SCAN_R; ++r) {
-      const uint32_t i = i0 + (uint32_t)r;
-      if (i < i1) {
-        a.pre_all[o + i] = xa;
-        a.pre_ge[o + i] = xg;
-        a.pre_eq[o + i] = xe;
+      for (int r = 0; r < SCAN_R; ++r) {
+        const uint32_t i = (uint32_t)r * NT + threadIdx.x;
+        if (i < ns) outs[q][i] = buf[i];
       }
-      xa += ca[r];
-      xg += cg[r];
-      xe += ce[r];
+      __syncthreads();   // buf is rewritten for the next array
     }
+    ta = tots[0];
+    tg = tots[1];
+    te = tots[2];
   } else {
     for (uint32_t i = i0; i < i1; ++i) {
       sa += min(cnt[i], (uint32_t)g.ss);
