@@ -54,7 +54,7 @@ Layout make_layout(int32_t P, int64_t n, int32_t kb, int32_t rows = 0) {
   const int64_t maxlen = ceil_div(n, P);
   L.pairs_max = (int64_t)rows * mmax;
   L.units = std::max<int64_t>((int64_t)rows * P, L.pairs_max);
-  L.tiles_tk = ceil_div(maxlen, SLOT);
+  L.tiles_tk = spans_per_block(maxlen, SLOT);   // slots from each block's aligned origin
   L.tiles_mg = ceil_div(2ll * kb, MERGE_TILE);
   L.slot_n = std::max<int64_t>((int64_t)rows * P * L.tiles_tk, L.pairs_max * L.tiles_mg);
   size_t off = 256;
@@ -64,7 +64,7 @@ Layout make_layout(int32_t P, int64_t n, int32_t kb, int32_t rows = 0) {
   off += align256((size_t)L.units * HCOPIES * NB1 * 4);
   // speculative candidates of the fused residual add: per (worker, block) the
   // previous threshold bin + 1 (0: none) and the floor used; per add tile the count
-  L.add_tiles = ceil_div(maxlen, ADD_TILE);
+  L.add_tiles = add_tiles_per_block(maxlen);
   L.spec_t1 = off;
   off += align256((size_t)rows * P * 4);
   L.spec_used = off;

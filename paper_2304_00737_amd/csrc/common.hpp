@@ -86,6 +86,20 @@ inline Blocks make_blocks(int64_t n, int32_t P) {
   return Blocks{(uint32_t)n, (uint32_t)P, (uint32_t)(n / P), (uint32_t)(n % P)};
 }
 
+// Tiles of the fused residual add and slots of the block top-k start at a
+// block's aligned origin, its first element rounded down to a multiple of 32
+// (128 bytes): every tile and slot after a block's first then starts on a
+// 128-byte boundary of a row that does, and the first is short by the lead.
+__host__ __device__ __forceinline__ uint32_t block_lead(uint32_t s) { return s & 31u; }
+__host__ __device__ __forceinline__ uint32_t block_origin(uint32_t s) { return s & ~31u; }
+// Tiles (or slots of `len` elements) a block of up to maxlen elements spans from its origin.
+__host__ __device__ __forceinline__ int64_t spans_per_block(int64_t maxlen, int64_t len) {
+  return (maxlen + 31 + len - 1) / len;
+}
+__host__ __device__ __forceinline__ int64_t add_tiles_per_block(int64_t maxlen) {
+  return spans_per_block(maxlen, ADD_TILE);
+}
+
 // Selection units of a block top-k call over rows (workers) w0, w0 + 1, ...:
 // unit u selects in row u / m the block (d + u % m + (rel ? w : 0)) mod P,
 // w = w0 + u / m being the worker.  All blocks of all rows: m = P, d = 0,

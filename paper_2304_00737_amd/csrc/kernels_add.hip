@@ -29,18 +29,27 @@ __global__ __launch_bounds__(256) void k_fill(FillRanges r) {
 }
 
 // ============================================================================ a1: residual add
-// One workgroup = one tile of ADD_TILE elements of one block of one row.
-// With HIST, every sum's level-1 digit is counted in an LDS histogram that is
-// flushed (non-zero bins only) into the block's global one.  The gradient is
-// read once, so it is loaded non-temporally.
+// Tiles of ADD_TILE elements start at the block's aligned origin (its start
+// rounded down to 32 elements), so every tile after a block's first begins on
+// a 128-byte boundary of the row; tile g of block b is
+// [origin + g ADD_TILE, origin + (g+1) ADD_TILE) clipped to the block.
+// One workgroup per tile; chunk j of the tile is the 1024 elements at
+// 1024 j, thread t holding elements 4t .. 4t+3 of each chunk, so each wave's
+// float4 access covers 1 KB of whole lines.  The gradient is read once, so it
+// is loaded non-temporally; A is re-read only by a fallback, so it is stored
+// non-temporally.
 //
-// The float4 path with HIST also writes speculative candidates for the block
-// top-k that follows: every sum whose key is at or above a floor two level-1
-// bins below the block's previous threshold bin (nothing on a block's first
-// step), in index order at the tile's own span of the candidate arrays, with
-// the count per tile.  The exact threshold bin found from this pass's
-// histogram decides whether the floor was low enough; if not, the top-k reads
-// the block again.  Thread t owns the 8 consecutive elements at 8 t.
+// With HIST, every sum's level-1 digit is counted in an LDS histogram that is
+// flushed (non-zero bins only) into one of the block's global copies, and the
+// speculative candidates of the block top-k that follows are written: every
+// sum whose key is at or above a floor two level-1 bins below the block's
+// previous threshold bin (nothing on a block's first step), in index order at
+// the tile's own span of the candidate arrays, with the count per tile.  The
+// run is staged in LDS and written as whole 128-byte lines (padded past the
+// count inside the tile's span, non-temporal): small partial-line writes
+// into the candidate arrays cost far more than their bytes.  The exact
+// threshold bin found from this pass's histogram decides whether the floor
+// was low enough; if not, the top-k reads the block again.
 //
 // From a block's second step on, the histogram counts only keys at or above
 // a lower floor (two binades further down): the threshold lies there unless it
@@ -48,16 +57,145 @@ __global__ __launch_bounds__(256) void k_fill(FillRanges r) {
 // rebuilds the block's full histogram itself.
 constexpr int ADD_STAGE = 512;          // speculative candidates staged in LDS per tile
 
-
-template <int VEC, bool HIST>
-__global__ __launch_bounds__(256) void k_residual_add(float* __restrict__ acc, int64_t ld_acc,
-                                                      const float* __restrict__ grad, int64_t ld_grad,
-                                                      Blocks B, uint32_t G, AddSpec sp) {
-  constexpr bool SPEC = HIST && VEC == 4;
+template <bool HIST>
+__global__ __launch_bounds__(256) void k_residual_add4(float* __restrict__ acc, int64_t ld_acc,
+                                                       const float* __restrict__ grad, int64_t ld_grad, Blocks B,
+                                                       uint32_t G, AddSpec sp) {
+  static_assert(ADD_TILE == 2 * 1024, "two 1024-element chunks per tile");
   __shared__ __align__(16) uint32_t h[HIST ? NB1 : 4];
-  __shared__ int32_t s_idx[SPEC ? ADD_STAGE : 1];
-  __shared__ float s_val[SPEC ? ADD_STAGE : 1];
+  __shared__ int32_t s_idx[HIST ? ADD_STAGE : 1];
+  __shared__ float s_val[HIST ? ADD_STAGE : 1];
   __shared__ uint32_t wtot[4];
+  const uint32_t g = blockIdx.x % G;
+  const uint32_t wb = blockIdx.x / G;
+  const uint32_t b = wb % B.P, w = wb / B.P;
+  const uint32_t s = B.start(b), e = B.start(b + 1u);
+  const uint32_t ta = block_origin(s) + g * (uint32_t)ADD_TILE;
+  if (ta >= e) return;
+  float* __restrict__ A = acc + (int64_t)w * ld_acc;
+  const float* __restrict__ Gr = grad + (int64_t)w * ld_grad;
+  const uint32_t x0 = ta + threadIdx.x * 4u;
+  // block starts and ends are multiples of 4 here, so a float4 lies wholly inside or outside the block
+  bool in[2];
+  f4v a[2], gg[2];
+#pragma unroll
+  for (int j = 0; j < 2; ++j) {
+    const uint32_t x = x0 + 1024u * j;
+    in[j] = x >= s && x < e;
+    if (in[j]) {
+      a[j] = *reinterpret_cast<const f4v*>(A + x);
+      gg[j] = __builtin_nontemporal_load(reinterpret_cast<const f4v*>(Gr + x));
+    }
+  }
+  if (!HIST) {
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      if (in[j]) {
+        f4v q;
+        q.x = a[j].x + gg[j].x;
+        q.y = a[j].y + gg[j].y;
+        q.z = a[j].z + gg[j].z;
+        q.w = a[j].w + gg[j].w;
+        __builtin_nontemporal_store(q, reinterpret_cast<f4v*>(A + x0 + 1024u * j));
+      }
+    }
+    return;
+  }
+  // the histogram is cleared while the loads are in flight
+  for (int i = threadIdx.x; i < NB1 / 4; i += 256) reinterpret_cast<uint4*>(h)[i] = make_uint4(0u, 0u, 0u, 0u);
+  uint32_t F = SPEC_NONE;
+  const uint32_t sw = sp.spec_t1[wb];
+  if (sw != 0u) {
+    const uint32_t T1p = sw - 1u;
+    F = T1p > SPEC_MARGIN ? (T1p - SPEC_MARGIN) << D1_SHIFT : 0u;
+  }
+  if (g == 0u && threadIdx.x == 0) sp.spec_used[wb] = F;
+  const uint32_t FH = hist_floor(F);
+  __syncthreads();
+  float r[8];
+  uint32_t packed = 0;   // candidates of chunk 0 | chunk 1 << 16 (at most 1024 each)
+#pragma unroll
+  for (int j = 0; j < 2; ++j) {
+    if (in[j]) {
+      f4v q;
+      q.x = a[j].x + gg[j].x;
+      q.y = a[j].y + gg[j].y;
+      q.z = a[j].z + gg[j].z;
+      q.w = a[j].w + gg[j].w;
+      __builtin_nontemporal_store(q, reinterpret_cast<f4v*>(A + x0 + 1024u * j));
+      r[4 * j + 0] = q.x;
+      r[4 * j + 1] = q.y;
+      r[4 * j + 2] = q.z;
+      r[4 * j + 3] = q.w;
+#pragma unroll
+      for (int c = 0; c < 4; ++c) {
+        const uint32_t key = mag_key(r[4 * j + c]);
+        if (key >= FH) atomicAdd(&h[key >> D1_SHIFT], 1u);
+        packed += key >= F ? (1u << (16 * j)) : 0u;
+      }
+    } else {
+#pragma unroll
+      for (int c = 0; c < 4; ++c) r[4 * j + c] = 0.f;
+    }
+  }
+  // index-ordered compaction of the tile's candidates (keys >= F): chunk 0, then chunk 1
+  const int lane = lane_id(), wv = wave_id();
+  const uint32_t incl = wave_incl_scan(packed);
+  if (lane == WAVE - 1) wtot[wv] = incl;
+  __syncthreads();   // also ends the histogram's updates
+  uint32_t base = 0, tot = 0;
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    const uint32_t x = wtot[k];
+    base += k < wv ? x : 0u;
+    tot += x;
+  }
+  {
+    uint32_t* __restrict__ H = sp.hist1 + ((int64_t)wb * HCOPIES + blockIdx.x % HCOPIES) * NB1;
+    flush_hist(h, H);
+  }
+  const uint32_t tot0 = tot & 0xFFFFu, all = tot0 + (tot >> 16);
+  const uint32_t ex = base + incl - packed;
+  const uint32_t t0 = ta > s ? ta : s;   // the tile's first element: its candidate run starts there
+  const bool staged = all <= (uint32_t)ADD_STAGE;   // uniform
+  int32_t* __restrict__ CI = sp.cand_idx + (int64_t)w * B.n + t0;
+  float* __restrict__ CV = sp.cand_val + (int64_t)w * B.n + t0;
+  int32_t* __restrict__ oI = staged ? s_idx : CI;
+  float* __restrict__ oV = staged ? s_val : CV;
+  if (packed != 0u) {
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      uint32_t pos = j == 0 ? (ex & 0xFFFFu) : tot0 + (ex >> 16);
+#pragma unroll
+      for (int c = 0; c < 4; ++c) {
+        if (in[j] && mag_key(r[4 * j + c]) >= F) {
+          oI[pos] = (int32_t)(x0 + 1024u * j + (uint32_t)c);
+          oV[pos] = r[4 * j + c];
+          ++pos;
+        }
+      }
+    }
+  }
+  if (threadIdx.x == 0) sp.spec_cnt[(int64_t)wb * G + g] = all;
+  if (staged) {
+    __syncthreads();
+    // whole lines: pad the run to a multiple of 32 entries, inside the tile's span
+    const uint32_t span = min(e, ta + (uint32_t)ADD_TILE) - t0;
+    const uint32_t padded = min((all + 31u) & ~31u, span);
+    for (uint32_t k = threadIdx.x; k < padded; k += 256) {
+      __builtin_nontemporal_store(s_idx[k], CI + k);
+      __builtin_nontemporal_store(s_val[k], CV + k);
+    }
+  }
+}
+
+// Rows that are not float4-aligned: one element per thread and step, ADD_F4 * 4
+// steps per tile (tiles from the block start); histogram only, no candidates.
+template <bool HIST>
+__global__ __launch_bounds__(256) void k_residual_add1(float* __restrict__ acc, int64_t ld_acc,
+                                                       const float* __restrict__ grad, int64_t ld_grad, Blocks B,
+                                                       uint32_t G, AddSpec sp) {
+  __shared__ __align__(16) uint32_t h[HIST ? NB1 : 4];
   const uint32_t g = blockIdx.x % G;
   const uint32_t wb = blockIdx.x / G;
   const uint32_t b = wb % B.P, w = wb / B.P;
@@ -70,106 +208,17 @@ __global__ __launch_bounds__(256) void k_residual_add(float* __restrict__ acc, i
   }
   float* __restrict__ A = acc + (int64_t)w * ld_acc;
   const float* __restrict__ Gr = grad + (int64_t)w * ld_grad;
-  if (VEC == 4) {
-    static_assert(ADD_TILE == 256 * 8, "eight elements per thread");
-    const uint32_t my0 = t0 + threadIdx.x * 8u;
-    f4v a[2], gg[2];
 #pragma unroll
-    for (int j = 0; j < 2; ++j) {
-      if (my0 + 4u * j < e) {
-        a[j] = *reinterpret_cast<const f4v*>(A + my0 + 4u * j);
-        gg[j] = __builtin_nontemporal_load(reinterpret_cast<const f4v*>(Gr + my0 + 4u * j));
-      }
+  for (int j = 0; j < ADD_F4 * 4; ++j) {
+    const uint32_t off = t0 + j * 256u + threadIdx.x;
+    if (off < e) {
+      const float r = A[off] + Gr[off];
+      A[off] = r;
+      if (HIST) atomicAdd(&h[mag_key(r) >> D1_SHIFT], 1u);
     }
-    uint32_t F = SPEC_NONE;
-    if (SPEC) {
-      const uint32_t sw = sp.spec_t1[wb];
-      if (sw != 0u) {
-        const uint32_t T1p = sw - 1u;
-        F = T1p > SPEC_MARGIN ? (T1p - SPEC_MARGIN) << D1_SHIFT : 0u;
-      }
-      if (g == 0u && threadIdx.x == 0) sp.spec_used[wb] = F;
-    }
-    const uint32_t FH = hist_floor(F);
-    float r[8];
-    uint32_t nc = 0;
-#pragma unroll
-    for (int j = 0; j < 2; ++j) {
-      if (my0 + 4u * j < e) {
-        f4v q;
-        q.x = a[j].x + gg[j].x;
-        q.y = a[j].y + gg[j].y;
-        q.z = a[j].z + gg[j].z;
-        q.w = a[j].w + gg[j].w;
-        __builtin_nontemporal_store(q, reinterpret_cast<f4v*>(A + my0 + 4u * j));   // re-read only next step
-        r[4 * j + 0] = q.x;
-        r[4 * j + 1] = q.y;
-        r[4 * j + 2] = q.z;
-        r[4 * j + 3] = q.w;
-        if (HIST) {
-#pragma unroll
-          for (int c = 0; c < 4; ++c) {
-            const uint32_t key = mag_key(r[4 * j + c]);
-            if (key >= FH) atomicAdd(&h[key >> D1_SHIFT], 1u);
-            nc += key >= F ? 1u : 0u;
-          }
-        }
-      } else {
-#pragma unroll
-        for (int c = 0; c < 4; ++c) r[4 * j + c] = 0.f;
-      }
-    }
-    if (SPEC) {
-      // index-ordered compaction of the candidates (keys >= F) of the tile
-      const int lane = lane_id(), wv = wave_id();
-      const uint32_t incl = wave_incl_scan(nc);
-      if (lane == WAVE - 1) wtot[wv] = incl;
-      __syncthreads();
-      uint32_t base = 0, tot = 0;
-#pragma unroll
-      for (int k = 0; k < 4; ++k) {
-        const uint32_t x = wtot[k];
-        base += k < wv ? x : 0u;
-        tot += x;
-      }
-      const bool staged = tot <= (uint32_t)ADD_STAGE;   // uniform
-      int32_t* __restrict__ CI = sp.cand_idx + (int64_t)w * B.n + t0;
-      float* __restrict__ CV = sp.cand_val + (int64_t)w * B.n + t0;
-      int32_t* __restrict__ oI = staged ? s_idx : CI;
-      float* __restrict__ oV = staged ? s_val : CV;
-      uint32_t pos = base + incl - nc;
-      if (nc != 0u) {
-#pragma unroll
-        for (int k = 0; k < 8; ++k) {
-          if (my0 + (uint32_t)k < e && mag_key(r[k]) >= F) {
-            oI[pos] = (int32_t)(my0 + k);
-            oV[pos] = r[k];
-            ++pos;
-          }
-        }
-      }
-      if (threadIdx.x == 0) sp.spec_cnt[(int64_t)wb * G + g] = tot;
-      if (staged) {
-        __syncthreads();
-        for (uint32_t k = threadIdx.x; k < tot; k += 256) {
-          CI[k] = s_idx[k];
-          CV[k] = s_val[k];
-        }
-      }
-    }
-  } else {
-#pragma unroll
-    for (int j = 0; j < ADD_F4 * 4; ++j) {
-      const uint32_t off = t0 + j * 256u + threadIdx.x;
-      if (off < e) {
-        const float r = A[off] + Gr[off];
-        A[off] = r;
-        if (HIST) atomicAdd(&h[mag_key(r) >> D1_SHIFT], 1u);
-      }
-    }
-    if (HIST && g == 0u && threadIdx.x == 0) sp.spec_used[wb] = SPEC_NONE;   // no candidates on this path
   }
   if (HIST) {
+    if (g == 0u && threadIdx.x == 0) sp.spec_used[wb] = SPEC_NONE;   // no candidates on this path
     __syncthreads();
     uint32_t* __restrict__ H = sp.hist1 + ((int64_t)wb * HCOPIES + blockIdx.x % HCOPIES) * NB1;
     flush_hist(h, H);
@@ -230,16 +279,18 @@ hipError_t launch_residual_add(float* acc, int64_t ld_acc, const float* grad, in
   const bool hist = sp.hist1 != nullptr;
   const int32_t PP = hist ? P : 1;
   const int64_t maxlen = (n + PP - 1) / PP;
-  const int32_t G = (int32_t)((maxlen + ADD_TILE - 1) / ADD_TILE);
-  const dim3 grid((unsigned)((int64_t)nworkers * PP * G));
   const Blocks B = make_blocks(n, PP);
-  const uint32_t uG = (uint32_t)G;
-  if (hist) {
-    if (vec4) hipLaunchKernelGGL((k_residual_add<4, true>), grid, dim3(256), 0, s, acc, ld_acc, grad, ld_grad, B, uG, sp);
-    else hipLaunchKernelGGL((k_residual_add<1, true>), grid, dim3(256), 0, s, acc, ld_acc, grad, ld_grad, B, uG, sp);
+  if (vec4) {
+    // tiles from each block's aligned origin: up to 31 more elements per block
+    const uint32_t G = (uint32_t)add_tiles_per_block(maxlen);
+    const dim3 grid((unsigned)((int64_t)nworkers * PP * G));
+    if (hist) hipLaunchKernelGGL(k_residual_add4<true>, grid, dim3(256), 0, s, acc, ld_acc, grad, ld_grad, B, G, sp);
+    else hipLaunchKernelGGL(k_residual_add4<false>, grid, dim3(256), 0, s, acc, ld_acc, grad, ld_grad, B, G, sp);
   } else {
-    if (vec4) hipLaunchKernelGGL((k_residual_add<4, false>), grid, dim3(256), 0, s, acc, ld_acc, grad, ld_grad, B, uG, sp);
-    else hipLaunchKernelGGL((k_residual_add<1, false>), grid, dim3(256), 0, s, acc, ld_acc, grad, ld_grad, B, uG, sp);
+    const uint32_t G = (uint32_t)((maxlen + ADD_TILE - 1) / ADD_TILE);
+    const dim3 grid((unsigned)((int64_t)nworkers * PP * G));
+    if (hist) hipLaunchKernelGGL(k_residual_add1<true>, grid, dim3(256), 0, s, acc, ld_acc, grad, ld_grad, B, G, sp);
+    else hipLaunchKernelGGL(k_residual_add1<false>, grid, dim3(256), 0, s, acc, ld_acc, grad, ld_grad, B, G, sp);
   }
   return hipGetLastError();
 }

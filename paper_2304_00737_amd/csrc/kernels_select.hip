@@ -117,9 +117,16 @@ __global__ __launch_bounds__(1024) void k_select1(uint32_t* __restrict__ hist1, 
 //          rounded up to whole slots of MERGE_TILE positions.
 struct SlotGeom {
   int64_t base;    // first entry of the unit's region
-  int64_t len;     // length of the unit's region (slot s holds at most min(ss, len - s ss))
+  int64_t len;     // length of the unit's region
   int32_t ss;      // slot size
+  int32_t lead;    // slot 0 is short by this much (mode 0: slots start at the block's aligned origin)
   int32_t nslots;  // slots of this unit
+  // first entry of slot s in the region, and the entries the slot spans
+  __device__ __forceinline__ int64_t off(int32_t s) const { return s == 0 ? 0 : (int64_t)s * ss - lead; }
+  __device__ __forceinline__ int64_t cap(int32_t s) const {
+    const int64_t hi = (int64_t)(s + 1) * ss - lead;
+    return (hi < len ? hi : len) - off(s);
+  }
 };
 
 __device__ __forceinline__ SlotGeom slot_geom(int mode, uint32_t unit, const Blocks& B, const Units& U,
@@ -132,12 +139,14 @@ __device__ __forceinline__ SlotGeom slot_geom(int mode, uint32_t unit, const Blo
     g.base = (int64_t)w * B.n + s;
     g.len = e - s;
     g.ss = SLOT;
-    g.nslots = (int32_t)((e - s + SLOT - 1) / SLOT);
+    g.lead = (int32_t)block_lead(s);
+    g.nslots = (int32_t)((e - s + g.lead + SLOT - 1) / SLOT);
   } else {
     g.nslots = (int32_t)((2 * kb + MERGE_TILE - 1) / MERGE_TILE);
     g.base = (int64_t)unit * g.nslots * MERGE_TILE;   // whole slots per unit: float4-aligned, full last slot
     g.len = 2 * kb;
     g.ss = MERGE_TILE;
+    g.lead = 0;
   }
   return g;
 }
@@ -248,7 +257,8 @@ __device__ __forceinline__ void collect_slot(const float* __restrict__ A, uint32
 }
 
 // A slot whose candidates the fused residual add already wrote (every key at
-// or above its floor; per add tile, in index order at the tile's span) is
+// or above its floor; per add tile, in index order at the tile's span: the
+// second tile's list starts off1 entries after the slot's first) is
 // filtered by one wave: the entries at or above the level-1 threshold bin are
 // compacted in place in index order (the first tile's list, then the
 // second's) and the bin keys stored.  Each chunk is loaded into registers
@@ -256,7 +266,7 @@ __device__ __forceinline__ void collect_slot(const float* __restrict__ A, uint32
 // storage position of an entry not yet read, so no barrier is needed.
 static_assert(SLOT == 2 * ADD_TILE, "a slot holds two residual-add tiles");
 constexpr int RC_R = 16;  // entries per lane per chunk (a crowded slot holds up to 4096)
-__device__ __forceinline__ void recollect_wave(uint32_t c0, uint32_t c1, uint32_t tlo, uint32_t thi,
+__device__ __forceinline__ void recollect_wave(uint32_t c0, uint32_t c1, uint32_t off1, uint32_t tlo, uint32_t thi,
                                                uint32_t* cnt_out, uint32_t* nbin_out, int32_t* __restrict__ CI,
                                                float* __restrict__ CV, uint32_t* __restrict__ BK) {
   const int lane = lane_id();
@@ -272,7 +282,7 @@ __device__ __forceinline__ void recollect_wave(uint32_t c0, uint32_t c1, uint32_
       ix[r] = 0;
       vx[r] = 0.f;
       if (e < tot) {
-        const uint32_t src = e < c0 ? e : (uint32_t)ADD_TILE + (e - c0);
+        const uint32_t src = e < c0 ? e : off1 + (e - c0);
         ix[r] = CI[src];
         vx[r] = CV[src];
       }
@@ -305,7 +315,7 @@ __device__ __forceinline__ void recollect_wave(uint32_t c0, uint32_t c1, uint32_
 // slots are in flight together; later chunks of RC_R2 per lane.
 constexpr int RC_R2 = 8;
 template <int R1>
-__device__ __forceinline__ void recollect_wave_pre(uint32_t c0, uint32_t c1, uint32_t tlo, uint32_t thi,
+__device__ __forceinline__ void recollect_wave_pre(uint32_t c0, uint32_t c1, uint32_t off1, uint32_t tlo, uint32_t thi,
                                                    uint32_t* cnt_out, uint32_t* nbin_out, int32_t* __restrict__ CI,
                                                    float* __restrict__ CV, uint32_t* __restrict__ BK,
                                                    const int32_t (&ix1)[R1], const float (&vx1)[R1]) {
@@ -339,7 +349,7 @@ __device__ __forceinline__ void recollect_wave_pre(uint32_t c0, uint32_t c1, uin
       ix[r] = 0;
       vx[r] = 0.f;
       if (e < tot) {
-        const uint32_t src = e < c0 ? e : (uint32_t)ADD_TILE + (e - c0);
+        const uint32_t src = e < c0 ? e : off1 + (e - c0);
         ix[r] = CI[src];
         vx[r] = CV[src];
       }
@@ -385,25 +395,34 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(SPW >= 8 ? 
   U.decode(blockIdx.x / gq, B.P, &w, &b);
   const uint32_t unit = w * B.P + b;   // the block's arrays
   const uint32_t s = B.start(b), e = B.start(b + 1u);
-  if (s + slot0 * (uint32_t)SLOT >= e) return;
+  // slot i spans [o + i SLOT, o + (i+1) SLOT) clipped to the block, o its aligned origin; its two add
+  // tiles' candidate lists start at the slot's first element and at o + i SLOT + ADD_TILE
+  const uint32_t o = block_origin(s);
+  if (o + slot0 * (uint32_t)SLOT >= e) return;
   const uint32_t* st = state + (int64_t)unit * ST_WORDS;
+  // counts are clamped to the tiles' lengths inside the block, so reads stay in the slot
+  auto tiles = [&](uint32_t slot, uint32_t* t0, uint32_t* len0, uint32_t* len1) {
+    const uint32_t sa = o + slot * (uint32_t)SLOT;
+    *t0 = sa > s ? sa : s;
+    const uint32_t m = sa + (uint32_t)ADD_TILE;
+    *len0 = (m < e ? m : e) - *t0;
+    *len1 = m < e ? min(e - m, (uint32_t)ADD_TILE) : 0u;
+  };
   if constexpr (SPW == 1) {
     const uint32_t specok = st[ST_SPECOK];
     if (specok != 0u) {
       const uint32_t T1 = st[ST_T1];
       const uint32_t tlo = T1 << D1_SHIFT, thi = tlo + (1u << D1_SHIFT);
       const uint32_t slot = slot0 + (uint32_t)wave_id();
-      const uint32_t t0 = s + slot * (uint32_t)SLOT;
-      if (slot >= smax || t0 >= e) return;
+      if (slot >= smax || o + slot * (uint32_t)SLOT >= e) return;
+      uint32_t t0, len0, len1;
+      tiles(slot, &t0, &len0, &len1);
       const int64_t tile0 = (int64_t)unit * add_tiles + (int64_t)slot * (SLOT / ADD_TILE);
-      // counts are clamped to the tiles' lengths inside the block, so reads stay in the slot
-      const uint32_t len0 = min(e - t0, (uint32_t)ADD_TILE);
-      const uint32_t len1 = t0 + (uint32_t)ADD_TILE < e ? min(e - t0 - (uint32_t)ADD_TILE, (uint32_t)ADD_TILE) : 0u;
       const uint32_t c0 = min(spec_cnt[tile0], len0);
       const uint32_t c1 = len1 != 0u ? min(spec_cnt[tile0 + 1], len1) : 0u;
       const int64_t cbase = (int64_t)w * B.n + t0;
       const int64_t si = (int64_t)unit * smax + slot;
-      recollect_wave(c0, c1, tlo, thi, slot_cnt + si, slot_nbin + si, cand_idx + cbase, cand_val + cbase,
+      recollect_wave(c0, c1, len0, tlo, thi, slot_cnt + si, slot_nbin + si, cand_idx + cbase, cand_val + cbase,
                      bin_key + cbase);
       return;
     }
@@ -412,19 +431,20 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(SPW >= 8 ? 
     // state words (in bounds for any live slot)
     constexpr int R1 = SPW >= 8 ? 1 : 4;   // first entries per lane of each slot
     const uint32_t sw = slot0 + (uint32_t)wave_id() * (uint32_t)SPW;
-    uint32_t c0[SPW], c1[SPW];
+    uint32_t c0[SPW], c1[SPW], off1[SPW];
 #pragma unroll
     for (int j = 0; j < SPW; ++j) {
       const uint32_t slot = sw + (uint32_t)j;
-      const uint32_t t0 = s + slot * (uint32_t)SLOT;
       c0[j] = 0u;
       c1[j] = 0u;
-      if (slot < smax && t0 < e) {
+      off1[j] = 0u;
+      if (slot < smax && o + slot * (uint32_t)SLOT < e) {
+        uint32_t t0, len0, len1;
+        tiles(slot, &t0, &len0, &len1);
         const int64_t tile0 = (int64_t)unit * add_tiles + (int64_t)slot * (SLOT / ADD_TILE);
-        const uint32_t len0 = min(e - t0, (uint32_t)ADD_TILE);
-        const uint32_t len1 = t0 + (uint32_t)ADD_TILE < e ? min(e - t0 - (uint32_t)ADD_TILE, (uint32_t)ADD_TILE) : 0u;
         c0[j] = min(spec_cnt[tile0], len0);
         c1[j] = len1 != 0u ? min(spec_cnt[tile0 + 1], len1) : 0u;
+        off1[j] = len0;
       }
     }
     const uint32_t specok = st[ST_SPECOK];
@@ -437,14 +457,15 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(SPW >= 8 ? 
 #pragma unroll
       for (int j = 0; j < SPW; ++j) {
         const uint32_t tot = c0[j] + c1[j];
-        const int64_t cbase = (int64_t)w * B.n + s + (sw + (uint32_t)j) * (uint32_t)SLOT;
+        const uint32_t sa = o + (sw + (uint32_t)j) * (uint32_t)SLOT;
+        const int64_t cbase = (int64_t)w * B.n + (sa > s ? sa : s);
 #pragma unroll
         for (int r = 0; r < R1; ++r) {
           const uint32_t q = (uint32_t)(r * WAVE + lane);
           ix[j][r] = 0;
           vx[j][r] = 0.f;
           if (q < tot) {
-            const uint32_t src = q < c0[j] ? q : (uint32_t)ADD_TILE + (q - c0[j]);
+            const uint32_t src = q < c0[j] ? q : off1[j] + (q - c0[j]);
             ix[j][r] = cand_idx[cbase + src];
             vx[j][r] = cand_val[cbase + src];
           }
@@ -453,11 +474,11 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(SPW >= 8 ? 
 #pragma unroll
       for (int j = 0; j < SPW; ++j) {
         const uint32_t slot = sw + (uint32_t)j;
-        const uint32_t t0 = s + slot * (uint32_t)SLOT;
-        if (slot >= smax || t0 >= e) break;   // wave-uniform; later slots are past the block too
-        const int64_t cbase = (int64_t)w * B.n + t0;
+        if (slot >= smax || o + slot * (uint32_t)SLOT >= e) break;   // wave-uniform; later slots are past the block too
+        const uint32_t sa = o + slot * (uint32_t)SLOT;
+        const int64_t cbase = (int64_t)w * B.n + (sa > s ? sa : s);
         const int64_t si = (int64_t)unit * smax + slot;
-        recollect_wave_pre<R1>(c0[j], c1[j], tlo, thi, slot_cnt + si, slot_nbin + si, cand_idx + cbase,
+        recollect_wave_pre<R1>(c0[j], c1[j], off1[j], tlo, thi, slot_cnt + si, slot_nbin + si, cand_idx + cbase,
                                cand_val + cbase, bin_key + cbase, ix[j], vx[j]);
       }
       return;
@@ -465,11 +486,12 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(SPW >= 8 ? 
   }
   for (int k = 0; k < COLLECT_GROUP; ++k) {
     const uint32_t slot = slot0 + (uint32_t)k;
-    const uint32_t t0 = s + slot * (uint32_t)SLOT;
-    if (slot >= smax || t0 >= e) break;   // uniform
+    if (slot >= smax || o + slot * (uint32_t)SLOT >= e) break;   // uniform
     if (k > 0) __syncthreads();           // LDS reuse
-    const uint32_t rem = e - t0;          // entries of this slot inside the block, clamped in 32 bits
-    const uint32_t nvalid = rem < (uint32_t)SLOT ? rem : (uint32_t)SLOT;
+    const uint32_t sa = o + slot * (uint32_t)SLOT;
+    const uint32_t t0 = sa > s ? sa : s;
+    const uint32_t hi = sa + (uint32_t)SLOT;
+    const uint32_t nvalid = (hi < e ? hi : e) - t0;   // entries of this slot inside the block
     const float* __restrict__ A = acc + (int64_t)w * ld_acc + t0;
     const int64_t cbase = (int64_t)w * B.n + t0;
     const int64_t si = (int64_t)unit * smax + slot;
@@ -687,7 +709,7 @@ __device__ __forceinline__ uint32_t block_excl_max(uint32_t v, uint32_t* scratch
 // each entry by binary search.
 template <typename F>
 __device__ __forceinline__ void visit_bin_chunk(const uint32_t* __restrict__ K, const uint32_t* pref, int ns,
-                                                int64_t ss, uint32_t c0, uint32_t total, F fn) {
+                                                const SlotGeom& g, uint32_t c0, uint32_t total, F fn) {
   constexpr int B = 8;
   for (int r0 = 0; r0 < FAST_R0; r0 += B) {
     uint32_t key[B], sl[B];
@@ -698,7 +720,7 @@ __device__ __forceinline__ void visit_bin_chunk(const uint32_t* __restrict__ K, 
       sl[r] = 0u;
       if (f < total) {
         sl[r] = (uint32_t)slot_of_entry(pref, ns, f);
-        key[r] = K[(int64_t)sl[r] * ss + (f - pref[sl[r]])];
+        key[r] = K[g.off((int32_t)sl[r]) + (f - pref[sl[r]])];
       }
     }
 #pragma unroll
@@ -734,7 +756,7 @@ __device__ __forceinline__ void thresh_fast_topk(FastSmem& L, int64_t unit, cons
 #pragma unroll
     for (int u = 0; u < PS; ++u) {
       const int s = PS * t + u;
-      const uint32_t cap = s < ns ? (uint32_t)min((int64_t)g.ss, g.len - (int64_t)s * g.ss) : 0u;
+      const uint32_t cap = s < ns ? (uint32_t)g.cap(s) : 0u;
       nb[u] = min(nb[u], min(ca0[u], cap));
     }
   }
@@ -787,7 +809,7 @@ __device__ __forceinline__ void thresh_fast_topk(FastSmem& L, int64_t unit, cons
     uint32_t key = KEY_NONE, sl = 0u;
     if (f < m) {
       sl = L.u.slotid[map_half(f)];
-      key = K[(int64_t)sl * g.ss + (f - L.pref[sl])];
+      key = K[g.off((int32_t)sl) + (f - L.pref[sl])];
     }
     rk[r] = key;
     if (r & 1) rs[r / 2] |= sl << 16;
@@ -799,7 +821,7 @@ __device__ __forceinline__ void thresh_fast_topk(FastSmem& L, int64_t unit, cons
     for (int r = 0; r < FAST_R0; ++r)
       if ((rk[r] >> D1_SHIFT) == T1) fn(rk[r]);
     for (uint32_t c = 1; c < nchunks; ++c)
-      visit_bin_chunk(K, L.pref, ns, g.ss, c * FAST_CAP0, total, [&](uint32_t key, uint32_t) {
+      visit_bin_chunk(K, L.pref, ns, g, c * FAST_CAP0, total, [&](uint32_t key, uint32_t) {
         if ((key >> D1_SHIFT) == T1) fn(key);
       });
   };
@@ -817,7 +839,7 @@ __device__ __forceinline__ void thresh_fast_topk(FastSmem& L, int64_t unit, cons
 #pragma unroll
   for (int r = 0; r < FAST_R0; ++r)
     if (rk[r] != KEY_NONE) count1(rk[r], (r & 1) ? (rs[r / 2] >> 16) : (rs[r / 2] & 0xFFFFu));
-  for (uint32_t c = 1; c < nchunks; ++c) visit_bin_chunk(K, L.pref, ns, g.ss, c * FAST_CAP0, total, count1);
+  for (uint32_t c = 1; c < nchunks; ++c) visit_bin_chunk(K, L.pref, ns, g, c * FAST_CAP0, total, count1);
   __syncthreads();
   uint32_t sa = 0, sg = 0, se = 0, ca[PS], gq[PS], eq[PS];
 #pragma unroll
@@ -828,7 +850,7 @@ __device__ __forceinline__ void thresh_fast_topk(FastSmem& L, int64_t unit, cons
 #pragma unroll
   for (int u = 0; u < PS; ++u) {
     const int s = PS * t + u;
-    const uint32_t cap = s < ns ? (uint32_t)min((int64_t)g.ss, g.len - (int64_t)s * g.ss) : 0u;
+    const uint32_t cap = s < ns ? (uint32_t)g.cap(s) : 0u;
     ca[u] = min(ca[u], cap);
     const uint32_t nbu = s < ns ? L.pref[s + 1] - L.pref[s] : 0u;   // bin entries of the slot (<= ca)
     gq[u] = s < ns ? ca[u] - nbu + L.u.c.cg[s] : 0u;                 // entries above the bin are all selected
@@ -967,7 +989,7 @@ __device__ __forceinline__ void visit_bin_group(const SlotGeom& g, int32_t s0, i
           else hi = mid;
         }
         sl[r] = lo;
-        key[r] = K[(int64_t)(s0 + lo) * g.ss + (e - pref[lo])];
+        key[r] = K[g.off(s0 + lo) + (e - pref[lo])];
       }
     }
 #pragma unroll
@@ -985,9 +1007,8 @@ __device__ __forceinline__ void visit_bin_slots_topk(const SlotGeom& g, int32_t 
                                                      const uint32_t* __restrict__ nbn, F f) {
   const int nw = blockDim.x / WAVE;
   for (int32_t slot = s0 + wave_id(); slot < s1; slot += nw) {
-    const int64_t room = g.len - (int64_t)slot * g.ss;   // entries of the region in this slot
-    const uint32_t nb = (uint32_t)min(min((int64_t)nbn[slot], (int64_t)g.ss), room);
-    const uint32_t* __restrict__ Ks = K + (int64_t)slot * g.ss;
+    const uint32_t nb = (uint32_t)min((int64_t)nbn[slot], g.cap(slot));   // within the slot's span
+    const uint32_t* __restrict__ Ks = K + g.off(slot);
     for (uint32_t j = lane_id(); j < nb; j += WAVE) f(Ks[j], slot);
   }
 }
@@ -1000,7 +1021,7 @@ __device__ __forceinline__ void visit_bin_slots_merge(const SlotGeom& g, int32_t
                                                       uint32_t T1, F f) {
   for (int32_t slot = s0; slot < s1; ++slot) {
     const uint32_t c = min(cnt[slot], (uint32_t)g.ss);
-    const float* __restrict__ Vs = V + (int64_t)slot * g.ss;
+    const float* __restrict__ Vs = V + g.off(slot);
     for (uint32_t j0 = 0; j0 < c; j0 += BIG_THREADS * BIG_R1) {   // a merge slot is one chunk
       float v[BIG_R1];
 #pragma unroll
@@ -1089,8 +1110,7 @@ __global__ __launch_bounds__(256) void k_big_hist(BigArgs a, uint32_t ngroups) {
     const int32_t slot = s0 + (int32_t)threadIdx.x;
     uint32_t nb = 0u;
     if (slot < s1) {
-      const int64_t room = g.len - (int64_t)slot * g.ss;   // entries of the region in this slot
-      nb = (uint32_t)min(min((int64_t)a.slot_nbin[ua * a.smax + slot], (int64_t)g.ss), room);
+      nb = (uint32_t)min((int64_t)a.slot_nbin[ua * a.smax + slot], g.cap(slot));   // within the slot's span
     }
     visit_bin_group(g, s0, a.group, a.bin_key + g.base, nb, pref, scratch, bump);   // its first barrier orders the zeroing
   } else if (mode == 0) {
@@ -1178,10 +1198,9 @@ __global__ __launch_bounds__(256) void k_big_count(BigArgs a, uint32_t ngroups) 
     // a wave per slot: the entries above the bin are selected; count the bin's keys
     const int nw = blockDim.x / WAVE;
     for (int32_t slot = s0 + wave_id(); slot < s1; slot += nw) {
-      const int64_t room = g.len - (int64_t)slot * g.ss;
-      const uint32_t c = (uint32_t)min(min((int64_t)cnt[slot], (int64_t)g.ss), room);
+      const uint32_t c = (uint32_t)min((int64_t)cnt[slot], g.cap(slot));
       const uint32_t nb = min(nbn[slot], c);
-      const uint32_t* __restrict__ Ks = a.bin_key + g.base + (int64_t)slot * g.ss;
+      const uint32_t* __restrict__ Ks = a.bin_key + g.base + g.off(slot);
       uint32_t ge = 0, eq = 0;
       for (uint32_t j = lane_id(); j < nb; j += WAVE) {
         const uint32_t key = Ks[j];
@@ -1204,8 +1223,7 @@ __global__ __launch_bounds__(256) void k_big_count(BigArgs a, uint32_t ngroups) 
     const int32_t slot = s0 + (int32_t)threadIdx.x;
     uint32_t c = 0u, nb = 0u;
     if (slot < s1) {
-      const int64_t room = g.len - (int64_t)slot * g.ss;
-      c = (uint32_t)min(min((int64_t)cnt[slot], (int64_t)g.ss), room);
+      c = (uint32_t)min((int64_t)cnt[slot], g.cap(slot));
       nb = min(nbn[slot], c);
     }
     sge[threadIdx.x] = 0u;
@@ -1223,7 +1241,7 @@ __global__ __launch_bounds__(256) void k_big_count(BigArgs a, uint32_t ngroups) 
     (void)T1;
     for (int32_t slot = s0; slot < s1; ++slot) {
       const uint32_t c = min(cnt[slot], (uint32_t)g.ss);
-      const float* __restrict__ Vs = a.U_val + g.base + (int64_t)slot * g.ss;
+      const float* __restrict__ Vs = a.U_val + g.base + g.off(slot);
       uint32_t ge = 0, eq = 0;
       for (uint32_t j0 = 0; j0 < c; j0 += BIG_THREADS * BIG_R1) {   // a merge slot is one chunk
         float v[BIG_R1];
@@ -1289,7 +1307,7 @@ __global__ __launch_bounds__(1024) void k_big_scan(BigArgs a) {
 #pragma unroll
     for (int r = 0; r < SCAN_R; ++r) {
       const uint32_t i = (uint32_t)r * NT + threadIdx.x;
-      v[0][r] = i < ns ? min(cnt[i], (uint32_t)g.ss) : 0u;
+      v[0][r] = i < ns ? (uint32_t)min((int64_t)cnt[i], g.cap((int32_t)i)) : 0u;
       v[1][r] = i < ns ? a.pre_ge[o + i] : 0u;
       v[2][r] = i < ns ? a.pre_eq[o + i] : 0u;
     }
@@ -1321,7 +1339,7 @@ __global__ __launch_bounds__(1024) void k_big_scan(BigArgs a) {
     te = tots[2];
   } else {
     for (uint32_t i = i0; i < i1; ++i) {
-      sa += min(cnt[i], (uint32_t)g.ss);
+      sa += (uint32_t)min((int64_t)cnt[i], g.cap((int32_t)i));
       sg += a.pre_ge[o + i];
       se += a.pre_eq[o + i];
     }
@@ -1329,7 +1347,7 @@ __global__ __launch_bounds__(1024) void k_big_scan(BigArgs a) {
     uint32_t xg = block_excl_scan(sg, scratch, &tg);
     uint32_t xe = block_excl_scan(se, scratch, &te);
     for (uint32_t i = i0; i < i1; ++i) {
-      const uint32_t ca = min(cnt[i], (uint32_t)g.ss), cg = a.pre_ge[o + i], ce = a.pre_eq[o + i];
+      const uint32_t ca = (uint32_t)min((int64_t)cnt[i], g.cap((int32_t)i)), cg = a.pre_ge[o + i], ce = a.pre_eq[o + i];
       a.pre_all[o + i] = xa;
       a.pre_ge[o + i] = xg;
       a.pre_eq[o + i] = xe;
@@ -1441,10 +1459,10 @@ __global__ __launch_bounds__(256) void k_emit(
     const int64_t si = (int64_t)au * smax + slot;
     const uint32_t* st = state + (int64_t)au * ST_WORDS;
     // independent loads: the slot's count and prefixes, the unit's threshold
-    const uint32_t cnt = min(slot_cnt[si], (uint32_t)g.ss);
+    const uint32_t cnt = (uint32_t)min((int64_t)slot_cnt[si], g.cap(slot));
     uint32_t run_g = pre_ge[si], run_e = pre_eq[si];
     const uint32_t tge = st[ST_TGE], teq = st[ST_TEQ], need_eq = st[ST_NEEDEQ];
-    const int64_t base = g.base + (int64_t)slot * g.ss;
+    const int64_t base = g.base + g.off(slot);
     uint32_t w, b;
     U.decode(unit, B.P, &w, &b);
     const int64_t o = ((int64_t)w * B.P + b) * kb;
@@ -1503,7 +1521,7 @@ __global__ __launch_bounds__(256) void k_emit(
       re[j] = 0u;
       if (sw + j < g.nslots) {
         const int64_t si = (int64_t)au * smax + sw + j;
-        cnt[j] = min(slot_cnt[si], (uint32_t)g.ss);
+        cnt[j] = (uint32_t)min((int64_t)slot_cnt[si], g.cap(sw + j));
         rg[j] = pre_ge[si];
         re[j] = pre_eq[si];
       }
@@ -1513,7 +1531,7 @@ __global__ __launch_bounds__(256) void k_emit(
     float vx[SPW][R1];
 #pragma unroll
     for (int j = 0; j < SPW; ++j) {
-      const int64_t base = g.base + (int64_t)(sw + j) * g.ss;
+      const int64_t base = g.base + g.off(sw + j);
 #pragma unroll
       for (int r = 0; r < R1; ++r) {
         const uint32_t p = (uint32_t)(r * WAVE + lane);
@@ -1531,7 +1549,7 @@ __global__ __launch_bounds__(256) void k_emit(
 #pragma unroll
     for (int j = 0; j < SPW; ++j) {
       if (sw + j >= g.nslots) break;   // wave-uniform
-      const int64_t base = g.base + (int64_t)(sw + j) * g.ss;
+      const int64_t base = g.base + g.off(sw + j);
       emit_topk_slot<R1>(cnt[j], rg[j], re[j], tge, teq, need_eq, kb, cand_idx + base, cand_val + base, ix[j], vx[j],
                      out_idx + o, out_val + o, local_idx ? local_idx + o : nullptr, err);
     }
@@ -1549,7 +1567,7 @@ __global__ __launch_bounds__(256) void k_emit(
     const uint32_t all_before = pre_all[si];
     uint32_t run_g = pre_ge[si], run_e = pre_eq[si];
     const uint32_t tge = st[ST_TGE], teq = st[ST_TEQ], need_eq = st[ST_NEEDEQ];
-    const int64_t base = g.base + (int64_t)slot * g.ss;
+    const int64_t base = g.base + g.off(slot);
     int64_t hb, rb;
     bool both;
     PM.decode(unit, &hb, &rb, &both);

@@ -103,9 +103,9 @@ def ws_layout(P: int, n: int, kb: int, ws_bytes: int) -> dict:
     maxlen = -(-n // P)
     pairs_max = P * mmax
     units = max(P * P, pairs_max)
-    tiles_tk = -(-maxlen // 4096)
+    tiles_tk = -(-(maxlen + 31) // 4096)     # slots and add tiles start at a block's 32-aligned origin
     tiles_mg = -(-2 * kb // 4096)
-    add_tiles = -(-maxlen // 2048)
+    add_tiles = -(-(maxlen + 31) // 2048)
     slot_n = max(P * P * tiles_tk, pairs_max * tiles_mg)
     L, off = {}, 256
     L["bitmap"] = off; off += al(-(-n // 32) * 4)
