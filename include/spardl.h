@@ -150,6 +150,33 @@ int spardl_sparse_merge_topk(int32_t* sp_idx, float* sp_val, int32_t P, int64_t 
                              int32_t round, int32_t* drop_idx, float* drop_val, int32_t* drop_cnt,
                              void* ws, size_t ws_bytes, hipStream_t stream);
 
+/* The same SRS step without a workspace, for callers that cannot allocate
+ * device memory (code under HIP graph capture, tight serving loops, hosts
+ * that forbid hipMalloc).  Its scratch (per merge pair: the level-1
+ * histogram, selection state, slot counts and the summed union) lives in one
+ * array of SPARDL_NOALLOC_SCRATCH_BYTES inside the library, which every GPU
+ * the library runs on holds from its first such call until the process ends;
+ * the call allocates nothing, and it neither synchronises nor copies.
+ * Results are bit-identical to spardl_sparse_merge_topk with the same
+ * arguments.  err (device, 4 bytes, caller owned) is an output: the call
+ * clears it and its kernels OR in SPARDL_WS_ERR_* bits if an internal check
+ * fails.  The scratch is shared by every call on one GPU and keeps the last
+ * call's contents (each call clears what it needs zeroed), so calls that
+ * overlap on one GPU (different streams, or different host threads) race and
+ * must not be issued.
+ * Errors: as spardl_sparse_merge_topk (EINVAL also for NULL err);
+ * ECAPACITY when the step needs more than SPARDL_NOALLOC_SCRATCH_BYTES of
+ * scratch, checked before any GPU call: each of the P m merge pairs of the
+ * step (m = its bag_blocks) takes 16 KiB + 64 bytes, plus 32 KiB + 20 bytes
+ * per slot of 4096 merged positions (ceil(2 k_blk / 4096) slots), each
+ * array rounded up to 256 bytes (the ResNet-50-sized step 1: 32 pairs,
+ * 16 slots each, 16.5 MiB); EDEVICE if the scratch's device address cannot
+ * be obtained. */
+#define SPARDL_NOALLOC_SCRATCH_BYTES (64u << 20)
+int spardl_sparse_merge_topk_noalloc(int32_t* sp_idx, float* sp_val, int32_t P, int64_t n, int32_t k_blk,
+                                     int32_t round, int32_t* drop_idx, float* drop_val, int32_t* drop_cnt,
+                                     uint32_t* err, hipStream_t stream);
+
 /* Final All-Gather and decode (end of Sec. III-B; Algorithm 1 "All-Gather all
  * blocks from all workers").  After step l, worker b holds the reduced block
  * b in sp[b][b]; the All-Gather gives every worker all P of them, which on

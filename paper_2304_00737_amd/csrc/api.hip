@@ -6,6 +6,7 @@
 #include <stdint.h>
 
 #include <algorithm>
+#include <mutex>
 
 #include "../../include/spardl.h"
 #include "common.hpp"
@@ -285,6 +286,71 @@ size_t team_ws_bytes(int32_t P, int32_t d, int64_t n, int32_t kb) {
   return L.fixed_end + cand_bytes(cand);
 }
 
+// ---- scratch of the workspace-free SRS step (spardl_sparse_merge_topk_noalloc):
+// per merge pair a level-1 histogram and the selection state, per slot the
+// counts and prefixes, then the summed union (index, value).
+struct NoallocLayout {
+  size_t hist, state, slot_cnt, slot_nbin, pre_all, pre_ge, pre_eq, uidx, uval, end;
+};
+
+NoallocLayout make_noalloc_layout(int64_t npairs, int32_t kb) {
+  NoallocLayout L;
+  const int64_t slots = npairs * ceil_div(2ll * kb, MERGE_TILE);
+  size_t off = 0;
+  auto take = [&](int64_t bytes) {
+    const size_t at = off;
+    off += align256((size_t)bytes);
+    return at;
+  };
+  L.hist = take(npairs * NB1 * 4);
+  L.state = take(npairs * ST_WORDS * 4);
+  L.slot_cnt = take(slots * 4);
+  L.slot_nbin = take(slots * 4);
+  L.pre_all = take(slots * 4);
+  L.pre_ge = take(slots * 4);
+  L.pre_eq = take(slots * 4);
+  L.uidx = take(slots * MERGE_TILE * 4);
+  L.uval = take(slots * MERGE_TILE * 4);
+  L.end = off;
+  return L;
+}
+
+}  // namespace
+
+// The scratch array of spardl_sparse_merge_topk_noalloc.  In host code its
+// name is a host-side stand-in: the device address (one per GPU) comes from
+// hipGetSymbolAddress and only that address is handed to kernels.
+static __device__ __align__(256) unsigned char scratch[SPARDL_NOALLOC_SCRATCH_BYTES];
+
+namespace {
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_addr[kMaxDevices];
+
+// Device address of `scratch` on the GPU that runs `stream`: looked up once
+// per GPU, with that GPU current, and kept.  Null if it cannot be obtained.
+void* noalloc_scratch(hipStream_t stream) {
+  int cur = -1, dev = -1;
+  if (hipGetDevice(&cur) != hipSuccess) return nullptr;
+  if (stream) {
+    if (hipStreamGetDevice(stream, &dev) != hipSuccess) return nullptr;
+  } else {
+    dev = cur;
+  }
+  if (dev < 0 || dev >= kMaxDevices) return nullptr;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_addr[dev]) {
+    if (dev != cur && hipSetDevice(dev) != hipSuccess) return nullptr;
+    void* p = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (dev != cur) (void)hipSetDevice(cur);
+    if (e != hipSuccess || !p) return nullptr;
+    g_scratch_addr[dev] = p;
+  }
+  return g_scratch_addr[dev];
+}
+
 }  // namespace
 
 extern "C" {
@@ -293,7 +359,7 @@ const char* spardl_strerror(int status) {
   switch (status) {
     case SPARDL_OK: return "ok";
     case SPARDL_EINVAL: return "invalid argument";
-    case SPARDL_ECAPACITY: return "workspace too small";
+    case SPARDL_ECAPACITY: return "workspace (or the library's static scratch) too small for these sizes";
     case SPARDL_EDEVICE: return "kernel launch failed";
     default: return "unknown status";
   }
@@ -401,6 +467,42 @@ int spardl_sparse_merge_topk(int32_t* sp_idx, float* sp_val, int32_t P, int64_t 
                            w.bin_key, w.pre_all, w.pre_ge, w.pre_eq, drop_cnt, w.err, stream));
   SPARDL_TRY(launch_emit(1, w.cand_idx, w.cand_val, pairs, all_blocks(P), n, P, k_blk, PM, smax, w.state, w.slot_cnt, w.pre_all,
                          w.pre_ge, w.pre_eq, sp_idx, sp_val, nullptr, drop_idx, drop_val, w.err, stream));
+  return SPARDL_OK;
+}
+
+int spardl_sparse_merge_topk_noalloc(int32_t* sp_idx, float* sp_val, int32_t P, int64_t n, int32_t k_blk,
+                                     int32_t round, int32_t* drop_idx, float* drop_val, int32_t* drop_cnt,
+                                     uint32_t* err, hipStream_t stream) {
+  if (!sp_idx || !sp_val || !drop_idx || !drop_val || !drop_cnt || !err || P < 2 || !sizes_ok(P, n, k_blk))
+    return SPARDL_EINVAL;
+  const int32_t l = steps_of(P);
+  if (round < 1 || round > l) return SPARDL_EINVAL;
+  const int32_t d = 1 << (l - round);
+  const int32_t m = bag_of(P, l, round);
+  const int64_t pairs = (int64_t)P * m;
+  const NoallocLayout L = make_noalloc_layout(pairs, k_blk);
+  if (L.end > (size_t)SPARDL_NOALLOC_SCRATCH_BYTES) return SPARDL_ECAPACITY;
+  char* base = (char*)noalloc_scratch(stream);
+  if (!base) return SPARDL_EDEVICE;
+  auto at = [&](size_t off) { return (uint32_t*)(base + off); };
+  uint32_t* hist = at(L.hist);
+  uint32_t* state = at(L.state);
+  uint32_t *slot_cnt = at(L.slot_cnt), *slot_nbin = at(L.slot_nbin);
+  uint32_t *pre_all = at(L.pre_all), *pre_ge = at(L.pre_ge), *pre_eq = at(L.pre_eq);
+  int32_t* uidx = (int32_t*)(base + L.uidx);
+  float* uval = (float*)(base + L.uval);
+  const int32_t smax = (int32_t)ceil_div(2ll * k_blk, MERGE_TILE);
+  const Pairs PM = srs_pairs(P, m, d);
+  // the scratch keeps the previous call's contents: the histograms the merge
+  // accumulates into start from zero, and so does the caller's error word
+  SPARDL_TRY(launch_fill(Fill().add(hist, pairs * NB1).add(err, 1).r, stream));
+  SPARDL_TRY(launch_merge(sp_idx, sp_val, PM, pairs, k_blk, smax, hist, slot_cnt, uidx, uval, stream));
+  // a merge's threshold reads keys from the union values (the bin-key array is a block top-k's)
+  SPARDL_TRY(launch_thresh(1, pairs, all_blocks(P), n, P, k_blk, smax, hist, uval, state, slot_cnt, slot_nbin,
+                           reinterpret_cast<const uint32_t*>(uval), pre_all, pre_ge, pre_eq, drop_cnt, err,
+                           stream));
+  SPARDL_TRY(launch_emit(1, uidx, uval, pairs, all_blocks(P), n, P, k_blk, PM, smax, state, slot_cnt, pre_all,
+                         pre_ge, pre_eq, sp_idx, sp_val, nullptr, drop_idx, drop_val, err, stream));
   return SPARDL_OK;
 }
 

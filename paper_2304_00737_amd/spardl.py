@@ -40,6 +40,7 @@ _lib.spardl_workspace_init.restype = ctypes.c_int
 _lib.spardl_residual_add.argtypes = [_p, _i64, _p, _i64, _i32, _i64, _i32, _i32, _p, _sz, _p]
 _lib.spardl_block_topk.argtypes = [_p, _i64, _i32, _i64, _i32, _i32, _i32, _p, _p, _p, _p, _sz, _p]
 _lib.spardl_sparse_merge_topk.argtypes = [_p, _p, _i32, _i64, _i32, _i32, _p, _p, _p, _p, _sz, _p]
+_lib.spardl_sparse_merge_topk_noalloc.argtypes = [_p, _p, _i32, _i64, _i32, _i32, _p, _p, _p, _p, _p]
 _lib.spardl_allgather_densify.argtypes = [_p, _p, _i32, _i64, _i32, _p, _p, _p]
 _lib.spardl_residual_collect.argtypes = [_p, _i64, _i32, _i64, _i32, _p, _p, _p, _p, _p, _p, _p, _sz, _p]
 _lib.spardl_lazy_topk.argtypes = [_p, _i64, _i32, _i32, _i64, _i32, _i32, _i32, _i32, _p, _p, _p, _sz, _p]
@@ -61,7 +62,7 @@ _lib.spardl_bsag_workspace_bytes.restype = _sz
 _lib.spardl_bsag_workspace_init.argtypes = [_i32, _i32, _i64, _i32, _p, _sz, _p]
 _lib.spardl_bsag_exchange.argtypes = [_p, _p, _i32, _i32, _i64, _i32, _p, _p, _p, _p, _p, _sz, _p]
 _lib.spardl_bsag_residual.argtypes = [_p, _i64, _i32, _i32, _i64, _i32, _p, _p, _p, _p, _p]
-for _f in ("residual_add", "block_topk", "sparse_merge_topk", "allgather_densify", "residual_collect",
+for _f in ("residual_add", "block_topk", "sparse_merge_topk", "sparse_merge_topk_noalloc", "allgather_densify", "residual_collect",
            "lazy_topk", "lazy_receive", "lazy_residual_collect", "rsag_workspace_init", "rsag_merge_topk",
            "rsag_residual", "bsag_workspace_init", "bsag_exchange", "bsag_residual", "team_workspace_init",
            "team_residual_add", "team_block_topk", "team_merge_topk"):
@@ -151,6 +152,18 @@ def sparse_merge_topk(sp_idx, sp_val, P: int, n: int, k_blk: int, round: int, dr
     _check("sparse_merge_topk", _lib.spardl_sparse_merge_topk(
         _ptr(sp_idx), _ptr(sp_val), P, n, k_blk, round, _ptr(drop_idx), _ptr(drop_val), _ptr(drop_cnt),
         _ptr(ws), ws.numel() * ws.element_size(), _stream(stream)))
+
+
+NOALLOC_SCRATCH_BYTES = 64 << 20
+
+
+def sparse_merge_topk_noalloc(sp_idx, sp_val, P: int, n: int, k_blk: int, round: int, drop_idx, drop_val,
+                              drop_cnt, err, *, stream=None) -> None:
+    """The SRS step without a workspace (the library's static scratch); err: a
+    4-byte device tensor the call clears and its kernels OR error bits into."""
+    _check("sparse_merge_topk_noalloc", _lib.spardl_sparse_merge_topk_noalloc(
+        _ptr(sp_idx), _ptr(sp_val), P, n, k_blk, round, _ptr(drop_idx), _ptr(drop_val), _ptr(drop_cnt), _ptr(err),
+        _stream(stream)))
 
 
 def member_words(n: int) -> int:

@@ -233,6 +233,17 @@ def test_argument_errors_enqueue_nothing():
                                       null) == EINVAL
     assert lib.spardl_team_residual_add(p, i64(1199), p, i64(1200), i32(12), i32(4), i64(1200), i32(5), p, big,
                                         null) == EINVAL
+    # the workspace-free SRS step: NULL err, P < 2, round out of range; a step whose scratch exceeds the
+    # library's static array is refused before any GPU call (P = 32, k_blk = 46875: 512 pairs of 23 slots)
+    na = lambda P_, n_, kb_, rnd, err: lib.spardl_sparse_merge_topk_noalloc(p, p, i32(P_), i64(n_), i32(kb_), i32(rnd),
+                                                                           p, p, p, err, null)
+    assert na(8, 800, 5, 1, null) == EINVAL
+    assert na(1, 800, 5, 1, p) == EINVAL
+    assert na(8, 800, 5, 0, p) == EINVAL
+    assert na(8, 800, 5, 4, p) == EINVAL
+    assert na(8, 800, 101, 1, p) == EINVAL
+    assert na(32, 1_500_000_000, 46875, 1, p) == ECAP
+    assert na(16, 110_000_000, 68750, 1, p) == ECAP
     for s in (0, -1, -2, -3, 7):
         assert lib.spardl_strerror(s)
 
