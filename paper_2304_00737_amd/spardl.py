@@ -302,6 +302,58 @@ def bsag_residual(acc, P: int, d: int, n: int, k_blk: int, member, drop_idx, dro
                                                       _stream(stream)))
 
 
+def ws_layout(P: int, n: int, kb: int, ws_bytes: int) -> dict:
+    """Byte offsets of the arrays in a workspace of spardl_workspace_bytes(...,
+    P, n, kb) (host bookkeeping mirroring csrc/api.hip's layout, for reading
+    per-block statistics; tests/test_abi_cpu.py keeps the two in step)."""
+    al = lambda x: (x + 255) & ~255
+    l = 0
+    while (1 << l) < P:
+        l += 1
+    bags = [P - (1 << (l - 1)) if i == 1 else (1 << (l - i)) for i in range(1, l + 1)]
+    mmax = max(bags) if bags else 0
+    maxlen = -(-n // P)
+    pairs_max = P * mmax
+    units = max(P * P, pairs_max)
+    tiles_tk = -(-(maxlen + 31) // 4096)     # slots and add tiles start at a block's 32-aligned origin
+    tiles_mg = -(-2 * kb // 4096)
+    add_tiles = -(-(maxlen + 31) // 2048)
+    slot_n = max(P * P * tiles_tk, pairs_max * tiles_mg)
+    L, off = {"add_tiles": add_tiles}, 256
+    L["bitmap"] = off; off += al(-(-n // 32) * 4)
+    L["hist1"] = off; off += al(units * 4 * 4096 * 4)     # 4 level-1 histogram copies per unit
+    L["spec_t1"] = off; off += al(P * P * 4)
+    L["spec_used"] = off; off += al(P * P * 4)
+    L["spec_cnt"] = off; off += al(P * P * add_tiles * 4)
+    L["state"] = off; off += al(units * 16 * 4)
+    for k in ("slot_cnt", "slot_nbin", "pre_all", "pre_ge", "pre_eq"):
+        L[k] = off; off += al(slot_n * 4)
+    L["fixed_end"] = off
+    L["cand_entries"] = max(P * n, pairs_max * tiles_mg * 4096)
+    q = ((ws_bytes - off) // 3) & ~255
+    L["cand_idx"], L["cand_val"], L["bin_key"] = off, off + q, off + 2 * q
+    return L
+
+
+def topk_stats(ws, rows: int, P: int, n: int, kb: int) -> dict:
+    """After spardl_residual_add (fused) and spardl_block_topk on `rows` rows:
+    per (row, block), the speculative candidates the add wrote and whether the
+    selection used them instead of reading the block again (reads the
+    workspace; synchronises the current stream)."""
+    L = ws_layout(P, n, kb, ws.numel())
+    G = L["add_tiles"]
+    cnt = ws[L["spec_cnt"]:L["spec_cnt"] + rows * P * G * 4].view(torch.int32).cpu().view(rows * P, G)
+    state = ws[L["state"]:L["state"] + rows * P * 16 * 4].view(torch.int32).cpu().view(rows * P, 16)
+    cands, used = [], []
+    for u in range(rows * P):
+        b = u % P
+        s, e = (b * n) // P, ((b + 1) * n) // P
+        tiles = -(-(e - s + (s & 31)) // 2048)   # the block's tiles (the rest of the row's slots are unused)
+        cands.append(int(cnt[u, :tiles].clamp(min=0).sum()))
+        used.append(bool(state[u, 7]))
+    return {"candidates": cands, "spec_ok": used}
+
+
 def ws_error(ws) -> int:
     """Error word at the start of a workspace (synchronises the current stream)."""
     return int(ws[:4].view(torch.int32).cpu().item())

@@ -92,35 +92,10 @@ def compare_step(st, res, P: int, n: int, kb: int, blocks=None, acc_host=None) -
 
 
 def ws_layout(P: int, n: int, kb: int, ws_bytes: int) -> dict:
-    """Byte offsets of the workspace arrays, mirroring the library's layout
-    (kept in step with it by tests/test_abi_cpu.py::test_ws_layout_mirror)."""
-    al = lambda x: (x + 255) & ~255
-    l = 0
-    while (1 << l) < P:
-        l += 1
-    bags = [P - (1 << (l - 1)) if i == 1 else (1 << (l - i)) for i in range(1, l + 1)]
-    mmax = max(bags) if bags else 0
-    maxlen = -(-n // P)
-    pairs_max = P * mmax
-    units = max(P * P, pairs_max)
-    tiles_tk = -(-(maxlen + 31) // 4096)     # slots and add tiles start at a block's 32-aligned origin
-    tiles_mg = -(-2 * kb // 4096)
-    add_tiles = -(-(maxlen + 31) // 2048)
-    slot_n = max(P * P * tiles_tk, pairs_max * tiles_mg)
-    L, off = {}, 256
-    L["bitmap"] = off; off += al(-(-n // 32) * 4)
-    L["hist1"] = off; off += al(units * 4 * 4096 * 4)     # 4 level-1 histogram copies per unit
-    L["spec_t1"] = off; off += al(P * P * 4)
-    L["spec_used"] = off; off += al(P * P * 4)
-    L["spec_cnt"] = off; off += al(P * P * add_tiles * 4)
-    L["state"] = off; off += al(units * 16 * 4)
-    for k in ("slot_cnt", "slot_nbin", "pre_all", "pre_ge", "pre_eq"):
-        L[k] = off; off += al(slot_n * 4)
-    L["fixed_end"] = off
-    L["cand_entries"] = max(P * n, pairs_max * tiles_mg * 4096)
-    q = ((ws_bytes - off) // 3) & ~255
-    L["cand_idx"], L["cand_val"], L["bin_key"] = off, off + q, off + 2 * q
-    return L
+    """The binding's mirror of the workspace layout (imported on use: the
+    binding needs the built library)."""
+    from paper_2304_00737_amd.spardl import ws_layout as _ws_layout
+    return _ws_layout(P, n, kb, ws_bytes)
 
 
 def ws_spec_ok(st) -> list:

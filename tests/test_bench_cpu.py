@@ -44,7 +44,11 @@ def test_more_than_one_gpu_is_refused():
 
 
 def test_cpu_baseline_reports_its_sample():
+    """The oracle on every block index over a pool of fresh processes, with the
+    host's core count and CPU model and the single-thread figure beside it."""
     from paper_2304_00737_amd import workloads as W
-    out = bench.cpu_baseline(W.config(1), max_seconds=0.5)
-    assert out["kind"] == "oracle" and out["unit"] == "elements/s" and out["cores"] == 1
-    assert out["value"] > 0 and "block index, step" in out["sample"]
+    out = bench.cpu_baseline(W.config(1))
+    assert out["kind"] == "oracle" and out["unit"] == "elements/s"
+    assert out["cores"] == min(os.cpu_count(), bench.CPU_SHARE, 4) and out["nproc"] == os.cpu_count()
+    assert out["value"] > 0 and out["single_thread_value"] > 0 and out["cpu_model"]
+    assert "block indices" in out["sample"] and "single-thread" in out["sample"]
