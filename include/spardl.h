@@ -15,7 +15,12 @@
  * elements).  "Top-k" always means: larger |v| first, where |v| is compared
  * as the fp32 bit pattern with the sign bit cleared; equal |v| -> lower index
  * first.  All value arithmetic is IEEE fp32 round-to-nearest-even addition;
- * results are deterministic (bit-identical run to run).
+ * results are deterministic (bit-identical run to run).  Non-finite values are
+ * allowed: +-Inf ranks above every finite |v| and NaN above +-Inf (by its
+ * bits), -0 ties with +0, subnormals are kept (no flush to zero), and sums
+ * overflow to +-Inf.  A NaN that an addition creates or propagates has the
+ * sign and payload the hardware gives it (IEEE 754 leaves them open), so
+ * another implementation may hold different NaN bits at the same positions.
  *
  * Sparse state layout used by the SRS calls: sp_idx/sp_val[w][b][k_blk] for
  * worker w and block b (row-major, P * P * k_blk entries each).

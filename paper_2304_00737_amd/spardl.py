@@ -359,7 +359,27 @@ def ws_error(ws) -> int:
     return int(ws[:4].view(torch.int32).cpu().item())
 
 
-class SparDLStep:
+class _Checkpoint:
+    """What a later step needs from the earlier ones (Algorithm 1's input
+    residual xi^{t-1}; for B-SAG also Algorithm 2's per-block h, step, flag
+    and N, which live in its workspace), copied to host memory and back.
+    Everything else a step object holds is recomputed by the next step; a
+    fresh object's speculation hints are empty, which only makes its first
+    top-k read the blocks once more."""
+
+    def state_dict(self) -> dict:
+        d = {"acc": self.acc.cpu()}
+        if getattr(self, "bruck", False):
+            d["bsag_ws"] = self.ws_sag.cpu()
+        return d
+
+    def load_state_dict(self, d: dict) -> None:
+        self.acc.copy_(d["acc"])
+        if getattr(self, "bruck", False):
+            self.ws_sag.copy_(d["bsag_ws"])
+
+
+class SparDLStep(_Checkpoint):
     """Buffers for P simulated workers and one synchronisation step through the C ABI.
 
     acc[P, n] holds the residual between steps.  After step(grad): dense holds
@@ -446,7 +466,7 @@ class SparDLStep:
         self.finish(stream)
 
 
-class SparDLLazyStep:
+class SparDLLazyStep(_Checkpoint):
     """Buffers for P simulated workers and one lazy-sparsification step
     (Sec. III-B "Optimization for SRS", Algorithm 1) through the C ABI.
 
@@ -517,7 +537,7 @@ class SparDLLazyStep:
         self.finish(stream)
 
 
-class SparDLSagStep:
+class SparDLSagStep(_Checkpoint):
     """P simulated workers in d teams of Q = P / d joined by R-SAG (Sec. III-D,
     d a power of 2) or, with bruck=True, by B-SAG (any d dividing P, top-h
     counts from Algorithm 2), one synchronisation step through the C ABI.
