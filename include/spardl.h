@@ -117,11 +117,17 @@ int spardl_workspace_init(int32_t nworkers, int32_t P, int64_t n, int32_t k_blk,
  * entries at or above a floor just below the block's previous threshold, so
  * that the top-k need not read acc again when the floor held.  P = 0 (k_blk
  * and ws ignored) is a plain add.
+ * w0: the worker that row 0 of acc and grad belongs to, when a call covers
+ * workers w0 .. w0 + nworkers - 1 of the P (a workspace for fewer rows than
+ * P, the workers taken a few at a time): the floor of each block comes from
+ * that worker's own previous threshold, kept in ws per worker and block.
+ * 0 when the call covers all workers; ignored for the plain add.
  * Errors: EINVAL for NULL acc/grad, nworkers < 1, n < 1 or n >= 2^31,
- * ld < n, P < 0, P > n, and with ws: nworkers > P, misaligned ws or k_blk
- * out of [1, floor(n / P)]; ECAPACITY if ws is smaller than
- * spardl_workspace_bytes(nworkers, P, n, k_blk). */
-int spardl_residual_add(float* acc, int64_t ld_acc, const float* grad, int64_t ld_grad,
+ * ld < n, P < 0, P > n, w0 < 0, and with ws: nworkers > P,
+ * w0 + nworkers > P, misaligned ws or k_blk out of [1, floor(n / P)];
+ * ECAPACITY if ws is smaller than spardl_workspace_bytes(nworkers, P, n,
+ * k_blk). */
+int spardl_residual_add(float* acc, int64_t ld_acc, const float* grad, int64_t ld_grad, int32_t w0,
                         int32_t nworkers, int64_t n, int32_t P, int32_t k_blk, void* ws, size_t ws_bytes,
                         hipStream_t stream);
 
@@ -131,10 +137,13 @@ int spardl_residual_add(float* acc, int64_t ld_acc, const float* grad, int64_t l
  *   block b of row w of acc, sorted by ascending index.
  * local_idx (optional, may be NULL) receives a second copy of the indices;
  * spardl_residual_collect needs it after the SRS steps have overwritten sp.
- * flags: 0 or SPARDL_TOPK_HIST_READY.
- * Errors: EINVAL for NULL acc/sp/ws, nworkers < 1, P < 1, n < P, n >= 2^31,
- * ld_acc < n, k_blk < 1 or k_blk > floor(n / P); ECAPACITY if ws is small. */
-int spardl_block_topk(const float* acc, int64_t ld_acc, int32_t nworkers, int64_t n, int32_t P,
+ * flags: 0 or SPARDL_TOPK_HIST_READY.  w0: as for spardl_residual_add (the
+ * worker of row 0; the call records each block's threshold for that
+ * worker's next residual add).
+ * Errors: EINVAL for NULL acc/sp/ws, nworkers < 1, w0 < 0,
+ * w0 + nworkers > P, P < 1, n < P, n >= 2^31, ld_acc < n, k_blk < 1 or
+ * k_blk > floor(n / P); ECAPACITY if ws is small. */
+int spardl_block_topk(const float* acc, int64_t ld_acc, int32_t w0, int32_t nworkers, int64_t n, int32_t P,
                       int32_t k_blk, int32_t flags, int32_t* sp_idx, float* sp_val,
                       int32_t* local_idx, void* ws, size_t ws_bytes, hipStream_t stream);
 

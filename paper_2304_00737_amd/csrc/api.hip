@@ -250,7 +250,7 @@ struct Fill {
 // kept for the all-blocks map (the fused add of the next step reads it).
 int topk_units(const float* acc, int64_t ld_acc, int64_t units, const Units& U, int64_t n, int32_t P, int32_t k_blk,
                bool make_hist, bool spec, int32_t* sp_idx, float* sp_val, int32_t* local_idx, const Ws& w,
-               const Layout& L, hipStream_t stream) {
+               const Layout& L, hipStream_t stream, int64_t hint_off = 0) {
   const bool v4 = aligned16(acc) && ld_acc % 4 == 0 && blocks_vec4(n, P);
   const int32_t smax = (int32_t)L.tiles_tk;
   if (make_hist) {
@@ -258,8 +258,9 @@ int topk_units(const float* acc, int64_t ld_acc, int64_t units, const Units& U, 
     SPARDL_TRY(launch_hist1(acc, ld_acc, units, U, n, P, v4, w.hist1, stream));
   }
   // the previous-threshold hint feeds the next fused add: kept unless this is a
-  // lazy selection that did not start from a fused add
-  uint32_t* hint = (U.rel && !spec) ? nullptr : w.spec_t1;
+  // lazy selection that did not start from a fused add; hint_off: the words of
+  // the workers before the call's rows (hints are kept per absolute worker)
+  uint32_t* hint = (U.rel && !spec) ? nullptr : w.spec_t1 + hint_off;
   SPARDL_TRY(launch_select1(w.hist1, w.state, units, U, n, P, (uint32_t)k_blk, hint, w.spec_used, spec, acc, ld_acc,
                             v4, w.err, stream));
   SPARDL_TRY(launch_collect(acc, ld_acc, units, U, n, P, k_blk, v4, smax, w.state, w.spec_cnt, (int32_t)L.add_tiles,
@@ -400,18 +401,18 @@ int spardl_workspace_init(int32_t nworkers, int32_t P, int64_t n, int32_t k_blk,
   return SPARDL_OK;
 }
 
-int spardl_residual_add(float* acc, int64_t ld_acc, const float* grad, int64_t ld_grad,
+int spardl_residual_add(float* acc, int64_t ld_acc, const float* grad, int64_t ld_grad, int32_t w0,
                         int32_t nworkers, int64_t n, int32_t P, int32_t k_blk, void* ws, size_t ws_bytes,
                         hipStream_t stream) {
   if (!acc || !grad || nworkers < 1 || n < 1 || n > kMaxN || ld_acc < n || ld_grad < n || P < 0 ||
-      P > n)
+      P > n || w0 < 0)
     return SPARDL_EINVAL;
   if (P == 0 || ws == nullptr) {
     const bool v4 = aligned16(acc) && aligned16(grad) && ld_acc % 4 == 0 && ld_grad % 4 == 0 && n % 4 == 0;
     SPARDL_TRY(launch_residual_add(acc, ld_acc, grad, ld_grad, nworkers, n, 1, v4, AddSpec{}, stream));
     return SPARDL_OK;
   }
-  if (nworkers > P || ws_misaligned(ws) || !sizes_ok(P, n, k_blk)) return SPARDL_EINVAL;
+  if (nworkers > P || w0 > P - nworkers || ws_misaligned(ws) || !sizes_ok(P, n, k_blk)) return SPARDL_EINVAL;
   const size_t need = spardl_workspace_bytes(nworkers, P, n, k_blk);
   if (need == 0) return SPARDL_EINVAL;
   if (ws_bytes < need) return SPARDL_ECAPACITY;
@@ -420,7 +421,7 @@ int spardl_residual_add(float* acc, int64_t ld_acc, const float* grad, int64_t l
   const bool v4 = aligned16(acc) && aligned16(grad) && ld_acc % 4 == 0 && ld_grad % 4 == 0 && blocks_vec4(n, P);
   AddSpec sp;
   sp.hist1 = w.hist1;
-  sp.spec_t1 = w.spec_t1;
+  sp.spec_t1 = w.spec_t1 + (int64_t)w0 * P;   // the hints of workers w0 .. w0 + nworkers - 1
   sp.spec_used = w.spec_used;
   sp.spec_cnt = w.spec_cnt;
   sp.cand_idx = w.cand_idx;
@@ -429,11 +430,11 @@ int spardl_residual_add(float* acc, int64_t ld_acc, const float* grad, int64_t l
   return SPARDL_OK;
 }
 
-int spardl_block_topk(const float* acc, int64_t ld_acc, int32_t nworkers, int64_t n, int32_t P,
+int spardl_block_topk(const float* acc, int64_t ld_acc, int32_t w0, int32_t nworkers, int64_t n, int32_t P,
                       int32_t k_blk, int32_t flags, int32_t* sp_idx, float* sp_val, int32_t* local_idx,
                       void* ws, size_t ws_bytes, hipStream_t stream) {
-  if (!acc || !sp_idx || !sp_val || !ws || nworkers < 1 || nworkers > P || !sizes_ok(P, n, k_blk) ||
-      ld_acc < n || (flags & ~SPARDL_TOPK_HIST_READY) || ws_misaligned(ws))
+  if (!acc || !sp_idx || !sp_val || !ws || nworkers < 1 || nworkers > P || w0 < 0 || w0 > P - nworkers ||
+      !sizes_ok(P, n, k_blk) || ld_acc < n || (flags & ~SPARDL_TOPK_HIST_READY) || ws_misaligned(ws))
     return SPARDL_EINVAL;
   const size_t need = spardl_workspace_bytes(nworkers, P, n, k_blk);
   if (need == 0) return SPARDL_EINVAL;
@@ -442,7 +443,7 @@ int spardl_block_topk(const float* acc, int64_t ld_acc, int32_t nworkers, int64_
   Ws w = carve(ws, ws_bytes, L);
   const bool spec = (flags & SPARDL_TOPK_HIST_READY) != 0;   // candidates of the fused add may be used
   return topk_units(acc, ld_acc, (int64_t)nworkers * P, all_blocks(P), n, P, k_blk, !spec, spec, sp_idx, sp_val,
-                    local_idx, w, L, stream);
+                    local_idx, w, L, stream, (int64_t)w0 * P);
 }
 
 int spardl_sparse_merge_topk(int32_t* sp_idx, float* sp_val, int32_t P, int64_t n, int32_t k_blk,

@@ -37,8 +37,8 @@ _lib.spardl_workspace_bytes.argtypes = [_i32, _i32, _i64, _i32]
 _lib.spardl_workspace_bytes.restype = _sz
 _lib.spardl_workspace_init.argtypes = [_i32, _i32, _i64, _i32, _p, _sz, _p]
 _lib.spardl_workspace_init.restype = ctypes.c_int
-_lib.spardl_residual_add.argtypes = [_p, _i64, _p, _i64, _i32, _i64, _i32, _i32, _p, _sz, _p]
-_lib.spardl_block_topk.argtypes = [_p, _i64, _i32, _i64, _i32, _i32, _i32, _p, _p, _p, _p, _sz, _p]
+_lib.spardl_residual_add.argtypes = [_p, _i64, _p, _i64, _i32, _i32, _i64, _i32, _i32, _p, _sz, _p]
+_lib.spardl_block_topk.argtypes = [_p, _i64, _i32, _i32, _i64, _i32, _i32, _i32, _p, _p, _p, _p, _sz, _p]
 _lib.spardl_sparse_merge_topk.argtypes = [_p, _p, _i32, _i64, _i32, _i32, _p, _p, _p, _p, _sz, _p]
 _lib.spardl_sparse_merge_topk_noalloc.argtypes = [_p, _p, _i32, _i64, _i32, _i32, _p, _p, _p, _p, _p]
 _lib.spardl_allgather_densify.argtypes = [_p, _p, _i32, _i64, _i32, _p, _p, _p]
@@ -130,19 +130,21 @@ def workspace(nworkers: int, P: int, n: int, k_blk: int, device="cuda", *, strea
     return ws
 
 
-def residual_add(acc, grad, nworkers: int, n: int, P: int = 0, ws=None, k_blk: int = 0, *, ld_acc=None,
-                 ld_grad=None, stream=None) -> None:
+def residual_add(acc, grad, nworkers: int, n: int, P: int = 0, ws=None, k_blk: int = 0, *, w0: int = 0,
+                 ld_acc=None, ld_grad=None, stream=None) -> None:
+    """w0: the worker of row 0 when the call covers workers w0 .. w0 + nworkers - 1."""
     ld_acc = _ld(acc, n) if ld_acc is None else ld_acc
     ld_grad = _ld(grad, n) if ld_grad is None else ld_grad
     ws_bytes = ws.numel() * ws.element_size() if ws is not None else 0
-    _check("residual_add", _lib.spardl_residual_add(_ptr(acc), ld_acc, _ptr(grad), ld_grad, nworkers, n, P,
+    _check("residual_add", _lib.spardl_residual_add(_ptr(acc), ld_acc, _ptr(grad), ld_grad, w0, nworkers, n, P,
                                                     k_blk, _ptr(ws), ws_bytes, _stream(stream)))
 
 
 def block_topk(acc, nworkers: int, n: int, P: int, k_blk: int, sp_idx, sp_val, local_idx=None, ws=None,
-               flags: int = 0, *, ld_acc=None, stream=None) -> None:
+               flags: int = 0, *, w0: int = 0, ld_acc=None, stream=None) -> None:
+    """w0: the worker of row 0 when the call covers workers w0 .. w0 + nworkers - 1."""
     ld_acc = _ld(acc, n) if ld_acc is None else ld_acc
-    _check("block_topk", _lib.spardl_block_topk(_ptr(acc), ld_acc, nworkers, n, P, k_blk, flags, _ptr(sp_idx),
+    _check("block_topk", _lib.spardl_block_topk(_ptr(acc), ld_acc, w0, nworkers, n, P, k_blk, flags, _ptr(sp_idx),
                                                 _ptr(sp_val), _ptr(local_idx), _ptr(ws),
                                                 ws.numel() * ws.element_size(), _stream(stream)))
 
@@ -411,14 +413,14 @@ class SparDLStep(_Checkpoint):
         r = grad_rows.shape[0]
         acc = self.acc[w0:w0 + r]
         if self.fused:
-            residual_add(acc, grad_rows, r, self.n, self.P, self.ws, self.k_blk, stream=stream)
+            residual_add(acc, grad_rows, r, self.n, self.P, self.ws, self.k_blk, w0=w0, stream=stream)
         else:
             residual_add(acc, grad_rows, r, self.n, 0, None, stream=stream)
 
     def block_topk_rows(self, w0: int, r: int, stream=None):
         s = slice(w0, w0 + r)
         block_topk(self.acc[s], r, self.n, self.P, self.k_blk, self.sp_idx[s], self.sp_val[s], self.local_idx[s],
-                   self.ws, TOPK_HIST_READY if self.fused else 0, stream=stream)
+                   self.ws, TOPK_HIST_READY if self.fused else 0, w0=w0, stream=stream)
 
     def residual_add(self, grad, stream=None):
         self._all_rows()

@@ -85,25 +85,34 @@ def test_argument_errors_enqueue_nothing():
     i64, i32, sz = ctypes.c_int64, ctypes.c_int32, ctypes.c_size_t
     EINVAL, ECAP = -1, -2
     # residual_add: NULL acc, ld < n, P > n
-    assert lib.spardl_residual_add(null, i64(10), p, i64(10), i32(1), i64(10), i32(0), i32(0), null, sz(0),
+    assert lib.spardl_residual_add(null, i64(10), p, i64(10), i32(0), i32(1), i64(10), i32(0), i32(0), null, sz(0),
                                    null) == EINVAL
-    assert lib.spardl_residual_add(p, i64(9), p, i64(10), i32(1), i64(10), i32(0), i32(0), null, sz(0),
+    assert lib.spardl_residual_add(p, i64(9), p, i64(10), i32(0), i32(1), i64(10), i32(0), i32(0), null, sz(0),
                                    null) == EINVAL
-    assert lib.spardl_residual_add(p, i64(10), p, i64(10), i32(1), i64(10), i32(11), i32(1), p, sz(1 << 20),
+    assert lib.spardl_residual_add(p, i64(10), p, i64(10), i32(0), i32(1), i64(10), i32(11), i32(1), p, sz(1 << 20),
                                    null) == EINVAL
-    assert lib.spardl_residual_add(p, i64(100), p, i64(100), i32(2), i64(100), i32(4), i32(3), p, sz(16),
+    assert lib.spardl_residual_add(p, i64(100), p, i64(100), i32(0), i32(2), i64(100), i32(4), i32(3), p, sz(16),
                                    null) == ECAP
     # with ws: k_blk outside [1, n / P]
-    assert lib.spardl_residual_add(p, i64(100), p, i64(100), i32(2), i64(100), i32(4), i32(26), p, sz(1 << 30),
+    assert lib.spardl_residual_add(p, i64(100), p, i64(100), i32(0), i32(2), i64(100), i32(4), i32(26), p, sz(1 << 30),
                                    null) == EINVAL
+    # the first worker of the call's rows: negative, or rows past P
+    assert lib.spardl_residual_add(p, i64(100), p, i64(100), i32(-1), i32(1), i64(100), i32(4), i32(3), p,
+                                   sz(1 << 30), null) == EINVAL
+    assert lib.spardl_residual_add(p, i64(100), p, i64(100), i32(3), i32(2), i64(100), i32(4), i32(3), p,
+                                   sz(1 << 30), null) == EINVAL
+    assert lib.spardl_block_topk(p, i64(100), i32(3), i32(2), i64(100), i32(4), i32(3), i32(0), p, p, null, p,
+                                 sz(1 << 30), null) == EINVAL
+    assert lib.spardl_block_topk(p, i64(100), i32(-1), i32(1), i64(100), i32(4), i32(3), i32(0), p, p, null, p,
+                                 sz(1 << 30), null) == EINVAL
     # block_topk: k_blk too large, flags unknown, nworkers > P, small workspace
-    assert lib.spardl_block_topk(p, i64(100), i32(1), i64(100), i32(4), i32(26), i32(0), p, p, null, p,
+    assert lib.spardl_block_topk(p, i64(100), i32(0), i32(1), i64(100), i32(4), i32(26), i32(0), p, p, null, p,
                                  sz(1 << 30), null) == EINVAL
-    assert lib.spardl_block_topk(p, i64(100), i32(1), i64(100), i32(4), i32(3), i32(4), p, p, null, p,
+    assert lib.spardl_block_topk(p, i64(100), i32(0), i32(1), i64(100), i32(4), i32(3), i32(4), p, p, null, p,
                                  sz(1 << 30), null) == EINVAL
-    assert lib.spardl_block_topk(p, i64(100), i32(5), i64(100), i32(4), i32(3), i32(0), p, p, null, p,
+    assert lib.spardl_block_topk(p, i64(100), i32(0), i32(5), i64(100), i32(4), i32(3), i32(0), p, p, null, p,
                                  sz(1 << 30), null) == EINVAL
-    assert lib.spardl_block_topk(p, i64(100), i32(1), i64(100), i32(4), i32(3), i32(0), p, p, null, p,
+    assert lib.spardl_block_topk(p, i64(100), i32(0), i32(1), i64(100), i32(4), i32(3), i32(0), p, p, null, p,
                                  sz(64), null) == ECAP
     # workspace_init: NULL, misaligned, too small, bad sizes
     lib.spardl_workspace_init.argtypes = [i32, i32, i64, i32, ctypes.c_void_p, sz, ctypes.c_void_p]
@@ -114,7 +123,7 @@ def test_argument_errors_enqueue_nothing():
     assert lib.spardl_workspace_init(i32(5), i32(4), i64(100), i32(3), p, sz(1 << 30), null) == EINVAL
     # a workspace that is not 256-byte aligned
     q = ctypes.c_void_p(0x1010)
-    assert lib.spardl_block_topk(p, i64(100), i32(1), i64(100), i32(4), i32(3), i32(0), p, p, null, q,
+    assert lib.spardl_block_topk(p, i64(100), i32(0), i32(1), i64(100), i32(4), i32(3), i32(0), p, p, null, q,
                                  sz(1 << 30), null) == EINVAL
     assert lib.spardl_sparse_merge_topk(p, p, i32(6), i64(600), i32(3), i32(1), p, p, p, q, sz(1 << 30),
                                         null) == EINVAL

@@ -242,6 +242,31 @@ def test_step_rows_per_call(P, n, kb, rows):
         compare_step(st, res, P, n, kb)
 
 
+def test_threshold_hints_are_per_worker():
+    """Workers taken one at a time on a one-row workspace: the previous
+    threshold each fused add starts from is that worker's own, so after a
+    step the hint of (worker w, block b) is the level-1 bin of the k/P-th
+    largest |A| of worker w's block b (plus one), for every worker."""
+    from paper_2304_00737_amd.spardl import ws_layout
+    P, n, kb = 6, 60000, 40
+    st = spardl.SparDLStep(P, n, kb, rows_per_call=1)
+    acc = np.zeros((P, n), np.float32)
+    L = ws_layout(P, n, kb, st.ws.numel())
+    for t in range(3):
+        # worker w's gradient scaled by 4^w: every worker's thresholds sit in different bins
+        grad = (_rows("normal", P, n, 610 + t) * (np.float32(4.0) ** np.arange(P, dtype=np.float32))[:, None])
+        grad = grad.astype(np.float32)
+        st.step(_dev(grad))
+        check_ws(st)
+        res = so.spardl_step([acc[w] for w in range(P)], [grad[w] for w in range(P)], P, n, kb)
+        compare_step(st, res, P, n, kb)
+        hint = st.ws[L["spec_t1"]:L["spec_t1"] + P * P * 4].view(torch.int32).cpu().numpy()
+        for w in range(P):
+            for b in range(P):
+                keys = np.asarray(res.local[(w, b)][1], np.float32).view(np.uint32) & 0x7FFFFFFF
+                assert int(hint[w * P + b]) == int(keys.min() >> 19) + 1, f"hint of worker {w} block {b}"
+
+
 def test_cfg1_full():
     wl = W.config(1)
     P, n, kb = wl.P, wl.n, wl.k_blk
