@@ -291,7 +291,7 @@ size_t team_ws_bytes(int32_t P, int32_t d, int64_t n, int32_t kb) {
 // per merge pair a level-1 histogram and the selection state, per slot the
 // counts and prefixes, then the summed union (index, value).
 struct NoallocLayout {
-  size_t hist, state, slot_cnt, slot_nbin, pre_all, pre_ge, pre_eq, uidx, uval, end;
+  size_t hist, state, slot_cnt, slot_nbin, pre_all, pre_ge, pre_eq, uidx, uval, ukey, end;
 };
 
 NoallocLayout make_noalloc_layout(int64_t npairs, int32_t kb) {
@@ -312,6 +312,7 @@ NoallocLayout make_noalloc_layout(int64_t npairs, int32_t kb) {
   L.pre_eq = take(slots * 4);
   L.uidx = take(slots * MERGE_TILE * 4);
   L.uval = take(slots * MERGE_TILE * 4);
+  L.ukey = take(slots * MERGE_TILE * 4);
   L.end = off;
   return L;
 }
@@ -462,8 +463,8 @@ int spardl_sparse_merge_topk(int32_t* sp_idx, float* sp_val, int32_t P, int64_t 
   const int64_t pairs = (int64_t)P * m;
   const int32_t smax = (int32_t)L.tiles_mg;
   const Pairs PM = srs_pairs(P, m, d);
-  SPARDL_TRY(launch_merge(sp_idx, sp_val, PM, pairs, k_blk, smax, w.hist1, w.slot_cnt, w.cand_idx, w.cand_val,
-                          stream));
+  SPARDL_TRY(launch_merge(sp_idx, sp_val, PM, pairs, k_blk, smax, w.hist1, w.state, w.slot_cnt, w.cand_idx, w.cand_val,
+                          w.bin_key, stream));
   SPARDL_TRY(launch_thresh(1, pairs, all_blocks(P), n, P, k_blk, smax, w.hist1, w.cand_val, w.state, w.slot_cnt, w.slot_nbin,
                            w.bin_key, w.pre_all, w.pre_ge, w.pre_eq, drop_cnt, w.err, stream));
   SPARDL_TRY(launch_emit(1, w.cand_idx, w.cand_val, pairs, all_blocks(P), n, P, k_blk, PM, smax, w.state, w.slot_cnt, w.pre_all,
@@ -492,16 +493,15 @@ int spardl_sparse_merge_topk_noalloc(int32_t* sp_idx, float* sp_val, int32_t P, 
   uint32_t *pre_all = at(L.pre_all), *pre_ge = at(L.pre_ge), *pre_eq = at(L.pre_eq);
   int32_t* uidx = (int32_t*)(base + L.uidx);
   float* uval = (float*)(base + L.uval);
+  uint32_t* ukey = at(L.ukey);
   const int32_t smax = (int32_t)ceil_div(2ll * k_blk, MERGE_TILE);
   const Pairs PM = srs_pairs(P, m, d);
   // the scratch keeps the previous call's contents: the histograms the merge
   // accumulates into start from zero, and so does the caller's error word
   SPARDL_TRY(launch_fill(Fill().add(hist, pairs * NB1).add(err, 1).r, stream));
-  SPARDL_TRY(launch_merge(sp_idx, sp_val, PM, pairs, k_blk, smax, hist, slot_cnt, uidx, uval, stream));
-  // a merge's threshold reads keys from the union values (the bin-key array is a block top-k's)
-  SPARDL_TRY(launch_thresh(1, pairs, all_blocks(P), n, P, k_blk, smax, hist, uval, state, slot_cnt, slot_nbin,
-                           reinterpret_cast<const uint32_t*>(uval), pre_all, pre_ge, pre_eq, drop_cnt, err,
-                           stream));
+  SPARDL_TRY(launch_merge(sp_idx, sp_val, PM, pairs, k_blk, smax, hist, state, slot_cnt, uidx, uval, ukey, stream));
+  SPARDL_TRY(launch_thresh(1, pairs, all_blocks(P), n, P, k_blk, smax, hist, uval, state, slot_cnt, slot_nbin, ukey,
+                           pre_all, pre_ge, pre_eq, drop_cnt, err, stream));
   SPARDL_TRY(launch_emit(1, uidx, uval, pairs, all_blocks(P), n, P, k_blk, PM, smax, state, slot_cnt, pre_all,
                          pre_ge, pre_eq, sp_idx, sp_val, nullptr, drop_idx, drop_val, err, stream));
   return SPARDL_OK;
@@ -640,8 +640,8 @@ int spardl_rsag_merge_topk(int32_t* sp_idx, float* sp_val, int32_t P, int32_t d,
   Ws w = carve(ws, ws_bytes, L);
   const Pairs PM = rsag_pairs(Q, t);
   const int32_t smax = (int32_t)L.tiles_mg;
-  SPARDL_TRY(launch_merge(sp_idx, sp_val, PM, npairs, k_blk, smax, w.hist1, w.slot_cnt, w.cand_idx, w.cand_val,
-                          stream));
+  SPARDL_TRY(launch_merge(sp_idx, sp_val, PM, npairs, k_blk, smax, w.hist1, w.state, w.slot_cnt, w.cand_idx, w.cand_val,
+                          w.bin_key, stream));
   SPARDL_TRY(launch_thresh(1, npairs, all_blocks(Q), n, Q, k_blk, smax, w.hist1, w.cand_val, w.state,
                            w.slot_cnt, w.slot_nbin, w.bin_key, w.pre_all, w.pre_ge, w.pre_eq, drop_cnt, w.err,
                            stream));
@@ -817,8 +817,8 @@ int spardl_team_merge_topk(int32_t* sp_idx, float* sp_val, int32_t P, int32_t d,
   const int64_t pairs = (int64_t)P * m;
   const int32_t smax = (int32_t)L.tiles_mg;
   const Pairs PM = team_srs_pairs(Q, m, dist);
-  SPARDL_TRY(launch_merge(sp_idx, sp_val, PM, pairs, k_blk, smax, w.hist1, w.slot_cnt, w.cand_idx, w.cand_val,
-                          stream));
+  SPARDL_TRY(launch_merge(sp_idx, sp_val, PM, pairs, k_blk, smax, w.hist1, w.state, w.slot_cnt, w.cand_idx, w.cand_val,
+                          w.bin_key, stream));
   SPARDL_TRY(launch_thresh(1, pairs, all_blocks(Q), n, Q, k_blk, smax, w.hist1, w.cand_val, w.state, w.slot_cnt,
                            w.slot_nbin, w.bin_key, w.pre_all, w.pre_ge, w.pre_eq, drop_cnt, w.err, stream));
   SPARDL_TRY(launch_emit(1, w.cand_idx, w.cand_val, pairs, all_blocks(Q), n, Q, k_blk, PM, smax, w.state,

@@ -31,6 +31,22 @@ constexpr int MERGE_TILE = MERGE_THREADS * MERGE_PER_THREAD;   // merged positio
 constexpr int DENSE_TILE = 16384;
 constexpr int HCOPIES = 4;                       // level-1 histogram copies per block (spreads the flush atomics)
 
+// ---------------------------------------------------------------- merge threshold
+// A merge's union (two index-sorted top-k blocks, summed on shared indices)
+// keeps half its entries, whose keys crowd just above the blocks' own
+// thresholds: a level-1 bin of 2^D1_SHIFT keys (1/16 binade) can hold half
+// the union.  Unions of up to MT_SLOTS slots therefore take a finer level 1:
+// NB1 bins of 2^FINE_SHIFT keys (1/256 binade), a window starting FINE_BELOW
+// bins (4 binades) below the larger of the two blocks' smallest sampled keys;
+// keys outside the window are counted in its first or last bin.  If the
+// threshold falls in one of those two bins the threshold kernel builds the
+// 2^D1_SHIFT-key histogram itself (exact either way).
+constexpr int MT_SLOTS = 1024;                   // merge slots per unit of the one-workgroup merge threshold
+constexpr int FINE_SHIFT = 15;
+constexpr uint32_t FINE_BELOW = 1024;
+constexpr int FINE_SAMPLE = 256;                 // leading entries of each block sampled for the window
+__host__ __device__ __forceinline__ bool merge_fine(int64_t kb) { return 2 * kb <= (int64_t)MT_SLOTS * MERGE_TILE; }
+
 // ---------------------------------------------------------------- state words
 // Per selection unit (a (worker, block) pair or a merge pair), 16 u32:
 enum : int {
@@ -46,6 +62,7 @@ enum : int {
   ST_PRE23 = 9,     // ... top 23 key bits fixed by level 2
   ST_NEED2 = 10,    // ... entries still needed from that level-2 bin
   ST_STAGE = 11,    // ... 2 while level 3 is still needed, else 0
+  ST_WBASE = 12,    // merge: first fine key bin (key >> FINE_SHIFT) of the union's level-1 histogram window
   ST_WORDS = 16
 };
 

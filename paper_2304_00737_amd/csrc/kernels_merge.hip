@@ -18,15 +18,59 @@ namespace spardl {
 // leaves a hole.  Tile = MERGE_TILE merged positions; its hole-free part is
 // written densely into the tile's slot, and the level-1 histogram of the
 // union is accumulated for the selection.
+//
+// The tile's two merge-path splits (held entries before its first and past
+// its last position) are bracketed by one wave each, MERGE_PROBES-ary
+// searches over global memory (two rounds for blocks of up to about 260 Ki
+// entries; a probe per lane, no barrier), and resolved exactly in LDS after
+// the tile's entries and the brackets' slack have been loaded there in one
+// round of coalesced loads.  Meanwhile the other waves read the leading
+// FINE_SAMPLE entries of both blocks, whose smallest keys place the fine
+// level-1 window (FINE; see merge_fine in common.hpp); every tile of a pair
+// reads the same entries, so all of them use the same window.
+constexpr int MERGE_PROBES = WAVE;                 // probes per search round (a lane each)
+constexpr int MERGE_BRK = 32;                      // bracket width resolved in LDS
+constexpr int MERGE_WIN = MERGE_TILE + 4 * MERGE_BRK + 8;   // LDS entries: the tile, the slack and sentinels
+static_assert(2 * MERGE_BRK <= MERGE_THREADS, "both brackets are tested in one pass");
+static_assert(MERGE_THREADS / WAVE >= 4 && FINE_SAMPLE % WAVE == 0, "two searching and two sampling waves");
+
+// The bracket [lo, hi] of a monotone partition point (pred true below it),
+// narrowed by one wave until at most MERGE_BRK wide.
+template <typename Pred>
+__device__ __forceinline__ void wave_bracket(int32_t& lo, int32_t& hi, Pred pred) {
+  const int lane = lane_id();
+  while (hi - lo > MERGE_BRK) {   // uniform over the wave
+    const int32_t S = hi - lo;
+    const int32_t p = lo + (int32_t)(((int64_t)S * (lane + 1)) / (MERGE_PROBES + 1));
+    const int32_t c = (int32_t)popc64(__ballot(pred(p)));
+    const int32_t nlo = c == 0 ? lo : lo + (int32_t)(((int64_t)S * c) / (MERGE_PROBES + 1)) + 1;
+    const int32_t nhi = c == MERGE_PROBES ? hi : lo + (int32_t)(((int64_t)S * (c + 1)) / (MERGE_PROBES + 1));
+    lo = nlo;
+    hi = nhi;
+  }
+}
+
+// Level-1 bin of a union key: FINE, NB1 bins of 2^FINE_SHIFT keys from
+// `base` (clamped to the first and last); else the top 12 key bits.
+template <bool FINE>
+__device__ __forceinline__ uint32_t merge_bin(uint32_t key, uint32_t base) {
+  if (!FINE) return key >> D1_SHIFT;
+  const int32_t b = (int32_t)(key >> FINE_SHIFT) - (int32_t)base;
+  return (uint32_t)min(max(b, 0), NB1 - 1);
+}
+
+template <bool FINE>
 __global__ __launch_bounds__(MERGE_THREADS) void k_merge(
     const int32_t* __restrict__ sp_idx, const float* __restrict__ sp_val, Pairs PM, int32_t kb,
-    int32_t tiles_per_pair, uint32_t* __restrict__ hist1,
-    uint32_t* __restrict__ slot_cnt, int32_t* __restrict__ U_idx, float* __restrict__ U_val) {
-  // held entries a0-1 .. a1 at [0, nh + 2), received b0 .. b1 at [nh + 2, nh + nr + 3)
-  __shared__ int32_t cI[MERGE_TILE + 3];
-  __shared__ float cV[MERGE_TILE + 3];
+    int32_t tiles_per_pair, uint32_t* __restrict__ hist1, uint32_t* __restrict__ state,
+    uint32_t* __restrict__ slot_cnt, int32_t* __restrict__ U_idx, float* __restrict__ U_val,
+    uint32_t* __restrict__ U_key) {
+  __shared__ int32_t cI[MERGE_WIN];
+  __shared__ float cV[MERGE_WIN];
   __shared__ __align__(16) uint32_t hist[NB1];
   __shared__ uint32_t scratch[2 * (MERGE_THREADS / WAVE) + 1];
+  __shared__ int32_t brk[4];
+  __shared__ uint32_t smin[2];
   const uint32_t pair = blockIdx.x / (uint32_t)tiles_per_pair;
   const int32_t tile = (int32_t)(blockIdx.x % (uint32_t)tiles_per_pair);
   int64_t hb, rb;
@@ -42,49 +86,100 @@ __global__ __launch_bounds__(MERGE_THREADS) void k_merge(
   const int32_t Q1 = min(Q0 + MERGE_TILE, L2);
   // split(q) = number of held entries among the first q merged positions:
   // the first a in [max(0, q-kb), min(q, kb)) whose held entry does not go
-  // before received entry q-a-1 (held goes first on equal indices).  The
-  // tile's two splits are searched together.
-  int32_t a0, a1;
-  wg_partition_point2(max(0, Q0 - kb), min(Q0, kb), [&](int32_t a) { return Hi[a] <= Ri[Q0 - a - 1]; },
-                      max(0, Q1 - kb), min(Q1, kb), [&](int32_t a) { return Hi[a] <= Ri[Q1 - a - 1]; }, scratch,
-                      &a0, &a1);
-  const int32_t b0 = Q0 - a0, b1 = Q1 - a1;
-  const int32_t nh = a1 - a0, nr = b1 - b0;
-  int32_t* hI = cI;
-  float* hV = cV;
-  int32_t* rI = cI + nh + 2;
-  float* rV = cV + nh + 2;
+  // before received entry q-a-1 (held goes first on equal indices).
+  const int wv = wave_id(), lane = lane_id();
+  if (wv < 2) {
+    const int32_t q = wv == 0 ? Q0 : Q1;
+    int32_t lo = max(0, q - kb), hi = min(q, kb);
+    wave_bracket(lo, hi, [&](int32_t a) { return Hi[a] <= Ri[q - a - 1]; });
+    if (lane == 0) {
+      brk[2 * wv] = lo;
+      brk[2 * wv + 1] = hi;
+    }
+  } else if (FINE) {
+    // smallest key among the leading entries of the held (wave 2) or received (wave 3) block
+    const float* __restrict__ V = wv == 2 ? Hv : Rv;
+    float v[FINE_SAMPLE / WAVE];
+#pragma unroll
+    for (int u = 0; u < FINE_SAMPLE / WAVE; ++u) {
+      const int32_t j = u * WAVE + lane;
+      v[u] = j < kb ? V[j] : __uint_as_float(0x7F7FFFFFu);
+    }
+    uint32_t m = 0x7FFFFFFFu;
+#pragma unroll
+    for (int u = 0; u < FINE_SAMPLE / WAVE; ++u) m = min(m, mag_key(v[u]));
+#pragma unroll
+    for (int d = WAVE / 2; d > 0; d >>= 1) m = min(m, (uint32_t)__shfl_xor((int)m, d, WAVE));
+    if (lane == 0 && wv < 4) smin[wv - 2] = m;
+  }
+  __syncthreads();
+  const int32_t lo0 = brk[0], hi0 = brk[1], lo1 = brk[2], hi1 = brk[3];
+  uint32_t wbase = 0;
+  if (FINE) {
+    const uint32_t top = max(smin[0], smin[1]) >> FINE_SHIFT;
+    wbase = top > FINE_BELOW ? top - FINE_BELOW : 0u;
+    if (tile == 0 && threadIdx.x == 0) state[(int64_t)pair * ST_WORDS + ST_WBASE] = wbase;
+  }
+  // the LDS window: held [ha, hz) and received [ra, rz) cover both brackets'
+  // tests and every entry the merge reads (held a0-1 .. a1, received b0 .. b1)
+  const int32_t ha = lo0 - 1, hz = max(hi0, hi1) + 1;
+  const int32_t ra = min(Q0 - hi0, Q1 - hi1), rz = max(Q0 - lo0, Q1 - lo1) + 1;
+  const int32_t nhw = hz - ha, nrw = rz - ra;
   {
-    // hI[i] = held[a0 - 1 + i] (outside [0, kb): -1 before, INT_MAX after), i <= nh + 1;
-    // rI[i] = recv[b0 + i] (INT_MAX past the end), i <= nr.  All loads first.
-    constexpr int SU = (MERGE_TILE + 3 + MERGE_THREADS - 1) / MERGE_THREADS;
+    // held(i) = cI[i - ha] (-1 before the block, INT_MAX past it), received(j) = cI[nhw + j - ra]
+    // (INT_MAX past the block); all loads first
+    constexpr int SU = (MERGE_WIN + MERGE_THREADS - 1) / MERGE_THREADS;
     int32_t ti[SU];
     float tv[SU];
 #pragma unroll
     for (int u = 0; u < SU; ++u) {
-      const int i = threadIdx.x + u * MERGE_THREADS;   // position in the combined buffer
+      const int i = threadIdx.x + u * MERGE_THREADS;
       ti[u] = INT32_MAX;
       tv[u] = 0.f;
-      if (i <= nh + 1) {
-        const int32_t gi = a0 - 1 + i;
+      if (i < nhw) {
+        const int32_t gi = ha + i;
         if (gi < 0) ti[u] = -1;
         else if (gi < kb) { ti[u] = Hi[gi]; tv[u] = Hv[gi]; }
-      } else if (i <= nh + 2 + nr) {
-        const int32_t gj = b0 + (i - nh - 2);
+      } else if (i < nhw + nrw) {
+        const int32_t gj = ra + (i - nhw);
         if (gj < kb) { ti[u] = Ri[gj]; tv[u] = Rv[gj]; }
       }
     }
 #pragma unroll
     for (int u = 0; u < SU; ++u) {
       const int i = threadIdx.x + u * MERGE_THREADS;
-      if (i <= nh + 2 + nr) {
+      if (i < nhw + nrw && i < MERGE_WIN) {
         cI[i] = ti[u];
         cV[i] = tv[u];
       }
     }
   }
   __syncthreads();
-  // held(i) = hI[i - a0 + 1], recv(j) = rI[j - b0]
+  const int32_t* hI = cI - ha;          // hI[a]: held(a) for a in [ha, hz)
+  const int32_t* rI = cI + nhw - ra;    // rI[j]: received(j) for j in [ra, rz)
+  const float* hV = cV - ha;
+  const float* rV = cV + nhw - ra;
+  // exact splits: half the workgroup tests each bracket
+  int32_t a0, a1;
+  {
+    const int half = MERGE_THREADS / 2;
+    const bool second = (int)threadIdx.x >= half;
+    const int32_t lo = second ? lo1 : lo0, hi = second ? hi1 : hi0, q = second ? Q1 : Q0;
+    const int32_t a = lo + ((int)threadIdx.x - (second ? half : 0));
+    const bool p = a < hi && hI[a] <= rI[q - a - 1];
+    const uint32_t c = popc64(__ballot(p));
+    if (lane_id() == 0) scratch[wave_id()] = c;
+    __syncthreads();
+    int32_t c0 = 0, c1 = 0;
+    for (int i = 0; i < MERGE_THREADS / WAVE; ++i) {
+      if (i < half / WAVE) c0 += (int32_t)scratch[i];
+      else c1 += (int32_t)scratch[i];
+    }
+    a0 = lo0 + c0;
+    a1 = lo1 + c1;
+    __syncthreads();
+  }
+  const int32_t b1 = Q1 - a1;
   int32_t ei[MERGE_PER_THREAD];
   float ev[MERGE_PER_THREAD];
   bool eok[MERGE_PER_THREAD];
@@ -95,7 +190,7 @@ __global__ __launch_bounds__(MERGE_THREADS) void k_merge(
     int32_t lo = max(a0, a1 - (Q1 - q_lo)), hi = min(a1, a0 + (q_lo - Q0));
     while (lo < hi) {
       const int32_t mid = (lo + hi) >> 1;
-      if (hI[mid - a0 + 1] <= rI[q_lo - mid - 1 - b0]) lo = mid + 1;
+      if (hI[mid] <= rI[q_lo - mid - 1]) lo = mid + 1;
       else hi = mid;
     }
     a = lo;
@@ -109,26 +204,26 @@ __global__ __launch_bounds__(MERGE_THREADS) void k_merge(
     if (q_lo + k < Q1) {
       a = min(a, a1);     // only reachable with unsorted input; keeps LDS reads in range
       bb = min(bb, b1);
-      const int32_t hx = hI[a - a0 + 1];
-      const int32_t rx = rI[bb - b0];
+      const int32_t hx = hI[a];
+      const int32_t rx = rI[bb];
       if (hx <= rx) {
-        float v = hV[a - a0 + 1];
-        if (rx == hx) v = v + rV[bb - b0];
+        float v = hV[a];
+        if (rx == hx) v = v + rV[bb];
         ei[k] = hx;
         ev[k] = v;
         eok[k] = true;
         ++a;
       } else {
-        if (hI[a - a0] != rx) {
+        if (hI[a - 1] != rx) {
           ei[k] = rx;
-          ev[k] = rV[bb - b0];
+          ev[k] = rV[bb];
           eok[k] = true;
         }
         ++bb;
       }
       if (eok[k]) {
         ++cnt;
-        atomicAdd(&hist[mag_key(ev[k]) >> D1_SHIFT], 1u);
+        atomicAdd(&hist[merge_bin<FINE>(mag_key(ev[k]), wbase)], 1u);
       }
     }
   }
@@ -152,14 +247,58 @@ __global__ __launch_bounds__(MERGE_THREADS) void k_merge(
     U_val[ubase + k] = cV[k];
   }
   flush_hist(hist, hist1 + (int64_t)pair * NB1);
+  if (FINE) {
+    // the tile's keys ordered by fine bin (a counting sort in LDS), for the
+    // threshold kernel: in the slot's MERGE_TILE words of U_key, the low
+    // FINE_SHIFT bits of each key (uint16, bin order) and then the exclusive
+    // prefix of the bin counts (uint16 per bin)
+    static_assert(NB1 == 16 * MERGE_THREADS && FINE_SHIFT <= 16, "16 bins per thread, keys' low bits in 16 bits");
+    uint16_t* __restrict__ SK = reinterpret_cast<uint16_t*>(U_key + ubase);
+    uint16_t* __restrict__ PRE = SK + MERGE_TILE;
+    uint32_t hc[16], sum = 0;
+#pragma unroll
+    for (int j = 0; j < 16; ++j) {
+      hc[j] = hist[16 * threadIdx.x + j];
+      sum += hc[j];
+    }
+    uint32_t tot2;
+    uint32_t x = block_excl_scan(sum, scratch, &tot2);   // its barriers end the flush's and write-out's reads
+    uint32_t pk[8];
+#pragma unroll
+    for (int j = 0; j < 16; ++j) {
+      hist[16 * threadIdx.x + j] = x;
+      if (j & 1) pk[j / 2] |= x << 16;
+      else pk[j / 2] = x;
+      x += hc[j];
+    }
+    uint4* P4 = reinterpret_cast<uint4*>(PRE + 16 * threadIdx.x);
+    P4[0] = make_uint4(pk[0], pk[1], pk[2], pk[3]);
+    P4[1] = make_uint4(pk[4], pk[5], pk[6], pk[7]);
+    __syncthreads();
+    uint16_t* sk = reinterpret_cast<uint16_t*>(cI);   // the staged indices are written out already
+    for (uint32_t k = threadIdx.x; k < tot; k += blockDim.x) {
+      const uint32_t key = mag_key(cV[k]);
+      const uint32_t pos = atomicAdd(&hist[merge_bin<true>(key, wbase)], 1u);
+      sk[pos] = (uint16_t)(key & ((1u << FINE_SHIFT) - 1u));
+    }
+    __syncthreads();
+    const uint32_t* sk2 = reinterpret_cast<const uint32_t*>(sk);
+    uint32_t* SK2 = reinterpret_cast<uint32_t*>(SK);
+    for (uint32_t k = threadIdx.x; 2 * k < tot; k += blockDim.x) SK2[k] = sk2[k];
+  }
 }
 
 // ============================================================================ launchers
 hipError_t launch_merge(const int32_t* sp_idx, const float* sp_val, const Pairs& PM, int64_t npairs, int32_t kb,
-                        int32_t tiles_per_pair, uint32_t* hist1, uint32_t* slot_cnt, int32_t* U_idx,
-                        float* U_val, hipStream_t s) {
+                        int32_t tiles_per_pair, uint32_t* hist1, uint32_t* state, uint32_t* slot_cnt, int32_t* U_idx,
+                        float* U_val, uint32_t* U_key, hipStream_t s) {
   const dim3 grid((unsigned)(npairs * tiles_per_pair));
-  hipLaunchKernelGGL(k_merge, grid, dim3(MERGE_THREADS), 0, s, sp_idx, sp_val, PM, kb, tiles_per_pair, hist1, slot_cnt, U_idx, U_val);
+  if (merge_fine(kb))
+    hipLaunchKernelGGL(k_merge<true>, grid, dim3(MERGE_THREADS), 0, s, sp_idx, sp_val, PM, kb, tiles_per_pair, hist1,
+                       state, slot_cnt, U_idx, U_val, U_key);
+  else
+    hipLaunchKernelGGL(k_merge<false>, grid, dim3(MERGE_THREADS), 0, s, sp_idx, sp_val, PM, kb, tiles_per_pair, hist1,
+                       state, slot_cnt, U_idx, U_val, U_key);
   return hipGetLastError();
 }
 

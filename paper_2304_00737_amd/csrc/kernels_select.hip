@@ -510,29 +510,20 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(SPW >= 8 ? 
 // counts into exclusive prefixes in index order for the emitter.
 //
 // Only the entries of the level-1 threshold bin need levels 2 and 3.  For a
-// dense block they were stored per slot by k_collect; for a merge they are
-// picked out of the union (after the level-1 select on the union's histogram,
-// which is done here too).  This kernel takes units whose bin entries (block
-// top-k) or whole union (merge) fit its register-resident paths; longer units
-// take the staged threshold over slot groups below, which writes the same
-// results (launch_thresh chooses).
-struct ThreshSmem {
-  uint32_t h[NB1];
-  uint32_t scratch[24];
-};
+// dense block they were stored per slot by k_collect (k_thresh below); for a
+// merge they are picked out of the union after the level-1 select on the
+// union's histogram (k_mthresh).  Units too long for these one-workgroup
+// kernels take the staged threshold over slot groups further below, which
+// writes the same results (launch_thresh chooses).
 
-// ---- resident fast paths
-// When a unit's threshold-bin entries (block top-k) or its whole union
-// (merge) fit in registers -- 16 entries per thread -- they are loaded once,
-// with every load in flight together, and levels 2, 3 and the per-slot counts
-// run on registers and LDS only.  Otherwise the general path below re-reads
-// global memory for each pass.
+// ---- resident fast path (block top-k)
+// When a unit's threshold-bin entries fit in registers -- 32 entries per
+// thread -- they are loaded once, with every load in flight together, and
+// levels 2, 3 and the per-slot counts run on registers and LDS only.
 constexpr int FAST_SLOTS = 8192;                 // block top-k: slots per unit
 constexpr int FAST_R0 = 32;                      // block top-k: consecutive bin entries per thread
 constexpr int FAST_CAP0 = 1024 * FAST_R0;        // block top-k: bin entries per register-resident chunk
-constexpr int FAST_ROWS = 16;                    // merge: slots per unit, one float4 per thread each
 constexpr uint32_t KEY_NONE = 0xFFFFFFFFu;       // marks a register that holds no entry (keys are 31-bit)
-static_assert(MERGE_TILE == 4 * 1024, "a merge slot is one float4 per thread of the threshold kernel");
 
 // The slot map of chunk 0 holds two 16-bit slot ids per word, with one pad
 // word after every 16 so that a thread walking its 16 consecutive words hits
@@ -541,7 +532,7 @@ __device__ __forceinline__ uint32_t map_word(uint32_t w) { return w + (w >> 4); 
 __device__ __forceinline__ uint32_t map_half(uint32_t f) { return 2u * map_word(f >> 1) + (f & 1u); }
 
 struct FastSmem {
-  uint32_t pref[FAST_SLOTS + 1];   // block top-k: exclusive prefix of bin entries per slot; merge: slot counts
+  uint32_t pref[FAST_SLOTS + 1];   // exclusive prefix of bin entries per slot
   union {
     uint16_t slotid[FAST_CAP0 + FAST_CAP0 / 16];   // block top-k: slot of each entry of chunk 0, padded
     struct {
@@ -551,11 +542,6 @@ struct FastSmem {
     } c;
   } u;
   uint32_t scratch[24];
-};
-
-union ThreshLds {
-  ThreshSmem g;
-  FastSmem f;
 };
 
 __device__ __forceinline__ void finish_unit(uint32_t* st, uint32_t T1, uint32_t tge, uint32_t teq, uint32_t need_eq,
@@ -568,99 +554,6 @@ __device__ __forceinline__ void finish_unit(uint32_t* st, uint32_t T1, uint32_t 
   st[ST_TEQ] = teq;
   st[ST_NEEDEQ] = need_eq;
   if (drop_cnt) drop_cnt[unit] = (int32_t)(tot_all - (uint32_t)kb);
-}
-
-// Merge unit with at most FAST_ROWS slots: row r of the register file is slot
-// r; thread t holds merged positions 4t .. 4t+3 of every slot.  The caller
-// loads the union (fast_merge_load) before its level-1 select, so that the
-// loads overlap the select's barriers.
-__device__ __forceinline__ void fast_merge_load(const SlotGeom& g, const float* __restrict__ V,
-                                                const uint32_t* __restrict__ cnt, uint32_t (&c)[FAST_ROWS],
-                                                f4v (&v)[FAST_ROWS]) {
-  const f4v* __restrict__ V4 = reinterpret_cast<const f4v*>(V);
-#pragma unroll
-  for (int r = 0; r < FAST_ROWS; ++r) {
-    c[r] = 0u;
-    v[r] = f4v{0.f, 0.f, 0.f, 0.f};
-    if (r < g.nslots) {
-      c[r] = cnt[r];
-      v[r] = V4[r * (MERGE_TILE / 4) + threadIdx.x];
-    }
-  }
-}
-
-__device__ __forceinline__ void thresh_fast_merge(FastSmem& L, int64_t unit, const SlotGeom& g, int32_t kb,
-                                                  int32_t smax, const uint32_t (&c)[FAST_ROWS],
-                                                  const f4v (&v)[FAST_ROWS], uint32_t T1, uint32_t need1,
-                                                  uint32_t cnt1, uint32_t* st, uint32_t* __restrict__ pre_all,
-                                                  uint32_t* __restrict__ pre_ge, uint32_t* __restrict__ pre_eq,
-                                                  int32_t* __restrict__ drop_cnt, uint32_t* err, uint32_t hist_total) {
-  const int t = threadIdx.x, lane = lane_id(), wv = wave_id();
-  const int ns = g.nslots;
-  uint32_t key[FAST_ROWS][4];
-#pragma unroll
-  for (int r = 0; r < FAST_ROWS; ++r) {
-    const uint32_t cr = min(c[r], (uint32_t)MERGE_TILE);
-#pragma unroll
-    for (int q = 0; q < 4; ++q) key[r][q] = (uint32_t)(4 * t + q) < cr ? mag_key(v[r][q]) : KEY_NONE;
-    if (t == r) L.pref[r] = cr;
-  }
-  auto visit = [&](auto f) {
-#pragma unroll
-    for (int r = 0; r < FAST_ROWS; ++r)
-#pragma unroll
-      for (int q = 0; q < 4; ++q)
-        if ((key[r][q] >> D1_SHIFT) == T1) f(key[r][q]);
-  };
-  uint32_t tge, teq, need_eq;
-  resolve_low_digits(T1, need1, cnt1, L.u.c.h, L.scratch, err, visit, tge, teq, need_eq);
-  if (t < FAST_ROWS) {
-    L.u.c.cg[t] = 0u;
-    L.u.c.ce[t] = 0u;
-  }
-  __syncthreads();
-  // ties at the threshold key are rare: without them only the >= count is needed
-  if (need_eq == 0u) {
-#pragma unroll
-    for (int r = 0; r < FAST_ROWS; ++r) {
-      if (r < ns) {
-        uint32_t ng = 0;
-#pragma unroll
-        for (int q = 0; q < 4; ++q) ng += popc64(__ballot(key[r][q] != KEY_NONE && key[r][q] >= tge));
-        if (lane == 0 && ng) atomicAdd(&L.u.c.cg[r], ng);
-      }
-    }
-  } else {
-#pragma unroll
-    for (int r = 0; r < FAST_ROWS; ++r) {
-      if (r < ns) {
-        uint32_t ng = 0, ne = 0;
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          ng += popc64(__ballot(key[r][q] != KEY_NONE && key[r][q] >= tge));
-          ne += popc64(__ballot(key[r][q] == teq));
-        }
-        if (lane == 0) {
-          if (ng) atomicAdd(&L.u.c.cg[r], ng);
-          if (ne) atomicAdd(&L.u.c.ce[r], ne);
-        }
-      }
-    }
-  }
-  __syncthreads();
-  if (wv == 0) {   // exclusive prefixes over the unit's (at most 16) slots
-    const uint32_t a = lane < ns ? L.pref[lane] : 0u;
-    const uint32_t gg = lane < ns ? L.u.c.cg[lane] : 0u;
-    const uint32_t ee = lane < ns ? L.u.c.ce[lane] : 0u;
-    const uint32_t ai = wave_incl_scan(a), gi = wave_incl_scan(gg), ei = wave_incl_scan(ee);
-    const int64_t o = unit * smax;
-    if (lane < ns) {
-      pre_all[o + lane] = ai - a;
-      pre_ge[o + lane] = gi - gg;
-      pre_eq[o + lane] = ei - ee;
-    }
-    if (lane == WAVE - 1) finish_unit(st, T1, tge, teq, need_eq, ai, gi, ei, kb, drop_cnt, unit, err, hist_total);
-  }
 }
 
 // Block top-k unit with at most FAST_SLOTS slots.  Its threshold-bin entries
@@ -879,63 +772,300 @@ __device__ __forceinline__ void thresh_fast_topk(FastSmem& L, int64_t unit, cons
   if (t == 0) finish_unit(st, T1, tge, teq, need_eq, ta, tg, te, kb, nullptr, unit, err, 0u);
 }
 
-template <int mode>
 __global__ __launch_bounds__(1024) void k_thresh(Blocks B, Units U, int32_t kb, int32_t smax,
-                                                 uint32_t* __restrict__ hist1,
-                                                 const float* __restrict__ U_val, uint32_t* __restrict__ state,
-                                                 const uint32_t* __restrict__ slot_cnt,
+                                                 uint32_t* __restrict__ state, const uint32_t* __restrict__ slot_cnt,
                                                  const uint32_t* __restrict__ slot_nbin,
                                                  const uint32_t* __restrict__ bin_key,
                                                  uint32_t* __restrict__ pre_all, uint32_t* __restrict__ pre_ge,
-                                                 uint32_t* __restrict__ pre_eq, int32_t* __restrict__ drop_cnt,
-                                                 uint32_t* __restrict__ err) {
-  __shared__ ThreshLds S;
-  ThreshSmem& L = S.g;
-  constexpr int NT = 1024;
+                                                 uint32_t* __restrict__ pre_eq, uint32_t* __restrict__ err) {
+  __shared__ FastSmem S;
   const int64_t cunit = blockIdx.x;
-  const SlotGeom g = slot_geom(mode, (uint32_t)cunit, B, U, kb);
-  const int64_t unit = mode == 0 ? (int64_t)U.canon((uint32_t)cunit, B.P) : cunit;   // the unit's arrays
+  const SlotGeom g = slot_geom(0, (uint32_t)cunit, B, U, kb);
+  const int64_t unit = (int64_t)U.canon((uint32_t)cunit, B.P);   // the unit's arrays
   uint32_t* st = state + unit * ST_WORDS;
-  const uint32_t* __restrict__ cnt = slot_cnt + unit * smax;
-  const uint32_t* __restrict__ nbn = slot_nbin + unit * smax;
-  const uint32_t* __restrict__ K = bin_key + g.base;
-  const float* __restrict__ V = U_val + g.base;
-  uint32_t ok;
-
-  // ---- level 1
-  uint32_t T1, need1, cnt1;
-  uint32_t hist_total = 0;
-  uint32_t mc[mode == 1 ? FAST_ROWS : 1];
-  f4v mv[mode == 1 ? FAST_ROWS : 1];
-  if constexpr (mode == 1) {
-    if (g.nslots <= FAST_ROWS) fast_merge_load(g, V, cnt, mc, mv);   // uniform
-    uint32_t* __restrict__ H = hist1 + unit * NB1;
-    g2lds<NB1 / NT>(L.h, H, NB1);
-#pragma unroll
-    for (int q = 0; q < NB1 / NT; ++q) H[q * NT + threadIdx.x] = 0u;   // histograms rest at zero
-    __syncthreads();
-    uint32_t above1;
-    block_select_desc(L.h, NB1, (uint32_t)kb, L.scratch, &T1, &above1, &cnt1, &ok, &hist_total);
-    if (!ok && threadIdx.x == 0) atomicOr(err, ERR_COUNT);
-    need1 = ok ? (uint32_t)kb - above1 : 0u;
-  } else {
-    T1 = st[ST_T1];
-    need1 = st[ST_NEED1];
-    cnt1 = st[ST_CNT1];
-  }
-  if constexpr (mode == 1) {
-    if (g.nslots <= FAST_ROWS) {
-      thresh_fast_merge(S.f, unit, g, kb, smax, mc, mv, T1, need1, cnt1, st, pre_all, pre_ge, pre_eq, drop_cnt,
-                        err, hist_total);
-      return;
-    }
-  } else {
-    if (g.nslots <= FAST_SLOTS) {
-      thresh_fast_topk(S.f, unit, g, kb, smax, K, cnt, nbn, T1, need1, cnt1, st, pre_all, pre_ge, pre_eq, err);
-      return;
-    }
+  // level 1 was resolved by the level-1 select
+  const uint32_t T1 = st[ST_T1], need1 = st[ST_NEED1], cnt1 = st[ST_CNT1];
+  if (g.nslots <= FAST_SLOTS) {
+    thresh_fast_topk(S, unit, g, kb, smax, bin_key + g.base, slot_cnt + unit * smax, slot_nbin + unit * smax, T1,
+                     need1, cnt1, st, pre_all, pre_ge, pre_eq, err);
+    return;
   }
   if (threadIdx.x == 0) atomicOr(err, ERR_COUNT);   // longer units are routed to the staged threshold
+}
+
+// ---- merge threshold
+// One workgroup per merge unit (a union of up to MT_SLOTS slots of
+// MERGE_TILE positions).  The union's level-1 histogram, summed by k_merge
+// over the fine window (merge_fine in common.hpp), gives the threshold bin:
+// the keys k with k >> S == pfx, S = FINE_SHIFT.  k_merge also left, per
+// slot, its keys' low bits in bin order and the bins' prefix, so the bin's
+// entries of every slot are one contiguous run there: two prefix words per
+// slot give the run (and the entries above the bin), and one round of loads
+// gathers the runs into a list in LDS -- a few hundred or thousand entries --
+// over which the last S key bits (two digits) and the per-slot counts of
+// selected and tied keys are resolved.  If the threshold fell in one of the
+// window's two clamped bins, a pass over the union builds the histogram of
+// the top 12 key bits and a second one counts and lists the bin's entries
+// (S = D1_SHIFT).  A bin too large for the list is visited from the union
+// again instead (the same results, more passes).
+constexpr int MT_THREADS = 1024;
+constexpr int MT_LIST = 16384;    // threshold-bin entries held in LDS
+static_assert(MERGE_TILE == 4 * MT_THREADS, "a merge slot is one float4 per thread of the merge threshold");
+static_assert(MT_SLOTS <= MT_THREADS, "one slot per thread in the per-slot scans");
+static_assert((MT_SLOTS - 1) < (1 << (32 - D1_SHIFT)), "slot and low key bits share a list word");
+
+struct MThreshSmem {
+  uint32_t h[NB1];
+  uint32_t list[MT_LIST];
+  uint32_t above[MT_SLOTS];   // per slot: entries above the threshold bin
+  uint32_t cg[MT_SLOTS];      // per slot: bin entries with key >= TGE
+  uint32_t ce[MT_SLOTS];      // per slot: bin entries with key == TEQ
+  uint32_t roff[MT_SLOTS];    // per slot: the run's first position in the list
+  uint32_t rlo[MT_SLOTS];     // per slot: the run's first position among the slot's keys
+  uint32_t nlist;
+  uint32_t scratch[40];
+};
+
+// f(key, slot) for every union entry of a unit, read in chunks of 4 slots
+// (slot s0 + r, positions 4t .. 4t+3 of it in thread t).
+template <typename F>
+__device__ __forceinline__ void mt_each(const f4v* __restrict__ V4, const uint32_t* __restrict__ cnt, int32_t ns,
+                                        uint32_t cap_last, F f) {
+  for (int32_t s0 = 0; s0 < ns; s0 += 4) {
+    uint32_t c[4];
+    f4v v[4];
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int32_t s = s0 + r;
+      c[r] = 0u;
+      v[r] = f4v{0.f, 0.f, 0.f, 0.f};
+      if (s < ns) {
+        c[r] = min(cnt[s], s == ns - 1 ? cap_last : (uint32_t)MERGE_TILE);
+        v[r] = V4[(int64_t)s * (MERGE_TILE / 4) + threadIdx.x];
+      }
+    }
+#pragma unroll
+    for (int r = 0; r < 4; ++r)
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+        if ((uint32_t)(4 * threadIdx.x + q) < c[r]) f(mag_key(v[r][q]), (uint32_t)(s0 + r));
+  }
+}
+
+// Levels 2 and 3 over the keys of one bin, k >> S == pfx (visit(f) calls
+// f(key) for each of them): the low S bits in two digits, the last of D3
+// bits.  Returns the threshold as (tge, teq, need_eq).
+template <typename Visit>
+__device__ __forceinline__ void resolve_bin(uint32_t pfx, int S, uint32_t need1, uint32_t cnt1, uint32_t* h,
+                                            uint32_t* scratch, uint32_t* err, Visit visit, uint32_t& tge,
+                                            uint32_t& teq, uint32_t& need_eq) {
+  const int D3 = S == FINE_SHIFT ? 7 : 8;
+  const int nb2 = 1 << (S - D3), nb3 = 1 << D3;
+  tge = pfx << S;
+  teq = 0u;
+  need_eq = 0u;
+  if (need1 == cnt1) return;
+  __syncthreads();
+  for (int i = threadIdx.x; i < nb2; i += MT_THREADS) h[i] = 0u;
+  __syncthreads();
+  visit([&](uint32_t key) { atomicAdd(&h[(key >> D3) & (uint32_t)(nb2 - 1)], 1u); });
+  __syncthreads();
+  uint32_t T2, above2, cnt2, ok;
+  block_select_desc(h, nb2, need1, scratch, &T2, &above2, &cnt2, &ok);
+  if (!ok) {
+    if (threadIdx.x == 0) atomicOr(err, ERR_COUNT_L23);
+    return;
+  }
+  const uint32_t need2 = need1 - above2;
+  const uint32_t pre = (pfx << (S - D3)) | T2;   // all but the last D3 key bits
+  tge = pre << D3;
+  if (need2 == cnt2) return;
+  for (int i = threadIdx.x; i < nb3; i += MT_THREADS) h[i] = 0u;
+  __syncthreads();
+  visit([&](uint32_t key) {
+    if ((key >> D3) == pre) atomicAdd(&h[key & (uint32_t)(nb3 - 1)], 1u);
+  });
+  __syncthreads();
+  uint32_t T3, above3, cnt3;
+  block_select_desc(h, nb3, need2, scratch, &T3, &above3, &cnt3, &ok);
+  if (!ok) {
+    if (threadIdx.x == 0) atomicOr(err, ERR_COUNT_L23);
+    return;
+  }
+  const uint32_t need3 = need2 - above3;
+  const uint32_t T = (pre << D3) | T3;
+  if (need3 == cnt3) {
+    tge = T;
+  } else {
+    tge = T + 1u;
+    teq = T;
+    need_eq = need3;
+  }
+}
+
+// Exclusive prefix over the unit's slots of one value per thread (slot t):
+// one wave when the unit has at most WAVE slots, else the whole workgroup.
+// *total gets the sum.  Uniform over the workgroup; may contain barriers.
+__device__ __forceinline__ uint32_t slot_excl_scan(uint32_t v, int32_t ns, uint32_t* scratch, uint32_t* total) {
+  if (ns <= WAVE) {
+    const uint32_t incl = wave_incl_scan(v);   // every wave scans lanes 0..63 alike; wave 0 holds the slots
+    *total = __shfl(incl, WAVE - 1, WAVE);
+    return incl - v;
+  }
+  return block_excl_scan(v, scratch, total);
+}
+
+__global__ __launch_bounds__(MT_THREADS) void k_mthresh(int32_t kb, int32_t smax, uint32_t* __restrict__ hist1,
+                                                        const float* __restrict__ U_val,
+                                                        const uint32_t* __restrict__ U_key,
+                                                        uint32_t* __restrict__ state,
+                                                        const uint32_t* __restrict__ slot_cnt,
+                                                        uint32_t* __restrict__ pre_all, uint32_t* __restrict__ pre_ge,
+                                                        uint32_t* __restrict__ pre_eq, int32_t* __restrict__ drop_cnt,
+                                                        uint32_t* __restrict__ err) {
+  __shared__ MThreshSmem L;
+  const int t = threadIdx.x;
+  const int64_t unit = blockIdx.x;
+  const int32_t ns = (int32_t)((2ll * kb + MERGE_TILE - 1) / MERGE_TILE);   // the merge's slots of this unit
+  const uint32_t cap_last = (uint32_t)(2ll * kb - (int64_t)(ns - 1) * MERGE_TILE);
+  const int64_t ubase = unit * ns * (int64_t)MERGE_TILE;
+  const f4v* __restrict__ V4 = reinterpret_cast<const f4v*>(U_val + ubase);
+  const uint32_t* __restrict__ cnt = slot_cnt + unit * smax;
+  uint32_t* st = state + unit * ST_WORDS;
+  const uint32_t wbase = st[ST_WBASE];
+  // the slot's entry count (its own thread), loaded with the histogram
+  const uint32_t my_c = t < ns ? min(cnt[t], t == ns - 1 ? cap_last : (uint32_t)MERGE_TILE) : 0u;
+
+  // ---- level 1 on the union's fine histogram (which is left at zero for the next merge)
+  uint32_t* __restrict__ H = hist1 + unit * NB1;
+  g2lds<NB1 / MT_THREADS>(L.h, H, NB1);
+#pragma unroll
+  for (int q = 0; q < NB1 / MT_THREADS; ++q) H[q * MT_THREADS + t] = 0u;
+  if (t < ns) {
+    L.above[t] = 0u;
+    L.cg[t] = 0u;
+    L.ce[t] = 0u;
+  }
+  if (t == 0) L.nlist = 0u;
+  __syncthreads();
+  uint32_t T1, above1, cnt1, ok, hist_total;
+  block_select_desc(L.h, NB1, (uint32_t)kb, L.scratch, &T1, &above1, &cnt1, &ok, &hist_total);
+  const bool fine = ok && T1 != 0u && T1 != (uint32_t)NB1 - 1u;   // uniform: inside the window
+  int S = FINE_SHIFT;
+  uint32_t pfx = wbase + T1;
+  if (!fine) {
+    // the histogram of the top 12 key bits, from the union itself
+    __syncthreads();
+    for (int i = t; i < NB1; i += MT_THREADS) L.h[i] = 0u;
+    __syncthreads();
+    mt_each(V4, cnt, ns, cap_last, [&](uint32_t key, uint32_t) { atomicAdd(&L.h[key >> D1_SHIFT], 1u); });
+    __syncthreads();
+    uint32_t tot2;
+    block_select_desc(L.h, NB1, (uint32_t)kb, L.scratch, &T1, &above1, &cnt1, &ok, &tot2);
+    S = D1_SHIFT;
+    pfx = T1;
+  }
+  if (!ok && t == 0) atomicOr(err, ERR_COUNT);
+  const uint32_t need1 = ok ? (uint32_t)kb - above1 : 0u;
+  const uint32_t lowm = (1u << S) - 1u;
+  const bool listed = cnt1 <= (uint32_t)MT_LIST;   // uniform
+
+  if (fine) {
+    // ---- the bin's run in every slot: [p0, p1) among the slot's keys in bin order
+    uint32_t p0 = 0, p1 = 0;
+    if (t < ns) {
+      const uint16_t* PRE = reinterpret_cast<const uint16_t*>(U_key + ubase + (int64_t)t * MERGE_TILE) + MERGE_TILE;
+      p0 = min((uint32_t)PRE[T1], my_c);
+      p1 = min(max((uint32_t)PRE[T1 + 1u], p0), my_c);
+      L.above[t] = my_c - p1;
+      L.rlo[t] = p0;
+    }
+    uint32_t run_total;
+    const uint32_t roff = slot_excl_scan(p1 - p0, ns, L.scratch, &run_total);
+    if (t < ns) L.roff[t] = roff;
+    if (t == 0) L.nlist = run_total;
+    if (run_total != cnt1 && t == 0) atomicOr(err, ERR_COUNT);
+    __syncthreads();
+    if (listed) {
+      // gather: list entry i belongs to the last slot whose run starts at or before it
+      constexpr int GR = 4;   // loads in flight per thread
+      const uint32_t n = min(L.nlist, (uint32_t)MT_LIST);   // the total, from the scan's wave
+      for (uint32_t i0 = 0; i0 < n; i0 += GR * MT_THREADS) {
+        uint32_t low[GR], sl[GR];
+#pragma unroll
+        for (int g = 0; g < GR; ++g) {
+          const uint32_t i = i0 + (uint32_t)(g * MT_THREADS + t);
+          sl[g] = 0u;
+          low[g] = 0u;
+          if (i < n) {
+            int32_t lo = 0, hi = ns;
+            while (hi - lo > 1) {
+              const int32_t mid = (lo + hi) >> 1;
+              if (L.roff[mid] <= i) lo = mid;
+              else hi = mid;
+            }
+            sl[g] = (uint32_t)lo;
+            const uint16_t* SK = reinterpret_cast<const uint16_t*>(U_key + ubase + (int64_t)lo * MERGE_TILE);
+            low[g] = SK[L.rlo[lo] + (i - L.roff[lo])];
+          }
+        }
+#pragma unroll
+        for (int g = 0; g < GR; ++g) {
+          const uint32_t i = i0 + (uint32_t)(g * MT_THREADS + t);
+          if (i < n) L.list[i] = (sl[g] << S) | (low[g] & lowm);
+        }
+      }
+    }
+  } else {
+    // ---- a pass over the union: per-slot counts above the bin, the bin's entries into the list
+    mt_each(V4, cnt, ns, cap_last, [&](uint32_t key, uint32_t s) {
+      const uint32_t k = key >> S;
+      if (k > pfx) atomicAdd(&L.above[s], 1u);
+      else if (k == pfx && listed) {
+        const uint32_t pos = atomicAdd(&L.nlist, 1u);
+        if (pos < (uint32_t)MT_LIST) L.list[pos] = (s << S) | (key & lowm);
+      }
+    });
+  }
+  __syncthreads();
+  const uint32_t nl = min(L.nlist, (uint32_t)MT_LIST);
+  if (listed && nl != cnt1 && t == 0) atomicOr(err, ERR_COUNT);
+  // f(key, slot) for every entry of the threshold bin: from the list, or from the union again
+  auto each_bin_entry = [&](auto f) {
+    if (listed) {
+      for (uint32_t i = t; i < nl; i += MT_THREADS) {
+        const uint32_t w = L.list[i];
+        f((pfx << S) | (w & lowm), w >> S);
+      }
+    } else {
+      mt_each(V4, cnt, ns, cap_last, [&](uint32_t key, uint32_t s) {
+        if ((key >> S) == pfx) f(key, s);
+      });
+    }
+  };
+  uint32_t tge, teq, need_eq;
+  resolve_bin(pfx, S, need1, cnt1, L.h, L.scratch, err,
+              [&](auto f) { each_bin_entry([&](uint32_t key, uint32_t) { f(key); }); }, tge, teq, need_eq);
+  __syncthreads();
+  each_bin_entry([&](uint32_t key, uint32_t s) {
+    if (key >= tge) atomicAdd(&L.cg[s], 1u);
+    else if (need_eq != 0u && key == teq) atomicAdd(&L.ce[s], 1u);
+  });
+  __syncthreads();
+  // ---- per-slot exclusive prefixes (slot t)
+  const uint32_t gq = t < ns ? L.above[t] + L.cg[t] : 0u;
+  const uint32_t eq = t < ns ? L.ce[t] : 0u;
+  uint32_t ta, tg, te;
+  const uint32_t xa = slot_excl_scan(my_c, ns, L.scratch, &ta);
+  const uint32_t xg = slot_excl_scan(gq, ns, L.scratch, &tg);
+  const uint32_t xe = slot_excl_scan(eq, ns, L.scratch, &te);
+  if (t < ns) {
+    const int64_t o = unit * smax + t;
+    pre_all[o] = xa;
+    pre_ge[o] = xg;
+    pre_eq[o] = xe;
+  }
+  if (t == 0) finish_unit(st, pfx, tge, teq, need_eq, ta, tg, te, kb, drop_cnt, unit, err, hist_total);
 }
 
 // ============================================================================ exact threshold, large units
@@ -1681,8 +1811,7 @@ hipError_t launch_thresh(int mode, int64_t nunits, const Units& U, int64_t n, in
                          const uint32_t* slot_nbin, const uint32_t* bin_key, uint32_t* pre_all, uint32_t* pre_ge,
                          uint32_t* pre_eq, int32_t* drop_cnt, uint32_t* err, hipStream_t s) {
   // few long units: the staged threshold over slot groups (same results)
-  const bool big = mode == 0 ? (smax > FAST_SLOTS || (nunits < 32 && smax > 1024))
-                             : (2ll * kb > (int64_t)FAST_ROWS * MERGE_TILE);
+  const bool big = mode == 0 ? (smax > FAST_SLOTS || (nunits < 32 && smax > 1024)) : !merge_fine(kb);
   if (big) {
     if (!hist1) return hipErrorInvalidValue;   // the staged threshold needs the histogram space
     BigArgs a;
@@ -1725,11 +1854,11 @@ hipError_t launch_thresh(int mode, int64_t nunits, const Units& U, int64_t n, in
     return hipGetLastError();
   }
   if (mode == 0)
-    hipLaunchKernelGGL(k_thresh<0>, dim3((unsigned)nunits), dim3(1024), 0, s, make_blocks(n, P), U, kb, smax, hist1, U_val,
-                       state, slot_cnt, slot_nbin, bin_key, pre_all, pre_ge, pre_eq, drop_cnt, err);
+    hipLaunchKernelGGL(k_thresh, dim3((unsigned)nunits), dim3(1024), 0, s, make_blocks(n, P), U, kb, smax, state,
+                       slot_cnt, slot_nbin, bin_key, pre_all, pre_ge, pre_eq, err);
   else
-    hipLaunchKernelGGL(k_thresh<1>, dim3((unsigned)nunits), dim3(1024), 0, s, make_blocks(n, P), U, kb, smax, hist1, U_val,
-                       state, slot_cnt, slot_nbin, bin_key, pre_all, pre_ge, pre_eq, drop_cnt, err);
+    hipLaunchKernelGGL(k_mthresh, dim3((unsigned)nunits), dim3(MT_THREADS), 0, s, kb, smax, hist1, U_val, bin_key,
+                       state, slot_cnt, pre_all, pre_ge, pre_eq, drop_cnt, err);
   return hipGetLastError();
 }
 

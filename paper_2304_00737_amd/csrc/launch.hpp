@@ -48,9 +48,12 @@ hipError_t launch_emit(int mode, const int32_t* cand_idx, const float* cand_val,
                        const uint32_t* slot_cnt, const uint32_t* pre_all, const uint32_t* pre_ge,
                        const uint32_t* pre_eq, int32_t* out_idx, float* out_val, int32_t* local_idx,
                        int32_t* drop_idx, float* drop_val, uint32_t* err, hipStream_t s);
+// Union tiles and their level-1 histogram; with merge_fine(kb) the fine window
+// (its first bin in the pairs' state word ST_WBASE) and, per slot, the keys'
+// low bits in bin order and the bins' prefix in the slot's words of U_key.
 hipError_t launch_merge(const int32_t* sp_idx, const float* sp_val, const Pairs& PM, int64_t npairs, int32_t kb,
-                        int32_t tiles_per_pair, uint32_t* hist1, uint32_t* slot_cnt, int32_t* U_idx,
-                        float* U_val, hipStream_t s);
+                        int32_t tiles_per_pair, uint32_t* hist1, uint32_t* state, uint32_t* slot_cnt, int32_t* U_idx,
+                        float* U_val, uint32_t* U_key, hipStream_t s);
 hipError_t launch_densify(const int32_t* sp_idx, const float* sp_val, int32_t P, int64_t n, int32_t kb,
                           float* dense, uint32_t* member, bool vec4, hipStream_t s);
 hipError_t launch_bm_mark(const int32_t* sp_idx, int32_t P, int64_t n, int32_t kb, uint32_t* bm, bool set,
