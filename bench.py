@@ -329,6 +329,22 @@ def main() -> int:
     torch.cuda.synchronize()
     add_ms = sum(a.elapsed_time(b) for a, b in k_mid) / args.steps - marker_ms
     ws_check(st)
+    # the same rows through the plain residual add (no histogram, no candidates): the
+    # streaming ceiling of this access pattern, beside the fused kernel; run on the
+    # workspace's copy of acc so the step's state is untouched (g0 and -g0 alternate)
+    plain_ms = None
+    if d == 1 and not lazy:
+        scratch_acc = st.acc.clone()
+        neg = -g0
+        pm = [(ev(), ev()) for _ in range(args.steps)]
+        for j in range(args.steps):
+            pm[j][0].record(stream)
+            spardl.residual_add(scratch_acc, g0 if j % 2 == 0 else neg, P, n, 0, None)
+            pm[j][1].record(stream)
+        torch.cuda.synchronize()
+        plain_ms = sum(a.elapsed_time(b) for a, b in pm) / args.steps - marker_ms
+        del scratch_acc, neg
+        torch.cuda.empty_cache()
 
     elems = P * n
     value = elems / (ms_per_step * 1e-3)
@@ -418,7 +434,9 @@ def main() -> int:
         "roofline": {"bound": "hbm", "kernel": "k_residual_add" if dominant == "residual_add" else dominant,
                      "achieved": achieved, "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS, "traffic": traffic,
-                     "alg_bytes_per_launch": alg[dominant], "avg_launch_ms": dom_ms},
+                     "alg_bytes_per_launch": alg[dominant], "avg_launch_ms": dom_ms,
+                     "plain_add_ms": plain_ms,
+                     "plain_add_GBs": (12.0 * P * n / (plain_ms * 1e-3) / 1e9) if plain_ms else None},
         "step_roofline": _step_roofline(moved, alg, ms_per_step, cand, reread, stats),
         "per_call_ms": per_call_ms,
         "event_marker_ms": marker_ms,
