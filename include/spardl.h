@@ -119,9 +119,13 @@ int spardl_workspace_init(int32_t nworkers, int32_t P, int64_t n, int32_t k_blk,
  * and ws ignored) is a plain add.
  * w0: the worker that row 0 of acc and grad belongs to, when a call covers
  * workers w0 .. w0 + nworkers - 1 of the P (a workspace for fewer rows than
- * P, the workers taken a few at a time): the floor of each block comes from
- * that worker's own previous threshold, kept in ws per worker and block.
- * 0 when the call covers all workers; ignored for the plain add.
+ * P, the workers taken a few at a time).  The floor of each block comes from
+ * the larger of two thresholds kept in ws per worker and block: the worker's
+ * own from its previous top-k and the same block's latest at the preceding
+ * worker (w - 1, or P - 1 for worker 0) -- this step's when that worker was
+ * selected earlier in it, a closer estimate while the residual grows.  The
+ * floor only decides how much the top-k reads; its results never depend on
+ * it.  0 when the call covers all workers; ignored for the plain add.
  * Errors: EINVAL for NULL acc/grad, nworkers < 1, n < 1 or n >= 2^31,
  * ld < n, P < 0, P > n, w0 < 0, and with ws: nworkers > P,
  * w0 + nworkers > P, misaligned ws or k_blk out of [1, floor(n / P)];

@@ -423,6 +423,7 @@ int spardl_residual_add(float* acc, int64_t ld_acc, const float* grad, int64_t l
   AddSpec sp;
   sp.hist1 = w.hist1;
   sp.spec_t1 = w.spec_t1 + (int64_t)w0 * P;   // the hints of workers w0 .. w0 + nworkers - 1
+  if (P > 1) sp.spec_prev = w.spec_t1 + (int64_t)((w0 + P - 1) % P) * P;
   sp.spec_used = w.spec_used;
   sp.spec_cnt = w.spec_cnt;
   sp.cand_idx = w.cand_idx;

@@ -54,7 +54,9 @@ __global__ __launch_bounds__(256) void k_fill(FillRanges r) {
 // From a block's second step on, the histogram counts only keys at or above
 // a lower floor (two binades further down): the threshold lies there unless it
 // fell by more than that since the previous step, and then the level-1 select
-// rebuilds the block's full histogram itself.
+// rebuilds the block's full histogram itself.  The previous threshold is the
+// larger of the worker's own from its previous step and the same block's
+// latest at the preceding worker.
 constexpr int ADD_STAGE = 512;          // speculative candidates staged in LDS per tile
 
 template <bool HIST>
@@ -104,7 +106,15 @@ __global__ __launch_bounds__(256) void k_residual_add4(float* __restrict__ acc, 
   // the histogram is cleared while the loads are in flight
   for (int i = threadIdx.x; i < NB1 / 4; i += 256) reinterpret_cast<uint4*>(h)[i] = make_uint4(0u, 0u, 0u, 0u);
   uint32_t F = SPEC_NONE;
-  const uint32_t sw = sp.spec_t1[wb];
+  uint32_t sw = sp.spec_t1[wb];
+  if (sp.spec_prev) {
+    // the same block's latest hint at the preceding worker: when workers run a few at
+    // a time it is this step's, a closer estimate while the residual is still growing
+    // (a threshold from the step before can lie several bins lower then); the larger
+    // of the two is used
+    const uint32_t pw = w == 0u ? sp.spec_prev[b] : sp.spec_t1[wb - B.P];
+    sw = max(sw, pw);
+  }
   if (sw != 0u) {
     const uint32_t T1p = sw - 1u;
     F = T1p > SPEC_MARGIN ? (T1p - SPEC_MARGIN) << D1_SHIFT : 0u;
