@@ -28,7 +28,7 @@ constexpr int SLOT = 4096;                       // elements per candidate slot 
 constexpr int MERGE_THREADS = 256;
 constexpr int MERGE_PER_THREAD = 16;
 constexpr int MERGE_TILE = MERGE_THREADS * MERGE_PER_THREAD;   // merged positions per workgroup
-constexpr int DENSE_TILE = 16384;
+constexpr int DENSE_TILE = 8192;                 // output elements per densify workgroup (an LDS image)
 constexpr int HCOPIES = 4;                       // level-1 histogram copies per block (spreads the flush atomics)
 
 // ---------------------------------------------------------------- merge threshold

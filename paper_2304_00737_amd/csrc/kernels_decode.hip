@@ -9,40 +9,28 @@
 namespace spardl {
 
 // ============================================================================ a5: all-gather + densify
-// One workgroup per tile [t0, t0 + DENSE_TILE) of the output.  The tile's
-// zeros are stored first, straight to memory, so that the write stream does
-// not wait for anything; then the final entries whose index falls in the
-// tile are found (both ends by one joint binary search in the index-sorted
-// final blocks sp[b][b]) and stored over them after a barrier, whose
-// workgroup-scope ordering makes the entry the last write to its element.
-// With `member`, the tile's words of the membership bitmap of the final
-// index set I are written as well (bit x & 31 of word x >> 5 set iff x is in
-// I), every word of [0, ceil(n/32)) exactly once.
+// One workgroup per tile [t0, t0 + DENSE_TILE) of the output.  The tile is
+// built in LDS as an image -- zeros, then the final entries whose index falls
+// in the tile (both ends found by one joint search in the index-sorted final
+// blocks sp[b][b], whose loads overlap the image's zeroing) -- and written
+// once with whole-line stores, so no line of the output is written twice.
+// With `member`, the tile's words of the membership bitmap of the final index
+// set I are written as well (bit x & 31 of word x >> 5 set iff x is in I),
+// every word of [0, ceil(n/32)) exactly once.
 template <int VEC>
 __global__ __launch_bounds__(256) void k_densify(const int32_t* __restrict__ sp_idx,
                                                  const float* __restrict__ sp_val, Blocks B,
                                                  int32_t kb, float* __restrict__ dense,
                                                  uint32_t* __restrict__ member) {
   static_assert(DENSE_TILE % 1024 == 0, "whole float4 rounds and bitmap words");
+  __shared__ __align__(16) float img[DENSE_TILE];
   __shared__ uint32_t bits[DENSE_TILE / 32];
   __shared__ uint32_t cnt[8];
   const int64_t n = B.n;
   const int64_t t0 = (int64_t)blockIdx.x * DENSE_TILE;
   const int64_t t1 = min(t0 + DENSE_TILE, n);
-  if (VEC == 4) {
-    for (int i = threadIdx.x * 4; i < DENSE_TILE; i += blockDim.x * 4) {
-      const int64_t x = t0 + i;
-      if (x + 3 < t1) {
-        *reinterpret_cast<float4*>(dense + x) = make_float4(0.f, 0.f, 0.f, 0.f);
-      } else {
-        for (int c = 0; c < 4; ++c)
-          if (x + c < t1) dense[x + c] = 0.f;
-      }
-    }
-  } else {
-    for (int i = threadIdx.x; i < DENSE_TILE; i += blockDim.x)
-      if (t0 + i < t1) dense[t0 + i] = 0.f;
-  }
+  for (int i = threadIdx.x; i < DENSE_TILE / 4; i += blockDim.x)
+    reinterpret_cast<float4*>(img)[i] = make_float4(0.f, 0.f, 0.f, 0.f);
   for (int i = threadIdx.x; i < DENSE_TILE / 32; i += blockDim.x) bits[i] = 0u;
   const uint32_t blo = B.of((uint32_t)t0), bhi = B.of((uint32_t)(t1 - 1));
   for (uint32_t b = blo; b <= bhi; ++b) {
@@ -51,18 +39,24 @@ __global__ __launch_bounds__(256) void k_densify(const int32_t* __restrict__ sp_
     int32_t lo, hi;
     wg_partition_point2(
         0, kb, [&](int32_t p) { return (int64_t)Fi[p] < t0; }, 0, kb,
-        [&](int32_t p) { return (int64_t)Fi[p] < t1; }, cnt, &lo, &hi);
-    if (b == blo) __syncthreads();   // uniform: the zero stores and the bitmap clear come first
+        [&](int32_t p) { return (int64_t)Fi[p] < t1; }, cnt, &lo, &hi);   // its barriers order the zeroing
     for (int32_t j = lo + (int32_t)threadIdx.x; j < hi; j += blockDim.x) {
       const int64_t r = (int64_t)Fi[j] - t0;
       if (r >= 0 && r < t1 - t0) {
-        dense[t0 + r] = Fv[j];
-        if (member) atomicOr(&bits[r >> 5], 1u << (r & 31));
+        img[r] = Fv[j];
+        atomicOr(&bits[r >> 5], 1u << (r & 31));
       }
     }
   }
+  __syncthreads();
+  const int64_t len = t1 - t0;
+  if (VEC == 4 && len == DENSE_TILE) {
+    for (int i = threadIdx.x; i < DENSE_TILE / 4; i += blockDim.x)
+      __builtin_nontemporal_store(reinterpret_cast<const f4v*>(img)[i], reinterpret_cast<f4v*>(dense + t0) + i);
+  } else {
+    for (int i = threadIdx.x; i < len; i += blockDim.x) dense[t0 + i] = img[i];
+  }
   if (member) {
-    __syncthreads();
     for (int i = threadIdx.x; i < DENSE_TILE / 32 && t0 + 32 * (int64_t)i < t1; i += blockDim.x)
       member[(t0 >> 5) + i] = bits[i];
   }
