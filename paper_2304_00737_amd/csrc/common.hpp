@@ -50,7 +50,7 @@ __host__ __device__ __forceinline__ bool merge_fine(int64_t kb) { return 2 * kb 
 // ---------------------------------------------------------------- state words
 // Per selection unit (a (worker, block) pair or a merge pair), 16 u32:
 enum : int {
-  ST_T1 = 0,        // level-1 threshold bin
+  ST_T1 = 0,        // level-1 threshold bin (its key prefix; see ST_SHIFT)
   ST_ABOVE1 = 1,    // entries in bins above ST_T1
   ST_NEED1 = 2,     // entries still needed from bin ST_T1
   ST_CNT1 = 3,      // entries in bin ST_T1
@@ -59,10 +59,11 @@ enum : int {
   ST_NEEDEQ = 6,
   ST_SPECOK = 7,    // block top-k: the fused add's speculative candidates cover the threshold bin
   ST_HTOT = 8,      // large-unit threshold: entries in the merge union's histogram
-  ST_PRE23 = 9,     // ... top 23 key bits fixed by level 2
+  ST_PRE23 = 9,     // ... the key bits fixed by level 2 (all but the last digit's)
   ST_NEED2 = 10,    // ... entries still needed from that level-2 bin
   ST_STAGE = 11,    // ... 2 while level 3 is still needed, else 0
   ST_WBASE = 12,    // merge: first fine key bin (key >> FINE_SHIFT) of the union's level-1 histogram window
+  ST_SHIFT = 14,    // block top-k and staged threshold: the level-1 bin is the keys k with k >> ST_SHIFT == ST_T1
   ST_WORDS = 16
 };
 

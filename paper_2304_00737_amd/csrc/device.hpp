@@ -33,6 +33,109 @@ __device__ __forceinline__ uint32_t hist_floor(uint32_t F) {
   return fb > HIST_MARGIN ? (fb - HIST_MARGIN) << D1_SHIFT : 0u;
 }
 
+// Level-1 bins of a block's histogram, given the word the fused add left in
+// spec_used for the block (its candidate floor F; SPEC_NONE: none).  With a
+// floor the histogram counts only keys at or above FH = hist_floor(F), two
+// binades lower: the keys in [FH, F) in bins of the top 12 key bits (bins 0
+// .. M_MARGIN - 1), the keys from F up -- the speculative candidates, a few
+// per cent of the block -- in bins of 2^FINE_SHIFT keys (1/256 binade, bins
+// M_MARGIN .. NB1 - 1, the last also holding every larger key), so that a
+// threshold bin among the candidates holds few entries while a tile still
+// touches few bins.  Bin order is key order throughout.  Without a floor (a
+// block's first step, or a histogram made without the add) every key counts
+// and a bin is the top 12 key bits.  The fused add, the lazy receipts that
+// keep its histograms exact and the level-1 select all bin through this map.
+constexpr uint32_t M_MARGIN = HIST_MARGIN;   // 12-bit bins below the candidate floor
+struct L1Map {
+  uint32_t floor;   // smallest key counted (FH)
+  uint32_t cand;    // the candidate floor F (fine bins from here)
+  bool fine;
+  __device__ __forceinline__ uint32_t bin(uint32_t key) const {
+    if (!fine) return key >> D1_SHIFT;
+    if (key < cand) return (key >> D1_SHIFT) - (floor >> D1_SHIFT);   // key >= floor
+    return M_MARGIN + min((key >> FINE_SHIFT) - (cand >> FINE_SHIFT), (uint32_t)NB1 - 1u - M_MARGIN);
+  }
+  // the keys of bin T: k >> *S == *pfx; false for the last fine bin, which
+  // also holds every larger key
+  __device__ __forceinline__ bool bin_keys(uint32_t T, uint32_t* pfx, uint32_t* S) const {
+    if (!fine) {
+      *pfx = T;
+      *S = D1_SHIFT;
+      return true;
+    }
+    if (T < M_MARGIN) {
+      *pfx = (floor >> D1_SHIFT) + T;
+      *S = D1_SHIFT;
+      return true;
+    }
+    *pfx = (cand >> FINE_SHIFT) + (T - M_MARGIN);
+    *S = FINE_SHIFT;
+    return T != (uint32_t)NB1 - 1u;
+  }
+};
+__device__ __forceinline__ L1Map l1_map(uint32_t used) {
+  L1Map m;
+  m.fine = used != SPEC_NONE;
+  m.cand = used & ~SPEC_DIRTY;
+  m.floor = hist_floor(used);
+  return m;
+}
+static_assert(HIST_MARGIN < (uint32_t)NB1 / 2, "the 12-bit margin bins leave most bins fine");
+
+// Levels 2 and 3 over the keys of one level-1 bin, the keys k with
+// k >> S == pfx (visit(f) calls f(key) for each of them), in two digits of
+// the low S bits, the last of S == FINE_SHIFT ? 7 : 8 bits; h holds at
+// least 2^(S - that) words.  Returns the threshold as (tge, teq, need_eq):
+// every key >= tge is selected, and the first need_eq (by index) with key
+// == teq.
+template <typename Visit>
+__device__ __forceinline__ void resolve_bin(uint32_t pfx, int S, uint32_t need1, uint32_t cnt1, uint32_t* h,
+                                            uint32_t* scratch, uint32_t* err, Visit visit, uint32_t& tge,
+                                            uint32_t& teq, uint32_t& need_eq) {
+  const int D3 = S == FINE_SHIFT ? 7 : 8;
+  const int nb2 = 1 << (S - D3), nb3 = 1 << D3;
+  tge = pfx << S;
+  teq = 0u;
+  need_eq = 0u;
+  if (need1 == cnt1) return;
+  __syncthreads();
+  for (int i = threadIdx.x; i < nb2; i += blockDim.x) h[i] = 0u;
+  __syncthreads();
+  visit([&](uint32_t key) { atomicAdd(&h[(key >> D3) & (uint32_t)(nb2 - 1)], 1u); });
+  __syncthreads();
+  uint32_t T2, above2, cnt2, ok;
+  block_select_desc(h, nb2, need1, scratch, &T2, &above2, &cnt2, &ok);
+  if (!ok) {
+    if (threadIdx.x == 0) atomicOr(err, ERR_COUNT_L23);
+    return;
+  }
+  const uint32_t need2 = need1 - above2;
+  const uint32_t pre = (pfx << (S - D3)) | T2;   // all but the last D3 key bits
+  tge = pre << D3;
+  if (need2 == cnt2) return;
+  for (int i = threadIdx.x; i < nb3; i += blockDim.x) h[i] = 0u;
+  __syncthreads();
+  visit([&](uint32_t key) {
+    if ((key >> D3) == pre) atomicAdd(&h[key & (uint32_t)(nb3 - 1)], 1u);
+  });
+  __syncthreads();
+  uint32_t T3, above3, cnt3;
+  block_select_desc(h, nb3, need2, scratch, &T3, &above3, &cnt3, &ok);
+  if (!ok) {
+    if (threadIdx.x == 0) atomicOr(err, ERR_COUNT_L23);
+    return;
+  }
+  const uint32_t need3 = need2 - above3;
+  const uint32_t T = (pre << D3) | T3;
+  if (need3 == cnt3) {
+    tge = T;
+  } else {
+    tge = T + 1u;
+    teq = T;
+    need_eq = need3;
+  }
+}
+
 // Levels 2 and 3 over the threshold-bin keys: visit(f) calls f(key) for
 // every entry in bin T1.  Returns the threshold as (tge, teq, need_eq).
 template <typename Visit>

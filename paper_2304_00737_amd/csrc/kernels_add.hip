@@ -39,8 +39,9 @@ __global__ __launch_bounds__(256) void k_fill(FillRanges r) {
 // is loaded non-temporally; A is re-read only by a fallback, so it is stored
 // non-temporally.
 //
-// With HIST, every sum's level-1 digit is counted in an LDS histogram that is
-// flushed (non-zero bins only) into one of the block's global copies, and the
+// With HIST, every sum's level-1 bin (L1Map in device.hpp) is counted in an
+// LDS histogram that is flushed (non-zero bins only) into one of the block's
+// global copies, and the
 // speculative candidates of the block top-k that follows are written: every
 // sum whose key is at or above a floor two level-1 bins below the block's
 // previous threshold bin (nothing on a block's first step), in index order at
@@ -120,7 +121,8 @@ __global__ __launch_bounds__(256) void k_residual_add4(float* __restrict__ acc, 
     F = T1p > SPEC_MARGIN ? (T1p - SPEC_MARGIN) << D1_SHIFT : 0u;
   }
   if (g == 0u && threadIdx.x == 0) sp.spec_used[wb] = F;
-  const uint32_t FH = hist_floor(F);
+  const L1Map M = l1_map(F);
+  const uint32_t FH = M.floor;
   __syncthreads();
   float r[8];
   uint32_t packed = 0;   // candidates of chunk 0 | chunk 1 << 16 (at most 1024 each)
@@ -140,7 +142,7 @@ __global__ __launch_bounds__(256) void k_residual_add4(float* __restrict__ acc, 
 #pragma unroll
       for (int c = 0; c < 4; ++c) {
         const uint32_t key = mag_key(r[4 * j + c]);
-        if (key >= FH) atomicAdd(&h[key >> D1_SHIFT], 1u);
+        if (key >= FH) atomicAdd(&h[M.bin(key)], 1u);
         packed += key >= F ? (1u << (16 * j)) : 0u;
       }
     } else {

@@ -23,10 +23,12 @@ namespace spardl {
 // The block's histogram is the sum of its HCOPIES copies; every load is in
 // flight before the first add.  The copies are cleared once read (the
 // workspace keeps its histograms at zero between steps).  A histogram of the
-// fused add covers keys at or above hist_floor(its candidate floor) (a bin
-// boundary), which decides the select exactly whenever the threshold bin lies
-// there; otherwise the workgroup rebuilds the block's full histogram from acc.
-// A full histogram must hold exactly the block's entries.
+// fused add covers keys at or above hist_floor(its candidate floor) in fine
+// bins (L1Map in device.hpp), which decides the select exactly whenever the
+// threshold bin lies inside that window; otherwise the workgroup rebuilds the
+// block's full histogram of the top 12 key bits from acc.  A full histogram
+// must hold exactly the block's entries.  The threshold bin goes to the state
+// as a key prefix and its shift (ST_T1, ST_SHIFT).
 __global__ __launch_bounds__(1024) void k_select1(uint32_t* __restrict__ hist1, uint32_t* __restrict__ state,
                                                   Blocks B, Units U, uint32_t need, uint32_t* __restrict__ spec_t1,
                                                   const uint32_t* __restrict__ spec_used, int spec,
@@ -55,13 +57,16 @@ __global__ __launch_bounds__(1024) void k_select1(uint32_t* __restrict__ hist1, 
     h[q * NT + threadIdx.x] = c;
   }
   const uint32_t used = spec ? spec_used[u] : SPEC_NONE;
-  const uint32_t FH = hist_floor(used);
+  const L1Map M = l1_map(used);
   __syncthreads();
   uint32_t T, above, cnt, ok, total;
   block_select_desc(h, NB1, need, scratch, &T, &above, &cnt, &ok, &total);
   const uint32_t s = B.start(b), e = B.start(b + 1u);
-  bool full = FH == 0u;
-  if (!ok && !full) {   // the threshold fell below the histogram's floor: count the whole block
+  bool full = !M.fine;   // the top-12-bit histogram of every key
+  uint32_t pfx = T, S = D1_SHIFT;   // the threshold bin: the keys k with k >> S == pfx
+  // the threshold fell below the histogram's floor, or above its fine window:
+  // count the whole block by its top 12 key bits
+  if (!full && (!ok || !M.bin_keys(T, &pfx, &S))) {
     for (int i = threadIdx.x; i < NB1; i += NT) h[i] = 0u;
     __syncthreads();
     const float* __restrict__ A = acc + (int64_t)w * ld_acc;
@@ -90,6 +95,8 @@ __global__ __launch_bounds__(1024) void k_select1(uint32_t* __restrict__ hist1, 
     __syncthreads();
     block_select_desc(h, NB1, need, scratch, &T, &above, &cnt, &ok, &total);
     full = true;
+    pfx = T;
+    S = D1_SHIFT;
   }
   if (threadIdx.x == 0) {
     uint32_t* st = state + u * ST_WORDS;
@@ -97,9 +104,10 @@ __global__ __launch_bounds__(1024) void k_select1(uint32_t* __restrict__ hist1, 
     if (!ok || (full ? total != len : total > len)) atomicOr(err, ERR_COUNT);
     // the fused add's speculative candidates hold every key >= its floor, so
     // they are usable when the floor is at or below the threshold bin
-    st[ST_SPECOK] = (spec && ok && used <= (T << D1_SHIFT)) ? 1u : 0u;
-    if (spec_t1) spec_t1[u] = ok ? T + 1u : 0u;
-    st[ST_T1] = T;
+    st[ST_SPECOK] = (spec && ok && used <= (pfx << S)) ? 1u : 0u;
+    if (spec_t1) spec_t1[u] = ok ? ((pfx << S) >> D1_SHIFT) + 1u : 0u;   // the next add's floor: 12-bit bins
+    st[ST_T1] = pfx;
+    st[ST_SHIFT] = S;
     st[ST_ABOVE1] = above;
     st[ST_NEED1] = ok ? need - above : 0u;
     st[ST_CNT1] = cnt;
@@ -175,7 +183,7 @@ struct CollectSmem {
 
 template <int VEC, bool FULL>
 __device__ __forceinline__ void collect_slot(const float* __restrict__ A, uint32_t nvalid, int32_t pos0,
-                                             const uint32_t* __restrict__ t1_word, CollectSmem& L,
+                                             const uint32_t* __restrict__ st, CollectSmem& L,
                                              uint32_t* cnt_out, uint32_t* nbin_out, int32_t* __restrict__ CI,
                                              float* __restrict__ CV, uint32_t* __restrict__ BK) {
   constexpr int PT = SLOT / 256;
@@ -198,9 +206,9 @@ __device__ __forceinline__ void collect_slot(const float* __restrict__ A, uint32
   }
   // the threshold bin is read only now, so its latency overlaps the data loads
   __builtin_amdgcn_sched_barrier(0);
-  const uint32_t T1 = *t1_word;
-  const uint32_t tlo = T1 << D1_SHIFT;
-  const uint32_t thi = tlo + (1u << D1_SHIFT);   // T1 < 4096, so this fits in 32 bits
+  const uint32_t S = st[ST_SHIFT];
+  const uint32_t tlo = st[ST_T1] << S;
+  const uint32_t thi = tlo + (1u << S);   // the bin's keys are below 2^31, so this fits in 32 bits
   uint32_t tc = 0, tb = 0;
 #pragma unroll
   for (int i = 0; i < PT; ++i) {
@@ -411,8 +419,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(SPW >= 8 ? 
   if constexpr (SPW == 1) {
     const uint32_t specok = st[ST_SPECOK];
     if (specok != 0u) {
-      const uint32_t T1 = st[ST_T1];
-      const uint32_t tlo = T1 << D1_SHIFT, thi = tlo + (1u << D1_SHIFT);
+      const uint32_t tlo = st[ST_T1] << st[ST_SHIFT], thi = tlo + (1u << st[ST_SHIFT]);
       const uint32_t slot = slot0 + (uint32_t)wave_id();
       if (slot >= smax || o + slot * (uint32_t)SLOT >= e) return;
       uint32_t t0, len0, len1;
@@ -448,9 +455,9 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(SPW >= 8 ? 
       }
     }
     const uint32_t specok = st[ST_SPECOK];
-    const uint32_t T1 = st[ST_T1];
+    const uint32_t pfx = st[ST_T1], S = st[ST_SHIFT];
     if (specok != 0u) {
-      const uint32_t tlo = T1 << D1_SHIFT, thi = tlo + (1u << D1_SHIFT);
+      const uint32_t tlo = pfx << S, thi = tlo + (1u << S);
       const int lane = lane_id();
       int32_t ix[SPW][R1];
       float vx[SPW][R1];
@@ -496,10 +503,10 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(SPW >= 8 ? 
     const int64_t cbase = (int64_t)w * B.n + t0;
     const int64_t si = (int64_t)unit * smax + slot;
     if (nvalid == (uint32_t)SLOT)
-      collect_slot<VEC, true>(A, nvalid, (int32_t)t0, st + ST_T1, L, slot_cnt + si, slot_nbin + si,
+      collect_slot<VEC, true>(A, nvalid, (int32_t)t0, st, L, slot_cnt + si, slot_nbin + si,
                               cand_idx + cbase, cand_val + cbase, bin_key + cbase);
     else
-      collect_slot<VEC, false>(A, nvalid, (int32_t)t0, st + ST_T1, L, slot_cnt + si, slot_nbin + si,
+      collect_slot<VEC, false>(A, nvalid, (int32_t)t0, st, L, slot_cnt + si, slot_nbin + si,
                                cand_idx + cbase, cand_val + cbase, bin_key + cbase);
   }
 }
@@ -625,7 +632,7 @@ __device__ __forceinline__ void visit_bin_chunk(const uint32_t* __restrict__ K, 
 __device__ __forceinline__ void thresh_fast_topk(FastSmem& L, int64_t unit, const SlotGeom& g, int32_t kb,
                                                  int32_t smax, const uint32_t* __restrict__ K,
                                                  const uint32_t* __restrict__ cnt, const uint32_t* __restrict__ nbn,
-                                                 uint32_t T1, uint32_t need1, uint32_t cnt1, uint32_t* st,
+                                                 uint32_t T1, uint32_t S, uint32_t need1, uint32_t cnt1, uint32_t* st,
                                                  uint32_t* __restrict__ pre_all, uint32_t* __restrict__ pre_ge,
                                                  uint32_t* __restrict__ pre_eq, uint32_t* err) {
   constexpr int NT = 1024, PS = FAST_SLOTS / NT;   // thread t owns slots PS t .. PS t + PS - 1
@@ -712,14 +719,14 @@ __device__ __forceinline__ void thresh_fast_topk(FastSmem& L, int64_t unit, cons
   auto visit = [&](auto fn) {
 #pragma unroll
     for (int r = 0; r < FAST_R0; ++r)
-      if ((rk[r] >> D1_SHIFT) == T1) fn(rk[r]);
+      if ((rk[r] >> S) == T1) fn(rk[r]);
     for (uint32_t c = 1; c < nchunks; ++c)
       visit_bin_chunk(K, L.pref, ns, g, c * FAST_CAP0, total, [&](uint32_t key, uint32_t) {
-        if ((key >> D1_SHIFT) == T1) fn(key);
+        if ((key >> S) == T1) fn(key);
       });
   };
   uint32_t tge, teq, need_eq;
-  resolve_low_digits(T1, need1, cnt1, L.u.c.h, L.scratch, err, visit, tge, teq, need_eq);
+  resolve_bin(T1, (int)S, need1, cnt1, L.u.c.h, L.scratch, err, visit, tge, teq, need_eq);
   for (int i = t; i < ns; i += NT) {
     L.u.c.cg[i] = 0u;
     L.u.c.ce[i] = 0u;
@@ -784,10 +791,10 @@ __global__ __launch_bounds__(1024) void k_thresh(Blocks B, Units U, int32_t kb, 
   const int64_t unit = (int64_t)U.canon((uint32_t)cunit, B.P);   // the unit's arrays
   uint32_t* st = state + unit * ST_WORDS;
   // level 1 was resolved by the level-1 select
-  const uint32_t T1 = st[ST_T1], need1 = st[ST_NEED1], cnt1 = st[ST_CNT1];
+  const uint32_t T1 = st[ST_T1], S1 = st[ST_SHIFT], need1 = st[ST_NEED1], cnt1 = st[ST_CNT1];
   if (g.nslots <= FAST_SLOTS) {
     thresh_fast_topk(S, unit, g, kb, smax, bin_key + g.base, slot_cnt + unit * smax, slot_nbin + unit * smax, T1,
-                     need1, cnt1, st, pre_all, pre_ge, pre_eq, err);
+                     S1, need1, cnt1, st, pre_all, pre_ge, pre_eq, err);
     return;
   }
   if (threadIdx.x == 0) atomicOr(err, ERR_COUNT);   // longer units are routed to the staged threshold
@@ -849,57 +856,6 @@ __device__ __forceinline__ void mt_each(const f4v* __restrict__ V4, const uint32
 #pragma unroll
       for (int q = 0; q < 4; ++q)
         if ((uint32_t)(4 * threadIdx.x + q) < c[r]) f(mag_key(v[r][q]), (uint32_t)(s0 + r));
-  }
-}
-
-// Levels 2 and 3 over the keys of one bin, k >> S == pfx (visit(f) calls
-// f(key) for each of them): the low S bits in two digits, the last of D3
-// bits.  Returns the threshold as (tge, teq, need_eq).
-template <typename Visit>
-__device__ __forceinline__ void resolve_bin(uint32_t pfx, int S, uint32_t need1, uint32_t cnt1, uint32_t* h,
-                                            uint32_t* scratch, uint32_t* err, Visit visit, uint32_t& tge,
-                                            uint32_t& teq, uint32_t& need_eq) {
-  const int D3 = S == FINE_SHIFT ? 7 : 8;
-  const int nb2 = 1 << (S - D3), nb3 = 1 << D3;
-  tge = pfx << S;
-  teq = 0u;
-  need_eq = 0u;
-  if (need1 == cnt1) return;
-  __syncthreads();
-  for (int i = threadIdx.x; i < nb2; i += MT_THREADS) h[i] = 0u;
-  __syncthreads();
-  visit([&](uint32_t key) { atomicAdd(&h[(key >> D3) & (uint32_t)(nb2 - 1)], 1u); });
-  __syncthreads();
-  uint32_t T2, above2, cnt2, ok;
-  block_select_desc(h, nb2, need1, scratch, &T2, &above2, &cnt2, &ok);
-  if (!ok) {
-    if (threadIdx.x == 0) atomicOr(err, ERR_COUNT_L23);
-    return;
-  }
-  const uint32_t need2 = need1 - above2;
-  const uint32_t pre = (pfx << (S - D3)) | T2;   // all but the last D3 key bits
-  tge = pre << D3;
-  if (need2 == cnt2) return;
-  for (int i = threadIdx.x; i < nb3; i += MT_THREADS) h[i] = 0u;
-  __syncthreads();
-  visit([&](uint32_t key) {
-    if ((key >> D3) == pre) atomicAdd(&h[key & (uint32_t)(nb3 - 1)], 1u);
-  });
-  __syncthreads();
-  uint32_t T3, above3, cnt3;
-  block_select_desc(h, nb3, need2, scratch, &T3, &above3, &cnt3, &ok);
-  if (!ok) {
-    if (threadIdx.x == 0) atomicOr(err, ERR_COUNT_L23);
-    return;
-  }
-  const uint32_t need3 = need2 - above3;
-  const uint32_t T = (pre << D3) | T3;
-  if (need3 == cnt3) {
-    tge = T;
-  } else {
-    tge = T + 1u;
-    teq = T;
-    need_eq = need3;
   }
 }
 
@@ -1148,7 +1104,7 @@ __device__ __forceinline__ void visit_bin_slots_topk(const SlotGeom& g, int32_t 
 template <typename F>
 __device__ __forceinline__ void visit_bin_slots_merge(const SlotGeom& g, int32_t s0, int32_t s1,
                                                       const float* __restrict__ V, const uint32_t* __restrict__ cnt,
-                                                      uint32_t T1, F f) {
+                                                      uint32_t T1, uint32_t S, F f) {
   for (int32_t slot = s0; slot < s1; ++slot) {
     const uint32_t c = min(cnt[slot], (uint32_t)g.ss);
     const float* __restrict__ Vs = V + g.off(slot);
@@ -1162,7 +1118,7 @@ __device__ __forceinline__ void visit_bin_slots_merge(const SlotGeom& g, int32_t
 #pragma unroll
       for (int r = 0; r < BIG_R1; ++r) {
         const uint32_t key = mag_key(v[r]);
-        if (j0 + (uint32_t)(r * BIG_THREADS) + threadIdx.x < c && (key >> D1_SHIFT) == T1) f(key, slot);
+        if (j0 + (uint32_t)(r * BIG_THREADS) + threadIdx.x < c && (key >> S) == T1) f(key, slot);
       }
     }
   }
@@ -1207,23 +1163,29 @@ __global__ __launch_bounds__(1024) void k_big_level1(BigArgs a) {
     uint32_t* st = a.state + ua * ST_WORDS;
     if (!ok) atomicOr(a.err, ERR_COUNT);
     st[ST_T1] = T1;
+    st[ST_SHIFT] = D1_SHIFT;
     st[ST_NEED1] = ok ? (uint32_t)a.kb - above1 : 0u;
     st[ST_CNT1] = cnt1;
     st[ST_HTOT] = total;
   }
 }
 
-// LEVEL 2: histogram of key bits 8..18 of the bin-T1 keys; LEVEL 3: of bits
-// 0..7 of the keys whose top 23 bits are ST_PRE23
+// The level-1 bin is the keys k with k >> S == ST_T1 (S = ST_SHIFT); its last
+// S bits are resolved in two digits, the last of D3 = (S == FINE_SHIFT ? 7 : 8)
+// bits.  LEVEL 2: histogram of the first digit of the bin's keys; LEVEL 3: of
+// the last digit of the keys whose other bits are ST_PRE23.
+__device__ __forceinline__ int digit3_bits(uint32_t S) { return S == (uint32_t)FINE_SHIFT ? 7 : 8; }
 template <int mode, int LEVEL>
 __global__ __launch_bounds__(256) void k_big_hist(BigArgs a, uint32_t ngroups) {
-  constexpr int NB = LEVEL == 2 ? NB2 : NB3;
+  constexpr int NB = LEVEL == 2 ? NB2 : NB3;   // the most bins either digit has
   __shared__ uint32_t h[NB];
   const int64_t unit = blockIdx.x / ngroups;
   const int64_t ua = big_unit(a, unit);
   const int32_t grp = (int32_t)(blockIdx.x % ngroups);
   const uint32_t* st = a.state + ua * ST_WORDS;
-  const uint32_t T1 = st[ST_T1];
+  const uint32_t T1 = st[ST_T1], S = st[ST_SHIFT];
+  const int D3 = digit3_bits(S);
+  const uint32_t m2 = (1u << (S - (uint32_t)D3)) - 1u, m3 = (1u << D3) - 1u;
   if (LEVEL == 2 ? st[ST_NEED1] == st[ST_CNT1] : st[ST_STAGE] != 2u) return;   // uniform: resolved already
   const uint32_t pre23 = st[ST_PRE23];
   const SlotGeom g = slot_geom(mode, (uint32_t)unit, a.B, a.U, a.kb);
@@ -1231,8 +1193,8 @@ __global__ __launch_bounds__(256) void k_big_hist(BigArgs a, uint32_t ngroups) {
   if (s0 >= s1) return;
   for (int i = threadIdx.x; i < NB; i += blockDim.x) h[i] = 0u;
   auto bump = [&](uint32_t key, int32_t) {
-    if (LEVEL == 2) atomicAdd(&h[(key >> D2_SHIFT) & (NB2 - 1)], 1u);
-    else if ((key >> D2_SHIFT) == pre23) atomicAdd(&h[key & (NB3 - 1)], 1u);
+    if (LEVEL == 2) atomicAdd(&h[(key >> D3) & m2], 1u);
+    else if ((key >> D3) == pre23) atomicAdd(&h[key & m3], 1u);
   };
   if (mode == 0 && a.group == BIG_GROUP0_MANY) {
     __shared__ uint32_t pref[BIG_THREADS];
@@ -1248,7 +1210,7 @@ __global__ __launch_bounds__(256) void k_big_hist(BigArgs a, uint32_t ngroups) {
     visit_bin_slots_topk(g, s0, s1, a.bin_key + g.base, a.slot_nbin + ua * a.smax, bump);
   } else {
     __syncthreads();
-    visit_bin_slots_merge(g, s0, s1, a.U_val + g.base, a.slot_cnt + ua * a.smax, T1, bump);
+    visit_bin_slots_merge(g, s0, s1, a.U_val + g.base, a.slot_cnt + ua * a.smax, T1, S, bump);
   }
   __syncthreads();
   uint32_t* H = a.hist1 + ua * a.hstride + (LEVEL == 2 ? 0 : NB2);
@@ -1266,10 +1228,12 @@ __global__ __launch_bounds__(1024) void k_big_select(BigArgs a) {
   const int64_t unit = blockIdx.x;
   const int64_t ua = big_unit(a, unit);
   uint32_t* st = a.state + ua * ST_WORDS;
-  const uint32_t T1 = st[ST_T1], need1 = st[ST_NEED1], cnt1 = st[ST_CNT1];
+  const uint32_t T1 = st[ST_T1], S = st[ST_SHIFT], need1 = st[ST_NEED1], cnt1 = st[ST_CNT1];
+  const int D3 = digit3_bits(S);
+  const int nb = LEVEL == 2 ? 1 << (S - (uint32_t)D3) : 1 << D3;
   if (LEVEL == 2 && need1 == cnt1) {   // the whole bin is selected
     if (threadIdx.x == 0) {
-      st[ST_TGE] = T1 << D1_SHIFT;
+      st[ST_TGE] = T1 << S;
       st[ST_TEQ] = 0u;
       st[ST_NEEDEQ] = 0u;
       st[ST_STAGE] = 0u;
@@ -1285,20 +1249,20 @@ __global__ __launch_bounds__(1024) void k_big_select(BigArgs a) {
   __syncthreads();
   const uint32_t need = LEVEL == 2 ? need1 : st[ST_NEED2];
   uint32_t T, above, cnt, ok;
-  block_select_desc(h, NB, need, scratch, &T, &above, &cnt, &ok);
+  block_select_desc(h, nb, need, scratch, &T, &above, &cnt, &ok);
   if (threadIdx.x != 0) return;
   if (!ok) atomicOr(a.err, ERR_COUNT_L23);
   const uint32_t rest = need - above;
   if (LEVEL == 2) {
-    const uint32_t pre23 = (T1 << (D1_SHIFT - D2_SHIFT)) | T;
-    st[ST_TGE] = pre23 << D2_SHIFT;
+    const uint32_t pre23 = (T1 << (S - (uint32_t)D3)) | T;
+    st[ST_TGE] = pre23 << D3;
     st[ST_TEQ] = 0u;
     st[ST_NEEDEQ] = 0u;
     st[ST_PRE23] = pre23;
     st[ST_NEED2] = rest;
     st[ST_STAGE] = (ok && rest != cnt) ? 2u : 0u;
   } else {
-    const uint32_t key = (st[ST_PRE23] << D2_SHIFT) | T;
+    const uint32_t key = (st[ST_PRE23] << D3) | T;
     if (rest == cnt) {
       st[ST_TGE] = key;
     } else {

@@ -436,7 +436,8 @@ __global__ __launch_bounds__(256) void k_lazy_step(float* __restrict__ acc, int6
     float* __restrict__ A = acc + (int64_t)r * ld_acc;
     if constexpr (HIST) {
       const int64_t cu = (int64_t)r * B.P + b;   // the receiver block's arrays
-      const uint32_t FH = hist_floor(spec_used[cu]);
+      const L1Map M = l1_map(spec_used[cu]);   // the add's bins
+      const uint32_t FH = M.floor;
       const uint32_t j0 = blockIdx.x * LAZY_CHUNK;
       if (j0 >= kb) continue;
       if (blockIdx.x == 0 && threadIdx.x == 0) atomicOr(&spec_used[cu], SPEC_DIRTY);
@@ -472,8 +473,8 @@ __global__ __launch_bounds__(256) void k_lazy_step(float* __restrict__ acc, int6
         saved[o + j] = old;
         A[xs[q]] = nv;
         const uint32_t k0 = mag_key(old), k1 = mag_key(nv);
-        if (k0 >= FH) atomicSub(&dh[k0 >> D1_SHIFT], 1u);
-        if (k1 >= FH) atomicAdd(&dh[k1 >> D1_SHIFT], 1u);
+        if (k0 >= FH) atomicSub(&dh[M.bin(k0)], 1u);
+        if (k1 >= FH) atomicAdd(&dh[M.bin(k1)], 1u);
       }
       __syncthreads();
       uint32_t* __restrict__ H = hist1 + (cu * HCOPIES + (blockIdx.x % HCOPIES)) * NB1;
