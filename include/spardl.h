@@ -326,7 +326,8 @@ int spardl_lazy_residual_collect(float* acc, int64_t ld_acc, int32_t P, int64_t 
  *   spardl_rsag_merge_topk(t);
  * then the final blocks are sp[q][q], q < Q (any team): decode them with
  * spardl_allgather_densify(sp, P = Q, ..., member) and collect residuals per
- * team with spardl_residual_collect(..., member), then
+ * team with spardl_residual_collect(..., member) (or all teams at once with
+ * spardl_team_residual_collect), then
  * spardl_rsag_residual(..., member).  sp below is the whole P x Q x k_blk
  * array (row w = worker w, Q blocks per row).
  * ------------------------------------------------------------------------- */
@@ -362,6 +363,20 @@ int spardl_team_block_topk(const float* acc, int64_t ld_acc, int32_t P, int32_t 
 int spardl_team_merge_topk(int32_t* sp_idx, float* sp_val, int32_t P, int32_t d, int64_t n, int32_t k_blk,
                            int32_t round, int32_t* drop_idx, float* drop_val, int32_t* drop_cnt, void* ws,
                            size_t ws_bytes, hipStream_t stream);
+
+/* spardl_residual_collect(..., member) for all P rows at once (Sec. III-C,
+ * global residual collection inside every team): worker w's residual keeps
+ * what it selected or dropped at the team's SRS steps minus the final
+ * indices.  local_idx as written by spardl_team_block_topk; member the
+ * bitmap spardl_allgather_densify wrote (required); drop_idx / drop_val /
+ * drop_cnt HOST arrays of ceil(log2 Q) DEVICE pointers, element i-1 = the
+ * buffers of spardl_team_merge_topk round i (may be NULL when Q = 1).  No
+ * workspace.  Errors: EINVAL for NULL acc/local_idx/member or a NULL drop
+ * pointer, misaligned member, invalid sizes (as for the team workspace),
+ * ld_acc < n. */
+int spardl_team_residual_collect(float* acc, int64_t ld_acc, int32_t P, int32_t d, int64_t n, int32_t k_blk,
+                                 const int32_t* local_idx, const uint32_t* member, const int32_t* const* drop_idx,
+                                 const float* const* drop_val, const int32_t* const* drop_cnt, hipStream_t stream);
 
 /* Workspace of spardl_rsag_merge_topk (separate from the teams' workspaces):
  * 256-byte aligned device memory of this many bytes, prepared once by

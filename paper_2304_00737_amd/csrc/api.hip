@@ -537,7 +537,7 @@ int spardl_residual_collect(float* acc, int64_t ld_acc, int32_t P, int64_t n, in
     SPARDL_TRY(launch_bm_mark(sp_idx, P, n, k_blk, bm, true, stream));
   }
   const uint32_t* in_I = member ? member : bm;
-  SPARDL_TRY(launch_grc_zero(acc, ld_acc, P, n, k_blk, local_idx, in_I, stream));
+  SPARDL_TRY(launch_grc_zero(acc, ld_acc, P, P, n, k_blk, local_idx, in_I, stream));
   for (int32_t i = 1; i <= l; ++i) {
     const int32_t m = bag_of(P, l, i);
     SPARDL_TRY(launch_grc_drops(acc, ld_acc, n, m, k_blk, P * m, drop_idx[i - 1], drop_val[i - 1],
@@ -599,7 +599,7 @@ int spardl_lazy_residual_collect(float* acc, int64_t ld_acc, int32_t P, int64_t 
   const int32_t l = steps_of(P);
   if (l > 0 && !saved) return SPARDL_EINVAL;
   // selected and final -> 0 (every (w, b) pair of sp is a selection of worker w)
-  SPARDL_TRY(launch_grc_zero(acc, ld_acc, P, n, k_blk, sp_idx, member, stream));
+  SPARDL_TRY(launch_grc_zero(acc, ld_acc, P, P, n, k_blk, sp_idx, member, stream));
   // received and not final -> the value before the first receipt
   for (int32_t i = l; i >= 1; --i)
     SPARDL_TRY(launch_lazy_step(acc, ld_acc, P, n, k_blk, 1 << (l - i), bag_of(P, l, i), sp_idx, nullptr,
@@ -825,6 +825,26 @@ int spardl_team_merge_topk(int32_t* sp_idx, float* sp_val, int32_t P, int32_t d,
   SPARDL_TRY(launch_emit(1, w.cand_idx, w.cand_val, pairs, all_blocks(Q), n, Q, k_blk, PM, smax, w.state,
                          w.slot_cnt, w.pre_all, w.pre_ge, w.pre_eq, sp_idx, sp_val, nullptr, drop_idx, drop_val,
                          w.err, stream));
+  return SPARDL_OK;
+}
+
+int spardl_team_residual_collect(float* acc, int64_t ld_acc, int32_t P, int32_t d, int64_t n, int32_t k_blk,
+                                 const int32_t* local_idx, const uint32_t* member, const int32_t* const* drop_idx,
+                                 const float* const* drop_val, const int32_t* const* drop_cnt, hipStream_t stream) {
+  if (!acc || !local_idx || !member || (reinterpret_cast<uintptr_t>(member) & 3u) || !team_sizes_ok(P, d, n, k_blk) ||
+      ld_acc < n)
+    return SPARDL_EINVAL;
+  const int32_t Q = P / d;
+  const int32_t l = steps_of(Q);
+  if (l > 0 && (!drop_idx || !drop_val || !drop_cnt)) return SPARDL_EINVAL;
+  for (int32_t i = 0; i < l; ++i)
+    if (!drop_idx[i] || !drop_val[i] || !drop_cnt[i]) return SPARDL_EINVAL;
+  SPARDL_TRY(launch_grc_zero(acc, ld_acc, P, Q, n, k_blk, local_idx, member, stream));
+  for (int32_t i = 1; i <= l; ++i) {
+    const int32_t m = bag_of(Q, l, i);
+    SPARDL_TRY(launch_grc_drops(acc, ld_acc, n, m, k_blk, P * m, drop_idx[i - 1], drop_val[i - 1], drop_cnt[i - 1],
+                                member, stream));
+  }
   return SPARDL_OK;
 }
 

@@ -36,14 +36,16 @@ constexpr int HCOPIES = 4;                       // level-1 histogram copies per
 // keeps half its entries, whose keys crowd just above the blocks' own
 // thresholds: a level-1 bin of 2^D1_SHIFT keys (1/16 binade) can hold half
 // the union.  Unions of up to MT_SLOTS slots therefore take a finer level 1:
-// NB1 bins of 2^FINE_SHIFT keys (1/256 binade), a window starting FINE_BELOW
-// bins (4 binades) below the larger of the two blocks' smallest sampled keys;
-// keys outside the window are counted in its first or last bin.  If the
-// threshold falls in one of those two bins the threshold kernel builds the
-// 2^D1_SHIFT-key histogram itself (exact either way).
+// NB1 bins of 2^FINE_SHIFT keys (1/256 binade, a window of 16 binades)
+// centred on the two blocks' median keys, each the median of the block's
+// leading FINE_SAMPLE entries (the union keeps its larger half, so its
+// threshold lies near them; a median is not moved by a few entries that
+// nearly cancelled); keys outside the window are counted in its first or
+// last bin.  If the threshold falls in one of those two bins the threshold
+// kernel builds the 2^D1_SHIFT-key histogram itself (exact either way).
 constexpr int MT_SLOTS = 1024;                   // merge slots per unit of the one-workgroup merge threshold
 constexpr int FINE_SHIFT = 15;
-constexpr uint32_t FINE_BELOW = 1024;
+constexpr uint32_t FINE_BELOW = NB1 / 2;        // fine bins from the window's first to its centre (8 binades)
 constexpr int FINE_SAMPLE = 256;                 // leading entries of each block sampled for the window
 __host__ __device__ __forceinline__ bool merge_fine(int64_t kb) { return 2 * kb <= (int64_t)MT_SLOTS * MERGE_TILE; }
 

@@ -84,11 +84,11 @@ __global__ __launch_bounds__(256) void k_bm_mark(const int32_t* __restrict__ sp_
 
 // acc[w][x] = 0 where worker w selected x locally and x is a final index.
 // Grid: x over the worker's P k_blk local indices, y over workers.
-__global__ __launch_bounds__(256) void k_grc_zero(float* __restrict__ acc, int64_t ld_acc, uint32_t P, uint32_t n,
-                                                  uint32_t kb, const int32_t* __restrict__ local_idx,
+__global__ __launch_bounds__(256) void k_grc_zero(float* __restrict__ acc, int64_t ld_acc, uint32_t nw, uint32_t Q,
+                                                  uint32_t n, uint32_t kb, const int32_t* __restrict__ local_idx,
                                                   const uint32_t* __restrict__ bm) {
-  const uint32_t per_w = P * kb;   // <= n < 2^31
-  for (uint32_t w = blockIdx.y; w < P; w += gridDim.y) {
+  const uint32_t per_w = Q * kb;   // <= n < 2^31
+  for (uint32_t w = blockIdx.y; w < nw; w += gridDim.y) {
     const int32_t* __restrict__ L = local_idx + (int64_t)w * per_w;
     float* __restrict__ A = acc + (int64_t)w * ld_acc;
     for (uint32_t i = blockIdx.x * 256u + threadIdx.x; i < per_w; i += gridDim.x * 256u) {
@@ -168,10 +168,11 @@ hipError_t launch_bm_mark(const int32_t* sp_idx, int32_t P, int64_t n, int32_t k
   return hipGetLastError();
 }
 
-hipError_t launch_grc_zero(float* acc, int64_t ld_acc, int32_t P, int64_t n, int32_t kb, const int32_t* local_idx,
-                           const uint32_t* bm, hipStream_t s) {
-  const dim3 grid(grid_for((int64_t)P * kb, 256, 1024), (unsigned)std::min<int32_t>(P, 65535));
-  hipLaunchKernelGGL(k_grc_zero, grid, dim3(256), 0, s, acc, ld_acc, (uint32_t)P, (uint32_t)n, (uint32_t)kb, local_idx, bm);
+hipError_t launch_grc_zero(float* acc, int64_t ld_acc, int32_t nw, int32_t Q, int64_t n, int32_t kb,
+                           const int32_t* local_idx, const uint32_t* bm, hipStream_t s) {
+  const dim3 grid(grid_for((int64_t)Q * kb, 256, 1024), (unsigned)std::min<int32_t>(nw, 65535));
+  hipLaunchKernelGGL(k_grc_zero, grid, dim3(256), 0, s, acc, ld_acc, (uint32_t)nw, (uint32_t)Q, (uint32_t)n,
+                     (uint32_t)kb, local_idx, bm);
   return hipGetLastError();
 }
 

@@ -25,7 +25,7 @@ namespace spardl {
 // entries; a probe per lane, no barrier), and resolved exactly in LDS after
 // the tile's entries and the brackets' slack have been loaded there in one
 // round of coalesced loads.  Meanwhile the other waves read the leading
-// FINE_SAMPLE entries of both blocks, whose smallest keys place the fine
+// FINE_SAMPLE entries of both blocks, whose median keys place the fine
 // level-1 window (FINE; see merge_fine in common.hpp); every tile of a pair
 // reads the same entries, so all of them use the same window.
 constexpr int MERGE_PROBES = WAVE;                 // probes per search round (a lane each)
@@ -70,7 +70,7 @@ __global__ __launch_bounds__(MERGE_THREADS) void k_merge(
   __shared__ __align__(16) uint32_t hist[NB1];
   __shared__ uint32_t scratch[2 * (MERGE_THREADS / WAVE) + 1];
   __shared__ int32_t brk[4];
-  __shared__ uint32_t smin[2];
+  __shared__ uint32_t smin[2];   // the two blocks' median keys (reused as a flag below)
   const uint32_t pair = blockIdx.x / (uint32_t)tiles_per_pair;
   const int32_t tile = (int32_t)(blockIdx.x % (uint32_t)tiles_per_pair);
   int64_t hb, rb;
@@ -96,28 +96,37 @@ __global__ __launch_bounds__(MERGE_THREADS) void k_merge(
       brk[2 * wv] = lo;
       brk[2 * wv + 1] = hi;
     }
-  } else if (FINE) {
-    // smallest key among the leading entries of the held (wave 2) or received (wave 3) block
+  } else if (FINE && wv < 4) {
+    // the median key among the leading entries of the held (wave 2) or received (wave 3)
+    // block: the largest T with at least half of them >= T, found bit by bit
     const float* __restrict__ V = wv == 2 ? Hv : Rv;
-    float v[FINE_SAMPLE / WAVE];
+    constexpr int U = FINE_SAMPLE / WAVE;
+    uint32_t key[U];
+    bool ok[U];
 #pragma unroll
-    for (int u = 0; u < FINE_SAMPLE / WAVE; ++u) {
+    for (int u = 0; u < U; ++u) {
       const int32_t j = u * WAVE + lane;
-      v[u] = j < kb ? V[j] : __uint_as_float(0x7F7FFFFFu);
+      ok[u] = j < kb;
+      key[u] = ok[u] ? mag_key(V[j]) : 0u;
     }
-    uint32_t m = 0x7FFFFFFFu;
+    const uint32_t half = ((uint32_t)min(kb, FINE_SAMPLE) + 1u) / 2u;
+    uint32_t T = 0;
+    for (int bit = 30; bit >= 0; --bit) {
+      const uint32_t c = T | (1u << bit);
+      uint32_t nge = 0;
 #pragma unroll
-    for (int u = 0; u < FINE_SAMPLE / WAVE; ++u) m = min(m, mag_key(v[u]));
-#pragma unroll
-    for (int d = WAVE / 2; d > 0; d >>= 1) m = min(m, (uint32_t)__shfl_xor((int)m, d, WAVE));
-    if (lane == 0 && wv < 4) smin[wv - 2] = m;
+      for (int u = 0; u < U; ++u) nge += popc64(__ballot(ok[u] && key[u] >= c));
+      if (nge >= half) T = c;
+    }
+    if (lane == 0) smin[wv - 2] = T;
   }
   __syncthreads();
   const int32_t lo0 = brk[0], hi0 = brk[1], lo1 = brk[2], hi1 = brk[3];
   uint32_t wbase = 0;
   if (FINE) {
-    const uint32_t top = max(smin[0], smin[1]) >> FINE_SHIFT;
-    wbase = top > FINE_BELOW ? top - FINE_BELOW : 0u;
+    // the window's centre: the mean of the two median keys (the geometric mean of the values)
+    const uint32_t mid = ((smin[0] >> 1) + (smin[1] >> 1)) >> FINE_SHIFT;
+    wbase = mid > FINE_BELOW ? mid - FINE_BELOW : 0u;
     if (tile == 0 && threadIdx.x == 0) state[(int64_t)pair * ST_WORDS + ST_WBASE] = wbase;
   }
   // the LDS window: held [ha, hz) and received [ra, rz) cover both brackets'

@@ -59,8 +59,8 @@ hipError_t launch_densify(const int32_t* sp_idx, const float* sp_val, int32_t P,
                           float* dense, uint32_t* member, bool vec4, hipStream_t s);
 hipError_t launch_bm_mark(const int32_t* sp_idx, int32_t P, int64_t n, int32_t kb, uint32_t* bm, bool set,
                           hipStream_t s);
-hipError_t launch_grc_zero(float* acc, int64_t ld_acc, int32_t P, int64_t n, int32_t kb, const int32_t* local_idx,
-                           const uint32_t* bm, hipStream_t s);
+hipError_t launch_grc_zero(float* acc, int64_t ld_acc, int32_t nw, int32_t Q, int64_t n, int32_t kb,
+                           const int32_t* local_idx, const uint32_t* bm, hipStream_t s);
 hipError_t launch_grc_sag_drops(float* acc, int64_t ld_acc, int64_t n, int32_t Q, int32_t t, int32_t kb,
                                 int32_t npairs, const int32_t* drop_idx, const float* drop_val,
                                 const int32_t* drop_cnt, const uint32_t* bm, hipStream_t s);

@@ -57,6 +57,7 @@ _lib.spardl_team_workspace_init.argtypes = [_i32, _i32, _i64, _i32, _p, _sz, _p]
 _lib.spardl_team_residual_add.argtypes = [_p, _i64, _p, _i64, _i32, _i32, _i64, _i32, _p, _sz, _p]
 _lib.spardl_team_block_topk.argtypes = [_p, _i64, _i32, _i32, _i64, _i32, _i32, _p, _p, _p, _p, _sz, _p]
 _lib.spardl_team_merge_topk.argtypes = [_p, _p, _i32, _i32, _i64, _i32, _i32, _p, _p, _p, _p, _sz, _p]
+_lib.spardl_team_residual_collect.argtypes = [_p, _i64, _i32, _i32, _i64, _i32, _p, _p, _p, _p, _p, _p]
 _lib.spardl_bsag_workspace_bytes.argtypes = [_i32, _i32, _i64, _i32]
 _lib.spardl_bsag_workspace_bytes.restype = _sz
 _lib.spardl_bsag_workspace_init.argtypes = [_i32, _i32, _i64, _i32, _p, _sz, _p]
@@ -65,7 +66,7 @@ _lib.spardl_bsag_residual.argtypes = [_p, _i64, _i32, _i32, _i64, _i32, _p, _p, 
 for _f in ("residual_add", "block_topk", "sparse_merge_topk", "sparse_merge_topk_noalloc", "allgather_densify", "residual_collect",
            "lazy_topk", "lazy_receive", "lazy_residual_collect", "rsag_workspace_init", "rsag_merge_topk",
            "rsag_residual", "bsag_workspace_init", "bsag_exchange", "bsag_residual", "team_workspace_init",
-           "team_residual_add", "team_block_topk", "team_merge_topk"):
+           "team_residual_add", "team_block_topk", "team_merge_topk", "team_residual_collect"):
     getattr(_lib, "spardl_" + _f).restype = ctypes.c_int
 
 
@@ -277,6 +278,17 @@ def team_merge_topk(sp_idx, sp_val, P: int, d: int, n: int, k_blk: int, round: i
     _check("team_merge_topk", _lib.spardl_team_merge_topk(_ptr(sp_idx), _ptr(sp_val), P, d, n, k_blk, round,
                                                           _ptr(drop_idx), _ptr(drop_val), _ptr(drop_cnt), _ptr(ws),
                                                           _nb(ws), _stream(stream)))
+
+
+def team_residual_collect(acc, P: int, d: int, n: int, k_blk: int, local_idx, member, drop_idx, drop_val, drop_cnt,
+                          *, ld_acc=None, stream=None) -> None:
+    """drop_*: sequences of ceil(log2(P / d)) tensors (the team_merge_topk buffers, one per round)."""
+    ld_acc = _ld(acc, n) if ld_acc is None else ld_acc
+    l = len(drop_idx)
+    arr = lambda ts: (ctypes.c_void_p * max(l, 1))(*[_ptr(t) for t in ts]) if l else None
+    _check("team_residual_collect", _lib.spardl_team_residual_collect(
+        _ptr(acc), ld_acc, P, d, n, k_blk, _ptr(local_idx), _ptr(member), arr(drop_idx), arr(drop_val),
+        arr(drop_cnt), _stream(stream)))
 
 
 def bsag_workspace(P: int, d: int, n: int, k_blk: int, device="cuda", *, stream=None):
@@ -641,11 +653,15 @@ class SparDLSagStep(_Checkpoint):
                           stream=stream)
 
     def collect(self, stream=None):
-        for tau in range(self.d):
-            r = self._rows(tau)
-            residual_collect(self.acc[r], self.Q, self.n, self.k_blk, self.local_idx[r], self.sp_idx[r],
-                             [t[r] for t in self.drop_idx], [t[r] for t in self.drop_val],
-                             [t[r] for t in self.drop_cnt], None, self.member, stream=stream)
+        if self.batched:
+            team_residual_collect(self.acc, self.P, self.d, self.n, self.k_blk, self.local_idx, self.member,
+                                  self.drop_idx, self.drop_val, self.drop_cnt, stream=stream)
+        else:
+            for tau in range(self.d):
+                r = self._rows(tau)
+                residual_collect(self.acc[r], self.Q, self.n, self.k_blk, self.local_idx[r], self.sp_idx[r],
+                                 [t[r] for t in self.drop_idx], [t[r] for t in self.drop_val],
+                                 [t[r] for t in self.drop_cnt], None, self.member, stream=stream)
         if self.bruck:
             bsag_residual(self.acc, self.P, self.d, self.n, self.k_blk, self.member, self.toph_idx, self.toph_val,
                           self.toph_cnt, stream=stream)

@@ -242,6 +242,14 @@ def test_argument_errors_enqueue_nothing():
                                       null) == EINVAL
     assert lib.spardl_team_residual_add(p, i64(1199), p, i64(1200), i32(12), i32(4), i64(1200), i32(5), p, big,
                                         null) == EINVAL
+    # team residual collect (Q = 3: two rounds of drops): member required and aligned, every drop pointer, d | P
+    tc = lambda d_, mem, a: lib.spardl_team_residual_collect(p, i64(1200), i32(12), i32(d_), i64(1200), i32(5), p,
+                                                             mem, a, a, a, null)
+    assert tc(4, null, ok3) == EINVAL
+    assert tc(4, ctypes.c_void_p(0x1002), ok3) == EINVAL
+    assert tc(4, p, arr) == EINVAL
+    assert tc(4, p, null) == EINVAL
+    assert tc(5, p, ok3) == EINVAL
     # the workspace-free SRS step: NULL err, P < 2, round out of range; a step whose scratch exceeds the
     # library's static array is refused before any GPU call (P = 32, k_blk = 46875: 512 pairs of 23 slots)
     na = lambda P_, n_, kb_, rnd, err: lib.spardl_sparse_merge_topk_noalloc(p, p, i32(P_), i64(n_), i32(kb_), i32(rnd),
