@@ -164,6 +164,10 @@ def main() -> int:
                     help="with --teams d: join the teams by B-SAG (any d dividing P; Algorithm 2 sets h)")
     ap.add_argument("--rows-per-call", type=int, default=0,
                     help="workload 5: workers per residual-add / block top-k call (default PER_WORKER_ROWS)")
+    ap.add_argument("--separate-collect", action="store_true",
+                    help="eager variant: run the global residual collection as its own call at the end of "
+                         "each step (by default it runs inside the next step's residual add, which reads "
+                         "and writes every element of the residual anyway)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-extra", action="store_true",
                     help="skip the GPT-2-XL-sized and HIP-graph sub-objects of the default run")
@@ -255,7 +259,7 @@ def main() -> int:
                 fns += [lambda i=i: st.topk_round(i), lambda i=i: st.receive(i)]
             return fns + [lambda: st.topk_round(0), st.densify, st.collect]
     else:
-        st = spardl.SparDLStep(P, n, kb, device=dev)
+        st = spardl.SparDLStep(P, n, kb, device=dev, fuse_collect=not args.separate_collect)
         calls = ["residual_add", "block_topk"] + [f"merge_step{i}" for i in range(1, st.l + 1)] + \
                 ["allgather_densify", "residual_collect"]
 
@@ -310,8 +314,9 @@ def main() -> int:
     per_call_ms = {c: max(sum(evs[j][ci][0].elapsed_time(evs[j][ci][1]) for j in range(args.steps))
                           / args.steps - marker_ms, 0.0) for ci, c in enumerate(calls)}
 
-    # ---- dominant kernel: the residual add is one kernel per call; each
-    # launch is bracketed by an event pair on its stream (marker cost removed)
+    # ---- dominant kernel: the residual add is one kernel per call (with the
+    # collection fused in, the call's small drop-index build and the add); each
+    # call is bracketed by an event pair on its stream (marker cost removed)
     g0 = grads[0]
     k_mid = [(ev(), ev()) for _ in range(args.steps)]
     for j in range(args.steps):
@@ -326,6 +331,8 @@ def main() -> int:
             st.residual_add(g0)
             k_mid[j][1].record(stream)
             st.block_topk()
+            if st.fuse_collect:
+                st.finish()   # the next add takes this step's collection, as in the timed steps
     torch.cuda.synchronize()
     add_ms = sum(a.elapsed_time(b) for a, b in k_mid) / args.steps - marker_ms
     ws_check(st)
@@ -430,8 +437,12 @@ def main() -> int:
                    "k_per_block": kb, "gradient_batches": wl.steps, "residual": "carried across steps",
                    "segments": len(wl.seg_len), "seed": W.SEED_BASE, "variant": args.variant, "teams": d,
                    "team_join": ("B-SAG" if args.bruck else "R-SAG") if d > 1 else None,
-                   "L_per_team_block": st.k_blk if d > 1 else None},
-        "roofline": {"bound": "hbm", "kernel": "k_residual_add" if dominant == "residual_add" else dominant,
+                   "L_per_team_block": st.k_blk if d > 1 else None,
+                   "residual_collection": ("inside the next step's residual add" if getattr(st, "fuse_collect", False)
+                                           else "its own call at the end of the step")},
+        "roofline": {"bound": "hbm", "kernel": (("k_residual_add4<true, true> (the previous step's collection fused in)"
+                                                  if getattr(st, "fuse_collect", False) else "k_residual_add4<true, false>")
+                                                 if dominant == "residual_add" else dominant),
                      "achieved": achieved, "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS, "traffic": traffic,
                      "alg_bytes_per_launch": alg[dominant], "avg_launch_ms": dom_ms,
@@ -449,7 +460,9 @@ def main() -> int:
         del st, grads, g0
         torch.cuda.synchronize()
         torch.cuda.empty_cache()
-        w5 = per_worker_measure(W.config(5), dev, args.w5_steps, args.w5_warmup, PER_WORKER_ROWS, False)
+        # (the GPT-2-XL-sized rows keep the separate collection: at 0.1 % density the fused add's
+        # reads of the final-index bitmap, n/8 bytes per row, cost more than the scattered writes)
+        w5 = per_worker_measure(W.config(5), dev, args.w5_steps, args.w5_warmup, PER_WORKER_ROWS, False, False)
         out["workload5"] = {k: w5[k] for k in ("metric", "value", "ms_per_step", "steps", "warmup", "config",
                                                "roofline", "step_roofline", "per_call_ms", "span_ms_per_step")}
         torch.cuda.empty_cache()
@@ -497,12 +510,12 @@ def run_per_worker(args, wl, dev) -> int:
     if wl.P % R:
         print(json.dumps({"error": f"--rows-per-call must divide P = {wl.P}"}))
         return 2
-    out = per_worker_measure(wl, dev, args.steps, args.warmup, R, args.variant == "lazy")
+    out = per_worker_measure(wl, dev, args.steps, args.warmup, R, args.variant == "lazy", False)
     print(json.dumps(out), flush=True)
     return 0
 
 
-def per_worker_measure(wl, dev, steps: int, warmup: int, R: int, lazy: bool) -> dict:
+def per_worker_measure(wl, dev, steps: int, warmup: int, R: int, lazy: bool, fuse_collect: bool = True) -> dict:
     """A workload whose gradients cannot all be resident beside the residual:
     the workers' gradients are generated on the GPU R at a time (untimed
     input plumbing), then their residual add and block top-k run on a
@@ -520,7 +533,7 @@ def per_worker_measure(wl, dev, steps: int, warmup: int, R: int, lazy: bool) -> 
     if lazy:
         st = spardl.SparDLLazyStep(P, n, kb, device=dev, rows_per_call=R)
     else:
-        st = spardl.SparDLStep(P, n, kb, device=dev, rows_per_call=R)
+        st = spardl.SparDLStep(P, n, kb, device=dev, rows_per_call=R, fuse_collect=fuse_collect)
     gen = W.DeviceGenerator(wl, device=dev)
     g = torch.empty((R, n), dtype=torch.float32, device=dev)
     stream = torch.cuda.current_stream()
@@ -617,10 +630,14 @@ def per_worker_measure(wl, dev, steps: int, warmup: int, R: int, lazy: bool) -> 
         "config": {"workload": wl.name, "P": P, "n_per_worker": n, "density": f"{wl.density[0]}/{wl.density[1]}",
                    "k_per_block": kb, "gradient_batches": wl.steps, "residual": "carried across steps",
                    "segments": len(wl.seg_len), "seed": W.SEED_BASE, "variant": "lazy" if lazy else "eager",
+                   "residual_collection": ("inside the next step's residual add" if getattr(st, "fuse_collect", False)
+                                           else "its own call at the end of the step"),
                    "timing": "ms_per_step: sum of the event-timed hot calls; span_ms_per_step: the whole step's "
                              "span on the stream less the gradient generation inside it; the workers' gradients "
                              f"are generated on the GPU between their calls, {R} rows per call ({R}-row workspace)"},
-        "roofline": {"bound": "hbm", "kernel": "k_residual_add4<true>", "achieved": achieved, "peak": HBM_PEAK_GBS,
+        "roofline": {"bound": "hbm", "kernel": ("k_residual_add4<true, true> (the previous step's collection fused in)"
+                                                if getattr(st, "fuse_collect", False) else "k_residual_add4<true, false>"),
+                     "achieved": achieved, "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS, "traffic": None,
                      "alg_bytes_per_launch": alg_add, "avg_launch_ms": add_launch_ms},
         "step_roofline": ({"bytes": "moved by this design", "alg_bytes_full": moved,
@@ -659,7 +676,7 @@ def graph_measure(wl, dev, steps: int) -> dict:
     side.wait_stream(torch.cuda.current_stream())
     out = {"workload": wl.name, "P": P, "n_per_worker": n, "k_per_block": kb, "steps": steps}
     with torch.cuda.stream(side):
-        st = spardl.SparDLStep(P, n, kb, device=dev)
+        st = spardl.SparDLStep(P, n, kb, device=dev, fuse_collect=True)
         for _ in range(10):
             st.step(g)
         torch.cuda.synchronize()

@@ -70,6 +70,7 @@ enum {
  * selection without exactly k_blk entries); bits 2-5 tell which check. */
 #define SPARDL_WS_ERR_LOOKBACK 1u  /* reserved (no kernel waits on another workgroup) */
 #define SPARDL_WS_ERR_COUNT 2u     /* a selection's counts are inconsistent */
+#define SPARDL_WS_ERR_DROPS 64u    /* spardl_residual_add_collect: a drop list not sorted inside its block */
 
 /* Flag for spardl_block_topk: the level-1 |v| histograms (and speculative
  * candidates) of acc are already in ws, written by the immediately preceding
@@ -134,6 +135,34 @@ int spardl_workspace_init(int32_t nworkers, int32_t P, int64_t n, int32_t k_blk,
 int spardl_residual_add(float* acc, int64_t ld_acc, const float* grad, int64_t ld_grad, int32_t w0,
                         int32_t nworkers, int64_t n, int32_t P, int32_t k_blk, void* ws, size_t ws_bytes,
                         hipStream_t stream);
+
+/* The previous step's global residual collection (Sec. III-C) and this
+ * step's residual add (Algorithm 1, G + xi) in one pass over acc: the same
+ * acc, bit for bit, as spardl_residual_collect(..., member) followed by
+ * spardl_residual_add with ws, and the same histograms and candidates for
+ * spardl_block_topk(SPARDL_TOPK_HIST_READY) after it.  Each tile of acc is
+ * read once and written once, whole; the separate collection writes single
+ * words all over acc instead.
+ * The zeroing half finds a worker's selections from the values themselves:
+ * the previous step's spardl_block_topk on these rows, with this ws, keeps
+ * each block's selection rule in ws, so acc must be unchanged since that
+ * call.  member, drop_idx, drop_val, drop_cnt: as the previous step left
+ * them and as for spardl_residual_collect (the decode's bitmap; HOST arrays
+ * of l DEVICE pointers, element i-1 the buffers of SRS step i for all P
+ * workers; they may be NULL when P = 1).  acc, grad, local_idx: the rows
+ * w0 .. w0 + nworkers - 1 (local_idx as spardl_block_topk wrote it; read
+ * only for rows the float4 add does not take, which are collected by the
+ * separate kernels before the add).  The call builds a per-tile index of
+ * the drops in ws before the add.
+ * Errors: as for spardl_residual_add with ws, plus EINVAL for NULL
+ * local_idx, member or ws, a misaligned member, or a NULL drop pointer.  The
+ * error word gets SPARDL_WS_ERR_DROPS if a drop list is not sorted by index
+ * inside its block. */
+int spardl_residual_add_collect(float* acc, int64_t ld_acc, const float* grad, int64_t ld_grad, int32_t w0,
+                                int32_t nworkers, int64_t n, int32_t P, int32_t k_blk, const int32_t* local_idx,
+                                const uint32_t* member, const int32_t* const* drop_idx,
+                                const float* const* drop_val, const int32_t* const* drop_cnt, void* ws,
+                                size_t ws_bytes, hipStream_t stream);
 
 /* Block-wise top-k (Sec. III-B: every worker sparsifies each of its P blocks
  * to its top k/P values; top-k as in Sec. II).  For w < nworkers, b < P:

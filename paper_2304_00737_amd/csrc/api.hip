@@ -39,7 +39,8 @@ inline int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 // candidate value, threshold-bin key).
 struct Layout {
   size_t err = 0, bitmap = 0, hist1 = 0, spec_t1 = 0, spec_used = 0, spec_cnt = 0, state = 0, slot_cnt = 0,
-         slot_nbin = 0, pre_all = 0, pre_ge = 0, pre_eq = 0;
+         slot_nbin = 0, pre_all = 0, pre_ge = 0, pre_eq = 0, keep = 0, dtile = 0;
+  int64_t dtile_pairs = 0;   // (pair, step) lists of all rows over the SRS steps
   size_t fixed_end = 0;
   int64_t units = 0, tiles_tk = 0, tiles_mg = 0, slot_n = 0, pairs_max = 0, add_tiles = 0;
 };
@@ -84,6 +85,14 @@ Layout make_layout(int32_t P, int64_t n, int32_t kb, int32_t rows = 0) {
   off += align256((size_t)L.slot_n * 4);
   L.pre_eq = off;
   off += align256((size_t)L.slot_n * 4);
+  // a residual collection fused into the next add: per (worker, block) the
+  // block top-k's selection rule; per SRS step, pair and add tile the range
+  // of the pair's drops in the tile (step i's pairs after those of steps < i)
+  L.keep = off;
+  off += align256((size_t)rows * P * KEEP_WORDS * 4);
+  for (int32_t i = 1; i <= l; ++i) L.dtile_pairs += (int64_t)rows * bag_of(P, l, i);
+  L.dtile = off;
+  off += align256((size_t)L.dtile_pairs * L.add_tiles * 8);
   L.fixed_end = off;
   return L;
 }
@@ -128,7 +137,8 @@ inline int32_t log2_exact(int32_t d) {
 struct Ws {
   char* base;
   uint32_t *err, *bitmap, *hist1, *spec_t1, *spec_used, *spec_cnt, *state, *slot_cnt, *slot_nbin, *pre_all, *pre_ge,
-      *pre_eq;
+      *pre_eq, *keep;
+  uint2* dtile;
   int32_t* cand_idx;
   float* cand_val;
   uint32_t* bin_key;
@@ -150,6 +160,8 @@ Ws carve(void* ws, size_t ws_bytes, const Layout& L) {
   w.pre_all = at(L.pre_all);
   w.pre_ge = at(L.pre_ge);
   w.pre_eq = at(L.pre_eq);
+  w.keep = at(L.keep);
+  w.dtile = (uint2*)at(L.dtile);
   const size_t q = ws_bytes > L.fixed_end ? ((ws_bytes - L.fixed_end) / 3) & ~(size_t)255 : 0;
   w.cand_idx = (int32_t*)(w.base + L.fixed_end);
   w.cand_val = (float*)(w.base + L.fixed_end + q);
@@ -250,7 +262,7 @@ struct Fill {
 // kept for the all-blocks map (the fused add of the next step reads it).
 int topk_units(const float* acc, int64_t ld_acc, int64_t units, const Units& U, int64_t n, int32_t P, int32_t k_blk,
                bool make_hist, bool spec, int32_t* sp_idx, float* sp_val, int32_t* local_idx, const Ws& w,
-               const Layout& L, hipStream_t stream, int64_t hint_off = 0) {
+               const Layout& L, hipStream_t stream, int64_t hint_off = 0, bool keep_rule = false) {
   const bool v4 = aligned16(acc) && ld_acc % 4 == 0 && blocks_vec4(n, P);
   const int32_t smax = (int32_t)L.tiles_tk;
   if (make_hist) {
@@ -270,7 +282,8 @@ int topk_units(const float* acc, int64_t ld_acc, int64_t units, const Units& U, 
   SPARDL_TRY(launch_thresh(0, units, U, n, P, k_blk, smax, w.hist1, w.cand_val, w.state, w.slot_cnt,
                            w.slot_nbin, w.bin_key, w.pre_all, w.pre_ge, w.pre_eq, nullptr, w.err, stream));
   SPARDL_TRY(launch_emit(0, w.cand_idx, w.cand_val, units, U, n, P, k_blk, Pairs{}, smax, w.state, w.slot_cnt,
-                         w.pre_all, w.pre_ge, w.pre_eq, sp_idx, sp_val, local_idx, nullptr, nullptr, w.err, stream));
+                         w.pre_all, w.pre_ge, w.pre_eq, sp_idx, sp_val, local_idx, nullptr, nullptr, w.err, stream,
+                         keep_rule ? w.keep + hint_off * KEEP_WORDS : nullptr));
   return SPARDL_OK;
 }
 
@@ -397,6 +410,8 @@ int spardl_workspace_init(int32_t nworkers, int32_t P, int64_t n, int32_t k_blk,
                              .add(w.bitmap, ceil_div(n, 32))
                              .add(w.hist1, L.units * HCOPIES * NB1)
                              .add(w.spec_t1, (int64_t)P * P)
+                             .add(w.keep, (int64_t)P * P * KEEP_WORDS)
+                             .add((uint32_t*)w.dtile, L.dtile_pairs * L.add_tiles * 2)
                              .r,
                          stream));
   return SPARDL_OK;
@@ -432,6 +447,66 @@ int spardl_residual_add(float* acc, int64_t ld_acc, const float* grad, int64_t l
   return SPARDL_OK;
 }
 
+int spardl_residual_add_collect(float* acc, int64_t ld_acc, const float* grad, int64_t ld_grad, int32_t w0,
+                                int32_t nworkers, int64_t n, int32_t P, int32_t k_blk, const int32_t* local_idx,
+                                const uint32_t* member, const int32_t* const* drop_idx,
+                                const float* const* drop_val, const int32_t* const* drop_cnt, void* ws,
+                                size_t ws_bytes, hipStream_t stream) {
+  if (!acc || !grad || !local_idx || !member || (reinterpret_cast<uintptr_t>(member) & 3u) || !ws ||
+      ws_misaligned(ws) || nworkers < 1 || nworkers > P || w0 < 0 || w0 > P - nworkers || !sizes_ok(P, n, k_blk) ||
+      ld_acc < n || ld_grad < n)
+    return SPARDL_EINVAL;
+  const int32_t l = steps_of(P);
+  if (l > 0 && (!drop_idx || !drop_val || !drop_cnt)) return SPARDL_EINVAL;
+  for (int32_t i = 0; i < l; ++i)
+    if (!drop_idx[i] || !drop_val[i] || !drop_cnt[i]) return SPARDL_EINVAL;
+  const size_t need = spardl_workspace_bytes(nworkers, P, n, k_blk);
+  if (need == 0) return SPARDL_EINVAL;
+  if (ws_bytes < need) return SPARDL_ECAPACITY;
+  const Layout L = make_layout(P, n, k_blk);
+  Ws w = carve(ws, ws_bytes, L);
+  const bool v4 = aligned16(acc) && aligned16(grad) && ld_acc % 4 == 0 && ld_grad % 4 == 0 && blocks_vec4(n, P);
+  AddSpec sp;
+  sp.hist1 = w.hist1;
+  sp.spec_t1 = w.spec_t1 + (int64_t)w0 * P;
+  if (P > 1) sp.spec_prev = w.spec_t1 + (int64_t)((w0 + P - 1) % P) * P;
+  sp.spec_used = w.spec_used;
+  sp.spec_cnt = w.spec_cnt;
+  sp.cand_idx = w.cand_idx;
+  sp.cand_val = w.cand_val;
+  if (!v4 || l > COLLECT_MAX_STEPS) {
+    // rows the float4 add does not take: the separate collection of these rows, then the add
+    SPARDL_TRY(launch_grc_zero(acc, ld_acc, nworkers, P, n, k_blk, local_idx, member, stream));
+    for (int32_t i = 1; i <= l; ++i) {
+      const int32_t m = bag_of(P, l, i);
+      const int64_t skip = (int64_t)w0 * m;   // the pairs of the rows before w0
+      SPARDL_TRY(launch_grc_drops(acc, ld_acc, n, m, k_blk, nworkers * m, drop_idx[i - 1] + skip * k_blk,
+                                  drop_val[i - 1] + skip * k_blk, drop_cnt[i - 1] + skip, member, stream));
+    }
+    SPARDL_TRY(launch_residual_add(acc, ld_acc, grad, ld_grad, nworkers, n, P, v4, sp, stream));
+    return SPARDL_OK;
+  }
+  AddCollect C;
+  C.member = member;
+  C.keep = w.keep;
+  C.l = l;
+  C.w0 = (uint32_t)w0;
+  C.kb = (uint32_t)k_blk;
+  C.G = (uint32_t)L.add_tiles;
+  int64_t pairs_before = 0;
+  for (int32_t i = 1; i <= l; ++i) {
+    const int32_t m = bag_of(P, l, i);
+    C.didx[i - 1] = drop_idx[i - 1];
+    C.dval[i - 1] = drop_val[i - 1];
+    C.m[i - 1] = (uint32_t)m;
+    C.tile[i - 1] = w.dtile + pairs_before * L.add_tiles;
+    pairs_before += (int64_t)P * m;
+  }
+  SPARDL_TRY(launch_drop_tiles(C, drop_cnt, nworkers, n, P, w.err, stream));
+  SPARDL_TRY(launch_residual_add(acc, ld_acc, grad, ld_grad, nworkers, n, P, v4, sp, stream, C));
+  return SPARDL_OK;
+}
+
 int spardl_block_topk(const float* acc, int64_t ld_acc, int32_t w0, int32_t nworkers, int64_t n, int32_t P,
                       int32_t k_blk, int32_t flags, int32_t* sp_idx, float* sp_val, int32_t* local_idx,
                       void* ws, size_t ws_bytes, hipStream_t stream) {
@@ -445,7 +520,7 @@ int spardl_block_topk(const float* acc, int64_t ld_acc, int32_t w0, int32_t nwor
   Ws w = carve(ws, ws_bytes, L);
   const bool spec = (flags & SPARDL_TOPK_HIST_READY) != 0;   // candidates of the fused add may be used
   return topk_units(acc, ld_acc, (int64_t)nworkers * P, all_blocks(P), n, P, k_blk, !spec, spec, sp_idx, sp_val,
-                    local_idx, w, L, stream, (int64_t)w0 * P);
+                    local_idx, w, L, stream, (int64_t)w0 * P, true);
 }
 
 int spardl_sparse_merge_topk(int32_t* sp_idx, float* sp_val, int32_t P, int64_t n, int32_t k_blk,

@@ -74,6 +74,16 @@ constexpr uint32_t ERR_COUNT_L23 = 2u | 4u;   // ... at level 2 or 3
 constexpr uint32_t ERR_COUNT_POS = 2u | 8u;   // an emitted position fell outside [0, k_blk)
 constexpr uint32_t ERR_COUNT_DROP = 2u | 16u; // a drop position fell outside [0, k_blk)
 constexpr uint32_t ERR_COUNT_SUM = 2u | 32u;  // the emitted selection does not have k_blk entries
+constexpr uint32_t ERR_DROPS = 64u;           // a drop list of the fused collection is not an index-sorted
+                                              // list inside its block
+
+// ---------------------------------------------------------------- deferred residual collection
+// Per (worker, block) the block top-k keeps its selection rule for the
+// residual collection that a later fused residual add applies: it selected
+// every key >= KEEP_TGE and, when KEEP_NEEDEQ != 0, the keys == KEEP_TEQ
+// whose index is at most KEEP_CUT (ties are taken in index order).
+enum KeepWord : int { KEEP_TGE = 0, KEEP_TEQ = 1, KEEP_NEEDEQ = 2, KEEP_CUT = 3, KEEP_WORDS = 4 };
+constexpr int COLLECT_MAX_STEPS = 16;   // SRS steps the fused collection takes (P <= 2^16)
 
 __device__ __forceinline__ uint32_t mag_key(float v) { return __float_as_uint(v) & 0x7FFFFFFFu; }
 

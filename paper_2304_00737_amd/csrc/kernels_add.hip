@@ -58,17 +58,39 @@ __global__ __launch_bounds__(256) void k_fill(FillRanges r) {
 // rebuilds the block's full histogram itself.  The previous threshold is the
 // larger of the worker's own from its previous step and the same block's
 // latest at the preceding worker.
-constexpr int ADD_STAGE = 512;          // speculative candidates staged in LDS per tile
+//
+// With COLL, the previous step's global residual collection (Sec. III-C) is
+// applied to the tile before the gradient is added, in the order of the
+// separate collection: the worker's own selections that became final are
+// zeroed -- the block top-k's rule (KEEP_WORDS) recomputed on the values it
+// selected from, which nothing changed since -- and then, SRS step by step,
+// its final drops are added back.  The drops of one step are distinct
+// indices, so a step's additions run in parallel on an LDS image of the tile.
+// The separate collection's scattered writes leave ~1M partially written
+// lines in the caches, which are written back during the next add; here
+// every line of acc is written once, whole.
+constexpr int ADD_STAGE = 512;          // speculative candidates (or drops) staged in LDS per tile
 
-template <bool HIST>
+template <bool HIST, bool COLL>
 __global__ __launch_bounds__(256) void k_residual_add4(float* __restrict__ acc, int64_t ld_acc,
                                                        const float* __restrict__ grad, int64_t ld_grad, Blocks B,
-                                                       uint32_t G, AddSpec sp) {
+                                                       uint32_t G, AddSpec sp, AddCollect C) {
   static_assert(ADD_TILE == 2 * 1024, "two 1024-element chunks per tile");
+  static_assert(!COLL || HIST, "the fused collection runs in the fused add");
   __shared__ __align__(16) uint32_t h[HIST ? NB1 : 4];
   __shared__ int32_t s_idx[HIST ? ADD_STAGE : 1];
   __shared__ float s_val[HIST ? ADD_STAGE : 1];
   __shared__ uint32_t wtot[4];
+  // COLL: the tile image (in the histogram's space, which is cleared after
+  // the collection), its final-index bitmap words, and per SRS step the range
+  // of the worker's drops inside the tile with their arrays
+  static_assert(NB1 >= ADD_TILE, "the tile image fits in the histogram's space");
+  float* cimg = reinterpret_cast<float*>(h);
+  __shared__ uint32_t cmw[COLL ? ADD_TILE / 32 : 1];
+  __shared__ uint32_t c_lo[COLL ? COLLECT_MAX_STEPS : 1], c_hi[COLL ? COLLECT_MAX_STEPS : 1];
+  __shared__ uint32_t c_cum[COLL ? COLLECT_MAX_STEPS + 1 : 1];
+  __shared__ const int32_t* c_di[COLL ? COLLECT_MAX_STEPS : 1];
+  __shared__ const float* c_dv[COLL ? COLLECT_MAX_STEPS : 1];
   const uint32_t g = blockIdx.x % G;
   const uint32_t wb = blockIdx.x / G;
   const uint32_t b = wb % B.P, w = wb / B.P;
@@ -90,6 +112,22 @@ __global__ __launch_bounds__(256) void k_residual_add4(float* __restrict__ acc, 
       gg[j] = __builtin_nontemporal_load(reinterpret_cast<const f4v*>(Gr + x));
     }
   }
+  // COLL: the final-index bitmap words of this thread's two float4 (the four
+  // elements share a word: tiles start on 32-element boundaries)
+  uint32_t mw[2] = {0u, 0u};
+  uint32_t k_tge = 0, k_teq = 0, k_need = 0, k_cut = 0;   // COLL: the block top-k's selection rule
+  if constexpr (COLL) {
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      const uint32_t x = x0 + 1024u * j;
+      if (x < B.n) mw[j] = C.member[x >> 5];
+    }
+    const uint32_t* __restrict__ kp = C.keep + ((int64_t)(C.w0 + w) * B.P + b) * KEEP_WORDS;
+    k_tge = kp[KEEP_TGE];
+    k_teq = kp[KEEP_TEQ];
+    k_need = kp[KEEP_NEEDEQ];
+    k_cut = kp[KEEP_CUT];
+  }
   if (!HIST) {
 #pragma unroll
     for (int j = 0; j < 2; ++j) {
@@ -104,7 +142,8 @@ __global__ __launch_bounds__(256) void k_residual_add4(float* __restrict__ acc, 
     }
     return;
   }
-  // the histogram is cleared while the loads are in flight
+  // the histogram is cleared while the loads are in flight (with COLL, a tile
+  // with drops clears its image's words again after the collection)
   for (int i = threadIdx.x; i < NB1 / 4; i += 256) reinterpret_cast<uint4*>(h)[i] = make_uint4(0u, 0u, 0u, 0u);
   uint32_t F = SPEC_NONE;
   uint32_t sw = sp.spec_t1[wb];
@@ -123,7 +162,104 @@ __global__ __launch_bounds__(256) void k_residual_add4(float* __restrict__ acc, 
   if (g == 0u && threadIdx.x == 0) sp.spec_used[wb] = F;
   const L1Map M = l1_map(F);
   const uint32_t FH = M.floor;
+  const uint32_t wa = C.w0 + w;   // COLL: the absolute worker
+  const uint32_t tt = (b + B.P - wa % B.P) % B.P;   // COLL: this block's place in the worker's bags
+  if constexpr (COLL) {
+    // one thread reads the ranges (all loads in flight together) and, after
+    // the barrier, clears them (a later index build writes only tiles with
+    // drops), so no other wave reads a cleared word
+    if (threadIdx.x == 0) {
+      uint2 rr[COLLECT_MAX_STEPS];
+#pragma unroll
+      for (int i = 0; i < COLLECT_MAX_STEPS; ++i) {
+        rr[i] = make_uint2(0u, 0u);
+        if (i < C.l && tt < C.m[i]) rr[i] = C.tile[i][((int64_t)wa * C.m[i] + tt) * C.G + g];
+      }
+      uint32_t cum = 0;
+#pragma unroll
+      for (int i = 0; i < COLLECT_MAX_STEPS; ++i) {
+        if (i < C.l) {
+          const uint32_t lo = min(rr[i].x, C.kb), hi = min(max(rr[i].y, lo), C.kb);
+          if (hi > lo) {
+            const int64_t p = (int64_t)wa * C.m[i] + tt;
+            c_di[i] = C.didx[i] + p * C.kb;
+            c_dv[i] = C.dval[i] + p * C.kb;
+          }
+          c_lo[i] = lo;
+          c_hi[i] = hi;
+          c_cum[i] = cum;
+          cum += hi - lo;
+        }
+      }
+      c_cum[C.l] = cum;
+    }
+  }
   __syncthreads();
+  if constexpr (COLL) {
+    if (threadIdx.x == 0)
+      for (int i = 0; i < C.l; ++i)
+        if (c_hi[i] > c_lo[i]) C.tile[i][((int64_t)wa * C.m[i] + tt) * C.G + g] = make_uint2(0u, 0u);
+  }
+  if constexpr (COLL) {
+    // the worker's selections of this block that became final -> 0
+    const uint32_t tge = k_tge, teq = k_teq, need_eq = k_need, xcut = k_cut;
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      if (in[j]) {
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+          const uint32_t x = x0 + 1024u * j + (uint32_t)c;
+          const uint32_t key = mag_key(a[j][c]);
+          const bool sel = key >= tge || (need_eq != 0u && key == teq && x <= xcut);
+          if (sel && ((mw[j] >> (x & 31u)) & 1u)) a[j][c] = 0.0f;
+        }
+      }
+    }
+    const uint32_t ndrop = c_cum[C.l];   // uniform
+    if (ndrop != 0u) {
+      // the final drops of SRS steps 1..l, in order, on the tile image
+#pragma unroll
+      for (int j = 0; j < 2; ++j)
+        if (in[j]) *reinterpret_cast<f4v*>(cimg + threadIdx.x * 4u + 1024u * j) = a[j];
+      if ((threadIdx.x & 7u) == 0u) {
+        cmw[threadIdx.x >> 3] = mw[0];
+        cmw[32u + (threadIdx.x >> 3)] = mw[1];
+      }
+      const bool staged = ndrop <= (uint32_t)ADD_STAGE;   // uniform: every step's drops in one round of loads
+      if (staged) {
+        for (uint32_t f = threadIdx.x; f < ndrop; f += 256u) {
+          int i = 0;
+          while (f >= c_cum[i + 1]) ++i;
+          const uint32_t jj = c_lo[i] + (f - c_cum[i]);
+          s_idx[f] = c_di[i][jj];
+          s_val[f] = c_dv[i][jj];
+        }
+      }
+      __syncthreads();
+      for (int i = 0; i < C.l; ++i) {
+        const uint32_t lo = c_lo[i], hi = c_hi[i];
+        if (hi == lo) continue;   // uniform
+        for (uint32_t jj = lo + threadIdx.x; jj < hi; jj += 256u) {
+          const uint32_t f = c_cum[i] + (jj - lo);
+          const int32_t x = staged ? s_idx[f] : c_di[i][jj];
+          const float v = staged ? s_val[f] : c_dv[i][jj];
+          const uint32_t o = (uint32_t)x - ta;
+          if (o < (uint32_t)ADD_TILE && (uint32_t)x >= s && (uint32_t)x < e && ((cmw[o >> 5] >> (o & 31u)) & 1u))
+            cimg[o] = cimg[o] + v;
+        }
+        __syncthreads();
+      }
+      // each thread reads back its own words of the image and clears them for the
+      // histogram; the barrier orders every clear before any histogram update
+#pragma unroll
+      for (int j = 0; j < 2; ++j) {
+        f4v* q = reinterpret_cast<f4v*>(cimg + threadIdx.x * 4u + 1024u * j);
+        if (in[j]) a[j] = *q;
+        *q = f4v{0.f, 0.f, 0.f, 0.f};
+      }
+      __syncthreads();
+    }
+  }
   float r[8];
   uint32_t packed = 0;   // candidates of chunk 0 | chunk 1 << 16 (at most 1024 each)
 #pragma unroll
@@ -287,8 +423,9 @@ hipError_t launch_fill(const FillRanges& r, hipStream_t s) {
 
 hipError_t launch_residual_add(float* acc, int64_t ld_acc, const float* grad, int64_t ld_grad,
                                int32_t nworkers, int64_t n, int32_t P, bool vec4, const AddSpec& sp,
-                               hipStream_t s) {
+                               hipStream_t s, const AddCollect& C) {
   const bool hist = sp.hist1 != nullptr;
+  if (C.member && !(hist && vec4)) return hipErrorInvalidValue;   // the fused collection needs the fused float4 add
   const int32_t PP = hist ? P : 1;
   const int64_t maxlen = (n + PP - 1) / PP;
   const Blocks B = make_blocks(n, PP);
@@ -296,8 +433,12 @@ hipError_t launch_residual_add(float* acc, int64_t ld_acc, const float* grad, in
     // tiles from each block's aligned origin: up to 31 more elements per block
     const uint32_t G = (uint32_t)add_tiles_per_block(maxlen);
     const dim3 grid((unsigned)((int64_t)nworkers * PP * G));
-    if (hist) hipLaunchKernelGGL(k_residual_add4<true>, grid, dim3(256), 0, s, acc, ld_acc, grad, ld_grad, B, G, sp);
-    else hipLaunchKernelGGL(k_residual_add4<false>, grid, dim3(256), 0, s, acc, ld_acc, grad, ld_grad, B, G, sp);
+    if (C.member)
+      hipLaunchKernelGGL((k_residual_add4<true, true>), grid, dim3(256), 0, s, acc, ld_acc, grad, ld_grad, B, G, sp, C);
+    else if (hist)
+      hipLaunchKernelGGL((k_residual_add4<true, false>), grid, dim3(256), 0, s, acc, ld_acc, grad, ld_grad, B, G, sp, C);
+    else
+      hipLaunchKernelGGL((k_residual_add4<false, false>), grid, dim3(256), 0, s, acc, ld_acc, grad, ld_grad, B, G, sp, C);
   } else {
     const uint32_t G = (uint32_t)((maxlen + ADD_TILE - 1) / ADD_TILE);
     const dim3 grid((unsigned)((int64_t)nworkers * PP * G));

@@ -120,6 +120,66 @@ __global__ __launch_bounds__(256) void k_grc_drops(float* __restrict__ acc, int6
   }
 }
 
+// The per-tile index of a fused residual collection: for every pair of the
+// call's rows at SRS step i (worker w, bag block t, merging block
+// b = (w + t) mod P) and every add tile g of block b with drops, the range
+// [first, end) of the pair's drop list inside the tile.  A list is index
+// sorted inside its block (an SRS step emits its drops in index order), so
+// an entry starts its tile's range if the entry before it lies in another
+// tile, and ends it if the entry after it does.  Tiles without drops keep
+// the (0, 0) the consuming add leaves.  Grid: x over a list, y over the
+// (step, pair) lists of the call's rows.
+constexpr int DT_PER = 4;   // list entries per thread of the index build
+
+struct DropTiles {
+  AddCollect C;
+  const int32_t* cnt[COLLECT_MAX_STEPS];
+  uint32_t pcum[COLLECT_MAX_STEPS + 1];   // lists of the call's rows before step i
+  uint32_t nw;
+};
+
+__global__ __launch_bounds__(256) void k_drop_tiles(DropTiles D, Blocks B, uint32_t* __restrict__ err) {
+  const AddCollect& C = D.C;
+  for (uint32_t y = blockIdx.y; y < D.pcum[C.l]; y += gridDim.y) {
+    int i = 0;
+    while (y >= D.pcum[i + 1]) ++i;
+    const uint32_t m = C.m[i];
+    const uint32_t q = y - D.pcum[i];
+    const uint32_t w = C.w0 + q / m, tt = q - (q / m) * m;
+    const uint32_t b = (w + tt) % B.P;
+    const int64_t p = (int64_t)w * m + tt;
+    const int32_t c = D.cnt[i][p];
+    const uint32_t cnt = c < 0 ? 0u : min((uint32_t)c, C.kb);
+    const int32_t* __restrict__ X = C.didx[i] + p * C.kb;
+    uint2* __restrict__ T = C.tile[i] + p * C.G;
+    const uint32_t s = B.start(b), e = B.start(b + 1u), o = block_origin(s);
+    // DT_PER consecutive entries per thread, with the entries on either side
+    for (uint32_t j0 = (blockIdx.x * 256u + threadIdx.x) * DT_PER; j0 < cnt; j0 += gridDim.x * 256u * DT_PER) {
+      uint32_t xs[DT_PER + 2];
+#pragma unroll
+      for (int u = 0; u < DT_PER + 2; ++u) {
+        const uint32_t j = j0 + (uint32_t)u - 1u;   // j0 - 1 wraps for j0 = 0 and fails the test
+        xs[u] = j < cnt ? (uint32_t)X[j] : 0u;
+      }
+#pragma unroll
+      for (int u = 1; u <= DT_PER; ++u) {
+        const uint32_t j = j0 + (uint32_t)u - 1u;
+        if (j >= cnt) break;
+        const uint32_t x = xs[u];
+        if (x < s || x >= e || (j > 0u && xs[u - 1] >= x)) {
+          atomicOr(err, ERR_DROPS);
+          continue;
+        }
+        const uint32_t t = (x - o) / (uint32_t)ADD_TILE;
+        const bool first = j == 0u || (xs[u - 1] - o) / (uint32_t)ADD_TILE != t;
+        const bool last = j + 1u == cnt || (xs[u + 1] - o) / (uint32_t)ADD_TILE != t;
+        if (first) T[t].x = j;
+        if (last) T[t].y = j + 1u;
+      }
+    }
+  }
+}
+
 // acc[w][x] += share * v for the drops (x, v) of R-SAG exchange t with x a
 // final index, on both workers of each pair (they made the same merge;
 // share = 2^-(t+1), the product exact unless it is subnormal).  Grid: x over
@@ -181,6 +241,23 @@ hipError_t launch_grc_drops(float* acc, int64_t ld_acc, int64_t n, int32_t m, in
                             const uint32_t* bm, hipStream_t s) {
   const dim3 grid(grid_for(kb, 256, 1024), (unsigned)std::min<int32_t>(npairs, 65535));
   hipLaunchKernelGGL(k_grc_drops, grid, dim3(256), 0, s, acc, ld_acc, (uint32_t)n, (uint32_t)m, (uint32_t)kb, (uint32_t)npairs, drop_idx, drop_val, drop_cnt, bm);
+  return hipGetLastError();
+}
+
+hipError_t launch_drop_tiles(const AddCollect& C, const int32_t* const* drop_cnt, int32_t nw, int64_t n, int32_t P,
+                             uint32_t* err, hipStream_t s) {
+  if (C.l <= 0) return hipSuccess;
+  if (C.l > COLLECT_MAX_STEPS) return hipErrorInvalidValue;
+  DropTiles D;
+  D.C = C;
+  D.nw = (uint32_t)nw;
+  D.pcum[0] = 0u;
+  for (int i = 0; i < C.l; ++i) {
+    D.cnt[i] = drop_cnt[i];
+    D.pcum[i + 1] = D.pcum[i] + (uint32_t)nw * C.m[i];
+  }
+  const dim3 grid(grid_for(((int64_t)C.kb + DT_PER - 1) / DT_PER, 256, 1024), (unsigned)std::min<uint32_t>(D.pcum[C.l], 65535u));
+  hipLaunchKernelGGL(k_drop_tiles, grid, dim3(256), 0, s, D, make_blocks(n, P), err);
   return hipGetLastError();
 }
 

@@ -1489,7 +1489,8 @@ __device__ __forceinline__ void emit_topk_slot(uint32_t cnt, uint32_t run_g, uin
                                                const int32_t* __restrict__ CI, const float* __restrict__ CV,
                                                const int32_t (&ix1)[R1], const float (&vx1)[R1],
                                                int32_t* __restrict__ oI, float* __restrict__ oV,
-                                               int32_t* __restrict__ oL, uint32_t* __restrict__ err) {
+                                               int32_t* __restrict__ oL, uint32_t* __restrict__ err,
+                                               uint32_t* __restrict__ kcut) {
   const int lane = lane_id();
   const uint64_t lt = __lanemask_lt();
   auto put = [&](uint32_t p, int32_t ix, float vx) {
@@ -1499,6 +1500,7 @@ __device__ __forceinline__ void emit_topk_slot(uint32_t cnt, uint32_t run_g, uin
     const uint64_t mg = __ballot(is_ge), me = __ballot(is_eq);
     const uint32_t ge_pre = run_g + popc64(mg & lt);
     const uint32_t eq_pre = run_e + popc64(me & lt);
+    if (kcut && is_eq && eq_pre + 1u == need_eq) *kcut = (uint32_t)ix;   // the last tie taken
     if (is_ge || (is_eq && eq_pre < need_eq)) {
       const uint32_t sel_before = ge_pre + (eq_pre < need_eq ? eq_pre : need_eq);
       if (sel_before < (uint32_t)kb) {
@@ -1540,7 +1542,7 @@ __global__ __launch_bounds__(256) void k_emit(
     const uint32_t* __restrict__ slot_cnt, const uint32_t* __restrict__ pre_all,
     const uint32_t* __restrict__ pre_ge, const uint32_t* __restrict__ pre_eq, int32_t* __restrict__ out_idx,
     float* __restrict__ out_val, int32_t* __restrict__ local_idx, int32_t* __restrict__ drop_idx,
-    float* __restrict__ drop_val, uint32_t* __restrict__ err) {
+    float* __restrict__ drop_val, uint32_t* __restrict__ err, uint32_t* __restrict__ keep) {
   const uint32_t unit = blockIdx.x / gq;
   const int wv = wave_id();
   if constexpr (MODE == 0 && SPW == 1) {
@@ -1560,6 +1562,13 @@ __global__ __launch_bounds__(256) void k_emit(
     uint32_t w, b;
     U.decode(unit, B.P, &w, &b);
     const int64_t o = ((int64_t)w * B.P + b) * kb;
+    // the selection rule, kept for a residual collection fused into the next add
+    uint32_t* __restrict__ kp = keep ? keep + (int64_t)au * KEEP_WORDS : nullptr;
+    if (kp && slot == 0 && lane == 0) {
+      kp[KEEP_TGE] = tge;
+      kp[KEEP_TEQ] = teq;
+      kp[KEEP_NEEDEQ] = need_eq;
+    }
     for (uint32_t e0 = 0; e0 < cnt; e0 += WAVE * EMIT_R) {
       int32_t ix[EMIT_R];
       float vx[EMIT_R];
@@ -1584,6 +1593,7 @@ __global__ __launch_bounds__(256) void k_emit(
           const uint32_t ge_pre = run_g + popc64(mg & lt);
           const uint32_t eq_pre = run_e + popc64(me & lt);
           const uint32_t sel_before = ge_pre + (eq_pre < need_eq ? eq_pre : need_eq);
+          if (kp && is_eq && eq_pre + 1u == need_eq) kp[KEEP_CUT] = (uint32_t)ix[r];   // the last tie taken
           if (is_ge || (is_eq && eq_pre < need_eq)) {
             if (sel_before < (uint32_t)kb) {
               out_idx[o + sel_before] = ix[r];
@@ -1640,12 +1650,20 @@ __global__ __launch_bounds__(256) void k_emit(
     uint32_t w, b;
     U.decode(unit, B.P, &w, &b);
     const int64_t o = ((int64_t)w * B.P + b) * kb;
+    // the selection rule, kept for a residual collection fused into the next add
+    uint32_t* __restrict__ kp = keep ? keep + (int64_t)au * KEEP_WORDS : nullptr;
+    if (kp && sw == 0 && lane == 0) {
+      kp[KEEP_TGE] = tge;
+      kp[KEEP_TEQ] = teq;
+      kp[KEEP_NEEDEQ] = need_eq;
+    }
 #pragma unroll
     for (int j = 0; j < SPW; ++j) {
       if (sw + j >= g.nslots) break;   // wave-uniform
       const int64_t base = g.base + g.off(sw + j);
       emit_topk_slot<R1>(cnt[j], rg[j], re[j], tge, teq, need_eq, kb, cand_idx + base, cand_val + base, ix[j], vx[j],
-                     out_idx + o, out_val + o, local_idx ? local_idx + o : nullptr, err);
+                     out_idx + o, out_val + o, local_idx ? local_idx + o : nullptr, err,
+                     kp ? kp + KEEP_CUT : nullptr);
     }
   } else {
     constexpr int NPART = 4;   // waves sharing one slot
@@ -1830,20 +1848,20 @@ hipError_t launch_emit(int mode, const int32_t* cand_idx, const float* cand_val,
                        int64_t n, int32_t P, int32_t kb, const Pairs& PM, int32_t smax, const uint32_t* state,
                        const uint32_t* slot_cnt, const uint32_t* pre_all, const uint32_t* pre_ge,
                        const uint32_t* pre_eq, int32_t* out_idx, float* out_val, int32_t* local_idx,
-                       int32_t* drop_idx, float* drop_val, uint32_t* err, hipStream_t s) {
+                       int32_t* drop_idx, float* drop_val, uint32_t* err, hipStream_t s, uint32_t* keep) {
   // block top-k: 4 spw slots per workgroup (spw per wave); merge: one slot per workgroup
   const int spw = mode == 0 ? topk_slots_per_wave(nunits, smax, kb) : 1;
   const uint32_t gq = mode == 0 ? (uint32_t)((smax + 4 * spw - 1) / (4 * spw)) : (uint32_t)smax;
   const dim3 grid((unsigned)(nunits * gq));
   const Blocks B = make_blocks(n, P);
   if (mode == 0 && spw == 8)
-    hipLaunchKernelGGL((k_emit<0, 8>), grid, dim3(256), 0, s, cand_idx, cand_val, B, U, PM, kb, smax, gq, state, slot_cnt, pre_all, pre_ge, pre_eq, out_idx, out_val, local_idx, drop_idx, drop_val, err);
+    hipLaunchKernelGGL((k_emit<0, 8>), grid, dim3(256), 0, s, cand_idx, cand_val, B, U, PM, kb, smax, gq, state, slot_cnt, pre_all, pre_ge, pre_eq, out_idx, out_val, local_idx, drop_idx, drop_val, err, keep);
   else if (mode == 0 && spw == 2)
-    hipLaunchKernelGGL((k_emit<0, 2>), grid, dim3(256), 0, s, cand_idx, cand_val, B, U, PM, kb, smax, gq, state, slot_cnt, pre_all, pre_ge, pre_eq, out_idx, out_val, local_idx, drop_idx, drop_val, err);
+    hipLaunchKernelGGL((k_emit<0, 2>), grid, dim3(256), 0, s, cand_idx, cand_val, B, U, PM, kb, smax, gq, state, slot_cnt, pre_all, pre_ge, pre_eq, out_idx, out_val, local_idx, drop_idx, drop_val, err, keep);
   else if (mode == 0)
-    hipLaunchKernelGGL(k_emit<0>, grid, dim3(256), 0, s, cand_idx, cand_val, B, U, PM, kb, smax, gq, state, slot_cnt, pre_all, pre_ge, pre_eq, out_idx, out_val, local_idx, drop_idx, drop_val, err);
+    hipLaunchKernelGGL(k_emit<0>, grid, dim3(256), 0, s, cand_idx, cand_val, B, U, PM, kb, smax, gq, state, slot_cnt, pre_all, pre_ge, pre_eq, out_idx, out_val, local_idx, drop_idx, drop_val, err, keep);
   else
-    hipLaunchKernelGGL(k_emit<1>, grid, dim3(256), 0, s, cand_idx, cand_val, B, U, PM, kb, smax, gq, state, slot_cnt, pre_all, pre_ge, pre_eq, out_idx, out_val, local_idx, drop_idx, drop_val, err);
+    hipLaunchKernelGGL(k_emit<1>, grid, dim3(256), 0, s, cand_idx, cand_val, B, U, PM, kb, smax, gq, state, slot_cnt, pre_all, pre_ge, pre_eq, out_idx, out_val, local_idx, drop_idx, drop_val, err, keep);
   return hipGetLastError();
 }
 

@@ -26,10 +26,27 @@ struct AddSpec {
   float* cand_val = nullptr;
 };
 
+// The previous step's global residual collection, applied by the fused
+// residual add to each tile before it adds the gradient (member null: none).
+struct AddCollect {
+  const uint32_t* member = nullptr;              // bitmap of the final indices
+  const uint32_t* keep = nullptr;                // per absolute (worker, block): the top-k's KEEP_WORDS
+  const int32_t* didx[COLLECT_MAX_STEPS] = {};   // per SRS step: the drops, [pair][k_blk]
+  const float* dval[COLLECT_MAX_STEPS] = {};
+  uint2* tile[COLLECT_MAX_STEPS] = {};           // per step: [pair][add tile] -> (first, end) of its drops there
+  uint32_t m[COLLECT_MAX_STEPS] = {};            // per step: blocks per bag
+  int32_t l = 0;
+  uint32_t w0 = 0, kb = 0, G = 0;                // first worker of the call's rows; add tiles per block
+};
+
 hipError_t launch_fill(const FillRanges& r, hipStream_t s);
 hipError_t launch_residual_add(float* acc, int64_t ld_acc, const float* grad, int64_t ld_grad,
                                int32_t nworkers, int64_t n, int32_t P, bool vec4, const AddSpec& sp,
-                               hipStream_t s);
+                               hipStream_t s, const AddCollect& C = AddCollect{});
+// The per-tile ranges of the drops of the call's rows (C.w0 .. C.w0 + nw - 1)
+// for a fused collection: tile words of tiles without drops must be zero.
+hipError_t launch_drop_tiles(const AddCollect& C, const int32_t* const* drop_cnt, int32_t nw, int64_t n, int32_t P,
+                             uint32_t* err, hipStream_t s);
 // Block top-k stages over nunits selection units (Units in common.hpp).
 hipError_t launch_hist1(const float* acc, int64_t ld_acc, int64_t nunits, const Units& U, int64_t n, int32_t P,
                         bool vec4, uint32_t* hist1, hipStream_t s);
@@ -48,7 +65,7 @@ hipError_t launch_emit(int mode, const int32_t* cand_idx, const float* cand_val,
                        int64_t n, int32_t P, int32_t kb, const Pairs& PM, int32_t smax, const uint32_t* state,
                        const uint32_t* slot_cnt, const uint32_t* pre_all, const uint32_t* pre_ge,
                        const uint32_t* pre_eq, int32_t* out_idx, float* out_val, int32_t* local_idx,
-                       int32_t* drop_idx, float* drop_val, uint32_t* err, hipStream_t s);
+                       int32_t* drop_idx, float* drop_val, uint32_t* err, hipStream_t s, uint32_t* keep = nullptr);
 // Union tiles and their level-1 histogram; with merge_fine(kb) the fine window
 // (its first bin in the pairs' state word ST_WBASE) and, per slot, the keys'
 // low bits in bin order and the bins' prefix in the slot's words of U_key.

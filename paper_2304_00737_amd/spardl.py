@@ -38,6 +38,8 @@ _lib.spardl_workspace_bytes.restype = _sz
 _lib.spardl_workspace_init.argtypes = [_i32, _i32, _i64, _i32, _p, _sz, _p]
 _lib.spardl_workspace_init.restype = ctypes.c_int
 _lib.spardl_residual_add.argtypes = [_p, _i64, _p, _i64, _i32, _i32, _i64, _i32, _i32, _p, _sz, _p]
+_lib.spardl_residual_add_collect.argtypes = [_p, _i64, _p, _i64, _i32, _i32, _i64, _i32, _i32, _p, _p, _p, _p, _p, _p,
+                                             _sz, _p]
 _lib.spardl_block_topk.argtypes = [_p, _i64, _i32, _i32, _i64, _i32, _i32, _i32, _p, _p, _p, _p, _sz, _p]
 _lib.spardl_sparse_merge_topk.argtypes = [_p, _p, _i32, _i64, _i32, _i32, _p, _p, _p, _p, _sz, _p]
 _lib.spardl_sparse_merge_topk_noalloc.argtypes = [_p, _p, _i32, _i64, _i32, _i32, _p, _p, _p, _p, _p]
@@ -63,7 +65,7 @@ _lib.spardl_bsag_workspace_bytes.restype = _sz
 _lib.spardl_bsag_workspace_init.argtypes = [_i32, _i32, _i64, _i32, _p, _sz, _p]
 _lib.spardl_bsag_exchange.argtypes = [_p, _p, _i32, _i32, _i64, _i32, _p, _p, _p, _p, _p, _sz, _p]
 _lib.spardl_bsag_residual.argtypes = [_p, _i64, _i32, _i32, _i64, _i32, _p, _p, _p, _p, _p]
-for _f in ("residual_add", "block_topk", "sparse_merge_topk", "sparse_merge_topk_noalloc", "allgather_densify", "residual_collect",
+for _f in ("residual_add", "residual_add_collect", "block_topk", "sparse_merge_topk", "sparse_merge_topk_noalloc", "allgather_densify", "residual_collect",
            "lazy_topk", "lazy_receive", "lazy_residual_collect", "rsag_workspace_init", "rsag_merge_topk",
            "rsag_residual", "bsag_workspace_init", "bsag_exchange", "bsag_residual", "team_workspace_init",
            "team_residual_add", "team_block_topk", "team_merge_topk", "team_residual_collect"):
@@ -139,6 +141,20 @@ def residual_add(acc, grad, nworkers: int, n: int, P: int = 0, ws=None, k_blk: i
     ws_bytes = ws.numel() * ws.element_size() if ws is not None else 0
     _check("residual_add", _lib.spardl_residual_add(_ptr(acc), ld_acc, _ptr(grad), ld_grad, w0, nworkers, n, P,
                                                     k_blk, _ptr(ws), ws_bytes, _stream(stream)))
+
+
+def residual_add_collect(acc, grad, nworkers: int, n: int, P: int, ws, k_blk: int, local_idx, member, drop_idx,
+                         drop_val, drop_cnt, *, w0: int = 0, ld_acc=None, ld_grad=None, stream=None) -> None:
+    """The previous step's residual collection fused into this step's add.
+    acc / grad / local_idx: the rows w0 .. w0 + nworkers - 1; member and
+    drop_* (sequences of l tensors, one per SRS step) as for residual_collect."""
+    ld_acc = _ld(acc, n) if ld_acc is None else ld_acc
+    ld_grad = _ld(grad, n) if ld_grad is None else ld_grad
+    l = len(drop_idx)
+    arr = lambda ts: (ctypes.c_void_p * max(l, 1))(*[_ptr(t) for t in ts]) if l else None
+    _check("residual_add_collect", _lib.spardl_residual_add_collect(
+        _ptr(acc), ld_acc, _ptr(grad), ld_grad, w0, nworkers, n, P, k_blk, _ptr(local_idx), _ptr(member),
+        arr(drop_idx), arr(drop_val), arr(drop_cnt), _ptr(ws), _nb(ws), _stream(stream)))
 
 
 def block_topk(acc, nworkers: int, n: int, P: int, k_blk: int, sp_idx, sp_val, local_idx=None, ws=None,
@@ -342,6 +358,8 @@ def ws_layout(P: int, n: int, kb: int, ws_bytes: int) -> dict:
     L["state"] = off; off += al(units * 16 * 4)
     for k in ("slot_cnt", "slot_nbin", "pre_all", "pre_ge", "pre_eq"):
         L[k] = off; off += al(slot_n * 4)
+    L["keep"] = off; off += al(P * P * 4 * 4)             # the block top-k's selection rule per (worker, block)
+    L["dtile"] = off; off += al(sum(P * m for m in bags) * add_tiles * 8)   # per (step, pair, add tile)
     L["fixed_end"] = off
     L["cand_entries"] = max(P * n, pairs_max * tiles_mg * 4096)
     q = ((ws_bytes - off) // 3) & ~255
@@ -399,13 +417,21 @@ class SparDLStep(_Checkpoint):
     acc[P, n] holds the residual between steps.  After step(grad): dense holds
     the global update, sp_idx/sp_val the sparse state (final block b in
     sp[b, b]), local_idx the local selections and drop_* the per-step drops.
+    With fuse_collect, a step leaves its residual collection to the next
+    step's add (spardl_residual_add_collect): acc holds the residual only
+    after flush(), which runs the pending collection on its own.
     """
 
-    def __init__(self, P: int, n: int, k_blk: int, device="cuda", fused: bool = True, rows_per_call: int = 0):
+    def __init__(self, P: int, n: int, k_blk: int, device="cuda", fused: bool = True, rows_per_call: int = 0,
+                 fuse_collect: bool = False):
         """rows_per_call: workers per residual-add / block top-k call (0: all P).
         The workspace is sized for that many rows, so a model too large for a
         P-row workspace runs its workers a few at a time."""
+        if fuse_collect and not fused:
+            raise ValueError("the collection fuses into the fused residual add only")
         self.P, self.n, self.k_blk, self.fused = P, n, k_blk, fused
+        self.fuse_collect = fuse_collect
+        self.pending = [False] * P   # per worker: its residual collection waits for its next add
         self.rows = P if rows_per_call <= 0 else min(rows_per_call, P)
         dev = torch.device(device)
         self.acc = torch.zeros((P, n), dtype=torch.float32, device=dev)
@@ -424,7 +450,14 @@ class SparDLStep(_Checkpoint):
         """Rows w0 .. w0 + len(grad_rows) - 1 (at most rows_per_call)."""
         r = grad_rows.shape[0]
         acc = self.acc[w0:w0 + r]
-        if self.fused:
+        pend = self.pending[w0:w0 + r]
+        if any(pend) and not all(pend):
+            raise ValueError("rows with and without a pending collection in one call")
+        if pend and pend[0]:
+            residual_add_collect(acc, grad_rows, r, self.n, self.P, self.ws, self.k_blk, self.local_idx[w0:w0 + r],
+                                 self.member, self.drop_idx, self.drop_val, self.drop_cnt, w0=w0, stream=stream)
+            self.pending[w0:w0 + r] = [False] * r
+        elif self.fused:
             residual_add(acc, grad_rows, r, self.n, self.P, self.ws, self.k_blk, w0=w0, stream=stream)
         else:
             residual_add(acc, grad_rows, r, self.n, 0, None, stream=stream)
@@ -456,9 +489,33 @@ class SparDLStep(_Checkpoint):
                           self.member if self.fused else None, stream=stream)
 
     def collect(self, stream=None):
+        """The residual collection now (with fuse_collect: the next add's, after
+        which acc holds the residual)."""
+        if self.fuse_collect:
+            self.pending = [True] * self.P
+            return
+        self._collect(stream)
+
+    def _collect(self, stream=None):
         residual_collect(self.acc, self.P, self.n, self.k_blk, self.local_idx, self.sp_idx, self.drop_idx,
                          self.drop_val, self.drop_cnt, self.ws, self.member if self.fused else None,
                          stream=stream)
+
+    def flush(self, stream=None):
+        """Run a pending residual collection on its own, so that acc holds the residual."""
+        if any(self.pending):
+            if not all(self.pending):
+                raise ValueError("a partly applied collection")
+            self._collect(stream)
+            self.pending = [False] * self.P
+
+    def state_dict(self) -> dict:
+        self.flush()
+        return super().state_dict()
+
+    def load_state_dict(self, d: dict) -> None:
+        super().load_state_dict(d)
+        self.pending = [False] * self.P
 
     def finish(self, stream=None):
         """The SRS steps, the decode and the residual collection, after every

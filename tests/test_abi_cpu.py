@@ -242,6 +242,21 @@ def test_argument_errors_enqueue_nothing():
                                       null) == EINVAL
     assert lib.spardl_team_residual_add(p, i64(1199), p, i64(1200), i32(12), i32(4), i64(1200), i32(5), p, big,
                                         null) == EINVAL
+    # residual add with the previous step's collection (P = 4: two SRS steps): member, local_idx, ws and
+    # every drop pointer required; rows inside [0, P); a workspace too small
+    ac = lambda ld, w0, nw, li, mem, a, ws, wsz: lib.spardl_residual_add_collect(
+        p, i64(ld), p, i64(100), i32(w0), i32(nw), i64(100), i32(4), i32(3), li, mem, a, a, a, ws, wsz, null)
+    assert ac(100, 0, 4, p, null, ok3, p, big) == EINVAL
+    assert ac(100, 0, 4, null, p, ok3, p, big) == EINVAL
+    assert ac(100, 0, 4, p, ctypes.c_void_p(0x1002), ok3, p, big) == EINVAL
+    assert ac(100, 0, 4, p, p, arr, p, big) == EINVAL
+    assert ac(100, 0, 4, p, p, null, p, big) == EINVAL
+    assert ac(100, 0, 4, p, p, ok3, null, big) == EINVAL
+    assert ac(100, 0, 4, p, p, ok3, q, big) == EINVAL
+    assert ac(99, 0, 4, p, p, ok3, p, big) == EINVAL
+    assert ac(100, 2, 3, p, p, ok3, p, big) == EINVAL
+    assert ac(100, -1, 1, p, p, ok3, p, big) == EINVAL
+    assert ac(100, 0, 4, p, p, ok3, p, sz(64)) == ECAP
     # team residual collect (Q = 3: two rounds of drops): member required and aligned, every drop pointer, d | P
     tc = lambda d_, mem, a: lib.spardl_team_residual_collect(p, i64(1200), i32(12), i32(d_), i64(1200), i32(5), p,
                                                              mem, a, a, a, null)

@@ -4,8 +4,11 @@ produced on the CPU (tests/golden/full_digests.py; tests/digest.py defines
 the output streams and the checksum).
 
 Covered: the VGG-16-, BERT- and GPT-2-XL-sized workloads (eager and lazy
-sparsification) and the ResNet-50-sized workload with d = 2, 4, 8 teams
-joined by R-SAG and by B-SAG, every step of each with the residual carried.
+sparsification; eager also with each step's residual collection left to the
+next step's add, compared with the same checksums: every output of every
+step but the pending residual, and the residual after the last step's
+flush) and the ResNet-50-sized workload with d = 2, 4, 8 teams joined by
+R-SAG and by B-SAG, every step of each with the residual carried.
 Besides the checksums, the membership bitmap of the final index set is
 compared with the final blocks the GPU holds, and B-SAG's final blocks with
 their sentinel padding, on the device.
@@ -30,7 +33,8 @@ if gpu_available():
     from tests.digest import device_digest, device_streams
 
 GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden")
-CASES = [(3, "eager", 1), (4, "eager", 1), (5, "eager", 1), (3, "lazy", 1), (4, "lazy", 1), (5, "lazy", 1),
+CASES = [(3, "eager", 1), (4, "eager", 1), (5, "eager", 1), (3, "eager_fc", 1), (4, "eager_fc", 1), (5, "eager_fc", 1),
+         (3, "lazy", 1), (4, "lazy", 1), (5, "lazy", 1),
          (2, "rsag", 2), (2, "rsag", 4), (2, "rsag", 8), (2, "bsag", 2), (2, "bsag", 4), (2, "bsag", 8)]
 INT32_MAX = 2 ** 31 - 1
 
@@ -53,6 +57,8 @@ def _check_member(st, finals, n):
 
 
 def _run(workload, form, d):
+    fc = form == "eager_fc"   # the same outputs as the eager form
+    form = "eager" if fc else form
     gold = _gold(workload, form, d)
     wl = W.config(workload)
     P, n, kb = wl.P, wl.n, wl.k_blk
@@ -71,7 +77,7 @@ def _run(workload, form, d):
     elif form == "lazy":
         st = spardl.SparDLLazyStep(P, n, kb, rows_per_call=1 if per_worker else 0)
     else:
-        st = spardl.SparDLStep(P, n, kb, rows_per_call=1 if per_worker else 0)
+        st = spardl.SparDLStep(P, n, kb, rows_per_call=1 if per_worker else 0, fuse_collect=fc)
     g = torch.empty((1 if per_worker else P, n), dtype=torch.float32, device="cuda")
     for t in range(1, wl.steps + 1):
         if per_worker:
@@ -85,6 +91,9 @@ def _run(workload, form, d):
             for w in range(P):
                 gen.fill(g[w], t, w)
             st.step(g)
+        pending = fc and t < wl.steps   # the residual is collected by the next step's add
+        if fc and not pending:
+            st.flush()
         torch.cuda.synchronize()
         if form in ("rsag", "bsag"):
             for ws in st.ws_team + [st.ws_sag]:
@@ -94,8 +103,13 @@ def _run(workload, form, d):
         bad = []
         for b in range(nb):
             lo, hi = int(bounds[b]), int(bounds[b + 1])
-            got = device_digest(device_streams(form, st, P, b, lo, hi, Q=nb, d=d))
-            want = gold["digests"][str(b)][t - 1]
+            streams = device_streams(form, st, P, b, lo, hi, Q=nb, d=d)
+            if pending:
+                del streams["residual"]
+            got = device_digest(streams)
+            want = dict(gold["digests"][str(b)][t - 1])
+            if pending:
+                del want["residual"]
             assert set(got) == set(want), (sorted(got), sorted(want))
             bad += [(b, k) for k in want if got[k] != want[k]]
         assert not bad, f"step {t}: (block index, output) checksums differ: {bad[:12]}"

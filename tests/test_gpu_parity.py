@@ -228,6 +228,42 @@ def test_step_unfused(P, n, kb, kind, steps):
         compare_step(st, res, P, n, kb)
 
 
+FUSED_COLLECT_CASES = [STEP_CASES[i] for i in (0, 1, 2, 3, 4, 5, 6, 7, 8, 10)]
+
+
+@pytest.mark.parametrize("rows", [0, 1, 3])
+@pytest.mark.parametrize("P,n,kb,kind,steps", FUSED_COLLECT_CASES)
+def test_step_fused_collect(P, n, kb, kind, steps, rows):
+    """The residual collection left to the next step's add: after every add,
+    acc equals the oracle's residual plus the gradient, bit for bit; every
+    step's selections, drops and update are the oracle's; flush() leaves the
+    last residual.  rows: workers per call (0: all); rows the float4 add does
+    not take run the separate collection inside the same call."""
+    if rows > P:
+        pytest.skip("fewer workers than rows per call")
+    log(f"step fused collect P={P} n={n} kb={kb} kind={kind} steps={steps + 1} rows={rows}")
+    st = spardl.SparDLStep(P, n, kb, fuse_collect=True, rows_per_call=rows)
+    acc = np.zeros((P, n), np.float32)
+    for t in range(steps + 1):
+        grad = _rows(kind, P, n, 100 * t + P + 7)
+        g = _dev(grad)
+        for w0 in range(0, P, st.rows):
+            r = min(st.rows, P - w0)
+            st.residual_add_rows(w0, g[w0:w0 + r])
+            got = st.acc[w0:w0 + r].cpu().numpy()
+            for w in range(w0, w0 + r):
+                assert_bits_equal(got[w - w0], so.residual_add(acc[w], grad[w]), f"add step {t} worker {w}")
+            st.block_topk_rows(w0, r)
+        st.finish()
+        check_ws(st)
+        res = so.spardl_step([acc[w] for w in range(P)], [grad[w] for w in range(P)], P, n, kb)
+        compare_step(st, res, P, n, kb, residual=False)
+    st.flush()
+    check_ws(st)
+    for w in range(P):
+        assert_bits_equal(st.acc[w].cpu().numpy(), acc[w], f"residual after flush worker {w}")
+
+
 @pytest.mark.parametrize("P,n,kb,rows", [(8, 50000, 100, 1), (7, 70001, 501, 3), (5, 10007, 3, 2)])
 def test_step_rows_per_call(P, n, kb, rows):
     """Workers a few at a time (a workspace for `rows` rows): the same step."""
