@@ -41,6 +41,7 @@ struct Layout {
   size_t err = 0, bitmap = 0, hist1 = 0, spec_t1 = 0, spec_used = 0, spec_cnt = 0, state = 0, slot_cnt = 0,
          slot_nbin = 0, pre_all = 0, pre_ge = 0, pre_eq = 0, keep = 0, dtile = 0;
   int64_t dtile_pairs = 0;   // (pair, step) lists of all rows over the SRS steps
+  uint32_t hcopies = HCOPIES_MIN;   // level-1 histogram copies per unit
   size_t fixed_end = 0;
   int64_t units = 0, tiles_tk = 0, tiles_mg = 0, slot_n = 0, pairs_max = 0, add_tiles = 0;
 };
@@ -63,7 +64,8 @@ Layout make_layout(int32_t P, int64_t n, int32_t kb, int32_t rows = 0) {
   L.bitmap = off;
   off += align256((size_t)ceil_div(n, 32) * 4);
   L.hist1 = off;
-  off += align256((size_t)L.units * HCOPIES * NB1 * 4);
+  L.hcopies = hist_copies_for(n, P);
+  off += align256((size_t)L.units * L.hcopies * NB1 * 4);
   // speculative candidates of the fused residual add: per (worker, block) the
   // previous threshold bin + 1 (0: none) and the floor used; per add tile the count
   L.add_tiles = add_tiles_per_block(maxlen);
@@ -266,7 +268,7 @@ int topk_units(const float* acc, int64_t ld_acc, int64_t units, const Units& U, 
   const bool v4 = aligned16(acc) && ld_acc % 4 == 0 && blocks_vec4(n, P);
   const int32_t smax = (int32_t)L.tiles_tk;
   if (make_hist) {
-    SPARDL_TRY(launch_fill(Fill().add(w.hist1, units * HCOPIES * NB1).r, stream));
+    SPARDL_TRY(launch_fill(Fill().add(w.hist1, units * L.hcopies * NB1).r, stream));
     SPARDL_TRY(launch_hist1(acc, ld_acc, units, U, n, P, v4, w.hist1, stream));
   }
   // the previous-threshold hint feeds the next fused add: kept unless this is a
@@ -408,7 +410,7 @@ int spardl_workspace_init(int32_t nworkers, int32_t P, int64_t n, int32_t k_blk,
   SPARDL_TRY(launch_fill(Fill()
                              .add(w.err, 64)
                              .add(w.bitmap, ceil_div(n, 32))
-                             .add(w.hist1, L.units * HCOPIES * NB1)
+                             .add(w.hist1, L.units * L.hcopies * NB1)
                              .add(w.spec_t1, (int64_t)P * P)
                              .add(w.keep, (int64_t)P * P * KEEP_WORDS)
                              .add((uint32_t*)w.dtile, L.dtile_pairs * L.add_tiles * 2)
@@ -834,7 +836,7 @@ int spardl_team_workspace_init(int32_t P, int32_t d, int64_t n, int32_t k_blk, v
   SPARDL_TRY(launch_fill(Fill()
                              .add(w.err, 64)
                              .add(w.bitmap, ceil_div(n, 32))
-                             .add(w.hist1, L.units * HCOPIES * NB1)
+                             .add(w.hist1, L.units * L.hcopies * NB1)
                              .add(w.spec_t1, (int64_t)P * Q)
                              .r,
                          stream));

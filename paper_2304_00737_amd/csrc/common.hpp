@@ -29,7 +29,8 @@ constexpr int MERGE_THREADS = 256;
 constexpr int MERGE_PER_THREAD = 16;
 constexpr int MERGE_TILE = MERGE_THREADS * MERGE_PER_THREAD;   // merged positions per workgroup
 constexpr int DENSE_TILE = 8192;                 // output elements per densify workgroup (an LDS image)
-constexpr int HCOPIES = 4;                       // level-1 histogram copies per block (spreads the flush atomics)
+constexpr uint32_t HCOPIES_MIN = 4;               // level-1 histogram copies per block (spread the flush atomics)
+constexpr uint32_t HCOPIES_MAX = 32;
 
 // ---------------------------------------------------------------- merge threshold
 // A merge's union (two index-sorted top-k blocks, summed on shared indices)
@@ -128,6 +129,18 @@ __host__ __device__ __forceinline__ int64_t spans_per_block(int64_t maxlen, int6
 }
 __host__ __device__ __forceinline__ int64_t add_tiles_per_block(int64_t maxlen) {
   return spans_per_block(maxlen, ADD_TILE);
+}
+
+// Level-1 histogram copies of each of the P blocks of a row of n elements:
+// every add tile flushes its histogram into copy (workgroup mod copies), and
+// the flushes into one copy serialise on its words, so a block has a copy per
+// ~512 of its add tiles (a power of two in [HCOPIES_MIN, HCOPIES_MAX]); the
+// level-1 select sums them.  Other writers use the first HCOPIES_MIN copies.
+__host__ __device__ inline uint32_t hist_copies_for(int64_t n, int64_t P) {
+  const int64_t tiles = add_tiles_per_block((n + P - 1) / P);
+  uint32_t c = HCOPIES_MIN;
+  while (c < HCOPIES_MAX && (int64_t)c * 512 < tiles) c *= 2;
+  return c;
 }
 
 // Selection units of a block top-k call over rows (workers) w0, w0 + 1, ...:

@@ -299,7 +299,7 @@ __global__ __launch_bounds__(256) void k_residual_add4(float* __restrict__ acc, 
     tot += x;
   }
   {
-    uint32_t* __restrict__ H = sp.hist1 + ((int64_t)wb * HCOPIES + blockIdx.x % HCOPIES) * NB1;
+    uint32_t* __restrict__ H = sp.hist1 + ((int64_t)wb * sp.hcopies + blockIdx.x % sp.hcopies) * NB1;
     flush_hist(h, H);
   }
   const uint32_t tot0 = tot & 0xFFFFu, all = tot0 + (tot >> 16);
@@ -368,7 +368,7 @@ __global__ __launch_bounds__(256) void k_residual_add1(float* __restrict__ acc, 
   if (HIST) {
     if (g == 0u && threadIdx.x == 0) sp.spec_used[wb] = SPEC_NONE;   // no candidates on this path
     __syncthreads();
-    uint32_t* __restrict__ H = sp.hist1 + ((int64_t)wb * HCOPIES + blockIdx.x % HCOPIES) * NB1;
+    uint32_t* __restrict__ H = sp.hist1 + ((int64_t)wb * sp.hcopies + blockIdx.x % HCOPIES_MIN) * NB1;
     flush_hist(h, H);
   }
 }
@@ -376,7 +376,7 @@ __global__ __launch_bounds__(256) void k_residual_add1(float* __restrict__ acc, 
 // Level-1 histogram only (block_topk without a fused residual add).
 template <int VEC>
 __global__ __launch_bounds__(256) void k_hist1(const float* __restrict__ acc, int64_t ld_acc, Blocks B, Units U,
-                                               uint32_t G, uint32_t* __restrict__ hist1) {
+                                               uint32_t G, uint32_t hc, uint32_t* __restrict__ hist1) {
   __shared__ __align__(16) uint32_t h[NB1];
   const uint32_t g = blockIdx.x % G;
   uint32_t w, b;
@@ -408,7 +408,7 @@ __global__ __launch_bounds__(256) void k_hist1(const float* __restrict__ acc, in
     }
   }
   __syncthreads();
-  uint32_t* __restrict__ H = hist1 + ((int64_t)wb * HCOPIES + blockIdx.x % HCOPIES) * NB1;
+  uint32_t* __restrict__ H = hist1 + ((int64_t)wb * hc + blockIdx.x % HCOPIES_MIN) * NB1;
   flush_hist(h, H);
 }
 
@@ -425,6 +425,8 @@ hipError_t launch_residual_add(float* acc, int64_t ld_acc, const float* grad, in
                                int32_t nworkers, int64_t n, int32_t P, bool vec4, const AddSpec& sp,
                                hipStream_t s, const AddCollect& C) {
   const bool hist = sp.hist1 != nullptr;
+  AddSpec spc = sp;
+  spc.hcopies = hist_copies_for(n, P);
   if (C.member && !(hist && vec4)) return hipErrorInvalidValue;   // the fused collection needs the fused float4 add
   const int32_t PP = hist ? P : 1;
   const int64_t maxlen = (n + PP - 1) / PP;
@@ -434,15 +436,15 @@ hipError_t launch_residual_add(float* acc, int64_t ld_acc, const float* grad, in
     const uint32_t G = (uint32_t)add_tiles_per_block(maxlen);
     const dim3 grid((unsigned)((int64_t)nworkers * PP * G));
     if (C.member)
-      hipLaunchKernelGGL((k_residual_add4<true, true>), grid, dim3(256), 0, s, acc, ld_acc, grad, ld_grad, B, G, sp, C);
+      hipLaunchKernelGGL((k_residual_add4<true, true>), grid, dim3(256), 0, s, acc, ld_acc, grad, ld_grad, B, G, spc, C);
     else if (hist)
-      hipLaunchKernelGGL((k_residual_add4<true, false>), grid, dim3(256), 0, s, acc, ld_acc, grad, ld_grad, B, G, sp, C);
+      hipLaunchKernelGGL((k_residual_add4<true, false>), grid, dim3(256), 0, s, acc, ld_acc, grad, ld_grad, B, G, spc, C);
     else
-      hipLaunchKernelGGL((k_residual_add4<false, false>), grid, dim3(256), 0, s, acc, ld_acc, grad, ld_grad, B, G, sp, C);
+      hipLaunchKernelGGL((k_residual_add4<false, false>), grid, dim3(256), 0, s, acc, ld_acc, grad, ld_grad, B, G, spc, C);
   } else {
     const uint32_t G = (uint32_t)((maxlen + ADD_TILE - 1) / ADD_TILE);
     const dim3 grid((unsigned)((int64_t)nworkers * PP * G));
-    if (hist) hipLaunchKernelGGL(k_residual_add1<true>, grid, dim3(256), 0, s, acc, ld_acc, grad, ld_grad, B, G, sp);
+    if (hist) hipLaunchKernelGGL(k_residual_add1<true>, grid, dim3(256), 0, s, acc, ld_acc, grad, ld_grad, B, G, spc);
     else hipLaunchKernelGGL(k_residual_add1<false>, grid, dim3(256), 0, s, acc, ld_acc, grad, ld_grad, B, G, sp);
   }
   return hipGetLastError();
@@ -454,8 +456,9 @@ hipError_t launch_hist1(const float* acc, int64_t ld_acc, int64_t nunits, const 
   const int32_t G = (int32_t)((maxlen + ADD_TILE - 1) / ADD_TILE);
   const dim3 grid((unsigned)(nunits * G));
   const Blocks B = make_blocks(n, P);
-  if (vec4) hipLaunchKernelGGL(k_hist1<4>, grid, dim3(256), 0, s, acc, ld_acc, B, U, (uint32_t)G, hist1);
-  else hipLaunchKernelGGL(k_hist1<1>, grid, dim3(256), 0, s, acc, ld_acc, B, U, (uint32_t)G, hist1);
+  const uint32_t hc = hist_copies_for(n, P);
+  if (vec4) hipLaunchKernelGGL(k_hist1<4>, grid, dim3(256), 0, s, acc, ld_acc, B, U, (uint32_t)G, hc, hist1);
+  else hipLaunchKernelGGL(k_hist1<1>, grid, dim3(256), 0, s, acc, ld_acc, B, U, (uint32_t)G, hc, hist1);
   return hipGetLastError();
 }
 

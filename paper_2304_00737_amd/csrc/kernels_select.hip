@@ -20,8 +20,8 @@
 namespace spardl {
 
 // ============================================================================ level-1 select
-// The block's histogram is the sum of its HCOPIES copies; every load is in
-// flight before the first add.  The copies are cleared once read (the
+// The block's histogram is the sum of its hc copies (hist_copies_for);
+// four copies' loads are in flight at a time.  The copies are cleared once read (the
 // workspace keeps its histograms at zero between steps).  A histogram of the
 // fused add covers keys at or above hist_floor(its candidate floor) in fine
 // bins (L1Map in device.hpp), which decides the select exactly whenever the
@@ -33,29 +33,34 @@ __global__ __launch_bounds__(1024) void k_select1(uint32_t* __restrict__ hist1, 
                                                   Blocks B, Units U, uint32_t need, uint32_t* __restrict__ spec_t1,
                                                   const uint32_t* __restrict__ spec_used, int spec,
                                                   const float* __restrict__ acc, int64_t ld_acc, int vec4,
-                                                  uint32_t* __restrict__ err) {
+                                                  uint32_t hc, uint32_t* __restrict__ err) {
   constexpr int NT = 1024, PER = NB1 / NT;
+  static_assert(HCOPIES_MIN == 4, "copies are summed four at a time");
   __shared__ uint32_t h[NB1];
   __shared__ uint32_t scratch[24];
   uint32_t w, b;
   U.decode(blockIdx.x, B.P, &w, &b);
   const int64_t u = (int64_t)w * B.P + b;   // the block's arrays
-  uint32_t* __restrict__ H = hist1 + u * HCOPIES * NB1;
-  uint32_t r[PER][HCOPIES];
+  uint32_t* __restrict__ H = hist1 + u * hc * NB1;
+  uint32_t c[PER];
 #pragma unroll
-  for (int q = 0; q < PER; ++q)
+  for (int q = 0; q < PER; ++q) c[q] = 0u;
+  for (uint32_t k0 = 0; k0 < hc; k0 += HCOPIES_MIN) {
+    uint32_t r[PER][HCOPIES_MIN];
 #pragma unroll
-    for (int k = 0; k < HCOPIES; ++k) r[q][k] = H[k * NB1 + q * NT + threadIdx.x];
+    for (int q = 0; q < PER; ++q)
 #pragma unroll
-  for (int q = 0; q < PER; ++q) {
-    uint32_t c = 0;
+      for (uint32_t k = 0; k < HCOPIES_MIN; ++k) r[q][k] = H[(k0 + k) * NB1 + q * NT + threadIdx.x];
 #pragma unroll
-    for (int k = 0; k < HCOPIES; ++k) {
-      c += r[q][k];
-      H[k * NB1 + q * NT + threadIdx.x] = 0u;
-    }
-    h[q * NT + threadIdx.x] = c;
+    for (int q = 0; q < PER; ++q)
+#pragma unroll
+      for (uint32_t k = 0; k < HCOPIES_MIN; ++k) {
+        c[q] += r[q][k];
+        H[(k0 + k) * NB1 + q * NT + threadIdx.x] = 0u;
+      }
   }
+#pragma unroll
+  for (int q = 0; q < PER; ++q) h[q * NT + threadIdx.x] = c[q];
   const uint32_t used = spec ? spec_used[u] : SPEC_NONE;
   const L1Map M = l1_map(used);
   __syncthreads();
@@ -1768,7 +1773,7 @@ hipError_t launch_select1(uint32_t* hist1, uint32_t* state, int64_t nunits, cons
                           uint32_t need, uint32_t* spec_t1, const uint32_t* spec_used, bool spec, const float* acc,
                           int64_t ld_acc, bool vec4, uint32_t* err, hipStream_t s) {
   hipLaunchKernelGGL(k_select1, dim3((unsigned)nunits), dim3(1024), 0, s, hist1, state, make_blocks(n, P), U, need,
-                     spec_t1, spec_used, spec ? 1 : 0, acc, ld_acc, vec4 ? 1 : 0, err);
+                     spec_t1, spec_used, spec ? 1 : 0, acc, ld_acc, vec4 ? 1 : 0, hist_copies_for(n, P), err);
   return hipGetLastError();
 }
 
@@ -1803,7 +1808,7 @@ hipError_t launch_thresh(int mode, int64_t nunits, const Units& U, int64_t n, in
     a.kb = kb;
     a.smax = smax;
     a.group = mode == 0 ? (nunits * smax >= MULTI_SLOT_MIN ? BIG_GROUP0_MANY : BIG_GROUP0) : 1;
-    a.hstride = mode == 0 ? (int64_t)HCOPIES * NB1 : NB1;
+    a.hstride = mode == 0 ? (int64_t)hist_copies_for(n, P) * NB1 : NB1;
     a.hist1 = hist1;
     a.U_val = U_val;
     a.state = state;

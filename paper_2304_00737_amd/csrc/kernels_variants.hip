@@ -425,7 +425,8 @@ __global__ __launch_bounds__(256) void k_lazy_step(float* __restrict__ acc, int6
                                                    uint32_t d, uint32_t m, const int32_t* __restrict__ sp_idx,
                                                    const float* __restrict__ sp_val, float* __restrict__ saved,
                                                    const uint32_t* __restrict__ bm, int restore,
-                                                   uint32_t* __restrict__ hist1, uint32_t* __restrict__ spec_used) {
+                                                   uint32_t* __restrict__ hist1, uint32_t* __restrict__ spec_used,
+                                                   uint32_t hc) {
   __shared__ uint32_t dh[HIST ? NB1 : 1];   // histogram deltas
   const uint32_t npairs = B.P * m;
   for (uint32_t pair = blockIdx.y; pair < npairs; pair += gridDim.y) {
@@ -477,7 +478,7 @@ __global__ __launch_bounds__(256) void k_lazy_step(float* __restrict__ acc, int6
         if (k1 >= FH) atomicAdd(&dh[M.bin(k1)], 1u);
       }
       __syncthreads();
-      uint32_t* __restrict__ H = hist1 + (cu * HCOPIES + (blockIdx.x % HCOPIES)) * NB1;
+      uint32_t* __restrict__ H = hist1 + (cu * hc + (blockIdx.x % HCOPIES_MIN)) * NB1;
       for (int i = threadIdx.x; i < NB1; i += 256) {
         const uint32_t c = dh[i];   // a signed delta, added modulo 2^32
         if (c) atomicAdd(&H[i], c);
@@ -558,10 +559,12 @@ hipError_t launch_lazy_step(float* acc, int64_t ld_acc, int32_t P, int64_t n, in
   const dim3 grid(gx, (unsigned)std::min<int64_t>((int64_t)P * m, 65535));
   if (hist1)
     hipLaunchKernelGGL(k_lazy_step<true>, grid, dim3(256), 0, s, acc, ld_acc, make_blocks(n, P), (uint32_t)kb,
-                       (uint32_t)d, (uint32_t)m, sp_idx, sp_val, saved, bm, restore ? 1 : 0, hist1, spec_used);
+                       (uint32_t)d, (uint32_t)m, sp_idx, sp_val, saved, bm, restore ? 1 : 0, hist1, spec_used,
+                       hist_copies_for(n, P));
   else
     hipLaunchKernelGGL(k_lazy_step<false>, grid, dim3(256), 0, s, acc, ld_acc, make_blocks(n, P), (uint32_t)kb,
-                       (uint32_t)d, (uint32_t)m, sp_idx, sp_val, saved, bm, restore ? 1 : 0, hist1, spec_used);
+                       (uint32_t)d, (uint32_t)m, sp_idx, sp_val, saved, bm, restore ? 1 : 0, hist1, spec_used,
+                       hist_copies_for(n, P));
   return hipGetLastError();
 }
 

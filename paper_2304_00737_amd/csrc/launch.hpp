@@ -17,13 +17,14 @@ struct FillRanges {
 
 // Workspace arrays of the fused residual add (all null: plain add).
 struct AddSpec {
-  uint32_t* hist1 = nullptr;       // level-1 histograms, HCOPIES per (worker, block)
+  uint32_t* hist1 = nullptr;       // level-1 histograms, hist_copies_for(n, P) per (worker, block)
   const uint32_t* spec_t1 = nullptr;  // previous threshold bin + 1 per (worker, block), 0 = none
   const uint32_t* spec_prev = nullptr;   // the hints of the worker before row 0 (null: only each row's own)
   uint32_t* spec_used = nullptr;   // floor used for the speculative candidates per (worker, block)
   uint32_t* spec_cnt = nullptr;    // speculative candidates per add tile
   int32_t* cand_idx = nullptr;     // candidate index / value arrays (row-sized)
   float* cand_val = nullptr;
+  uint32_t hcopies = HCOPIES_MIN;  // histogram copies per (worker, block) (set by the launcher)
 };
 
 // The previous step's global residual collection, applied by the fused

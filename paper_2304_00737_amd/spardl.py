@@ -351,7 +351,11 @@ def ws_layout(P: int, n: int, kb: int, ws_bytes: int) -> dict:
     slot_n = max(P * P * tiles_tk, pairs_max * tiles_mg)
     L, off = {"add_tiles": add_tiles}, 256
     L["bitmap"] = off; off += al(-(-n // 32) * 4)
-    L["hist1"] = off; off += al(units * 4 * 4096 * 4)     # 4 level-1 histogram copies per unit
+    copies = 4                                           # level-1 histogram copies per unit: one per ~512
+    while copies < 32 and copies * 512 < add_tiles:      # add tiles of a block, a power of two in [4, 32]
+        copies *= 2
+    L["hcopies"] = copies
+    L["hist1"] = off; off += al(units * copies * 4096 * 4)
     L["spec_t1"] = off; off += al(P * P * 4)
     L["spec_used"] = off; off += al(P * P * 4)
     L["spec_cnt"] = off; off += al(P * P * add_tiles * 4)

@@ -286,7 +286,9 @@ def test_ws_layout_mirror():
     from tests.gpu_util import ws_layout
     lib = _lib()
     al = lambda x: (x + 255) & ~255
+    # (the last three have blocks of 3357, 8423 and 22889 add tiles: 8, 32 and 32 histogram copies)
     for P, n, kb in [(1, 5000, 7), (4, 1 << 20, 2622), (5, 6000, 1200), (8, 25_600_000, 32_000), (16, 65536, 41),
-                     (12, 60000, 50), (3, 100003, 33334)]:
+                     (12, 60000, 50), (3, 100003, 33334), (16, 110_000_000, 68_750), (8, 138_000_000, 86_250),
+                     (32, 1_500_000_000, 46_875)]:
         L = ws_layout(P, n, kb, 0)
         assert L["fixed_end"] + 3 * al(L["cand_entries"] * 4) == lib.spardl_workspace_bytes(P, P, n, kb), (P, n, kb)
