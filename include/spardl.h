@@ -200,7 +200,8 @@ int spardl_sparse_merge_topk(int32_t* sp_idx, float* sp_val, int32_t P, int64_t 
 /* The same SRS step without a workspace, for callers that cannot allocate
  * device memory (code under HIP graph capture, tight serving loops, hosts
  * that forbid hipMalloc).  Its scratch (per merge pair: the level-1
- * histogram, selection state, slot counts and the summed union) lives in one
+ * histogram, selection state, slot counts, the summed union and its sorted
+ * key bits) lives in one
  * array of SPARDL_NOALLOC_SCRATCH_BYTES inside the library, which every GPU
  * the library runs on holds from its first such call until the process ends;
  * the call allocates nothing, and it neither synchronises nor copies.
@@ -214,10 +215,10 @@ int spardl_sparse_merge_topk(int32_t* sp_idx, float* sp_val, int32_t P, int64_t 
  * Errors: as spardl_sparse_merge_topk (EINVAL also for NULL err);
  * ECAPACITY when the step needs more than SPARDL_NOALLOC_SCRATCH_BYTES of
  * scratch, checked before any GPU call: each of the P m merge pairs of the
- * step (m = its bag_blocks) takes 16 KiB + 64 bytes, plus 32 KiB + 20 bytes
+ * step (m = its bag_blocks) takes 16 KiB + 64 bytes, plus 48 KiB + 20 bytes
  * per slot of 4096 merged positions (ceil(2 k_blk / 4096) slots), each
  * array rounded up to 256 bytes (the ResNet-50-sized step 1: 32 pairs,
- * 16 slots each, 16.5 MiB); EDEVICE if the scratch's device address cannot
+ * 16 slots each, 24.5 MiB); EDEVICE if the scratch's device address cannot
  * be obtained. */
 #define SPARDL_NOALLOC_SCRATCH_BYTES (64u << 20)
 int spardl_sparse_merge_topk_noalloc(int32_t* sp_idx, float* sp_val, int32_t P, int64_t n, int32_t k_blk,
