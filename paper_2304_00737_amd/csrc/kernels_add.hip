@@ -91,9 +91,10 @@ __global__ __launch_bounds__(256) void k_residual_add4(float* __restrict__ acc, 
   __shared__ uint32_t c_cum[COLL ? COLLECT_MAX_STEPS + 1 : 1];
   __shared__ const int32_t* c_di[COLL ? COLLECT_MAX_STEPS : 1];
   __shared__ const float* c_dv[COLL ? COLLECT_MAX_STEPS : 1];
-  const uint32_t g = blockIdx.x % G;
-  const uint32_t wb = blockIdx.x / G;
-  const uint32_t b = wb % B.P, w = wb / B.P;
+  // grid: x = tile of the block, y = block, z = row (no division decodes it)
+  const uint32_t g = blockIdx.x;
+  const uint32_t b = blockIdx.y, w = blockIdx.z;
+  const uint32_t wb = w * B.P + b;
   const uint32_t s = B.start(b), e = B.start(b + 1u);
   const uint32_t ta = block_origin(s) + g * (uint32_t)ADD_TILE;
   if (ta >= e) return;
@@ -299,7 +300,7 @@ __global__ __launch_bounds__(256) void k_residual_add4(float* __restrict__ acc, 
     tot += x;
   }
   {
-    uint32_t* __restrict__ H = sp.hist1 + ((int64_t)wb * sp.hcopies + blockIdx.x % sp.hcopies) * NB1;
+    uint32_t* __restrict__ H = sp.hist1 + ((int64_t)wb * sp.hcopies + (g & (sp.hcopies - 1u))) * NB1;   // a power of 2
     flush_hist(h, H);
   }
   const uint32_t tot0 = tot & 0xFFFFu, all = tot0 + (tot >> 16);
@@ -434,7 +435,7 @@ hipError_t launch_residual_add(float* acc, int64_t ld_acc, const float* grad, in
   if (vec4) {
     // tiles from each block's aligned origin: up to 31 more elements per block
     const uint32_t G = (uint32_t)add_tiles_per_block(maxlen);
-    const dim3 grid((unsigned)((int64_t)nworkers * PP * G));
+    const dim3 grid(G, (unsigned)PP, (unsigned)nworkers);
     if (C.member)
       hipLaunchKernelGGL((k_residual_add4<true, true>), grid, dim3(256), 0, s, acc, ld_acc, grad, ld_grad, B, G, spc, C);
     else if (hist)
