@@ -20,8 +20,8 @@ P, N, KB = 6, 60000, 90
 
 
 def _make(form):
-    if form == "eager":
-        return spardl.SparDLStep(P, N, KB)
+    if form in ("eager", "eager_fc"):   # eager_fc: each collection inside the next step's add
+        return spardl.SparDLStep(P, N, KB, fuse_collect=form == "eager_fc")
     if form == "lazy":
         return spardl.SparDLLazyStep(P, N, KB)
     if form == "rsag":
@@ -30,13 +30,15 @@ def _make(form):
 
 
 def _outputs(st):
+    if hasattr(st, "flush"):
+        st.flush()   # the last step's pending collection, if any
     t = [st.acc, st.dense, st.sp_idx, st.sp_val]
     if hasattr(st, "info"):
         t.append(st.info)
     return [x.cpu().numpy().tobytes() for x in t]
 
 
-@pytest.mark.parametrize("form", ["eager", "lazy", "rsag", "bsag"])
+@pytest.mark.parametrize("form", ["eager", "eager_fc", "lazy", "rsag", "bsag"])
 def test_resume_from_checkpoint(form):
     log(f"checkpoint and resume: {form}")
     rows = 8 if form == "rsag" else P

@@ -83,10 +83,21 @@ def _nan_aware_bits_equal(got, want, what):
     assert np.array_equal(g.view(np.uint32)[~wn], w.view(np.uint32)[~wn]), f"{what}: values differ"
 
 
+def _final_residual(st, acc, eq) -> None:
+    """With the collection left to the next add: run it, then compare acc."""
+    st.flush()
+    check_ws(st)
+    for w in range(st.P):
+        eq(st.acc[w].cpu().numpy(), acc[w], f"residual after flush worker {w}")
+
+
+# fc: each step's residual collection inside the next step's add (the residual is compared after a flush)
+@pytest.mark.parametrize("fc", [False, True])
 @pytest.mark.parametrize("P,n,kb", [(4, 40000, 60), (5, 30011, 25)])
-def test_infinities_overflow_zeros_subnormals_bit_exact(P, n, kb):
-    log(f"non-finite step P={P} n={n} kb={kb}: +-Inf, overflowing merges, signed zeros, subnormals")
-    st = spardl.SparDLStep(P, n, kb)
+def test_infinities_overflow_zeros_subnormals_bit_exact(P, n, kb, fc):
+    log(f"non-finite step P={P} n={n} kb={kb} fused collection={fc}: +-Inf, overflowing merges, signed zeros, "
+        f"subnormals")
+    st = spardl.SparDLStep(P, n, kb, fuse_collect=fc)
     acc = np.zeros((P, n), F32)
     with np.errstate(over="ignore", invalid="ignore"):
         for t in range(3):
@@ -94,16 +105,19 @@ def test_infinities_overflow_zeros_subnormals_bit_exact(P, n, kb):
             st.step(_dev(grad))
             check_ws(st)
             res = so.spardl_step([acc[w] for w in range(P)], [grad[w] for w in range(P)], P, n, kb)
-            compare_step(st, res, P, n, kb)
+            compare_step(st, res, P, n, kb, residual=not fc)
             dense = st.dense.cpu().numpy()
             assert np.isinf(dense).any(), "infinities reach the update"
+    if fc:
+        _final_residual(st, acc, gu.assert_bits_equal)
 
 
+@pytest.mark.parametrize("fc", [False, True])
 @pytest.mark.parametrize("P,n,kb", [(4, 40000, 60), (3, 20011, 30)])
-def test_nans_positions_exact(P, n, kb, monkeypatch):
-    log(f"NaN step P={P} n={n} kb={kb}: NaN inputs and Inf + -Inf in a merge")
+def test_nans_positions_exact(P, n, kb, fc, monkeypatch):
+    log(f"NaN step P={P} n={n} kb={kb} fused collection={fc}: NaN inputs and Inf + -Inf in a merge")
     monkeypatch.setattr(gu, "assert_bits_equal", _nan_aware_bits_equal)
-    st = spardl.SparDLStep(P, n, kb)
+    st = spardl.SparDLStep(P, n, kb, fuse_collect=fc)
     acc = np.zeros((P, n), F32)
     with np.errstate(over="ignore", invalid="ignore"):
         for t in range(2):
@@ -111,5 +125,7 @@ def test_nans_positions_exact(P, n, kb, monkeypatch):
             st.step(_dev(grad))
             check_ws(st)
             res = so.spardl_step([acc[w] for w in range(P)], [grad[w] for w in range(P)], P, n, kb)
-            compare_step(st, res, P, n, kb)
+            compare_step(st, res, P, n, kb, residual=not fc)
             assert np.isnan(st.dense.cpu().numpy()).any(), "NaNs reach the update"
+    if fc:
+        _final_residual(st, acc, _nan_aware_bits_equal)
