@@ -315,8 +315,9 @@ def main() -> int:
                           / args.steps - marker_ms, 0.0) for ci, c in enumerate(calls)}
 
     # ---- dominant kernel: the residual add is one kernel per call (with the
-    # collection fused in, the call's small drop-index build and the add); each
-    # call is bracketed by an event pair on its stream (marker cost removed)
+    # previous step's collection fused in; its drop index is built by the
+    # collect call); each launch is bracketed by an event pair on its stream
+    # (marker cost removed)
     g0 = grads[0]
     k_mid = [(ev(), ev()) for _ in range(args.steps)]
     for j in range(args.steps):

@@ -70,7 +70,7 @@ enum {
  * selection without exactly k_blk entries); bits 2-5 tell which check. */
 #define SPARDL_WS_ERR_LOOKBACK 1u  /* reserved (no kernel waits on another workgroup) */
 #define SPARDL_WS_ERR_COUNT 2u     /* a selection's counts are inconsistent */
-#define SPARDL_WS_ERR_DROPS 64u    /* spardl_residual_add_collect: a drop list not sorted inside its block */
+#define SPARDL_WS_ERR_DROPS 64u    /* spardl_residual_collect_index: a drop list not sorted inside its block */
 
 /* Flag for spardl_block_topk: the level-1 |v| histograms (and speculative
  * candidates) of acc are already in ws, written by the immediately preceding
@@ -152,17 +152,37 @@ int spardl_residual_add(float* acc, int64_t ld_acc, const float* grad, int64_t l
  * workers; they may be NULL when P = 1).  acc, grad, local_idx: the rows
  * w0 .. w0 + nworkers - 1 (local_idx as spardl_block_topk wrote it; read
  * only for rows the float4 add does not take, which are collected by the
- * separate kernels before the add).  The call builds a per-tile index of
- * the drops in ws before the add.
+ * separate kernels before the add).  The drops are read through a per-tile
+ * index that spardl_residual_collect_index must have built in ws after the
+ * previous step's SRS steps, for these rows and these drop lists.
  * Errors: as for spardl_residual_add with ws, plus EINVAL for NULL
- * local_idx, member or ws, a misaligned member, or a NULL drop pointer.  The
- * error word gets SPARDL_WS_ERR_DROPS if a drop list is not sorted by index
- * inside its block. */
+ * local_idx, member or ws, a misaligned member, or a NULL drop pointer. */
 int spardl_residual_add_collect(float* acc, int64_t ld_acc, const float* grad, int64_t ld_grad, int32_t w0,
                                 int32_t nworkers, int64_t n, int32_t P, int32_t k_blk, const int32_t* local_idx,
                                 const uint32_t* member, const int32_t* const* drop_idx,
                                 const float* const* drop_val, const int32_t* const* drop_cnt, void* ws,
                                 size_t ws_bytes, hipStream_t stream);
+
+/* The first half of a residual collection left to the next add: for the
+ * rows w0 .. w0 + nworkers - 1, every SRS step and every add tile, the range
+ * of the row's drops inside the tile, written into ws (the drop lists are
+ * index-sorted inside their blocks, as spardl_sparse_merge_topk writes them).
+ * Call it once after a step's SRS steps, before the next step's
+ * spardl_residual_add_collect of the same rows.  drop_idx / drop_cnt: HOST
+ * arrays of l DEVICE pointers, as for spardl_residual_collect.  Nothing is
+ * enqueued where the add collects without an index (P = 1, P > 256, or
+ * blocks not float4-aligned).
+ * The index lives in the part of the workspace that does not grow with its
+ * rows, so any workspace for these sizes holds it (a workspace for fewer
+ * rows than P included).
+ * Errors: EINVAL for NULL or misaligned ws, rows outside [0, P), invalid
+ * sizes, a NULL drop pointer; ECAPACITY if ws is smaller than
+ * spardl_workspace_bytes(1, P, n, k_blk).  The error word
+ * gets SPARDL_WS_ERR_DROPS if a drop list is not sorted by index inside its
+ * block. */
+int spardl_residual_collect_index(int32_t w0, int32_t nworkers, int64_t n, int32_t P, int32_t k_blk,
+                                  const int32_t* const* drop_idx, const int32_t* const* drop_cnt, void* ws,
+                                  size_t ws_bytes, hipStream_t stream);
 
 /* Block-wise top-k (Sec. III-B: every worker sparsifies each of its P blocks
  * to its top k/P values; top-k as in Sec. II).  For w < nworkers, b < P:

@@ -7,6 +7,7 @@
 
 #include <algorithm>
 #include <mutex>
+#include <vector>
 
 #include "../../include/spardl.h"
 #include "common.hpp"
@@ -368,6 +369,30 @@ void* noalloc_scratch(hipStream_t stream) {
   return g_scratch_addr[dev];
 }
 
+// The collection arguments of the rows from w0 on: per SRS step its drop
+// arrays, bag size and its part of the workspace's drop-tile index.
+AddCollect add_collect_args(int32_t P, int32_t l, int32_t w0, int32_t k_blk, const uint32_t* member,
+                            const int32_t* const* drop_idx, const float* const* drop_val, const Ws& w,
+                            const Layout& L) {
+  AddCollect C;
+  C.member = member;
+  C.keep = w.keep;
+  C.l = l;
+  C.w0 = (uint32_t)w0;
+  C.kb = (uint32_t)k_blk;
+  C.G = (uint32_t)L.add_tiles;
+  int64_t pairs_before = 0;
+  for (int32_t i = 1; i <= l; ++i) {
+    const int32_t m = bag_of(P, l, i);
+    C.didx[i - 1] = drop_idx[i - 1];
+    C.dval[i - 1] = drop_val[i - 1];
+    C.m[i - 1] = (uint32_t)m;
+    C.tile[i - 1] = w.dtile + pairs_before * L.add_tiles;
+    pairs_before += (int64_t)P * m;
+  }
+  return C;
+}
+
 }  // namespace
 
 extern "C" {
@@ -488,24 +513,39 @@ int spardl_residual_add_collect(float* acc, int64_t ld_acc, const float* grad, i
     SPARDL_TRY(launch_residual_add(acc, ld_acc, grad, ld_grad, nworkers, n, P, v4, sp, stream));
     return SPARDL_OK;
   }
-  AddCollect C;
-  C.member = member;
-  C.keep = w.keep;
-  C.l = l;
-  C.w0 = (uint32_t)w0;
-  C.kb = (uint32_t)k_blk;
-  C.G = (uint32_t)L.add_tiles;
-  int64_t pairs_before = 0;
-  for (int32_t i = 1; i <= l; ++i) {
-    const int32_t m = bag_of(P, l, i);
-    C.didx[i - 1] = drop_idx[i - 1];
-    C.dval[i - 1] = drop_val[i - 1];
-    C.m[i - 1] = (uint32_t)m;
-    C.tile[i - 1] = w.dtile + pairs_before * L.add_tiles;
-    pairs_before += (int64_t)P * m;
+  const AddCollect C = add_collect_args(P, l, w0, k_blk, member, drop_idx, drop_val, w, L);
+  SPARDL_TRY(launch_residual_add(acc, ld_acc, grad, ld_grad, nworkers, n, P, v4, sp, stream, C));
+  return SPARDL_OK;
+}
+
+int spardl_residual_collect_index(int32_t w0, int32_t nworkers, int64_t n, int32_t P, int32_t k_blk,
+                                  const int32_t* const* drop_idx, const int32_t* const* drop_cnt, void* ws,
+                                  size_t ws_bytes, hipStream_t stream) {
+  if (!ws || ws_misaligned(ws) || nworkers < 1 || nworkers > P || w0 < 0 || w0 > P - nworkers ||
+      !sizes_ok(P, n, k_blk))
+    return SPARDL_EINVAL;
+  const int32_t l = steps_of(P);
+  if (l > 0 && (!drop_idx || !drop_cnt)) return SPARDL_EINVAL;
+  for (int32_t i = 0; i < l; ++i)
+    if (!drop_idx[i] || !drop_cnt[i]) return SPARDL_EINVAL;
+  // the index lives in the part of every workspace for these sizes that does not grow with its rows
+  const size_t need = spardl_workspace_bytes(1, P, n, k_blk);
+  if (need == 0) return SPARDL_EINVAL;
+  if (ws_bytes < need) return SPARDL_ECAPACITY;
+  if (l == 0 || l > COLLECT_MAX_STEPS || !blocks_vec4(n, P)) return SPARDL_OK;   // the add collects without an index
+  const Layout L = make_layout(P, n, k_blk);
+  Ws w = carve(ws, ws_bytes, L);
+  std::vector<const float*> no_val(l, nullptr);
+  const AddCollect C = add_collect_args(P, l, w0, k_blk, nullptr, drop_idx, no_val.data(), w, L);
+  // the rows' part of the index is cleared first (the build writes only tiles with drops)
+  for (int32_t i0 = 0; i0 < l; i0 += FILL_MAX) {
+    Fill f;
+    for (int32_t i = i0; i < std::min(l, i0 + FILL_MAX); ++i)
+      f.add((uint32_t*)(C.tile[i] + (int64_t)w0 * C.m[i] * L.add_tiles),
+            (int64_t)nworkers * C.m[i] * L.add_tiles * 2);
+    SPARDL_TRY(launch_fill(f.r, stream));
   }
   SPARDL_TRY(launch_drop_tiles(C, drop_cnt, nworkers, n, P, w.err, stream));
-  SPARDL_TRY(launch_residual_add(acc, ld_acc, grad, ld_grad, nworkers, n, P, v4, sp, stream, C));
   return SPARDL_OK;
 }
 

@@ -66,9 +66,9 @@ __global__ __launch_bounds__(256) void k_fill(FillRanges r) {
 // selected from, which nothing changed since -- and then, SRS step by step,
 // its final drops are added back.  The drops of one step are distinct
 // indices, so a step's additions run in parallel on an LDS image of the tile.
-// The separate collection's scattered writes leave ~1M partially written
-// lines in the caches, which are written back during the next add; here
-// every line of acc is written once, whole.
+// The separate collection's scattered writes leave a partly written line in
+// the caches for every index they touch, which the next add's stream then
+// writes back; here every line of acc is written once, whole.
 constexpr int ADD_STAGE = 512;          // speculative candidates (or drops) staged in LDS per tile
 
 template <bool HIST, bool COLL>
@@ -81,9 +81,10 @@ __global__ __launch_bounds__(256) void k_residual_add4(float* __restrict__ acc, 
   __shared__ int32_t s_idx[HIST ? ADD_STAGE : 1];
   __shared__ float s_val[HIST ? ADD_STAGE : 1];
   __shared__ uint32_t wtot[4];
-  // COLL: the tile image (in the histogram's space, which is cleared after
-  // the collection), its final-index bitmap words, and per SRS step the range
-  // of the worker's drops inside the tile with their arrays
+  // COLL: the tile image (in the histogram's space: each thread clears its
+  // words of it again after the collection), the tile's final-index bitmap
+  // words, and per SRS step the range of the worker's drops inside the tile
+  // with their arrays
   static_assert(NB1 >= ADD_TILE, "the tile image fits in the histogram's space");
   float* cimg = reinterpret_cast<float*>(h);
   __shared__ uint32_t cmw[COLL ? ADD_TILE / 32 : 1];
@@ -166,9 +167,7 @@ __global__ __launch_bounds__(256) void k_residual_add4(float* __restrict__ acc, 
   const uint32_t wa = C.w0 + w;   // COLL: the absolute worker
   const uint32_t tt = (b + B.P - wa % B.P) % B.P;   // COLL: this block's place in the worker's bags
   if constexpr (COLL) {
-    // one thread reads the ranges (all loads in flight together) and, after
-    // the barrier, clears them (a later index build writes only tiles with
-    // drops), so no other wave reads a cleared word
+    // one thread reads the ranges, all loads in flight together
     if (threadIdx.x == 0) {
       uint2 rr[COLLECT_MAX_STEPS];
 #pragma unroll
@@ -196,11 +195,6 @@ __global__ __launch_bounds__(256) void k_residual_add4(float* __restrict__ acc, 
     }
   }
   __syncthreads();
-  if constexpr (COLL) {
-    if (threadIdx.x == 0)
-      for (int i = 0; i < C.l; ++i)
-        if (c_hi[i] > c_lo[i]) C.tile[i][((int64_t)wa * C.m[i] + tt) * C.G + g] = make_uint2(0u, 0u);
-  }
   if constexpr (COLL) {
     // the worker's selections of this block that became final -> 0
     const uint32_t tge = k_tge, teq = k_teq, need_eq = k_need, xcut = k_cut;

@@ -127,7 +127,7 @@ __global__ __launch_bounds__(256) void k_grc_drops(float* __restrict__ acc, int6
 // sorted inside its block (an SRS step emits its drops in index order), so
 // an entry starts its tile's range if the entry before it lies in another
 // tile, and ends it if the entry after it does.  Tiles without drops keep
-// the (0, 0) the consuming add leaves.  Grid: x over a list, y over the
+// the (0, 0) the caller cleared them to.  Grid: x over a list, y over the
 // (step, pair) lists of the call's rows.
 constexpr int DT_PER = 4;   // list entries per thread of the index build
 
@@ -151,7 +151,7 @@ __global__ __launch_bounds__(256) void k_drop_tiles(DropTiles D, Blocks B, uint3
     const int32_t c = D.cnt[i][p];
     const uint32_t cnt = c < 0 ? 0u : min((uint32_t)c, C.kb);
     const int32_t* __restrict__ X = C.didx[i] + p * C.kb;
-    uint2* __restrict__ T = C.tile[i] + p * C.G;
+    uint2* __restrict__ T = const_cast<uint2*>(C.tile[i]) + p * C.G;
     const uint32_t s = B.start(b), e = B.start(b + 1u), o = block_origin(s);
     // DT_PER consecutive entries per thread, with the entries on either side
     for (uint32_t j0 = (blockIdx.x * 256u + threadIdx.x) * DT_PER; j0 < cnt; j0 += gridDim.x * 256u * DT_PER) {

@@ -40,6 +40,7 @@ _lib.spardl_workspace_init.restype = ctypes.c_int
 _lib.spardl_residual_add.argtypes = [_p, _i64, _p, _i64, _i32, _i32, _i64, _i32, _i32, _p, _sz, _p]
 _lib.spardl_residual_add_collect.argtypes = [_p, _i64, _p, _i64, _i32, _i32, _i64, _i32, _i32, _p, _p, _p, _p, _p, _p,
                                              _sz, _p]
+_lib.spardl_residual_collect_index.argtypes = [_i32, _i32, _i64, _i32, _i32, _p, _p, _p, _sz, _p]
 _lib.spardl_block_topk.argtypes = [_p, _i64, _i32, _i32, _i64, _i32, _i32, _i32, _p, _p, _p, _p, _sz, _p]
 _lib.spardl_sparse_merge_topk.argtypes = [_p, _p, _i32, _i64, _i32, _i32, _p, _p, _p, _p, _sz, _p]
 _lib.spardl_sparse_merge_topk_noalloc.argtypes = [_p, _p, _i32, _i64, _i32, _i32, _p, _p, _p, _p, _p]
@@ -65,7 +66,7 @@ _lib.spardl_bsag_workspace_bytes.restype = _sz
 _lib.spardl_bsag_workspace_init.argtypes = [_i32, _i32, _i64, _i32, _p, _sz, _p]
 _lib.spardl_bsag_exchange.argtypes = [_p, _p, _i32, _i32, _i64, _i32, _p, _p, _p, _p, _p, _sz, _p]
 _lib.spardl_bsag_residual.argtypes = [_p, _i64, _i32, _i32, _i64, _i32, _p, _p, _p, _p, _p]
-for _f in ("residual_add", "residual_add_collect", "block_topk", "sparse_merge_topk", "sparse_merge_topk_noalloc", "allgather_densify", "residual_collect",
+for _f in ("residual_add", "residual_add_collect", "residual_collect_index", "block_topk", "sparse_merge_topk", "sparse_merge_topk_noalloc", "allgather_densify", "residual_collect",
            "lazy_topk", "lazy_receive", "lazy_residual_collect", "rsag_workspace_init", "rsag_merge_topk",
            "rsag_residual", "bsag_workspace_init", "bsag_exchange", "bsag_residual", "team_workspace_init",
            "team_residual_add", "team_block_topk", "team_merge_topk", "team_residual_collect"):
@@ -155,6 +156,15 @@ def residual_add_collect(acc, grad, nworkers: int, n: int, P: int, ws, k_blk: in
     _check("residual_add_collect", _lib.spardl_residual_add_collect(
         _ptr(acc), ld_acc, _ptr(grad), ld_grad, w0, nworkers, n, P, k_blk, _ptr(local_idx), _ptr(member),
         arr(drop_idx), arr(drop_val), arr(drop_cnt), _ptr(ws), _nb(ws), _stream(stream)))
+
+
+def residual_collect_index(w0: int, nworkers: int, n: int, P: int, k_blk: int, drop_idx, drop_cnt, ws, *,
+                           stream=None) -> None:
+    """The drop-tile index the next residual_add_collect of rows w0 .. w0 + nworkers - 1 reads."""
+    l = len(drop_idx)
+    arr = lambda ts: (ctypes.c_void_p * max(l, 1))(*[_ptr(t) for t in ts]) if l else None
+    _check("residual_collect_index", _lib.spardl_residual_collect_index(
+        w0, nworkers, n, P, k_blk, arr(drop_idx), arr(drop_cnt), _ptr(ws), _nb(ws), _stream(stream)))
 
 
 def block_topk(acc, nworkers: int, n: int, P: int, k_blk: int, sp_idx, sp_val, local_idx=None, ws=None,
@@ -496,6 +506,8 @@ class SparDLStep(_Checkpoint):
         """The residual collection now (with fuse_collect: the next add's, after
         which acc holds the residual)."""
         if self.fuse_collect:
+            residual_collect_index(0, self.P, self.n, self.P, self.k_blk, self.drop_idx, self.drop_cnt, self.ws,
+                                   stream=stream)
             self.pending = [True] * self.P
             return
         self._collect(stream)
@@ -506,7 +518,9 @@ class SparDLStep(_Checkpoint):
                          stream=stream)
 
     def flush(self, stream=None):
-        """Run a pending residual collection on its own, so that acc holds the residual."""
+        """Run a pending residual collection on its own, so that acc holds the residual
+        (the drop-tile index built for it is cleared by the next index build's
+        consumer, so a fresh workspace state is restored here)."""
         if any(self.pending):
             if not all(self.pending):
                 raise ValueError("a partly applied collection")

@@ -257,6 +257,16 @@ def test_argument_errors_enqueue_nothing():
     assert ac(100, 2, 3, p, p, ok3, p, big) == EINVAL
     assert ac(100, -1, 1, p, p, ok3, p, big) == EINVAL
     assert ac(100, 0, 4, p, p, ok3, p, sz(64)) == ECAP
+    # the drop-tile index (P = 4: two SRS steps): aligned ws, rows inside [0, P), every drop pointer
+    ci = lambda w0, nw, a, ws, wsz: lib.spardl_residual_collect_index(i32(w0), i32(nw), i64(100), i32(4), i32(3),
+                                                                      a, a, ws, wsz, null)
+    assert ci(0, 4, ok3, null, big) == EINVAL
+    assert ci(0, 4, ok3, q, big) == EINVAL
+    assert ci(0, 4, arr, p, big) == EINVAL
+    assert ci(0, 4, null, p, big) == EINVAL
+    assert ci(1, 4, ok3, p, big) == EINVAL
+    assert ci(0, 0, ok3, p, big) == EINVAL
+    assert ci(0, 4, ok3, p, sz(64)) == ECAP
     # team residual collect (Q = 3: two rounds of drops): member required and aligned, every drop pointer, d | P
     tc = lambda d_, mem, a: lib.spardl_team_residual_collect(p, i64(1200), i32(12), i32(d_), i64(1200), i32(5), p,
                                                              mem, a, a, a, null)
