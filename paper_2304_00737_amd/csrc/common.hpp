@@ -25,8 +25,8 @@ constexpr int WAVE = 64;
 constexpr int ADD_F4 = 2;                        // float4 per lane per array in the residual add
 constexpr int ADD_TILE = 256 * ADD_F4 * 4;       // elements per residual-add workgroup
 constexpr int SLOT = 4096;                       // elements per candidate slot (one collect workgroup)
-constexpr int MERGE_THREADS = 256;
-constexpr int MERGE_PER_THREAD = 16;
+constexpr int MERGE_THREADS = 1024;               // a merge tile's serial steps (split search, merge,
+constexpr int MERGE_PER_THREAD = 4;                // histogram flush, bin sort) shrink with the positions per thread
 constexpr int MERGE_TILE = MERGE_THREADS * MERGE_PER_THREAD;   // merged positions per workgroup
 constexpr int DENSE_TILE = 8192;                 // output elements per densify workgroup (an LDS image)
 constexpr uint32_t HCOPIES_MIN = 4;               // level-1 histogram copies per block (spread the flush atomics)
@@ -39,15 +39,17 @@ constexpr uint32_t HCOPIES_MAX = 32;
 // the union.  Unions of up to MT_SLOTS slots therefore take a finer level 1:
 // NB1 bins of 2^FINE_SHIFT keys (1/256 binade, a window of 16 binades)
 // centred on the two blocks' median keys, each the median of the block's
-// leading FINE_SAMPLE entries (the union keeps its larger half, so its
-// threshold lies near them; a median is not moved by a few entries that
-// nearly cancelled); keys outside the window are counted in its first or
+// leading FINE_SAMPLE entries to 1/8 binade (the union keeps its larger half,
+// so its threshold lies near them; a median is not moved by a few entries
+// that nearly cancelled); keys outside the window are counted in its first or
 // last bin.  If the threshold falls in one of those two bins the threshold
-// kernel builds the 2^D1_SHIFT-key histogram itself (exact either way).
+// kernel builds the 2^D1_SHIFT-key histogram itself (exact either way, so the
+// centre only needs to be close).
 constexpr int MT_SLOTS = 1024;                   // merge slots per unit of the one-workgroup merge threshold
 constexpr int FINE_SHIFT = 15;
 constexpr uint32_t FINE_BELOW = NB1 / 2;        // fine bins from the window's first to its centre (8 binades)
 constexpr int FINE_SAMPLE = 256;                 // leading entries of each block sampled for the window
+constexpr int FINE_CENTRE_BIT = 20;              // the sampled medians' lowest key bit (1/8 binade)
 __host__ __device__ __forceinline__ bool merge_fine(int64_t kb) { return 2 * kb <= (int64_t)MT_SLOTS * MERGE_TILE; }
 
 // ---------------------------------------------------------------- state words
@@ -238,14 +240,13 @@ __device__ __forceinline__ uint32_t block_excl_scan(uint32_t v, uint32_t* scratc
   uint32_t incl = wave_incl_scan(v);
   if (lane_id() == WAVE - 1) scratch[wave_id()] = incl;
   __syncthreads();
-  if (threadIdx.x == 0) {
-    uint32_t run = 0;
-    for (int i = 0; i < nw; ++i) {
-      uint32_t t = scratch[i];
-      scratch[i] = run;
-      run += t;
-    }
-    scratch[nw] = run;
+  if (wave_id() == 0) {
+    // the wave totals' exclusive prefix, one lane per wave (at most 16 waves)
+    const int l = lane_id();
+    const uint32_t x = l < nw ? scratch[l] : 0u;
+    const uint32_t xi = wave_incl_scan(x);
+    if (l < nw) scratch[l] = xi - x;
+    if (l == WAVE - 1) scratch[nw] = xi;
   }
   __syncthreads();
   uint32_t r = scratch[wave_id()] + incl - v;

@@ -98,7 +98,8 @@ __global__ __launch_bounds__(MERGE_THREADS) void k_merge(
     }
   } else if (FINE && wv < 4) {
     // the median key among the leading entries of the held (wave 2) or received (wave 3)
-    // block: the largest T with at least half of them >= T, found bit by bit
+    // block to 1/8 binade: the largest multiple T of 2^FINE_CENTRE_BIT with at least
+    // half of them >= T, found bit by bit
     const float* __restrict__ V = wv == 2 ? Hv : Rv;
     constexpr int U = FINE_SAMPLE / WAVE;
     uint32_t key[U];
@@ -111,7 +112,7 @@ __global__ __launch_bounds__(MERGE_THREADS) void k_merge(
     }
     const uint32_t half = ((uint32_t)min(kb, FINE_SAMPLE) + 1u) / 2u;
     uint32_t T = 0;
-    for (int bit = 30; bit >= 0; --bit) {
+    for (int bit = 30; bit >= FINE_CENTRE_BIT; --bit) {
       const uint32_t c = T | (1u << bit);
       uint32_t nge = 0;
 #pragma unroll
@@ -261,28 +262,23 @@ __global__ __launch_bounds__(MERGE_THREADS) void k_merge(
     // threshold kernel: in the slot's MERGE_TILE words of U_key, the low
     // FINE_SHIFT bits of each key (uint16, bin order) and then the exclusive
     // prefix of the bin counts (uint16 per bin)
-    static_assert(NB1 == 16 * MERGE_THREADS && FINE_SHIFT <= 16, "16 bins per thread, keys' low bits in 16 bits");
+    constexpr int BPT = NB1 / MERGE_THREADS;   // bins per thread, one uint4 of LDS
+    static_assert(BPT == 4 && FINE_SHIFT <= 16, "4 bins per thread, keys' low bits in 16 bits");
     uint16_t* __restrict__ SK = reinterpret_cast<uint16_t*>(U_key + ubase);
     uint16_t* __restrict__ PRE = SK + MERGE_TILE;
-    uint32_t hc[16], sum = 0;
-#pragma unroll
-    for (int j = 0; j < 16; ++j) {
-      hc[j] = hist[16 * threadIdx.x + j];
-      sum += hc[j];
-    }
+    const uint4 h4 = reinterpret_cast<const uint4*>(hist)[threadIdx.x];
+    const uint32_t hc[BPT] = {h4.x, h4.y, h4.z, h4.w};
     uint32_t tot2;
-    uint32_t x = block_excl_scan(sum, scratch, &tot2);   // its barriers end the flush's and write-out's reads
-    uint32_t pk[8];
+    // the scan's barriers end the flush's and the write-out's reads
+    uint32_t x = block_excl_scan(hc[0] + hc[1] + hc[2] + hc[3], scratch, &tot2);
+    uint32_t ex[BPT];
 #pragma unroll
-    for (int j = 0; j < 16; ++j) {
-      hist[16 * threadIdx.x + j] = x;
-      if (j & 1) pk[j / 2] |= x << 16;
-      else pk[j / 2] = x;
+    for (int j = 0; j < BPT; ++j) {
+      ex[j] = x;
       x += hc[j];
     }
-    uint4* P4 = reinterpret_cast<uint4*>(PRE + 16 * threadIdx.x);
-    P4[0] = make_uint4(pk[0], pk[1], pk[2], pk[3]);
-    P4[1] = make_uint4(pk[4], pk[5], pk[6], pk[7]);
+    reinterpret_cast<uint4*>(hist)[threadIdx.x] = make_uint4(ex[0], ex[1], ex[2], ex[3]);
+    reinterpret_cast<uint2*>(PRE)[threadIdx.x] = make_uint2(ex[0] | (ex[1] << 16), ex[2] | (ex[3] << 16));
     __syncthreads();
     uint16_t* sk = reinterpret_cast<uint16_t*>(cI);   // the staged indices are written out already
     for (uint32_t k = threadIdx.x; k < tot; k += blockDim.x) {
