@@ -216,14 +216,38 @@ __device__ __forceinline__ int wave_id() { return threadIdx.x / WAVE; }
 __device__ __forceinline__ uint32_t popc64(uint64_t m) { return (uint32_t)__popcll(m); }
 
 // Inclusive prefix sum across the 64 lanes of a wave.
+// Wave-wide inclusive scans in DPP: Hillis-Steele steps of 1, 2, 4 and 8
+// lanes inside each row of 16 (a lane with no source in its row takes 0, the
+// identity of both operations), then the totals of the rows before each row
+// (v_readlane) added in.  Every lane of the wave must be active.
+template <int CTRL>
+__device__ __forceinline__ uint32_t dpp_shr(uint32_t v) {
+  return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, CTRL, 0xF, 0xF, false);
+}
+constexpr int DPP_ROW_SHR1 = 0x111, DPP_ROW_SHR2 = 0x112, DPP_ROW_SHR4 = 0x114, DPP_ROW_SHR8 = 0x118;
+
 __device__ __forceinline__ uint32_t wave_incl_scan(uint32_t v) {
-  const int lane = lane_id();
-#pragma unroll
-  for (int d = 1; d < WAVE; d <<= 1) {
-    uint32_t t = __shfl_up(v, d, WAVE);
-    if (lane >= d) v += t;
-  }
-  return v;
+  v += dpp_shr<DPP_ROW_SHR1>(v);
+  v += dpp_shr<DPP_ROW_SHR2>(v);
+  v += dpp_shr<DPP_ROW_SHR4>(v);
+  v += dpp_shr<DPP_ROW_SHR8>(v);
+  const uint32_t r0 = (uint32_t)__builtin_amdgcn_readlane((int)v, 15);
+  const uint32_t r1 = r0 + (uint32_t)__builtin_amdgcn_readlane((int)v, 31);
+  const uint32_t r2 = r1 + (uint32_t)__builtin_amdgcn_readlane((int)v, 47);
+  const int row = lane_id() >> 4;
+  return v + (row == 0 ? 0u : row == 1 ? r0 : row == 2 ? r1 : r2);
+}
+
+__device__ __forceinline__ uint32_t wave_incl_max(uint32_t v) {
+  v = max(v, dpp_shr<DPP_ROW_SHR1>(v));
+  v = max(v, dpp_shr<DPP_ROW_SHR2>(v));
+  v = max(v, dpp_shr<DPP_ROW_SHR4>(v));
+  v = max(v, dpp_shr<DPP_ROW_SHR8>(v));
+  const uint32_t r0 = (uint32_t)__builtin_amdgcn_readlane((int)v, 15);
+  const uint32_t r1 = max(r0, (uint32_t)__builtin_amdgcn_readlane((int)v, 31));
+  const uint32_t r2 = max(r1, (uint32_t)__builtin_amdgcn_readlane((int)v, 47));
+  const int row = lane_id() >> 4;
+  return max(v, row == 0 ? 0u : row == 1 ? r0 : row == 2 ? r1 : r2);
 }
 
 __device__ __forceinline__ uint32_t wave_sum(uint32_t v) {
@@ -237,22 +261,17 @@ __device__ __forceinline__ uint32_t wave_sum(uint32_t v) {
 // prefix and writes the workgroup total to *total.  Contains barriers.
 __device__ __forceinline__ uint32_t block_excl_scan(uint32_t v, uint32_t* scratch, uint32_t* total) {
   const int nw = blockDim.x / WAVE;
-  uint32_t incl = wave_incl_scan(v);
+  const uint32_t incl = wave_incl_scan(v);
   if (lane_id() == WAVE - 1) scratch[wave_id()] = incl;
   __syncthreads();
-  if (wave_id() == 0) {
-    // the wave totals' exclusive prefix, one lane per wave (at most 16 waves)
-    const int l = lane_id();
-    const uint32_t x = l < nw ? scratch[l] : 0u;
-    const uint32_t xi = wave_incl_scan(x);
-    if (l < nw) scratch[l] = xi - x;
-    if (l == WAVE - 1) scratch[nw] = xi;
-  }
-  __syncthreads();
-  uint32_t r = scratch[wave_id()] + incl - v;
-  *total = scratch[nw];
-  __syncthreads();
-  return r;
+  // every wave scans the wave totals itself (one lane per wave, at most 16)
+  const int l = lane_id();
+  const uint32_t x = l < nw ? scratch[l] : 0u;
+  const uint32_t xi = wave_incl_scan(x);
+  const uint32_t before = (uint32_t)__builtin_amdgcn_readlane((int)(xi - x), wave_id());
+  *total = (uint32_t)__builtin_amdgcn_readlane((int)xi, WAVE - 1);
+  __syncthreads();   // the caller may write scratch next
+  return before + incl - v;
 }
 
 // Select on a histogram in descending bin order: find bin T such that

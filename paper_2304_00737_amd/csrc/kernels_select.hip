@@ -592,12 +592,7 @@ __device__ __forceinline__ int slot_of_entry(const uint32_t* pref, int ns, uint3
 // (0 for thread 0).  `scratch` needs blockDim/64 + 1 words.  Contains barriers.
 __device__ __forceinline__ uint32_t block_excl_max(uint32_t v, uint32_t* scratch) {
   const int nw = blockDim.x / WAVE, lane = lane_id();
-  uint32_t incl = v;
-#pragma unroll
-  for (int d = 1; d < WAVE; d <<= 1) {
-    const uint32_t o = __shfl_up(incl, d, WAVE);
-    if (lane >= d) incl = max(incl, o);
-  }
+  const uint32_t incl = wave_incl_max(v);
   uint32_t excl = __shfl_up(incl, 1, WAVE);
   if (lane == 0) excl = 0u;
   if (lane == WAVE - 1) scratch[wave_id()] = incl;
