@@ -274,6 +274,29 @@ __device__ __forceinline__ uint32_t block_excl_scan(uint32_t v, uint32_t* scratc
   return before + incl - v;
 }
 
+// Three exclusive prefix sums at once (one set of barriers): v[q] becomes
+// its prefix and total[q] the workgroup total.  `scratch` needs
+// 3 blockDim/64 words of LDS.  Contains barriers.
+__device__ __forceinline__ void block_excl_scan3(uint32_t (&v)[3], uint32_t* scratch, uint32_t (&total)[3]) {
+  const int nw = blockDim.x / WAVE, l = lane_id(), w = wave_id();
+  uint32_t incl[3];
+#pragma unroll
+  for (int q = 0; q < 3; ++q) {
+    incl[q] = wave_incl_scan(v[q]);
+    if (l == WAVE - 1) scratch[q * nw + w] = incl[q];
+  }
+  __syncthreads();
+#pragma unroll
+  for (int q = 0; q < 3; ++q) {
+    const uint32_t x = l < nw ? scratch[q * nw + l] : 0u;
+    const uint32_t xi = wave_incl_scan(x);
+    const uint32_t before = (uint32_t)__builtin_amdgcn_readlane((int)(xi - x), w);
+    total[q] = (uint32_t)__builtin_amdgcn_readlane((int)xi, WAVE - 1);
+    v[q] = before + incl[q] - v[q];
+  }
+  __syncthreads();   // the caller may write scratch next
+}
+
 // Select on a histogram in descending bin order: find bin T such that
 // count(bins > T) < need <= count(bins >= T).  hist is in LDS with nb bins.
 // Every thread gets the answer.  `scratch` needs blockDim/64 + 4 words of LDS.
@@ -293,14 +316,13 @@ __device__ __forceinline__ void block_select_desc(const uint32_t* hist, int nb, 
   uint32_t ex = block_excl_scan(s, scratch, &tot);
   if (total) *total = tot;
   const int nw = nt / WAVE;
-  if (threadIdx.x == 0) scratch[nw + 1] = 0;   // found flag
-  __syncthreads();
+  // exactly one thread's bins hold the crossing when the histogram holds need >= 1 entries
+  *ok = need != 0u && tot >= need ? 1u : 0u;
   if (ex < need && ex + s >= need) {
     uint32_t run = ex;
     for (int bin = hi - 1; bin >= lo && bin >= 0; --bin) {
       uint32_t h = hist[bin];
       if (run + h >= need) {
-        scratch[nw + 1] = 1;
         scratch[nw + 2] = (uint32_t)bin;
         scratch[nw + 3] = run;
         break;
@@ -309,7 +331,6 @@ __device__ __forceinline__ void block_select_desc(const uint32_t* hist, int nb, 
     }
   }
   __syncthreads();
-  *ok = scratch[nw + 1];
   if (*ok) {
     *T = scratch[nw + 2];
     *above = scratch[nw + 3];

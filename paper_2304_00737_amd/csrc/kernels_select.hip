@@ -553,7 +553,7 @@ struct FastSmem {
       uint32_t ce[FAST_SLOTS];     // per-slot count of key == TEQ
     } c;
   } u;
-  uint32_t scratch[24];
+  uint32_t scratch[48];
 };
 
 __device__ __forceinline__ void finish_unit(uint32_t* st, uint32_t T1, uint32_t tge, uint32_t teq, uint32_t need_eq,
@@ -591,16 +591,16 @@ __device__ __forceinline__ int slot_of_entry(const uint32_t* pref, int ns, uint3
 // Exclusive prefix maximum of one value per thread over the workgroup
 // (0 for thread 0).  `scratch` needs blockDim/64 + 1 words.  Contains barriers.
 __device__ __forceinline__ uint32_t block_excl_max(uint32_t v, uint32_t* scratch) {
-  const int nw = blockDim.x / WAVE, lane = lane_id();
+  const int nw = blockDim.x / WAVE, lane = lane_id(), w = wave_id();
   const uint32_t incl = wave_incl_max(v);
   uint32_t excl = __shfl_up(incl, 1, WAVE);
   if (lane == 0) excl = 0u;
-  if (lane == WAVE - 1) scratch[wave_id()] = incl;
+  if (lane == WAVE - 1) scratch[w] = incl;
   __syncthreads();
-  uint32_t carry = 0;
-  for (int i = 0; i < wave_id(); ++i) carry = max(carry, scratch[i]);
+  // the waves before this one: every wave scans the wave maxima itself
+  const uint32_t xi = wave_incl_max(lane < nw ? scratch[lane] : 0u);
+  const uint32_t carry = w == 0 ? 0u : (uint32_t)__builtin_amdgcn_readlane((int)xi, w - 1);
   __syncthreads();
-  (void)nw;
   return max(carry, excl);
 }
 
@@ -759,10 +759,10 @@ __device__ __forceinline__ void thresh_fast_topk(FastSmem& L, int64_t unit, cons
     sg += gq[u];
     se += eq[u];
   }
-  uint32_t ta, tg, te;
-  uint32_t xa = block_excl_scan(sa, L.scratch, &ta);
-  uint32_t xg = block_excl_scan(sg, L.scratch, &tg);
-  uint32_t xe = block_excl_scan(se, L.scratch, &te);
+  uint32_t x3[3] = {sa, sg, se}, t3[3];
+  block_excl_scan3(x3, L.scratch, t3);
+  uint32_t xa = x3[0], xg = x3[1], xe = x3[2];
+  const uint32_t ta = t3[0], tg = t3[1], te = t3[2];
   const int64_t o = unit * smax;
 #pragma unroll
   for (int u = 0; u < PS; ++u) {
