@@ -640,25 +640,24 @@ __device__ __forceinline__ void thresh_fast_topk(FastSmem& L, int64_t unit, cons
   static_assert(FAST_SLOTS <= 65536, "slot ids are 16-bit");
   const int t = threadIdx.x;
   const int ns = g.nslots;
-  uint32_t nb[PS];
-  {
-    uint32_t ca0[PS];
+  // per owned slot: its entries (clamped to the slot's span) and its bin entries
+  uint32_t nb[PS], ca[PS];
 #pragma unroll
-    for (int u = 0; u < PS; ++u) {
-      const int s = PS * t + u;
-      ca0[u] = 0u;
-      nb[u] = 0u;
-      if (s < ns) {
-        ca0[u] = cnt[s];
-        nb[u] = nbn[s];
-      }
+  for (int u = 0; u < PS; ++u) {
+    const int s = PS * t + u;
+    ca[u] = 0u;
+    nb[u] = 0u;
+    if (s < ns) {
+      ca[u] = cnt[s];
+      nb[u] = nbn[s];
     }
+  }
 #pragma unroll
-    for (int u = 0; u < PS; ++u) {
-      const int s = PS * t + u;
-      const uint32_t cap = s < ns ? (uint32_t)g.cap(s) : 0u;
-      nb[u] = min(nb[u], min(ca0[u], cap));
-    }
+  for (int u = 0; u < PS; ++u) {
+    const int s = PS * t + u;
+    const uint32_t cap = s < ns ? (uint32_t)g.cap(s) : 0u;
+    ca[u] = min(ca[u], cap);
+    nb[u] = min(nb[u], ca[u]);
   }
   uint32_t sb = 0;
 #pragma unroll
@@ -741,17 +740,10 @@ __device__ __forceinline__ void thresh_fast_topk(FastSmem& L, int64_t unit, cons
     if (rk[r] != KEY_NONE) count1(rk[r], (r & 1) ? (rs[r / 2] >> 16) : (rs[r / 2] & 0xFFFFu));
   for (uint32_t c = 1; c < nchunks; ++c) visit_bin_chunk(K, L.pref, ns, g, c * FAST_CAP0, total, count1);
   __syncthreads();
-  uint32_t sa = 0, sg = 0, se = 0, ca[PS], gq[PS], eq[PS];
+  uint32_t sa = 0, sg = 0, se = 0, gq[PS], eq[PS];
 #pragma unroll
   for (int u = 0; u < PS; ++u) {
     const int s = PS * t + u;
-    ca[u] = s < ns ? cnt[s] : 0u;
-  }
-#pragma unroll
-  for (int u = 0; u < PS; ++u) {
-    const int s = PS * t + u;
-    const uint32_t cap = s < ns ? (uint32_t)g.cap(s) : 0u;
-    ca[u] = min(ca[u], cap);
     const uint32_t nbu = s < ns ? L.pref[s + 1] - L.pref[s] : 0u;   // bin entries of the slot (<= ca)
     gq[u] = s < ns ? ca[u] - nbu + L.u.c.cg[s] : 0u;                 // entries above the bin are all selected
     eq[u] = s < ns ? L.u.c.ce[s] : 0u;
@@ -1685,23 +1677,23 @@ __global__ __launch_bounds__(256) void k_emit(
     PM.decode(unit, &hb, &rb, &both);
     const int64_t o = hb * kb, o2 = both ? rb * kb : -1;   // output block(s); o2: the other side of an R-SAG exchange
     // this wave's quarter of the slot, loaded once into registers (a quarter
-    // is one chunk); the ge / eq counts of the quarters before it through LDS
+    // is one chunk) together with the loads above: a merge slot is full but
+    // for the union's last one and its holes, and its whole MERGE_TILE
+    // entries lie in the union's region (entries past the count are not
+    // used); the ge / eq counts of the quarters before it through LDS
     static_assert(MERGE_TILE == NPART * WAVE * EMIT_R, "a quarter of a merge slot is one chunk");
     __shared__ uint32_t part_cnt[2 * NPART];
-    const uint32_t p_lo = min(cnt, (uint32_t)(wv * WAVE * EMIT_R));
-    const uint32_t p_hi = min(cnt, p_lo + (uint32_t)(WAVE * EMIT_R));
+    const uint32_t q_lo = (uint32_t)(wv * WAVE * EMIT_R);
     int32_t ix[EMIT_R];
     float vx[EMIT_R];
 #pragma unroll
     for (int r = 0; r < EMIT_R; ++r) {
-      const uint32_t p = p_lo + r * WAVE + lane;
-      ix[r] = -1;
-      vx[r] = 0.f;
-      if (p < p_hi) {
-        ix[r] = cand_idx[base + p];
-        vx[r] = cand_val[base + p];
-      }
+      const uint32_t p = q_lo + r * WAVE + lane;
+      ix[r] = cand_idx[base + p];
+      vx[r] = cand_val[base + p];
     }
+    const uint32_t p_lo = min(cnt, q_lo);
+    const uint32_t p_hi = min(cnt, q_lo + (uint32_t)(WAVE * EMIT_R));
     {
       uint32_t cg = 0, ce = 0;
 #pragma unroll
