@@ -7,14 +7,21 @@ namespace spardl {
 
 typedef float f4v __attribute__((ext_vector_type(4)));
 
-// Adds the non-zero bins of an LDS histogram of NB1 bins into a global one.
-// Consecutive lanes take consecutive bins, so one wave's atomics fall on a
-// few cache lines (a lane-strided split multiplies the L2 atomic requests).
+// Adds the non-zero bins of an LDS histogram of NB1 bins into a global one,
+// by a workgroup of NT threads.  Consecutive lanes take consecutive bins
+// (thread t bins t, t + NT, ...), so one wave's atomics fall on a few cache
+// lines (a lane-strided split multiplies the L2 atomic requests); a thread
+// issues all its LDS reads before its atomics.
+template <int NT>
 __device__ __forceinline__ void flush_hist(const uint32_t* h, uint32_t* __restrict__ H) {
-  for (int i = threadIdx.x; i < NB1; i += blockDim.x) {
-    const uint32_t c = h[i];
-    if (c) atomicAdd(&H[i], c);
-  }
+  constexpr int PER = NB1 / NT;
+  static_assert(PER * NT == NB1, "whole bins per thread");
+  uint32_t c[PER];
+#pragma unroll
+  for (int k = 0; k < PER; ++k) c[k] = h[threadIdx.x + k * NT];
+#pragma unroll
+  for (int k = 0; k < PER; ++k)
+    if (c[k]) atomicAdd(&H[threadIdx.x + k * NT], c[k]);
 }
 
 // Speculative candidates of the fused residual add (kernels_add.hip) and the

@@ -295,7 +295,7 @@ __global__ __launch_bounds__(256) void k_residual_add4(float* __restrict__ acc, 
   }
   {
     uint32_t* __restrict__ H = sp.hist1 + ((int64_t)wb * sp.hcopies + (g & (sp.hcopies - 1u))) * NB1;   // a power of 2
-    flush_hist(h, H);
+    flush_hist<256>(h, H);
   }
   const uint32_t tot0 = tot & 0xFFFFu, all = tot0 + (tot >> 16);
   const uint32_t ex = base + incl - packed;
@@ -364,7 +364,7 @@ __global__ __launch_bounds__(256) void k_residual_add1(float* __restrict__ acc, 
     if (g == 0u && threadIdx.x == 0) sp.spec_used[wb] = SPEC_NONE;   // no candidates on this path
     __syncthreads();
     uint32_t* __restrict__ H = sp.hist1 + ((int64_t)wb * sp.hcopies + blockIdx.x % HCOPIES_MIN) * NB1;
-    flush_hist(h, H);
+    flush_hist<256>(h, H);
   }
 }
 
@@ -404,7 +404,7 @@ __global__ __launch_bounds__(256) void k_hist1(const float* __restrict__ acc, in
   }
   __syncthreads();
   uint32_t* __restrict__ H = hist1 + ((int64_t)wb * hc + blockIdx.x % HCOPIES_MIN) * NB1;
-  flush_hist(h, H);
+  flush_hist<256>(h, H);
 }
 
 // ============================================================================ launchers

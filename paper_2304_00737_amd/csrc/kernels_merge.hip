@@ -256,7 +256,7 @@ __global__ __launch_bounds__(MERGE_THREADS) void k_merge(
     U_idx[ubase + k] = cI[k];
     U_val[ubase + k] = cV[k];
   }
-  flush_hist(hist, hist1 + (int64_t)pair * NB1);
+  flush_hist<MERGE_THREADS>(hist, hist1 + (int64_t)pair * NB1);
   if (FINE) {
     // the tile's keys ordered by fine bin (a counting sort in LDS), for the
     // threshold kernel: in the slot's MERGE_TILE words of U_key, the low

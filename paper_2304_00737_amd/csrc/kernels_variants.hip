@@ -131,7 +131,7 @@ __global__ __launch_bounds__(256) void k_lsel_hist(ListSel S, uint32_t nch, uint
   __syncthreads();
   for (uint32_t j = j0 + threadIdx.x; j < j1; j += 256u) atomicAdd(&h[mag_key(D.iv[j]) >> D1_SHIFT], 1u);
   __syncthreads();
-  flush_hist(h, hist + (int64_t)i * NB1);
+  flush_hist<256>(h, hist + (int64_t)i * NB1);
 }
 
 // st[4 i ..]: key bound tge, tie key teq, ties to keep need_eq, entries kept
