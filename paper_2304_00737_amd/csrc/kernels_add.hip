@@ -28,6 +28,13 @@ __global__ __launch_bounds__(256) void k_fill(FillRanges r) {
   }
 }
 
+// A relaxed atomic load: an ordinary load to the hardware, which the compiler
+// keeps where it is written relative to a compiler fence (no wait follows it).
+template <typename T>
+__device__ __forceinline__ T early_load(const T* p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
 // ============================================================================ a1: residual add
 // Tiles of ADD_TILE elements start at the block's aligned origin (its start
 // rounded down to 32 elements), so every tile after a block's first begins on
@@ -102,17 +109,58 @@ __global__ __launch_bounds__(256) void k_residual_add4(float* __restrict__ acc, 
   float* __restrict__ A = acc + (int64_t)w * ld_acc;
   const float* __restrict__ Gr = grad + (int64_t)w * ld_grad;
   const uint32_t x0 = ta + threadIdx.x * 4u;
-  // block starts and ends are multiples of 4 here, so a float4 lies wholly inside or outside the block
+  // The workgroup's own words are loaded before the tile's stream: a wave's
+  // loads complete in order, so a word loaded after the stream could only be
+  // used once the whole stream had arrived.  HIST: the previous threshold
+  // hints (every wave); COLL: the drop-tile ranges of the SRS steps (thread
+  // 0; steps past RR_EARLY, only for P > 256, are loaded later).  They are
+  // relaxed atomic loads behind a compiler-only fence, which the compiler
+  // neither sinks below the stream nor waits for at once.
+  const uint32_t wa = C.w0 + w;   // COLL: the absolute worker
+  const uint32_t tt = (b + B.P - wa % B.P) % B.P;   // COLL: this block's place in the worker's bags
+  constexpr int RR_EARLY = 8;
+  uint2 rr[RR_EARLY];
+  if constexpr (COLL) {
+    if (threadIdx.x == 0) {
+#pragma unroll
+      for (int i = 0; i < RR_EARLY; ++i) {
+        rr[i] = make_uint2(0u, 0u);
+        if (i < C.l && tt < C.m[i]) {
+          const uint64_t v = early_load(reinterpret_cast<const uint64_t*>(C.tile[i] + ((int64_t)wa * C.m[i] + tt) * C.G + g));
+          rr[i] = make_uint2((uint32_t)v, (uint32_t)(v >> 32));
+        }
+      }
+    }
+  }
+  uint32_t sw = 0u, pw = 0u;
+  if constexpr (HIST) {
+    // a zero the compiler cannot see through keeps the hints in vector
+    // registers (a uniform value would be moved to a scalar one at once,
+    // which waits for the load)
+    uint32_t z;
+    asm volatile("v_mov_b32 %0, 0" : "=v"(z));
+    sw = early_load(sp.spec_t1 + wb + z);
+    // the same block's latest hint at the preceding worker: when workers run a few at
+    // a time it is this step's, a closer estimate while the residual is still growing
+    // (a threshold from the step before can lie several bins lower then); the larger
+    // of the two is used (without that hint, the worker's own again)
+    const uint32_t* pa = !sp.spec_prev ? sp.spec_t1 + wb : w == 0u ? sp.spec_prev + b : sp.spec_t1 + (wb - B.P);
+    pw = early_load(pa + z);
+  }
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_sched_barrier(0);
+  // block starts and ends are multiples of 4 here, so a float4 lies wholly
+  // inside or outside the block; one outside loads the block's first float4
+  // instead (unused), so that the loads need no branch
   bool in[2];
   f4v a[2], gg[2];
 #pragma unroll
   for (int j = 0; j < 2; ++j) {
     const uint32_t x = x0 + 1024u * j;
     in[j] = x >= s && x < e;
-    if (in[j]) {
-      a[j] = *reinterpret_cast<const f4v*>(A + x);
-      gg[j] = __builtin_nontemporal_load(reinterpret_cast<const f4v*>(Gr + x));
-    }
+    const uint32_t xl = in[j] ? x : s;
+    a[j] = *reinterpret_cast<const f4v*>(A + xl);
+    gg[j] = __builtin_nontemporal_load(reinterpret_cast<const f4v*>(Gr + xl));
   }
   // COLL: the final-index bitmap words of this thread's two float4 (the four
   // elements share a word: tiles start on 32-element boundaries)
@@ -148,15 +196,7 @@ __global__ __launch_bounds__(256) void k_residual_add4(float* __restrict__ acc, 
   // with drops clears its image's words again after the collection)
   for (int i = threadIdx.x; i < NB1 / 4; i += 256) reinterpret_cast<uint4*>(h)[i] = make_uint4(0u, 0u, 0u, 0u);
   uint32_t F = SPEC_NONE;
-  uint32_t sw = sp.spec_t1[wb];
-  if (sp.spec_prev) {
-    // the same block's latest hint at the preceding worker: when workers run a few at
-    // a time it is this step's, a closer estimate while the residual is still growing
-    // (a threshold from the step before can lie several bins lower then); the larger
-    // of the two is used
-    const uint32_t pw = w == 0u ? sp.spec_prev[b] : sp.spec_t1[wb - B.P];
-    sw = max(sw, pw);
-  }
+  sw = max(sw, pw);
   if (sw != 0u) {
     const uint32_t T1p = sw - 1u;
     F = T1p > SPEC_MARGIN ? (T1p - SPEC_MARGIN) << D1_SHIFT : 0u;
@@ -164,22 +204,17 @@ __global__ __launch_bounds__(256) void k_residual_add4(float* __restrict__ acc, 
   if (g == 0u && threadIdx.x == 0) sp.spec_used[wb] = F;
   const L1Map M = l1_map(F);
   const uint32_t FH = M.floor;
-  const uint32_t wa = C.w0 + w;   // COLL: the absolute worker
-  const uint32_t tt = (b + B.P - wa % B.P) % B.P;   // COLL: this block's place in the worker's bags
   if constexpr (COLL) {
-    // one thread reads the ranges, all loads in flight together
+    // one thread turns the ranges into the tile's drop runs
     if (threadIdx.x == 0) {
-      uint2 rr[COLLECT_MAX_STEPS];
-#pragma unroll
-      for (int i = 0; i < COLLECT_MAX_STEPS; ++i) {
-        rr[i] = make_uint2(0u, 0u);
-        if (i < C.l && tt < C.m[i]) rr[i] = C.tile[i][((int64_t)wa * C.m[i] + tt) * C.G + g];
-      }
       uint32_t cum = 0;
 #pragma unroll
       for (int i = 0; i < COLLECT_MAX_STEPS; ++i) {
         if (i < C.l) {
-          const uint32_t lo = min(rr[i].x, C.kb), hi = min(max(rr[i].y, lo), C.kb);
+          uint2 ri = make_uint2(0u, 0u);
+          if (i < RR_EARLY) ri = rr[i];
+          else if (tt < C.m[i]) ri = C.tile[i][((int64_t)wa * C.m[i] + tt) * C.G + g];
+          const uint32_t lo = min(ri.x, C.kb), hi = min(max(ri.y, lo), C.kb);
           if (hi > lo) {
             const int64_t p = (int64_t)wa * C.m[i] + tt;
             c_di[i] = C.didx[i] + p * C.kb;
