@@ -48,7 +48,7 @@ constexpr uint32_t HCOPIES_MAX = 32;
 constexpr int MT_SLOTS = 1024;                   // merge slots per unit of the one-workgroup merge threshold
 constexpr int FINE_SHIFT = 15;
 constexpr uint32_t FINE_BELOW = NB1 / 2;        // fine bins from the window's first to its centre (8 binades)
-constexpr int FINE_SAMPLE = 256;                 // leading entries of each block sampled for the window
+constexpr int FINE_SAMPLE = 64;                  // leading entries of each block sampled for the window
 constexpr int FINE_CENTRE_BIT = 20;              // the sampled medians' lowest key bit (1/8 binade)
 __host__ __device__ __forceinline__ bool merge_fine(int64_t kb) { return 2 * kb <= (int64_t)MT_SLOTS * MERGE_TILE; }
 
