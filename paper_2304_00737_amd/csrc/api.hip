@@ -581,6 +581,10 @@ int spardl_sparse_merge_topk(int32_t* sp_idx, float* sp_val, int32_t P, int64_t 
   const int64_t pairs = (int64_t)P * m;
   const int32_t smax = (int32_t)L.tiles_mg;
   const Pairs PM = srs_pairs(P, m, d);
+  if (merge_small(k_blk)) {
+    SPARDL_TRY(launch_merge_small(sp_idx, sp_val, PM, pairs, k_blk, drop_idx, drop_val, drop_cnt, w.err, stream));
+    return SPARDL_OK;
+  }
   SPARDL_TRY(launch_merge(sp_idx, sp_val, PM, pairs, k_blk, smax, w.hist1, w.state, w.slot_cnt, w.cand_idx, w.cand_val,
                           w.bin_key, stream));
   SPARDL_TRY(launch_thresh(1, pairs, all_blocks(P), n, P, k_blk, smax, w.hist1, w.cand_val, w.state, w.slot_cnt, w.slot_nbin,
@@ -616,6 +620,11 @@ int spardl_sparse_merge_topk_noalloc(int32_t* sp_idx, float* sp_val, int32_t P, 
   const Pairs PM = srs_pairs(P, m, d);
   // the scratch keeps the previous call's contents: the histograms the merge
   // accumulates into start from zero, and so does the caller's error word
+  if (merge_small(k_blk)) {
+    SPARDL_TRY(launch_fill(Fill().add(err, 1).r, stream));
+    SPARDL_TRY(launch_merge_small(sp_idx, sp_val, PM, pairs, k_blk, drop_idx, drop_val, drop_cnt, err, stream));
+    return SPARDL_OK;
+  }
   SPARDL_TRY(launch_fill(Fill().add(hist, pairs * NB1).add(err, 1).r, stream));
   SPARDL_TRY(launch_merge(sp_idx, sp_val, PM, pairs, k_blk, smax, hist, state, slot_cnt, uidx, uval, ukey, stream));
   SPARDL_TRY(launch_thresh(1, pairs, all_blocks(P), n, P, k_blk, smax, hist, uval, state, slot_cnt, slot_nbin, ukey,

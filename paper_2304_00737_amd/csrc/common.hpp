@@ -50,6 +50,11 @@ constexpr int FINE_SHIFT = 15;
 constexpr uint32_t FINE_BELOW = NB1 / 2;        // fine bins from the window's first to its centre (8 binades)
 constexpr int FINE_SAMPLE = 64;                  // leading entries of each block sampled for the window
 constexpr int FINE_CENTRE_BIT = 20;              // the sampled medians' lowest key bit (1/8 binade)
+// Pairs whose union fits in one workgroup's LDS take one launch for the
+// merge, threshold and emit (k_merge_small).
+constexpr int SMALL_THREADS = 1024;
+constexpr int SMALL_UNION = 8192;                // union entries (both blocks) held in LDS
+__host__ __device__ __forceinline__ bool merge_small(int64_t kb) { return 2 * kb <= (int64_t)SMALL_UNION; }
 __host__ __device__ __forceinline__ bool merge_fine(int64_t kb) { return 2 * kb <= (int64_t)MT_SLOTS * MERGE_TILE; }
 
 // ---------------------------------------------------------------- state words

@@ -293,6 +293,184 @@ __global__ __launch_bounds__(MERGE_THREADS) void k_merge(
   }
 }
 
+// ============================================================================ a4: small unions, one workgroup per pair
+// When a pair's union fits in LDS (merge_small in common.hpp), one workgroup
+// does the merge, the exact threshold and the emit of the tiled path in one
+// launch: both blocks are loaded into LDS, merged by merge-path splits
+// (SMALL_MP positions per thread; held first on equal indices, the held
+// entry carrying held + received and the received one leaving a hole), the
+// union compacted in index order over the same LDS, its threshold found on
+// the 12-bit level-1 histogram and resolve_bin's levels 2 and 3, and its
+// entries written in index order: the selected ones into the held block's
+// place, the rest into the step's drop list.  The held block is in LDS
+// before it is overwritten, and an SRS step never writes a block it
+// receives.  The results are the tiled path's: the same sums, selection rule
+// and orders.
+constexpr int SMALL_MP = SMALL_UNION / SMALL_THREADS;   // merged positions per thread
+
+__global__ __launch_bounds__(SMALL_THREADS) void k_merge_small(int32_t* __restrict__ sp_idx, float* __restrict__ sp_val,
+                                                               Pairs PM, int32_t kb, int32_t* __restrict__ drop_idx,
+                                                               float* __restrict__ drop_val,
+                                                               int32_t* __restrict__ drop_cnt, uint32_t* __restrict__ err) {
+  __shared__ int32_t sI[SMALL_UNION];
+  __shared__ float sV[SMALL_UNION];
+  __shared__ __align__(16) uint32_t h[NB1];
+  __shared__ uint32_t scratch[3 * (SMALL_THREADS / WAVE) + 8];
+  const uint32_t unit = blockIdx.x;
+  const int t = threadIdx.x;
+  int64_t hb, rb;
+  bool both;
+  PM.decode(unit, &hb, &rb, &both);
+  const int32_t L2 = 2 * kb;   // <= SMALL_UNION
+  {
+    // held at [0, kb), received at [kb, 2 kb); every load first
+    int32_t ti[SMALL_MP];
+    float tv[SMALL_MP];
+#pragma unroll
+    for (int u = 0; u < SMALL_MP; ++u) {
+      const int32_t i = t + u * SMALL_THREADS;
+      ti[u] = 0;
+      tv[u] = 0.f;
+      if (i < L2) {
+        const int64_t g = i < kb ? hb * kb + i : rb * kb + (i - kb);
+        ti[u] = sp_idx[g];
+        tv[u] = sp_val[g];
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < SMALL_MP; ++u) {
+      const int32_t i = t + u * SMALL_THREADS;
+      if (i < L2) {
+        sI[i] = ti[u];
+        sV[i] = tv[u];
+      }
+    }
+    static_assert(NB1 == 4 * SMALL_THREADS, "one uint4 of the histogram per thread");
+    reinterpret_cast<uint4*>(h)[t] = make_uint4(0u, 0u, 0u, 0u);
+  }
+  __syncthreads();
+  // held(a) (-1 before the block, INT_MAX past it), received(b) (INT_MAX past it)
+  auto hI = [&](int32_t a) { return a < 0 ? -1 : a < kb ? sI[a] : INT32_MAX; };
+  auto rI = [&](int32_t b) { return b < kb ? sI[kb + b] : INT32_MAX; };
+  int32_t ei[SMALL_MP];
+  float ev[SMALL_MP];
+  bool eok[SMALL_MP];
+  uint32_t cnt = 0;
+  const int32_t q_lo = t * SMALL_MP;
+  int32_t a = 0, bb = 0;
+  if (q_lo < L2) {
+    int32_t lo = max(0, q_lo - kb), hi = min(q_lo, kb);
+    while (lo < hi) {
+      const int32_t mid = (lo + hi) >> 1;
+      if (hI(mid) <= rI(q_lo - mid - 1)) lo = mid + 1;
+      else hi = mid;
+    }
+    a = lo;
+    bb = q_lo - a;
+  }
+#pragma unroll
+  for (int k = 0; k < SMALL_MP; ++k) {
+    eok[k] = false;
+    ei[k] = 0;
+    ev[k] = 0.f;
+    if (q_lo + k < L2) {
+      a = min(a, kb);     // only reachable with unsorted input; keeps LDS reads in range
+      bb = min(bb, kb);
+      const int32_t hx = hI(a), rx = rI(bb);
+      if (hx <= rx) {
+        float v = a < kb ? sV[a] : 0.f;
+        if (rx == hx && bb < kb) v = v + sV[kb + bb];
+        ei[k] = hx;
+        ev[k] = v;
+        eok[k] = true;
+        ++a;
+      } else {
+        if (hI(a - 1) != rx) {
+          ei[k] = rx;
+          ev[k] = sV[kb + bb];
+          eok[k] = true;
+        }
+        ++bb;
+      }
+      if (eok[k]) ++cnt;
+    }
+  }
+  // the union, compacted in index order over the blocks (the scan's barriers
+  // put every thread past its reads of them)
+  uint32_t tot;
+  uint32_t pos = block_excl_scan(cnt, scratch, &tot);
+#pragma unroll
+  for (int k = 0; k < SMALL_MP; ++k) {
+    if (eok[k]) {
+      sI[pos] = ei[k];
+      sV[pos] = ev[k];
+      ++pos;
+    }
+  }
+  __syncthreads();
+  // the exact threshold: every key >= tge, and the first need_eq with key == teq
+  for (uint32_t i = (uint32_t)t; i < tot; i += SMALL_THREADS) atomicAdd(&h[mag_key(sV[i]) >> D1_SHIFT], 1u);
+  __syncthreads();
+  uint32_t T1, above1, cnt1, ok;
+  block_select_desc(h, NB1, (uint32_t)kb, scratch, &T1, &above1, &cnt1, &ok);
+  if (!ok && t == 0) atomicOr(err, ERR_COUNT);
+  const uint32_t need1 = ok ? (uint32_t)kb - above1 : 0u;
+  uint32_t tge, teq, need_eq;
+  resolve_bin(T1, D1_SHIFT, need1, cnt1, h, scratch, err,
+              [&](auto f) {
+                for (uint32_t i = (uint32_t)t; i < tot; i += SMALL_THREADS) {
+                  const uint32_t key = mag_key(sV[i]);
+                  if ((key >> D1_SHIFT) == T1) f(key);
+                }
+              },
+              tge, teq, need_eq);
+  // emit: each thread's SMALL_MP consecutive union entries, in index order
+  const uint32_t e0 = min((uint32_t)q_lo, tot), e1 = min(e0 + (uint32_t)SMALL_MP, tot);
+  uint32_t x3[3] = {0u, 0u, 0u}, t3[3];
+  for (uint32_t i = e0; i < e1; ++i) {
+    const uint32_t key = mag_key(sV[i]);
+    x3[0] += key >= tge ? 1u : 0u;
+    x3[1] += need_eq != 0u && key == teq ? 1u : 0u;
+  }
+  block_excl_scan3(x3, scratch, t3);
+  uint32_t run_g = x3[0], run_e = x3[1];
+  const int64_t o = hb * kb, o2 = both ? rb * kb : -1;
+  for (uint32_t i = e0; i < e1; ++i) {
+    const int32_t ix = sI[i];
+    const float vx = sV[i];
+    const uint32_t key = mag_key(vx);
+    const bool is_ge = key >= tge;
+    const bool is_eq = need_eq != 0u && key == teq;
+    const uint32_t sel_before = run_g + (run_e < need_eq ? run_e : need_eq);
+    if (is_ge || (is_eq && run_e < need_eq)) {
+      if (sel_before < (uint32_t)kb) {
+        sp_idx[o + sel_before] = ix;
+        sp_val[o + sel_before] = vx;
+        if (o2 >= 0) {
+          sp_idx[o2 + sel_before] = ix;
+          sp_val[o2 + sel_before] = vx;
+        }
+      } else {
+        atomicOr(err, ERR_COUNT_POS);
+      }
+    } else {
+      const uint32_t dpos = i - sel_before;
+      if (dpos < (uint32_t)kb) {
+        drop_idx[(int64_t)unit * kb + dpos] = ix;
+        drop_val[(int64_t)unit * kb + dpos] = vx;
+      } else {
+        atomicOr(err, ERR_COUNT_DROP);
+      }
+    }
+    run_g += is_ge ? 1u : 0u;
+    run_e += is_eq ? 1u : 0u;
+  }
+  if (t == 0) {
+    if (t3[0] + (t3[1] < need_eq ? t3[1] : need_eq) != (uint32_t)kb) atomicOr(err, ERR_COUNT_SUM);
+    drop_cnt[unit] = (int32_t)(tot - (uint32_t)kb);
+  }
+}
+
 // ============================================================================ launchers
 hipError_t launch_merge(const int32_t* sp_idx, const float* sp_val, const Pairs& PM, int64_t npairs, int32_t kb,
                         int32_t tiles_per_pair, uint32_t* hist1, uint32_t* state, uint32_t* slot_cnt, int32_t* U_idx,
@@ -304,6 +482,14 @@ hipError_t launch_merge(const int32_t* sp_idx, const float* sp_val, const Pairs&
   else
     hipLaunchKernelGGL(k_merge<false>, grid, dim3(MERGE_THREADS), 0, s, sp_idx, sp_val, PM, kb, tiles_per_pair, hist1,
                        state, slot_cnt, U_idx, U_val, U_key);
+  return hipGetLastError();
+}
+
+hipError_t launch_merge_small(int32_t* sp_idx, float* sp_val, const Pairs& PM, int64_t npairs, int32_t kb,
+                              int32_t* drop_idx, float* drop_val, int32_t* drop_cnt, uint32_t* err, hipStream_t s) {
+  if (!merge_small(kb)) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(k_merge_small, dim3((unsigned)npairs), dim3(SMALL_THREADS), 0, s, sp_idx, sp_val, PM, kb, drop_idx,
+                     drop_val, drop_cnt, err);
   return hipGetLastError();
 }
 

@@ -74,6 +74,11 @@ hipError_t launch_emit(int mode, const int32_t* cand_idx, const float* cand_val,
 hipError_t launch_merge(const int32_t* sp_idx, const float* sp_val, const Pairs& PM, int64_t npairs, int32_t kb,
                         int32_t tiles_per_pair, uint32_t* hist1, uint32_t* state, uint32_t* slot_cnt, int32_t* U_idx,
                         float* U_val, uint32_t* U_key, hipStream_t s);
+// One SRS step for unions of up to SMALL_UNION entries: merge, threshold
+// and emit in one launch (the same results as launch_merge + launch_thresh +
+// launch_emit).
+hipError_t launch_merge_small(int32_t* sp_idx, float* sp_val, const Pairs& PM, int64_t npairs, int32_t kb,
+                              int32_t* drop_idx, float* drop_val, int32_t* drop_cnt, uint32_t* err, hipStream_t s);
 hipError_t launch_densify(const int32_t* sp_idx, const float* sp_val, int32_t P, int64_t n, int32_t kb,
                           float* dense, uint32_t* member, bool vec4, hipStream_t s);
 hipError_t launch_bm_mark(const int32_t* sp_idx, int32_t P, int64_t n, int32_t kb, uint32_t* bm, bool set,
