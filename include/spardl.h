@@ -168,7 +168,10 @@ int spardl_residual_add_collect(float* acc, int64_t ld_acc, const float* grad, i
  * of the row's drops inside the tile, written into ws (the drop lists are
  * index-sorted inside their blocks, as spardl_sparse_merge_topk writes them).
  * Call it once after a step's SRS steps, before the next step's
- * spardl_residual_add_collect of the same rows.  drop_idx / drop_cnt: HOST
+ * spardl_residual_add_collect of the same rows.  Only tiles that hold drops
+ * are written; the add bounds every range by the pair's drop count (it reads
+ * drop_cnt too) and adds only entries inside its tile, so a range a tile
+ * kept from an earlier step adds nothing.  drop_idx / drop_cnt: HOST
  * arrays of l DEVICE pointers, as for spardl_residual_collect.  Nothing is
  * enqueued where the add collects without an index (P = 1, P > 256, or
  * blocks not float4-aligned).

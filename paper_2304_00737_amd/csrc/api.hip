@@ -372,8 +372,8 @@ void* noalloc_scratch(hipStream_t stream) {
 // The collection arguments of the rows from w0 on: per SRS step its drop
 // arrays, bag size and its part of the workspace's drop-tile index.
 AddCollect add_collect_args(int32_t P, int32_t l, int32_t w0, int32_t k_blk, const uint32_t* member,
-                            const int32_t* const* drop_idx, const float* const* drop_val, const Ws& w,
-                            const Layout& L) {
+                            const int32_t* const* drop_idx, const float* const* drop_val,
+                            const int32_t* const* drop_cnt, const Ws& w, const Layout& L) {
   AddCollect C;
   C.member = member;
   C.keep = w.keep;
@@ -386,6 +386,7 @@ AddCollect add_collect_args(int32_t P, int32_t l, int32_t w0, int32_t k_blk, con
     const int32_t m = bag_of(P, l, i);
     C.didx[i - 1] = drop_idx[i - 1];
     C.dval[i - 1] = drop_val[i - 1];
+    C.dcnt[i - 1] = drop_cnt[i - 1];
     C.m[i - 1] = (uint32_t)m;
     C.tile[i - 1] = w.dtile + pairs_before * L.add_tiles;
     pairs_before += (int64_t)P * m;
@@ -513,7 +514,7 @@ int spardl_residual_add_collect(float* acc, int64_t ld_acc, const float* grad, i
     SPARDL_TRY(launch_residual_add(acc, ld_acc, grad, ld_grad, nworkers, n, P, v4, sp, stream));
     return SPARDL_OK;
   }
-  const AddCollect C = add_collect_args(P, l, w0, k_blk, member, drop_idx, drop_val, w, L);
+  const AddCollect C = add_collect_args(P, l, w0, k_blk, member, drop_idx, drop_val, drop_cnt, w, L);
   SPARDL_TRY(launch_residual_add(acc, ld_acc, grad, ld_grad, nworkers, n, P, v4, sp, stream, C));
   return SPARDL_OK;
 }
@@ -536,15 +537,10 @@ int spardl_residual_collect_index(int32_t w0, int32_t nworkers, int64_t n, int32
   const Layout L = make_layout(P, n, k_blk);
   Ws w = carve(ws, ws_bytes, L);
   std::vector<const float*> no_val(l, nullptr);
-  const AddCollect C = add_collect_args(P, l, w0, k_blk, nullptr, drop_idx, no_val.data(), w, L);
-  // the rows' part of the index is cleared first (the build writes only tiles with drops)
-  for (int32_t i0 = 0; i0 < l; i0 += FILL_MAX) {
-    Fill f;
-    for (int32_t i = i0; i < std::min(l, i0 + FILL_MAX); ++i)
-      f.add((uint32_t*)(C.tile[i] + (int64_t)w0 * C.m[i] * L.add_tiles),
-            (int64_t)nworkers * C.m[i] * L.add_tiles * 2);
-    SPARDL_TRY(launch_fill(f.r, stream));
-  }
+  const AddCollect C = add_collect_args(P, l, w0, k_blk, nullptr, drop_idx, no_val.data(), drop_cnt, w, L);
+  // only tiles with drops are written: the add clamps every range to the
+  // pair's drop count and takes only entries inside its tile, so a range a
+  // tile kept from an earlier step adds nothing
   SPARDL_TRY(launch_drop_tiles(C, drop_cnt, nworkers, n, P, w.err, stream));
   return SPARDL_OK;
 }

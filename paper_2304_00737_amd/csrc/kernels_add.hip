@@ -120,14 +120,18 @@ __global__ __launch_bounds__(256) void k_residual_add4(float* __restrict__ acc, 
   const uint32_t tt = (b + B.P - wa % B.P) % B.P;   // COLL: this block's place in the worker's bags
   constexpr int RR_EARLY = 8;
   uint2 rr[RR_EARLY];
+  int32_t rc[RR_EARLY];   // COLL: the pair's drop count of each step
   if constexpr (COLL) {
     if (threadIdx.x == 0) {
 #pragma unroll
       for (int i = 0; i < RR_EARLY; ++i) {
         rr[i] = make_uint2(0u, 0u);
+        rc[i] = 0;
         if (i < C.l && tt < C.m[i]) {
-          const uint64_t v = early_load(reinterpret_cast<const uint64_t*>(C.tile[i] + ((int64_t)wa * C.m[i] + tt) * C.G + g));
+          const int64_t p = (int64_t)wa * C.m[i] + tt;
+          const uint64_t v = early_load(reinterpret_cast<const uint64_t*>(C.tile[i] + p * C.G + g));
           rr[i] = make_uint2((uint32_t)v, (uint32_t)(v >> 32));
+          rc[i] = early_load(C.dcnt[i] + p);
         }
       }
     }
@@ -212,9 +216,19 @@ __global__ __launch_bounds__(256) void k_residual_add4(float* __restrict__ acc, 
       for (int i = 0; i < COLLECT_MAX_STEPS; ++i) {
         if (i < C.l) {
           uint2 ri = make_uint2(0u, 0u);
-          if (i < RR_EARLY) ri = rr[i];
-          else if (tt < C.m[i]) ri = C.tile[i][((int64_t)wa * C.m[i] + tt) * C.G + g];
-          const uint32_t lo = min(ri.x, C.kb), hi = min(max(ri.y, lo), C.kb);
+          int32_t ci = 0;
+          if (i < RR_EARLY) {
+            ri = rr[i];
+            ci = rc[i];
+          } else if (tt < C.m[i]) {
+            const int64_t p = (int64_t)wa * C.m[i] + tt;
+            ri = C.tile[i][p * C.G + g];
+            ci = C.dcnt[i][p];
+          }
+          // a tile without drops this step may hold an older range: within
+          // this step's count its entries lie in other tiles and are skipped
+          const uint32_t cap = min((uint32_t)max(ci, 0), C.kb);
+          const uint32_t lo = min(ri.x, cap), hi = min(max(ri.y, lo), cap);
           if (hi > lo) {
             const int64_t p = (int64_t)wa * C.m[i] + tt;
             c_di[i] = C.didx[i] + p * C.kb;

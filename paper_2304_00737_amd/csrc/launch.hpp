@@ -34,7 +34,9 @@ struct AddCollect {
   const uint32_t* keep = nullptr;                // per absolute (worker, block): the top-k's KEEP_WORDS
   const int32_t* didx[COLLECT_MAX_STEPS] = {};   // per SRS step: the drops, [pair][k_blk]
   const float* dval[COLLECT_MAX_STEPS] = {};
+  const int32_t* dcnt[COLLECT_MAX_STEPS] = {};   // per step: the drop count of every pair
   const uint2* tile[COLLECT_MAX_STEPS] = {};     // per step: [pair][add tile] -> (first, end) of its drops there
+                                                 // (tiles without drops this step may hold an older range)
   uint32_t m[COLLECT_MAX_STEPS] = {};            // per step: blocks per bag
   int32_t l = 0;
   uint32_t w0 = 0, kb = 0, G = 0;                // first worker of the call's rows; add tiles per block
@@ -45,8 +47,10 @@ hipError_t launch_residual_add(float* acc, int64_t ld_acc, const float* grad, in
                                int32_t nworkers, int64_t n, int32_t P, bool vec4, const AddSpec& sp,
                                hipStream_t s, const AddCollect& C = AddCollect{});
 // The per-tile ranges of the drops of the call's rows (C.w0 .. C.w0 + nw - 1)
-// for a fused collection, into the index C.tile (cleared beforehand: only
-// tiles with drops are written).
+// for a fused collection, into the index C.tile.  Only tiles with drops are
+// written; the others keep whatever range they held, which the add reads
+// harmlessly (it clamps a range to the pair's drop count and adds only
+// entries inside its tile).
 hipError_t launch_drop_tiles(const AddCollect& C, const int32_t* const* drop_cnt, int32_t nw, int64_t n, int32_t P,
                              uint32_t* err, hipStream_t s);
 // Block top-k stages over nunits selection units (Units in common.hpp).
