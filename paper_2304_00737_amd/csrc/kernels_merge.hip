@@ -300,7 +300,8 @@ __global__ __launch_bounds__(MERGE_THREADS) void k_merge(
 // (SMALL_MP positions per thread; held first on equal indices, the held
 // entry carrying held + received and the received one leaving a hole), the
 // union compacted in index order over the same LDS, its threshold found on
-// the 12-bit level-1 histogram and resolve_bin's levels 2 and 3, and its
+// a fine level-1 histogram placed from the union's largest key and
+// resolve_bin's levels 2 and 3, and its
 // entries written in index order: the selected ones into the held block's
 // place, the rest into the step's drop list.  The held block is in LDS
 // before it is overwritten, and an SRS step never writes a block it
@@ -316,6 +317,7 @@ __global__ __launch_bounds__(SMALL_THREADS) void k_merge_small(int32_t* __restri
   __shared__ float sV[SMALL_UNION];
   __shared__ __align__(16) uint32_t h[NB1];
   __shared__ uint32_t scratch[3 * (SMALL_THREADS / WAVE) + 8];
+  __shared__ uint32_t s_top;   // the union's largest key
   const uint32_t unit = blockIdx.x;
   const int t = threadIdx.x;
   int64_t hb, rb;
@@ -347,6 +349,7 @@ __global__ __launch_bounds__(SMALL_THREADS) void k_merge_small(int32_t* __restri
     }
     static_assert(NB1 == 4 * SMALL_THREADS, "one uint4 of the histogram per thread");
     reinterpret_cast<uint4*>(h)[t] = make_uint4(0u, 0u, 0u, 0u);
+    if (t == 0) s_top = 0u;
   }
   __syncthreads();
   // held(a) (-1 before the block, INT_MAX past it), received(b) (INT_MAX past it)
@@ -395,6 +398,13 @@ __global__ __launch_bounds__(SMALL_THREADS) void k_merge_small(int32_t* __restri
       if (eok[k]) ++cnt;
     }
   }
+  {
+    uint32_t mk = 0;
+#pragma unroll
+    for (int k = 0; k < SMALL_MP; ++k) mk = eok[k] ? max(mk, mag_key(ev[k])) : mk;
+    mk = wave_incl_max(mk);
+    if (lane_id() == WAVE - 1) atomicMax(&s_top, mk);
+  }
   // the union, compacted in index order over the blocks (the scan's barriers
   // put every thread past its reads of them)
   uint32_t tot;
@@ -408,19 +418,40 @@ __global__ __launch_bounds__(SMALL_THREADS) void k_merge_small(int32_t* __restri
     }
   }
   __syncthreads();
-  // the exact threshold: every key >= tge, and the first need_eq with key == teq
-  for (uint32_t i = (uint32_t)t; i < tot; i += SMALL_THREADS) atomicAdd(&h[mag_key(sV[i]) >> D1_SHIFT], 1u);
+  // the exact threshold: every key >= tge, and the first need_eq with key ==
+  // teq.  Level 1 on NB1 fine bins of 2^FINE_SHIFT keys (1/256 binade) from
+  // the union's largest key down (the union keeps its larger half, whose keys
+  // crowd into a few 1/16-binade bins); keys further down share the lowest
+  // bin, and a threshold there takes the 2^D1_SHIFT-key bins instead
+  const uint32_t top = s_top >> FINE_SHIFT;
+  auto fine_bin = [&](uint32_t key) {
+    const uint32_t d = top - (key >> FINE_SHIFT);
+    return d >= (uint32_t)NB1 - 1u ? 0u : (uint32_t)NB1 - 1u - d;
+  };
+  for (uint32_t i = (uint32_t)t; i < tot; i += SMALL_THREADS) atomicAdd(&h[fine_bin(mag_key(sV[i]))], 1u);
   __syncthreads();
   uint32_t T1, above1, cnt1, ok;
   block_select_desc(h, NB1, (uint32_t)kb, scratch, &T1, &above1, &cnt1, &ok);
+  uint32_t pfx = top - ((uint32_t)NB1 - 1u - T1);
+  int S = FINE_SHIFT;
+  if (!ok || T1 == 0u) {   // uniform: the threshold below the window
+    __syncthreads();
+    reinterpret_cast<uint4*>(h)[t] = make_uint4(0u, 0u, 0u, 0u);
+    __syncthreads();
+    for (uint32_t i = (uint32_t)t; i < tot; i += SMALL_THREADS) atomicAdd(&h[mag_key(sV[i]) >> D1_SHIFT], 1u);
+    __syncthreads();
+    block_select_desc(h, NB1, (uint32_t)kb, scratch, &T1, &above1, &cnt1, &ok);
+    pfx = T1;
+    S = D1_SHIFT;
+  }
   if (!ok && t == 0) atomicOr(err, ERR_COUNT);
   const uint32_t need1 = ok ? (uint32_t)kb - above1 : 0u;
   uint32_t tge, teq, need_eq;
-  resolve_bin(T1, D1_SHIFT, need1, cnt1, h, scratch, err,
+  resolve_bin(pfx, S, need1, cnt1, h, scratch, err,
               [&](auto f) {
                 for (uint32_t i = (uint32_t)t; i < tot; i += SMALL_THREADS) {
                   const uint32_t key = mag_key(sV[i]);
-                  if ((key >> D1_SHIFT) == T1) f(key);
+                  if ((key >> S) == pfx) f(key);
                 }
               },
               tge, teq, need_eq);
