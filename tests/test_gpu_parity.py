@@ -134,7 +134,14 @@ def _random_state(P, n, kb, overlap, kind, seed):
             pool = L if overlap == "low" else min(L, kb + max(1, kb // 5))
             pool = kb if overlap == "full" else pool
             idx[w, b] = np.sort(rng.choice(pool, size=kb, replace=False)) + bounds[b]
-    val = W.small_rows(kind, P * P, kb, seed + 1).reshape(P, P, kb)
+    if kind == "outlier":
+        # one entry per block 2^40 times the rest: the union's threshold lies
+        # far below its largest key (a single-workgroup merge's level 1 then
+        # takes the 1/16-binade bins)
+        val = W.small_rows("normal", P * P, kb, seed + 1).reshape(P, P, kb)
+        val[:, :, kb // 2] *= np.float32(2.0 ** 40)
+    else:
+        val = W.small_rows(kind, P * P, kb, seed + 1).reshape(P, P, kb)
     return idx, val
 
 
@@ -142,6 +149,7 @@ def _random_state(P, n, kb, overlap, kind, seed):
     (2, 1, "full", "normal"), (3, 3, "high", "ties"), (5, 700, "high", "normal"),
     (6, 5000, "low", "normal"), (8, 2100, "high", "ties"), (14, 33, "full", "dyadic"),
     (4, 9000, "full", "ties"), (7, 4097, "high", "normal"), (16, 200, "low", "ties"),
+    (4, 4096, "full", "normal"), (6, 300, "high", "outlier"), (5, 2000, "low", "zeros"),
 ])
 def test_merge_rounds(P, kb, overlap, kind):
     log(f"merge P={P} kb={kb} overlap={overlap} kind={kind}")
