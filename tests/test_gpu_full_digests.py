@@ -64,11 +64,11 @@ def _run(workload, form, d):
     P, n, kb = wl.P, wl.n, wl.k_blk
     nb = P if d == 1 else P // d
     assert gold["P"] == P and gold["n"] == n and gold["teams"] == d and gold["blocks_per_row"] == nb
-    if sorted(int(b) for b in gold["digests"]) != list(range(nb)):
-        pytest.skip(f"checksums of {len(gold['digests'])} of {nb} block indices computed so far")
+    done = sorted(int(b) for b in gold["digests"])   # a file still being written holds some of them
+    assert done and set(done) <= set(range(nb)), done
     bounds = so.block_bounds(n, nb)
     assert gold["bounds"] == [int(x) for x in bounds]
-    log(f"full digests: {wl.describe()} form={form} d={d}")
+    log(f"full digests: {wl.describe()} form={form} d={d}: {len(done)} of {nb} block indices")
     torch.cuda.empty_cache()
     gen = W.DeviceGenerator(wl)
     per_worker = 4.0 * P * n * 2 > 100e9   # the GPT-2-XL-sized rows: one worker's gradient at a time, as bench.py
@@ -101,7 +101,7 @@ def _run(workload, form, d):
         else:
             check_ws(st)
         bad = []
-        for b in range(nb):
+        for b in done:
             lo, hi = int(bounds[b]), int(bounds[b + 1])
             streams = device_streams(form, st, P, b, lo, hi, Q=nb, d=d)
             if pending:
@@ -124,7 +124,7 @@ def _run(workload, form, d):
         else:
             finals = [st.sp_idx[q, q] for q in range(nb)]
         _check_member(st, finals, n)
-        log(f"  step {t}: {nb} block indices x {len(want)} outputs match")
+        log(f"  step {t}: {len(done)} block indices x {len(want)} outputs match")
     del st, g, gen
     torch.cuda.empty_cache()
 
