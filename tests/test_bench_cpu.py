@@ -49,6 +49,6 @@ def test_cpu_baseline_reports_its_sample():
     from paper_2304_00737_amd import workloads as W
     out = bench.cpu_baseline(W.config(1))
     assert out["kind"] == "oracle" and out["unit"] == "elements/s"
-    assert out["cores"] == min(os.cpu_count(), bench.CPU_SHARE, 4) and out["nproc"] == os.cpu_count()
+    assert out["cores"] == min(os.cpu_count(), bench.CPU_SHARE) and out["nproc"] == os.cpu_count()
     assert out["value"] > 0 and out["single_thread_value"] > 0 and out["cpu_model"]
     assert "block indices" in out["sample"] and "single-thread" in out["sample"]
